@@ -1,0 +1,269 @@
+/*
+ * atp.h -- C ABI of the MI355X (gfx950) ATP shard-block library.
+ *
+ * One device's share of a transformer layer under ATP's row-first /
+ * column-first 2D tensor parallelism (Cheng, Liu, Du, You, "ATP: Adaptive
+ * Tensor Parallelism for Foundation Models", arXiv 2301.08658):
+ * the sharded QKV, out-projection, fc1 (+bias+GeLU) and fc2 GEMMs, the
+ * reduction of their Partial(SUM) outputs, and the token-chunk pipeline
+ * that overlaps each chunk's reduction with the next chunk's GEMM.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Mesh (Sec. 3.1): DeviceMesh(d1, d2); this device sits at (i1, i2),
+ *    rank = i1 * d2 + i2.
+ *  - Y = X W with X [tokens, k] and W [k, n] (Sec. 3.2, "Y = XW").
+ *      ATP_ROW_FIRST: W spec [Shard(0), Shard(1)]: local W rows
+ *        [i1*k/d1, (i1+1)*k/d1), columns [i2*n/d2, (i2+1)*n/d2); X holds
+ *        the matching k/d1 columns; the output block is Partial(SUM) over
+ *        the d1 devices that share i2 (mesh axis 0).
+ *      ATP_COL_FIRST: W spec [Shard(1), Shard(0)]: local W rows
+ *        [i2*k/d2, ...), columns [i1*n/d1, ...); the output is Partial(SUM)
+ *        over the d2 devices that share i1 (mesh axis 1).
+ *    In the backward pass (Sec. 4.2) the input gradient dX = dY W^T is
+ *    partial over the other axis (the one that split n).
+ *  - Tensors are row-major device buffers owned by the caller: element
+ *    (r, c) of a matrix with leading dimension ld is at base[r * ld + c].
+ *    bf16 = IEEE bfloat16 bits (uint16), f32 = IEEE binary32.
+ *    Every device pointer must be 16-byte aligned, every leading dimension
+ *    and every local column count a multiple of 8 elements.
+ *  - Streams and events are hipStream_t / hipEvent_t passed as void*;
+ *    NULL means the default stream.  Calls only enqueue work and return.
+ *  - Chunks (Sec. 4.1): the token rows are split into `chunks` contiguous
+ *    equal parts; tokens % chunks must be 0.  Chunking never changes a
+ *    value: every output element is computed by the same instructions in
+ *    the same order whatever the chunk count.
+ *  - Reductions sum the group's buffers in group order 0..d-1, so every
+ *    member of a group obtains bit-identical results.
+ *  - Errors: all arguments are checked before anything is enqueued; a
+ *    non-OK status means nothing was enqueued.  atp_last_error() returns
+ *    a per-thread message for the last failure.  A HIP launch failure
+ *    after checks passed returns ATP_ERR_DEVICE (work enqueued before it
+ *    may have run).
+ *  - The library never allocates device memory.
+ */
+#ifndef ATP_H
+#define ATP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    ATP_OK = 0,
+    ATP_ERR_INVALID_ARGUMENT = 1, /* null pointer, coordinate out of range, bad enum, ld < cols */
+    ATP_ERR_SHAPE = 2,            /* k or n not divisible by the mesh, tokens % chunks != 0 */
+    ATP_ERR_UNSUPPORTED = 3,      /* alignment, multiple-of-8 rule, group larger than ATP_MAX_GROUP */
+    ATP_ERR_DEVICE = 4            /* a HIP call failed */
+} atp_status;
+
+typedef enum { ATP_ROW_FIRST = 0, ATP_COL_FIRST = 1 } atp_mode;
+
+/* ATP_BLOCK_COL: the layer of Sec. 3.2.1 -- QKV and fc1 column-first,
+ * out-proj and fc2 row-first.  ATP_BLOCK_ROW: the transposed arrangement
+ * (QKV and fc1 row-first, out-proj and fc2 column-first); on mesh (d1, d2)
+ * it has the local shapes of ATP_BLOCK_COL on (d2, d1). */
+typedef enum { ATP_BLOCK_COL = 0, ATP_BLOCK_ROW = 1 } atp_block_mode;
+
+/* Epilogues (Sec. 2.1 and 3.2.1).  With s the reduced sum:
+ *   NONE: s;  BIAS: s + b[n];  BIAS_GELU: GeLU(s + b[n]) with the exact erf
+ *   form, optionally saving s + b[n];  GELU_BWD: s * GeLU'(pre[t, n]). */
+typedef enum {
+    ATP_EPI_NONE = 0,
+    ATP_EPI_BIAS = 1,
+    ATP_EPI_BIAS_GELU = 2,
+    ATP_EPI_GELU_BWD = 3
+} atp_epilogue;
+
+typedef enum { ATP_F32 = 0, ATP_BF16 = 1 } atp_dtype;
+
+#define ATP_MAX_GROUP 64   /* largest reduction group (d1 or d2) */
+#define ATP_MAX_CHUNKS 64
+
+typedef struct { int32_t d1, d2, i1, i2; } atp_mesh;
+
+/* Local block of one linear (Sec. 3.2): W rows [k_off, k_off + k_loc),
+ * columns [n_off, n_off + n_loc); forward reduction over mesh axis
+ * red_axis (group size red_size, this device at red_index); backward
+ * input-gradient reduction over bwd_axis (bwd_size, bwd_index). */
+typedef struct {
+    int64_t k_loc, n_loc, k_off, n_off;
+    int32_t red_axis, red_size, red_index;
+    int32_t bwd_axis, bwd_size, bwd_index;
+} atp_shard;
+
+/* Shard geometry of Y = XW, Sec. 3.2 (local sizes [b, h1/d1] x [h1/d1, h2/d2]
+ * for row-first; communicated block [b, h2/d1] for column-first).
+ * Host only, no device work.  Errors: INVALID_ARGUMENT (null, d <= 0,
+ * coordinate out of range, bad mode), SHAPE (k or n not divisible). */
+atp_status atp_shard_geometry(const atp_mesh* mesh, int32_t mode, int64_t k, int64_t n,
+                              atp_shard* out);
+
+/* Local GEMM of one shard linear, chunked (Sec. 3.2, Sec. 4.1):
+ *   y[t, :] = epi( x_loc[t, :] . w_loc )   for t in each chunk, in order.
+ * x_loc  bf16 [tokens, k_loc], ld ldx.   w_loc bf16 [k_loc, n_loc], ld ldw.
+ * If the reduction group has more than one member, y is this device's
+ * Partial(SUM) block: y_dtype must be ATP_F32 and epi ATP_EPI_NONE (the
+ * bias and GeLU belong after the reduction).  With a group of one, epi may
+ * be NONE, BIAS or BIAS_GELU and y f32 or bf16; bias_loc bf16 [n_loc]
+ * (the block n_off..), preact (nullable, bf16, ld ldy) receives s + b for
+ * BIAS_GELU.  chunk_done (nullable) holds `chunks` caller-created events;
+ * event c is recorded on `stream` once chunk c's rows of y are written. */
+atp_status atp_shard_linear_fwd(const atp_mesh* mesh, int32_t mode, int64_t tokens,
+                                int64_t k, int64_t n, int32_t chunks,
+                                const void* x_loc, int64_t ldx,
+                                const void* w_loc, int64_t ldw,
+                                const void* bias_loc, int32_t epi,
+                                void* y, int32_t y_dtype, int64_t ldy, void* preact,
+                                void* stream, void* const* chunk_done);
+
+/* Reduction of a group's Partial(SUM) blocks -- the arithmetic of the
+ * grouped all-reduce of Sec. 3.2 (Sec. 3.1, Partial(SUM)) -- chunked so
+ * that chunk c can start as soon as its partials are ready (Sec. 4.1):
+ *   out[t, n] = epi( sum_{j=0..red_size-1} partials[j][t * ldp + n] ).
+ * partials: host array of red_size device pointers, f32 [tokens, ldp];
+ * on one GPU the other members' buffers stand in for the peers' data.
+ * bias_loc bf16 [n_loc] for BIAS / BIAS_GELU.  preact_in (bf16, ld ldo)
+ * for GELU_BWD; preact_out (nullable, bf16, ld ldo) for BIAS_GELU.
+ * out is f32 or bf16 (round to nearest even).  chunk_ready (nullable):
+ * `chunks` events; the stream waits for event c before reducing chunk c.
+ * Errors: INVALID_ARGUMENT for red_size < 1, a null entry, missing bias or
+ * preact_in; UNSUPPORTED for red_size > ATP_MAX_GROUP. */
+atp_status atp_chunked_partial_reduce(int32_t red_size, int64_t tokens, int64_t n_loc,
+                                      int32_t chunks, const float* const* partials,
+                                      int64_t ldp, const void* bias_loc, int32_t epi,
+                                      const void* preact_in, void* out, int32_t out_dtype,
+                                      int64_t ldo, void* preact_out, void* stream,
+                                      void* const* chunk_ready);
+
+/* Backward of one shard linear (Sec. 4.2): with dy the gradient of this
+ * device's reduced output block (bf16 [tokens, n_loc], ld lddy),
+ *   dx_partial = dy . w_loc^T   f32 [tokens, k_loc], ld lddx -- partial over
+ *                               the backward group (bwd_size members);
+ *   dw         = x_loc^T . dy   f32 [k_loc, n_loc], ld lddw (complete);
+ *   db         = sum_t dy       f32 [n_loc] (nullable).
+ * dX is computed first, chunk by chunk, recording dx_chunk_done[c]
+ * (nullable) so its reduction can overlap the dW GEMM that follows on the
+ * same stream. */
+atp_status atp_shard_linear_bwd(const atp_mesh* mesh, int32_t mode, int64_t tokens,
+                                int64_t k, int64_t n, int32_t chunks,
+                                const void* x_loc, int64_t ldx,
+                                const void* w_loc, int64_t ldw,
+                                const void* dy, int64_t lddy,
+                                float* dx_partial, int64_t lddx,
+                                float* dw, int64_t lddw, float* db,
+                                void* stream, void* const* dx_chunk_done);
+
+/* Local weights of the block; index 0..3 = qkv [h,3h], out [h,h],
+ * fc1 [h,4h], fc2 [4h,h] (Sec. 2.1).  Each w[i] is the device's bf16
+ * block [k_loc, n_loc] (ld ldw[i]); b[i] its bf16 bias block [n_loc]. */
+typedef struct {
+    const void* w[4];
+    int64_t ldw[4];
+    const void* b[4];
+} atp_block_weights;
+
+/* Forward inputs and outputs of the block (Sec. 3.2.1).
+ *  x_loc   bf16 [tokens, h_x]: the layer-input columns QKV and fc1
+ *          contract over (h/d2 for COL, h/d1 for ROW).
+ *  attn_loc bf16 [tokens, h_a]: the attention-core output columns that
+ *          feed out-proj (h/d1 for COL, h/d2 for ROW).
+ *  partials[i]: host array of the red_size device pointers of linear i's
+ *          group (f32 [tokens, ldp[i]]); entry red_index is this device's
+ *          own buffer and is written, the others are read.  Unused (may
+ *          be NULL) when the group has one member.
+ *  qkv, o, h, z: bf16 reduced outputs (+bias; h = GeLU(...)); pre: bf16
+ *          fc1 pre-activation saved for the backward, ld ld_h. */
+typedef struct {
+    const void* x_loc;
+    int64_t ldx;
+    const void* attn_loc;
+    int64_t lda;
+    float* const* partials[4];
+    int64_t ldp[4];
+    void* qkv; int64_t ld_qkv;
+    void* o;   int64_t ld_o;
+    void* h;   int64_t ld_h;
+    void* pre;
+    void* z;   int64_t ld_z;
+} atp_block_fwd_io;
+
+/* Backward inputs and outputs of the block (Sec. 4.2).
+ *  x_loc, attn_loc, h, pre: the forward's inputs and saved activations.
+ *  dz, dqkv, d_o: bf16 gradients of the reduced outputs z, qkv, o.
+ *  dx_partials[i]: host array of the bwd_size device pointers of linear
+ *          i's backward group (f32 [tokens, ld_dxp[i]]), own entry written.
+ *  dh_pre: bf16 fc1 upstream gradient = (reduced fc2 dX) * GeLU'(pre).
+ *  dx_qkv, dx_fc1, d_attn: bf16 reduced input gradients.
+ *  dw[i] f32 [k_loc, n_loc] (ld ldw of the weights), db[i] f32 [n_loc]. */
+typedef struct {
+    const void* x_loc;    int64_t ldx;
+    const void* attn_loc; int64_t lda;
+    const void* h;        int64_t ld_h;
+    const void* pre;
+    const void* dz;   int64_t ld_dz;
+    const void* dqkv; int64_t ld_dqkv;
+    const void* d_o;  int64_t ld_do;
+    float* const* dx_partials[4];
+    int64_t ld_dxp[4];
+    void* dh_pre;
+    void* dx_qkv; int64_t ld_dx_qkv;
+    void* dx_fc1; int64_t ld_dx_fc1;
+    void* d_attn; int64_t ld_d_attn;
+    float* dw[4];
+    float* db[4];
+} atp_block_bwd_io;
+
+/* Scratch the block calls need beyond the caller's buffers (bytes). */
+size_t atp_block_workspace_bytes(const atp_mesh* mesh, int32_t block_mode, int64_t tokens,
+                                 int64_t h, int32_t chunks);
+
+/* One device's forward share of the layer (Sec. 3.2.1) with chunk-based
+ * overlapping (Sec. 4.1).  GEMMs run on compute_stream in the order
+ * qkv, out, fc1, fc2, chunk by chunk; each chunk's reduction runs on
+ * comm_stream as soon as its partial is written; fc2's chunk c waits for
+ * fc1's reduced chunk c.  On return compute_stream is ordered after all
+ * of the block's work.  A group of one needs no reduction: its bias (and
+ * GeLU) are applied in the GEMM epilogue. */
+atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
+                         int32_t chunks, const atp_block_weights* w,
+                         const atp_block_fwd_io* io, void* workspace, size_t ws_bytes,
+                         void* compute_stream, void* comm_stream);
+
+/* One device's backward share of the layer (Sec. 4.2): fc2, fc1, out,
+ * qkv in turn; for each, dX chunks on compute_stream, their reductions on
+ * comm_stream overlapping the dW GEMM.  fc1's dY is fc2's reduced dX
+ * times GeLU'(pre).  On return compute_stream is ordered after all work. */
+atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
+                         int32_t chunks, const atp_block_weights* w,
+                         const atp_block_bwd_io* io, void* workspace, size_t ws_bytes,
+                         void* compute_stream, void* comm_stream);
+
+/* Per-kernel timing of the library's own launches.  When enabled, every
+ * kernel the library enqueues is bracketed by HIP events on its stream;
+ * atp_profile_collect synchronises those events, fills up to `max`
+ * records (one per kernel name: launches, total milliseconds, total
+ * algorithmic FLOPs and bytes) and clears the log.  Returns the number of
+ * records, or -1 on a HIP error. */
+typedef struct {
+    char name[48];
+    int64_t launches;
+    double total_ms;
+    double flops;
+    double bytes;
+} atp_kernel_stat;
+
+void atp_profile_enable(int32_t on);
+int32_t atp_profile_collect(atp_kernel_stat* out, int32_t max);
+
+const char* atp_status_string(int32_t status);
+const char* atp_last_error(void);
+const char* atp_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

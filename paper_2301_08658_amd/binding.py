@@ -1,0 +1,442 @@
+"""ctypes binding of libatp.so (include/atp.h).
+
+Argument marshalling only: every step of the path runs in the library's
+HIP kernels.  Functions keep the C names; tensors are passed as torch
+tensors (device pointer + leading dimension), streams as torch streams.
+Sizes a C call cannot see (row counts of the buffers) are checked here so
+that a short buffer never reaches a kernel.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libatp.so")
+
+ATP_OK = 0
+ATP_ERR_INVALID_ARGUMENT = 1
+ATP_ERR_SHAPE = 2
+ATP_ERR_UNSUPPORTED = 3
+ATP_ERR_DEVICE = 4
+
+ATP_ROW_FIRST = 0
+ATP_COL_FIRST = 1
+ATP_BLOCK_COL = 0
+ATP_BLOCK_ROW = 1
+ATP_EPI_NONE = 0
+ATP_EPI_BIAS = 1
+ATP_EPI_BIAS_GELU = 2
+ATP_EPI_GELU_BWD = 3
+ATP_F32 = 0
+ATP_BF16 = 1
+ATP_MAX_GROUP = 64
+ATP_MAX_CHUNKS = 64
+
+LINEARS = ("qkv", "out", "fc1", "fc2")
+
+
+class AtpError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{status_string(status)}: {msg}")
+        self.status = status
+
+
+class atp_mesh(ctypes.Structure):
+    _fields_ = [("d1", ctypes.c_int32), ("d2", ctypes.c_int32),
+                ("i1", ctypes.c_int32), ("i2", ctypes.c_int32)]
+
+
+class atp_shard(ctypes.Structure):
+    _fields_ = [("k_loc", ctypes.c_int64), ("n_loc", ctypes.c_int64),
+                ("k_off", ctypes.c_int64), ("n_off", ctypes.c_int64),
+                ("red_axis", ctypes.c_int32), ("red_size", ctypes.c_int32),
+                ("red_index", ctypes.c_int32), ("bwd_axis", ctypes.c_int32),
+                ("bwd_size", ctypes.c_int32), ("bwd_index", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+_vp = ctypes.c_void_p
+_fpp = ctypes.POINTER(ctypes.c_void_p)   # float* const* (host array of device ptrs)
+
+
+class atp_block_weights(ctypes.Structure):
+    _fields_ = [("w", _vp * 4), ("ldw", ctypes.c_int64 * 4), ("b", _vp * 4)]
+
+
+class atp_block_fwd_io(ctypes.Structure):
+    _fields_ = [("x_loc", _vp), ("ldx", ctypes.c_int64),
+                ("attn_loc", _vp), ("lda", ctypes.c_int64),
+                ("partials", _fpp * 4), ("ldp", ctypes.c_int64 * 4),
+                ("qkv", _vp), ("ld_qkv", ctypes.c_int64),
+                ("o", _vp), ("ld_o", ctypes.c_int64),
+                ("h", _vp), ("ld_h", ctypes.c_int64),
+                ("pre", _vp),
+                ("z", _vp), ("ld_z", ctypes.c_int64)]
+
+
+class atp_block_bwd_io(ctypes.Structure):
+    _fields_ = [("x_loc", _vp), ("ldx", ctypes.c_int64),
+                ("attn_loc", _vp), ("lda", ctypes.c_int64),
+                ("h", _vp), ("ld_h", ctypes.c_int64),
+                ("pre", _vp),
+                ("dz", _vp), ("ld_dz", ctypes.c_int64),
+                ("dqkv", _vp), ("ld_dqkv", ctypes.c_int64),
+                ("d_o", _vp), ("ld_do", ctypes.c_int64),
+                ("dx_partials", _fpp * 4), ("ld_dxp", ctypes.c_int64 * 4),
+                ("dh_pre", _vp),
+                ("dx_qkv", _vp), ("ld_dx_qkv", ctypes.c_int64),
+                ("dx_fc1", _vp), ("ld_dx_fc1", ctypes.c_int64),
+                ("d_attn", _vp), ("ld_d_attn", ctypes.c_int64),
+                ("dw", _vp * 4), ("db", _vp * 4)]
+
+
+class atp_kernel_stat(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 48), ("launches", ctypes.c_int64),
+                ("total_ms", ctypes.c_double), ("flops", ctypes.c_double),
+                ("bytes", ctypes.c_double)]
+
+
+EXPORTS = (
+    "atp_shard_geometry", "atp_shard_linear_fwd", "atp_chunked_partial_reduce",
+    "atp_shard_linear_bwd", "atp_block_workspace_bytes", "atp_block_fwd", "atp_block_bwd",
+    "atp_profile_enable", "atp_profile_collect", "atp_status_string", "atp_last_error",
+    "atp_version",
+)
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libatp.so.  Raises if it has not been built: there is no fallback."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is missing: build the HIP library first "
+                          "(python -m paper_2301_08658_amd.build)")
+    lib = ctypes.CDLL(path)
+    i32, i64, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    mp = ctypes.POINTER(atp_mesh)
+    lib.atp_shard_geometry.argtypes = [mp, i32, i64, i64, ctypes.POINTER(atp_shard)]
+    lib.atp_shard_geometry.restype = i32
+    lib.atp_shard_linear_fwd.argtypes = [mp, i32, i64, i64, i64, i32, _vp, i64, _vp, i64, _vp,
+                                         i32, _vp, i32, i64, _vp, _vp, _fpp]
+    lib.atp_shard_linear_fwd.restype = i32
+    lib.atp_chunked_partial_reduce.argtypes = [i32, i64, i64, i32, _fpp, i64, _vp, i32, _vp, _vp,
+                                               i32, i64, _vp, _vp, _fpp]
+    lib.atp_chunked_partial_reduce.restype = i32
+    lib.atp_shard_linear_bwd.argtypes = [mp, i32, i64, i64, i64, i32, _vp, i64, _vp, i64, _vp, i64,
+                                         _vp, i64, _vp, i64, _vp, _vp, _fpp]
+    lib.atp_shard_linear_bwd.restype = i32
+    lib.atp_block_workspace_bytes.argtypes = [mp, i32, i64, i64, i32]
+    lib.atp_block_workspace_bytes.restype = sz
+    lib.atp_block_fwd.argtypes = [mp, i32, i64, i64, i32, ctypes.POINTER(atp_block_weights),
+                                  ctypes.POINTER(atp_block_fwd_io), _vp, sz, _vp, _vp]
+    lib.atp_block_fwd.restype = i32
+    lib.atp_block_bwd.argtypes = [mp, i32, i64, i64, i32, ctypes.POINTER(atp_block_weights),
+                                  ctypes.POINTER(atp_block_bwd_io), _vp, sz, _vp, _vp]
+    lib.atp_block_bwd.restype = i32
+    lib.atp_profile_enable.argtypes = [i32]
+    lib.atp_profile_enable.restype = None
+    lib.atp_profile_collect.argtypes = [ctypes.POINTER(atp_kernel_stat), i32]
+    lib.atp_profile_collect.restype = i32
+    lib.atp_status_string.argtypes = [i32]
+    lib.atp_status_string.restype = ctypes.c_char_p
+    lib.atp_last_error.argtypes = []
+    lib.atp_last_error.restype = ctypes.c_char_p
+    lib.atp_version.argtypes = []
+    lib.atp_version.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def status_string(s: int) -> str:
+    return load_library().atp_status_string(int(s)).decode()
+
+
+def last_error() -> str:
+    return load_library().atp_last_error().decode()
+
+
+def _check(status: int):
+    if status != ATP_OK:
+        raise AtpError(status, last_error())
+
+
+# ---------------------------------------------------------------- marshalling
+def mesh(d1, d2, i1=0, i2=0) -> atp_mesh:
+    return atp_mesh(int(d1), int(d2), int(i1), int(i2))
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _mat(t: Optional[torch.Tensor], rows: int, cols: int, dtype, name: str):
+    """(pointer, ld) of a row-major matrix with at least rows x cols."""
+    if t is None:
+        return None, 0
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    if t.dim() != 2 or (t.size(1) > 1 and t.stride(1) != 1):
+        raise ValueError(f"{name}: needs a 2-D row-major tensor")
+    if t.size(0) < rows or t.size(1) < cols:
+        raise ValueError(f"{name}: {tuple(t.shape)} smaller than [{rows}, {cols}]")
+    return t.data_ptr(), (t.stride(0) if t.size(0) > 1 else max(t.size(1), cols))
+
+
+def _vec(t: Optional[torch.Tensor], n: int, dtype, name: str):
+    if t is None:
+        return None
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    if t.numel() < n or not t.is_contiguous():
+        raise ValueError(f"{name}: needs {n} contiguous elements")
+    return t.data_ptr()
+
+
+def _stream(s) -> Optional[int]:
+    if s is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def _events(evs: Optional[Sequence]) -> Optional[ctypes.Array]:
+    if evs is None:
+        return None
+    return (ctypes.c_void_p * len(evs))(*[e.handle if isinstance(e, HipEvent) else e
+                                          for e in evs])
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return ATP_F32
+    if t.dtype == torch.bfloat16:
+        return ATP_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr_table(ts: Sequence[torch.Tensor], rows: int, cols: int, name: str):
+    arr = (ctypes.c_void_p * len(ts))()
+    ld = None
+    for j, t in enumerate(ts):
+        p, l = _mat(t, rows, cols, torch.float32, f"{name}[{j}]")
+        arr[j] = p
+        if ld is None:
+            ld = l
+        elif l != ld:
+            raise ValueError(f"{name}: all buffers need the same leading dimension")
+    return ctypes.cast(arr, _fpp), arr, (ld or cols)
+
+
+class HipEvent:
+    """A raw hipEvent_t (created through the HIP runtime) for chunk signalling."""
+    _hip = None
+
+    def __init__(self, timing: bool = False):
+        if HipEvent._hip is None:
+            HipEvent._hip = ctypes.CDLL("libamdhip64.so")
+        h = ctypes.c_void_p()
+        flags = 0 if timing else 0x2   # hipEventDisableTiming
+        rc = HipEvent._hip.hipEventCreateWithFlags(ctypes.byref(h), ctypes.c_uint(flags))
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags failed ({rc})")
+        self.handle = h.value
+
+    def synchronize(self):
+        rc = HipEvent._hip.hipEventSynchronize(ctypes.c_void_p(self.handle))
+        if rc != 0:
+            raise RuntimeError(f"hipEventSynchronize failed ({rc})")
+
+    def __del__(self):
+        if HipEvent._hip is not None and getattr(self, "handle", None):
+            HipEvent._hip.hipEventDestroy(ctypes.c_void_p(self.handle))
+
+
+# ---------------------------------------------------------------- the ABI
+def atp_version() -> str:
+    return load_library().atp_version().decode()
+
+
+def atp_shard_geometry(m: atp_mesh, mode: int, k: int, n: int) -> atp_shard:
+    out = atp_shard()
+    _check(load_library().atp_shard_geometry(ctypes.byref(m), int(mode), int(k), int(n),
+                                             ctypes.byref(out)))
+    return out
+
+
+def atp_shard_linear_fwd(m: atp_mesh, mode: int, tokens: int, k: int, n: int, chunks: int,
+                         x_loc, w_loc, bias_loc, epi: int, y, preact=None, stream=None,
+                         chunk_done=None):
+    g = atp_shard_geometry(m, mode, k, n)
+    xp, ldx = _mat(x_loc, tokens, g.k_loc, torch.bfloat16, "x_loc")
+    wp, ldw = _mat(w_loc, g.k_loc, g.n_loc, torch.bfloat16, "w_loc")
+    yp, ldy = _mat(y, tokens, g.n_loc, y.dtype, "y")
+    pp, ldp = _mat(preact, tokens, g.n_loc, torch.bfloat16, "preact")
+    if preact is not None and ldp != ldy:
+        raise ValueError("preact must share y's leading dimension")
+    bp = _vec(bias_loc, g.n_loc, torch.bfloat16, "bias_loc")
+    _check(load_library().atp_shard_linear_fwd(
+        ctypes.byref(m), int(mode), int(tokens), int(k), int(n), int(chunks), xp, ldx, wp, ldw,
+        bp, int(epi), yp, _dtype_code(y), ldy, pp, _stream(stream), _events(chunk_done)))
+
+
+def atp_chunked_partial_reduce(red_size: int, tokens: int, n_loc: int, chunks: int, partials,
+                               bias_loc, epi: int, out, preact_in=None, preact_out=None,
+                               stream=None, chunk_ready=None):
+    if len(partials) != red_size:
+        raise ValueError("need exactly red_size partial buffers")
+    tab, _keep, ldp = _ptr_table(partials, tokens, n_loc, "partials")
+    op, ldo = _mat(out, tokens, n_loc, out.dtype, "out")
+    ip, ldi = _mat(preact_in, tokens, n_loc, torch.bfloat16, "preact_in")
+    qp, ldq = _mat(preact_out, tokens, n_loc, torch.bfloat16, "preact_out")
+    for t, l in ((preact_in, ldi), (preact_out, ldq)):
+        if t is not None and l != ldo:
+            raise ValueError("pre-activation buffers must share out's leading dimension")
+    bp = _vec(bias_loc, n_loc, torch.bfloat16, "bias_loc")
+    _check(load_library().atp_chunked_partial_reduce(
+        int(red_size), int(tokens), int(n_loc), int(chunks), tab, ldp, bp, int(epi), ip, op,
+        _dtype_code(out), ldo, qp, _stream(stream), _events(chunk_ready)))
+
+
+def atp_shard_linear_bwd(m: atp_mesh, mode: int, tokens: int, k: int, n: int, chunks: int,
+                         x_loc, w_loc, dy, dx_partial, dw, db=None, stream=None,
+                         dx_chunk_done=None):
+    g = atp_shard_geometry(m, mode, k, n)
+    xp, ldx = _mat(x_loc, tokens, g.k_loc, torch.bfloat16, "x_loc")
+    wp, ldw = _mat(w_loc, g.k_loc, g.n_loc, torch.bfloat16, "w_loc")
+    yp, ldy = _mat(dy, tokens, g.n_loc, torch.bfloat16, "dy")
+    dxp, lddx = _mat(dx_partial, tokens, g.k_loc, torch.float32, "dx_partial")
+    dwp, lddw = _mat(dw, g.k_loc, g.n_loc, torch.float32, "dw")
+    dbp = _vec(db, g.n_loc, torch.float32, "db")
+    _check(load_library().atp_shard_linear_bwd(
+        ctypes.byref(m), int(mode), int(tokens), int(k), int(n), int(chunks), xp, ldx, wp, ldw,
+        yp, ldy, dxp, lddx, dwp, lddw, dbp, _stream(stream), _events(dx_chunk_done)))
+
+
+def block_geometry(m: atp_mesh, block_mode: int, h: int):
+    """Shard geometry of the block's four linears (qkv, out, fc1, fc2)."""
+    modes = ((ATP_COL_FIRST, ATP_ROW_FIRST, ATP_COL_FIRST, ATP_ROW_FIRST)
+             if block_mode == ATP_BLOCK_COL else
+             (ATP_ROW_FIRST, ATP_COL_FIRST, ATP_ROW_FIRST, ATP_COL_FIRST))
+    shapes = ((h, 3 * h), (h, h), (h, 4 * h), (4 * h, h))
+    return [atp_shard_geometry(m, md, k, n) for md, (k, n) in zip(modes, shapes)]
+
+
+def atp_block_workspace_bytes(m: atp_mesh, block_mode: int, tokens: int, h: int,
+                              chunks: int) -> int:
+    return int(load_library().atp_block_workspace_bytes(ctypes.byref(m), int(block_mode),
+                                                         int(tokens), int(h), int(chunks)))
+
+
+def _weights(G, w: Sequence[torch.Tensor], b: Sequence[torch.Tensor]):
+    W = atp_block_weights()
+    for i, g in enumerate(G):
+        p, ld = _mat(w[i], g.k_loc, g.n_loc, torch.bfloat16, f"w[{LINEARS[i]}]")
+        W.w[i] = p
+        W.ldw[i] = ld
+        W.b[i] = _vec(b[i], g.n_loc, torch.bfloat16, f"b[{LINEARS[i]}]")
+    return W
+
+
+def atp_block_fwd(m: atp_mesh, block_mode: int, tokens: int, h: int, chunks: int, w, b,
+                  x_loc, attn_loc, partials, qkv, o, h_out, pre, z, workspace=None,
+                  compute_stream=None, comm_stream=None):
+    """partials[i]: list of the red_size f32 buffers of linear i's group (own
+    entry written), or None for a group of one."""
+    G = block_geometry(m, block_mode, h)
+    W = _weights(G, w, b)
+    io = atp_block_fwd_io()
+    io.x_loc, io.ldx = _mat(x_loc, tokens, G[0].k_loc, torch.bfloat16, "x_loc")
+    io.attn_loc, io.lda = _mat(attn_loc, tokens, G[1].k_loc, torch.bfloat16, "attn_loc")
+    keep = []
+    for i, g in enumerate(G):
+        if g.red_size > 1:
+            tab, arr, ld = _ptr_table(partials[i], tokens, g.n_loc, f"partials[{LINEARS[i]}]")
+            if len(partials[i]) != g.red_size:
+                raise ValueError(f"partials[{LINEARS[i]}] needs {g.red_size} buffers")
+            io.partials[i] = tab
+            io.ldp[i] = ld
+            keep.append(arr)
+    io.qkv, io.ld_qkv = _mat(qkv, tokens, G[0].n_loc, torch.bfloat16, "qkv")
+    io.o, io.ld_o = _mat(o, tokens, G[1].n_loc, torch.bfloat16, "o")
+    io.h, io.ld_h = _mat(h_out, tokens, G[2].n_loc, torch.bfloat16, "h")
+    pp, ldpre = _mat(pre, tokens, G[2].n_loc, torch.bfloat16, "pre")
+    if ldpre != io.ld_h:
+        raise ValueError("pre must share h's leading dimension")
+    io.pre = pp
+    io.z, io.ld_z = _mat(z, tokens, G[3].n_loc, torch.bfloat16, "z")
+    wsp = _ptr(workspace)
+    wsb = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(load_library().atp_block_fwd(ctypes.byref(m), int(block_mode), int(tokens), int(h),
+                                        int(chunks), ctypes.byref(W), ctypes.byref(io), wsp, wsb,
+                                        _stream(compute_stream), _stream(comm_stream)))
+
+
+def atp_block_bwd(m: atp_mesh, block_mode: int, tokens: int, h: int, chunks: int, w, b,
+                  x_loc, attn_loc, h_act, pre, dz, dqkv, d_o, dx_partials, dh_pre, dx_qkv,
+                  dx_fc1, d_attn, dw, db, workspace=None, compute_stream=None,
+                  comm_stream=None):
+    """dx_partials[i]: list of the bwd_size f32 buffers of linear i's backward
+    group (own entry written), or None for a group of one.  dw[i] must share
+    the leading dimension of w[i]."""
+    G = block_geometry(m, block_mode, h)
+    W = _weights(G, w, b)
+    io = atp_block_bwd_io()
+    io.x_loc, io.ldx = _mat(x_loc, tokens, G[0].k_loc, torch.bfloat16, "x_loc")
+    io.attn_loc, io.lda = _mat(attn_loc, tokens, G[1].k_loc, torch.bfloat16, "attn_loc")
+    io.h, io.ld_h = _mat(h_act, tokens, G[2].n_loc, torch.bfloat16, "h")
+    pp, ldpre = _mat(pre, tokens, G[2].n_loc, torch.bfloat16, "pre")
+    dp, lddp = _mat(dh_pre, tokens, G[2].n_loc, torch.bfloat16, "dh_pre")
+    if ldpre != io.ld_h or lddp != io.ld_h:
+        raise ValueError("pre and dh_pre must share h's leading dimension")
+    io.pre, io.dh_pre = pp, dp
+    io.dz, io.ld_dz = _mat(dz, tokens, G[3].n_loc, torch.bfloat16, "dz")
+    io.dqkv, io.ld_dqkv = _mat(dqkv, tokens, G[0].n_loc, torch.bfloat16, "dqkv")
+    io.d_o, io.ld_do = _mat(d_o, tokens, G[1].n_loc, torch.bfloat16, "d_o")
+    keep = []
+    for i, g in enumerate(G):
+        if g.bwd_size > 1:
+            if len(dx_partials[i]) != g.bwd_size:
+                raise ValueError(f"dx_partials[{LINEARS[i]}] needs {g.bwd_size} buffers")
+            tab, arr, ld = _ptr_table(dx_partials[i], tokens, g.k_loc,
+                                      f"dx_partials[{LINEARS[i]}]")
+            io.dx_partials[i] = tab
+            io.ld_dxp[i] = ld
+            keep.append(arr)
+    io.dx_qkv, io.ld_dx_qkv = _mat(dx_qkv, tokens, G[0].k_loc, torch.bfloat16, "dx_qkv")
+    io.dx_fc1, io.ld_dx_fc1 = _mat(dx_fc1, tokens, G[2].k_loc, torch.bfloat16, "dx_fc1")
+    io.d_attn, io.ld_d_attn = _mat(d_attn, tokens, G[1].k_loc, torch.bfloat16, "d_attn")
+    for i, g in enumerate(G):
+        p, ld = _mat(dw[i], g.k_loc, g.n_loc, torch.float32, f"dw[{LINEARS[i]}]")
+        if ld != W.ldw[i]:
+            raise ValueError(f"dw[{LINEARS[i]}] must share the weight's leading dimension")
+        io.dw[i] = p
+        io.db[i] = _vec(db[i], g.n_loc, torch.float32, f"db[{LINEARS[i]}]") if db else None
+    wsp = _ptr(workspace)
+    wsb = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(load_library().atp_block_bwd(ctypes.byref(m), int(block_mode), int(tokens), int(h),
+                                        int(chunks), ctypes.byref(W), ctypes.byref(io), wsp, wsb,
+                                        _stream(compute_stream), _stream(comm_stream)))
+
+
+def atp_profile_enable(on: bool = True):
+    load_library().atp_profile_enable(1 if on else 0)
+
+
+def atp_profile_collect(max_records: int = 32):
+    arr = (atp_kernel_stat * max_records)()
+    n = load_library().atp_profile_collect(arr, max_records)
+    if n < 0:
+        raise AtpError(ATP_ERR_DEVICE, last_error())
+    return [dict(name=arr[i].name.decode(), launches=arr[i].launches,
+                 total_ms=arr[i].total_ms, flops=arr[i].flops, bytes=arr[i].bytes)
+            for i in range(n)]

@@ -1,0 +1,696 @@
+// C ABI of the ATP shard-block library: argument checking, shard geometry
+// (Sec. 3.2), and the two-stream chunk pipeline (Sec. 4.1, Sec. 4.2) that
+// drives the gfx950 kernels.  Declarations and contracts: include/atp.h.
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/atp.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+atp_status fail(atp_status s, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return s;
+}
+
+atp_status hip_fail(hipError_t e, const char* what) {
+    return fail(ATP_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define ATP_CHECK(expr)                                   \
+    do {                                                  \
+        atp_status _s = (expr);                           \
+        if (_s != ATP_OK) return _s;                      \
+    } while (0)
+
+#define HIP_CHECK(expr, what)                             \
+    do {                                                  \
+        hipError_t _e = (expr);                           \
+        if (_e != hipSuccess) return hip_fail(_e, what);  \
+    } while (0)
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+atp_status check_mesh(const atp_mesh* m) {
+    if (!m) return fail(ATP_ERR_INVALID_ARGUMENT, "mesh is NULL");
+    if (m->d1 <= 0 || m->d2 <= 0)
+        return fail(ATP_ERR_INVALID_ARGUMENT, "mesh dims must be positive (d1=%d d2=%d)", m->d1,
+                    m->d2);
+    if (m->i1 < 0 || m->i1 >= m->d1 || m->i2 < 0 || m->i2 >= m->d2)
+        return fail(ATP_ERR_INVALID_ARGUMENT, "coordinate (%d,%d) outside mesh (%d,%d)", m->i1,
+                    m->i2, m->d1, m->d2);
+    return ATP_OK;
+}
+
+atp_status geometry(const atp_mesh* m, int32_t mode, int64_t k, int64_t n, atp_shard* g) {
+    ATP_CHECK(check_mesh(m));
+    if (mode != ATP_ROW_FIRST && mode != ATP_COL_FIRST)
+        return fail(ATP_ERR_INVALID_ARGUMENT, "mode %d is neither row- nor column-first", mode);
+    if (k <= 0 || n <= 0) return fail(ATP_ERR_INVALID_ARGUMENT, "k and n must be positive");
+    // Row-first: W [Shard(0), Shard(1)] -> rows split by d1, columns by d2,
+    // output partial over mesh axis 0.  Column-first: W [Shard(1), Shard(0)]
+    // -> columns split by d1, rows by d2, output partial over mesh axis 1.
+    const bool row = (mode == ATP_ROW_FIRST);
+    const int32_t dk = row ? m->d1 : m->d2;   // splits k
+    const int32_t dn = row ? m->d2 : m->d1;   // splits n
+    const int32_t ik = row ? m->i1 : m->i2;
+    const int32_t in = row ? m->i2 : m->i1;
+    if (k % dk != 0 || n % dn != 0)
+        return fail(ATP_ERR_SHAPE, "k=%lld not divisible by %d or n=%lld not divisible by %d",
+                    (long long)k, dk, (long long)n, dn);
+    g->k_loc = k / dk;
+    g->n_loc = n / dn;
+    g->k_off = (int64_t)ik * g->k_loc;
+    g->n_off = (int64_t)in * g->n_loc;
+    g->red_axis = row ? 0 : 1;
+    g->red_size = dk;
+    g->red_index = ik;
+    g->bwd_axis = row ? 1 : 0;
+    g->bwd_size = dn;
+    g->bwd_index = in;
+    return ATP_OK;
+}
+
+atp_status check_chunks(int64_t tokens, int32_t chunks) {
+    if (tokens < 0) return fail(ATP_ERR_INVALID_ARGUMENT, "tokens must be >= 0");
+    if (chunks < 1 || chunks > ATP_MAX_CHUNKS)
+        return fail(ATP_ERR_INVALID_ARGUMENT, "chunks=%d outside [1, %d]", chunks,
+                    ATP_MAX_CHUNKS);
+    if (tokens % chunks != 0)
+        return fail(ATP_ERR_SHAPE, "tokens=%lld not divisible by chunks=%d", (long long)tokens,
+                    chunks);
+    return ATP_OK;
+}
+
+// A matrix with zero rows is never touched and may be NULL.
+atp_status check_mat(const void* p, int64_t rows, int64_t ld, int64_t cols, const char* name) {
+    if (rows == 0 && !p) return ATP_OK;
+    if (!p) return fail(ATP_ERR_INVALID_ARGUMENT, "%s is NULL", name);
+    if (ld < cols) return fail(ATP_ERR_INVALID_ARGUMENT, "%s: ld %lld < %lld columns", name,
+                               (long long)ld, (long long)cols);
+    if (!aligned16(p)) return fail(ATP_ERR_UNSUPPORTED, "%s is not 16-byte aligned", name);
+    if (ld % 8 != 0 || cols % 8 != 0)
+        return fail(ATP_ERR_UNSUPPORTED, "%s: ld %lld and columns %lld must be multiples of 8",
+                    name, (long long)ld, (long long)cols);
+    return ATP_OK;
+}
+
+atp_status check_vec(const void* p, const char* name) {
+    if (!p) return fail(ATP_ERR_INVALID_ARGUMENT, "%s is NULL", name);
+    if (!aligned16(p)) return fail(ATP_ERR_UNSUPPORTED, "%s is not 16-byte aligned", name);
+    return ATP_OK;
+}
+
+bool valid_epi(int32_t e) { return e >= ATP_EPI_NONE && e <= ATP_EPI_GELU_BWD; }
+bool valid_dtype(int32_t d) { return d == ATP_F32 || d == ATP_BF16; }
+
+// ---------------------------------------------------------------------------
+// events: a per-device pool of synchronisation events, and timing records
+// ---------------------------------------------------------------------------
+std::mutex g_mu;
+std::map<int, std::vector<hipEvent_t>> g_sync_events;   // device -> pool
+
+atp_status sync_events(size_t count, hipEvent_t** out) {
+    int dev = 0;
+    HIP_CHECK(hipGetDevice(&dev), "hipGetDevice");
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto& pool = g_sync_events[dev];
+    while (pool.size() < count) {
+        hipEvent_t e;
+        HIP_CHECK(hipEventCreateWithFlags(&e, hipEventDisableTiming), "hipEventCreateWithFlags");
+        pool.push_back(e);
+    }
+    *out = pool.data();
+    return ATP_OK;
+}
+
+struct ProfRec {
+    const char* name;
+    hipEvent_t beg, end;
+    double flops, bytes;
+};
+bool g_prof_on = false;
+std::vector<ProfRec> g_prof;
+std::vector<hipEvent_t> g_prof_free;
+
+hipEvent_t prof_event() {
+    if (!g_prof_free.empty()) {
+        hipEvent_t e = g_prof_free.back();
+        g_prof_free.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// Run `launch` on stream s, bracketed by timing events when profiling is on.
+template <class F>
+atp_status timed(const char* name, double flops, double bytes, hipStream_t s, F&& launch) {
+    hipEvent_t b = nullptr, e = nullptr;
+    if (g_prof_on) {
+        std::lock_guard<std::mutex> lk(g_mu);
+        b = prof_event();
+        e = prof_event();
+        if (b) (void)hipEventRecord(b, s);
+    }
+    hipError_t err = launch();
+    if (err != hipSuccess) return hip_fail(err, name);
+    if (b && e) {
+        (void)hipEventRecord(e, s);
+        std::lock_guard<std::mutex> lk(g_mu);
+        g_prof.push_back(ProfRec{name, b, e, flops, bytes});
+    }
+    return ATP_OK;
+}
+
+atp_status run_gemm(const atp::GemmProblem& p, hipStream_t s) {
+    if (p.M <= 0 || p.N <= 0) return ATP_OK;
+    const double flops = 2.0 * (double)p.M * (double)p.N * (double)p.K;
+    const double bytes = 2.0 * ((double)p.M * p.K + (double)p.K * p.N) +
+                         (double)p.M * p.N * (p.out_bf16 ? 2.0 : 4.0) +
+                         ((p.epi == atp::EPI_GELU_BWD || p.pre_out) ? 2.0 * p.M * p.N : 0.0);
+    return timed(atp::gemm_kernel_name(p.layout), flops, bytes, s,
+                 [&] { return atp::launch_gemm(p, s); });
+}
+
+atp_status run_reduce(const atp::ReduceProblem& p, hipStream_t s) {
+    if (p.rows <= 0 || p.ncols <= 0) return ATP_OK;
+    const double el = (double)p.rows * (double)p.ncols;
+    const double bytes = el * (4.0 * p.nparts + (p.out_bf16 ? 2.0 : 4.0)) +
+                         ((p.epi == atp::EPI_GELU_BWD || p.pre_out) ? 2.0 * el : 0.0);
+    return timed("partial_reduce", 0.0, bytes, s, [&] { return atp::launch_reduce(p, s); });
+}
+
+atp_status run_colsum(const void* dy, int64_t ld, int64_t T, int64_t N, float* db,
+                      hipStream_t s) {
+    return timed("colsum", (double)T * N, 2.0 * T * N + 4.0 * N, s,
+                 [&] { return atp::launch_colsum(dy, ld, T, N, db, s); });
+}
+
+atp::GemmProblem gemm_problem(int layout, const void* A, int64_t lda, const void* B, int64_t ldb,
+                              void* C, int64_t ldc, bool out_bf16, int epi, int64_t M,
+                              int64_t N, int64_t K) {
+    atp::GemmProblem p;
+    p.layout = layout;
+    p.A = A; p.lda = lda;
+    p.B = B; p.ldb = ldb;
+    p.C = C; p.ldc = ldc;
+    p.out_bf16 = out_bf16;
+    p.epi = epi;
+    p.bias = nullptr;
+    p.pre_in = nullptr;
+    p.pre_out = nullptr;
+    p.M = M; p.N = N; p.K = K;
+    return p;
+}
+
+atp::ReduceProblem reduce_problem(int nparts, const float* const* parts, int64_t ldp,
+                                  int64_t row0, int64_t rows, int64_t ncols, int epi,
+                                  const void* bias, const void* pre_in, void* out, int64_t ldo,
+                                  bool out_bf16, void* pre_out) {
+    atp::ReduceProblem p;
+    memset(&p, 0, sizeof p);
+    p.nparts = nparts;
+    for (int j = 0; j < nparts; ++j) p.parts[j] = parts[j];
+    p.ldp = ldp;
+    p.row0 = row0;
+    p.rows = rows;
+    p.ncols = ncols;
+    p.epi = epi;
+    p.bias = bias;
+    p.pre_in = pre_in;
+    p.out = out;
+    p.ldo = ldo;
+    p.out_bf16 = out_bf16;
+    p.pre_out = pre_out;
+    return p;
+}
+
+// Block-level linear plan: index 0..3 = qkv, out, fc1, fc2.
+struct BlockPlan {
+    atp_shard g[4];
+    int32_t mode[4];
+    int64_t K[4], N[4];
+};
+
+atp_status block_plan(const atp_mesh* m, int32_t bm, int64_t h, BlockPlan* p) {
+    if (bm != ATP_BLOCK_COL && bm != ATP_BLOCK_ROW)
+        return fail(ATP_ERR_INVALID_ARGUMENT, "block mode %d unknown", bm);
+    if (h <= 0) return fail(ATP_ERR_INVALID_ARGUMENT, "h must be positive");
+    const int32_t pc = ATP_COL_FIRST, pr = ATP_ROW_FIRST;
+    const int32_t modes_col[4] = {pc, pr, pc, pr};
+    const int32_t modes_row[4] = {pr, pc, pr, pc};
+    const int64_t K[4] = {h, h, h, 4 * h};
+    const int64_t N[4] = {3 * h, h, 4 * h, h};
+    for (int i = 0; i < 4; ++i) {
+        p->mode[i] = (bm == ATP_BLOCK_COL) ? modes_col[i] : modes_row[i];
+        p->K[i] = K[i];
+        p->N[i] = N[i];
+        ATP_CHECK(geometry(m, p->mode[i], K[i], N[i], &p->g[i]));
+        if (p->g[i].k_loc % 8 || p->g[i].n_loc % 8)
+            return fail(ATP_ERR_UNSUPPORTED, "local block %lldx%lld of linear %d: sizes must be "
+                        "multiples of 8", (long long)p->g[i].k_loc, (long long)p->g[i].n_loc, i);
+    }
+    return ATP_OK;
+}
+
+atp_status check_group(float* const* tab, int32_t size, int64_t rows, int64_t ld, int64_t cols,
+                       const char* name) {
+    if (size > ATP_MAX_GROUP)
+        return fail(ATP_ERR_UNSUPPORTED, "%s: group of %d exceeds %d", name, size,
+                    ATP_MAX_GROUP);
+    if (size == 1) return ATP_OK;
+    if (!tab) return fail(ATP_ERR_INVALID_ARGUMENT, "%s: pointer table is NULL", name);
+    for (int j = 0; j < size; ++j) {
+        char nm[64];
+        snprintf(nm, sizeof nm, "%s[%d]", name, j);
+        ATP_CHECK(check_mat(tab[j], rows, ld, cols, nm));
+    }
+    return ATP_OK;
+}
+
+const char* const kLinearName[4] = {"qkv", "out", "fc1", "fc2"};
+
+}  // namespace
+
+// ===========================================================================
+// exported
+// ===========================================================================
+extern "C" {
+
+const char* atp_status_string(int32_t s) {
+    switch (s) {
+    case ATP_OK: return "ATP_OK";
+    case ATP_ERR_INVALID_ARGUMENT: return "ATP_ERR_INVALID_ARGUMENT";
+    case ATP_ERR_SHAPE: return "ATP_ERR_SHAPE";
+    case ATP_ERR_UNSUPPORTED: return "ATP_ERR_UNSUPPORTED";
+    case ATP_ERR_DEVICE: return "ATP_ERR_DEVICE";
+    default: return "ATP_ERR_UNKNOWN";
+    }
+}
+
+const char* atp_last_error(void) { return g_last_error.c_str(); }
+
+const char* atp_version(void) { return "atp-mi355x 0.1 (gfx950)"; }
+
+atp_status atp_shard_geometry(const atp_mesh* mesh, int32_t mode, int64_t k, int64_t n,
+                              atp_shard* out) {
+    if (!out) return fail(ATP_ERR_INVALID_ARGUMENT, "out is NULL");
+    return geometry(mesh, mode, k, n, out);
+}
+
+atp_status atp_shard_linear_fwd(const atp_mesh* mesh, int32_t mode, int64_t tokens, int64_t k,
+                                int64_t n, int32_t chunks, const void* x_loc, int64_t ldx,
+                                const void* w_loc, int64_t ldw, const void* bias_loc,
+                                int32_t epi, void* y, int32_t y_dtype, int64_t ldy,
+                                void* preact, void* stream, void* const* chunk_done) {
+    atp_shard g;
+    ATP_CHECK(geometry(mesh, mode, k, n, &g));
+    ATP_CHECK(check_chunks(tokens, chunks));
+    ATP_CHECK(check_mat(x_loc, tokens, ldx, g.k_loc, "x_loc"));
+    ATP_CHECK(check_mat(w_loc, g.k_loc, ldw, g.n_loc, "w_loc"));
+    ATP_CHECK(check_mat(y, tokens, ldy, g.n_loc, "y"));
+    if (!valid_epi(epi) || epi == ATP_EPI_GELU_BWD)
+        return fail(ATP_ERR_INVALID_ARGUMENT, "epilogue %d not valid for a forward GEMM", epi);
+    if (!valid_dtype(y_dtype)) return fail(ATP_ERR_INVALID_ARGUMENT, "y_dtype %d", y_dtype);
+    if (g.red_size > 1 && (epi != ATP_EPI_NONE || y_dtype != ATP_F32))
+        return fail(ATP_ERR_INVALID_ARGUMENT,
+                    "reduction group of %d: y is a Partial(SUM) block, it must be f32 with no "
+                    "epilogue (bias and GeLU act after the reduction)", g.red_size);
+    if (epi == ATP_EPI_BIAS || epi == ATP_EPI_BIAS_GELU) ATP_CHECK(check_vec(bias_loc, "bias"));
+    if (preact) {
+        if (epi != ATP_EPI_BIAS_GELU)
+            return fail(ATP_ERR_INVALID_ARGUMENT, "preact is only written by BIAS_GELU");
+        ATP_CHECK(check_mat(preact, tokens, ldy, g.n_loc, "preact"));
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int64_t mc = tokens / chunks;
+    const bool b16 = (y_dtype == ATP_BF16);
+    const size_t esz = b16 ? 2 : 4;
+    for (int32_t c = 0; c < chunks; ++c) {
+        const int64_t r0 = (int64_t)c * mc;
+        atp::GemmProblem p = gemm_problem(
+            atp::LAYOUT_NN, static_cast<const uint16_t*>(x_loc) + r0 * ldx, ldx, w_loc, ldw,
+            static_cast<char*>(y) + r0 * ldy * esz, ldy, b16, epi, mc, g.n_loc, g.k_loc);
+        p.bias = bias_loc;
+        if (preact) p.pre_out = static_cast<uint16_t*>(preact) + r0 * ldy;
+        ATP_CHECK(run_gemm(p, s));
+        if (chunk_done && chunk_done[c])
+            HIP_CHECK(hipEventRecord(static_cast<hipEvent_t>(chunk_done[c]), s), "hipEventRecord");
+    }
+    return ATP_OK;
+}
+
+atp_status atp_chunked_partial_reduce(int32_t red_size, int64_t tokens, int64_t n_loc,
+                                      int32_t chunks, const float* const* partials, int64_t ldp,
+                                      const void* bias_loc, int32_t epi, const void* preact_in,
+                                      void* out, int32_t out_dtype, int64_t ldo, void* preact_out,
+                                      void* stream, void* const* chunk_ready) {
+    if (red_size < 1) return fail(ATP_ERR_INVALID_ARGUMENT, "red_size must be >= 1");
+    if (red_size > ATP_MAX_GROUP)
+        return fail(ATP_ERR_UNSUPPORTED, "red_size %d exceeds %d", red_size, ATP_MAX_GROUP);
+    if (n_loc <= 0) return fail(ATP_ERR_INVALID_ARGUMENT, "n_loc must be positive");
+    ATP_CHECK(check_chunks(tokens, chunks));
+    if (!partials) return fail(ATP_ERR_INVALID_ARGUMENT, "partials is NULL");
+    for (int j = 0; j < red_size; ++j) {
+        char nm[32];
+        snprintf(nm, sizeof nm, "partials[%d]", j);
+        ATP_CHECK(check_mat(partials[j], tokens, ldp, n_loc, nm));
+    }
+    ATP_CHECK(check_mat(out, tokens, ldo, n_loc, "out"));
+    if (!valid_epi(epi)) return fail(ATP_ERR_INVALID_ARGUMENT, "epilogue %d", epi);
+    if (!valid_dtype(out_dtype)) return fail(ATP_ERR_INVALID_ARGUMENT, "out_dtype %d", out_dtype);
+    if (epi == ATP_EPI_BIAS || epi == ATP_EPI_BIAS_GELU) ATP_CHECK(check_vec(bias_loc, "bias"));
+    if (epi == ATP_EPI_GELU_BWD) ATP_CHECK(check_mat(preact_in, tokens, ldo, n_loc, "preact_in"));
+    if (preact_out) {
+        if (epi != ATP_EPI_BIAS_GELU)
+            return fail(ATP_ERR_INVALID_ARGUMENT, "preact_out is only written by BIAS_GELU");
+        ATP_CHECK(check_mat(preact_out, tokens, ldo, n_loc, "preact_out"));
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int64_t mc = tokens / chunks;
+    for (int32_t c = 0; c < chunks; ++c) {
+        if (chunk_ready && chunk_ready[c])
+            HIP_CHECK(hipStreamWaitEvent(s, static_cast<hipEvent_t>(chunk_ready[c]), 0),
+                      "hipStreamWaitEvent");
+        atp::ReduceProblem p = reduce_problem(red_size, partials, ldp, (int64_t)c * mc, mc, n_loc,
+                                              epi, bias_loc, preact_in, out, ldo,
+                                              out_dtype == ATP_BF16, preact_out);
+        ATP_CHECK(run_reduce(p, s));
+    }
+    return ATP_OK;
+}
+
+atp_status atp_shard_linear_bwd(const atp_mesh* mesh, int32_t mode, int64_t tokens, int64_t k,
+                                int64_t n, int32_t chunks, const void* x_loc, int64_t ldx,
+                                const void* w_loc, int64_t ldw, const void* dy, int64_t lddy,
+                                float* dx_partial, int64_t lddx, float* dw, int64_t lddw,
+                                float* db, void* stream, void* const* dx_chunk_done) {
+    atp_shard g;
+    ATP_CHECK(geometry(mesh, mode, k, n, &g));
+    ATP_CHECK(check_chunks(tokens, chunks));
+    ATP_CHECK(check_mat(x_loc, tokens, ldx, g.k_loc, "x_loc"));
+    ATP_CHECK(check_mat(w_loc, g.k_loc, ldw, g.n_loc, "w_loc"));
+    ATP_CHECK(check_mat(dy, tokens, lddy, g.n_loc, "dy"));
+    ATP_CHECK(check_mat(dx_partial, tokens, lddx, g.k_loc, "dx_partial"));
+    ATP_CHECK(check_mat(dw, g.k_loc, lddw, g.n_loc, "dw"));
+    if (db) ATP_CHECK(check_vec(db, "db"));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int64_t mc = tokens / chunks;
+    for (int32_t c = 0; c < chunks; ++c) {
+        const int64_t r0 = (int64_t)c * mc;
+        // dX = dY W^T : B(k=n', col=k') = W[k'][n'], contiguous along the contraction
+        atp::GemmProblem p = gemm_problem(atp::LAYOUT_NT,
+                                          static_cast<const uint16_t*>(dy) + r0 * lddy, lddy,
+                                          w_loc, ldw, dx_partial + r0 * lddx, lddx, false,
+                                          atp::EPI_NONE, mc, g.k_loc, g.n_loc);
+        ATP_CHECK(run_gemm(p, s));
+        if (dx_chunk_done && dx_chunk_done[c])
+            HIP_CHECK(hipEventRecord(static_cast<hipEvent_t>(dx_chunk_done[c]), s),
+                      "hipEventRecord");
+    }
+    // dW = X^T dY over all tokens
+    atp::GemmProblem p = gemm_problem(atp::LAYOUT_TN, x_loc, ldx, dy, lddy, dw, lddw, false,
+                                      atp::EPI_NONE, g.k_loc, g.n_loc, tokens);
+    ATP_CHECK(run_gemm(p, s));
+    if (db) ATP_CHECK(run_colsum(dy, lddy, tokens, g.n_loc, db, s));
+    return ATP_OK;
+}
+
+size_t atp_block_workspace_bytes(const atp_mesh* mesh, int32_t block_mode, int64_t tokens,
+                                 int64_t h, int32_t chunks) {
+    (void)mesh; (void)block_mode; (void)tokens; (void)h; (void)chunks;
+    return 0;
+}
+
+atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
+                         int32_t chunks, const atp_block_weights* w, const atp_block_fwd_io* io,
+                         void* workspace, size_t ws_bytes, void* compute_stream,
+                         void* comm_stream) {
+    (void)workspace; (void)ws_bytes;
+    BlockPlan P;
+    ATP_CHECK(check_mesh(mesh));
+    ATP_CHECK(block_plan(mesh, block_mode, h, &P));
+    ATP_CHECK(check_chunks(tokens, chunks));
+    if (!w || !io) return fail(ATP_ERR_INVALID_ARGUMENT, "weights or io is NULL");
+    for (int i = 0; i < 4; ++i) {
+        char nm[32];
+        snprintf(nm, sizeof nm, "w[%s]", kLinearName[i]);
+        ATP_CHECK(check_mat(w->w[i], P.g[i].k_loc, w->ldw[i], P.g[i].n_loc, nm));
+        snprintf(nm, sizeof nm, "b[%s]", kLinearName[i]);
+        ATP_CHECK(check_vec(w->b[i], nm));
+    }
+    // inputs: x feeds qkv and fc1 (same k split), attn feeds out
+    if (P.g[0].k_loc != P.g[2].k_loc)
+        return fail(ATP_ERR_SHAPE, "qkv and fc1 contract over different blocks of x");
+    ATP_CHECK(check_mat(io->x_loc, tokens, io->ldx, P.g[0].k_loc, "x_loc"));
+    ATP_CHECK(check_mat(io->attn_loc, tokens, io->lda, P.g[1].k_loc, "attn_loc"));
+    ATP_CHECK(check_mat(io->qkv, tokens, io->ld_qkv, P.g[0].n_loc, "qkv"));
+    ATP_CHECK(check_mat(io->o, tokens, io->ld_o, P.g[1].n_loc, "o"));
+    ATP_CHECK(check_mat(io->h, tokens, io->ld_h, P.g[2].n_loc, "h"));
+    ATP_CHECK(check_mat(io->pre, tokens, io->ld_h, P.g[2].n_loc, "pre"));
+    ATP_CHECK(check_mat(io->z, tokens, io->ld_z, P.g[3].n_loc, "z"));
+    if (P.g[3].k_loc != P.g[2].n_loc)
+        return fail(ATP_ERR_SHAPE, "fc2 contracts over %lld columns, fc1 produces %lld",
+                    (long long)P.g[3].k_loc, (long long)P.g[2].n_loc);
+    for (int i = 0; i < 4; ++i) {
+        char nm[32];
+        snprintf(nm, sizeof nm, "partials[%s]", kLinearName[i]);
+        ATP_CHECK(check_group(io->partials[i], P.g[i].red_size, tokens, io->ldp[i], P.g[i].n_loc, nm));
+    }
+
+    hipStream_t cs = static_cast<hipStream_t>(compute_stream);
+    hipStream_t ms = static_cast<hipStream_t>(comm_stream);
+    hipEvent_t* ev = nullptr;
+    // [0]: start, [1]: end, then per linear per chunk GEMM-done, then fc1 reduce-done
+    const size_t n_ev = 2 + 4 * (size_t)chunks + (size_t)chunks;
+    ATP_CHECK(sync_events(n_ev, &ev));
+    hipEvent_t* ev_gemm = ev + 2;
+    hipEvent_t* ev_red1 = ev + 2 + 4 * chunks;
+
+    HIP_CHECK(hipEventRecord(ev[0], cs), "hipEventRecord");
+    HIP_CHECK(hipStreamWaitEvent(ms, ev[0], 0), "hipStreamWaitEvent");
+
+    const int64_t mc = tokens / chunks;
+    const void* A_in[4] = {io->x_loc, io->attn_loc, io->x_loc, io->h};
+    const int64_t lda_in[4] = {io->ldx, io->lda, io->ldx, io->ld_h};
+    void* outp[4] = {io->qkv, io->o, io->h, io->z};
+    const int64_t ldo[4] = {io->ld_qkv, io->ld_o, io->ld_h, io->ld_z};
+    const bool fc1_reduced = P.g[2].red_size > 1;
+
+    for (int L = 0; L < 4; ++L) {
+        const atp_shard& g = P.g[L];
+        const int epi = (L == 2) ? atp::EPI_BIAS_GELU : atp::EPI_BIAS;
+        void* pre = (L == 2) ? io->pre : nullptr;
+        if (g.red_size == 1) {
+            // nothing to reduce: bias (+GeLU) fused in the GEMM, one launch
+            if (L == 3 && fc1_reduced)
+                HIP_CHECK(hipStreamWaitEvent(cs, ev_red1[chunks - 1], 0), "hipStreamWaitEvent");
+            atp::GemmProblem p = gemm_problem(atp::LAYOUT_NN, A_in[L], lda_in[L], w->w[L],
+                                              w->ldw[L], outp[L], ldo[L], true, epi, tokens,
+                                              g.n_loc, g.k_loc);
+            p.bias = w->b[L];
+            p.pre_out = pre;
+            ATP_CHECK(run_gemm(p, cs));
+            continue;
+        }
+        float* own = io->partials[L][g.red_index];
+        for (int32_t c = 0; c < chunks; ++c) {
+            const int64_t r0 = (int64_t)c * mc;
+            if (L == 3 && fc1_reduced)
+                HIP_CHECK(hipStreamWaitEvent(cs, ev_red1[c], 0), "hipStreamWaitEvent");
+            atp::GemmProblem p = gemm_problem(
+                atp::LAYOUT_NN, static_cast<const uint16_t*>(A_in[L]) + r0 * lda_in[L],
+                lda_in[L], w->w[L], w->ldw[L], own + r0 * io->ldp[L], io->ldp[L], false,
+                atp::EPI_NONE, mc, g.n_loc, g.k_loc);
+            ATP_CHECK(run_gemm(p, cs));
+            hipEvent_t e = ev_gemm[L * chunks + c];
+            HIP_CHECK(hipEventRecord(e, cs), "hipEventRecord");
+            HIP_CHECK(hipStreamWaitEvent(ms, e, 0), "hipStreamWaitEvent");
+            atp::ReduceProblem r = reduce_problem(
+                g.red_size, io->partials[L], io->ldp[L], r0, mc, g.n_loc, epi, w->b[L], nullptr,
+                outp[L], ldo[L], true, pre);
+            ATP_CHECK(run_reduce(r, ms));
+            if (L == 2) HIP_CHECK(hipEventRecord(ev_red1[c], ms), "hipEventRecord");
+        }
+    }
+    HIP_CHECK(hipEventRecord(ev[1], ms), "hipEventRecord");
+    HIP_CHECK(hipStreamWaitEvent(cs, ev[1], 0), "hipStreamWaitEvent");
+    return ATP_OK;
+}
+
+atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
+                         int32_t chunks, const atp_block_weights* w, const atp_block_bwd_io* io,
+                         void* workspace, size_t ws_bytes, void* compute_stream,
+                         void* comm_stream) {
+    (void)workspace; (void)ws_bytes;
+    BlockPlan P;
+    ATP_CHECK(check_mesh(mesh));
+    ATP_CHECK(block_plan(mesh, block_mode, h, &P));
+    ATP_CHECK(check_chunks(tokens, chunks));
+    if (!w || !io) return fail(ATP_ERR_INVALID_ARGUMENT, "weights or io is NULL");
+    for (int i = 0; i < 4; ++i) {
+        char nm[32];
+        snprintf(nm, sizeof nm, "w[%s]", kLinearName[i]);
+        ATP_CHECK(check_mat(w->w[i], P.g[i].k_loc, w->ldw[i], P.g[i].n_loc, nm));
+        snprintf(nm, sizeof nm, "dw[%s]", kLinearName[i]);
+        ATP_CHECK(check_mat(io->dw[i], P.g[i].k_loc, w->ldw[i], P.g[i].n_loc, nm));
+        if (io->db[i]) {
+            snprintf(nm, sizeof nm, "db[%s]", kLinearName[i]);
+            ATP_CHECK(check_vec(io->db[i], nm));
+        }
+    }
+    ATP_CHECK(check_mat(io->x_loc, tokens, io->ldx, P.g[0].k_loc, "x_loc"));
+    ATP_CHECK(check_mat(io->attn_loc, tokens, io->lda, P.g[1].k_loc, "attn_loc"));
+    ATP_CHECK(check_mat(io->h, tokens, io->ld_h, P.g[2].n_loc, "h"));
+    ATP_CHECK(check_mat(io->pre, tokens, io->ld_h, P.g[2].n_loc, "pre"));
+    ATP_CHECK(check_mat(io->dz, tokens, io->ld_dz, P.g[3].n_loc, "dz"));
+    ATP_CHECK(check_mat(io->dqkv, tokens, io->ld_dqkv, P.g[0].n_loc, "dqkv"));
+    ATP_CHECK(check_mat(io->d_o, tokens, io->ld_do, P.g[1].n_loc, "d_o"));
+    ATP_CHECK(check_mat(io->dh_pre, tokens, io->ld_h, P.g[2].n_loc, "dh_pre"));
+    ATP_CHECK(check_mat(io->dx_qkv, tokens, io->ld_dx_qkv, P.g[0].k_loc, "dx_qkv"));
+    ATP_CHECK(check_mat(io->dx_fc1, tokens, io->ld_dx_fc1, P.g[2].k_loc, "dx_fc1"));
+    ATP_CHECK(check_mat(io->d_attn, tokens, io->ld_d_attn, P.g[1].k_loc, "d_attn"));
+    if (P.g[3].k_loc != P.g[2].n_loc)
+        return fail(ATP_ERR_SHAPE, "fc2 / fc1 block mismatch");
+    for (int i = 0; i < 4; ++i) {
+        char nm[32];
+        snprintf(nm, sizeof nm, "dx_partials[%s]", kLinearName[i]);
+        ATP_CHECK(check_group(io->dx_partials[i], P.g[i].bwd_size, tokens, io->ld_dxp[i], P.g[i].k_loc,
+                              nm));
+    }
+
+    hipStream_t cs = static_cast<hipStream_t>(compute_stream);
+    hipStream_t ms = static_cast<hipStream_t>(comm_stream);
+    hipEvent_t* ev = nullptr;
+    const size_t n_ev = 2 + 4 * (size_t)chunks + (size_t)chunks;
+    ATP_CHECK(sync_events(n_ev, &ev));
+    hipEvent_t* ev_gemm = ev + 2;
+    hipEvent_t* ev_red2 = ev + 2 + 4 * chunks;
+
+    HIP_CHECK(hipEventRecord(ev[0], cs), "hipEventRecord");
+    HIP_CHECK(hipStreamWaitEvent(ms, ev[0], 0), "hipStreamWaitEvent");
+
+    const int64_t mc = tokens / chunks;
+    const void* Xin[4] = {io->x_loc, io->attn_loc, io->x_loc, io->h};
+    const int64_t ldx_in[4] = {io->ldx, io->lda, io->ldx, io->ld_h};
+    const void* dY[4] = {io->dqkv, io->d_o, io->dh_pre, io->dz};
+    const int64_t ld_dy[4] = {io->ld_dqkv, io->ld_do, io->ld_h, io->ld_dz};
+    void* dXo[4] = {io->dx_qkv, io->d_attn, io->dx_fc1, io->dh_pre};
+    const int64_t ld_dxo[4] = {io->ld_dx_qkv, io->ld_d_attn, io->ld_dx_fc1, io->ld_h};
+    const bool fc2_reduced = P.g[3].bwd_size > 1;
+    const int order[4] = {3, 2, 1, 0};
+
+    for (int oi = 0; oi < 4; ++oi) {
+        const int L = order[oi];
+        const atp_shard& g = P.g[L];
+        const int epi = (L == 3) ? atp::EPI_GELU_BWD : atp::EPI_NONE;
+        const void* pre_in = (L == 3) ? io->pre : nullptr;
+        if (g.bwd_size == 1) {
+            if (L == 2 && fc2_reduced)
+                HIP_CHECK(hipStreamWaitEvent(cs, ev_red2[chunks - 1], 0), "hipStreamWaitEvent");
+            atp::GemmProblem p = gemm_problem(atp::LAYOUT_NT, dY[L], ld_dy[L], w->w[L], w->ldw[L],
+                                              dXo[L], ld_dxo[L], true, epi, tokens, g.k_loc,
+                                              g.n_loc);
+            p.pre_in = pre_in;
+            ATP_CHECK(run_gemm(p, cs));
+        } else {
+            float* own = io->dx_partials[L][g.bwd_index];
+            for (int32_t c = 0; c < chunks; ++c) {
+                const int64_t r0 = (int64_t)c * mc;
+                if (L == 2 && fc2_reduced)
+                    HIP_CHECK(hipStreamWaitEvent(cs, ev_red2[c], 0), "hipStreamWaitEvent");
+                atp::GemmProblem p = gemm_problem(
+                    atp::LAYOUT_NT, static_cast<const uint16_t*>(dY[L]) + r0 * ld_dy[L], ld_dy[L],
+                    w->w[L], w->ldw[L], own + r0 * io->ld_dxp[L], io->ld_dxp[L], false,
+                    atp::EPI_NONE, mc, g.k_loc, g.n_loc);
+                ATP_CHECK(run_gemm(p, cs));
+                hipEvent_t e = ev_gemm[L * chunks + c];
+                HIP_CHECK(hipEventRecord(e, cs), "hipEventRecord");
+                HIP_CHECK(hipStreamWaitEvent(ms, e, 0), "hipStreamWaitEvent");
+                atp::ReduceProblem r = reduce_problem(
+                    g.bwd_size, io->dx_partials[L], io->ld_dxp[L], r0, mc, g.k_loc, epi, nullptr,
+                    pre_in, dXo[L], ld_dxo[L], true, nullptr);
+                ATP_CHECK(run_reduce(r, ms));
+                if (L == 3) HIP_CHECK(hipEventRecord(ev_red2[c], ms), "hipEventRecord");
+            }
+        }
+        // dW = X^T dY (all tokens) runs while the dX reductions drain on ms
+        atp::GemmProblem p = gemm_problem(atp::LAYOUT_TN, Xin[L], ldx_in[L], dY[L], ld_dy[L],
+                                          io->dw[L], w->ldw[L], false, atp::EPI_NONE, g.k_loc,
+                                          g.n_loc, tokens);
+        ATP_CHECK(run_gemm(p, cs));
+        if (io->db[L]) ATP_CHECK(run_colsum(dY[L], ld_dy[L], tokens, g.n_loc, io->db[L], cs));
+    }
+    HIP_CHECK(hipEventRecord(ev[1], ms), "hipEventRecord");
+    HIP_CHECK(hipStreamWaitEvent(cs, ev[1], 0), "hipStreamWaitEvent");
+    return ATP_OK;
+}
+
+void atp_profile_enable(int32_t on) {
+    std::lock_guard<std::mutex> lk(g_mu);
+    g_prof_on = (on != 0);
+}
+
+int32_t atp_profile_collect(atp_kernel_stat* out, int32_t max) {
+    std::vector<ProfRec> recs;
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        recs.swap(g_prof);
+    }
+    std::vector<atp_kernel_stat> agg;
+    int32_t rc = 0;
+    for (const ProfRec& r : recs) {
+        float ms = 0.0f;
+        if (hipEventSynchronize(r.end) != hipSuccess ||
+            hipEventElapsedTime(&ms, r.beg, r.end) != hipSuccess) {
+            rc = -1;
+        }
+        size_t i = 0;
+        for (; i < agg.size(); ++i)
+            if (strcmp(agg[i].name, r.name) == 0) break;
+        if (i == agg.size()) {
+            atp_kernel_stat st;
+            memset(&st, 0, sizeof st);
+            snprintf(st.name, sizeof st.name, "%s", r.name);
+            agg.push_back(st);
+        }
+        agg[i].launches += 1;
+        agg[i].total_ms += ms;
+        agg[i].flops += r.flops;
+        agg[i].bytes += r.bytes;
+    }
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        for (const ProfRec& r : recs) {
+            g_prof_free.push_back(r.beg);
+            g_prof_free.push_back(r.end);
+        }
+    }
+    if (rc < 0) {
+        g_last_error = "hipEventElapsedTime failed";
+        return -1;
+    }
+    int32_t n = 0;
+    for (; n < (int32_t)agg.size() && n < max; ++n) out[n] = agg[n];
+    return n;
+}
+
+}  // extern "C"

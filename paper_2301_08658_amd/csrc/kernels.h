@@ -1,0 +1,56 @@
+// Internal launch interface between the C ABI / pipeline and the gfx950
+// kernels.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace atp {
+
+// Epilogue codes; identical values to atp_epilogue in include/atp.h.
+enum Epi : int { EPI_NONE = 0, EPI_BIAS = 1, EPI_BIAS_GELU = 2, EPI_GELU_BWD = 3 };
+
+// Operand layouts of C[M,N] = sum_k A(m,k) B(k,n):
+//   NN: A(m,k) = A[m*lda + k],  B(k,n) = B[k*ldb + n]   (forward  Y  = X W)
+//   NT: A(m,k) = A[m*lda + k],  B(k,n) = B[n*ldb + k]   (backward dX = dY W^T)
+//   TN: A(m,k) = A[k*lda + m],  B(k,n) = B[k*ldb + n]   (backward dW = X^T dY)
+enum Layout : int { LAYOUT_NN = 0, LAYOUT_NT = 1, LAYOUT_TN = 2 };
+
+struct GemmProblem {
+    int layout;
+    const void* A; int64_t lda;   // bf16
+    const void* B; int64_t ldb;   // bf16
+    void* C; int64_t ldc;         // f32 or bf16, row-major [M, N]
+    bool out_bf16;
+    int epi;
+    const void* bias;             // bf16 [N] for BIAS / BIAS_GELU
+    const void* pre_in;           // bf16 [M, N] (ld ldc) for GELU_BWD
+    void* pre_out;                // bf16 [M, N] (ld ldc) for BIAS_GELU, nullable
+    int64_t M, N, K;
+};
+
+// True if the kernel set has an instance for this (layout, epi, out) combination.
+bool gemm_supported(int layout, int epi, bool out_bf16);
+hipError_t launch_gemm(const GemmProblem& p, hipStream_t s);
+const char* gemm_kernel_name(int layout);
+
+constexpr int kMaxParts = 64;
+
+struct ReduceProblem {
+    int nparts;
+    const float* parts[kMaxParts];  // each f32 [.., ldp]
+    int64_t ldp;
+    int64_t row0, rows, ncols;      // rows [row0, row0+rows), columns [0, ncols)
+    int epi;
+    const void* bias;               // bf16 [ncols]
+    const void* pre_in;             // bf16, ld ldo
+    void* out; int64_t ldo; bool out_bf16;
+    void* pre_out;                  // bf16, ld ldo, nullable
+};
+hipError_t launch_reduce(const ReduceProblem& p, hipStream_t s);
+
+// db[n] = sum_t dy[t*ld + n], dy bf16 [T, N], db f32 [N]; fixed summation order.
+hipError_t launch_colsum(const void* dy, int64_t ld, int64_t T, int64_t N, float* db,
+                         hipStream_t s);
+
+}  // namespace atp

@@ -1,0 +1,203 @@
+// Partial-sum reduction (the arithmetic of the grouped all-reduce of a
+// Partial(SUM) output, Sec. 3.1 / 3.2) with fused bias, GeLU and GeLU'
+// epilogues, and the bias-gradient column sum (Sec. 4.2).
+//
+// The reduction is HBM-bound: per output element it streams nparts fp32
+// values in and one bf16/fp32 value out.  Each thread owns 8 consecutive
+// columns of one row: two 16-byte non-temporal loads per part, all parts
+// of a group of 8 issued before the first add so up to 16 loads are in
+// flight per thread; parts are then summed in group order 0..d-1, so the
+// result is bit-identical on every member of the group.  Rows of a chunk
+// are contiguous, so a launch is one linear sweep of [rows x ncols].
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kernels.h"
+
+namespace atp {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int RT = 256;        // threads per block
+constexpr int PGROUP = 8;      // parts loaded before summing
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+    return __uint_as_float(bits16 << 16);
+}
+
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return 0x7fc0u;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+__device__ __forceinline__ float gelu_f(float x) {
+    return 0.5f * x * (1.0f + erff(x * 0.70710678118654752440f));
+}
+
+__device__ __forceinline__ float gelu_grad_f(float x) {
+    const float cdf = 0.5f * (1.0f + erff(x * 0.70710678118654752440f));
+    const float pdf = 0.39894228040143267794f * expf(-0.5f * x * x);
+    return cdf + x * pdf;
+}
+
+__device__ __forceinline__ void unpack8(const u32x4& w, float* f) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        f[2 * i] = bf16_to_f32(w[i] & 0xffffu);
+        f[2 * i + 1] = bf16_to_f32(w[i] >> 16);
+    }
+}
+
+__device__ __forceinline__ u32x4 pack8(const float* f) {
+    u32x4 w;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        w[i] = f32_to_bf16_rne(f[2 * i]) | (f32_to_bf16_rne(f[2 * i + 1]) << 16);
+    return w;
+}
+
+template <int EPI, bool OUT_BF16>
+__global__ __launch_bounds__(RT) void reduce_kernel(ReduceProblem p) {
+    const int64_t cols8 = p.ncols >> 3;
+    const int64_t total = p.rows * cols8;
+    const int64_t g = (int64_t)blockIdx.x * RT + threadIdx.x;
+    if (g >= total) return;
+    const int64_t r = g / cols8;
+    const int64_t c = (g - r * cols8) << 3;
+    const int64_t row = p.row0 + r;
+    const int64_t off = row * p.ldp + c;
+
+    float s[8];
+    for (int j0 = 0; j0 < p.nparts; j0 += PGROUP) {
+        f32x4 lo[PGROUP], hi[PGROUP];
+#pragma unroll
+        for (int u = 0; u < PGROUP; ++u) {
+            if (j0 + u < p.nparts) {
+                const f32x4* q = reinterpret_cast<const f32x4*>(p.parts[j0 + u] + off);
+                lo[u] = __builtin_nontemporal_load(q);
+                hi[u] = __builtin_nontemporal_load(q + 1);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < PGROUP; ++u) {
+            if (j0 + u < p.nparts) {
+                if (j0 + u == 0) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) { s[e] = lo[u][e]; s[4 + e] = hi[u][e]; }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) { s[e] += lo[u][e]; s[4 + e] += hi[u][e]; }
+                }
+            }
+        }
+    }
+
+    const int64_t oo = row * p.ldo + c;
+    if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_GELU) {
+        float b[8];
+        unpack8(*reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(p.bias) + c), b);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s[e] += b[e];
+    }
+    if constexpr (EPI == EPI_BIAS_GELU) {
+        if (p.pre_out) {
+            const u32x4 w = pack8(s);
+            __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(
+                                               static_cast<uint16_t*>(p.pre_out) + oo));
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s[e] = gelu_f(s[e]);
+    }
+    if constexpr (EPI == EPI_GELU_BWD) {
+        float x[8];
+        unpack8(*reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(p.pre_in) + oo), x);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s[e] *= gelu_grad_f(x[e]);
+    }
+    if constexpr (OUT_BF16) {
+        __builtin_nontemporal_store(pack8(s),
+                                    reinterpret_cast<u32x4*>(static_cast<uint16_t*>(p.out) + oo));
+    } else {
+        f32x4* q = reinterpret_cast<f32x4*>(static_cast<float*>(p.out) + oo);
+        __builtin_nontemporal_store(f32x4{s[0], s[1], s[2], s[3]}, q);
+        __builtin_nontemporal_store(f32x4{s[4], s[5], s[6], s[7]}, q + 1);
+    }
+}
+
+template <int EPI, bool OUT_BF16>
+hipError_t launch_r(const ReduceProblem& p, hipStream_t s) {
+    const int64_t total = p.rows * (p.ncols >> 3);
+    if (total == 0) return hipSuccess;
+    const int64_t blocks = (total + RT - 1) / RT;
+    hipLaunchKernelGGL((reduce_kernel<EPI, OUT_BF16>), dim3((unsigned)blocks), dim3(RT), 0, s, p);
+    return hipGetLastError();
+}
+
+// Column sums: a block owns 64 columns; 32 row lanes x 8 column lanes, each
+// thread 8 columns (one 16-byte load per row), rows t = ty, ty+32, ... in
+// ascending order; the 32 row-lane sums are then added in ascending order.
+constexpr int CS_COLS = 64;
+constexpr int CS_ROWL = 32;
+
+__global__ __launch_bounds__(256) void colsum_kernel(const uint16_t* __restrict__ dy, int64_t ld,
+                                                     int64_t T, int64_t N, float* __restrict__ db) {
+    __shared__ float part[CS_ROWL][CS_COLS];
+    const int tx = threadIdx.x & 7;
+    const int ty = threadIdx.x >> 3;
+    const int64_t c = (int64_t)blockIdx.x * CS_COLS + tx * 8;
+    float s[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s[e] = 0.0f;
+    if (c < N) {
+        for (int64_t t = ty; t < T; t += CS_ROWL) {
+            float f[8];
+            unpack8(*reinterpret_cast<const u32x4*>(dy + t * ld + c), f);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) s[e] += f[e];
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) part[ty][tx * 8 + e] = s[e];
+    __syncthreads();
+    if (threadIdx.x < CS_COLS) {
+        const int64_t col = (int64_t)blockIdx.x * CS_COLS + threadIdx.x;
+        if (col < N) {
+            float acc = part[0][threadIdx.x];
+            for (int r = 1; r < CS_ROWL; ++r) acc += part[r][threadIdx.x];
+            db[col] = acc;
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_reduce(const ReduceProblem& p, hipStream_t s) {
+    const bool b = p.out_bf16;
+    switch (p.epi) {
+    case EPI_NONE:
+        return b ? launch_r<EPI_NONE, true>(p, s) : launch_r<EPI_NONE, false>(p, s);
+    case EPI_BIAS:
+        return b ? launch_r<EPI_BIAS, true>(p, s) : launch_r<EPI_BIAS, false>(p, s);
+    case EPI_BIAS_GELU:
+        return b ? launch_r<EPI_BIAS_GELU, true>(p, s) : launch_r<EPI_BIAS_GELU, false>(p, s);
+    case EPI_GELU_BWD:
+        return b ? launch_r<EPI_GELU_BWD, true>(p, s) : launch_r<EPI_GELU_BWD, false>(p, s);
+    default:
+        return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_colsum(const void* dy, int64_t ld, int64_t T, int64_t N, float* db,
+                         hipStream_t s) {
+    if (N <= 0) return hipSuccess;
+    const int64_t blocks = (N + CS_COLS - 1) / CS_COLS;
+    hipLaunchKernelGGL(colsum_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
+                       static_cast<const uint16_t*>(dy), ld, T, N, db);
+    return hipGetLastError();
+}
+
+}  // namespace atp

@@ -1,0 +1,204 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads and
+exports every symbol include/atp.h declares, the shard geometry agrees with
+the oracle's spec-derived geometry (Sec. 3.2), and every argument error is
+reported before any device work (the pointers used here are never
+dereferenced: each call fails validation first)."""
+import ctypes
+import itertools
+import os
+import re
+
+import pytest
+
+import oracle as O
+import paper_2301_08658_amd as atp
+from paper_2301_08658_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x10000          # 16-byte aligned, never dereferenced
+MISALIGNED = 0x10004
+
+
+def _declared_symbols():
+    txt = open(os.path.join(ROOT, "include", "atp.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(atp_[a-z_0-9]+)\s*\(", txt)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = atp.load_library()
+    decl = _declared_symbols()
+    assert len(decl) >= 10
+    for name in decl:
+        assert hasattr(lib, name), name
+    assert set(decl) == set(B.EXPORTS)
+    assert "gfx950" in atp.atp_version()
+
+
+@pytest.mark.parametrize("mesh", [(1, 1), (2, 2), (2, 4), (4, 2), (8, 1), (1, 8), (3, 2)])
+@pytest.mark.parametrize("mode", [0, 1])
+def test_geometry_matches_oracle(mesh, mode):
+    d1, d2 = mesh
+    K, N = 48 * 8, 96 * 8
+    for i1, i2 in itertools.product(range(d1), range(d2)):
+        g = atp.atp_shard_geometry(atp.mesh(d1, d2, i1, i2), mode, K, N)
+        o = O.shard_geometry(mesh, (i1, i2), mode, K, N)
+        assert (g.k_off, g.k_off + g.k_loc) == (o["k_lo"], o["k_hi"])
+        assert (g.n_off, g.n_off + g.n_loc) == (o["n_lo"], o["n_hi"])
+        assert (g.red_axis, g.red_size, g.red_index) == (o["red_axis"], o["red_size"],
+                                                          o["red_index"])
+        # backward reduces over the other mesh axis (the one that split N)
+        other = 1 - o["red_axis"]
+        assert (g.bwd_axis, g.bwd_size, g.bwd_index) == (other, mesh[other], (i1, i2)[other])
+
+
+def _status(fn, *args):
+    lib = atp.load_library()
+    return getattr(lib, fn)(*args), atp.binding.last_error()
+
+
+def test_geometry_errors():
+    lib = atp.load_library()
+    out = B.atp_shard()
+    m = atp.mesh(2, 4, 1, 3)
+    assert lib.atp_shard_geometry(None, 0, 8, 8, ctypes.byref(out)) == B.ATP_ERR_INVALID_ARGUMENT
+    assert lib.atp_shard_geometry(ctypes.byref(m), 0, 8, 8, None) == B.ATP_ERR_INVALID_ARGUMENT
+    assert lib.atp_shard_geometry(ctypes.byref(m), 2, 8, 8, ctypes.byref(out)) == \
+        B.ATP_ERR_INVALID_ARGUMENT
+    assert lib.atp_shard_geometry(ctypes.byref(m), 0, 7, 8, ctypes.byref(out)) == B.ATP_ERR_SHAPE
+    assert lib.atp_shard_geometry(ctypes.byref(m), 0, 8, 6, ctypes.byref(out)) == B.ATP_ERR_SHAPE
+    bad = atp.mesh(2, 4, 2, 0)
+    assert lib.atp_shard_geometry(ctypes.byref(bad), 0, 8, 8, ctypes.byref(out)) == \
+        B.ATP_ERR_INVALID_ARGUMENT
+    assert "outside" in atp.binding.last_error()
+    z = atp.mesh(0, 4, 0, 0)
+    assert lib.atp_shard_geometry(ctypes.byref(z), 0, 8, 8, ctypes.byref(out)) == \
+        B.ATP_ERR_INVALID_ARGUMENT
+
+
+def _fwd(m, mode=0, tokens=64, k=256, n=256, chunks=2, x=FAKE, ldx=None, w=FAKE, ldw=None,
+         bias=None, epi=0, y=FAKE, ydt=0, ldy=None, pre=None):
+    g = atp.atp_shard_geometry(m, mode, 256, 256)
+    lib = atp.load_library()
+    return lib.atp_shard_linear_fwd(ctypes.byref(m), mode, tokens, k, n, chunks, x,
+                                    ldx or g.k_loc, w, ldw or g.n_loc, bias, epi, y, ydt,
+                                    ldy or g.n_loc, pre, None, None)
+
+
+def test_linear_fwd_validation():
+    m = atp.mesh(2, 2, 1, 0)
+    assert _fwd(m, chunks=3) == B.ATP_ERR_SHAPE                 # 64 % 3
+    assert _fwd(m, chunks=0) == B.ATP_ERR_INVALID_ARGUMENT
+    assert _fwd(m, chunks=B.ATP_MAX_CHUNKS + 1, tokens=0) == B.ATP_ERR_INVALID_ARGUMENT
+    assert _fwd(m, tokens=-1) == B.ATP_ERR_INVALID_ARGUMENT
+    assert _fwd(m, x=None) == B.ATP_ERR_INVALID_ARGUMENT
+    assert _fwd(m, x=MISALIGNED) == B.ATP_ERR_UNSUPPORTED
+    assert _fwd(m, ldx=64) == B.ATP_ERR_INVALID_ARGUMENT         # ld < k_loc = 128
+    assert _fwd(m, ldw=132) == B.ATP_ERR_UNSUPPORTED             # ld not a multiple of 8
+    assert _fwd(m, k=255) == B.ATP_ERR_SHAPE
+    # a partial output (group of 2) cannot take the bias / GeLU or a bf16 store
+    assert _fwd(m, epi=1, bias=FAKE) == B.ATP_ERR_INVALID_ARGUMENT
+    assert "Partial" in atp.binding.last_error()
+    assert _fwd(m, ydt=1) == B.ATP_ERR_INVALID_ARGUMENT
+    # group of one: BIAS needs the bias vector; GELU_BWD is not a forward epilogue
+    m1 = atp.mesh(1, 1, 0, 0)
+    assert _fwd(m1, epi=1, bias=None) == B.ATP_ERR_INVALID_ARGUMENT
+    assert _fwd(m1, epi=3) == B.ATP_ERR_INVALID_ARGUMENT
+    assert _fwd(m1, epi=0, pre=FAKE) == B.ATP_ERR_INVALID_ARGUMENT   # preact only with GeLU
+    assert _fwd(m1, ydt=7) == B.ATP_ERR_INVALID_ARGUMENT
+
+
+def _red(red_size=2, tokens=64, n=256, chunks=2, parts=(FAKE, FAKE), ldp=256, bias=None,
+         epi=0, pin=None, out=FAKE, odt=0, ldo=256, pout=None):
+    lib = atp.load_library()
+    arr = (ctypes.c_void_p * max(1, len(parts)))(*parts) if parts is not None else None
+    tab = ctypes.cast(arr, B._fpp) if arr is not None else None
+    return lib.atp_chunked_partial_reduce(red_size, tokens, n, chunks, tab, ldp, bias, epi, pin,
+                                          out, odt, ldo, pout, None, None)
+
+
+def test_reduce_validation():
+    assert _red(red_size=0) == B.ATP_ERR_INVALID_ARGUMENT
+    assert _red(red_size=B.ATP_MAX_GROUP + 1) == B.ATP_ERR_UNSUPPORTED
+    assert _red(parts=None) == B.ATP_ERR_INVALID_ARGUMENT
+    assert _red(parts=(FAKE, 0)) == B.ATP_ERR_INVALID_ARGUMENT
+    assert "partials[1]" in atp.binding.last_error()
+    assert _red(parts=(FAKE, MISALIGNED)) == B.ATP_ERR_UNSUPPORTED
+    assert _red(chunks=5) == B.ATP_ERR_SHAPE
+    assert _red(n=250, ldp=256, ldo=256) == B.ATP_ERR_UNSUPPORTED
+    assert _red(ldp=128) == B.ATP_ERR_INVALID_ARGUMENT
+    assert _red(epi=1) == B.ATP_ERR_INVALID_ARGUMENT               # bias missing
+    assert _red(epi=3) == B.ATP_ERR_INVALID_ARGUMENT               # preact_in missing
+    assert _red(epi=9) == B.ATP_ERR_INVALID_ARGUMENT
+    assert _red(epi=1, bias=FAKE, pout=FAKE) == B.ATP_ERR_INVALID_ARGUMENT
+    assert _red(odt=5) == B.ATP_ERR_INVALID_ARGUMENT
+
+
+def test_linear_bwd_validation():
+    lib = atp.load_library()
+    m = atp.mesh(2, 4, 1, 1)
+    g = atp.atp_shard_geometry(m, 1, 256, 512)
+
+    def call(**kw):
+        a = dict(x=FAKE, ldx=g.k_loc, w=FAKE, ldw=g.n_loc, dy=FAKE, lddy=g.n_loc, dx=FAKE,
+                 lddx=g.k_loc, dw=FAKE, lddw=g.n_loc, db=None, tokens=64, chunks=4)
+        a.update(kw)
+        return lib.atp_shard_linear_bwd(ctypes.byref(m), 1, a["tokens"], 256, 512, a["chunks"],
+                                        a["x"], a["ldx"], a["w"], a["ldw"], a["dy"], a["lddy"],
+                                        a["dx"], a["lddx"], a["dw"], a["lddw"], a["db"], None,
+                                        None)
+    assert call(dy=None) == B.ATP_ERR_INVALID_ARGUMENT
+    assert call(dx=MISALIGNED) == B.ATP_ERR_UNSUPPORTED
+    assert call(lddw=8) == B.ATP_ERR_INVALID_ARGUMENT
+    assert call(chunks=3) == B.ATP_ERR_SHAPE
+    assert call(db=MISALIGNED) == B.ATP_ERR_UNSUPPORTED
+
+
+def test_block_validation():
+    lib = atp.load_library()
+    h, T = 512, 256
+    m = atp.mesh(2, 2, 0, 1)
+    G = atp.block_geometry(m, B.ATP_BLOCK_COL, h)
+    W = B.atp_block_weights()
+    for i, g in enumerate(G):
+        W.w[i] = FAKE
+        W.ldw[i] = g.n_loc
+        W.b[i] = FAKE
+    io = B.atp_block_fwd_io()
+    io.x_loc, io.ldx = FAKE, G[0].k_loc
+    io.attn_loc, io.lda = FAKE, G[1].k_loc
+    io.qkv, io.ld_qkv = FAKE, G[0].n_loc
+    io.o, io.ld_o = FAKE, G[1].n_loc
+    io.h, io.ld_h = FAKE, G[2].n_loc
+    io.pre = FAKE
+    io.z, io.ld_z = FAKE, G[3].n_loc
+    keep = []
+    for i, g in enumerate(G):
+        arr = (ctypes.c_void_p * g.red_size)(*([FAKE] * g.red_size))
+        keep.append(arr)
+        io.partials[i] = ctypes.cast(arr, B._fpp)
+        io.ldp[i] = g.n_loc
+
+    def call(mm=m, bm=0, tokens=T, hh=h, chunks=2):
+        return lib.atp_block_fwd(ctypes.byref(mm), bm, tokens, hh, chunks, ctypes.byref(W),
+                                 ctypes.byref(io), None, 0, None, None)
+    assert call(bm=5) == B.ATP_ERR_INVALID_ARGUMENT
+    assert call(hh=500) == B.ATP_ERR_UNSUPPORTED or call(hh=500) == B.ATP_ERR_SHAPE
+    assert call(chunks=3) == B.ATP_ERR_SHAPE
+    assert call(mm=atp.mesh(2, 2, 2, 0)) == B.ATP_ERR_INVALID_ARGUMENT
+    io.partials[3] = None
+    assert call() == B.ATP_ERR_INVALID_ARGUMENT
+    assert "partials[fc2]" in atp.binding.last_error()
+    io.partials[3] = ctypes.cast(keep[3], B._fpp)
+    W.b[2] = None
+    assert call() == B.ATP_ERR_INVALID_ARGUMENT
+    W.b[2] = FAKE
+    io.ld_h = G[2].n_loc - 8
+    assert call() == B.ATP_ERR_INVALID_ARGUMENT
+    assert lib.atp_block_workspace_bytes(ctypes.byref(m), 0, T, h, 2) == 0
+
+
+def test_status_strings():
+    assert atp.binding.status_string(0) == "ATP_OK"
+    assert atp.binding.status_string(2) == "ATP_ERR_SHAPE"
+    assert atp.binding.status_string(99) == "ATP_ERR_UNKNOWN"
