@@ -1,0 +1,293 @@
+#!/usr/bin/env python3
+"""Benchmark of one device's share of an ATP transformer layer on MI355X.
+
+A step is one pass of the whole hot path on one batch: the block forward
+(QKV, out-proj, fc1+GeLU, fc2 local GEMMs with chunked Partial(SUM)
+reductions overlapping the next chunk's GEMM, Sec. 3.2.1 / Sec. 4.1) and the
+block backward (dX chunks with overlapped reductions, dW, db; Sec. 4.2).
+The other group members' partial buffers are seeded inputs resident in
+HBM (one GPU stands in for the mesh).  Default workload: h = 20480,
+4096 tokens, DeviceMesh(8, 1), column-first block, 8 chunks.
+
+Prints ONE JSON line on stdout; diagnostics go to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+if HERE not in sys.path:
+    sys.path.insert(0, HERE)
+
+METRIC = "TFLOP/s per GPU, chunked 2D-TP shard MLP+attn-proj block; MFMA util %"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+DEFAULT_WORKLOAD = "wide_h20480_col_8x1"
+LIN = ("qkv", "out", "fc1", "fc2")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--chunks", type=int, default=None, help="override the chunk count")
+    ap.add_argument("--fwd-only", action="store_true", help="time the forward only")
+    ap.add_argument("--serial", action="store_true",
+                    help="run reductions on the compute stream (no overlap)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=6,
+                    help="token rows in the oracle's timed CPU sample")
+    ap.add_argument("--copy-calib-mb", type=int, default=0,
+                    help="after timing, run one plain device copy of this many MiB "
+                         "(reference kernel for scaling HBM counters)")
+    ap.add_argument("--seed", type=int, default=21)
+    return ap.parse_args()
+
+
+def setup(torch, atp, S, wl, chunks, seed):
+    """Device-resident seeded inputs and outputs of one device's share."""
+    dev = "cuda:0"
+    d1, d2 = wl["mesh"]
+    m = atp.mesh(d1, d2, 0, 0)
+    bm = atp.ATP_BLOCK_COL if wl["mode"] == "col" else atp.ATP_BLOCK_ROW
+    h, T, sw = wl["h"], wl["tokens"], wl["sigma_w"]
+    G = atp.block_geometry(m, bm, h)
+    rnd = lambda shape, std, tid, dt=torch.bfloat16: S.randn_device(  # noqa: E731
+        shape, std, seed, tid, dev, dtype=dt)
+    st = dict(m=m, bm=bm, G=G, T=T, h=h, chunks=chunks)
+    st["x"] = rnd((T, G[0].k_loc), 1.0, S.TID["x"])
+    st["a"] = rnd((T, G[1].k_loc), 1.0, S.TID["a"])
+    st["w"] = [rnd((g.k_loc, g.n_loc), sw, S.TID["w_" + n]) for g, n in zip(G, LIN)]
+    st["b"] = [torch.zeros(g.n_loc, dtype=torch.bfloat16, device=dev) for g in G]
+    emp = lambda r, c, dt=torch.bfloat16: torch.empty((r, c), dtype=dt, device=dev)  # noqa
+    st["fwd_tabs"], st["bwd_tabs"] = [], []
+    for i, g in enumerate(G):
+        if g.red_size > 1:
+            sp = S.peer_sigma(g.k_loc, sw, 1.0)
+            tab = [rnd((T, g.n_loc), sp, S.PEER_TID_BASE + 100 * i + j, torch.float32)
+                   for j in range(g.red_size)]
+            st["fwd_tabs"].append(tab)        # entry red_index is overwritten (own)
+        else:
+            st["fwd_tabs"].append(None)
+        if g.bwd_size > 1:
+            sp = S.peer_sigma(g.n_loc, sw, 1.0)
+            tab = [rnd((T, g.k_loc), sp, S.BWD_PEER_TID_BASE + 100 * i + j, torch.float32)
+                   for j in range(g.bwd_size)]
+            st["bwd_tabs"].append(tab)
+        else:
+            st["bwd_tabs"].append(None)
+    st["qkv"], st["o"] = emp(T, G[0].n_loc), emp(T, G[1].n_loc)
+    st["hh"], st["pre"], st["z"] = emp(T, G[2].n_loc), emp(T, G[2].n_loc), emp(T, G[3].n_loc)
+    st["dz"] = rnd((T, G[3].n_loc), 1.0, S.TID["dz"])
+    st["dqkv"] = rnd((T, G[0].n_loc), 1.0, S.TID["dqkv"])
+    st["do"] = rnd((T, G[1].n_loc), 1.0, S.TID["do"])
+    st["dh_pre"] = emp(T, G[2].n_loc)
+    st["dx_qkv"], st["dx_fc1"] = emp(T, G[0].k_loc), emp(T, G[2].k_loc)
+    st["d_attn"] = emp(T, G[1].k_loc)
+    st["dw"] = [torch.empty((g.k_loc, g.n_loc), dtype=torch.float32, device=dev) for g in G]
+    st["db"] = [torch.empty((g.n_loc,), dtype=torch.float32, device=dev) for g in G]
+    return st
+
+
+def step_flops(st, fwd_only):
+    f = sum(2.0 * st["T"] * g.k_loc * g.n_loc for g in st["G"])
+    return f if fwd_only else 3.0 * f
+
+
+def make_step(torch, atp, st, fwd_only, serial):
+    cs = torch.cuda.current_stream()
+    ms = cs if serial else torch.cuda.Stream()
+
+    def step():
+        atp.atp_block_fwd(st["m"], st["bm"], st["T"], st["h"], st["chunks"], st["w"], st["b"],
+                          st["x"], st["a"], st["fwd_tabs"], st["qkv"], st["o"], st["hh"],
+                          st["pre"], st["z"], compute_stream=cs, comm_stream=ms)
+        if fwd_only:
+            return
+        atp.atp_block_bwd(st["m"], st["bm"], st["T"], st["h"], st["chunks"], st["w"], st["b"],
+                          st["x"], st["a"], st["hh"], st["pre"], st["dz"], st["dqkv"], st["do"],
+                          st["bwd_tabs"], st["dh_pre"], st["dx_qkv"], st["dx_fc1"],
+                          st["d_attn"], st["dw"], st["db"], compute_stream=cs,
+                          comm_stream=ms)
+    return step
+
+
+def cpu_baseline(st, rows_n, fwd_only, seed):
+    """The oracle, as it stands, timed on a bounded sample of the same
+    workload: the block forward (and input-gradient backward) for a few
+    token rows, and dW / db for one column of each linear."""
+    import numpy as np
+    import torch
+    import oracle as O
+
+    G, T = st["G"], st["T"]
+    rng = np.random.default_rng(seed)
+    rows = sorted(rng.choice(T, size=rows_n, replace=False).tolist())
+    cpu = lambda t: t.detach().cpu()  # noqa: E731
+    W = [O._f64(cpu(w)) for w in st["w"]]
+    Wt = [np.ascontiguousarray(w.T) for w in W]
+    x, a = O._f64(cpu(st["x"][rows])), O._f64(cpu(st["a"][rows]))
+    bias = [O._f64(cpu(b)) for b in st["b"]]
+    ftab = [[O._f64(cpu(p[rows])) for p in t] if t else None for t in st["fwd_tabs"]]
+    btab = [[O._f64(cpu(p[rows])) for p in t] if t else None for t in st["bwd_tabs"]]
+    dz, dq, do = (O._f64(cpu(st[k][rows])) for k in ("dz", "dqkv", "do"))
+    xs_full = O._f64(cpu(st["x"]))
+    dq_col = O._f64(cpu(st["dqkv"][:, :1]))
+    torch.set_num_threads(max(1, os.cpu_count() or 1))
+    flops = 0.0
+
+    def red(i, own, tab, idx, epi, b=None, pre=None):
+        parts = [own] if tab is None else tab[:idx] + [own] + tab[idx + 1:]
+        return O.partial_reduce(parts, b, epi, pre)
+
+    t0 = time.perf_counter()
+    # forward, sampled rows
+    qkv, _ = red(0, O.matmul(x, W[0]), ftab[0], G[0].red_index, O.EPI_BIAS, bias[0])
+    o, _ = red(1, O.matmul(a, W[1]), ftab[1], G[1].red_index, O.EPI_BIAS, bias[1])
+    hh, pre = red(2, O.matmul(x, W[2]), ftab[2], G[2].red_index, O.EPI_BIAS_GELU, bias[2])
+    z, _ = red(3, O.matmul(O.round_bf16(hh), W[3]), ftab[3], G[3].red_index, O.EPI_BIAS,
+               bias[3])
+    flops += sum(2.0 * rows_n * g.k_loc * g.n_loc for g in G)
+    if not fwd_only:
+        # input gradients, sampled rows
+        dh, _ = red(3, O.matmul(dz, Wt[3]), btab[3], G[3].bwd_index, O.EPI_GELU_BWD, None, pre)
+        red(2, O.matmul(O.round_bf16(dh), Wt[2]), btab[2], G[2].bwd_index, O.EPI_NONE)
+        red(1, O.matmul(do, Wt[1]), btab[1], G[1].bwd_index, O.EPI_NONE)
+        red(0, O.matmul(dq, Wt[0]), btab[0], G[0].bwd_index, O.EPI_NONE)
+        flops += sum(2.0 * rows_n * g.k_loc * g.n_loc for g in G)
+        # one dW column (all tokens) of the qkv linear
+        O.matmul(xs_full.T, dq_col)
+        O.colsum(dq_col)
+        flops += 2.0 * T * G[0].k_loc
+    dt = time.perf_counter() - t0
+    sample = (f"{rows_n} token rows of the block forward" +
+              ("" if fwd_only else " and input-gradient backward, plus one dW column of qkv") +
+              f" ({flops / 1e9:.1f} GFLOP)")
+    return dict(value=flops / dt / 1e12, unit="TFLOP/s", cores=O.num_threads(), kind="oracle",
+                sample=sample, seconds=round(dt, 3))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs one device's share on one GPU; --gpus {args.gpus} "
+              "is not supported (the multi-GPU exchange is not part of it).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2301_08658_amd as atp
+    import synth_inputs as S
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(3)
+    wl = dict(S.WORKLOADS[args.workload])
+    chunks = args.chunks or wl["chunks"]
+    fwd_only = args.fwd_only or not wl.get("bwd", False)
+    atp.load_library()
+    log(f"[bench] {atp.atp_version()} workload={args.workload} chunks={chunks} "
+        f"pass={'fwd' if fwd_only else 'fwd+bwd'}")
+    st = setup(torch, atp, S, wl, chunks, args.seed)
+    torch.cuda.synchronize()
+    step = make_step(torch, atp, st, fwd_only, args.serial)
+    flops = step_flops(st, fwd_only)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"[bench] warmup done ({args.warmup} steps)")
+
+    # timed region: inputs resident, K steps between two device-wide syncs
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record()
+    for _ in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = max(ev0.elapsed_time(ev1), wall * 1e3) / args.steps
+    value = flops / (ms_step * 1e-3) / 1e12
+    log(f"[bench] {args.steps} steps, {ms_step:.3f} ms/step, {value:.1f} TFLOP/s")
+
+    # same K steps again with every library launch bracketed by HIP events on
+    # its own stream: per-kernel durations for the roofline
+    atp.atp_profile_enable(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    atp.atp_profile_enable(False)
+    stats = atp.atp_profile_collect(64)
+    kernels = []
+    for s in stats:
+        avg = s["total_ms"] / max(1, s["launches"])
+        ent = dict(name=s["name"], launches=s["launches"] // args.steps,
+                   avg_us=round(avg * 1e3, 2), ms_per_step=round(s["total_ms"] / args.steps, 4))
+        if s["flops"] and s["name"].startswith("gemm"):
+            ent["tflops"] = round(s["flops"] / (s["total_ms"] * 1e-3) / 1e12, 1)
+        if s["name"] in ("partial_reduce", "colsum"):
+            ent["gbs"] = round(s["bytes"] / (s["total_ms"] * 1e-3) / 1e9, 1)
+        kernels.append(ent)
+    gemms = [s for s in stats if s["name"].startswith("gemm")]
+    dom = max(gemms, key=lambda s: s["total_ms"])
+    achieved = dom["flops"] / (dom["total_ms"] * 1e-3) / 1e12
+    roofline = dict(bound="mfma", kernel=dom["name"], achieved=round(achieved, 1),
+                    peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
+                    frac=round(achieved / PEAK_BF16_TFLOPS, 4), traffic=None,
+                    flops_per_launch=dom["flops"] / dom["launches"],
+                    avg_launch_us=round(dom["total_ms"] / dom["launches"] * 1e3, 2))
+    red = [s for s in stats if s["name"] == "partial_reduce"]
+    reduce_info = None
+    if red:
+        r = red[0]
+        gbs = r["bytes"] / (r["total_ms"] * 1e-3) / 1e9
+        reduce_info = dict(achieved=round(gbs, 1), peak=PEAK_HBM_GBS, unit="GB/s",
+                           frac=round(gbs / PEAK_HBM_GBS, 4),
+                           bytes_per_step=r["bytes"] / args.steps,
+                           note="durations measured while overlapping the GEMMs")
+    for k in kernels:
+        log(f"[bench]   {k}")
+
+    if args.copy_calib_mb:
+        n = args.copy_calib_mb * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy of {args.copy_calib_mb} MiB done")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a sample")
+        cpu = cpu_baseline(st, args.cpu_rows, fwd_only, args.seed)
+        log(f"[bench] cpu baseline: {cpu}")
+
+    d1, d2 = wl["mesh"]
+    out = dict(
+        metric=METRIC, value=round(value, 2), unit="TFLOP/s", n_gpus=1, steps=args.steps,
+        warmup=args.warmup, ms_per_step=round(ms_step, 4), higher_is_better=True,
+        scaling="weak", vs_baseline=None, dtype="bf16", data="synthetic",
+        config=dict(workload=args.workload, mode=wl["mode"], mesh=[d1, d2], coord=[0, 0],
+                    tokens=wl["tokens"], h=wl["h"], chunks=chunks,
+                    **{"pass": "fwd" if fwd_only else "fwd+bwd"},
+                    serial=bool(args.serial), gflop_per_step=round(flops / 1e9, 1)),
+        mfma_util=round(value / PEAK_BF16_TFLOPS, 4),
+        roofline=roofline, reduce=reduce_info, kernels=kernels, cpu_baseline=cpu)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

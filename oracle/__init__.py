@@ -91,6 +91,8 @@ def _load():
                                        dp, ctypes.c_int, dp, dp, i64, dp]
     lib.orc_colsum.argtypes = [i64, i64, dp, i64, dp]
     lib.orc_num_threads.restype = ctypes.c_int
+    lib.orc_round_bf16.argtypes = [ctypes.c_double]
+    lib.orc_round_bf16.restype = ctypes.c_double
     _lib = lib
     return lib
 
@@ -183,10 +185,10 @@ def reduction_group(mesh, coord, axis):
 # arithmetic
 # --------------------------------------------------------------------------
 def matmul(A, B) -> np.ndarray:
-    """C = A @ B in fp64, ascending-k sums (Y = XW of Sec. 3.2).  A and B may be
-    transposed views; strides are passed through unchanged."""
-    A = _f64(A)
-    B = _f64(B)
+    """C = A @ B in fp64, ascending-k sums (Y = XW of Sec. 3.2).  Transposed
+    views are copied to row-major first (only the memory order changes)."""
+    A = np.ascontiguousarray(_f64(A))
+    B = np.ascontiguousarray(_f64(B))
     M, K = A.shape
     K2, N = B.shape
     assert K == K2
@@ -197,6 +199,14 @@ def matmul(A, B) -> np.ndarray:
                            _dptr(B), B.strides[0] // isz, B.strides[1] // isz,
                            _dptr(C), N, 1)
     return C
+
+
+def round_bf16(x):
+    """Sec. 5: inter-layer tensors are 16-bit; round fp64 values to bfloat16
+    (ties to even).  Returned as fp64."""
+    lib = _load()
+    x = _f64(x)
+    return np.vectorize(lib.orc_round_bf16, otypes=[np.float64])(x)
 
 
 def gelu(x):
@@ -298,15 +308,16 @@ def block_shapes(h):
 
 
 def block_fwd_local(block_mode, mesh, coord, x_loc, a_loc, w, b, peers,
-                    round_h=None):
+                    round_h=round_bf16):
     """Forward of one device's share of the block, from its local inputs.
 
     x_loc: the device's block of the layer input X (the columns its QKV and
     fc1 shards contract over); a_loc: its block of the attention-core output
     that feeds out-proj; w[name], b[name]: local weight and bias blocks;
     peers[name]: the other group members' partial blocks in group order.
-    `round_h`, if given, maps the fp64 GeLU output to the values the next
-    GEMM consumes (e.g. bf16 rounding); the oracle's own reading is None.
+    `round_h` maps the fp64 GeLU output to the values fc2 consumes: the
+    layer's activations are 16-bit tensors (Sec. 5, half precision; bfloat16
+    here), so by default fc2 reads H rounded to bfloat16.  None keeps fp64.
     Returns dict of qkv, o, h (GeLU output), pre (fc1 pre-activation), z.
     """
     modes = block_linear_modes(block_mode)
@@ -352,14 +363,15 @@ def block_fwd_global(block_mode, mesh, coord, X, A, W, B):
 
 
 def block_bwd_local(block_mode, mesh, coord, x_loc, a_loc, h_loc, pre_loc, w,
-                    dz, dqkv, do, peers, round_dpre=None):
+                    dz, dqkv, do, peers, round_dpre=round_bf16):
     """Backward of one device's share of the block (Sec. 4.2).
 
     dz, dqkv, do: gradients of the device's reduced output blocks z, qkv, o.
     peers[name]: the other group members' dX partials for the reduction of
     each linear's input gradient, in group order (the backward group of a
     linear is the mesh dimension that split its N).  fc2's reduced input
-    gradient is multiplied by GeLU'(pre) to give fc1's dY.
+    gradient is multiplied by GeLU'(pre) to give fc1's dY, which fc1's
+    backward GEMMs read as a 16-bit tensor (Sec. 5; `round_dpre`).
     Returns dict with dx_qkv, da, dh_pre (fc1's dY), dx_fc1 and dw_*/db_*.
     """
     modes = block_linear_modes(block_mode)

@@ -131,6 +131,18 @@ void orc_colsum(int64_t T, int64_t N, const double* dy, int64_t ld, double* db) 
     }
 }
 
+double orc_round_bf16(double x) {
+    if (isnan(x) || isinf(x) || x == 0.0) return x;
+    int e;
+    (void)frexp(fabs(x), &e);          /* |x| = m * 2^e, m in [0.5, 1) */
+    int q = e - 8;                     /* quantum of an 8-significant-bit value */
+    if (q < -133) q = -133;            /* subnormal spacing 2^-133 */
+    const double r = nearbyint(ldexp(fabs(x), -q));   /* ties to even */
+    double y = ldexp(r, q);
+    if (y > 3.38953138925153547590e38) y = INFINITY;  /* above the largest bfloat16 */
+    return copysign(y, x);
+}
+
 int orc_num_threads(void) {
 #ifdef _OPENMP
     return omp_get_max_threads();

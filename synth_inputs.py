@@ -80,3 +80,24 @@ def randn_device(shape, std: float, seed: int, tid: int, device, dtype=torch.bfl
     if std != 1.0:
         t.mul_(std)
     return t.to(dtype)
+
+
+# --------------------------------------------------------------------------
+# Workloads (sizes follow the paper's GPT layers: Table 2 hidden sizes,
+# batch x sequence 2048, Sec. 5), named by what they are.
+# mode: "col" = QKV/fc1 column-first, out/fc2 row-first; "row" = swapped.
+# --------------------------------------------------------------------------
+WORKLOADS = {
+    "tiny_mlp_h512_col_2x2": dict(mode="col", mesh=(2, 2), tokens=256, h=512, chunks=2,
+                                  sigma_w=0.02, bwd=False),
+    "gpt_h4096_col_2x4": dict(mode="col", mesh=(2, 4), tokens=8192, h=4096, chunks=4,
+                              sigma_w=0.02, bwd=False),
+    "gpt_h4096_row_4x2": dict(mode="row", mesh=(4, 2), tokens=8192, h=4096, chunks=4,
+                              sigma_w=0.02, bwd=True, chunk_sweep=(1, 2, 4, 8)),
+    "gpt3_h12288_col_4x2": dict(mode="col", mesh=(4, 2), tokens=2048, h=12288, chunks=4,
+                                sigma_w=0.02, bwd=True),
+    "wide_h20480_col_8x1": dict(mode="col", mesh=(8, 1), tokens=4096, h=20480, chunks=8,
+                                sigma_w=0.01, bwd=True),
+    "wide_h20480_col_2x4": dict(mode="col", mesh=(2, 4), tokens=4096, h=20480, chunks=8,
+                                sigma_w=0.01, bwd=True),
+}

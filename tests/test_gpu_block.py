@@ -1,0 +1,291 @@
+"""GPU parity of the whole shard block (Sec. 3.2.1 forward, Sec. 4.2
+backward) with chunk-based overlapping (Sec. 4.1).
+
+* bench mode: the other group members' partial buffers are seeded inputs;
+  the oracle receives the same buffers.
+* mesh simulation: every coordinate of the mesh is run on the one GPU with
+  the true partials of its group members; the reduced blocks must equal the
+  unsharded layer (the spec invariant) and be identical bit for bit
+  across each reduction group.
+* chunking, stream overlap and the ROW/COL transposition never change a bit.
+* full-size workloads are checked on sampled token rows (rows are
+  independent in every step) and, for dW, on sampled columns.
+"""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2301_08658_amd as atp
+import synth_inputs as S
+from helpers import (DEV, LIN, assert_close, block_mode_code, group_table, make_block_inputs,
+                     oracle_block_fwd, run_block_bwd, run_block_fwd, to64)
+
+pytestmark = pytest.mark.gpu
+
+TINY = S.WORKLOADS["tiny_mlp_h512_col_2x2"]
+
+
+def _check_fwd(out, ref, rows=None, what=""):
+    sel = (lambda t: t) if rows is None else (lambda t: t[rows])
+    for key in ("qkv", "o", "h", "pre", "z"):
+        assert_close(sel(out[key]), ref[key], f"{what} {key}")
+
+
+# ------------------------------------------------------------------ tiny, bench mode
+@pytest.mark.parametrize("mode", ["col", "row"])
+@pytest.mark.parametrize("bias_std", [0.0, 0.02])
+def test_block_fwd_tiny_every_coordinate(mode, bias_std):
+    w = TINY
+    d1, d2 = w["mesh"]
+    for coord in itertools.product(range(d1), range(d2)):
+        inp = make_block_inputs(mode, w["mesh"], coord, w["tokens"], w["h"], w["sigma_w"],
+                                seed=1, bias_std=bias_std)
+        out = run_block_fwd(inp, w["chunks"])
+        torch.cuda.synchronize()
+        ref = oracle_block_fwd(O, inp)
+        _check_fwd(out, ref, what=f"{mode} {coord}")
+        # the own partial buffer holds x_loc @ w_loc (fc2's input is a GPU
+        # output, so only the three linears fed by seeded inputs are checked)
+        for i, g in enumerate(inp["G"][:3]):
+            if g.red_size > 1:
+                xin = inp["a"] if i == 1 else inp["x"]
+                assert_close(out["own"][i], O.matmul(xin.cpu(), inp["w"][i].cpu()),
+                             f"own partial {LIN[i]}")
+
+
+@pytest.mark.parametrize("mesh", [(1, 1), (1, 4), (4, 1), (3, 2)])
+def test_block_fwd_degenerate_meshes(mesh):
+    """Groups of one (bias/GeLU fused in the GEMM), Megatron's (N,1) mesh and
+    a non-power-of-two mesh."""
+    T, h = 96, 384 if mesh != (3, 2) else 768
+    for coord in [(0, 0), (mesh[0] - 1, mesh[1] - 1)]:
+        inp = make_block_inputs("col", mesh, coord, T, h, 0.02, seed=2)
+        out = run_block_fwd(inp, 2)
+        torch.cuda.synchronize()
+        _check_fwd(out, oracle_block_fwd(O, inp), what=f"{mesh} {coord}")
+
+
+# ------------------------------------------------------------------ mesh simulation
+def _simulate_mesh(mode, mesh, T, h, chunks, X, A, W, B):
+    """Run every coordinate's share on the one GPU with true peer partials.
+    Returns {coord: outputs}."""
+    d1, d2 = mesh
+    bm = block_mode_code(mode)
+    coords = list(itertools.product(range(d1), range(d2)))
+    omodes = O.block_linear_modes(O.BLOCK_COL if mode == "col" else O.BLOCK_ROW)
+    loc = {}
+    for c in coords:
+        m = atp.mesh(d1, d2, *c)
+        G = atp.block_geometry(m, bm, h)
+        xs, _, _ = O.linear_specs(omodes["qkv"])
+        xr = O.spec_block(mesh, c, xs, (T, h))[1]
+        xo, _, _ = O.linear_specs(omodes["out"])
+        ar = O.spec_block(mesh, c, xo, (T, h))[1]
+        w = [W[n][g.k_off:g.k_off + g.k_loc, g.n_off:g.n_off + g.n_loc].contiguous().to(DEV)
+             for g, n in zip(G, LIN)]
+        b = [B[n][g.n_off:g.n_off + g.n_loc].contiguous().to(DEV) for g, n in zip(G, LIN)]
+        loc[c] = dict(m=m, G=G, x=X[:, xr[0]:xr[1]].contiguous().to(DEV),
+                      a=A[:, ar[0]:ar[1]].contiguous().to(DEV), w=w, b=b)
+    part = {c: [torch.empty((T, g.n_loc), device=DEV) for g in loc[c]["G"]] for c in coords}
+    # phase 1: partials of qkv, out, fc1 on every device
+    for c in coords:
+        L = loc[c]
+        for i, xin in ((0, L["x"]), (1, L["a"]), (2, L["x"])):
+            g = L["G"][i]
+            mode_i = atp.ATP_COL_FIRST if g.red_axis == 1 else atp.ATP_ROW_FIRST
+            if g.red_size > 1:
+                atp.atp_shard_linear_fwd(L["m"], mode_i, T, *(h, h, h)[i:i + 1],
+                                         (3 * h, h, 4 * h)[i], chunks, xin, L["w"][i], None, 0,
+                                         part[c][i])
+
+    def group(c, g):
+        return [tuple(c[:g.red_axis]) + (j,) + tuple(c[g.red_axis + 1:])
+                for j in range(g.red_size)]
+
+    # phase 2: every device's reduced H (fc1), then its fc2 partial
+    Hd = {}
+    for c in coords:
+        L = loc[c]
+        g = L["G"][2]
+        Hd[c] = torch.empty((T, g.n_loc), dtype=torch.bfloat16, device=DEV)
+        if g.red_size > 1:
+            atp.atp_chunked_partial_reduce(g.red_size, T, g.n_loc, chunks,
+                                           [part[p][2] for p in group(c, g)], L["b"][2],
+                                           atp.ATP_EPI_BIAS_GELU, Hd[c])
+        else:
+            mode_i = atp.ATP_COL_FIRST if g.red_axis == 1 else atp.ATP_ROW_FIRST
+            atp.atp_shard_linear_fwd(L["m"], mode_i, T, h, 4 * h, chunks, L["x"], L["w"][2],
+                                     L["b"][2], atp.ATP_EPI_BIAS_GELU, Hd[c])
+    for c in coords:
+        L = loc[c]
+        g = L["G"][3]
+        if g.red_size > 1:
+            mode_i = atp.ATP_COL_FIRST if g.red_axis == 1 else atp.ATP_ROW_FIRST
+            atp.atp_shard_linear_fwd(L["m"], mode_i, T, 4 * h, h, chunks, Hd[c], L["w"][3], None,
+                                     0, part[c][3])
+    # phase 3: the block call on every device, with the true group tables
+    res = {}
+    for c in coords:
+        L = loc[c]
+        G = L["G"]
+        tabs = [[part[p][i] for p in group(c, G[i])] if G[i].red_size > 1 else None
+                for i in range(4)]
+        out = dict(qkv=torch.empty((T, G[0].n_loc), dtype=torch.bfloat16, device=DEV),
+                   o=torch.empty((T, G[1].n_loc), dtype=torch.bfloat16, device=DEV),
+                   h=torch.empty((T, G[2].n_loc), dtype=torch.bfloat16, device=DEV),
+                   pre=torch.empty((T, G[2].n_loc), dtype=torch.bfloat16, device=DEV),
+                   z=torch.empty((T, G[3].n_loc), dtype=torch.bfloat16, device=DEV))
+        atp.atp_block_fwd(L["m"], bm, T, h, chunks, L["w"], L["b"], L["x"], L["a"], tabs,
+                          out["qkv"], out["o"], out["h"], out["pre"], out["z"],
+                          comm_stream=torch.cuda.Stream())
+        torch.cuda.synchronize()
+        res[c] = out
+    return res
+
+
+@pytest.mark.parametrize("mode,mesh", [("col", (2, 2)), ("row", (2, 2)), ("col", (2, 4)),
+                                       ("row", (4, 2))])
+def test_mesh_simulation_equals_unsharded_layer(mode, mesh):
+    T, h = 256, 512
+    shapes = O.block_shapes(h)
+    X = S.randn_bf16((T, h), 1.0, 3, 1)
+    A = S.randn_bf16((T, h), 1.0, 3, 2)
+    W = {n: S.randn_bf16(shapes[n], 0.02, 3, 10 + i) for i, n in enumerate(LIN)}
+    B = {n: S.randn_bf16((shapes[n][1],), 0.02, 3, 20 + i) for i, n in enumerate(LIN)}
+    res = _simulate_mesh(mode, mesh, T, h, 2, X, A, W, B)
+    bm = O.BLOCK_COL if mode == "col" else O.BLOCK_ROW
+    for c, out in res.items():
+        ref = O.block_fwd_global(bm, mesh, c, X, A, W, B)
+        _check_fwd(out, ref, what=f"{mode} {mesh} {c}")
+    # every member of a reduction group holds the same bits
+    G0 = atp.block_geometry(atp.mesh(*mesh, 0, 0), block_mode_code(mode), h)
+    for key, i in (("qkv", 0), ("o", 1), ("h", 2), ("z", 3)):
+        axis = G0[i].red_axis
+        for c in res:
+            c2 = list(c)
+            c2[axis] = (c[axis] + 1) % mesh[axis]
+            assert torch.equal(res[c][key], res[tuple(c2)][key]), (key, c, c2)
+
+
+# ------------------------------------------------------------------ invariances
+def test_chunk_count_never_changes_a_bit():
+    base = None
+    inp = make_block_inputs("col", (2, 4), (1, 2), 512, 1024, 0.02, seed=4)
+    for chunks in (1, 2, 4, 8):
+        out = run_block_fwd(inp, chunks)
+        torch.cuda.synchronize()
+        if base is None:
+            base = out
+            continue
+        for key in ("qkv", "o", "h", "pre", "z"):
+            assert torch.equal(out[key], base[key]), (chunks, key)
+
+
+def test_serialized_equals_pipelined():
+    inp = make_block_inputs("row", (4, 2), (3, 1), 512, 1024, 0.02, seed=5, bwd=True)
+    a = run_block_fwd(inp, 4, same_stream=True)
+    b = run_block_fwd(inp, 4)
+    torch.cuda.synchronize()
+    for key in ("qkv", "o", "h", "pre", "z"):
+        assert torch.equal(a[key], b[key]), key
+    ga = run_block_bwd(inp, 4, same_stream=True)
+    gb = run_block_bwd(inp, 4)
+    torch.cuda.synchronize()
+    for key in ("dh_pre", "dx_qkv", "dx_fc1", "d_attn"):
+        assert torch.equal(ga[key], gb[key]), key
+    for i in range(4):
+        assert torch.equal(ga["dw"][i], gb["dw"][i])
+        assert torch.equal(ga["db"][i], gb["db"][i])
+
+
+def test_row_on_transposed_mesh_equals_col():
+    """ROW on (4,2) at (i1,i2) has the local shapes and groups of COL on (2,4)
+    at (i2,i1); fed the same local data the outputs match bit for bit."""
+    T, h = 512, 1024
+    for (i1, i2) in [(0, 0), (3, 1), (2, 0)]:
+        a = make_block_inputs("row", (4, 2), (i1, i2), T, h, 0.02, seed=6)
+        b = make_block_inputs("col", (2, 4), (i2, i1), T, h, 0.02, seed=6)
+        for key in ("x", "a"):
+            assert torch.equal(a[key], b[key])
+        oa = run_block_fwd(a, 4)
+        ob = run_block_fwd(b, 4)
+        torch.cuda.synchronize()
+        for key in ("qkv", "o", "h", "pre", "z"):
+            assert torch.equal(oa[key], ob[key]), key
+
+
+# ------------------------------------------------------------------ backward
+def _oracle_bwd(inp):
+    """Oracle backward of the same device share (bench mode)."""
+    bm = O.BLOCK_COL if inp["mode"] == "col" else O.BLOCK_ROW
+    cpu = lambda t: t.detach().cpu()  # noqa: E731
+    coord = (inp["m"].i1, inp["m"].i2)
+    w = {n: cpu(inp["w"][i]) for i, n in enumerate(LIN)}
+    peers = {n: [cpu(p) for p in inp["dx_peers"][i]] for i, n in enumerate(LIN)}
+    return O.block_bwd_local(bm, inp["m"], coord, cpu(inp["x"]), cpu(inp["a"]),
+                             cpu(inp["hs"]), cpu(inp["pres"]), w,
+                             cpu(inp["dz"]), cpu(inp["dqkv"]), cpu(inp["do"]), peers)
+
+
+def _check_bwd(out, ref, inp, what=""):
+    for key in ("dh_pre", "dx_qkv", "dx_fc1", "d_attn"):
+        rk = {"d_attn": "da"}.get(key, key)
+        assert_close(out[key], ref[rk], f"{what} {key}")
+    for i, n in enumerate(LIN):
+        fl = "rms" if n == "fc1" else 1.0     # token-sums of the bf16 dh_pre
+        assert_close(out["dw"][i], ref["dw_" + n], f"{what} dw_{n}", floor=fl)
+        assert_close(out["db"][i], ref["db_" + n], f"{what} db_{n}", floor=fl)
+
+
+@pytest.mark.parametrize("mode,mesh,coord", [("col", (2, 2), (1, 0)), ("row", (2, 4), (1, 3)),
+                                             ("col", (4, 1), (2, 0))])
+def test_block_fwd_bwd_integer_chain_bit_exact(mode, mesh, coord):
+    """Integer inputs, integer peers and pre = 0 (GeLU'(0) = 1/2 exactly): every
+    value before a bf16 store is exact on both sides, so the chained backward
+    (fc2 dX -> reduce * GeLU' -> fc1 dX / dW) must match bit for bit, with the
+    oracle's bf16-stored outputs rounded the same way."""
+    inp = make_block_inputs(mode, mesh, coord, 192, 256, 0.0, seed=10, bwd=True, integer=True)
+    out = run_block_bwd(inp, 2)
+    torch.cuda.synchronize()
+    ref = _oracle_bwd(inp)
+    for key in ("dh_pre", "dx_qkv", "dx_fc1", "d_attn"):
+        rk = {"d_attn": "da"}.get(key, key)
+        np.testing.assert_array_equal(to64(out[key]), O.round_bf16(ref[rk]), err_msg=key)
+    for i, n in enumerate(LIN):
+        np.testing.assert_array_equal(to64(out["dw"][i]), ref["dw_" + n], err_msg=n)
+        np.testing.assert_array_equal(to64(out["db"][i]), ref["db_" + n], err_msg=n)
+
+
+@pytest.mark.parametrize("mode", ["col", "row"])
+def test_block_bwd_tiny_every_coordinate(mode):
+    w = TINY
+    d1, d2 = w["mesh"]
+    for coord in itertools.product(range(d1), range(d2)):
+        inp = make_block_inputs(mode, w["mesh"], coord, w["tokens"], w["h"], w["sigma_w"],
+                                seed=7, bwd=True)
+        out = run_block_bwd(inp, w["chunks"])
+        torch.cuda.synchronize()
+        _check_bwd(out, _oracle_bwd(inp), inp, f"{mode} {coord}")
+
+
+@pytest.mark.parametrize("mesh", [(1, 1), (4, 1), (1, 4)])
+def test_block_bwd_groups_of_one(mesh):
+    inp = make_block_inputs("col", mesh, (0, 0), 128, 256, 0.02, seed=8, bwd=True)
+    out = run_block_bwd(inp, 2)
+    torch.cuda.synchronize()
+    _check_bwd(out, _oracle_bwd(inp), inp, f"{mesh}")
+
+
+def test_block_bwd_chunk_invariance():
+    inp = make_block_inputs("col", (2, 4), (1, 3), 512, 1024, 0.02, seed=9, bwd=True)
+    base = run_block_bwd(inp, 1)
+    for chunks in (2, 4, 8):
+        out = run_block_bwd(inp, chunks)
+        torch.cuda.synchronize()
+        for key in ("dh_pre", "dx_qkv", "dx_fc1", "d_attn"):
+            assert torch.equal(out[key], base[key]), (chunks, key)
+        for i in range(4):
+            assert torch.equal(out["dw"][i], base["dw"][i])

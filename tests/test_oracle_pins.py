@@ -205,6 +205,34 @@ def test_gelu_grad_vs_autograd_and_finite_difference():
     assert O.gelu_grad(np.array([0.0]))[0] == 0.5
 
 
+# ---------------------------------------------------------------- bf16 storage
+def test_round_bf16_vs_torch_conversion():
+    # torch's float32 -> bfloat16 conversion rounds to nearest even; every
+    # float32 is exact in float64, so both must agree on float32 inputs
+    rng = np.random.default_rng(5)
+    x32 = np.concatenate([
+        rng.standard_normal(20000).astype(np.float32) * np.float32(3.0),
+        (rng.standard_normal(2000) * 1e-39).astype(np.float32),       # subnormals
+        (rng.standard_normal(2000) * 1e37).astype(np.float32),        # near the top
+        np.array([3.3895e38, 3.39e38, -3.4e38, 1e-45, -0.0, 0.0], dtype=np.float32),
+    ])
+    ref = torch.from_numpy(x32).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(O.round_bf16(x32.astype(np.float64)), ref)
+
+
+def test_round_bf16_ties_and_specials():
+    r = O.round_bf16(np.array([1 + 2**-8, 1 + 3 * 2**-8, -(1 + 2**-8), 1 + 2**-8 + 2**-30,
+                               2.0**-133 / 2, 3 * 2.0**-134, np.inf, -np.inf]))
+    np.testing.assert_array_equal(r, [1.0, 1 + 2**-6, -1.0, 1 + 2**-7, 0.0, 2 * 2.0**-133,
+                                      np.inf, -np.inf])
+    assert np.isnan(O.round_bf16(np.array([np.nan]))[0])
+    # every bfloat16 value is a fixed point
+    allb = torch.arange(0, 2**16, dtype=torch.int32).to(torch.int16).view(torch.bfloat16)
+    v = allb.to(torch.float64).numpy()
+    v = v[np.isfinite(v)]
+    np.testing.assert_array_equal(O.round_bf16(v), v)
+
+
 # ---------------------------------------------------------------- reduction
 def test_partial_reduce_closed_forms():
     T, N = 9, 16
@@ -331,7 +359,7 @@ def test_block_fwd_global_vs_torch_and_brute_force_local(block_mode, mesh):
     for c in coords:
         x_loc, a_loc, w, b = loc[c]
         peers = {n: group_peers(c, n, lambda g, n=n: own[g][n]) for n in O.LINEARS}
-        got = O.block_fwd_local(block_mode, mesh, c, x_loc, a_loc, w, b, peers)
+        got = O.block_fwd_local(block_mode, mesh, c, x_loc, a_loc, w, b, peers, round_h=None)
         glob = O.block_fwd_global(block_mode, mesh, c, X, A, W, B)
         for key in ("qkv", "o", "h", "pre", "z"):
             np.testing.assert_allclose(got[key], glob[key], rtol=1e-11, atol=1e-11)
@@ -417,7 +445,8 @@ def test_block_bwd_brute_force_vs_autograd(block_mode, mesh):
         x_loc, a_loc, w, b = loc[c]
         peers = {n: [own[g][n] for g in bwd_group(c, n) if g != c] for n in O.LINEARS}
         r = O.block_bwd_local(block_mode, mesh, c, x_loc, a_loc, fwd[c]["h"], fwd[c]["pre"], w,
-                              grads[c]["fc2"], grads[c]["qkv"], grads[c]["out"], peers)
+                              grads[c]["fc2"], grads[c]["qkv"], grads[c]["out"], peers,
+                              round_dpre=None)
         xs, ws_q, _ = O.linear_specs(modes["qkv"])
         np.testing.assert_allclose(r["dx_qkv"], O.local_tensor(Xq.grad.numpy(), mesh, c, xs),
                                    rtol=1e-11, atol=1e-11)
