@@ -52,6 +52,8 @@ def parse():
                     help="after timing, run one plain device copy of this many MiB "
                          "(reference kernel for scaling HBM counters)")
     ap.add_argument("--seed", type=int, default=21)
+    ap.add_argument("--profile-detail", action="store_true",
+                    help="also print per-shape kernel timings to stderr")
     return ap.parse_args()
 
 
@@ -259,6 +261,19 @@ def main():
                            note="durations measured while overlapping the GEMMs")
     for k in kernels:
         log(f"[bench]   {k}")
+
+    if args.profile_detail:
+        atp.atp_profile_enable(2)
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        atp.atp_profile_enable(False)
+        for s in sorted(atp.atp_profile_collect(128), key=lambda s: -s["total_ms"]):
+            us = s["total_ms"] / s["launches"] * 1e3
+            tf = s["flops"] / (s["total_ms"] * 1e-3) / 1e12 if s["flops"] else 0.0
+            gb = s["bytes"] / (s["total_ms"] * 1e-3) / 1e9
+            log(f"[detail] {s['name']:<44} n={s['launches'] // args.steps:<3} "
+                f"avg={us:9.1f}us  {tf:7.1f} TFLOP/s  {gb:7.1f} GB/s")
 
     if args.copy_calib_mb:
         n = args.copy_calib_mb * (1 << 20) // 4

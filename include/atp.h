@@ -26,7 +26,8 @@
  *    (r, c) of a matrix with leading dimension ld is at base[r * ld + c].
  *    bf16 = IEEE bfloat16 bits (uint16), f32 = IEEE binary32.
  *    Every device pointer must be 16-byte aligned, every leading dimension
- *    and every local column count a multiple of 8 elements.
+ *    and every local column count a multiple of 8 elements, and leading
+ *    dimensions at most 4M (2^22) elements.
  *  - Streams and events are hipStream_t / hipEvent_t passed as void*;
  *    NULL means the default stream.  Calls only enqueue work and return.
  *  - Chunks (Sec. 4.1): the token rows are split into `chunks` contiguous
@@ -249,13 +250,15 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
  * algorithmic FLOPs and bytes) and clears the log.  Returns the number of
  * records, or -1 on a HIP error. */
 typedef struct {
-    char name[48];
+    char name[64];
     int64_t launches;
     double total_ms;
     double flops;
     double bytes;
 } atp_kernel_stat;
 
+/* on: 0 = off, 1 = one record per kernel, 2 = one record per kernel and
+ * problem shape (names carry M x N x K and the epilogue). */
 void atp_profile_enable(int32_t on);
 int32_t atp_profile_collect(atp_kernel_stat* out, int32_t max);
 

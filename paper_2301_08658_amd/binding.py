@@ -97,7 +97,7 @@ class atp_block_bwd_io(ctypes.Structure):
 
 
 class atp_kernel_stat(ctypes.Structure):
-    _fields_ = [("name", ctypes.c_char * 48), ("launches", ctypes.c_int64),
+    _fields_ = [("name", ctypes.c_char * 64), ("launches", ctypes.c_int64),
                 ("total_ms", ctypes.c_double), ("flops", ctypes.c_double),
                 ("bytes", ctypes.c_double)]
 
@@ -112,11 +112,12 @@ EXPORTS = (
 _lib = None
 
 
-def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     """Load libatp.so.  Raises if it has not been built: there is no fallback."""
     global _lib
     if _lib is not None:
         return _lib
+    path = path or LIB_PATH
     if not os.path.exists(path):
         raise ImportError(f"{path} is missing: build the HIP library first "
                           "(python -m paper_2301_08658_amd.build)")
@@ -428,8 +429,9 @@ def atp_block_bwd(m: atp_mesh, block_mode: int, tokens: int, h: int, chunks: int
                                         _stream(compute_stream), _stream(comm_stream)))
 
 
-def atp_profile_enable(on: bool = True):
-    load_library().atp_profile_enable(1 if on else 0)
+def atp_profile_enable(on=True):
+    """on: False/0 off, True/1 per kernel, 2 per kernel and problem shape."""
+    load_library().atp_profile_enable(int(on) if not isinstance(on, bool) else (1 if on else 0))
 
 
 def atp_profile_collect(max_records: int = 32):

@@ -100,6 +100,9 @@ atp_status check_chunks(int64_t tokens, int32_t chunks) {
 
 // A matrix with zero rows is never touched and may be NULL.
 atp_status check_mat(const void* p, int64_t rows, int64_t ld, int64_t cols, const char* name) {
+    if (ld > (int64_t)1 << 22)
+        return fail(ATP_ERR_UNSUPPORTED, "%s: leading dimension %lld above 4M elements", name,
+                    (long long)ld);
     if (rows == 0 && !p) return ATP_OK;
     if (!p) return fail(ATP_ERR_INVALID_ARGUMENT, "%s is NULL", name);
     if (ld < cols) return fail(ATP_ERR_INVALID_ARGUMENT, "%s: ld %lld < %lld columns", name,
@@ -141,11 +144,12 @@ atp_status sync_events(size_t count, hipEvent_t** out) {
 }
 
 struct ProfRec {
-    const char* name;
+    std::string name;
     hipEvent_t beg, end;
     double flops, bytes;
 };
 bool g_prof_on = false;
+bool g_prof_detail = false;   // key records by kernel and problem shape
 std::vector<ProfRec> g_prof;
 std::vector<hipEvent_t> g_prof_free;
 
@@ -162,7 +166,8 @@ hipEvent_t prof_event() {
 
 // Run `launch` on stream s, bracketed by timing events when profiling is on.
 template <class F>
-atp_status timed(const char* name, double flops, double bytes, hipStream_t s, F&& launch) {
+atp_status timed(const std::string& name, double flops, double bytes, hipStream_t s,
+                 F&& launch) {
     hipEvent_t b = nullptr, e = nullptr;
     if (g_prof_on) {
         std::lock_guard<std::mutex> lk(g_mu);
@@ -171,7 +176,7 @@ atp_status timed(const char* name, double flops, double bytes, hipStream_t s, F&
         if (b) (void)hipEventRecord(b, s);
     }
     hipError_t err = launch();
-    if (err != hipSuccess) return hip_fail(err, name);
+    if (err != hipSuccess) return hip_fail(err, name.c_str());
     if (b && e) {
         (void)hipEventRecord(e, s);
         std::lock_guard<std::mutex> lk(g_mu);
@@ -186,8 +191,14 @@ atp_status run_gemm(const atp::GemmProblem& p, hipStream_t s) {
     const double bytes = 2.0 * ((double)p.M * p.K + (double)p.K * p.N) +
                          (double)p.M * p.N * (p.out_bf16 ? 2.0 : 4.0) +
                          ((p.epi == atp::EPI_GELU_BWD || p.pre_out) ? 2.0 * p.M * p.N : 0.0);
-    return timed(atp::gemm_kernel_name(p.layout), flops, bytes, s,
-                 [&] { return atp::launch_gemm(p, s); });
+    std::string name = atp::gemm_kernel_name(p.layout);
+    if (g_prof_on && g_prof_detail) {
+        char buf[96];
+        snprintf(buf, sizeof buf, " %lldx%lldx%lld e%d%s", (long long)p.M, (long long)p.N,
+                 (long long)p.K, p.epi, p.out_bf16 ? " bf16" : "");
+        name += buf;
+    }
+    return timed(name, flops, bytes, s, [&] { return atp::launch_gemm(p, s); });
 }
 
 atp_status run_reduce(const atp::ReduceProblem& p, hipStream_t s) {
@@ -195,7 +206,14 @@ atp_status run_reduce(const atp::ReduceProblem& p, hipStream_t s) {
     const double el = (double)p.rows * (double)p.ncols;
     const double bytes = el * (4.0 * p.nparts + (p.out_bf16 ? 2.0 : 4.0)) +
                          ((p.epi == atp::EPI_GELU_BWD || p.pre_out) ? 2.0 * el : 0.0);
-    return timed("partial_reduce", 0.0, bytes, s, [&] { return atp::launch_reduce(p, s); });
+    std::string name = "partial_reduce";
+    if (g_prof_on && g_prof_detail) {
+        char buf[96];
+        snprintf(buf, sizeof buf, " %dx%lldx%lld e%d", p.nparts, (long long)p.rows,
+                 (long long)p.ncols, p.epi);
+        name += buf;
+    }
+    return timed(name, 0.0, bytes, s, [&] { return atp::launch_reduce(p, s); });
 }
 
 atp_status run_colsum(const void* dy, int64_t ld, int64_t T, int64_t N, float* db,
@@ -647,6 +665,7 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
 void atp_profile_enable(int32_t on) {
     std::lock_guard<std::mutex> lk(g_mu);
     g_prof_on = (on != 0);
+    g_prof_detail = (on == 2);
 }
 
 int32_t atp_profile_collect(atp_kernel_stat* out, int32_t max) {
@@ -665,11 +684,11 @@ int32_t atp_profile_collect(atp_kernel_stat* out, int32_t max) {
         }
         size_t i = 0;
         for (; i < agg.size(); ++i)
-            if (strcmp(agg[i].name, r.name) == 0) break;
+            if (strncmp(agg[i].name, r.name.c_str(), sizeof agg[i].name - 1) == 0) break;
         if (i == agg.size()) {
             atp_kernel_stat st;
             memset(&st, 0, sizeof st);
-            snprintf(st.name, sizeof st.name, "%s", r.name);
+            snprintf(st.name, sizeof st.name, "%s", r.name.c_str());
             agg.push_back(st);
         }
         agg[i].launches += 1;

@@ -1,32 +1,36 @@
 // bf16 x bf16 -> fp32 MFMA GEMM for gfx950 (CDNA4) with fused epilogues.
 //
 // One kernel template serves the three products of a shard linear
-// (Sec. 3.2 forward Y = X W; Sec. 4.2 backward dX = dY W^T, dW = X^T dY):
+// (Sec. 3.2 forward Y = X W; Sec. 4.2 backward dX = dY W^T, dW = X^T dY).
 //
-//   * Workgroup tile 256 x 256, K step 64, 256 threads = 4 wave64s in a
-//     2 x 2 arrangement; each wave owns a 128 x 128 sub-tile held as 4 x 4
-//     v_mfma_f32_32x32x16_bf16 accumulators (256 fp32 per lane).
-//   * Both operands live in LDS as [row][k] with k contiguous, so every
-//     MFMA fragment is one 16-byte LDS read.  Rows are padded to 72
-//     elements (144 B): consecutive rows then start 16 B apart modulo the
-//     bank width and a wave's fragment reads are conflict free.
-//   * An operand that is contiguous along k in memory (X, dY, W for dX) is
-//     copied in 16-byte chunks.  An operand contiguous along its M/N side
-//     (W in the forward, X and dY in dW) is fetched as 8 x 8 element blocks
-//     (eight coalesced 16-byte row loads) and transposed in registers
-//     before the 16-byte LDS stores.
-//   * Two LDS stages: global loads of step k+1 are in flight while step k
-//     is multiplied; one barrier per K step.
-//   * The MFMA is issued with the N-side fragment as its first operand, so
-//     each lane's 16 results are 4 runs of 4 consecutive output columns:
-//     the epilogue writes 16 B (fp32) or 8 B (bf16) per lane.
+// Data path
+//   * Operands go global -> LDS with buffer_load_dwordx4 ... lds (no
+//     register staging).  A buffer resource per operand gives zero fill for
+//     every out-of-range lane (its offset is pushed past num_records), so
+//     ragged M, N and K need no separate path.
+//   * STAGES LDS buffers form a ring: the loads of K-step kt+STAGES-1 are
+//     issued while step kt is multiplied, and a step is consumed after an
+//     explicit vmcnt wait plus one workgroup barrier.
+//   * An operand contiguous along K (X and dY as the M side; W in dX) is
+//     kept [row][k]; an MFMA fragment is one ds_read_b128.  An operand
+//     contiguous along its M/N side (W in the forward, X and dY in dW) is
+//     kept [k][row] and its fragments are read with two ds_read_b64_tr_b16
+//     (gfx950's transposing LDS read): no register transposes.
+//   * Both layouts are XOR-swizzled in 16-byte units.  The direct-to-LDS
+//     copy writes LDS linearly by lane, so the swizzle is applied by
+//     choosing which global chunk each lane fetches.  The swizzles are
+//     conflict free for 8- and 16-lane LDS phases.
+//   * Wave tile (BM/WGM) x (BN/WGN) of v_mfma_f32_32x32x16_bf16 blocks.  The
+//     MFMA takes the N-side fragment first, so a lane's 16 accumulators are
+//     4 runs of 4 consecutive output columns and the epilogue stores 16 B
+//     (fp32) or 8 B (bf16) per lane.
 //   * Every output element accumulates its K products in the same order
-//     (64-wide steps, MFMA k order inside) whatever M, so token chunking
-//     never changes a value.
-//   * Workgroups are renumbered so that consecutive tiles land on the same
-//     XCD (the dispatcher deals workgroups round-robin over the 8 XCDs),
-//     and tiles are visited in groups of 8 M-tiles so the tiles that
-//     share a weight panel run together and hit that XCD's L2.
+//     (K steps of BK, MFMA k order inside) for every tile shape, so token
+//     chunking never changes a value.
+//   * Workgroups are renumbered so consecutive tiles land on one XCD (the
+//     dispatcher deals workgroups round-robin over the 8 XCDs) and visited
+//     in groups of GROUP_M row tiles, so tiles sharing a weight panel run
+//     together on one L2.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -35,24 +39,26 @@
 namespace atp {
 namespace {
 
-constexpr int BM = 256;
-constexpr int BN = 256;
-constexpr int BK = 64;
-constexpr int LDK = BK + 8;       // padded LDS row length (elements)
-constexpr int NT = 256;           // threads per workgroup
-constexpr int WM = 128;           // wave sub-tile
-constexpr int WN = 128;
-constexpr int FM = WM / 32;       // MFMA blocks per wave along M
-constexpr int FN = WN / 32;       // ... along N
-constexpr int GROUP_M = 8;
+#ifndef ATP_GEMM_GROUP_M
+#define ATP_GEMM_GROUP_M 8
+#endif
+#ifndef ATP_GEMM_XCD_REMAP
+#define ATP_GEMM_XCD_REMAP 1
+#endif
+constexpr int GROUP_M = ATP_GEMM_GROUP_M;
 constexpr int NUM_XCD = 8;
-constexpr int STAGE_ELEMS = (BM + BN) * LDK;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+constexpr uint32_t kRsrcWord3 = 0x00020000u;   // raw 32-bit buffer access
+constexpr uint32_t kOob = 0x80000000u;          // offset beyond any num_records
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
     return __uint_as_float(bits16 << 16);
@@ -75,83 +81,20 @@ __device__ __forceinline__ float gelu_grad_f(float x) {
     return cdf + x * pdf;
 }
 
-// ---------------------------------------------------------------------------
-// Global -> register -> LDS copy of one operand tile (rows = M or N side).
-// ---------------------------------------------------------------------------
-template <bool KCONTIG>
-struct TileCopy;
+// 16-byte chunk swizzles.  K-major rows hold BK/8 chunks; MN-major rows
+// (one per k) hold at least 16 chunks.
+template <int CPR>
+__device__ __forceinline__ int swz_k(int r) {
+    if constexpr (CPR == 8) return (r + (r >> 3)) & 7;
+    else return ((r >> 1) + (r >> 3)) & 3;
+}
+__device__ __forceinline__ int swz_mn(int k) { return ((k & 2) << 1) | ((k & 1) * 10); }
 
-// Operand stored as [row][k] with k contiguous: 256 rows x 8 chunks of 16 B.
-template <>
-struct TileCopy<true> {
-    u32x4 r[8];
-    __device__ __forceinline__ void load(const uint16_t* __restrict__ base, int64_t ld,
-                                         int64_t row0, int64_t rows, int64_t k0, int64_t K,
-                                         int tid) {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int id = tid + NT * i;
-            const int row = id >> 3;
-            const int cc = id & 7;
-            const int64_t gr = row0 + row;
-            const int64_t gk = k0 + cc * 8;
-            const bool ok = (gr < rows) && (gk < K);
-            const uint16_t* p = base + (ok ? gr * ld + gk : 0);
-            const u32x4 v = *reinterpret_cast<const u32x4*>(p);
-            r[i] = ok ? v : u32x4{0u, 0u, 0u, 0u};
-        }
-    }
-    __device__ __forceinline__ void store(uint16_t* __restrict__ lds, int tid) const {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int id = tid + NT * i;
-            const int row = id >> 3;
-            const int cc = id & 7;
-            *reinterpret_cast<u32x4*>(lds + row * LDK + cc * 8) = r[i];
-        }
-    }
-};
-
-// Operand stored as [k][row] with the row index contiguous: each thread
-// fetches an 8 (k) x 8 (row) block and transposes it.
-template <>
-struct TileCopy<false> {
-    u32x4 r[8];
-    __device__ __forceinline__ void load(const uint16_t* __restrict__ base, int64_t ld,
-                                         int64_t row0, int64_t rows, int64_t k0, int64_t K,
-                                         int tid) {
-        const int kb = tid >> 5;     // 0..7  : k block of 8
-        const int rb = tid & 31;     // 0..31 : row block of 8
-        const int64_t gr = row0 + rb * 8;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int64_t gk = k0 + kb * 8 + i;
-            const bool ok = (gr < rows) && (gk < K);
-            const uint16_t* p = base + (ok ? gk * ld + gr : 0);
-            const u32x4 v = *reinterpret_cast<const u32x4*>(p);
-            r[i] = ok ? v : u32x4{0u, 0u, 0u, 0u};
-        }
-    }
-    __device__ __forceinline__ void store(uint16_t* __restrict__ lds, int tid) const {
-        const int kb = tid >> 5;
-        const int rb = tid & 31;
-        // r[e] holds k = kb*8+e, rows rb*8+0..7 (two per dword).  Output row
-        // j holds k = kb*8+0..7: dword p = (k 2p low half, k 2p+1 high half).
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int q = j >> 1;
-            u32x4 o;
-#pragma unroll
-            for (int p = 0; p < 4; ++p) {
-                const uint32_t lo = r[2 * p][q];
-                const uint32_t hi = r[2 * p + 1][q];
-                o[p] = (j & 1) ? ((lo >> 16) | (hi & 0xffff0000u))
-                               : ((lo & 0xffffu) | (hi << 16));
-            }
-            *reinterpret_cast<u32x4*>(lds + (rb * 8 + j) * LDK + kb * 8) = o;
-        }
-    }
-};
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+    const int64_t cap = 0x7fffff00;   // keep offsets and sizes in 31 bits
+    const int n = (int)(bytes < 0 ? 0 : (bytes > cap ? cap : bytes));
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, kRsrcWord3);
+}
 
 struct KArgs {
     const uint16_t* A; int64_t lda;
@@ -164,43 +107,143 @@ struct KArgs {
     int tiles_m, tiles_n;
 };
 
-__device__ __forceinline__ void tile_coords(const KArgs& a, int& tm, int& tn) {
+__device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
     const int G = gridDim.x;
     const int pid = blockIdx.x;
-    // renumber: workgroups dealt to XCD x become one contiguous range
     const int xcd = pid % NUM_XCD;
     const int idx = pid / NUM_XCD;
     const int per = G / NUM_XCD;
     const int rem = G % NUM_XCD;
-    const int logical = (xcd < rem) ? xcd * (per + 1) + idx
-                                    : rem * (per + 1) + (xcd - rem) * per + idx;
-    // grouped order: GROUP_M row tiles per column sweep
-    const int in_group = GROUP_M * a.tiles_n;
+    int logical = (xcd < rem) ? xcd * (per + 1) + idx
+                              : rem * (per + 1) + (xcd - rem) * per + idx;
+    if (!ATP_GEMM_XCD_REMAP) logical = pid;
+    const int in_group = GROUP_M * tiles_n;
     const int group = logical / in_group;
     const int first_m = group * GROUP_M;
-    const int gsize = min(a.tiles_m - first_m, GROUP_M);
+    const int gsize = min(tiles_m - first_m, GROUP_M);
     const int r = logical % in_group;
     tm = first_m + r % gsize;
     tn = r / gsize;
 }
 
-template <bool A_K, bool B_K, int EPI, bool OUT_BF16>
-__global__ __launch_bounds__(NT, 1) void gemm_kernel(KArgs a) {
-    __shared__ __attribute__((aligned(16))) uint16_t smem[2 * STAGE_ELEMS];
+// ---------------------------------------------------------------------------
+// One operand of the tile: issue the direct-to-LDS copy of one K step, and
+// read MFMA fragments back.  ROWS = BM or BN (the operand's M/N extent).
+// ---------------------------------------------------------------------------
+template <int ROWS, int BK, int NT, bool KCONTIG>
+struct Operand {
+    static constexpr int CHUNKS = ROWS * BK / 8;          // 16-byte chunks per K step
+    static constexpr int PER_THREAD = CHUNKS / NT;
+    static_assert(CHUNKS % NT == 0, "tile not divisible by the thread count");
+    static constexpr int CPR = KCONTIG ? BK / 8 : ROWS / 8;   // chunks per LDS row
+
+    const uint16_t* base;
+    int64_t ld;
+    int64_t row0, rows, K;
+
+    // Copy K step [k0, k0+BK) into LDS stage `dst` (ROWS*BK elements).  A
+    // step at or past K fills the stage with zeros (every lane out of range),
+    // so each step issues the same number of loads.
+    __device__ __forceinline__ void issue(uint16_t* dst, int64_t k0, int tid) const {
+        const int wave = tid >> 6;
+        const int lane = tid & 63;
+        if constexpr (KCONTIG) {
+            // rows row0.., columns k0..: byte range of this K step's rows
+            const bool live = k0 < K;
+            const uint16_t* b = base + row0 * ld + (live ? k0 : 0);
+            const int64_t left = rows - row0;
+            const int64_t valid_rows = live ? (left < ROWS ? left : ROWS) : 0;
+            const __amdgpu_buffer_rsrc_t rs = make_rsrc(b, valid_rows * ld * 2);
+#pragma unroll
+            for (int i = 0; i < PER_THREAD; ++i) {
+                const int p = (i * (NT / 64) + wave) * 64 + lane;     // LDS chunk slot
+                const int r = p / CPR;
+                const int c = (p % CPR) ^ swz_k<CPR>(r);               // logical chunk
+                const bool ok = (k0 + c * 8 < K) && (r < valid_rows);
+                const uint32_t off = ok ? (uint32_t)((r * ld + c * 8) * 2) : kOob;
+                lds_void* d = (lds_void*)(dst + (size_t)(i * (NT / 64) + wave) * 64 * 8);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, d, 16, off, 0, 0, 0);
+            }
+        } else {
+            // rows k0.. of a [K][ld] matrix, columns row0..row0+ROWS
+            const bool live = k0 < K;
+            const uint16_t* b = base + (live ? k0 : 0) * ld + row0;
+            const int64_t valid_k = live ? (K - k0 < BK ? K - k0 : BK) : 0;
+            const __amdgpu_buffer_rsrc_t rs = make_rsrc(b, valid_k * ld * 2);
+#pragma unroll
+            for (int i = 0; i < PER_THREAD; ++i) {
+                const int p = (i * (NT / 64) + wave) * 64 + lane;
+                const int k = p / CPR;
+                const int c = (p % CPR) ^ swz_mn(k);
+                const bool ok = (row0 + c * 8 < rows) && (k < valid_k);
+                const uint32_t off = ok ? (uint32_t)((k * ld + c * 8) * 2) : kOob;
+                lds_void* d = (lds_void*)(dst + (size_t)(i * (NT / 64) + wave) * 64 * 8);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, d, 16, off, 0, 0, 0);
+            }
+        }
+    }
+
+    // MFMA 32x32x16 fragment: lane holds rows r0 + lane%32, k = ks*16 + 8*(lane/32) + 0..7.
+    static __device__ __forceinline__ bf16x8 frag(const uint16_t* src, int r0, int ks,
+                                                  int lane) {
+        if constexpr (KCONTIG) {
+            const int r = r0 + (lane & 31);
+            const int c = (ks * 2 + (lane >> 5)) ^ swz_k<CPR>(r);
+            return *reinterpret_cast<const bf16x8*>(src + r * BK + c * 8);
+        } else {
+            // two transposing reads of 4 k values each (lane group of 16:
+            // rows r0 + 16*(g%2) + 0..15, k base ks*16 + 8*(g/2))
+            const int g = lane >> 4;
+            const int j = lane & 15;
+            const int mn = r0 + 16 * (g & 1) + 4 * (j & 3);
+            const int kb = ks * 16 + 8 * (g >> 1) + (j >> 2);
+            const int k0 = kb, k1 = kb + 4;
+            const uint16_t* p0 = src + k0 * ROWS + (((mn >> 3) ^ swz_mn(k0)) << 3) + (mn & 7);
+            const uint16_t* p1 = src + k1 * ROWS + (((mn >> 3) ^ swz_mn(k1)) << 3) + (mn & 7);
+            const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p0);
+            const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p1);
+            typedef short i16x8 __attribute__((ext_vector_type(8)));
+            const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            return __builtin_bit_cast(bf16x8, v);
+        }
+    }
+};
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, bool A_K, bool B_K, int EPI,
+          bool OUT_BF16>
+__global__ __launch_bounds__(WGM* WGN * 64, 1) void gemm_kernel(KArgs a) {
+    constexpr int NT = WGM * WGN * 64;
+    constexpr int WM = BM / WGM;
+    constexpr int WN = BN / WGN;
+    constexpr int FM = WM / 32;
+    constexpr int FN = WN / 32;
+    constexpr int A_ELEMS = BM * BK;
+    constexpr int STAGE = (BM + BN) * BK;
+    using OpA = Operand<BM, BK, NT, A_K>;
+    using OpB = Operand<BN, BK, NT, B_K>;
+    constexpr int LOADS = OpA::PER_THREAD + OpB::PER_THREAD;   // vm ops per stage per thread
+
+    __shared__ __attribute__((aligned(1024))) uint16_t smem[STAGES * STAGE];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int wm = wave >> 1;
-    const int wn = wave & 1;
+    const int wm = wave / WGN;
+    const int wn = wave % WGN;
 
     int tm, tn;
-    tile_coords(a, tm, tn);
+    tile_coords(a.tiles_m, a.tiles_n, tm, tn);
     const int64_t m0 = (int64_t)tm * BM;
     const int64_t n0 = (int64_t)tn * BN;
 
-    TileCopy<A_K> ca;
-    TileCopy<B_K> cb;
+    OpA opa{a.A, a.lda, m0, a.M, a.K};
+    OpB opb{a.B, a.ldb, n0, a.N, a.K};
 
     f32x16 acc[FM][FN];
 #pragma unroll
@@ -211,53 +254,67 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(KArgs a) {
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
     const int nk = (int)((a.K + BK - 1) / BK);
+    constexpr int KS = BK / 16;   // MFMA k-steps per K step
 
-    if (nk > 0) {   // K == 0 (no tokens in a dW product) reads nothing and writes zeros
-        ca.load(a.A, a.lda, m0, a.M, 0, a.K, tid);
-        cb.load(a.B, a.ldb, n0, a.N, 0, a.K, tid);
-        ca.store(smem, tid);
-        cb.store(smem + BM * LDK, tid);
+    // prologue: steps 0 .. STAGES-2 in flight (steps past K fill zeros)
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s) {
+        opa.issue(smem + s * STAGE, (int64_t)s * BK, tid);
+        opb.issue(smem + s * STAGE + A_ELEMS, (int64_t)s * BK, tid);
     }
-    __syncthreads();
-
-    const int frag_row = lane & 31;
-    const int frag_k = (lane >> 5) * 8;
 
     for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
-        const bool more = (kt + 1) < nk;
-        if (more) {
-            const int64_t k0 = (int64_t)(kt + 1) * BK;
-            ca.load(a.A, a.lda, m0, a.M, k0, a.K, tid);
-            cb.load(a.B, a.ldb, n0, a.N, k0, a.K, tid);
+        // step kt's copy is the oldest of STAGES-1 in flight
+        wait_vmcnt<LOADS * (STAGES - 2)>();
+        __syncthreads();
+        const uint16_t* sa = smem + (kt % STAGES) * STAGE;
+        const uint16_t* sb = sa + A_ELEMS;
+        bf16x8 fa[2][FM], fb[2][FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) fa[0][i] = OpA::frag(sa, wm * WM + i * 32, 0, lane);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) fb[0][j] = OpB::frag(sb, wn * WN + j * 32, 0, lane);
+        {
+            // refill the buffer step kt-1 used with step kt+STAGES-1
+            const int kn = kt + STAGES - 1;
+            uint16_t* dst = smem + (kn % STAGES) * STAGE;
+            opa.issue(dst, (int64_t)kn * BK, tid);
+            opb.issue(dst + A_ELEMS, (int64_t)kn * BK, tid);
         }
-        const uint16_t* sa = smem + cur * STAGE_ELEMS;
-        const uint16_t* sb = sa + BM * LDK;
 #pragma unroll
-        for (int s = 0; s < BK / 16; ++s) {
-            bf16x8 fa[FM], fb[FN];
+        for (int ks = 0; ks < KS; ++ks) {
+            const int cur = ks & 1;
+            if (ks + 1 < KS) {
 #pragma unroll
-            for (int i = 0; i < FM; ++i)
-                fa[i] = *reinterpret_cast<const bf16x8*>(
-                    sa + (wm * WM + i * 32 + frag_row) * LDK + s * 16 + frag_k);
+                for (int i = 0; i < FM; ++i)
+                    fa[cur ^ 1][i] = OpA::frag(sa, wm * WM + i * 32, ks + 1, lane);
 #pragma unroll
-            for (int j = 0; j < FN; ++j)
-                fb[j] = *reinterpret_cast<const bf16x8*>(
-                    sb + (wn * WN + j * 32 + frag_row) * LDK + s * 16 + frag_k);
+                for (int j = 0; j < FN; ++j)
+                    fb[cur ^ 1][j] = OpB::frag(sb, wn * WN + j * 32, ks + 1, lane);
+            }
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
                 for (int j = 0; j < FN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j],
-                                                                        0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cur][j], fa[cur][i],
+                                                                        acc[i][j], 0, 0, 0);
         }
-        if (more) {
-            uint16_t* nxt = smem + (cur ^ 1) * STAGE_ELEMS;
-            ca.store(nxt, tid);
-            cb.store(nxt + BM * LDK, tid);
+#if defined(ATP_GEMM_SCHED) && ATP_GEMM_SCHED
+        // interleave: the step's global loads and the next fragments' LDS
+        // reads are spread between the MFMAs
+#pragma unroll
+        for (int q = 0; q < LOADS; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
         }
-        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < (KS - 1) * (FM + FN) * (A_K ? 1 : 2) && q < KS * FM * FN; ++q) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+        }
+#endif
     }
+    wait_vmcnt<0>();
 
     // Epilogue.  Lane holds C(m = base_m + lane%32, n = base_n + 8g + 4*(lane/32) + 0..3)
     // in acc[..][..][4g .. 4g+3].
@@ -314,6 +371,28 @@ __global__ __launch_bounds__(NT, 1) void gemm_kernel(KArgs a) {
     }
 }
 
+// Tile configuration: 256 x 256 workgroup tile, 4 waves of 128 x 128.
+#ifndef ATP_GEMM_BK
+#define ATP_GEMM_BK 64
+#endif
+#ifndef ATP_GEMM_STAGES
+#define ATP_GEMM_STAGES 2
+#endif
+#ifndef ATP_GEMM_BM
+#define ATP_GEMM_BM 256
+#endif
+#ifndef ATP_GEMM_BN
+#define ATP_GEMM_BN 256
+#endif
+#ifndef ATP_GEMM_WGM
+#define ATP_GEMM_WGM 2
+#endif
+#ifndef ATP_GEMM_WGN
+#define ATP_GEMM_WGN 4
+#endif
+constexpr int CFG_BM = ATP_GEMM_BM, CFG_BN = ATP_GEMM_BN, CFG_BK = ATP_GEMM_BK,
+              CFG_STAGES = ATP_GEMM_STAGES, CFG_WGM = ATP_GEMM_WGM, CFG_WGN = ATP_GEMM_WGN;
+
 template <bool A_K, bool B_K, int EPI, bool OUT_BF16>
 hipError_t launch_t(const GemmProblem& p, hipStream_t s) {
     KArgs a;
@@ -329,11 +408,13 @@ hipError_t launch_t(const GemmProblem& p, hipStream_t s) {
     a.M = p.M;
     a.N = p.N;
     a.K = p.K;
-    a.tiles_m = (int)((p.M + BM - 1) / BM);
-    a.tiles_n = (int)((p.N + BN - 1) / BN);
+    a.tiles_m = (int)((p.M + CFG_BM - 1) / CFG_BM);
+    a.tiles_n = (int)((p.N + CFG_BN - 1) / CFG_BN);
     const int grid = a.tiles_m * a.tiles_n;
     if (grid == 0) return hipSuccess;
-    hipLaunchKernelGGL((gemm_kernel<A_K, B_K, EPI, OUT_BF16>), dim3(grid), dim3(NT), 0, s, a);
+    hipLaunchKernelGGL((gemm_kernel<CFG_BM, CFG_BN, CFG_BK, CFG_STAGES, CFG_WGM, CFG_WGN, A_K,
+                                    B_K, EPI, OUT_BF16>),
+                       dim3(grid), dim3(CFG_WGM * CFG_WGN * 64), 0, s, a);
     return hipGetLastError();
 }
 
@@ -363,6 +444,10 @@ const char* gemm_kernel_name(int layout) {
 
 hipError_t launch_gemm(const GemmProblem& p, hipStream_t s) {
     if (p.M <= 0 || p.N <= 0) return hipSuccess;
+    // buffer offsets are 32-bit: one tile's rows of either operand must span < 2 GiB
+    const int64_t span = (int64_t)(CFG_BM > CFG_BN ? CFG_BM : CFG_BN) *
+                         (p.lda > p.ldb ? p.lda : p.ldb) * 2;
+    if (span > 0x7fffff00) return hipErrorInvalidValue;
     const bool b16 = p.out_bf16;
     switch (p.layout) {
     case LAYOUT_NN:
