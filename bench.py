@@ -46,7 +46,7 @@ def parse():
     ap.add_argument("--serial", action="store_true",
                     help="run reductions on the compute stream (no overlap)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=6,
+    ap.add_argument("--cpu-rows", type=int, default=64,
                     help="token rows in the oracle's timed CPU sample")
     ap.add_argument("--copy-calib-mb", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB "
@@ -123,6 +123,22 @@ def make_step(torch, atp, st, fwd_only, serial):
                           st["d_attn"], st["dw"], st["db"], compute_stream=cs,
                           comm_stream=ms)
     return step
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE summary, or None if there is none for this kernel and workload
+    or the GEMM source changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(HERE, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    src = os.path.join(HERE, "paper_2301_08658_amd", "csrc", "gemm.hip")
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if rec.get("kernel") != kernel or rec.get("gemm_source_sha256") != sha:
+        return None
+    return rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"]
 
 
 def cpu_baseline(st, rows_n, fwd_only, seed):
@@ -245,9 +261,11 @@ def main():
     gemms = [s for s in stats if s["name"].startswith("gemm")]
     dom = max(gemms, key=lambda s: s["total_ms"])
     achieved = dom["flops"] / (dom["total_ms"] * 1e-3) / 1e12
+    traffic = measured_traffic(dom["name"], args.workload)
     roofline = dict(bound="mfma", kernel=dom["name"], achieved=round(achieved, 1),
                     peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
-                    frac=round(achieved / PEAK_BF16_TFLOPS, 4), traffic=None,
+                    frac=round(achieved / PEAK_BF16_TFLOPS, 4), traffic=traffic,
+                    algorithmic_bytes_per_launch=dom["bytes"] / dom["launches"],
                     flops_per_launch=dom["flops"] / dom["launches"],
                     avg_launch_us=round(dom["total_ms"] / dom["launches"] * 1e3, 2))
     red = [s for s in stats if s["name"] == "partial_reduce"]

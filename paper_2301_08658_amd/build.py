@@ -42,6 +42,12 @@ def build(verbose: bool = False) -> str:
     if r.returncode != 0:
         sys.stderr.write(r.stdout + r.stderr)
         raise RuntimeError("link of libatp.so failed")
+    # every kernel launched from host code must have its launch stub defined
+    nm = subprocess.run(["nm", tmp], capture_output=True, text=True)
+    missing = [ln.split()[-1] for ln in nm.stdout.splitlines()
+               if ln.split()[:1] == ["U"] and "__device_stub__" in ln]
+    if nm.returncode != 0 or missing:
+        raise RuntimeError(f"libatp.so has undefined kernel stubs: {missing[:4]}")
     os.replace(tmp, LIB)
     if verbose:
         print(f"built {LIB}")

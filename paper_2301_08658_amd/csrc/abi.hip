@@ -191,11 +191,13 @@ atp_status run_gemm(const atp::GemmProblem& p, hipStream_t s) {
     const double bytes = 2.0 * ((double)p.M * p.K + (double)p.K * p.N) +
                          (double)p.M * p.N * (p.out_bf16 ? 2.0 : 4.0) +
                          ((p.epi == atp::EPI_GELU_BWD || p.pre_out) ? 2.0 * p.M * p.N : 0.0);
+    // one name per kernel instantiation: layout, epilogue, output type
     std::string name = atp::gemm_kernel_name(p.layout);
+    name += "_e" + std::to_string(p.epi) + (p.out_bf16 ? "_bf16" : "_f32");
     if (g_prof_on && g_prof_detail) {
         char buf[96];
-        snprintf(buf, sizeof buf, " %lldx%lldx%lld e%d%s", (long long)p.M, (long long)p.N,
-                 (long long)p.K, p.epi, p.out_bf16 ? " bf16" : "");
+        snprintf(buf, sizeof buf, " %lldx%lldx%lld", (long long)p.M, (long long)p.N,
+                 (long long)p.K);
         name += buf;
     }
     return timed(name, flops, bytes, s, [&] { return atp::launch_gemm(p, s); });

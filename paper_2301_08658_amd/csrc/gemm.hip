@@ -36,15 +36,38 @@
 
 #include "kernels.h"
 
-namespace atp {
-namespace {
-
+// Tile and schedule parameters (compile-time).
 #ifndef ATP_GEMM_GROUP_M
 #define ATP_GEMM_GROUP_M 8
 #endif
 #ifndef ATP_GEMM_XCD_REMAP
 #define ATP_GEMM_XCD_REMAP 1
 #endif
+#ifndef ATP_GEMM_BK
+#define ATP_GEMM_BK 64
+#endif
+#ifndef ATP_GEMM_PIPE
+#define ATP_GEMM_PIPE 0
+#endif
+#ifndef ATP_GEMM_STAGES
+#define ATP_GEMM_STAGES 2
+#endif
+#ifndef ATP_GEMM_BM
+#define ATP_GEMM_BM 256
+#endif
+#ifndef ATP_GEMM_BN
+#define ATP_GEMM_BN 256
+#endif
+#ifndef ATP_GEMM_WGM
+#define ATP_GEMM_WGM 2
+#endif
+#ifndef ATP_GEMM_WGN
+#define ATP_GEMM_WGN 4
+#endif
+
+namespace atp {
+namespace {
+
 constexpr int GROUP_M = ATP_GEMM_GROUP_M;
 constexpr int NUM_XCD = 8;
 
@@ -85,7 +108,7 @@ __device__ __forceinline__ float gelu_grad_f(float x) {
 // (one per k) hold at least 16 chunks.
 template <int CPR>
 __device__ __forceinline__ int swz_k(int r) {
-    if constexpr (CPR == 8) return (r + (r >> 3)) & 7;
+    if constexpr (CPR == 8) return (r ^ ((r >> 3) & 1)) & 7;
     else return ((r >> 1) + (r >> 3)) & 3;
 }
 __device__ __forceinline__ int swz_mn(int k) { return ((k & 2) << 1) | ((k & 1) * 10); }
@@ -140,44 +163,61 @@ struct Operand {
     const uint16_t* base;
     int64_t ld;
     int64_t row0, rows, K;
+    // Per-lane byte offsets of this thread's chunks relative to the step's
+    // first element (row0, k0); out-of-range rows / columns hold kOob.  They
+    // do not depend on the K step.
+    uint32_t voff[PER_THREAD];
+    int kchunk[PER_THREAD];    // K-major: the chunk's first k within the step
+
+    __device__ __forceinline__ void init(int tid) {
+        const int wave = tid >> 6;
+        const int lane = tid & 63;
+#pragma unroll
+        for (int i = 0; i < PER_THREAD; ++i) {
+            const int p = (i * (NT / 64) + wave) * 64 + lane;     // LDS chunk slot
+            if constexpr (KCONTIG) {
+                const int r = p / CPR;
+                const int c = (p % CPR) ^ swz_k<CPR>(r);
+                kchunk[i] = c * 8;
+                voff[i] = (row0 + r < rows) ? (uint32_t)((r * ld + c * 8) * 2) : kOob;
+            } else {
+                const int k = p / CPR;
+                const int c = (p % CPR) ^ swz_mn(k);
+                kchunk[i] = k;
+                voff[i] = (row0 + c * 8 < rows) ? (uint32_t)((k * ld + c * 8) * 2) : kOob;
+            }
+        }
+    }
 
     // Copy K step [k0, k0+BK) into LDS stage `dst` (ROWS*BK elements).  A
     // step at or past K fills the stage with zeros (every lane out of range),
     // so each step issues the same number of loads.
     __device__ __forceinline__ void issue(uint16_t* dst, int64_t k0, int tid) const {
         const int wave = tid >> 6;
-        const int lane = tid & 63;
+        const bool live = k0 < K;
         if constexpr (KCONTIG) {
-            // rows row0.., columns k0..: byte range of this K step's rows
-            const bool live = k0 < K;
+            // whole rows bound the range; k past K inside a row is masked per
+            // lane, which only the last step of a ragged K needs
             const uint16_t* b = base + row0 * ld + (live ? k0 : 0);
             const int64_t left = rows - row0;
             const int64_t valid_rows = live ? (left < ROWS ? left : ROWS) : 0;
             const __amdgpu_buffer_rsrc_t rs = make_rsrc(b, valid_rows * ld * 2);
+            const bool tail = k0 + BK > K;
 #pragma unroll
             for (int i = 0; i < PER_THREAD; ++i) {
-                const int p = (i * (NT / 64) + wave) * 64 + lane;     // LDS chunk slot
-                const int r = p / CPR;
-                const int c = (p % CPR) ^ swz_k<CPR>(r);               // logical chunk
-                const bool ok = (k0 + c * 8 < K) && (r < valid_rows);
-                const uint32_t off = ok ? (uint32_t)((r * ld + c * 8) * 2) : kOob;
+                const uint32_t off = (tail && k0 + kchunk[i] >= K) ? kOob : voff[i];
                 lds_void* d = (lds_void*)(dst + (size_t)(i * (NT / 64) + wave) * 64 * 8);
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, d, 16, off, 0, 0, 0);
             }
         } else {
-            // rows k0.. of a [K][ld] matrix, columns row0..row0+ROWS
-            const bool live = k0 < K;
+            // rows k0.. of a [K][ld] matrix: the range ends at row K
             const uint16_t* b = base + (live ? k0 : 0) * ld + row0;
             const int64_t valid_k = live ? (K - k0 < BK ? K - k0 : BK) : 0;
             const __amdgpu_buffer_rsrc_t rs = make_rsrc(b, valid_k * ld * 2);
 #pragma unroll
             for (int i = 0; i < PER_THREAD; ++i) {
-                const int p = (i * (NT / 64) + wave) * 64 + lane;
-                const int k = p / CPR;
-                const int c = (p % CPR) ^ swz_mn(k);
-                const bool ok = (row0 + c * 8 < rows) && (k < valid_k);
-                const uint32_t off = ok ? (uint32_t)((k * ld + c * 8) * 2) : kOob;
                 lds_void* d = (lds_void*)(dst + (size_t)(i * (NT / 64) + wave) * 64 * 8);
+                const uint32_t off = voff[i];
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, d, 16, off, 0, 0, 0);
             }
         }
@@ -244,6 +284,8 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1) void gemm_kernel(KArgs a) {
 
     OpA opa{a.A, a.lda, m0, a.M, a.K};
     OpB opb{a.B, a.ldb, n0, a.N, a.K};
+    opa.init(tid);
+    opb.init(tid);
 
     f32x16 acc[FM][FN];
 #pragma unroll
@@ -292,6 +334,10 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1) void gemm_kernel(KArgs a) {
                 for (int j = 0; j < FN; ++j)
                     fb[cur ^ 1][j] = OpB::frag(sb, wn * WN + j * 32, ks + 1, lane);
             }
+#if ATP_GEMM_PIPE
+            // keep the next k-step's LDS reads ahead of this k-step's MFMAs
+            __builtin_amdgcn_sched_barrier(0);
+#endif
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -372,24 +418,6 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1) void gemm_kernel(KArgs a) {
 }
 
 // Tile configuration: 256 x 256 workgroup tile, 4 waves of 128 x 128.
-#ifndef ATP_GEMM_BK
-#define ATP_GEMM_BK 64
-#endif
-#ifndef ATP_GEMM_STAGES
-#define ATP_GEMM_STAGES 2
-#endif
-#ifndef ATP_GEMM_BM
-#define ATP_GEMM_BM 256
-#endif
-#ifndef ATP_GEMM_BN
-#define ATP_GEMM_BN 256
-#endif
-#ifndef ATP_GEMM_WGM
-#define ATP_GEMM_WGM 2
-#endif
-#ifndef ATP_GEMM_WGN
-#define ATP_GEMM_WGN 4
-#endif
 constexpr int CFG_BM = ATP_GEMM_BM, CFG_BN = ATP_GEMM_BN, CFG_BK = ATP_GEMM_BK,
               CFG_STAGES = ATP_GEMM_STAGES, CFG_WGM = ATP_GEMM_WGM, CFG_WGN = ATP_GEMM_WGN;
 
