@@ -45,6 +45,8 @@ def parse():
     ap.add_argument("--fwd-only", action="store_true", help="time the forward only")
     ap.add_argument("--serial", action="store_true",
                     help="run reductions on the compute stream (no overlap)")
+    ap.add_argument("--no-aux", action="store_true",
+                    help="no second compute stream (independent GEMMs do not share the chip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=64,
                     help="token rows in the oracle's timed CPU sample")
@@ -107,21 +109,23 @@ def step_flops(st, fwd_only):
     return f if fwd_only else 3.0 * f
 
 
-def make_step(torch, atp, st, fwd_only, serial):
+def make_step(torch, atp, st, fwd_only, serial, aux):
     cs = torch.cuda.current_stream()
     ms = cs if serial else torch.cuda.Stream()
+    ax = torch.cuda.Stream() if (aux and not serial) else None
 
     def step():
         atp.atp_block_fwd(st["m"], st["bm"], st["T"], st["h"], st["chunks"], st["w"], st["b"],
                           st["x"], st["a"], st["fwd_tabs"], st["qkv"], st["o"], st["hh"],
-                          st["pre"], st["z"], compute_stream=cs, comm_stream=ms)
+                          st["pre"], st["z"], compute_stream=cs, comm_stream=ms,
+                          aux_stream=ax)
         if fwd_only:
             return
         atp.atp_block_bwd(st["m"], st["bm"], st["T"], st["h"], st["chunks"], st["w"], st["b"],
                           st["x"], st["a"], st["hh"], st["pre"], st["dz"], st["dqkv"], st["do"],
                           st["bwd_tabs"], st["dh_pre"], st["dx_qkv"], st["dx_fc1"],
                           st["d_attn"], st["dw"], st["db"], compute_stream=cs,
-                          comm_stream=ms)
+                          comm_stream=ms, aux_stream=ax)
     return step
 
 
@@ -217,7 +221,7 @@ def main():
         f"pass={'fwd' if fwd_only else 'fwd+bwd'}")
     st = setup(torch, atp, S, wl, chunks, args.seed)
     torch.cuda.synchronize()
-    step = make_step(torch, atp, st, fwd_only, args.serial)
+    step = make_step(torch, atp, st, fwd_only, args.serial, not args.no_aux)
     flops = step_flops(st, fwd_only)
 
     for _ in range(args.warmup):
@@ -316,7 +320,8 @@ def main():
         config=dict(workload=args.workload, mode=wl["mode"], mesh=[d1, d2], coord=[0, 0],
                     tokens=wl["tokens"], h=wl["h"], chunks=chunks,
                     **{"pass": "fwd" if fwd_only else "fwd+bwd"},
-                    serial=bool(args.serial), gflop_per_step=round(flops / 1e9, 1)),
+                    serial=bool(args.serial), aux_stream=not args.no_aux,
+                    gflop_per_step=round(flops / 1e9, 1)),
         mfma_util=round(value / PEAK_BF16_TFLOPS, 4),
         roofline=roofline, reduce=reduce_info, kernels=kernels, cpu_baseline=cpu)
     print(json.dumps(out), flush=True)

@@ -223,25 +223,35 @@ size_t atp_block_workspace_bytes(const atp_mesh* mesh, int32_t block_mode, int64
                                  int64_t h, int32_t chunks);
 
 /* One device's forward share of the layer (Sec. 3.2.1) with chunk-based
- * overlapping (Sec. 4.1).  GEMMs run on compute_stream in the order
- * qkv, out, fc1, fc2, chunk by chunk; each chunk's reduction runs on
- * comm_stream as soon as its partial is written; fc2's chunk c waits for
- * fc1's reduced chunk c.  On return compute_stream is ordered after all
- * of the block's work.  A group of one needs no reduction: its bias (and
- * GeLU) are applied in the GEMM epilogue. */
+ * overlapping (Sec. 4.1).  Each linear's GEMM runs chunk by chunk; each
+ * chunk's reduction runs on comm_stream as soon as that chunk's partial is
+ * written; fc2's chunk c waits for fc1's reduced chunk c.  A group of one
+ * needs no reduction: its bias (and GeLU) are applied in the GEMM epilogue
+ * and it runs as one launch.
+ * aux_stream (nullable) is a second compute stream: the attention
+ * projections start on it while QKV and the MLP use compute_stream, and
+ * consecutive chunks of a linear alternate between the two compute streams,
+ * so independent GEMMs share the chip.  With aux_stream NULL all GEMMs run
+ * on compute_stream; with comm_stream == compute_stream nothing overlaps.
+ * Results do not depend on the streams used.  compute_stream's earlier work
+ * happens before the block's, and on return compute_stream is ordered after
+ * all of it. */
 atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
                          int32_t chunks, const atp_block_weights* w,
                          const atp_block_fwd_io* io, void* workspace, size_t ws_bytes,
-                         void* compute_stream, void* comm_stream);
+                         void* compute_stream, void* comm_stream, void* aux_stream);
 
-/* One device's backward share of the layer (Sec. 4.2): fc2, fc1, out,
- * qkv in turn; for each, dX chunks on compute_stream, their reductions on
- * comm_stream overlapping the dW GEMM.  fc1's dY is fc2's reduced dX
- * times GeLU'(pre).  On return compute_stream is ordered after all work. */
+/* One device's backward share of the layer (Sec. 4.2): for each linear the
+ * dX chunks come first and their reductions (comm_stream) overlap that
+ * linear's dW GEMM and db; fc1's dY is fc2's reduced dX times GeLU'(pre).
+ * The MLP chain (fc2, then fc1) runs on compute_stream and the attention
+ * projections (out, qkv) on aux_stream when one is given; chunks alternate
+ * between the two compute streams as in atp_block_fwd.  On return
+ * compute_stream is ordered after all work. */
 atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
                          int32_t chunks, const atp_block_weights* w,
                          const atp_block_bwd_io* io, void* workspace, size_t ws_bytes,
-                         void* compute_stream, void* comm_stream);
+                         void* compute_stream, void* comm_stream, void* aux_stream);
 
 /* Per-kernel timing of the library's own launches.  When enabled, every
  * kernel the library enqueues is bracketed by HIP events on its stream;

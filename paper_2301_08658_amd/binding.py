@@ -138,10 +138,10 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.atp_block_workspace_bytes.argtypes = [mp, i32, i64, i64, i32]
     lib.atp_block_workspace_bytes.restype = sz
     lib.atp_block_fwd.argtypes = [mp, i32, i64, i64, i32, ctypes.POINTER(atp_block_weights),
-                                  ctypes.POINTER(atp_block_fwd_io), _vp, sz, _vp, _vp]
+                                  ctypes.POINTER(atp_block_fwd_io), _vp, sz, _vp, _vp, _vp]
     lib.atp_block_fwd.restype = i32
     lib.atp_block_bwd.argtypes = [mp, i32, i64, i64, i32, ctypes.POINTER(atp_block_weights),
-                                  ctypes.POINTER(atp_block_bwd_io), _vp, sz, _vp, _vp]
+                                  ctypes.POINTER(atp_block_bwd_io), _vp, sz, _vp, _vp, _vp]
     lib.atp_block_bwd.restype = i32
     lib.atp_profile_enable.argtypes = [i32]
     lib.atp_profile_enable.restype = None
@@ -208,6 +208,11 @@ def _stream(s) -> Optional[int]:
     if isinstance(s, int):
         return s
     return s.cuda_stream
+
+
+def _opt_stream(s) -> Optional[int]:
+    """A stream that may be absent (NULL)."""
+    return None if s is None else _stream(s)
 
 
 def _events(evs: Optional[Sequence]) -> Optional[ctypes.Array]:
@@ -350,7 +355,7 @@ def _weights(G, w: Sequence[torch.Tensor], b: Sequence[torch.Tensor]):
 
 def atp_block_fwd(m: atp_mesh, block_mode: int, tokens: int, h: int, chunks: int, w, b,
                   x_loc, attn_loc, partials, qkv, o, h_out, pre, z, workspace=None,
-                  compute_stream=None, comm_stream=None):
+                  compute_stream=None, comm_stream=None, aux_stream=None):
     """partials[i]: list of the red_size f32 buffers of linear i's group (own
     entry written), or None for a group of one."""
     G = block_geometry(m, block_mode, h)
@@ -379,13 +384,14 @@ def atp_block_fwd(m: atp_mesh, block_mode: int, tokens: int, h: int, chunks: int
     wsb = workspace.numel() * workspace.element_size() if workspace is not None else 0
     _check(load_library().atp_block_fwd(ctypes.byref(m), int(block_mode), int(tokens), int(h),
                                         int(chunks), ctypes.byref(W), ctypes.byref(io), wsp, wsb,
-                                        _stream(compute_stream), _stream(comm_stream)))
+                                        _stream(compute_stream), _stream(comm_stream),
+                                        _opt_stream(aux_stream)))
 
 
 def atp_block_bwd(m: atp_mesh, block_mode: int, tokens: int, h: int, chunks: int, w, b,
                   x_loc, attn_loc, h_act, pre, dz, dqkv, d_o, dx_partials, dh_pre, dx_qkv,
                   dx_fc1, d_attn, dw, db, workspace=None, compute_stream=None,
-                  comm_stream=None):
+                  comm_stream=None, aux_stream=None):
     """dx_partials[i]: list of the bwd_size f32 buffers of linear i's backward
     group (own entry written), or None for a group of one.  dw[i] must share
     the leading dimension of w[i]."""
@@ -426,7 +432,8 @@ def atp_block_bwd(m: atp_mesh, block_mode: int, tokens: int, h: int, chunks: int
     wsb = workspace.numel() * workspace.element_size() if workspace is not None else 0
     _check(load_library().atp_block_bwd(ctypes.byref(m), int(block_mode), int(tokens), int(h),
                                         int(chunks), ctypes.byref(W), ctypes.byref(io), wsp, wsb,
-                                        _stream(compute_stream), _stream(comm_stream)))
+                                        _stream(compute_stream), _stream(comm_stream),
+                                        _opt_stream(aux_stream)))
 
 
 def atp_profile_enable(on=True):

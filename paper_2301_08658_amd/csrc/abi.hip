@@ -308,6 +308,40 @@ atp_status check_group(float* const* tab, int32_t size, int64_t rows, int64_t ld
 
 const char* const kLinearName[4] = {"qkv", "out", "fc1", "fc2"};
 
+// The block's streams: compute (cs), comm (ms) and an optional auxiliary
+// compute stream (ax).  Chunk c of a linear runs on its home compute stream
+// for even c and on the other one for odd c, so consecutive chunks' GEMMs can
+// share the chip; without an auxiliary stream everything computes on cs.
+struct Streams {
+    hipStream_t cs, ms, ax;
+    bool two;
+    Streams(void* c, void* m, void* a)
+        : cs(static_cast<hipStream_t>(c)), ms(static_cast<hipStream_t>(m)),
+          ax(a ? static_cast<hipStream_t>(a) : static_cast<hipStream_t>(c)),
+          two(a != nullptr && a != c) {}
+    hipStream_t home(int h) const { return (h == 1 && two) ? ax : cs; }
+    hipStream_t pick(int h, int c) const { return home((c & 1) ? 1 - h : h); }
+    // everything already queued on cs happens before the block's work
+    atp_status begin(hipEvent_t start) const {
+        HIP_CHECK(hipEventRecord(start, cs), "hipEventRecord");
+        if (ms != cs) HIP_CHECK(hipStreamWaitEvent(ms, start, 0), "hipStreamWaitEvent");
+        if (two) HIP_CHECK(hipStreamWaitEvent(ax, start, 0), "hipStreamWaitEvent");
+        return ATP_OK;
+    }
+    // cs is ordered after all of the block's work on ms and ax
+    atp_status end(hipEvent_t ms_end, hipEvent_t ax_end) const {
+        if (ms != cs) {
+            HIP_CHECK(hipEventRecord(ms_end, ms), "hipEventRecord");
+            HIP_CHECK(hipStreamWaitEvent(cs, ms_end, 0), "hipStreamWaitEvent");
+        }
+        if (two) {
+            HIP_CHECK(hipEventRecord(ax_end, ax), "hipEventRecord");
+            HIP_CHECK(hipStreamWaitEvent(cs, ax_end, 0), "hipStreamWaitEvent");
+        }
+        return ATP_OK;
+    }
+};
+
 }  // namespace
 
 // ===========================================================================
@@ -463,7 +497,7 @@ size_t atp_block_workspace_bytes(const atp_mesh* mesh, int32_t block_mode, int64
 atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
                          int32_t chunks, const atp_block_weights* w, const atp_block_fwd_io* io,
                          void* workspace, size_t ws_bytes, void* compute_stream,
-                         void* comm_stream) {
+                         void* comm_stream, void* aux_stream) {
     (void)workspace; (void)ws_bytes;
     BlockPlan P;
     ATP_CHECK(check_mesh(mesh));
@@ -496,17 +530,15 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         ATP_CHECK(check_group(io->partials[i], P.g[i].red_size, tokens, io->ldp[i], P.g[i].n_loc, nm));
     }
 
-    hipStream_t cs = static_cast<hipStream_t>(compute_stream);
-    hipStream_t ms = static_cast<hipStream_t>(comm_stream);
+    Streams S(compute_stream, comm_stream, aux_stream);
     hipEvent_t* ev = nullptr;
-    // [0]: start, [1]: end, then per linear per chunk GEMM-done, then fc1 reduce-done
-    const size_t n_ev = 2 + 4 * (size_t)chunks + (size_t)chunks;
+    // [0] start  [1] comm end  [2] aux end  [3] fc1 done (one-member group)
+    // then per linear per chunk GEMM-done, then fc1 reduce-done per chunk
+    const size_t n_ev = 4 + 4 * (size_t)chunks + (size_t)chunks;
     ATP_CHECK(sync_events(n_ev, &ev));
-    hipEvent_t* ev_gemm = ev + 2;
-    hipEvent_t* ev_red1 = ev + 2 + 4 * chunks;
-
-    HIP_CHECK(hipEventRecord(ev[0], cs), "hipEventRecord");
-    HIP_CHECK(hipStreamWaitEvent(ms, ev[0], 0), "hipStreamWaitEvent");
+    hipEvent_t* ev_gemm = ev + 4;
+    hipEvent_t* ev_red1 = ev + 4 + 4 * chunks;
+    ATP_CHECK(S.begin(ev[0]));
 
     const int64_t mc = tokens / chunks;
     const void* A_in[4] = {io->x_loc, io->attn_loc, io->x_loc, io->h};
@@ -514,52 +546,79 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     void* outp[4] = {io->qkv, io->o, io->h, io->z};
     const int64_t ldo[4] = {io->ld_qkv, io->ld_o, io->ld_h, io->ld_z};
     const bool fc1_reduced = P.g[2].red_size > 1;
+    // home compute stream of each linear: the attention projections and the
+    // MLP run on different streams when an auxiliary stream is given
+    const int home[4] = {0, 1, 0, 0};
 
-    for (int L = 0; L < 4; ++L) {
+    // fc2 reads H: wait for fc1's reduced chunk c, or for fc1's single launch
+    auto wait_h = [&](hipStream_t s, int c) -> atp_status {
+        if (fc1_reduced) HIP_CHECK(hipStreamWaitEvent(s, ev_red1[c], 0), "hipStreamWaitEvent");
+        else if (s != S.cs) HIP_CHECK(hipStreamWaitEvent(s, ev[3], 0), "hipStreamWaitEvent");
+        return ATP_OK;
+    };
+    auto unchunked = [&](int L) -> atp_status {
         const atp_shard& g = P.g[L];
-        const int epi = (L == 2) ? atp::EPI_BIAS_GELU : atp::EPI_BIAS;
-        void* pre = (L == 2) ? io->pre : nullptr;
-        if (g.red_size == 1) {
-            // nothing to reduce: bias (+GeLU) fused in the GEMM, one launch
-            if (L == 3 && fc1_reduced)
-                HIP_CHECK(hipStreamWaitEvent(cs, ev_red1[chunks - 1], 0), "hipStreamWaitEvent");
-            atp::GemmProblem p = gemm_problem(atp::LAYOUT_NN, A_in[L], lda_in[L], w->w[L],
-                                              w->ldw[L], outp[L], ldo[L], true, epi, tokens,
-                                              g.n_loc, g.k_loc);
-            p.bias = w->b[L];
-            p.pre_out = pre;
-            ATP_CHECK(run_gemm(p, cs));
+        hipStream_t s = S.home(home[L]);
+        if (L == 3) ATP_CHECK(wait_h(s, chunks - 1));
+        atp::GemmProblem p = gemm_problem(atp::LAYOUT_NN, A_in[L], lda_in[L], w->w[L], w->ldw[L],
+                                          outp[L], ldo[L], true,
+                                          L == 2 ? atp::EPI_BIAS_GELU : atp::EPI_BIAS, tokens,
+                                          g.n_loc, g.k_loc);
+        p.bias = w->b[L];
+        p.pre_out = (L == 2) ? io->pre : nullptr;
+        ATP_CHECK(run_gemm(p, s));
+        if (L == 2) HIP_CHECK(hipEventRecord(ev[3], s), "hipEventRecord");
+        return ATP_OK;
+    };
+    auto chunk = [&](int L, int c) -> atp_status {
+        const atp_shard& g = P.g[L];
+        hipStream_t s = S.pick(home[L], c);
+        const int64_t r0 = (int64_t)c * mc;
+        if (L == 3) ATP_CHECK(wait_h(s, c));
+        float* own = io->partials[L][g.red_index];
+        atp::GemmProblem p = gemm_problem(
+            atp::LAYOUT_NN, static_cast<const uint16_t*>(A_in[L]) + r0 * lda_in[L], lda_in[L],
+            w->w[L], w->ldw[L], own + r0 * io->ldp[L], io->ldp[L], false, atp::EPI_NONE, mc,
+            g.n_loc, g.k_loc);
+        ATP_CHECK(run_gemm(p, s));
+        hipEvent_t e = ev_gemm[L * chunks + c];
+        HIP_CHECK(hipEventRecord(e, s), "hipEventRecord");
+        HIP_CHECK(hipStreamWaitEvent(S.ms, e, 0), "hipStreamWaitEvent");
+        atp::ReduceProblem r = reduce_problem(
+            g.red_size, io->partials[L], io->ldp[L], r0, mc, g.n_loc,
+            L == 2 ? atp::EPI_BIAS_GELU : atp::EPI_BIAS, w->b[L], nullptr, outp[L], ldo[L], true,
+            L == 2 ? io->pre : nullptr);
+        ATP_CHECK(run_reduce(r, S.ms));
+        if (L == 2) HIP_CHECK(hipEventRecord(ev_red1[c], S.ms), "hipEventRecord");
+        return ATP_OK;
+    };
+    // the two independent linears of each pair are issued chunk by chunk in
+    // turn, so their reductions reach the comm stream in completion order
+    const int pairs[2][2] = {{0, 1}, {2, 3}};
+    for (int q = 0; q < 2; ++q) {
+        const int La = pairs[q][0], Lb = pairs[q][1];
+        if (q == 1) {
+            // fc2 depends on fc1: fc1 first, then fc2 (chunk by chunk)
+            if (P.g[La].red_size == 1) ATP_CHECK(unchunked(La));
+            else for (int c = 0; c < chunks; ++c) ATP_CHECK(chunk(La, c));
+            if (P.g[Lb].red_size == 1) ATP_CHECK(unchunked(Lb));
+            else for (int c = 0; c < chunks; ++c) ATP_CHECK(chunk(Lb, c));
             continue;
         }
-        float* own = io->partials[L][g.red_index];
-        for (int32_t c = 0; c < chunks; ++c) {
-            const int64_t r0 = (int64_t)c * mc;
-            if (L == 3 && fc1_reduced)
-                HIP_CHECK(hipStreamWaitEvent(cs, ev_red1[c], 0), "hipStreamWaitEvent");
-            atp::GemmProblem p = gemm_problem(
-                atp::LAYOUT_NN, static_cast<const uint16_t*>(A_in[L]) + r0 * lda_in[L],
-                lda_in[L], w->w[L], w->ldw[L], own + r0 * io->ldp[L], io->ldp[L], false,
-                atp::EPI_NONE, mc, g.n_loc, g.k_loc);
-            ATP_CHECK(run_gemm(p, cs));
-            hipEvent_t e = ev_gemm[L * chunks + c];
-            HIP_CHECK(hipEventRecord(e, cs), "hipEventRecord");
-            HIP_CHECK(hipStreamWaitEvent(ms, e, 0), "hipStreamWaitEvent");
-            atp::ReduceProblem r = reduce_problem(
-                g.red_size, io->partials[L], io->ldp[L], r0, mc, g.n_loc, epi, w->b[L], nullptr,
-                outp[L], ldo[L], true, pre);
-            ATP_CHECK(run_reduce(r, ms));
-            if (L == 2) HIP_CHECK(hipEventRecord(ev_red1[c], ms), "hipEventRecord");
+        if (P.g[La].red_size == 1) ATP_CHECK(unchunked(La));
+        if (P.g[Lb].red_size == 1) ATP_CHECK(unchunked(Lb));
+        for (int c = 0; c < chunks; ++c) {
+            if (P.g[La].red_size > 1) ATP_CHECK(chunk(La, c));
+            if (P.g[Lb].red_size > 1) ATP_CHECK(chunk(Lb, c));
         }
     }
-    HIP_CHECK(hipEventRecord(ev[1], ms), "hipEventRecord");
-    HIP_CHECK(hipStreamWaitEvent(cs, ev[1], 0), "hipStreamWaitEvent");
-    return ATP_OK;
+    return S.end(ev[1], ev[2]);
 }
 
 atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
                          int32_t chunks, const atp_block_weights* w, const atp_block_bwd_io* io,
                          void* workspace, size_t ws_bytes, void* compute_stream,
-                         void* comm_stream) {
+                         void* comm_stream, void* aux_stream) {
     (void)workspace; (void)ws_bytes;
     BlockPlan P;
     ATP_CHECK(check_mesh(mesh));
@@ -597,16 +656,14 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
                               nm));
     }
 
-    hipStream_t cs = static_cast<hipStream_t>(compute_stream);
-    hipStream_t ms = static_cast<hipStream_t>(comm_stream);
+    Streams S(compute_stream, comm_stream, aux_stream);
     hipEvent_t* ev = nullptr;
-    const size_t n_ev = 2 + 4 * (size_t)chunks + (size_t)chunks;
+    // [0] start  [1] comm end  [2] aux end  [3] fc2 dX done (one-member group)
+    const size_t n_ev = 4 + 4 * (size_t)chunks + (size_t)chunks;
     ATP_CHECK(sync_events(n_ev, &ev));
-    hipEvent_t* ev_gemm = ev + 2;
-    hipEvent_t* ev_red2 = ev + 2 + 4 * chunks;
-
-    HIP_CHECK(hipEventRecord(ev[0], cs), "hipEventRecord");
-    HIP_CHECK(hipStreamWaitEvent(ms, ev[0], 0), "hipStreamWaitEvent");
+    hipEvent_t* ev_gemm = ev + 4;
+    hipEvent_t* ev_red2 = ev + 4 + 4 * chunks;
+    ATP_CHECK(S.begin(ev[0]));
 
     const int64_t mc = tokens / chunks;
     const void* Xin[4] = {io->x_loc, io->attn_loc, io->x_loc, io->h};
@@ -616,52 +673,82 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     void* dXo[4] = {io->dx_qkv, io->d_attn, io->dx_fc1, io->dh_pre};
     const int64_t ld_dxo[4] = {io->ld_dx_qkv, io->ld_d_attn, io->ld_dx_fc1, io->ld_h};
     const bool fc2_reduced = P.g[3].bwd_size > 1;
-    const int order[4] = {3, 2, 1, 0};
+    // MLP chain (fc2 -> fc1) on the compute stream, attention projections
+    // (out, qkv) on the auxiliary stream when one is given
+    const int home[4] = {1, 1, 0, 0};
 
-    for (int oi = 0; oi < 4; ++oi) {
-        const int L = order[oi];
+    // fc1's dY is dh_pre: wait for fc2's reduced chunk c (or all of it), or
+    // for fc2's single dX launch
+    auto wait_dpre = [&](hipStream_t s, int c) -> atp_status {
+        if (fc2_reduced) HIP_CHECK(hipStreamWaitEvent(s, ev_red2[c], 0), "hipStreamWaitEvent");
+        else if (s != S.cs) HIP_CHECK(hipStreamWaitEvent(s, ev[3], 0), "hipStreamWaitEvent");
+        return ATP_OK;
+    };
+    auto dx_unchunked = [&](int L) -> atp_status {
         const atp_shard& g = P.g[L];
-        const int epi = (L == 3) ? atp::EPI_GELU_BWD : atp::EPI_NONE;
-        const void* pre_in = (L == 3) ? io->pre : nullptr;
-        if (g.bwd_size == 1) {
-            if (L == 2 && fc2_reduced)
-                HIP_CHECK(hipStreamWaitEvent(cs, ev_red2[chunks - 1], 0), "hipStreamWaitEvent");
-            atp::GemmProblem p = gemm_problem(atp::LAYOUT_NT, dY[L], ld_dy[L], w->w[L], w->ldw[L],
-                                              dXo[L], ld_dxo[L], true, epi, tokens, g.k_loc,
-                                              g.n_loc);
-            p.pre_in = pre_in;
-            ATP_CHECK(run_gemm(p, cs));
-        } else {
-            float* own = io->dx_partials[L][g.bwd_index];
-            for (int32_t c = 0; c < chunks; ++c) {
-                const int64_t r0 = (int64_t)c * mc;
-                if (L == 2 && fc2_reduced)
-                    HIP_CHECK(hipStreamWaitEvent(cs, ev_red2[c], 0), "hipStreamWaitEvent");
-                atp::GemmProblem p = gemm_problem(
-                    atp::LAYOUT_NT, static_cast<const uint16_t*>(dY[L]) + r0 * ld_dy[L], ld_dy[L],
-                    w->w[L], w->ldw[L], own + r0 * io->ld_dxp[L], io->ld_dxp[L], false,
-                    atp::EPI_NONE, mc, g.k_loc, g.n_loc);
-                ATP_CHECK(run_gemm(p, cs));
-                hipEvent_t e = ev_gemm[L * chunks + c];
-                HIP_CHECK(hipEventRecord(e, cs), "hipEventRecord");
-                HIP_CHECK(hipStreamWaitEvent(ms, e, 0), "hipStreamWaitEvent");
-                atp::ReduceProblem r = reduce_problem(
-                    g.bwd_size, io->dx_partials[L], io->ld_dxp[L], r0, mc, g.k_loc, epi, nullptr,
-                    pre_in, dXo[L], ld_dxo[L], true, nullptr);
-                ATP_CHECK(run_reduce(r, ms));
-                if (L == 3) HIP_CHECK(hipEventRecord(ev_red2[c], ms), "hipEventRecord");
-            }
-        }
-        // dW = X^T dY (all tokens) runs while the dX reductions drain on ms
+        hipStream_t s = S.home(home[L]);
+        if (L == 2) ATP_CHECK(wait_dpre(s, chunks - 1));
+        atp::GemmProblem p = gemm_problem(atp::LAYOUT_NT, dY[L], ld_dy[L], w->w[L], w->ldw[L],
+                                          dXo[L], ld_dxo[L], true,
+                                          L == 3 ? atp::EPI_GELU_BWD : atp::EPI_NONE, tokens,
+                                          g.k_loc, g.n_loc);
+        p.pre_in = (L == 3) ? io->pre : nullptr;
+        ATP_CHECK(run_gemm(p, s));
+        if (L == 3) HIP_CHECK(hipEventRecord(ev[3], s), "hipEventRecord");
+        return ATP_OK;
+    };
+    auto dx_chunk = [&](int L, int c) -> atp_status {
+        const atp_shard& g = P.g[L];
+        hipStream_t s = S.pick(home[L], c);
+        const int64_t r0 = (int64_t)c * mc;
+        if (L == 2) ATP_CHECK(wait_dpre(s, c));
+        float* own = io->dx_partials[L][g.bwd_index];
+        atp::GemmProblem p = gemm_problem(
+            atp::LAYOUT_NT, static_cast<const uint16_t*>(dY[L]) + r0 * ld_dy[L], ld_dy[L],
+            w->w[L], w->ldw[L], own + r0 * io->ld_dxp[L], io->ld_dxp[L], false, atp::EPI_NONE,
+            mc, g.k_loc, g.n_loc);
+        ATP_CHECK(run_gemm(p, s));
+        hipEvent_t e = ev_gemm[L * chunks + c];
+        HIP_CHECK(hipEventRecord(e, s), "hipEventRecord");
+        HIP_CHECK(hipStreamWaitEvent(S.ms, e, 0), "hipStreamWaitEvent");
+        atp::ReduceProblem r = reduce_problem(
+            g.bwd_size, io->dx_partials[L], io->ld_dxp[L], r0, mc, g.k_loc,
+            L == 3 ? atp::EPI_GELU_BWD : atp::EPI_NONE, nullptr, L == 3 ? io->pre : nullptr,
+            dXo[L], ld_dxo[L], true, nullptr);
+        ATP_CHECK(run_reduce(r, S.ms));
+        if (L == 3) HIP_CHECK(hipEventRecord(ev_red2[c], S.ms), "hipEventRecord");
+        return ATP_OK;
+    };
+    // dW = X^T dY over all tokens (and db) on the linear's home stream; it
+    // runs while the linear's dX reductions drain on the comm stream
+    auto dw = [&](int L) -> atp_status {
+        const atp_shard& g = P.g[L];
+        hipStream_t s = S.home(home[L]);
+        if (L == 2) ATP_CHECK(wait_dpre(s, chunks - 1));
         atp::GemmProblem p = gemm_problem(atp::LAYOUT_TN, Xin[L], ldx_in[L], dY[L], ld_dy[L],
                                           io->dw[L], w->ldw[L], false, atp::EPI_NONE, g.k_loc,
                                           g.n_loc, tokens);
-        ATP_CHECK(run_gemm(p, cs));
-        if (io->db[L]) ATP_CHECK(run_colsum(dY[L], ld_dy[L], tokens, g.n_loc, io->db[L], cs));
-    }
-    HIP_CHECK(hipEventRecord(ev[1], ms), "hipEventRecord");
-    HIP_CHECK(hipStreamWaitEvent(cs, ev[1], 0), "hipStreamWaitEvent");
-    return ATP_OK;
+        ATP_CHECK(run_gemm(p, s));
+        if (io->db[L]) ATP_CHECK(run_colsum(dY[L], ld_dy[L], tokens, g.n_loc, io->db[L], s));
+        return ATP_OK;
+    };
+    auto dx = [&](int La, int Lb) -> atp_status {
+        if (P.g[La].bwd_size == 1) ATP_CHECK(dx_unchunked(La));
+        if (P.g[Lb].bwd_size == 1) ATP_CHECK(dx_unchunked(Lb));
+        for (int c = 0; c < chunks; ++c) {
+            if (P.g[La].bwd_size > 1) ATP_CHECK(dx_chunk(La, c));
+            if (P.g[Lb].bwd_size > 1) ATP_CHECK(dx_chunk(Lb, c));
+        }
+        return ATP_OK;
+    };
+    // fc2 with out-proj, then fc1 with qkv: each pair is independent
+    ATP_CHECK(dx(3, 1));
+    ATP_CHECK(dw(3));
+    ATP_CHECK(dw(1));
+    ATP_CHECK(dx(2, 0));
+    ATP_CHECK(dw(2));
+    ATP_CHECK(dw(0));
+    return S.end(ev[1], ev[2]);
 }
 
 void atp_profile_enable(int32_t on) {

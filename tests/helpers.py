@@ -117,8 +117,9 @@ def group_table(own, peers, index):
     return list(peers[:index]) + [own] + list(peers[index:])
 
 
-def run_block_fwd(inp, chunks, compute=None, comm=None, same_stream=False):
-    """Allocate outputs, call atp_block_fwd, return outputs + own partials."""
+def run_block_fwd(inp, chunks, compute=None, comm=None, same_stream=False, aux=True):
+    """Allocate outputs, call atp_block_fwd, return outputs + own partials.
+    aux=True also gives the block a second compute stream."""
     T, G, m = inp["T"], inp["G"], inp["m"]
     dev_ = inp["x"].device
     own = [torch.full((T, g.n_loc), float("nan"), device=dev_) if g.red_size > 1 else None
@@ -132,14 +133,15 @@ def run_block_fwd(inp, chunks, compute=None, comm=None, same_stream=False):
                z=torch.empty((T, G[3].n_loc), dtype=torch.bfloat16, device=dev_))
     cs = compute or torch.cuda.current_stream()
     ms = cs if same_stream else (comm or torch.cuda.Stream())
+    ax = torch.cuda.Stream() if (aux and not same_stream) else None
     atp.atp_block_fwd(m, block_mode_code(inp["mode"]), T, inp["h"], chunks, inp["w"], inp["b"],
                       inp["x"], inp["a"], tabs, out["qkv"], out["o"], out["h"], out["pre"],
-                      out["z"], compute_stream=cs, comm_stream=ms)
+                      out["z"], compute_stream=cs, comm_stream=ms, aux_stream=ax)
     out["own"] = own
     return out
 
 
-def run_block_bwd(inp, chunks, h_act=None, pre=None, same_stream=False):
+def run_block_bwd(inp, chunks, h_act=None, pre=None, same_stream=False, aux=True):
     T, G, m = inp["T"], inp["G"], inp["m"]
     dev_ = inp["x"].device
     h_act = inp["hs"] if h_act is None else h_act
@@ -156,10 +158,11 @@ def run_block_bwd(inp, chunks, h_act=None, pre=None, same_stream=False):
                db=[torch.full((g.n_loc,), float("nan"), device=dev_) for g in G])
     cs = torch.cuda.current_stream()
     ms = cs if same_stream else torch.cuda.Stream()
+    ax = torch.cuda.Stream() if (aux and not same_stream) else None
     atp.atp_block_bwd(m, block_mode_code(inp["mode"]), T, inp["h"], chunks, inp["w"], inp["b"],
                       inp["x"], inp["a"], h_act, pre, inp["dz"], inp["dqkv"], inp["do"], tabs,
                       out["dh_pre"], out["dx_qkv"], out["dx_fc1"], out["d_attn"], out["dw"],
-                      out["db"], compute_stream=cs, comm_stream=ms)
+                      out["db"], compute_stream=cs, comm_stream=ms, aux_stream=ax)
     out["own"] = own
     return out
 

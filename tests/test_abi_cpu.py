@@ -181,7 +181,7 @@ def test_block_validation():
 
     def call(mm=m, bm=0, tokens=T, hh=h, chunks=2):
         return lib.atp_block_fwd(ctypes.byref(mm), bm, tokens, hh, chunks, ctypes.byref(W),
-                                 ctypes.byref(io), None, 0, None, None)
+                                 ctypes.byref(io), None, 0, None, None, None)
     assert call(bm=5) == B.ATP_ERR_INVALID_ARGUMENT
     assert call(hh=500) == B.ATP_ERR_UNSUPPORTED or call(hh=500) == B.ATP_ERR_SHAPE
     assert call(chunks=3) == B.ATP_ERR_SHAPE

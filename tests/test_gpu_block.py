@@ -140,7 +140,7 @@ def _simulate_mesh(mode, mesh, T, h, chunks, X, A, W, B):
                    z=torch.empty((T, G[3].n_loc), dtype=torch.bfloat16, device=DEV))
         atp.atp_block_fwd(L["m"], bm, T, h, chunks, L["w"], L["b"], L["x"], L["a"], tabs,
                           out["qkv"], out["o"], out["h"], out["pre"], out["z"],
-                          comm_stream=torch.cuda.Stream())
+                          comm_stream=torch.cuda.Stream(), aux_stream=torch.cuda.Stream())
         torch.cuda.synchronize()
         res[c] = out
     return res
@@ -184,21 +184,26 @@ def test_chunk_count_never_changes_a_bit():
             assert torch.equal(out[key], base[key]), (chunks, key)
 
 
-def test_serialized_equals_pipelined():
-    inp = make_block_inputs("row", (4, 2), (3, 1), 512, 1024, 0.02, seed=5, bwd=True)
-    a = run_block_fwd(inp, 4, same_stream=True)
-    b = run_block_fwd(inp, 4)
+@pytest.mark.parametrize("mode,mesh,coord", [("row", (4, 2), (3, 1)), ("col", (8, 1), (5, 0)),
+                                             ("col", (1, 4), (0, 2))])
+def test_serialized_equals_pipelined(mode, mesh, coord):
+    """One stream, compute + comm, and compute + comm + auxiliary compute give
+    the same bits (groups of one and of several members)."""
+    inp = make_block_inputs(mode, mesh, coord, 512, 1024, 0.02, seed=5, bwd=True)
+    runs = [dict(same_stream=True), dict(aux=False), dict(aux=True)]
+    fw = [run_block_fwd(inp, 4, **kw) for kw in runs]
     torch.cuda.synchronize()
-    for key in ("qkv", "o", "h", "pre", "z"):
-        assert torch.equal(a[key], b[key]), key
-    ga = run_block_bwd(inp, 4, same_stream=True)
-    gb = run_block_bwd(inp, 4)
+    for other in fw[1:]:
+        for key in ("qkv", "o", "h", "pre", "z"):
+            assert torch.equal(fw[0][key], other[key]), key
+    bw = [run_block_bwd(inp, 4, **kw) for kw in runs]
     torch.cuda.synchronize()
-    for key in ("dh_pre", "dx_qkv", "dx_fc1", "d_attn"):
-        assert torch.equal(ga[key], gb[key]), key
-    for i in range(4):
-        assert torch.equal(ga["dw"][i], gb["dw"][i])
-        assert torch.equal(ga["db"][i], gb["db"][i])
+    for other in bw[1:]:
+        for key in ("dh_pre", "dx_qkv", "dx_fc1", "d_attn"):
+            assert torch.equal(bw[0][key], other[key]), key
+        for i in range(4):
+            assert torch.equal(bw[0]["dw"][i], other["dw"][i])
+            assert torch.equal(bw[0]["db"][i], other["db"][i])
 
 
 def test_row_on_transposed_mesh_equals_col():
