@@ -7,6 +7,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <map>
 #include <mutex>
 #include <string>
@@ -308,19 +309,28 @@ atp_status check_group(float* const* tab, int32_t size, int64_t rows, int64_t ld
 
 const char* const kLinearName[4] = {"qkv", "out", "fc1", "fc2"};
 
-// The block's streams: compute (cs), comm (ms) and an optional auxiliary
-// compute stream (ax).  Chunk c of a linear runs on its home compute stream
-// for even c and on the other one for odd c, so consecutive chunks' GEMMs can
-// share the chip; without an auxiliary stream everything computes on cs.
+// The block's streams: the compute stream (cs), the comm stream (ms) that
+// runs the chunk reductions, and an optional auxiliary compute stream (ax).
+// GEMMs are issued in dependency order and each goes to the compute lane
+// (0 = cs, 1 = ax) with less work issued to it so far, counted in FLOPs, so
+// the two lanes stay busy side by side and one lane's tail wave shares the
+// chip with the other lane's work.  Without an auxiliary stream everything
+// computes on cs, in issue order.
 struct Streams {
     hipStream_t cs, ms, ax;
     bool two;
+    double load[2] = {0.0, 0.0};
     Streams(void* c, void* m, void* a)
         : cs(static_cast<hipStream_t>(c)), ms(static_cast<hipStream_t>(m)),
           ax(a ? static_cast<hipStream_t>(a) : static_cast<hipStream_t>(c)),
           two(a != nullptr && a != c) {}
-    hipStream_t home(int h) const { return (h == 1 && two) ? ax : cs; }
-    hipStream_t pick(int h, int c) const { return home((c & 1) ? 1 - h : h); }
+    hipStream_t lane(int i) const { return i ? ax : cs; }
+    // the less loaded lane (ties go to cs), charged with `flops`
+    int take(double flops) {
+        const int i = (two && load[1] < load[0]) ? 1 : 0;
+        load[i] += flops;
+        return i;
+    }
     // everything already queued on cs happens before the block's work
     atp_status begin(hipEvent_t start) const {
         HIP_CHECK(hipEventRecord(start, cs), "hipEventRecord");
@@ -341,6 +351,8 @@ struct Streams {
         return ATP_OK;
     }
 };
+
+double gemm_flops(int64_t m, int64_t n, int64_t k) { return 2.0 * (double)m * (double)n * (double)k; }
 
 }  // namespace
 
@@ -532,7 +544,7 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
 
     Streams S(compute_stream, comm_stream, aux_stream);
     hipEvent_t* ev = nullptr;
-    // [0] start  [1] comm end  [2] aux end  [3] fc1 done (one-member group)
+    // [0] start  [1] comm end  [2] aux end  [3] fc1's single launch done,
     // then per linear per chunk GEMM-done, then fc1 reduce-done per chunk
     const size_t n_ev = 4 + 4 * (size_t)chunks + (size_t)chunks;
     ATP_CHECK(sync_events(n_ev, &ev));
@@ -546,20 +558,22 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     void* outp[4] = {io->qkv, io->o, io->h, io->z};
     const int64_t ldo[4] = {io->ld_qkv, io->ld_o, io->ld_h, io->ld_z};
     const bool fc1_reduced = P.g[2].red_size > 1;
-    // home compute stream of each linear: the attention projections and the
-    // MLP run on different streams when an auxiliary stream is given
-    const int home[4] = {0, 1, 0, 0};
+    int h_lane = 0;  // lane of fc1's single launch
 
-    // fc2 reads H: wait for fc1's reduced chunk c, or for fc1's single launch
-    auto wait_h = [&](hipStream_t s, int c) -> atp_status {
-        if (fc1_reduced) HIP_CHECK(hipStreamWaitEvent(s, ev_red1[c], 0), "hipStreamWaitEvent");
-        else if (s != S.cs) HIP_CHECK(hipStreamWaitEvent(s, ev[3], 0), "hipStreamWaitEvent");
+    // fc2 reads H: wait for fc1's reduced chunk c (the comm stream runs in
+    // order, so chunk chunks-1 means all of H), or for fc1's single launch
+    auto wait_h = [&](int lane, int c) -> atp_status {
+        if (fc1_reduced)
+            HIP_CHECK(hipStreamWaitEvent(S.lane(lane), ev_red1[c], 0), "hipStreamWaitEvent");
+        else if (lane != h_lane)
+            HIP_CHECK(hipStreamWaitEvent(S.lane(lane), ev[3], 0), "hipStreamWaitEvent");
         return ATP_OK;
     };
     auto unchunked = [&](int L) -> atp_status {
         const atp_shard& g = P.g[L];
-        hipStream_t s = S.home(home[L]);
-        if (L == 3) ATP_CHECK(wait_h(s, chunks - 1));
+        const int lane = S.take(gemm_flops(tokens, g.n_loc, g.k_loc));
+        hipStream_t s = S.lane(lane);
+        if (L == 3) ATP_CHECK(wait_h(lane, chunks - 1));
         atp::GemmProblem p = gemm_problem(atp::LAYOUT_NN, A_in[L], lda_in[L], w->w[L], w->ldw[L],
                                           outp[L], ldo[L], true,
                                           L == 2 ? atp::EPI_BIAS_GELU : atp::EPI_BIAS, tokens,
@@ -567,14 +581,20 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         p.bias = w->b[L];
         p.pre_out = (L == 2) ? io->pre : nullptr;
         ATP_CHECK(run_gemm(p, s));
-        if (L == 2) HIP_CHECK(hipEventRecord(ev[3], s), "hipEventRecord");
+        if (L == 2) {
+            HIP_CHECK(hipEventRecord(ev[3], s), "hipEventRecord");
+            h_lane = lane;
+        }
         return ATP_OK;
     };
+    // chunk c: the GEMM writes this device's partial rows, the comm stream
+    // reduces the group's partials for those rows as soon as they are ready
     auto chunk = [&](int L, int c) -> atp_status {
         const atp_shard& g = P.g[L];
-        hipStream_t s = S.pick(home[L], c);
+        const int lane = S.take(gemm_flops(mc, g.n_loc, g.k_loc));
+        hipStream_t s = S.lane(lane);
         const int64_t r0 = (int64_t)c * mc;
-        if (L == 3) ATP_CHECK(wait_h(s, c));
+        if (L == 3) ATP_CHECK(wait_h(lane, c));
         float* own = io->partials[L][g.red_index];
         atp::GemmProblem p = gemm_problem(
             atp::LAYOUT_NN, static_cast<const uint16_t*>(A_in[L]) + r0 * lda_in[L], lda_in[L],
@@ -592,26 +612,18 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         if (L == 2) HIP_CHECK(hipEventRecord(ev_red1[c], S.ms), "hipEventRecord");
         return ATP_OK;
     };
-    // the two independent linears of each pair are issued chunk by chunk in
-    // turn, so their reductions reach the comm stream in completion order
-    const int pairs[2][2] = {{0, 1}, {2, 3}};
-    for (int q = 0; q < 2; ++q) {
-        const int La = pairs[q][0], Lb = pairs[q][1];
-        if (q == 1) {
-            // fc2 depends on fc1: fc1 first, then fc2 (chunk by chunk)
-            if (P.g[La].red_size == 1) ATP_CHECK(unchunked(La));
-            else for (int c = 0; c < chunks; ++c) ATP_CHECK(chunk(La, c));
-            if (P.g[Lb].red_size == 1) ATP_CHECK(unchunked(Lb));
-            else for (int c = 0; c < chunks; ++c) ATP_CHECK(chunk(Lb, c));
-            continue;
-        }
-        if (P.g[La].red_size == 1) ATP_CHECK(unchunked(La));
-        if (P.g[Lb].red_size == 1) ATP_CHECK(unchunked(Lb));
-        for (int c = 0; c < chunks; ++c) {
-            if (P.g[La].red_size > 1) ATP_CHECK(chunk(La, c));
-            if (P.g[Lb].red_size > 1) ATP_CHECK(chunk(Lb, c));
-        }
-    }
+    auto linear = [&](int L) -> atp_status {
+        if (P.g[L].red_size == 1) return unchunked(L);
+        for (int c = 0; c < chunks; ++c) ATP_CHECK(chunk(L, c));
+        return ATP_OK;
+    };
+    // fc1 first, since fc2 waits for it; the attention projections fill the
+    // other lane meanwhile (out first, so its reductions start early); fc2
+    // last, chunk by chunk behind fc1's output
+    ATP_CHECK(linear(2));
+    ATP_CHECK(linear(1));
+    ATP_CHECK(linear(0));
+    ATP_CHECK(linear(3));
     return S.end(ev[1], ev[2]);
 }
 
@@ -658,7 +670,8 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
 
     Streams S(compute_stream, comm_stream, aux_stream);
     hipEvent_t* ev = nullptr;
-    // [0] start  [1] comm end  [2] aux end  [3] fc2 dX done (one-member group)
+    // [0] start  [1] comm end  [2] aux end  [3] fc2's single dX launch done,
+    // then per linear per chunk GEMM-done, then fc2 reduce-done per chunk
     const size_t n_ev = 4 + 4 * (size_t)chunks + (size_t)chunks;
     ATP_CHECK(sync_events(n_ev, &ev));
     hipEvent_t* ev_gemm = ev + 4;
@@ -673,35 +686,41 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     void* dXo[4] = {io->dx_qkv, io->d_attn, io->dx_fc1, io->dh_pre};
     const int64_t ld_dxo[4] = {io->ld_dx_qkv, io->ld_d_attn, io->ld_dx_fc1, io->ld_h};
     const bool fc2_reduced = P.g[3].bwd_size > 1;
-    // MLP chain (fc2 -> fc1) on the compute stream, attention projections
-    // (out, qkv) on the auxiliary stream when one is given
-    const int home[4] = {1, 1, 0, 0};
+    int dpre_lane = 0;  // lane of fc2's single dX launch
 
-    // fc1's dY is dh_pre: wait for fc2's reduced chunk c (or all of it), or
-    // for fc2's single dX launch
-    auto wait_dpre = [&](hipStream_t s, int c) -> atp_status {
-        if (fc2_reduced) HIP_CHECK(hipStreamWaitEvent(s, ev_red2[c], 0), "hipStreamWaitEvent");
-        else if (s != S.cs) HIP_CHECK(hipStreamWaitEvent(s, ev[3], 0), "hipStreamWaitEvent");
+    // fc1's dY is dh_pre: wait for fc2's reduced chunk c (chunk chunks-1
+    // means all of it, the comm stream runs in order), or for fc2's single
+    // dX launch
+    auto wait_dpre = [&](int lane, int c) -> atp_status {
+        if (fc2_reduced)
+            HIP_CHECK(hipStreamWaitEvent(S.lane(lane), ev_red2[c], 0), "hipStreamWaitEvent");
+        else if (lane != dpre_lane)
+            HIP_CHECK(hipStreamWaitEvent(S.lane(lane), ev[3], 0), "hipStreamWaitEvent");
         return ATP_OK;
     };
     auto dx_unchunked = [&](int L) -> atp_status {
         const atp_shard& g = P.g[L];
-        hipStream_t s = S.home(home[L]);
-        if (L == 2) ATP_CHECK(wait_dpre(s, chunks - 1));
+        const int lane = S.take(gemm_flops(tokens, g.k_loc, g.n_loc));
+        hipStream_t s = S.lane(lane);
+        if (L == 2) ATP_CHECK(wait_dpre(lane, chunks - 1));
         atp::GemmProblem p = gemm_problem(atp::LAYOUT_NT, dY[L], ld_dy[L], w->w[L], w->ldw[L],
                                           dXo[L], ld_dxo[L], true,
                                           L == 3 ? atp::EPI_GELU_BWD : atp::EPI_NONE, tokens,
                                           g.k_loc, g.n_loc);
         p.pre_in = (L == 3) ? io->pre : nullptr;
         ATP_CHECK(run_gemm(p, s));
-        if (L == 3) HIP_CHECK(hipEventRecord(ev[3], s), "hipEventRecord");
+        if (L == 3) {
+            HIP_CHECK(hipEventRecord(ev[3], s), "hipEventRecord");
+            dpre_lane = lane;
+        }
         return ATP_OK;
     };
     auto dx_chunk = [&](int L, int c) -> atp_status {
         const atp_shard& g = P.g[L];
-        hipStream_t s = S.pick(home[L], c);
+        const int lane = S.take(gemm_flops(mc, g.k_loc, g.n_loc));
+        hipStream_t s = S.lane(lane);
         const int64_t r0 = (int64_t)c * mc;
-        if (L == 2) ATP_CHECK(wait_dpre(s, c));
+        if (L == 2) ATP_CHECK(wait_dpre(lane, c));
         float* own = io->dx_partials[L][g.bwd_index];
         atp::GemmProblem p = gemm_problem(
             atp::LAYOUT_NT, static_cast<const uint16_t*>(dY[L]) + r0 * ld_dy[L], ld_dy[L],
@@ -719,35 +738,36 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         if (L == 3) HIP_CHECK(hipEventRecord(ev_red2[c], S.ms), "hipEventRecord");
         return ATP_OK;
     };
-    // dW = X^T dY over all tokens (and db) on the linear's home stream; it
-    // runs while the linear's dX reductions drain on the comm stream
+    auto dx = [&](int L) -> atp_status {
+        if (P.g[L].bwd_size == 1) return dx_unchunked(L);
+        for (int c = 0; c < chunks; ++c) ATP_CHECK(dx_chunk(L, c));
+        return ATP_OK;
+    };
+    // db (column sums of dY), then dW = X^T dY over all tokens; these need
+    // no reduction and fill the lanes while the dX reductions drain
     auto dw = [&](int L) -> atp_status {
         const atp_shard& g = P.g[L];
-        hipStream_t s = S.home(home[L]);
-        if (L == 2) ATP_CHECK(wait_dpre(s, chunks - 1));
+        const int lane = S.take(gemm_flops(g.k_loc, g.n_loc, tokens));
+        hipStream_t s = S.lane(lane);
+        if (L == 2) ATP_CHECK(wait_dpre(lane, chunks - 1));
+        if (io->db[L]) ATP_CHECK(run_colsum(dY[L], ld_dy[L], tokens, g.n_loc, io->db[L], s));
         atp::GemmProblem p = gemm_problem(atp::LAYOUT_TN, Xin[L], ldx_in[L], dY[L], ld_dy[L],
                                           io->dw[L], w->ldw[L], false, atp::EPI_NONE, g.k_loc,
                                           g.n_loc, tokens);
-        ATP_CHECK(run_gemm(p, s));
-        if (io->db[L]) ATP_CHECK(run_colsum(dY[L], ld_dy[L], tokens, g.n_loc, io->db[L], s));
-        return ATP_OK;
+        return run_gemm(p, s);
     };
-    auto dx = [&](int La, int Lb) -> atp_status {
-        if (P.g[La].bwd_size == 1) ATP_CHECK(dx_unchunked(La));
-        if (P.g[Lb].bwd_size == 1) ATP_CHECK(dx_unchunked(Lb));
-        for (int c = 0; c < chunks; ++c) {
-            if (P.g[La].bwd_size > 1) ATP_CHECK(dx_chunk(La, c));
-            if (P.g[Lb].bwd_size > 1) ATP_CHECK(dx_chunk(Lb, c));
-        }
-        return ATP_OK;
-    };
-    // fc2 with out-proj, then fc1 with qkv: each pair is independent
-    ATP_CHECK(dx(3, 1));
-    ATP_CHECK(dw(3));
-    ATP_CHECK(dw(1));
-    ATP_CHECK(dx(2, 0));
-    ATP_CHECK(dw(2));
-    ATP_CHECK(dw(0));
+    // fc2's dX first (it makes dh_pre, which fc1 waits for); then the
+    // attention projections' dX, whose reductions can start at once; then
+    // fc1's dX; the four dW last, largest first
+    ATP_CHECK(dx(3));
+    ATP_CHECK(dx(0));
+    ATP_CHECK(dx(1));
+    ATP_CHECK(dx(2));
+    int order[4] = {3, 2, 0, 1};
+    std::stable_sort(order, order + 4, [&](int i, int j) {
+        return P.g[i].k_loc * P.g[i].n_loc > P.g[j].k_loc * P.g[j].n_loc;
+    });
+    for (int L : order) ATP_CHECK(dw(L));
     return S.end(ev[1], ev[2]);
 }
 
