@@ -38,7 +38,7 @@ def log(*a):
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--chunks", type=int, default=None, help="override the chunk count")
@@ -48,7 +48,7 @@ def parse():
     ap.add_argument("--no-aux", action="store_true",
                     help="no second compute stream (independent GEMMs do not share the chip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=64,
+    ap.add_argument("--cpu-rows", type=int, default=256,
                     help="token rows in the oracle's timed CPU sample")
     ap.add_argument("--copy-calib-mb", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB "
@@ -200,6 +200,36 @@ def cpu_baseline(st, rows_n, fwd_only, seed):
                 sample=sample, seconds=round(dt, 3))
 
 
+def reduce_alone(torch, atp, st, reps):
+    """The largest reduction of the step (one chunk), timed with nothing else
+    running: its group's partial buffers, the bias epilogue, bf16 output."""
+    cand = [(len(t), i) for i, t in enumerate(st["fwd_tabs"]) if t]
+    if not cand:
+        return None
+    _, L = max(cand, key=lambda c: (c[0], st["G"][c[1]].n_loc))
+    g, T, c = st["G"][L], st["T"], st["chunks"]
+    rows = T // c
+    tab = [p[:rows] for p in st["fwd_tabs"][L]]
+    out = torch.empty((rows, g.n_loc), dtype=torch.bfloat16, device="cuda:0")
+    run = lambda: atp.atp_chunked_partial_reduce(len(tab), rows, g.n_loc, 1, tab, st["b"][L],  # noqa: E731
+                                                 atp.ATP_EPI_BIAS, out)
+    for _ in range(3):
+        run()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    nbytes = len(tab) * rows * g.n_loc * 4 + rows * g.n_loc * 2 + g.n_loc * 2
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return dict(linear=LIN[L], red_size=len(tab), rows=rows, n_loc=g.n_loc,
+                avg_us=round(ms * 1e3, 2), achieved=round(gbs, 1), peak=PEAK_HBM_GBS,
+                frac=round(gbs / PEAK_HBM_GBS, 4))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -229,20 +259,26 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] warmup done ({args.warmup} steps)")
 
-    # timed region: inputs resident, K steps between two device-wide syncs
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
+    # timed region: inputs resident, K steps between two device-wide syncs;
+    # an event after each step (on the stream the block joins into) gives the
+    # per-step distribution
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    ev0.record()
-    for _ in range(args.steps):
+    evs[0].record()
+    for i in range(args.steps):
         step()
-    ev1.record()
+        evs[i + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms_step = max(ev0.elapsed_time(ev1), wall * 1e3) / args.steps
+    ms_step = max(evs[0].elapsed_time(evs[-1]), wall * 1e3) / args.steps
     value = flops / (ms_step * 1e-3) / 1e12
-    log(f"[bench] {args.steps} steps, {ms_step:.3f} ms/step, {value:.1f} TFLOP/s")
+    per = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
+    q = lambda f: per[min(len(per) - 1, int(round(f * (len(per) - 1))))]  # noqa: E731
+    step_ms = dict(median=round(q(0.5), 4), p10=round(q(0.1), 4), p90=round(q(0.9), 4),
+                   min=round(per[0], 4), max=round(per[-1], 4))
+    log(f"[bench] {args.steps} steps, {ms_step:.3f} ms/step, {value:.1f} TFLOP/s "
+        f"(per step median {step_ms['median']:.3f} p10 {step_ms['p10']:.3f} p90 {step_ms['p90']:.3f} ms)")
 
     # same K steps again with every library launch bracketed by HIP events on
     # its own stream: per-kernel durations for the roofline
@@ -283,6 +319,10 @@ def main():
                            note="durations measured while overlapping the GEMMs")
     for k in kernels:
         log(f"[bench]   {k}")
+    alone = reduce_alone(torch, atp, st, args.steps)
+    if alone and reduce_info is not None:
+        reduce_info["alone"] = alone
+        log(f"[bench] partial reduce alone: {alone}")
 
     if args.profile_detail:
         atp.atp_profile_enable(2)
@@ -322,7 +362,7 @@ def main():
                     **{"pass": "fwd" if fwd_only else "fwd+bwd"},
                     serial=bool(args.serial), aux_stream=not args.no_aux,
                     gflop_per_step=round(flops / 1e9, 1)),
-        mfma_util=round(value / PEAK_BF16_TFLOPS, 4),
+        step_ms=step_ms, mfma_util=round(value / PEAK_BF16_TFLOPS, 4),
         roofline=roofline, reduce=reduce_info, kernels=kernels, cpu_baseline=cpu)
     print(json.dumps(out), flush=True)
 

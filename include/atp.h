@@ -276,6 +276,88 @@ const char* atp_status_string(int32_t status);
 const char* atp_last_error(void);
 const char* atp_version(void);
 
+/* ------------------------------------------------------------------------
+ * Mesh planner (host only; no GPU needed, nothing is enqueued).
+ *
+ * Picks the DeviceMesh(d1, d2) of least tensor-parallel communication time
+ * for N devices on an interconnect described by a hierarchical
+ * communication matrix (HCM, Sec. 3.4): the search space is every (d1, d2)
+ * with d1 * d2 = N (Sec. 3.2), the per-axis all-reduce bandwidths come from
+ * Eq. (bwd) and Eq. (allreduce) (Sec. 3.5), the time from Eq. (tcomm)
+ * (Sec. 3.3).
+ *
+ * HCM: `n_layers` layers, outermost first (e.g. nodes, then GPUs in a
+ * node).  Device r of the mesh (r = i1 * d2 + i2) has, at layer j, the rank
+ * index (r / D_j) % R_j, with D_j the product of the rank counts of the
+ * layers inside j.  Axis 1 all-reduces run among the devices with equal i2,
+ * axis 2 among those with equal i1.
+ *
+ * B1' / B2' (Eq. (bwd)): at every layer an axis group spans with more than
+ * one rank of one parent, each spanned rank u offers the group
+ * min(group_bw, sum of p2p[u][v] over the group's other ranks v there),
+ * divided by the number of that axis's groups spanning the layer through u;
+ * B' is the least such value over the group's layers.  This is the paper's
+ * division by d2 when a node hosts d2 groups, its P2P correction of
+ * DeviceMesh(8, 2), and no division when ranks are single devices (its
+ * switch and torus cases).  B = d / (2 (d - 1)) B' (Eq. (allreduce)); an
+ * axis of size 1 has no all-reduce (B' = 0, B = +inf, its Eq. (tcomm) term
+ * is 0).  T_comm = 2 L b s elem_bytes (7 h / (d1 B2) + 2 h / (d2 B1)) / 1e9
+ * seconds for bandwidths in GB/s; +inf when a spanned rank has no
+ * bandwidth to the rest of its group.
+ *
+ * Errors: ATP_ERR_INVALID_ARGUMENT for NULL pointers, n_layers outside
+ * 1..ATP_PLAN_MAX_LAYERS, a rank count < 1, a group_bw <= 0 or not finite, a
+ * negative or non-finite p2p entry, model sizes < 1, elem_bytes < 1, a
+ * bandwidth given to atp_tcomm that is not > 0 (+inf is allowed), or a
+ * `costs` array too small; ATP_ERR_SHAPE when d1 * d2 differs from the
+ * HCM's device count; ATP_ERR_UNSUPPORTED above ATP_PLAN_MAX_DEVICES devices.
+ * ------------------------------------------------------------------------ */
+#define ATP_PLAN_MAX_LAYERS 16
+#define ATP_PLAN_MAX_DEVICES 65536
+
+typedef struct {
+    int32_t ranks;       /* ranks of this layer under one parent, >= 1 */
+    double group_bw;     /* GB/s from one rank of this layer to outside it */
+    const double* p2p;   /* [ranks][ranks] row-major GB/s between ranks of one
+                            parent (diagonal ignored); NULL = every pair at
+                            group_bw, as behind a switch.  Host memory, read
+                            during the call only. */
+} atp_hcm_layer;
+
+typedef struct {
+    int64_t layers;      /* L, transformer layers */
+    int64_t batch;       /* b */
+    int64_t seq;         /* s */
+    int64_t hidden;      /* h */
+    int32_t elem_bytes;  /* bytes per all-reduced element (2 for fp16 / bf16) */
+} atp_model_dims;
+
+typedef struct {
+    int32_t d1, d2;
+    double b1_eff, b2_eff;  /* B1', B2' in GB/s (0 for an axis of size 1) */
+    double b1, b2;          /* Eq. (allreduce) bandwidths, GB/s (+inf for size 1) */
+    double t_comm;          /* Eq. (tcomm), seconds */
+} atp_mesh_cost;
+
+/* Eq. (tcomm) for given algorithm bandwidths b1, b2 (GB/s, > 0, +inf = no
+ * all-reduce on that axis), e.g. calibrated from measured all-reduces
+ * (Sec. 5.3).  *t_out in seconds. */
+atp_status atp_tcomm(const atp_model_dims* dims, int32_t d1, int32_t d2, double b1, double b2,
+                     double* t_out);
+
+/* B1', B2', B1, B2 and T_comm of DeviceMesh(d1, d2) on the HCM. */
+atp_status atp_hcm_mesh_cost(const atp_hcm_layer* hcm, int32_t n_layers,
+                             const atp_model_dims* dims, int32_t d1, int32_t d2,
+                             atp_mesh_cost* out);
+
+/* Every candidate mesh of the HCM's N devices, largest d1 first: when
+ * `costs` is not NULL their costs go to costs[0 .. n-1] (max_costs must be
+ * >= n); *n_meshes (if not NULL) receives n; *best receives the cost of the
+ * mesh of least T_comm (ties: the larger d1). */
+atp_status atp_plan_mesh(const atp_hcm_layer* hcm, int32_t n_layers, const atp_model_dims* dims,
+                         atp_mesh_cost* best, atp_mesh_cost* costs, int32_t max_costs,
+                         int32_t* n_meshes);
+
 #ifdef __cplusplus
 }
 #endif

@@ -10,6 +10,8 @@ there is no fallback path: without ``libatp.so`` every call raises.
 """
 from .binding import *  # noqa: F401,F403
 from .binding import load_library, AtpError, HipEvent, LIB_PATH, EXPORTS  # noqa: F401
+from .binding import Hcm, hcm_mi355x_xgmi, model_dims  # noqa: F401
 
 __all__ = [n for n in dir() if n.startswith(("atp_", "ATP_"))] + [
-    "load_library", "AtpError", "HipEvent", "LIB_PATH", "EXPORTS", "mesh", "block_geometry"]
+    "load_library", "AtpError", "HipEvent", "LIB_PATH", "EXPORTS", "mesh", "block_geometry",
+    "Hcm", "hcm_mi355x_xgmi", "model_dims"]

@@ -102,11 +102,30 @@ class atp_kernel_stat(ctypes.Structure):
                 ("bytes", ctypes.c_double)]
 
 
+class atp_hcm_layer(ctypes.Structure):
+    _fields_ = [("ranks", ctypes.c_int32), ("group_bw", ctypes.c_double),
+                ("p2p", ctypes.POINTER(ctypes.c_double))]
+
+
+class atp_model_dims(ctypes.Structure):
+    _fields_ = [("layers", ctypes.c_int64), ("batch", ctypes.c_int64), ("seq", ctypes.c_int64),
+                ("hidden", ctypes.c_int64), ("elem_bytes", ctypes.c_int32)]
+
+
+class atp_mesh_cost(ctypes.Structure):
+    _fields_ = [("d1", ctypes.c_int32), ("d2", ctypes.c_int32),
+                ("b1_eff", ctypes.c_double), ("b2_eff", ctypes.c_double),
+                ("b1", ctypes.c_double), ("b2", ctypes.c_double), ("t_comm", ctypes.c_double)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
 EXPORTS = (
     "atp_shard_geometry", "atp_shard_linear_fwd", "atp_chunked_partial_reduce",
     "atp_shard_linear_bwd", "atp_block_workspace_bytes", "atp_block_fwd", "atp_block_bwd",
     "atp_profile_enable", "atp_profile_collect", "atp_status_string", "atp_last_error",
-    "atp_version",
+    "atp_version", "atp_tcomm", "atp_hcm_mesh_cost", "atp_plan_mesh",
 )
 
 _lib = None
@@ -153,6 +172,15 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.atp_last_error.restype = ctypes.c_char_p
     lib.atp_version.argtypes = []
     lib.atp_version.restype = ctypes.c_char_p
+    hp, dp, cp = (ctypes.POINTER(atp_hcm_layer), ctypes.POINTER(atp_model_dims),
+                  ctypes.POINTER(atp_mesh_cost))
+    lib.atp_tcomm.argtypes = [dp, i32, i32, ctypes.c_double, ctypes.c_double,
+                              ctypes.POINTER(ctypes.c_double)]
+    lib.atp_tcomm.restype = i32
+    lib.atp_hcm_mesh_cost.argtypes = [hp, i32, dp, i32, i32, cp]
+    lib.atp_hcm_mesh_cost.restype = i32
+    lib.atp_plan_mesh.argtypes = [hp, i32, dp, cp, cp, i32, ctypes.POINTER(i32)]
+    lib.atp_plan_mesh.restype = i32
     _lib = lib
     return lib
 
@@ -449,3 +477,63 @@ def atp_profile_collect(max_records: int = 32):
     return [dict(name=arr[i].name.decode(), launches=arr[i].launches,
                  total_ms=arr[i].total_ms, flops=arr[i].flops, bytes=arr[i].bytes)
             for i in range(n)]
+
+
+# ---------------------------------------------------------------------------
+# Mesh planner (host only)
+# ---------------------------------------------------------------------------
+class Hcm:
+    """A hierarchical communication matrix: `layers` is a list of
+    (ranks, group_bw, p2p) outermost first, p2p a ranks x ranks nested list of
+    GB/s or None (every pair at group_bw)."""
+
+    def __init__(self, layers):
+        self._keep = []
+        arr = (atp_hcm_layer * len(layers))()
+        for j, (ranks, group_bw, p2p) in enumerate(layers):
+            arr[j].ranks = int(ranks)
+            arr[j].group_bw = float(group_bw)
+            if p2p is None:
+                arr[j].p2p = None
+            else:
+                flat = (ctypes.c_double * (int(ranks) * int(ranks)))(
+                    *[float(x) for row in p2p for x in row])
+                self._keep.append(flat)
+                arr[j].p2p = ctypes.cast(flat, ctypes.POINTER(ctypes.c_double))
+        self.layers = arr
+        self.n = len(layers)
+
+
+def hcm_mi355x_xgmi(gpus: int = 8, link_gbs: float = 153.0) -> Hcm:
+    """One MI355X node: `gpus` GPUs, every pair joined by one xGMI link of
+    `link_gbs` GB/s, so a GPU's group bandwidth is (gpus - 1) links."""
+    p2p = [[0.0 if u == v else link_gbs for v in range(gpus)] for u in range(gpus)]
+    return Hcm([(gpus, (gpus - 1) * link_gbs, p2p)])
+
+
+def model_dims(layers: int, batch: int, seq: int, hidden: int, elem_bytes: int = 2):
+    return atp_model_dims(int(layers), int(batch), int(seq), int(hidden), int(elem_bytes))
+
+
+def atp_tcomm(dims: atp_model_dims, d1: int, d2: int, b1: float, b2: float) -> float:
+    t = ctypes.c_double()
+    _check(load_library().atp_tcomm(ctypes.byref(dims), int(d1), int(d2), float(b1), float(b2),
+                                    ctypes.byref(t)))
+    return t.value
+
+
+def atp_hcm_mesh_cost(hcm: Hcm, dims: atp_model_dims, d1: int, d2: int) -> dict:
+    c = atp_mesh_cost()
+    _check(load_library().atp_hcm_mesh_cost(hcm.layers, hcm.n, ctypes.byref(dims), int(d1),
+                                            int(d2), ctypes.byref(c)))
+    return c.as_dict()
+
+
+def atp_plan_mesh(hcm: Hcm, dims: atp_model_dims, max_costs: int = 256):
+    """(best mesh cost, costs of every candidate mesh, largest d1 first)."""
+    best = atp_mesh_cost()
+    arr = (atp_mesh_cost * max_costs)()
+    n = ctypes.c_int32()
+    _check(load_library().atp_plan_mesh(hcm.layers, hcm.n, ctypes.byref(dims), ctypes.byref(best),
+                                        arr, int(max_costs), ctypes.byref(n)))
+    return best.as_dict(), [arr[i].as_dict() for i in range(n.value)]

@@ -14,13 +14,15 @@
 #include <vector>
 
 #include "../../include/atp.h"
+#include "errors.h"
 #include "kernels.h"
 
 namespace {
-
 thread_local std::string g_last_error;
+}  // namespace
 
-atp_status fail(atp_status s, const char* fmt, ...) {
+namespace atp {
+atp_status set_error(atp_status s, const char* fmt, ...) {
     char buf[512];
     va_list ap;
     va_start(ap, fmt);
@@ -29,9 +31,14 @@ atp_status fail(atp_status s, const char* fmt, ...) {
     g_last_error = buf;
     return s;
 }
+}  // namespace atp
+
+namespace {
+
+using atp::set_error;
 
 atp_status hip_fail(hipError_t e, const char* what) {
-    return fail(ATP_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+    return set_error(ATP_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
 }
 
 #define ATP_CHECK(expr)                                   \
@@ -49,12 +56,12 @@ atp_status hip_fail(hipError_t e, const char* what) {
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 atp_status check_mesh(const atp_mesh* m) {
-    if (!m) return fail(ATP_ERR_INVALID_ARGUMENT, "mesh is NULL");
+    if (!m) return set_error(ATP_ERR_INVALID_ARGUMENT, "mesh is NULL");
     if (m->d1 <= 0 || m->d2 <= 0)
-        return fail(ATP_ERR_INVALID_ARGUMENT, "mesh dims must be positive (d1=%d d2=%d)", m->d1,
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "mesh dims must be positive (d1=%d d2=%d)", m->d1,
                     m->d2);
     if (m->i1 < 0 || m->i1 >= m->d1 || m->i2 < 0 || m->i2 >= m->d2)
-        return fail(ATP_ERR_INVALID_ARGUMENT, "coordinate (%d,%d) outside mesh (%d,%d)", m->i1,
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "coordinate (%d,%d) outside mesh (%d,%d)", m->i1,
                     m->i2, m->d1, m->d2);
     return ATP_OK;
 }
@@ -62,8 +69,8 @@ atp_status check_mesh(const atp_mesh* m) {
 atp_status geometry(const atp_mesh* m, int32_t mode, int64_t k, int64_t n, atp_shard* g) {
     ATP_CHECK(check_mesh(m));
     if (mode != ATP_ROW_FIRST && mode != ATP_COL_FIRST)
-        return fail(ATP_ERR_INVALID_ARGUMENT, "mode %d is neither row- nor column-first", mode);
-    if (k <= 0 || n <= 0) return fail(ATP_ERR_INVALID_ARGUMENT, "k and n must be positive");
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "mode %d is neither row- nor column-first", mode);
+    if (k <= 0 || n <= 0) return set_error(ATP_ERR_INVALID_ARGUMENT, "k and n must be positive");
     // Row-first: W [Shard(0), Shard(1)] -> rows split by d1, columns by d2,
     // output partial over mesh axis 0.  Column-first: W [Shard(1), Shard(0)]
     // -> columns split by d1, rows by d2, output partial over mesh axis 1.
@@ -73,7 +80,7 @@ atp_status geometry(const atp_mesh* m, int32_t mode, int64_t k, int64_t n, atp_s
     const int32_t ik = row ? m->i1 : m->i2;
     const int32_t in = row ? m->i2 : m->i1;
     if (k % dk != 0 || n % dn != 0)
-        return fail(ATP_ERR_SHAPE, "k=%lld not divisible by %d or n=%lld not divisible by %d",
+        return set_error(ATP_ERR_SHAPE, "k=%lld not divisible by %d or n=%lld not divisible by %d",
                     (long long)k, dk, (long long)n, dn);
     g->k_loc = k / dk;
     g->n_loc = n / dn;
@@ -89,12 +96,12 @@ atp_status geometry(const atp_mesh* m, int32_t mode, int64_t k, int64_t n, atp_s
 }
 
 atp_status check_chunks(int64_t tokens, int32_t chunks) {
-    if (tokens < 0) return fail(ATP_ERR_INVALID_ARGUMENT, "tokens must be >= 0");
+    if (tokens < 0) return set_error(ATP_ERR_INVALID_ARGUMENT, "tokens must be >= 0");
     if (chunks < 1 || chunks > ATP_MAX_CHUNKS)
-        return fail(ATP_ERR_INVALID_ARGUMENT, "chunks=%d outside [1, %d]", chunks,
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "chunks=%d outside [1, %d]", chunks,
                     ATP_MAX_CHUNKS);
     if (tokens % chunks != 0)
-        return fail(ATP_ERR_SHAPE, "tokens=%lld not divisible by chunks=%d", (long long)tokens,
+        return set_error(ATP_ERR_SHAPE, "tokens=%lld not divisible by chunks=%d", (long long)tokens,
                     chunks);
     return ATP_OK;
 }
@@ -102,22 +109,22 @@ atp_status check_chunks(int64_t tokens, int32_t chunks) {
 // A matrix with zero rows is never touched and may be NULL.
 atp_status check_mat(const void* p, int64_t rows, int64_t ld, int64_t cols, const char* name) {
     if (ld > (int64_t)1 << 22)
-        return fail(ATP_ERR_UNSUPPORTED, "%s: leading dimension %lld above 4M elements", name,
+        return set_error(ATP_ERR_UNSUPPORTED, "%s: leading dimension %lld above 4M elements", name,
                     (long long)ld);
     if (rows == 0 && !p) return ATP_OK;
-    if (!p) return fail(ATP_ERR_INVALID_ARGUMENT, "%s is NULL", name);
-    if (ld < cols) return fail(ATP_ERR_INVALID_ARGUMENT, "%s: ld %lld < %lld columns", name,
+    if (!p) return set_error(ATP_ERR_INVALID_ARGUMENT, "%s is NULL", name);
+    if (ld < cols) return set_error(ATP_ERR_INVALID_ARGUMENT, "%s: ld %lld < %lld columns", name,
                                (long long)ld, (long long)cols);
-    if (!aligned16(p)) return fail(ATP_ERR_UNSUPPORTED, "%s is not 16-byte aligned", name);
+    if (!aligned16(p)) return set_error(ATP_ERR_UNSUPPORTED, "%s is not 16-byte aligned", name);
     if (ld % 8 != 0 || cols % 8 != 0)
-        return fail(ATP_ERR_UNSUPPORTED, "%s: ld %lld and columns %lld must be multiples of 8",
+        return set_error(ATP_ERR_UNSUPPORTED, "%s: ld %lld and columns %lld must be multiples of 8",
                     name, (long long)ld, (long long)cols);
     return ATP_OK;
 }
 
 atp_status check_vec(const void* p, const char* name) {
-    if (!p) return fail(ATP_ERR_INVALID_ARGUMENT, "%s is NULL", name);
-    if (!aligned16(p)) return fail(ATP_ERR_UNSUPPORTED, "%s is not 16-byte aligned", name);
+    if (!p) return set_error(ATP_ERR_INVALID_ARGUMENT, "%s is NULL", name);
+    if (!aligned16(p)) return set_error(ATP_ERR_UNSUPPORTED, "%s is not 16-byte aligned", name);
     return ATP_OK;
 }
 
@@ -273,8 +280,8 @@ struct BlockPlan {
 
 atp_status block_plan(const atp_mesh* m, int32_t bm, int64_t h, BlockPlan* p) {
     if (bm != ATP_BLOCK_COL && bm != ATP_BLOCK_ROW)
-        return fail(ATP_ERR_INVALID_ARGUMENT, "block mode %d unknown", bm);
-    if (h <= 0) return fail(ATP_ERR_INVALID_ARGUMENT, "h must be positive");
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "block mode %d unknown", bm);
+    if (h <= 0) return set_error(ATP_ERR_INVALID_ARGUMENT, "h must be positive");
     const int32_t pc = ATP_COL_FIRST, pr = ATP_ROW_FIRST;
     const int32_t modes_col[4] = {pc, pr, pc, pr};
     const int32_t modes_row[4] = {pr, pc, pr, pc};
@@ -286,7 +293,7 @@ atp_status block_plan(const atp_mesh* m, int32_t bm, int64_t h, BlockPlan* p) {
         p->N[i] = N[i];
         ATP_CHECK(geometry(m, p->mode[i], K[i], N[i], &p->g[i]));
         if (p->g[i].k_loc % 8 || p->g[i].n_loc % 8)
-            return fail(ATP_ERR_UNSUPPORTED, "local block %lldx%lld of linear %d: sizes must be "
+            return set_error(ATP_ERR_UNSUPPORTED, "local block %lldx%lld of linear %d: sizes must be "
                         "multiples of 8", (long long)p->g[i].k_loc, (long long)p->g[i].n_loc, i);
     }
     return ATP_OK;
@@ -295,10 +302,10 @@ atp_status block_plan(const atp_mesh* m, int32_t bm, int64_t h, BlockPlan* p) {
 atp_status check_group(float* const* tab, int32_t size, int64_t rows, int64_t ld, int64_t cols,
                        const char* name) {
     if (size > ATP_MAX_GROUP)
-        return fail(ATP_ERR_UNSUPPORTED, "%s: group of %d exceeds %d", name, size,
+        return set_error(ATP_ERR_UNSUPPORTED, "%s: group of %d exceeds %d", name, size,
                     ATP_MAX_GROUP);
     if (size == 1) return ATP_OK;
-    if (!tab) return fail(ATP_ERR_INVALID_ARGUMENT, "%s: pointer table is NULL", name);
+    if (!tab) return set_error(ATP_ERR_INVALID_ARGUMENT, "%s: pointer table is NULL", name);
     for (int j = 0; j < size; ++j) {
         char nm[64];
         snprintf(nm, sizeof nm, "%s[%d]", name, j);
@@ -378,7 +385,7 @@ const char* atp_version(void) { return "atp-mi355x 0.1 (gfx950)"; }
 
 atp_status atp_shard_geometry(const atp_mesh* mesh, int32_t mode, int64_t k, int64_t n,
                               atp_shard* out) {
-    if (!out) return fail(ATP_ERR_INVALID_ARGUMENT, "out is NULL");
+    if (!out) return set_error(ATP_ERR_INVALID_ARGUMENT, "out is NULL");
     return geometry(mesh, mode, k, n, out);
 }
 
@@ -394,16 +401,16 @@ atp_status atp_shard_linear_fwd(const atp_mesh* mesh, int32_t mode, int64_t toke
     ATP_CHECK(check_mat(w_loc, g.k_loc, ldw, g.n_loc, "w_loc"));
     ATP_CHECK(check_mat(y, tokens, ldy, g.n_loc, "y"));
     if (!valid_epi(epi) || epi == ATP_EPI_GELU_BWD)
-        return fail(ATP_ERR_INVALID_ARGUMENT, "epilogue %d not valid for a forward GEMM", epi);
-    if (!valid_dtype(y_dtype)) return fail(ATP_ERR_INVALID_ARGUMENT, "y_dtype %d", y_dtype);
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "epilogue %d not valid for a forward GEMM", epi);
+    if (!valid_dtype(y_dtype)) return set_error(ATP_ERR_INVALID_ARGUMENT, "y_dtype %d", y_dtype);
     if (g.red_size > 1 && (epi != ATP_EPI_NONE || y_dtype != ATP_F32))
-        return fail(ATP_ERR_INVALID_ARGUMENT,
+        return set_error(ATP_ERR_INVALID_ARGUMENT,
                     "reduction group of %d: y is a Partial(SUM) block, it must be f32 with no "
                     "epilogue (bias and GeLU act after the reduction)", g.red_size);
     if (epi == ATP_EPI_BIAS || epi == ATP_EPI_BIAS_GELU) ATP_CHECK(check_vec(bias_loc, "bias"));
     if (preact) {
         if (epi != ATP_EPI_BIAS_GELU)
-            return fail(ATP_ERR_INVALID_ARGUMENT, "preact is only written by BIAS_GELU");
+            return set_error(ATP_ERR_INVALID_ARGUMENT, "preact is only written by BIAS_GELU");
         ATP_CHECK(check_mat(preact, tokens, ldy, g.n_loc, "preact"));
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -429,25 +436,25 @@ atp_status atp_chunked_partial_reduce(int32_t red_size, int64_t tokens, int64_t 
                                       const void* bias_loc, int32_t epi, const void* preact_in,
                                       void* out, int32_t out_dtype, int64_t ldo, void* preact_out,
                                       void* stream, void* const* chunk_ready) {
-    if (red_size < 1) return fail(ATP_ERR_INVALID_ARGUMENT, "red_size must be >= 1");
+    if (red_size < 1) return set_error(ATP_ERR_INVALID_ARGUMENT, "red_size must be >= 1");
     if (red_size > ATP_MAX_GROUP)
-        return fail(ATP_ERR_UNSUPPORTED, "red_size %d exceeds %d", red_size, ATP_MAX_GROUP);
-    if (n_loc <= 0) return fail(ATP_ERR_INVALID_ARGUMENT, "n_loc must be positive");
+        return set_error(ATP_ERR_UNSUPPORTED, "red_size %d exceeds %d", red_size, ATP_MAX_GROUP);
+    if (n_loc <= 0) return set_error(ATP_ERR_INVALID_ARGUMENT, "n_loc must be positive");
     ATP_CHECK(check_chunks(tokens, chunks));
-    if (!partials) return fail(ATP_ERR_INVALID_ARGUMENT, "partials is NULL");
+    if (!partials) return set_error(ATP_ERR_INVALID_ARGUMENT, "partials is NULL");
     for (int j = 0; j < red_size; ++j) {
         char nm[32];
         snprintf(nm, sizeof nm, "partials[%d]", j);
         ATP_CHECK(check_mat(partials[j], tokens, ldp, n_loc, nm));
     }
     ATP_CHECK(check_mat(out, tokens, ldo, n_loc, "out"));
-    if (!valid_epi(epi)) return fail(ATP_ERR_INVALID_ARGUMENT, "epilogue %d", epi);
-    if (!valid_dtype(out_dtype)) return fail(ATP_ERR_INVALID_ARGUMENT, "out_dtype %d", out_dtype);
+    if (!valid_epi(epi)) return set_error(ATP_ERR_INVALID_ARGUMENT, "epilogue %d", epi);
+    if (!valid_dtype(out_dtype)) return set_error(ATP_ERR_INVALID_ARGUMENT, "out_dtype %d", out_dtype);
     if (epi == ATP_EPI_BIAS || epi == ATP_EPI_BIAS_GELU) ATP_CHECK(check_vec(bias_loc, "bias"));
     if (epi == ATP_EPI_GELU_BWD) ATP_CHECK(check_mat(preact_in, tokens, ldo, n_loc, "preact_in"));
     if (preact_out) {
         if (epi != ATP_EPI_BIAS_GELU)
-            return fail(ATP_ERR_INVALID_ARGUMENT, "preact_out is only written by BIAS_GELU");
+            return set_error(ATP_ERR_INVALID_ARGUMENT, "preact_out is only written by BIAS_GELU");
         ATP_CHECK(check_mat(preact_out, tokens, ldo, n_loc, "preact_out"));
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -515,7 +522,7 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     ATP_CHECK(check_mesh(mesh));
     ATP_CHECK(block_plan(mesh, block_mode, h, &P));
     ATP_CHECK(check_chunks(tokens, chunks));
-    if (!w || !io) return fail(ATP_ERR_INVALID_ARGUMENT, "weights or io is NULL");
+    if (!w || !io) return set_error(ATP_ERR_INVALID_ARGUMENT, "weights or io is NULL");
     for (int i = 0; i < 4; ++i) {
         char nm[32];
         snprintf(nm, sizeof nm, "w[%s]", kLinearName[i]);
@@ -525,7 +532,7 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     }
     // inputs: x feeds qkv and fc1 (same k split), attn feeds out
     if (P.g[0].k_loc != P.g[2].k_loc)
-        return fail(ATP_ERR_SHAPE, "qkv and fc1 contract over different blocks of x");
+        return set_error(ATP_ERR_SHAPE, "qkv and fc1 contract over different blocks of x");
     ATP_CHECK(check_mat(io->x_loc, tokens, io->ldx, P.g[0].k_loc, "x_loc"));
     ATP_CHECK(check_mat(io->attn_loc, tokens, io->lda, P.g[1].k_loc, "attn_loc"));
     ATP_CHECK(check_mat(io->qkv, tokens, io->ld_qkv, P.g[0].n_loc, "qkv"));
@@ -534,7 +541,7 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     ATP_CHECK(check_mat(io->pre, tokens, io->ld_h, P.g[2].n_loc, "pre"));
     ATP_CHECK(check_mat(io->z, tokens, io->ld_z, P.g[3].n_loc, "z"));
     if (P.g[3].k_loc != P.g[2].n_loc)
-        return fail(ATP_ERR_SHAPE, "fc2 contracts over %lld columns, fc1 produces %lld",
+        return set_error(ATP_ERR_SHAPE, "fc2 contracts over %lld columns, fc1 produces %lld",
                     (long long)P.g[3].k_loc, (long long)P.g[2].n_loc);
     for (int i = 0; i < 4; ++i) {
         char nm[32];
@@ -636,7 +643,7 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     ATP_CHECK(check_mesh(mesh));
     ATP_CHECK(block_plan(mesh, block_mode, h, &P));
     ATP_CHECK(check_chunks(tokens, chunks));
-    if (!w || !io) return fail(ATP_ERR_INVALID_ARGUMENT, "weights or io is NULL");
+    if (!w || !io) return set_error(ATP_ERR_INVALID_ARGUMENT, "weights or io is NULL");
     for (int i = 0; i < 4; ++i) {
         char nm[32];
         snprintf(nm, sizeof nm, "w[%s]", kLinearName[i]);
@@ -660,7 +667,7 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     ATP_CHECK(check_mat(io->dx_fc1, tokens, io->ld_dx_fc1, P.g[2].k_loc, "dx_fc1"));
     ATP_CHECK(check_mat(io->d_attn, tokens, io->ld_d_attn, P.g[1].k_loc, "d_attn"));
     if (P.g[3].k_loc != P.g[2].n_loc)
-        return fail(ATP_ERR_SHAPE, "fc2 / fc1 block mismatch");
+        return set_error(ATP_ERR_SHAPE, "fc2 / fc1 block mismatch");
     for (int i = 0; i < 4; ++i) {
         char nm[32];
         snprintf(nm, sizeof nm, "dx_partials[%s]", kLinearName[i]);
