@@ -308,6 +308,24 @@ def main():
                     algorithmic_bytes_per_launch=dom["bytes"] / dom["launches"],
                     flops_per_launch=dom["flops"] / dom["launches"],
                     avg_launch_us=round(dom["total_ms"] / dom["launches"] * 1e3, 2))
+    if not args.serial:
+        # the same launches with nothing beside them: one more pass of the
+        # step with every launch serialized on the compute stream
+        solo = make_step(torch, atp, st, fwd_only, True, False)
+        atp.atp_profile_enable(True)
+        for _ in range(args.steps):
+            solo()
+        torch.cuda.synchronize()
+        atp.atp_profile_enable(False)
+        alone = [s for s in atp.atp_profile_collect(64) if s["name"] == dom["name"]]
+        if alone:
+            a = alone[0]
+            tf = a["flops"] / (a["total_ms"] * 1e-3) / 1e12
+            roofline["alone"] = dict(achieved=round(tf, 1), frac=round(tf / PEAK_BF16_TFLOPS, 4),
+                                     avg_launch_us=round(a["total_ms"] / a["launches"] * 1e3, 2))
+            roofline["note"] = ("achieved: launches of the pipelined step, which share the chip "
+                                "with the other compute lane and the reductions; alone: the same "
+                                "launches of a serialized pass of the step")
     red = [s for s in stats if s["name"] == "partial_reduce"]
     reduce_info = None
     if red:
