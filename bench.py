@@ -45,6 +45,8 @@ def parse():
     ap.add_argument("--fwd-only", action="store_true", help="time the forward only")
     ap.add_argument("--serial", action="store_true",
                     help="run reductions on the compute stream (no overlap)")
+    ap.add_argument("--no-workspace", action="store_true",
+                    help="no workspace: forward reads W directly (NN), dW reads X, dY (TN)")
     ap.add_argument("--no-aux", action="store_true",
                     help="no second compute stream (independent GEMMs do not share the chip)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -117,14 +119,14 @@ def make_step(torch, atp, st, fwd_only, serial, aux):
     def step():
         atp.atp_block_fwd(st["m"], st["bm"], st["T"], st["h"], st["chunks"], st["w"], st["b"],
                           st["x"], st["a"], st["fwd_tabs"], st["qkv"], st["o"], st["hh"],
-                          st["pre"], st["z"], compute_stream=cs, comm_stream=ms,
-                          aux_stream=ax)
+                          st["pre"], st["z"], workspace=st["ws"], compute_stream=cs,
+                          comm_stream=ms, aux_stream=ax)
         if fwd_only:
             return
         atp.atp_block_bwd(st["m"], st["bm"], st["T"], st["h"], st["chunks"], st["w"], st["b"],
                           st["x"], st["a"], st["hh"], st["pre"], st["dz"], st["dqkv"], st["do"],
                           st["bwd_tabs"], st["dh_pre"], st["dx_qkv"], st["dx_fc1"],
-                          st["d_attn"], st["dw"], st["db"], compute_stream=cs,
+                          st["d_attn"], st["dw"], st["db"], workspace=st["ws"], compute_stream=cs,
                           comm_stream=ms, aux_stream=ax)
     return step
 
@@ -250,6 +252,10 @@ def main():
     log(f"[bench] {atp.atp_version()} workload={args.workload} chunks={chunks} "
         f"pass={'fwd' if fwd_only else 'fwd+bwd'}")
     st = setup(torch, atp, S, wl, chunks, args.seed)
+    st["ws"] = None
+    if not args.no_workspace:
+        nb = atp.atp_block_workspace_bytes(st["m"], st["bm"], st["T"], st["h"], chunks)
+        st["ws"] = torch.empty(max(nb, 1), dtype=torch.uint8, device="cuda:0")
     torch.cuda.synchronize()
     step = make_step(torch, atp, st, fwd_only, args.serial, not args.no_aux)
     flops = step_flops(st, fwd_only)
@@ -295,7 +301,7 @@ def main():
                    avg_us=round(avg * 1e3, 2), ms_per_step=round(s["total_ms"] / args.steps, 4))
         if s["flops"] and s["name"].startswith("gemm"):
             ent["tflops"] = round(s["flops"] / (s["total_ms"] * 1e-3) / 1e12, 1)
-        if s["name"] in ("partial_reduce", "colsum"):
+        if s["name"] in ("partial_reduce", "colsum", "transpose"):
             ent["gbs"] = round(s["bytes"] / (s["total_ms"] * 1e-3) / 1e9, 1)
         kernels.append(ent)
     gemms = [s for s in stats if s["name"].startswith("gemm")]
@@ -379,6 +385,7 @@ def main():
                     tokens=wl["tokens"], h=wl["h"], chunks=chunks,
                     **{"pass": "fwd" if fwd_only else "fwd+bwd"},
                     serial=bool(args.serial), aux_stream=not args.no_aux,
+                    transposed_layout=not args.no_workspace,
                     gflop_per_step=round(flops / 1e9, 1)),
         step_ms=step_ms, mfma_util=round(value / PEAK_BF16_TFLOPS, 4),
         roofline=roofline, reduce=reduce_info, kernels=kernels, cpu_baseline=cpu)

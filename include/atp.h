@@ -218,9 +218,27 @@ typedef struct {
     float* db[4];
 } atp_block_bwd_io;
 
-/* Scratch the block calls need beyond the caller's buffers (bytes). */
+/* Workspace for the block calls' transposed-layout path (bytes): the larger
+ * of the forward's need (a transposed copy W^T of the four local weight
+ * shards, sum of k_loc * n_loc * 2 bytes) and the backward's (X^T of x, the
+ * attention block and H, and dY^T of the four linears, each tokens * cols *
+ * 2 bytes), every piece rounded up to 256 bytes.  Returns 0 for invalid
+ * arguments.  `chunks` does not change the size. */
 size_t atp_block_workspace_bytes(const atp_mesh* mesh, int32_t block_mode, int64_t tokens,
                                  int64_t h, int32_t chunks);
+
+/* Transpose a bf16 matrix: dst[c * ldd + r] = src[r * lds + c] for r < rows,
+ * c < cols.  A data-layout step for the products of Sec. 3.2 / 4.2 (it turns
+ * an operand contiguous along its M/N side into one contiguous along the
+ * contraction), not part of the paper's arithmetic.  src [rows][lds] and dst
+ * [cols][ldd] are 16-byte aligned with leading dimensions that are multiples
+ * of 8 (at most 2^22); rows and cols may be any size (with either 0 nothing
+ * is read or written and the pointers may be NULL); the buffers must not be
+ * the same.
+ * Errors: INVALID_ARGUMENT for negative sizes, NULL or aliased buffers,
+ * leading dimensions below the row length; UNSUPPORTED for alignment. */
+atp_status atp_transpose_bf16(int64_t rows, int64_t cols, const void* src, int64_t lds, void* dst,
+                              int64_t ldd, void* stream);
 
 /* One device's forward share of the layer (Sec. 3.2.1) with chunk-based
  * overlapping (Sec. 4.1).  Each linear's GEMM runs chunk by chunk; each
@@ -228,26 +246,35 @@ size_t atp_block_workspace_bytes(const atp_mesh* mesh, int32_t block_mode, int64
  * written; fc2's chunk c waits for fc1's reduced chunk c.  A group of one
  * needs no reduction: its bias (and GeLU) are applied in the GEMM epilogue
  * and it runs as one launch.
- * aux_stream (nullable) is a second compute stream: the attention
- * projections start on it while QKV and the MLP use compute_stream, and
- * consecutive chunks of a linear alternate between the two compute streams,
- * so independent GEMMs share the chip.  With aux_stream NULL all GEMMs run
- * on compute_stream; with comm_stream == compute_stream nothing overlaps.
- * Results do not depend on the streams used.  compute_stream's earlier work
+ * Issue order: fc1, out-proj, QKV, fc2.  aux_stream (nullable) is a second
+ * compute stream: each GEMM goes to whichever of compute_stream and
+ * aux_stream has less work issued so far (in FLOPs), with events for the
+ * data dependencies.  With aux_stream NULL all GEMMs run on compute_stream;
+ * with comm_stream == compute_stream nothing overlaps.
+ * workspace (nullable, 256-byte aligned): when ws_bytes is at least the
+ * forward's need (see atp_block_workspace_bytes) the call first writes W^T
+ * of each shard there and runs every product in the GEMM's NT layout;
+ * otherwise it reads W directly.  The results are bit-identical either way
+ * and do not depend on the streams used.  compute_stream's earlier work
  * happens before the block's, and on return compute_stream is ordered after
- * all of it. */
+ * all of it; the workspace may be reused once compute_stream reaches that
+ * point. */
 atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
                          int32_t chunks, const atp_block_weights* w,
                          const atp_block_fwd_io* io, void* workspace, size_t ws_bytes,
                          void* compute_stream, void* comm_stream, void* aux_stream);
 
-/* One device's backward share of the layer (Sec. 4.2): for each linear the
- * dX chunks come first and their reductions (comm_stream) overlap that
- * linear's dW GEMM and db; fc1's dY is fc2's reduced dX times GeLU'(pre).
- * The MLP chain (fc2, then fc1) runs on compute_stream and the attention
- * projections (out, qkv) on aux_stream when one is given; chunks alternate
- * between the two compute streams as in atp_block_fwd.  On return
- * compute_stream is ordered after all work. */
+/* One device's backward share of the layer (Sec. 4.2): dX = dY W^T per
+ * linear, chunked and reduced on comm_stream where its group has more than
+ * one member, dW = X^T dY and db = column sums of dY; fc1's dY is fc2's
+ * reduced dX times GeLU'(pre).  Issue order: fc2's dX (fc1 waits for it),
+ * QKV's and out-proj's dX, fc1's dX, then the four dW largest first, each
+ * GEMM on the less loaded of compute_stream and aux_stream (as in
+ * atp_block_fwd), so the dX reductions overlap the later GEMMs.
+ * workspace: when ws_bytes is at least the backward's need and tokens % 8
+ * == 0, X^T and dY^T are written there and every dW runs in the NT layout;
+ * otherwise dW reads X and dY directly.  Bit-identical either way.  On
+ * return compute_stream is ordered after all work. */
 atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
                          int32_t chunks, const atp_block_weights* w,
                          const atp_block_bwd_io* io, void* workspace, size_t ws_bytes,

@@ -125,7 +125,7 @@ EXPORTS = (
     "atp_shard_geometry", "atp_shard_linear_fwd", "atp_chunked_partial_reduce",
     "atp_shard_linear_bwd", "atp_block_workspace_bytes", "atp_block_fwd", "atp_block_bwd",
     "atp_profile_enable", "atp_profile_collect", "atp_status_string", "atp_last_error",
-    "atp_version", "atp_tcomm", "atp_hcm_mesh_cost", "atp_plan_mesh",
+    "atp_version", "atp_tcomm", "atp_hcm_mesh_cost", "atp_plan_mesh", "atp_transpose_bf16",
 )
 
 _lib = None
@@ -172,6 +172,8 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.atp_last_error.restype = ctypes.c_char_p
     lib.atp_version.argtypes = []
     lib.atp_version.restype = ctypes.c_char_p
+    lib.atp_transpose_bf16.argtypes = [i64, i64, _vp, i64, _vp, i64, _vp]
+    lib.atp_transpose_bf16.restype = i32
     hp, dp, cp = (ctypes.POINTER(atp_hcm_layer), ctypes.POINTER(atp_model_dims),
                   ctypes.POINTER(atp_mesh_cost))
     lib.atp_tcomm.argtypes = [dp, i32, i32, ctypes.c_double, ctypes.c_double,
@@ -477,6 +479,15 @@ def atp_profile_collect(max_records: int = 32):
     return [dict(name=arr[i].name.decode(), launches=arr[i].launches,
                  total_ms=arr[i].total_ms, flops=arr[i].flops, bytes=arr[i].bytes)
             for i in range(n)]
+
+
+def atp_transpose_bf16(src, dst, stream=None):
+    """dst[c, r] = src[r, c]; src [rows, cols] and dst [cols, rows] bf16 views."""
+    rows, cols = src.shape
+    sp, lds = _mat(src, rows, cols, torch.bfloat16, "src")
+    dp_, ldd = _mat(dst, cols, rows, torch.bfloat16, "dst")
+    _check(load_library().atp_transpose_bf16(int(rows), int(cols), sp, lds, dp_, ldd,
+                                             _stream(stream)))
 
 
 # ---------------------------------------------------------------------------

@@ -107,7 +107,10 @@ atp_status check_chunks(int64_t tokens, int32_t chunks) {
 }
 
 // A matrix with zero rows is never touched and may be NULL.
-atp_status check_mat(const void* p, int64_t rows, int64_t ld, int64_t cols, const char* name) {
+// `any_cols`: the column count need not be a multiple of 8 (the leading
+// dimension still must), for kernels that handle ragged rows element-wise.
+atp_status check_mat(const void* p, int64_t rows, int64_t ld, int64_t cols, const char* name,
+                     bool any_cols = false) {
     if (ld > (int64_t)1 << 22)
         return set_error(ATP_ERR_UNSUPPORTED, "%s: leading dimension %lld above 4M elements", name,
                     (long long)ld);
@@ -116,7 +119,7 @@ atp_status check_mat(const void* p, int64_t rows, int64_t ld, int64_t cols, cons
     if (ld < cols) return set_error(ATP_ERR_INVALID_ARGUMENT, "%s: ld %lld < %lld columns", name,
                                (long long)ld, (long long)cols);
     if (!aligned16(p)) return set_error(ATP_ERR_UNSUPPORTED, "%s is not 16-byte aligned", name);
-    if (ld % 8 != 0 || cols % 8 != 0)
+    if (ld % 8 != 0 || (!any_cols && cols % 8 != 0))
         return set_error(ATP_ERR_UNSUPPORTED, "%s: ld %lld and columns %lld must be multiples of 8",
                     name, (long long)ld, (long long)cols);
     return ATP_OK;
@@ -297,6 +300,43 @@ atp_status block_plan(const atp_mesh* m, int32_t bm, int64_t h, BlockPlan* p) {
                         "multiples of 8", (long long)p->g[i].k_loc, (long long)p->g[i].n_loc, i);
     }
     return ATP_OK;
+}
+
+// Workspace of the all-NT block path.  The forward keeps W^T of the four
+// linears ([n_loc][k_loc]); the backward keeps X^T of x (shared by QKV and
+// fc1), the attention block and H, and dY^T of the four linears, each
+// [cols][tokens].  Pieces are 256-byte aligned.
+constexpr size_t kWsAlign = 256;
+size_t ws_round(size_t b) { return (b + kWsAlign - 1) / kWsAlign * kWsAlign; }
+
+size_t ws_fwd_bytes(const BlockPlan& P) {
+    size_t b = 0;
+    for (int L = 0; L < 4; ++L) b += ws_round((size_t)P.g[L].n_loc * P.g[L].k_loc * 2);
+    return b;
+}
+
+size_t ws_bwd_bytes(const BlockPlan& P, int64_t tokens) {
+    const size_t t2 = (size_t)tokens * 2;
+    size_t b = ws_round(P.g[0].k_loc * t2) + ws_round(P.g[1].k_loc * t2) +
+               ws_round(P.g[3].k_loc * t2);
+    for (int L = 0; L < 4; ++L) b += ws_round(P.g[L].n_loc * t2);
+    return b;
+}
+
+// Carves consecutive aligned pieces out of the caller's workspace.
+struct Carver {
+    char* p;
+    uint16_t* take(size_t bytes) {
+        uint16_t* r = reinterpret_cast<uint16_t*>(p);
+        p += ws_round(bytes);
+        return r;
+    }
+};
+
+atp_status run_transpose(const void* src, int64_t lds, int64_t rows, int64_t cols, void* dst,
+                         int64_t ldd, hipStream_t s) {
+    return timed("transpose", 0.0, 4.0 * (double)rows * (double)cols, s,
+                 [&] { return atp::launch_transpose(src, lds, rows, cols, dst, ldd, s); });
 }
 
 atp_status check_group(float* const* tab, int32_t size, int64_t rows, int64_t ld, int64_t cols,
@@ -509,15 +549,29 @@ atp_status atp_shard_linear_bwd(const atp_mesh* mesh, int32_t mode, int64_t toke
 
 size_t atp_block_workspace_bytes(const atp_mesh* mesh, int32_t block_mode, int64_t tokens,
                                  int64_t h, int32_t chunks) {
-    (void)mesh; (void)block_mode; (void)tokens; (void)h; (void)chunks;
-    return 0;
+    (void)chunks;
+    BlockPlan P;
+    if (!mesh || check_mesh(mesh) != ATP_OK || block_plan(mesh, block_mode, h, &P) != ATP_OK ||
+        tokens < 0)
+        return 0;
+    return std::max(ws_fwd_bytes(P), ws_bwd_bytes(P, tokens));
+}
+
+atp_status atp_transpose_bf16(int64_t rows, int64_t cols, const void* src, int64_t lds, void* dst,
+                              int64_t ldd, void* stream) {
+    if (rows < 0 || cols < 0) return set_error(ATP_ERR_INVALID_ARGUMENT, "negative size");
+    if (rows == 0 || cols == 0) return ATP_OK;    // nothing is read or written
+    ATP_CHECK(check_mat(src, rows, lds, cols, "src", true));
+    ATP_CHECK(check_mat(dst, cols, ldd, rows, "dst", true));
+    if (src == dst)
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "src and dst must not be the same buffer");
+    return run_transpose(src, lds, rows, cols, dst, ldd, static_cast<hipStream_t>(stream));
 }
 
 atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
                          int32_t chunks, const atp_block_weights* w, const atp_block_fwd_io* io,
                          void* workspace, size_t ws_bytes, void* compute_stream,
                          void* comm_stream, void* aux_stream) {
-    (void)workspace; (void)ws_bytes;
     BlockPlan P;
     ATP_CHECK(check_mesh(mesh));
     ATP_CHECK(block_plan(mesh, block_mode, h, &P));
@@ -549,15 +603,55 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         ATP_CHECK(check_group(io->partials[i], P.g[i].red_size, tokens, io->ldp[i], P.g[i].n_loc, nm));
     }
 
+    // with a large enough workspace every product runs in the NT layout from
+    // a transposed weight copy (W^T is contiguous along k)
+    const bool nt = workspace && ws_bytes >= ws_fwd_bytes(P);
+    if (nt && reinterpret_cast<uintptr_t>(workspace) % kWsAlign)
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kWsAlign);
+
     Streams S(compute_stream, comm_stream, aux_stream);
     hipEvent_t* ev = nullptr;
     // [0] start  [1] comm end  [2] aux end  [3] fc1's single launch done,
-    // then per linear per chunk GEMM-done, then fc1 reduce-done per chunk
-    const size_t n_ev = 4 + 4 * (size_t)chunks + (size_t)chunks;
+    // then per linear per chunk GEMM-done, then fc1 reduce-done per chunk,
+    // then per linear its W^T done
+    const size_t n_ev = 4 + 4 * (size_t)chunks + (size_t)chunks + 4;
     ATP_CHECK(sync_events(n_ev, &ev));
     hipEvent_t* ev_gemm = ev + 4;
     hipEvent_t* ev_red1 = ev + 4 + 4 * chunks;
+    hipEvent_t* ev_wt = ev + 4 + 5 * chunks;
     ATP_CHECK(S.begin(ev[0]));
+
+    uint16_t* wt[4] = {nullptr, nullptr, nullptr, nullptr};
+    int wt_lane[4] = {-1, -1, -1, -1};
+    if (nt) {
+        Carver c{static_cast<char*>(workspace)};
+        for (int L = 0; L < 4; ++L) wt[L] = c.take((size_t)P.g[L].n_loc * P.g[L].k_loc * 2);
+    }
+    // W^T of linear L for a GEMM on `lane`: written once, on the lane of the
+    // linear's first GEMM; other lanes wait for it
+    auto need_wt = [&](int L, int lane) -> atp_status {
+        if (!nt) return ATP_OK;
+        const atp_shard& g = P.g[L];
+        if (wt_lane[L] < 0) {
+            ATP_CHECK(run_transpose(w->w[L], w->ldw[L], g.k_loc, g.n_loc, wt[L], g.k_loc,
+                                    S.lane(lane)));
+            HIP_CHECK(hipEventRecord(ev_wt[L], S.lane(lane)), "hipEventRecord");
+            wt_lane[L] = lane;
+        } else if (wt_lane[L] != lane) {
+            HIP_CHECK(hipStreamWaitEvent(S.lane(lane), ev_wt[L], 0), "hipStreamWaitEvent");
+        }
+        return ATP_OK;
+    };
+    // the product X W of linear L: NN from W, or NT from W^T
+    auto fwd_problem = [&](int L, const void* A, int64_t lda, void* C, int64_t ldc, bool b16,
+                           int epi, int64_t M) {
+        const atp_shard& g = P.g[L];
+        if (nt)
+            return gemm_problem(atp::LAYOUT_NT, A, lda, wt[L], g.k_loc, C, ldc, b16, epi, M,
+                                g.n_loc, g.k_loc);
+        return gemm_problem(atp::LAYOUT_NN, A, lda, w->w[L], w->ldw[L], C, ldc, b16, epi, M,
+                            g.n_loc, g.k_loc);
+    };
 
     const int64_t mc = tokens / chunks;
     const void* A_in[4] = {io->x_loc, io->attn_loc, io->x_loc, io->h};
@@ -581,10 +675,9 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         const int lane = S.take(gemm_flops(tokens, g.n_loc, g.k_loc));
         hipStream_t s = S.lane(lane);
         if (L == 3) ATP_CHECK(wait_h(lane, chunks - 1));
-        atp::GemmProblem p = gemm_problem(atp::LAYOUT_NN, A_in[L], lda_in[L], w->w[L], w->ldw[L],
-                                          outp[L], ldo[L], true,
-                                          L == 2 ? atp::EPI_BIAS_GELU : atp::EPI_BIAS, tokens,
-                                          g.n_loc, g.k_loc);
+        ATP_CHECK(need_wt(L, lane));
+        atp::GemmProblem p = fwd_problem(L, A_in[L], lda_in[L], outp[L], ldo[L], true,
+                                         L == 2 ? atp::EPI_BIAS_GELU : atp::EPI_BIAS, tokens);
         p.bias = w->b[L];
         p.pre_out = (L == 2) ? io->pre : nullptr;
         ATP_CHECK(run_gemm(p, s));
@@ -602,11 +695,11 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         hipStream_t s = S.lane(lane);
         const int64_t r0 = (int64_t)c * mc;
         if (L == 3) ATP_CHECK(wait_h(lane, c));
+        ATP_CHECK(need_wt(L, lane));
         float* own = io->partials[L][g.red_index];
-        atp::GemmProblem p = gemm_problem(
-            atp::LAYOUT_NN, static_cast<const uint16_t*>(A_in[L]) + r0 * lda_in[L], lda_in[L],
-            w->w[L], w->ldw[L], own + r0 * io->ldp[L], io->ldp[L], false, atp::EPI_NONE, mc,
-            g.n_loc, g.k_loc);
+        atp::GemmProblem p = fwd_problem(L, static_cast<const uint16_t*>(A_in[L]) + r0 * lda_in[L],
+                                         lda_in[L], own + r0 * io->ldp[L], io->ldp[L], false,
+                                         atp::EPI_NONE, mc);
         ATP_CHECK(run_gemm(p, s));
         hipEvent_t e = ev_gemm[L * chunks + c];
         HIP_CHECK(hipEventRecord(e, s), "hipEventRecord");
@@ -638,7 +731,6 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
                          int32_t chunks, const atp_block_weights* w, const atp_block_bwd_io* io,
                          void* workspace, size_t ws_bytes, void* compute_stream,
                          void* comm_stream, void* aux_stream) {
-    (void)workspace; (void)ws_bytes;
     BlockPlan P;
     ATP_CHECK(check_mesh(mesh));
     ATP_CHECK(block_plan(mesh, block_mode, h, &P));
@@ -675,15 +767,37 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
                               nm));
     }
 
+    // with a large enough workspace (and whole 16-byte rows of tokens) dW runs
+    // in the NT layout from X^T and dY^T (both contiguous along the tokens)
+    const bool nt = workspace && ws_bytes >= ws_bwd_bytes(P, tokens) && tokens % 8 == 0;
+    if (nt && reinterpret_cast<uintptr_t>(workspace) % kWsAlign)
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kWsAlign);
+
     Streams S(compute_stream, comm_stream, aux_stream);
     hipEvent_t* ev = nullptr;
     // [0] start  [1] comm end  [2] aux end  [3] fc2's single dX launch done,
-    // then per linear per chunk GEMM-done, then fc2 reduce-done per chunk
-    const size_t n_ev = 4 + 4 * (size_t)chunks + (size_t)chunks;
+    // then per linear per chunk GEMM-done, then fc2 reduce-done per chunk,
+    // then X^T done for x, the attention block and H
+    const size_t n_ev = 4 + 4 * (size_t)chunks + (size_t)chunks + 3;
     ATP_CHECK(sync_events(n_ev, &ev));
     hipEvent_t* ev_gemm = ev + 4;
     hipEvent_t* ev_red2 = ev + 4 + 4 * chunks;
+    hipEvent_t* ev_xt = ev + 4 + 5 * chunks;
     ATP_CHECK(S.begin(ev[0]));
+
+    // X^T pieces: 0 = x (QKV and fc1), 1 = attention block (out), 2 = H (fc2)
+    const int xsrc[4] = {0, 1, 0, 2};
+    uint16_t* xt[3] = {nullptr, nullptr, nullptr};
+    uint16_t* dyt[4] = {nullptr, nullptr, nullptr, nullptr};
+    int xt_lane[3] = {-1, -1, -1};
+    if (nt) {
+        Carver c{static_cast<char*>(workspace)};
+        const size_t t2 = (size_t)tokens * 2;
+        xt[0] = c.take(P.g[0].k_loc * t2);
+        xt[1] = c.take(P.g[1].k_loc * t2);
+        xt[2] = c.take(P.g[3].k_loc * t2);
+        for (int L = 0; L < 4; ++L) dyt[L] = c.take(P.g[L].n_loc * t2);
+    }
 
     const int64_t mc = tokens / chunks;
     const void* Xin[4] = {io->x_loc, io->attn_loc, io->x_loc, io->h};
@@ -758,7 +872,24 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         hipStream_t s = S.lane(lane);
         if (L == 2) ATP_CHECK(wait_dpre(lane, chunks - 1));
         if (io->db[L]) ATP_CHECK(run_colsum(dY[L], ld_dy[L], tokens, g.n_loc, io->db[L], s));
-        atp::GemmProblem p = gemm_problem(atp::LAYOUT_TN, Xin[L], ldx_in[L], dY[L], ld_dy[L],
+        if (!nt) {
+            atp::GemmProblem p = gemm_problem(atp::LAYOUT_TN, Xin[L], ldx_in[L], dY[L], ld_dy[L],
+                                              io->dw[L], w->ldw[L], false, atp::EPI_NONE,
+                                              g.k_loc, g.n_loc, tokens);
+            return run_gemm(p, s);
+        }
+        // X^T once per source (x serves QKV and fc1, maybe on two lanes), dY^T
+        // on this lane, then dW = X^T dY as an NT product over the tokens
+        const int xi = xsrc[L];
+        if (xt_lane[xi] < 0) {
+            ATP_CHECK(run_transpose(Xin[L], ldx_in[L], tokens, g.k_loc, xt[xi], tokens, s));
+            HIP_CHECK(hipEventRecord(ev_xt[xi], s), "hipEventRecord");
+            xt_lane[xi] = lane;
+        } else if (xt_lane[xi] != lane) {
+            HIP_CHECK(hipStreamWaitEvent(s, ev_xt[xi], 0), "hipStreamWaitEvent");
+        }
+        ATP_CHECK(run_transpose(dY[L], ld_dy[L], tokens, g.n_loc, dyt[L], tokens, s));
+        atp::GemmProblem p = gemm_problem(atp::LAYOUT_NT, xt[xi], tokens, dyt[L], tokens,
                                           io->dw[L], w->ldw[L], false, atp::EPI_NONE, g.k_loc,
                                           g.n_loc, tokens);
         return run_gemm(p, s);

@@ -453,7 +453,8 @@ bool gemm_supported(int layout, int epi, bool out_bf16) {
     case LAYOUT_NN:
         return epi == EPI_NONE || epi == EPI_BIAS || epi == EPI_BIAS_GELU;
     case LAYOUT_NT:
-        return epi == EPI_NONE || (epi == EPI_GELU_BWD && out_bf16);
+        return epi == EPI_NONE ||
+               (out_bf16 && (epi == EPI_GELU_BWD || epi == EPI_BIAS || epi == EPI_BIAS_GELU));
     case LAYOUT_TN:
         return epi == EPI_NONE && !out_bf16;
     default:
@@ -497,6 +498,9 @@ hipError_t launch_gemm(const GemmProblem& p, hipStream_t s) {
             return b16 ? launch_t<true, true, EPI_NONE, true>(p, s)
                        : launch_t<true, true, EPI_NONE, false>(p, s);
         if (p.epi == EPI_GELU_BWD && b16) return launch_t<true, true, EPI_GELU_BWD, true>(p, s);
+        // the forward with a transposed weight copy (B = W^T, contiguous along k)
+        if (p.epi == EPI_BIAS && b16) return launch_t<true, true, EPI_BIAS, true>(p, s);
+        if (p.epi == EPI_BIAS_GELU && b16) return launch_t<true, true, EPI_BIAS_GELU, true>(p, s);
         return hipErrorInvalidValue;
     case LAYOUT_TN:
         if (p.epi == EPI_NONE && !b16) return launch_t<false, false, EPI_NONE, false>(p, s);

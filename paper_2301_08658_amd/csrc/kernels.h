@@ -53,4 +53,8 @@ hipError_t launch_reduce(const ReduceProblem& p, hipStream_t s);
 hipError_t launch_colsum(const void* dy, int64_t ld, int64_t T, int64_t N, float* db,
                          hipStream_t s);
 
+// dst[c*ldd + r] = src[r*lds + c] for r < rows, c < cols (bf16).
+hipError_t launch_transpose(const void* src, int64_t lds, int64_t rows, int64_t cols, void* dst,
+                            int64_t ldd, hipStream_t s);
+
 }  // namespace atp

@@ -1,0 +1,85 @@
+// bf16 matrix transpose through LDS (HBM-bound).
+//
+// Turns an operand that is contiguous along its M/N side into one contiguous
+// along the contraction, so that every product of a shard linear (Sec. 3.2
+// forward, Sec. 4.2 backward) can run in the GEMM's NT layout: W -> W^T for
+// the forward, X -> X^T and dY -> dY^T for dW = X^T dY.
+//
+// One workgroup moves a 64 x 64 tile: 16-byte loads along the source rows,
+// a transposed write into LDS, 16-byte stores along the destination rows.
+// Partial tiles at the edges go element by element.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kernels.h"
+
+namespace atp {
+namespace {
+
+constexpr int TILE = 64;
+constexpr int PAD = 8;                 // LDS row pitch 72 elements (144 B)
+constexpr int THREADS = 256;
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(THREADS) void transpose_kernel(const uint16_t* __restrict__ src,
+                                                            int64_t lds, int64_t rows,
+                                                            int64_t cols, uint16_t* __restrict__ dst,
+                                                            int64_t ldd, int tiles_c) {
+    __shared__ __attribute__((aligned(16))) uint16_t tile[TILE][TILE + PAD];
+    const int tid = threadIdx.x;
+    const int64_t r0 = (int64_t)(blockIdx.x / tiles_c) * TILE;
+    const int64_t c0 = (int64_t)(blockIdx.x % tiles_c) * TILE;
+    // load: 64 rows x 8 chunks of 8 elements; tile[c][r] = src[r0 + r][c0 + c]
+#pragma unroll
+    for (int j = 0; j < TILE * TILE / 8 / THREADS; ++j) {
+        const int q = tid + j * THREADS;
+        const int r = q >> 3, c = (q & 7) * 8;
+        const int64_t gr = r0 + r, gc = c0 + c;
+        uint16_t v[8];
+        if (gr < rows && gc + 8 <= cols) {
+            const u32x4 w = *reinterpret_cast<const u32x4*>(src + gr * lds + gc);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                v[2 * e] = (uint16_t)(w[e] & 0xffffu);
+                v[2 * e + 1] = (uint16_t)(w[e] >> 16);
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                v[e] = (gr < rows && gc + e < cols) ? src[gr * lds + gc + e] : (uint16_t)0;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) tile[c + e][r] = v[e];
+    }
+    __syncthreads();
+    // store: dst[c0 + c][r0 + r .. +8] = tile[c][r .. r+8]
+#pragma unroll
+    for (int j = 0; j < TILE * TILE / 8 / THREADS; ++j) {
+        const int q = tid + j * THREADS;
+        const int c = q >> 3, r = (q & 7) * 8;
+        const int64_t gc = c0 + c, gr = r0 + r;
+        if (gc >= cols) continue;
+        if (gr + 8 <= rows) {
+            *reinterpret_cast<u32x4*>(dst + gc * ldd + gr) =
+                *reinterpret_cast<const u32x4*>(&tile[c][r]);
+        } else {
+            for (int e = 0; e < 8 && gr + e < rows; ++e) dst[gc * ldd + gr + e] = tile[c][r + e];
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_transpose(const void* src, int64_t lds, int64_t rows, int64_t cols, void* dst,
+                            int64_t ldd, hipStream_t s) {
+    if (rows <= 0 || cols <= 0) return hipSuccess;
+    const int64_t tr = (rows + TILE - 1) / TILE, tc = (cols + TILE - 1) / TILE;
+    if (tr * tc > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(transpose_kernel, dim3((unsigned)(tr * tc)), dim3(THREADS), 0, s,
+                       static_cast<const uint16_t*>(src), lds, rows, cols,
+                       static_cast<uint16_t*>(dst), ldd, (int)tc);
+    return hipGetLastError();
+}
+
+}  // namespace atp

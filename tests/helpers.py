@@ -117,9 +117,18 @@ def group_table(own, peers, index):
     return list(peers[:index]) + [own] + list(peers[index:])
 
 
-def run_block_fwd(inp, chunks, compute=None, comm=None, same_stream=False, aux=True):
+def block_workspace(inp):
+    """A workspace large enough for the block's transposed-layout path."""
+    n = atp.atp_block_workspace_bytes(inp["m"], block_mode_code(inp["mode"]), inp["T"], inp["h"],
+                                      1)
+    return torch.empty(max(n, 1), dtype=torch.uint8, device=inp["x"].device)
+
+
+def run_block_fwd(inp, chunks, compute=None, comm=None, same_stream=False, aux=True,
+                  workspace=False):
     """Allocate outputs, call atp_block_fwd, return outputs + own partials.
-    aux=True also gives the block a second compute stream."""
+    aux=True also gives the block a second compute stream; workspace=True
+    hands it a workspace, so it runs the transposed-layout path."""
     T, G, m = inp["T"], inp["G"], inp["m"]
     dev_ = inp["x"].device
     own = [torch.full((T, g.n_loc), float("nan"), device=dev_) if g.red_size > 1 else None
@@ -136,12 +145,14 @@ def run_block_fwd(inp, chunks, compute=None, comm=None, same_stream=False, aux=T
     ax = torch.cuda.Stream() if (aux and not same_stream) else None
     atp.atp_block_fwd(m, block_mode_code(inp["mode"]), T, inp["h"], chunks, inp["w"], inp["b"],
                       inp["x"], inp["a"], tabs, out["qkv"], out["o"], out["h"], out["pre"],
-                      out["z"], compute_stream=cs, comm_stream=ms, aux_stream=ax)
+                      out["z"], workspace=block_workspace(inp) if workspace else None,
+                      compute_stream=cs, comm_stream=ms, aux_stream=ax)
     out["own"] = own
     return out
 
 
-def run_block_bwd(inp, chunks, h_act=None, pre=None, same_stream=False, aux=True):
+def run_block_bwd(inp, chunks, h_act=None, pre=None, same_stream=False, aux=True,
+                  workspace=False):
     T, G, m = inp["T"], inp["G"], inp["m"]
     dev_ = inp["x"].device
     h_act = inp["hs"] if h_act is None else h_act
@@ -162,7 +173,8 @@ def run_block_bwd(inp, chunks, h_act=None, pre=None, same_stream=False, aux=True
     atp.atp_block_bwd(m, block_mode_code(inp["mode"]), T, inp["h"], chunks, inp["w"], inp["b"],
                       inp["x"], inp["a"], h_act, pre, inp["dz"], inp["dqkv"], inp["do"], tabs,
                       out["dh_pre"], out["dx_qkv"], out["dx_fc1"], out["d_attn"], out["dw"],
-                      out["db"], compute_stream=cs, comm_stream=ms, aux_stream=ax)
+                      out["db"], workspace=block_workspace(inp) if workspace else None,
+                      compute_stream=cs, comm_stream=ms, aux_stream=ax)
     out["own"] = own
     return out
 

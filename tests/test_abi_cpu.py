@@ -195,10 +195,28 @@ def test_block_validation():
     W.b[2] = FAKE
     io.ld_h = G[2].n_loc - 8
     assert call() == B.ATP_ERR_INVALID_ARGUMENT
-    assert lib.atp_block_workspace_bytes(ctypes.byref(m), 0, T, h, 2) == 0
+    assert lib.atp_block_workspace_bytes(ctypes.byref(m), 0, T, h, 2) > 0
 
 
 def test_status_strings():
     assert atp.binding.status_string(0) == "ATP_OK"
     assert atp.binding.status_string(2) == "ATP_ERR_SHAPE"
     assert atp.binding.status_string(99) == "ATP_ERR_UNKNOWN"
+
+
+def test_block_workspace_bytes_formula():
+    # forward: W^T of the four shards; backward: X^T of x, attention block, H
+    # and dY^T of the four linears over the tokens; pieces rounded to 256 B
+    r = lambda b: (b + 255) // 256 * 256  # noqa: E731
+    for (d1, d2), mode, T, h in [((8, 1), 0, 4096, 20480), ((2, 4), 1, 8192, 4096),
+                                 ((2, 2), 0, 132, 512), ((1, 1), 0, 0, 256)]:
+        m = B.mesh(d1, d2, 0, 0)
+        G = B.block_geometry(m, mode, h)
+        fwd = sum(r(g.k_loc * g.n_loc * 2) for g in G)
+        bwd = (r(G[0].k_loc * T * 2) + r(G[1].k_loc * T * 2) + r(G[3].k_loc * T * 2) +
+               sum(r(g.n_loc * T * 2) for g in G))
+        for chunks in (1, 2, 4):
+            assert B.atp_block_workspace_bytes(m, mode, T, h, chunks) == max(fwd, bwd)
+    # invalid arguments give 0
+    assert B.atp_block_workspace_bytes(B.mesh(2, 2, 0, 0), 7, 128, 512, 1) == 0
+    assert B.atp_block_workspace_bytes(B.mesh(2, 2, 0, 0), 0, 128, 500, 1) == 0

@@ -34,15 +34,16 @@ def _cols(n_loc, n=4, seed=1):
     return sorted(set([0, n_loc - 1] + rng.choice(n_loc, size=n, replace=False).tolist()))
 
 
+@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "transposed"])
 @pytest.mark.parametrize("name", BIG)
-def test_workload_forward_sampled_rows(name):
+def test_workload_forward_sampled_rows(name, workspace):
     w = S.WORKLOADS[name]
     d1, d2 = w["mesh"]
     coord = (d1 - 1, d2 - 1)
     inp = make_block_inputs(w["mode"], w["mesh"], coord, w["tokens"], w["h"], w["sigma_w"],
                             seed=11, on_device=True)
-    print(f"[{name}] forward, coord {coord}", flush=True)
-    out = run_block_fwd(inp, w["chunks"])
+    print(f"[{name}] forward, coord {coord}, workspace {workspace}", flush=True)
+    out = run_block_fwd(inp, w["chunks"], workspace=workspace)
     torch.cuda.synchronize()
     rows = _rows(w["tokens"], w["chunks"])
     ref = oracle_block_fwd(O, inp, rows)
@@ -91,15 +92,16 @@ def _oracle_bwd_sampled(inp, rows, cols):
     return r
 
 
+@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "transposed"])
 @pytest.mark.parametrize("name", [k for k in BIG if S.WORKLOADS[k]["bwd"]])
-def test_workload_backward_sampled(name):
+def test_workload_backward_sampled(name, workspace):
     w = S.WORKLOADS[name]
     d1, d2 = w["mesh"]
     coord = (0, d2 - 1)
     inp = make_block_inputs(w["mode"], w["mesh"], coord, w["tokens"], w["h"], w["sigma_w"],
                             seed=12, on_device=True, bwd=True)
-    print(f"[{name}] backward, coord {coord}", flush=True)
-    out = run_block_bwd(inp, w["chunks"])
+    print(f"[{name}] backward, coord {coord}, workspace {workspace}", flush=True)
+    out = run_block_bwd(inp, w["chunks"], workspace=workspace)
     torch.cuda.synchronize()
     rows = _rows(w["tokens"], w["chunks"], n=6)
     cols = [_cols(g.n_loc, n=3, seed=i) for i, g in enumerate(inp["G"])]
