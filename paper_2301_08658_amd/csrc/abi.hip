@@ -366,18 +366,21 @@ const char* const kLinearName[4] = {"qkv", "out", "fc1", "fc2"};
 struct Streams {
     hipStream_t cs, ms, ax;
     bool two;
+    bool gemm_one_lane = false;   // every kernel of the block on cs (ax unused)
     double load[2] = {0.0, 0.0};
     Streams(void* c, void* m, void* a)
         : cs(static_cast<hipStream_t>(c)), ms(static_cast<hipStream_t>(m)),
           ax(a ? static_cast<hipStream_t>(a) : static_cast<hipStream_t>(c)),
           two(a != nullptr && a != c) {}
     hipStream_t lane(int i) const { return i ? ax : cs; }
-    // the less loaded lane (ties go to cs), charged with `flops`
+    // the lane of the next GEMM: cs when GEMMs keep to one lane, else the
+    // less loaded lane (ties go to cs), charged with `flops`
     int take(double flops) {
-        const int i = (two && load[1] < load[0]) ? 1 : 0;
+        const int i = (!gemm_one_lane && two && load[1] < load[0]) ? 1 : 0;
         load[i] += flops;
         return i;
     }
+
     // everything already queued on cs happens before the block's work
     atp_status begin(hipEvent_t start) const {
         HIP_CHECK(hipEventRecord(start, cs), "hipEventRecord");
@@ -610,6 +613,12 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         return set_error(ATP_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kWsAlign);
 
     Streams S(compute_stream, comm_stream, aux_stream);
+    // The NT kernel's tiles fill the chip by themselves (a 512-row chunk is
+    // exactly one tile per CU), so any kernel beside one delays its last
+    // tiles (measured: a second GEMM lane, or transposes on the auxiliary
+    // lane, make the step 3-6% slower): on this path every GEMM and every
+    // transpose runs on the compute lane and the auxiliary stream is unused.
+    S.gemm_one_lane = nt;
     hipEvent_t* ev = nullptr;
     // [0] start  [1] comm end  [2] aux end  [3] fc1's single launch done,
     // then per linear per chunk GEMM-done, then fc1 reduce-done per chunk,
@@ -717,6 +726,14 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         for (int c = 0; c < chunks; ++c) ATP_CHECK(chunk(L, c));
         return ATP_OK;
     };
+    if (S.gemm_one_lane) {
+        // one lane: out-proj first (its weight is the smallest to transpose
+        // and its reductions start at once), then fc1, QKV, and fc2 behind
+        // fc1's output
+        const int order[4] = {1, 2, 0, 3};
+        for (int L : order) ATP_CHECK(linear(L));
+        return S.end(ev[1], ev[2]);
+    }
     // fc1 first, since fc2 waits for it; the attention projections fill the
     // other lane meanwhile (out first, so its reductions start early); fc2
     // last, chunk by chunk behind fc1's output
@@ -774,6 +791,7 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         return set_error(ATP_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kWsAlign);
 
     Streams S(compute_stream, comm_stream, aux_stream);
+    S.gemm_one_lane = nt;     // as in the forward: one lane on this path
     hipEvent_t* ev = nullptr;
     // [0] start  [1] comm end  [2] aux end  [3] fc2's single dX launch done,
     // then per linear per chunk GEMM-done, then fc2 reduce-done per chunk,

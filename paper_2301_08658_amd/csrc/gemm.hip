@@ -1,9 +1,16 @@
-// bf16 x bf16 -> fp32 MFMA GEMM for gfx950 (CDNA4) with fused epilogues.
+// bf16 x bf16 -> fp32 MFMA GEMMs for gfx950 (CDNA4) with fused epilogues.
 //
-// One kernel template serves the three products of a shard linear
-// (Sec. 3.2 forward Y = X W; Sec. 4.2 backward dX = dY W^T, dW = X^T dY).
+// Two kernels serve the three products of a shard linear (Sec. 3.2 forward
+// Y = X W; Sec. 4.2 backward dX = dY W^T, dW = X^T dY):
 //
-// Data path
+//   * gemm_nt_kernel: both operands contiguous along k (C = A B^T).  Every
+//     product of the block runs in this layout when a workspace holds the
+//     transposed copies, so it is the tuned kernel (described below, after
+//     the generic one).
+//   * gemm_kernel: the generic template, any of NN / NT / TN, used for the
+//     forward (NN) and dW (TN) products without a workspace.
+//
+// Generic kernel data path
 //   * Operands go global -> LDS with buffer_load_dwordx4 ... lds (no
 //     register staging).  A buffer resource per operand gives zero fill for
 //     every out-of-range lane (its offset is pushed past num_records), so
@@ -255,6 +262,47 @@ __device__ __forceinline__ void wait_vmcnt() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// Epilogue of four consecutive outputs C[m][n..n+3] (fp32 accumulators):
+// bias, bias + GeLU (optionally saving the bf16 pre-activation), GeLU'
+// (multiplying by the derivative at a saved pre-activation), then an fp32 or
+// bf16 (round to nearest even) store.
+template <int EPI, bool OUT_BF16>
+__device__ __forceinline__ void epilogue_store(const KArgs& a, int64_t m, int64_t n, float* v) {
+    if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_GELU) {
+        const u32x2 bb = *reinterpret_cast<const u32x2*>(a.bias + n);
+        v[0] += bf16_to_f32(bb[0] & 0xffffu);
+        v[1] += bf16_to_f32(bb[0] >> 16);
+        v[2] += bf16_to_f32(bb[1] & 0xffffu);
+        v[3] += bf16_to_f32(bb[1] >> 16);
+    }
+    if constexpr (EPI == EPI_BIAS_GELU) {
+        if (a.pre_out) {
+            u32x2 pp;
+            pp[0] = f32_to_bf16_rne(v[0]) | (f32_to_bf16_rne(v[1]) << 16);
+            pp[1] = f32_to_bf16_rne(v[2]) | (f32_to_bf16_rne(v[3]) << 16);
+            *reinterpret_cast<u32x2*>(a.pre_out + m * a.ldc + n) = pp;
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = gelu_f(v[r]);
+    }
+    if constexpr (EPI == EPI_GELU_BWD) {
+        const u32x2 pp = *reinterpret_cast<const u32x2*>(a.pre_in + m * a.ldc + n);
+        v[0] *= gelu_grad_f(bf16_to_f32(pp[0] & 0xffffu));
+        v[1] *= gelu_grad_f(bf16_to_f32(pp[0] >> 16));
+        v[2] *= gelu_grad_f(bf16_to_f32(pp[1] & 0xffffu));
+        v[3] *= gelu_grad_f(bf16_to_f32(pp[1] >> 16));
+    }
+    if constexpr (OUT_BF16) {
+        u32x2 o;
+        o[0] = f32_to_bf16_rne(v[0]) | (f32_to_bf16_rne(v[1]) << 16);
+        o[1] = f32_to_bf16_rne(v[2]) | (f32_to_bf16_rne(v[3]) << 16);
+        *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(a.C) + m * a.ldc + n) = o;
+    } else {
+        *reinterpret_cast<f32x4*>(static_cast<float*>(a.C) + m * a.ldc + n) =
+            f32x4{v[0], v[1], v[2], v[3]};
+    }
+}
+
 template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, bool A_K, bool B_K, int EPI,
           bool OUT_BF16>
 __global__ __launch_bounds__(WGM* WGN * 64, 1) void gemm_kernel(KArgs a) {
@@ -379,40 +427,212 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1) void gemm_kernel(KArgs a) {
                 float v[4];
 #pragma unroll
                 for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * g + r];
-                if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_GELU) {
-                    const u32x2 bb = *reinterpret_cast<const u32x2*>(a.bias + n);
-                    v[0] += bf16_to_f32(bb[0] & 0xffffu);
-                    v[1] += bf16_to_f32(bb[0] >> 16);
-                    v[2] += bf16_to_f32(bb[1] & 0xffffu);
-                    v[3] += bf16_to_f32(bb[1] >> 16);
-                }
-                if constexpr (EPI == EPI_BIAS_GELU) {
-                    if (a.pre_out) {
-                        u32x2 pp;
-                        pp[0] = f32_to_bf16_rne(v[0]) | (f32_to_bf16_rne(v[1]) << 16);
-                        pp[1] = f32_to_bf16_rne(v[2]) | (f32_to_bf16_rne(v[3]) << 16);
-                        *reinterpret_cast<u32x2*>(a.pre_out + m * a.ldc + n) = pp;
-                    }
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) v[r] = gelu_f(v[r]);
-                }
-                if constexpr (EPI == EPI_GELU_BWD) {
-                    const u32x2 pp = *reinterpret_cast<const u32x2*>(a.pre_in + m * a.ldc + n);
-                    v[0] *= gelu_grad_f(bf16_to_f32(pp[0] & 0xffffu));
-                    v[1] *= gelu_grad_f(bf16_to_f32(pp[0] >> 16));
-                    v[2] *= gelu_grad_f(bf16_to_f32(pp[1] & 0xffffu));
-                    v[3] *= gelu_grad_f(bf16_to_f32(pp[1] >> 16));
-                }
-                if constexpr (OUT_BF16) {
-                    u32x2 o;
-                    o[0] = f32_to_bf16_rne(v[0]) | (f32_to_bf16_rne(v[1]) << 16);
-                    o[1] = f32_to_bf16_rne(v[2]) | (f32_to_bf16_rne(v[3]) << 16);
-                    *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(a.C) + m * a.ldc + n) = o;
-                } else {
-                    *reinterpret_cast<f32x4*>(static_cast<float*>(a.C) + m * a.ldc + n) =
-                        f32x4{v[0], v[1], v[2], v[3]};
-                }
+                epilogue_store<EPI, OUT_BF16>(a, m, n, v);
             }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// NT kernel: C[M,N] = A[M,K] B[N,K]^T, 256 x 160 tiles, eight waves in two
+// groups that take turns on the matrix cores ("ping-pong").
+//
+//   * Tile 256 x 160 x 64: three LDS stages of (256 + 160) x 64 bf16 fill
+//     156 KB of the 160 KB, so the copy of step p+2 is issued while step p is
+//     multiplied.  160 divides every N of the block's products at the
+//     benchmark sizes (and a 512-row token chunk is exactly 256 tiles), so
+//     no launch ends on a partial wave of tiles.
+//   * Waves 0-3 (group A) and 4-7 (group B) share the four SIMDs pairwise.
+//     A K step is two phases separated by workgroup barriers: a memory phase
+//     (issue this wave's share of the direct-to-LDS copy of step p+2, read all
+//     of step p's MFMA fragments into registers) and a compute phase (the 40
+//     MFMAs of step p).  Group B starts one phase late, so on every SIMD one
+//     wave multiplies while the other one loads: the matrix core is fed from
+//     registers while the other wave's LDS reads and copy issue overlap it.
+//   * Each wave owns a 64 x 80 block of C as 4 x 5 tiles of
+//     v_mfma_f32_16x16x32_bf16.  A fragment is one ds_read_b128 (row r,
+//     8 consecutive k).  gfx950 serves a ds_read_b128 in lane groups
+//     {0-7, 24-31}, {8-15, 16-23} (and the same +32); the chunk swizzle
+//     s(r) = r & 6 gives the 16 lanes of each group distinct bank quads
+//     (measured: zero LDS bank conflicts).
+//   * The swizzle of a row depends only on the row's index within its copy
+//     instruction, so one byte offset per lane serves every copy; rows past
+//     the operand's end lie beyond the buffer's num_records and read zeros.
+//   * An output element's products are accumulated in the same order for
+//     every M (K steps of 64, two MFMA k-slices of 32 each), so token
+//     chunking never changes a value.
+// ---------------------------------------------------------------------------
+namespace nt {
+
+constexpr int BM = 256, BN = 160, BK = 64, STAGES = 3;
+constexpr int WGM = 4, WGN = 2, NW = WGM * WGN, NT = NW * 64;
+constexpr int MF = 16;
+constexpr int WM = BM / WGM, WN = BN / WGN;   // 64 x 80 per wave
+constexpr int FM = WM / MF, FN = WN / MF;     // 4 x 5 MFMA tiles
+constexpr int KS = BK / 32;                   // MFMA k-slices per step
+constexpr int A_EL = BM * BK, STAGE = (BM + BN) * BK;
+typedef short i16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ int swz(int r) { return r & 6; }
+
+// One operand tile: ROWS rows of a [rows][ld] matrix contiguous along k.
+template <int ROWS>
+struct Copy {
+    static constexpr int CPR = BK / 8;             // 16-byte chunks per LDS row
+    static constexpr int RPI = 64 / CPR;           // rows per copy instruction
+    static constexpr int WI = ROWS / RPI;          // copy instructions per stage
+    static constexpr int PER = (WI + NW - 1) / NW; // per wave (some waves one fewer)
+    static_assert(ROWS % RPI == 0, "rows per copy instruction");
+    __amdgpu_buffer_rsrc_t rs;
+    uint32_t vlane;       // this lane's byte offset within its instruction's rows
+    uint32_t ins_stride;  // bytes from one instruction's rows to the next
+    int kc;               // first k of this lane's chunk
+    int nmine;            // copy instructions this wave issues per stage
+    int64_t K;
+
+    __device__ __forceinline__ void init(const uint16_t* base, int64_t ld, int64_t row0,
+                                         int64_t rows, int64_t K_, int wave, int lane) {
+        K = K_;
+        const int64_t left = rows - row0;
+        const int64_t vr = left < 0 ? 0 : (left < ROWS ? left : ROWS);
+        rs = make_rsrc(base + row0 * ld, vr * ld * 2);
+        const int r = lane / CPR;
+        const int c = (lane % CPR) ^ swz(r);
+        kc = c * 8;
+        vlane = (uint32_t)((r * ld + c * 8) * 2);
+        ins_stride = (uint32_t)(RPI * ld * 2);
+        nmine = 0;
+#pragma unroll
+        for (int i = 0; i < PER; ++i)
+            if (wave + NW * i < WI) nmine = i + 1;
+    }
+    // Copy of the K step at k0 into LDS stage `dst` (k past K reads zeros).
+    __device__ __forceinline__ void issue(uint16_t* dst, int64_t k0, int wave) const {
+        const bool tail = k0 + BK > K;
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int ins = wave + NW * i;
+            if (PER * NW != WI && ins >= WI) break;   // wave-uniform
+            uint32_t off = vlane + (uint32_t)ins * ins_stride;
+            if (tail && k0 + kc >= K) off = kOob;
+            lds_void* d = (lds_void*)(dst + (size_t)ins * 64 * 8);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, d, 16, off, (int)(k0 * 2), 0, 0);
+        }
+    }
+};
+
+// 16x16x32 fragment: lane holds row r0 + lane%16, k = ks*32 + 8*(lane/16) + 0..7.
+__device__ __forceinline__ bf16x8 frag(const uint16_t* src, int r0, int ks, int lane) {
+    const int r = r0 + (lane & 15);
+    const int c = (ks * 4 + (lane >> 4)) ^ swz(r);
+    return *reinterpret_cast<const bf16x8*>(src + r * BK + c * 8);
+}
+
+__device__ __forceinline__ void barrier() {
+    // a bare s_barrier: __syncthreads() would also wait for every copy in
+    // flight (vmcnt(0)), which defeats the three-stage ring
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_barrier" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+}  // namespace nt
+
+template <int EPI, bool OUT_BF16>
+__global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
+    using namespace nt;
+    __shared__ __attribute__((aligned(1024))) uint16_t smem[STAGES * STAGE];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const bool grpB = wave >= 4;
+    const int wm = wave / WGN, wn = wave % WGN;
+    int tm, tn;
+    tile_coords(a.tiles_m, a.tiles_n, tm, tn);
+    const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+
+    Copy<BM> ca;
+    Copy<BN> cb;
+    ca.init(a.A, a.lda, m0, a.M, a.K, wave, lane);
+    cb.init(a.B, a.ldb, n0, a.N, a.K, wave, lane);
+    constexpr int LA = Copy<BM>::PER, LB = Copy<BN>::PER;
+    const int loads = ca.nmine + cb.nmine;   // copy instructions per step (wave-uniform)
+
+    f32x4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int nk = (int)((a.K + BK - 1) / BK);
+    auto issue_step = [&](int q) {
+        uint16_t* dst = smem + (q % STAGES) * STAGE;
+        ca.issue(dst, (int64_t)q * BK, wave);
+        cb.issue(dst + A_EL, (int64_t)q * BK, wave);
+    };
+    // wait until this wave's copies are complete except the newest step's
+    // (keep_one) or all of them; copies complete in issue order
+    auto wait_copies = [&](bool keep_one) {
+        if (!keep_one) { wait_vmcnt<0>(); return; }
+        if (loads == LA + LB) wait_vmcnt<LA + LB>();
+        else if (loads == LA + LB - 1) wait_vmcnt<LA + LB - 1>();
+        else wait_vmcnt<LA + LB - 2>();
+    };
+
+    if (nk > 0) {   // (uniform) every wave runs the same number of barriers
+        issue_step(0);
+        if (nk > 1) issue_step(1);
+        wait_copies(nk > 1);
+        barrier();               // step 0 visible to every wave
+        if (grpB) barrier();     // group B starts one phase late
+
+        bf16x8 fa[KS][FM], fb[KS][FN];
+        for (int p = 0; p < nk; ++p) {
+            // memory phase: copy step p+2 into the stage step p-1 used (both
+            // groups finished reading it before this phase), read step p
+            const uint16_t* sa = smem + (p % STAGES) * STAGE;
+            const uint16_t* sb = sa + A_EL;
+            const bool more = p + 2 < nk;
+            if (more) issue_step(p + 2);
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+                for (int i = 0; i < FM; ++i) fa[ks][i] = frag(sa, wm * WM + i * MF, ks, lane);
+#pragma unroll
+                for (int j = 0; j < FN; ++j) fb[ks][j] = frag(sb, wn * WN + j * MF, ks, lane);
+            }
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            // before group A's next memory phase this wave's copies of step
+            // p+1 have landed (those of step p+2 may still be in flight)
+            if (grpB) wait_copies(more);
+            barrier();
+            // compute phase
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < FN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[ks][j], fa[ks][i],
+                                                                            acc[i][j], 0, 0, 0);
+            if (!grpB) wait_copies(more);
+            if (!(grpB && p == nk - 1)) barrier();
+        }
+        wait_vmcnt<0>();
+    }
+
+    // Epilogue.  Lane holds C(m = base_m + lane%16, n = base_n + 4*(lane/16) + 0..3)
+    // in acc[i][j][0..3].
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int64_t m = m0 + wm * WM + i * MF + (lane & 15);
+        if (m >= a.M) continue;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int64_t n = n0 + wn * WN + j * MF + 4 * (lane >> 4);
+            if (n >= a.N) continue;
+            float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+            epilogue_store<EPI, OUT_BF16>(a, m, n, v);
         }
     }
 }
@@ -420,6 +640,34 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1) void gemm_kernel(KArgs a) {
 // Tile configuration: 256 x 256 workgroup tile, 4 waves of 128 x 128.
 constexpr int CFG_BM = ATP_GEMM_BM, CFG_BN = ATP_GEMM_BN, CFG_BK = ATP_GEMM_BK,
               CFG_STAGES = ATP_GEMM_STAGES, CFG_WGM = ATP_GEMM_WGM, CFG_WGN = ATP_GEMM_WGN;
+
+KArgs kargs(const GemmProblem& p, int bm, int bn) {
+    KArgs a;
+    a.A = static_cast<const uint16_t*>(p.A);
+    a.lda = p.lda;
+    a.B = static_cast<const uint16_t*>(p.B);
+    a.ldb = p.ldb;
+    a.C = p.C;
+    a.ldc = p.ldc;
+    a.bias = static_cast<const uint16_t*>(p.bias);
+    a.pre_in = static_cast<const uint16_t*>(p.pre_in);
+    a.pre_out = static_cast<uint16_t*>(p.pre_out);
+    a.M = p.M;
+    a.N = p.N;
+    a.K = p.K;
+    a.tiles_m = (int)((p.M + bm - 1) / bm);
+    a.tiles_n = (int)((p.N + bn - 1) / bn);
+    return a;
+}
+
+template <int EPI, bool OUT_BF16>
+hipError_t launch_nt(const GemmProblem& p, hipStream_t s) {
+    const KArgs a = kargs(p, nt::BM, nt::BN);
+    const int grid = a.tiles_m * a.tiles_n;
+    if (grid == 0) return hipSuccess;
+    hipLaunchKernelGGL((gemm_nt_kernel<EPI, OUT_BF16>), dim3(grid), dim3(nt::NT), 0, s, a);
+    return hipGetLastError();
+}
 
 template <bool A_K, bool B_K, int EPI, bool OUT_BF16>
 hipError_t launch_t(const GemmProblem& p, hipStream_t s) {
@@ -495,12 +743,11 @@ hipError_t launch_gemm(const GemmProblem& p, hipStream_t s) {
         }
     case LAYOUT_NT:
         if (p.epi == EPI_NONE)
-            return b16 ? launch_t<true, true, EPI_NONE, true>(p, s)
-                       : launch_t<true, true, EPI_NONE, false>(p, s);
-        if (p.epi == EPI_GELU_BWD && b16) return launch_t<true, true, EPI_GELU_BWD, true>(p, s);
+            return b16 ? launch_nt<EPI_NONE, true>(p, s) : launch_nt<EPI_NONE, false>(p, s);
+        if (p.epi == EPI_GELU_BWD && b16) return launch_nt<EPI_GELU_BWD, true>(p, s);
         // the forward with a transposed weight copy (B = W^T, contiguous along k)
-        if (p.epi == EPI_BIAS && b16) return launch_t<true, true, EPI_BIAS, true>(p, s);
-        if (p.epi == EPI_BIAS_GELU && b16) return launch_t<true, true, EPI_BIAS_GELU, true>(p, s);
+        if (p.epi == EPI_BIAS && b16) return launch_nt<EPI_BIAS, true>(p, s);
+        if (p.epi == EPI_BIAS_GELU && b16) return launch_nt<EPI_BIAS_GELU, true>(p, s);
         return hipErrorInvalidValue;
     case LAYOUT_TN:
         if (p.epi == EPI_NONE && !b16) return launch_t<false, false, EPI_NONE, false>(p, s);

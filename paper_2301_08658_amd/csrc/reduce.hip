@@ -137,22 +137,26 @@ hipError_t launch_r(const ReduceProblem& p, hipStream_t s) {
     return hipGetLastError();
 }
 
-// Column sums: a block owns 64 columns; 32 row lanes x 8 column lanes, each
+// Column sums: a block owns 16 columns; 32 row lanes x 2 column lanes, each
 // thread 8 columns (one 16-byte load per row), rows t = ty, ty+32, ... in
 // ascending order; the 32 row-lane sums are then added in ascending order.
-constexpr int CS_COLS = 64;
-constexpr int CS_ROWL = 32;
+// One wave per block and a short block keep every CU busy (N / 16 blocks).
+constexpr int CS_CL = 2;                 // column lanes
+constexpr int CS_COLS = CS_CL * 8;       // columns per block
+constexpr int CS_ROWL = 32;              // row lanes
+constexpr int CS_T = CS_CL * CS_ROWL;    // threads per block
 
-__global__ __launch_bounds__(256) void colsum_kernel(const uint16_t* __restrict__ dy, int64_t ld,
-                                                     int64_t T, int64_t N, float* __restrict__ db) {
+__global__ __launch_bounds__(CS_T) void colsum_kernel(const uint16_t* __restrict__ dy, int64_t ld,
+                                                      int64_t T, int64_t N, float* __restrict__ db) {
     __shared__ float part[CS_ROWL][CS_COLS];
-    const int tx = threadIdx.x & 7;
-    const int ty = threadIdx.x >> 3;
+    const int tx = threadIdx.x % CS_CL;
+    const int ty = threadIdx.x / CS_CL;
     const int64_t c = (int64_t)blockIdx.x * CS_COLS + tx * 8;
     float s[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) s[e] = 0.0f;
     if (c < N) {
+#pragma unroll 8
         for (int64_t t = ty; t < T; t += CS_ROWL) {
             float f[8];
             unpack8(*reinterpret_cast<const u32x4*>(dy + t * ld + c), f);
@@ -195,7 +199,7 @@ hipError_t launch_colsum(const void* dy, int64_t ld, int64_t T, int64_t N, float
                          hipStream_t s) {
     if (N <= 0) return hipSuccess;
     const int64_t blocks = (N + CS_COLS - 1) / CS_COLS;
-    hipLaunchKernelGGL(colsum_kernel, dim3((unsigned)blocks), dim3(256), 0, s,
+    hipLaunchKernelGGL(colsum_kernel, dim3((unsigned)blocks), dim3(CS_T), 0, s,
                        static_cast<const uint16_t*>(dy), ld, T, N, db);
     return hipGetLastError();
 }
