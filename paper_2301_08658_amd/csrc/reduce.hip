@@ -141,6 +141,9 @@ hipError_t launch_r(const ReduceProblem& p, hipStream_t s) {
 // thread 8 columns (one 16-byte load per row), rows t = ty, ty+32, ... in
 // ascending order; the 32 row-lane sums are then added in ascending order.
 // One wave per block and a short block keep every CU busy (N / 16 blocks).
+// Blocks are renumbered so that neighbouring column groups, which share
+// cache lines, run on the same XCD (the dispatcher deals blocks round-robin
+// over the 8 XCDs, each with its own L2).
 constexpr int CS_CL = 2;                 // column lanes
 constexpr int CS_COLS = CS_CL * 8;       // columns per block
 constexpr int CS_ROWL = 32;              // row lanes
@@ -151,7 +154,10 @@ __global__ __launch_bounds__(CS_T) void colsum_kernel(const uint16_t* __restrict
     __shared__ float part[CS_ROWL][CS_COLS];
     const int tx = threadIdx.x % CS_CL;
     const int ty = threadIdx.x / CS_CL;
-    const int64_t c = (int64_t)blockIdx.x * CS_COLS + tx * 8;
+    const int G = gridDim.x, xcd = blockIdx.x % 8, idx = blockIdx.x / 8;
+    const int per = G / 8, rem = G % 8;
+    const int64_t blk = (xcd < rem) ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
+    const int64_t c = blk * CS_COLS + tx * 8;
     float s[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) s[e] = 0.0f;
@@ -168,7 +174,7 @@ __global__ __launch_bounds__(CS_T) void colsum_kernel(const uint16_t* __restrict
     for (int e = 0; e < 8; ++e) part[ty][tx * 8 + e] = s[e];
     __syncthreads();
     if (threadIdx.x < CS_COLS) {
-        const int64_t col = (int64_t)blockIdx.x * CS_COLS + threadIdx.x;
+        const int64_t col = blk * CS_COLS + threadIdx.x;
         if (col < N) {
             float acc = part[0][threadIdx.x];
             for (int r = 1; r < CS_ROWL; ++r) acc += part[r][threadIdx.x];
