@@ -49,6 +49,9 @@ def parse():
                     help="no workspace: forward reads W directly (NN), dW reads X, dY (TN)")
     ap.add_argument("--no-aux", action="store_true",
                     help="no second compute stream (independent GEMMs do not share the chip)")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay the step as a captured HIP graph (measured slower than "
+                         "launching it: the replay loses part of the reduce/GEMM overlap)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=256,
                     help="token rows in the oracle's timed CPU sample")
@@ -112,23 +115,35 @@ def step_flops(st, fwd_only):
 
 
 def make_step(torch, atp, st, fwd_only, serial, aux):
-    cs = torch.cuda.current_stream()
-    ms = cs if serial else torch.cuda.Stream()
+    ms = None if serial else torch.cuda.Stream()
     ax = torch.cuda.Stream() if (aux and not serial) else None
 
     def step():
+        # the stream current at call time (the capture stream inside a graph)
+        cs = torch.cuda.current_stream()
+        ms_ = cs if serial else ms
         atp.atp_block_fwd(st["m"], st["bm"], st["T"], st["h"], st["chunks"], st["w"], st["b"],
                           st["x"], st["a"], st["fwd_tabs"], st["qkv"], st["o"], st["hh"],
                           st["pre"], st["z"], workspace=st["ws"], compute_stream=cs,
-                          comm_stream=ms, aux_stream=ax)
+                          comm_stream=ms_, aux_stream=ax)
         if fwd_only:
             return
         atp.atp_block_bwd(st["m"], st["bm"], st["T"], st["h"], st["chunks"], st["w"], st["b"],
                           st["x"], st["a"], st["hh"], st["pre"], st["dz"], st["dqkv"], st["do"],
                           st["bwd_tabs"], st["dh_pre"], st["dx_qkv"], st["dx_fc1"],
                           st["d_attn"], st["dw"], st["db"], workspace=st["ws"], compute_stream=cs,
-                          comm_stream=ms, aux_stream=ax)
+                          comm_stream=ms_, aux_stream=ax)
     return step
+
+
+def capture(torch, step):
+    """One step recorded as a HIP graph (hipStreamBeginCapture through torch):
+    the same kernels, events and stream joins, replayed without host launches."""
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    torch.cuda.synchronize()
+    return g
 
 
 def measured_traffic(kernel, workload):
@@ -264,6 +279,15 @@ def main():
         step()
     torch.cuda.synchronize()
     log(f"[bench] warmup done ({args.warmup} steps)")
+    run = step
+    # the direct path (no workspace) is not captured: the library refuses it
+    if args.graph and not args.no_workspace:
+        graph = capture(torch, step)
+        run = graph.replay
+        for _ in range(args.warmup):
+            run()
+        torch.cuda.synchronize()
+        log("[bench] step captured as a HIP graph")
 
     # timed region: inputs resident, K steps between two device-wide syncs;
     # an event after each step (on the stream the block joins into) gives the
@@ -273,7 +297,7 @@ def main():
     t0 = time.perf_counter()
     evs[0].record()
     for i in range(args.steps):
-        step()
+        run()
         evs[i + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -286,8 +310,8 @@ def main():
     log(f"[bench] {args.steps} steps, {ms_step:.3f} ms/step, {value:.1f} TFLOP/s "
         f"(per step median {step_ms['median']:.3f} p10 {step_ms['p10']:.3f} p90 {step_ms['p90']:.3f} ms)")
 
-    # same K steps again with every library launch bracketed by HIP events on
-    # its own stream: per-kernel durations for the roofline
+    # same K steps again, launched eagerly with every library launch bracketed
+    # by HIP events on its own stream: per-kernel durations for the roofline
     atp.atp_profile_enable(True)
     for _ in range(args.steps):
         step()
@@ -386,6 +410,7 @@ def main():
                     **{"pass": "fwd" if fwd_only else "fwd+bwd"},
                     serial=bool(args.serial), aux_stream=not args.no_aux,
                     transposed_layout=not args.no_workspace,
+                    hip_graph=bool(args.graph and not args.no_workspace),
                     gflop_per_step=round(flops / 1e9, 1)),
         step_ms=step_ms, mfma_util=round(value / PEAK_BF16_TFLOPS, 4),
         roofline=roofline, reduce=reduce_info, kernels=kernels, cpu_baseline=cpu)

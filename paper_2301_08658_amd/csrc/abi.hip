@@ -402,6 +402,21 @@ struct Streams {
     }
 };
 
+// Capturing the direct path into a HIP graph made hipStreamEndCapture crash
+// inside the runtime (host segmentation fault; the cause is not identified),
+// so that path refuses a capturing compute stream.  The workspace path is
+// captured and replayed bit for bit (tested).
+atp_status refuse_capture_of_direct_path(void* compute_stream) {
+    hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+    HIP_CHECK(hipStreamIsCapturing(static_cast<hipStream_t>(compute_stream), &st),
+              "hipStreamIsCapturing");
+    if (st != hipStreamCaptureStatusNone)
+        return set_error(ATP_ERR_UNSUPPORTED,
+                         "graph capture needs the workspace path (pass a workspace of "
+                         "atp_block_workspace_bytes bytes)");
+    return ATP_OK;
+}
+
 double gemm_flops(int64_t m, int64_t n, int64_t k) { return 2.0 * (double)m * (double)n * (double)k; }
 
 }  // namespace
@@ -611,6 +626,7 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     const bool nt = workspace && ws_bytes >= ws_fwd_bytes(P);
     if (nt && reinterpret_cast<uintptr_t>(workspace) % kWsAlign)
         return set_error(ATP_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kWsAlign);
+    if (!nt) ATP_CHECK(refuse_capture_of_direct_path(compute_stream));
 
     Streams S(compute_stream, comm_stream, aux_stream);
     // The NT kernel's tiles fill the chip by themselves (a 512-row chunk is
@@ -789,6 +805,7 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     const bool nt = workspace && ws_bytes >= ws_bwd_bytes(P, tokens) && tokens % 8 == 0;
     if (nt && reinterpret_cast<uintptr_t>(workspace) % kWsAlign)
         return set_error(ATP_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kWsAlign);
+    if (!nt) ATP_CHECK(refuse_capture_of_direct_path(compute_stream));
 
     Streams S(compute_stream, comm_stream, aux_stream);
     S.gemm_one_lane = nt;     // as in the forward: one lane on this path
