@@ -171,11 +171,12 @@ def test_mesh_simulation_equals_unsharded_layer(mode, mesh):
 
 
 # ------------------------------------------------------------------ invariances
-def test_chunk_count_never_changes_a_bit():
+@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "transposed"])
+def test_chunk_count_never_changes_a_bit(workspace):
     base = None
     inp = make_block_inputs("col", (2, 4), (1, 2), 512, 1024, 0.02, seed=4)
     for chunks in (1, 2, 4, 8):
-        out = run_block_fwd(inp, chunks)
+        out = run_block_fwd(inp, chunks, workspace=workspace)
         torch.cuda.synchronize()
         if base is None:
             base = out
@@ -245,15 +246,16 @@ def _check_bwd(out, ref, inp, what=""):
         assert_close(out["db"][i], ref["db_" + n], f"{what} db_{n}", floor=fl)
 
 
+@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "transposed"])
 @pytest.mark.parametrize("mode,mesh,coord", [("col", (2, 2), (1, 0)), ("row", (2, 4), (1, 3)),
                                              ("col", (4, 1), (2, 0))])
-def test_block_fwd_bwd_integer_chain_bit_exact(mode, mesh, coord):
+def test_block_fwd_bwd_integer_chain_bit_exact(mode, mesh, coord, workspace):
     """Integer inputs, integer peers and pre = 0 (GeLU'(0) = 1/2 exactly): every
     value before a bf16 store is exact on both sides, so the chained backward
     (fc2 dX -> reduce * GeLU' -> fc1 dX / dW) must match bit for bit, with the
     oracle's bf16-stored outputs rounded the same way."""
     inp = make_block_inputs(mode, mesh, coord, 192, 256, 0.0, seed=10, bwd=True, integer=True)
-    out = run_block_bwd(inp, 2)
+    out = run_block_bwd(inp, 2, workspace=workspace)
     torch.cuda.synchronize()
     ref = _oracle_bwd(inp)
     for key in ("dh_pre", "dx_qkv", "dx_fc1", "d_attn"):
@@ -264,14 +266,15 @@ def test_block_fwd_bwd_integer_chain_bit_exact(mode, mesh, coord):
         np.testing.assert_array_equal(to64(out["db"][i]), ref["db_" + n], err_msg=n)
 
 
+@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "transposed"])
 @pytest.mark.parametrize("mode", ["col", "row"])
-def test_block_bwd_tiny_every_coordinate(mode):
+def test_block_bwd_tiny_every_coordinate(mode, workspace):
     w = TINY
     d1, d2 = w["mesh"]
     for coord in itertools.product(range(d1), range(d2)):
         inp = make_block_inputs(mode, w["mesh"], coord, w["tokens"], w["h"], w["sigma_w"],
                                 seed=7, bwd=True)
-        out = run_block_bwd(inp, w["chunks"])
+        out = run_block_bwd(inp, w["chunks"], workspace=workspace)
         torch.cuda.synchronize()
         _check_bwd(out, _oracle_bwd(inp), inp, f"{mode} {coord}")
 
@@ -284,11 +287,12 @@ def test_block_bwd_groups_of_one(mesh):
     _check_bwd(out, _oracle_bwd(inp), inp, f"{mesh}")
 
 
-def test_block_bwd_chunk_invariance():
+@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "transposed"])
+def test_block_bwd_chunk_invariance(workspace):
     inp = make_block_inputs("col", (2, 4), (1, 3), 512, 1024, 0.02, seed=9, bwd=True)
-    base = run_block_bwd(inp, 1)
+    base = run_block_bwd(inp, 1, workspace=workspace)
     for chunks in (2, 4, 8):
-        out = run_block_bwd(inp, chunks)
+        out = run_block_bwd(inp, chunks, workspace=workspace)
         torch.cuda.synchronize()
         for key in ("dh_pre", "dx_qkv", "dx_fc1", "d_attn"):
             assert torch.equal(out[key], base[key]), (chunks, key)

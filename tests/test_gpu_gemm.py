@@ -50,6 +50,26 @@ def test_bwd_nt_tn_colsum_integer_bit_exact(T, K, N, chunks):
     np.testing.assert_array_equal(to64(db), rdb)
 
 
+@pytest.mark.parametrize("T,K,N,chunks", [(1, 8, 8, 1), (7, 16, 24, 1), (64, 40, 8, 2),
+                                          (257, 168, 40, 1), (700, 488, 1000, 2),
+                                          (512, 160, 2056, 4), (1024, 1288, 72, 8)])
+def test_dx_nt_ragged_integer_bit_exact(T, K, N, chunks):
+    """dX = dY W^T runs the NT kernel (256 x 160 tiles, K steps of 64):
+    outputs of one row, sub-tile and multi-tile sizes with ragged edges, and
+    contractions shorter than one K step or ending in a partial one."""
+    m = atp.mesh(1, 1)
+    x = S.randint_bf16((T, K), 6, 1).to(DEV)
+    w = S.randint_bf16((K, N), 6, 2).to(DEV)
+    dy = S.randint_bf16((T, N), 6, 3).to(DEV)
+    dx = torch.full((T, K), float("nan"), device=DEV)
+    dw = torch.full((K, N), float("nan"), device=DEV)
+    atp.atp_shard_linear_bwd(m, atp.ATP_ROW_FIRST, T, K, N, chunks, x, w, dy, dx, dw, None)
+    _sync()
+    rdx, rdw, _ = O.linear_bwd(x.cpu(), w.cpu(), dy.cpu())
+    np.testing.assert_array_equal(to64(dx), rdx)
+    np.testing.assert_array_equal(to64(dw), rdw)
+
+
 @pytest.mark.parametrize("epi", [atp.ATP_EPI_NONE, atp.ATP_EPI_BIAS, atp.ATP_EPI_BIAS_GELU])
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
 def test_fwd_epilogues_group_of_one(epi, out_dtype):
