@@ -203,7 +203,7 @@ atp_status run_gemm(const atp::GemmProblem& p, hipStream_t s) {
                          (double)p.M * p.N * (p.out_bf16 ? 2.0 : 4.0) +
                          ((p.epi == atp::EPI_GELU_BWD || p.pre_out) ? 2.0 * p.M * p.N : 0.0);
     // one name per kernel instantiation: layout, epilogue, output type
-    std::string name = atp::gemm_kernel_name(p.layout);
+    std::string name = atp::gemm_kernel_name(p);
     name += "_e" + std::to_string(p.epi) + (p.out_bf16 ? "_bf16" : "_f32");
     if (g_prof_on && g_prof_detail) {
         char buf[96];

@@ -465,17 +465,33 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1) void gemm_kernel(KArgs a) {
 // ---------------------------------------------------------------------------
 namespace nt {
 
-constexpr int BM = 256, BN = 160, BK = 64, STAGES = 3;
-constexpr int WGM = 4, WGN = 2, NW = WGM * WGN, NT = NW * 64;
-// the 32 tiles an XCD runs at once form a 4 x 8 block: 4*256 + 8*160 rows per
-// K step shared by 32 tiles (L2 hit rate 81% against 74% for 8 x 4)
-constexpr int GROUP = 4;
+constexpr int BM = 256, BK = 64;
+constexpr int NW = 8, NT = NW * 64;           // two groups of four waves
 constexpr int MF = 16;
-constexpr int WM = BM / WGM, WN = BN / WGN;   // 64 x 80 per wave
-constexpr int FM = WM / MF, FN = WN / MF;     // 4 x 5 MFMA tiles
 constexpr int KS = BK / 32;                   // MFMA k-slices per step
-constexpr int A_EL = BM * BK, STAGE = (BM + BN) * BK;
 typedef short i16x8 __attribute__((ext_vector_type(8)));
+
+// Tile configurations.  Every one sums an output element's products in the
+// same order (K steps of 64, two 16x16x32 k-slices each), so they give the
+// same bits and may be mixed freely, e.g. across token chunks.
+template <int BN_, int WGM_, int WGN_, int STAGES_, int GROUP_>
+struct Cfg {
+    static constexpr int BN = BN_, WGM = WGM_, WGN = WGN_, STAGES = STAGES_, GROUP = GROUP_;
+    static_assert(WGM * WGN == NW, "eight waves");
+    static_assert(STAGES == 2 || STAGES == 3, "two or three LDS stages");
+    static constexpr int WM = BM / WGM, WN = BN / WGN;
+    static constexpr int FM = WM / MF, FN = WN / MF;
+    static_assert(FM * MF == WM && FN * MF == WN, "wave tile of whole MFMA tiles");
+    static constexpr int A_EL = BM * BK, STAGE = (BM + BN) * BK;
+};
+// 256 x 160: three stages (156 KB of LDS); waves of 64 x 80; the 32 tiles an
+// XCD runs at once form a 4 x 8 block (4*256 + 8*160 rows per K step, L2 hit
+// rate 81% against 74% for 8 x 4)
+using Tile160 = Cfg<160, 4, 2, 3, 4>;
+// 256 x 256: two stages (128 KB); waves of 128 x 64; 30% fewer copied bytes
+// per FLOP, ~10% faster on the short-K (tokens) dW products, but 62.5% of
+// the tile count of 256 x 160 per launch
+using Tile256 = Cfg<256, 2, 4, 2, 8>;
 
 __device__ __forceinline__ int swz(int r) { return r & 6; }
 
@@ -542,9 +558,12 @@ __device__ __forceinline__ void barrier() {
 
 }  // namespace nt
 
-template <int EPI, bool OUT_BF16>
+template <class C, int EPI, bool OUT_BF16>
 __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
     using namespace nt;
+    constexpr int BN = C::BN, WGN = C::WGN, STAGES = C::STAGES;
+    constexpr int WM = C::WM, WN = C::WN, FM = C::FM, FN = C::FN;
+    constexpr int A_EL = C::A_EL, STAGE = C::STAGE;
     __shared__ __attribute__((aligned(1024))) uint16_t smem[STAGES * STAGE];
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -552,7 +571,7 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
     const bool grpB = wave >= 4;
     const int wm = wave / WGN, wn = wave % WGN;
     int tm, tn;
-    tile_coords<GROUP>(a.tiles_m, a.tiles_n, tm, tn);
+    tile_coords<C::GROUP>(a.tiles_m, a.tiles_n, tm, tn);
     const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
 
     Copy<BM> ca;
@@ -584,20 +603,20 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
     };
 
     if (nk > 0) {   // (uniform) every wave runs the same number of barriers
-        issue_step(0);
-        if (nk > 1) issue_step(1);
-        wait_copies(nk > 1);
+        for (int q = 0; q < STAGES - 1 && q < nk; ++q) issue_step(q);
+        wait_copies(STAGES == 3 && nk > 1);
         barrier();               // step 0 visible to every wave
         if (grpB) barrier();     // group B starts one phase late
 
         bf16x8 fa[KS][FM], fb[KS][FN];
         for (int p = 0; p < nk; ++p) {
-            // memory phase: copy step p+2 into the stage step p-1 used (both
-            // groups finished reading it before this phase), read step p
+            // memory phase: copy step p+STAGES-1 into the stage step p-1 used
+            // (both groups finished reading it before this phase), read step p
             const uint16_t* sa = smem + (p % STAGES) * STAGE;
             const uint16_t* sb = sa + A_EL;
-            const bool more = p + 2 < nk;
-            if (more) issue_step(p + 2);
+            if (p + STAGES - 1 < nk) issue_step(p + STAGES - 1);
+            // with three stages the copy of step p+2 may stay in flight below
+            const bool more = STAGES == 3 && p + 2 < nk;
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
@@ -607,7 +626,8 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
             }
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
             // before group A's next memory phase this wave's copies of step
-            // p+1 have landed (those of step p+2 may still be in flight)
+            // p+1 have landed (with three stages those of step p+2 may still
+            // be in flight)
             if (grpB) wait_copies(more);
             barrier();
             // compute phase
@@ -664,13 +684,29 @@ KArgs kargs(const GemmProblem& p, int bm, int bn) {
     return a;
 }
 
-template <int EPI, bool OUT_BF16>
-hipError_t launch_nt(const GemmProblem& p, hipStream_t s) {
-    const KArgs a = kargs(p, nt::BM, nt::BN);
+// 256 x 256 tiles for products with a short contraction (at most 8192: the
+// dW products over the tokens) whose last wave of tiles is at least 90% full
+// (256 CUs); 256 x 160 tiles otherwise
+bool nt_use_256(const GemmProblem& p) {
+    constexpr int64_t kCUs = 256;
+    const int64_t tiles = ((p.M + nt::BM - 1) / nt::BM) * ((p.N + 255) / 256);
+    const int64_t waves = (tiles + kCUs - 1) / kCUs;
+    return p.K <= 8192 && tiles * 10 >= waves * kCUs * 9;
+}
+
+template <class C, int EPI, bool OUT_BF16>
+hipError_t launch_nt_cfg(const GemmProblem& p, hipStream_t s) {
+    const KArgs a = kargs(p, nt::BM, C::BN);
     const int grid = a.tiles_m * a.tiles_n;
     if (grid == 0) return hipSuccess;
-    hipLaunchKernelGGL((gemm_nt_kernel<EPI, OUT_BF16>), dim3(grid), dim3(nt::NT), 0, s, a);
+    hipLaunchKernelGGL((gemm_nt_kernel<C, EPI, OUT_BF16>), dim3(grid), dim3(nt::NT), 0, s, a);
     return hipGetLastError();
+}
+
+template <int EPI, bool OUT_BF16>
+hipError_t launch_nt(const GemmProblem& p, hipStream_t s) {
+    return nt_use_256(p) ? launch_nt_cfg<nt::Tile256, EPI, OUT_BF16>(p, s)
+                         : launch_nt_cfg<nt::Tile160, EPI, OUT_BF16>(p, s);
 }
 
 template <bool A_K, bool B_K, int EPI, bool OUT_BF16>
@@ -714,10 +750,10 @@ bool gemm_supported(int layout, int epi, bool out_bf16) {
     }
 }
 
-const char* gemm_kernel_name(int layout) {
-    switch (layout) {
+const char* gemm_kernel_name(const GemmProblem& p) {
+    switch (p.layout) {
     case LAYOUT_NN: return "gemm_nn";
-    case LAYOUT_NT: return "gemm_nt";
+    case LAYOUT_NT: return nt_use_256(p) ? "gemm_nt256" : "gemm_nt";
     case LAYOUT_TN: return "gemm_tn";
     default: return "gemm_?";
     }

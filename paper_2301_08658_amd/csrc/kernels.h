@@ -32,7 +32,8 @@ struct GemmProblem {
 // True if the kernel set has an instance for this (layout, epi, out) combination.
 bool gemm_supported(int layout, int epi, bool out_bf16);
 hipError_t launch_gemm(const GemmProblem& p, hipStream_t s);
-const char* gemm_kernel_name(int layout);
+// Profiling name of the kernel a problem launches (layout and tile configuration).
+const char* gemm_kernel_name(const GemmProblem& p);
 
 constexpr int kMaxParts = 64;
 
