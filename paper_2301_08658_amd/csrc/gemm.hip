@@ -565,6 +565,9 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
     constexpr int WM = C::WM, WN = C::WN, FM = C::FM, FN = C::FN;
     constexpr int A_EL = C::A_EL, STAGE = C::STAGE;
     __shared__ __attribute__((aligned(1024))) uint16_t smem[STAGES * STAGE];
+    // issue priority above the reduction waves that share the CUs while
+    // the next chunk's reduction runs beside this GEMM (measured +0.4%)
+    __builtin_amdgcn_s_setprio(1);
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
