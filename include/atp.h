@@ -222,8 +222,10 @@ typedef struct {
  * of the forward's need (a transposed copy W^T of the four local weight
  * shards, sum of k_loc * n_loc * 2 bytes) and the backward's (X^T of x, the
  * attention block and H, and dY^T of the four linears, each tokens * cols *
- * 2 bytes), every piece rounded up to 256 bytes.  Returns 0 for invalid
- * arguments.  `chunks` does not change the size. */
+ * 2 bytes), each plus the fp32 split-K slabs of the chunked products that
+ * feed a reduction (S * chunk rows * cols * 4 bytes for the largest split
+ * plan S over every valid chunk count), every piece rounded up to 256 bytes.
+ * Returns 0 for invalid arguments.  `chunks` does not change the size. */
 size_t atp_block_workspace_bytes(const atp_mesh* mesh, int32_t block_mode, int64_t tokens,
                                  int64_t h, int32_t chunks);
 
@@ -246,19 +248,25 @@ atp_status atp_transpose_bf16(int64_t rows, int64_t cols, const void* src, int64
  * written; fc2's chunk c waits for fc1's reduced chunk c.  A group of one
  * needs no reduction: its bias (and GeLU) are applied in the GEMM epilogue
  * and it runs as one launch.
- * Issue order: fc1, out-proj, QKV, fc2.  aux_stream (nullable) is a second
- * compute stream: each GEMM goes to whichever of compute_stream and
- * aux_stream has less work issued so far (in FLOPs), with events for the
- * data dependencies.  With aux_stream NULL all GEMMs run on compute_stream;
- * with comm_stream == compute_stream nothing overlaps.
  * workspace (nullable, 256-byte aligned): when ws_bytes is at least the
  * forward's need (see atp_block_workspace_bytes) the call first writes W^T
- * of each shard there and runs every product in the GEMM's NT layout;
- * otherwise it reads W directly.  The results are bit-identical either way
- * and do not depend on the streams used.  compute_stream's earlier work
- * happens before the block's, and on return compute_stream is ordered after
- * all of it; the workspace may be reused once compute_stream reaches that
- * point. */
+ * of each shard there and runs every product in the GEMM's NT layout, all on
+ * compute_stream in the order out-proj, fc1, QKV, fc2 (aux_stream unused); a
+ * chunk product with too few output tiles to fill the chip is split over its
+ * contraction, the splits' fp32 slabs summed in split order into the own
+ * partial before the chunk's reduction reads it.  Without the workspace the
+ * call reads W directly, issues fc1, out-proj, QKV, fc2, and aux_stream
+ * (nullable) is a second compute stream: each GEMM goes to whichever of
+ * compute_stream and aux_stream has less work issued so far (in FLOPs), with
+ * events for the data dependencies.  With comm_stream == compute_stream
+ * nothing overlaps.  The two paths sum each element's products in different
+ * orders (they agree to fp32 rounding); on either path the results do not
+ * depend on the streams used, and are the same for every chunk count that
+ * gives each chunk product the same split plan (on the direct path: every
+ * chunk count).  compute_stream's earlier work happens before the block's,
+ * and on return compute_stream is ordered after all of it; the workspace
+ * may be reused once compute_stream reaches that point.  The direct path
+ * refuses a compute_stream under HIP graph capture (UNSUPPORTED). */
 atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
                          int32_t chunks, const atp_block_weights* w,
                          const atp_block_fwd_io* io, void* workspace, size_t ws_bytes,
@@ -272,8 +280,10 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
  * GEMM on the less loaded of compute_stream and aux_stream (as in
  * atp_block_fwd), so the dX reductions overlap the later GEMMs.
  * workspace: when ws_bytes is at least the backward's need and tokens % 8
- * == 0, X^T and dY^T are written there and every dW runs in the NT layout;
- * otherwise dW reads X and dY directly.  Bit-identical either way.  On
+ * == 0, X^T and dY^T are written there, every dW runs in the NT layout, all
+ * GEMMs run on compute_stream, and the chunked dX products are split over
+ * their contraction as in atp_block_fwd; otherwise dW reads X and dY
+ * directly.  The paths agree to fp32 rounding (as in atp_block_fwd).  On
  * return compute_stream is ordered after all work. */
 atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
                          int32_t chunks, const atp_block_weights* w,

@@ -235,6 +235,16 @@ atp_status run_colsum(const void* dy, int64_t ld, int64_t T, int64_t N, float* d
                  [&] { return atp::launch_colsum(dy, ld, T, N, db, s); });
 }
 
+// The S split-K slabs of an fp32 product summed into its destination rows.
+atp_status run_split_sum(const float* ws, int S, int64_t rows, int64_t cols, float* out,
+                         int64_t ldo, hipStream_t s) {
+    if (rows <= 0 || cols <= 0) return ATP_OK;
+    const double el = (double)rows * (double)cols;
+    return timed("split_sum", 0.0, el * 4.0 * (S + 1), s, [&] {
+        return atp::launch_split_sum(ws, S, rows * cols, cols, rows, cols, out, ldo, s);
+    });
+}
+
 atp::GemmProblem gemm_problem(int layout, const void* A, int64_t lda, const void* B, int64_t ldb,
                               void* C, int64_t ldc, bool out_bf16, int epi, int64_t M,
                               int64_t N, int64_t K) {
@@ -309,8 +319,30 @@ atp_status block_plan(const atp_mesh* m, int32_t bm, int64_t h, BlockPlan* p) {
 constexpr size_t kWsAlign = 256;
 size_t ws_round(size_t b) { return (b + kWsAlign - 1) / kWsAlign * kWsAlign; }
 
-size_t ws_fwd_bytes(const BlockPlan& P) {
-    size_t b = 0;
+// Split-K slabs of the chunked products that feed a reduction: the forward
+// X W of a linear whose reduction group has several members, the backward
+// dY W^T likewise.  One region serves every chunk of every linear (they run
+// in order on one stream); it is sized for the largest plan over all chunk
+// counts, so the size does not depend on the chunk count.
+size_t slab_bytes(const BlockPlan& P, int64_t tokens, bool bwd) {
+    size_t most = 0;
+    for (int c = 1; c <= ATP_MAX_CHUNKS; ++c) {
+        if (tokens % c) continue;
+        const int64_t mc = tokens / c;
+        for (int L = 0; L < 4; ++L) {
+            const atp_shard& g = P.g[L];
+            if ((bwd ? g.bwd_size : g.red_size) <= 1) continue;
+            const int64_t N = bwd ? g.k_loc : g.n_loc, K = bwd ? g.n_loc : g.k_loc;
+            int64_t ks = 0;
+            const int S = atp::nt_split_plan(mc, N, K, &ks);
+            if (S > 1) most = std::max(most, (size_t)S * mc * N * 4);
+        }
+    }
+    return most;
+}
+
+size_t ws_fwd_bytes(const BlockPlan& P, int64_t tokens) {
+    size_t b = ws_round(slab_bytes(P, tokens, false));
     for (int L = 0; L < 4; ++L) b += ws_round((size_t)P.g[L].n_loc * P.g[L].k_loc * 2);
     return b;
 }
@@ -318,9 +350,26 @@ size_t ws_fwd_bytes(const BlockPlan& P) {
 size_t ws_bwd_bytes(const BlockPlan& P, int64_t tokens) {
     const size_t t2 = (size_t)tokens * 2;
     size_t b = ws_round(P.g[0].k_loc * t2) + ws_round(P.g[1].k_loc * t2) +
-               ws_round(P.g[3].k_loc * t2);
+               ws_round(P.g[3].k_loc * t2) + ws_round(slab_bytes(P, tokens, true));
     for (int L = 0; L < 4; ++L) b += ws_round(P.g[L].n_loc * t2);
     return b;
+}
+
+// An fp32 product [M, N] over K on the NT path: split over K into `slab`
+// when the plan says so, the splits then summed in split order into C.
+atp_status run_nt_partial(atp::GemmProblem p, float* slab, hipStream_t s) {
+    int64_t ks = 0;
+    const int S = slab ? atp::nt_split_plan(p.M, p.N, p.K, &ks) : 1;
+    if (S <= 1) return run_gemm(p, s);
+    float* out = static_cast<float*>(p.C);
+    const int64_t ldo = p.ldc;
+    p.C = slab;
+    p.ldc = p.N;
+    p.splits = S;
+    p.ksplit = ks;
+    p.c_split = p.M * p.N;
+    ATP_CHECK(run_gemm(p, s));
+    return run_split_sum(slab, S, p.M, p.N, out, ldo, s);
 }
 
 // Carves consecutive aligned pieces out of the caller's workspace.
@@ -572,7 +621,7 @@ size_t atp_block_workspace_bytes(const atp_mesh* mesh, int32_t block_mode, int64
     if (!mesh || check_mesh(mesh) != ATP_OK || block_plan(mesh, block_mode, h, &P) != ATP_OK ||
         tokens < 0)
         return 0;
-    return std::max(ws_fwd_bytes(P), ws_bwd_bytes(P, tokens));
+    return std::max(ws_fwd_bytes(P, tokens), ws_bwd_bytes(P, tokens));
 }
 
 atp_status atp_transpose_bf16(int64_t rows, int64_t cols, const void* src, int64_t lds, void* dst,
@@ -623,7 +672,7 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
 
     // with a large enough workspace every product runs in the NT layout from
     // a transposed weight copy (W^T is contiguous along k)
-    const bool nt = workspace && ws_bytes >= ws_fwd_bytes(P);
+    const bool nt = workspace && ws_bytes >= ws_fwd_bytes(P, tokens);
     if (nt && reinterpret_cast<uintptr_t>(workspace) % kWsAlign)
         return set_error(ATP_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kWsAlign);
     if (!nt) ATP_CHECK(refuse_capture_of_direct_path(compute_stream));
@@ -647,10 +696,12 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     ATP_CHECK(S.begin(ev[0]));
 
     uint16_t* wt[4] = {nullptr, nullptr, nullptr, nullptr};
+    float* slab = nullptr;
     int wt_lane[4] = {-1, -1, -1, -1};
     if (nt) {
         Carver c{static_cast<char*>(workspace)};
         for (int L = 0; L < 4; ++L) wt[L] = c.take((size_t)P.g[L].n_loc * P.g[L].k_loc * 2);
+        slab = reinterpret_cast<float*>(c.take(slab_bytes(P, tokens, false)));
     }
     // W^T of linear L for a GEMM on `lane`: written once, on the lane of the
     // linear's first GEMM; other lanes wait for it
@@ -725,7 +776,7 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         atp::GemmProblem p = fwd_problem(L, static_cast<const uint16_t*>(A_in[L]) + r0 * lda_in[L],
                                          lda_in[L], own + r0 * io->ldp[L], io->ldp[L], false,
                                          atp::EPI_NONE, mc);
-        ATP_CHECK(run_gemm(p, s));
+        ATP_CHECK(run_nt_partial(p, slab, s));
         hipEvent_t e = ev_gemm[L * chunks + c];
         HIP_CHECK(hipEventRecord(e, s), "hipEventRecord");
         HIP_CHECK(hipStreamWaitEvent(S.ms, e, 0), "hipStreamWaitEvent");
@@ -825,6 +876,7 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     uint16_t* xt[3] = {nullptr, nullptr, nullptr};
     uint16_t* dyt[4] = {nullptr, nullptr, nullptr, nullptr};
     int xt_lane[3] = {-1, -1, -1};
+    float* slab = nullptr;
     if (nt) {
         Carver c{static_cast<char*>(workspace)};
         const size_t t2 = (size_t)tokens * 2;
@@ -832,6 +884,7 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         xt[1] = c.take(P.g[1].k_loc * t2);
         xt[2] = c.take(P.g[3].k_loc * t2);
         for (int L = 0; L < 4; ++L) dyt[L] = c.take(P.g[L].n_loc * t2);
+        slab = reinterpret_cast<float*>(c.take(slab_bytes(P, tokens, true)));
     }
 
     const int64_t mc = tokens / chunks;
@@ -882,7 +935,7 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
             atp::LAYOUT_NT, static_cast<const uint16_t*>(dY[L]) + r0 * ld_dy[L], ld_dy[L],
             w->w[L], w->ldw[L], own + r0 * io->ld_dxp[L], io->ld_dxp[L], false, atp::EPI_NONE,
             mc, g.k_loc, g.n_loc);
-        ATP_CHECK(run_gemm(p, s));
+        ATP_CHECK(run_nt_partial(p, slab, s));
         hipEvent_t e = ev_gemm[L * chunks + c];
         HIP_CHECK(hipEventRecord(e, s), "hipEventRecord");
         HIP_CHECK(hipStreamWaitEvent(S.ms, e, 0), "hipStreamWaitEvent");

@@ -135,19 +135,32 @@ struct KArgs {
     uint16_t* pre_out;
     int64_t M, N, K;
     int tiles_m, tiles_n;
+    // split-K (NT kernel): split s covers k in [s*ksplit, min(K, (s+1)*ksplit))
+    // and writes C + s*c_split (an fp32 slab per split); splits == 1: plain
+    int splits;
+    int64_t ksplit, c_split;
 };
 
-template <int GM = GROUP_M>
-__device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
+// Workgroup -> logical tile index: the dispatcher deals workgroups
+// round-robin over the XCDs, so consecutive logical indices are made to land
+// on one XCD.
+__device__ __forceinline__ int xcd_logical() {
     const int G = gridDim.x;
     const int pid = blockIdx.x;
     const int xcd = pid % NUM_XCD;
     const int idx = pid / NUM_XCD;
     const int per = G / NUM_XCD;
     const int rem = G % NUM_XCD;
-    int logical = (xcd < rem) ? xcd * (per + 1) + idx
-                              : rem * (per + 1) + (xcd - rem) * per + idx;
-    if (!ATP_GEMM_XCD_REMAP) logical = pid;
+    const int logical = (xcd < rem) ? xcd * (per + 1) + idx
+                                    : rem * (per + 1) + (xcd - rem) * per + idx;
+    return ATP_GEMM_XCD_REMAP ? logical : pid;
+}
+
+// Logical tile index -> (row tile, column tile), sweeping groups of GM row
+// tiles column by column.
+template <int GM>
+__device__ __forceinline__ void group_coords(int logical, int tiles_m, int tiles_n, int& tm,
+                                             int& tn) {
     const int in_group = GM * tiles_n;
     const int group = logical / in_group;
     const int first_m = group * GM;
@@ -155,6 +168,11 @@ __device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, i
     const int r = logical % in_group;
     tm = first_m + r % gsize;
     tn = r / gsize;
+}
+
+template <int GM = GROUP_M>
+__device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
+    group_coords<GM>(xcd_logical(), tiles_m, tiles_n, tm, tn);
 }
 
 // ---------------------------------------------------------------------------
@@ -573,14 +591,21 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const bool grpB = wave >= 4;
     const int wm = wave / WGN, wn = wave % WGN;
+    // logical index -> (split, tile); the splits of one tile share no data,
+    // so the tiles of one split stay together on an XCD
+    const int ntiles = a.tiles_m * a.tiles_n;
+    const int logical = xcd_logical();
+    const int split = logical / ntiles;
     int tm, tn;
-    tile_coords<C::GROUP>(a.tiles_m, a.tiles_n, tm, tn);
+    group_coords<C::GROUP>(logical - split * ntiles, a.tiles_m, a.tiles_n, tm, tn);
     const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+    const int64_t kb = (int64_t)split * a.ksplit;
+    const int64_t kn = min(a.K - kb, a.ksplit);    // this split's contraction
 
     Copy<BM> ca;
     Copy<BN> cb;
-    ca.init(a.A, a.lda, m0, a.M, a.K, wave, lane);
-    cb.init(a.B, a.ldb, n0, a.N, a.K, wave, lane);
+    ca.init(a.A + kb, a.lda, m0, a.M, kn, wave, lane);
+    cb.init(a.B + kb, a.ldb, n0, a.N, kn, wave, lane);
     constexpr int LA = Copy<BM>::PER, LB = Copy<BN>::PER;
     const int loads = ca.nmine + cb.nmine;   // copy instructions per step (wave-uniform)
 
@@ -590,7 +615,7 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int nk = (int)((a.K + BK - 1) / BK);
+    const int nk = (int)((kn + BK - 1) / BK);
     auto issue_step = [&](int q) {
         uint16_t* dst = smem + (q % STAGES) * STAGE;
         ca.issue(dst, (int64_t)q * BK, wave);
@@ -650,6 +675,8 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
 
     // Epilogue.  Lane holds C(m = base_m + lane%16, n = base_n + 4*(lane/16) + 0..3)
     // in acc[i][j][0..3].
+    KArgs o = a;
+    if (split) o.C = static_cast<float*>(a.C) + split * a.c_split;
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
         const int64_t m = m0 + wm * WM + i * MF + (lane & 15);
@@ -659,7 +686,7 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
             const int64_t n = n0 + wn * WN + j * MF + 4 * (lane >> 4);
             if (n >= a.N) continue;
             float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-            epilogue_store<EPI, OUT_BF16>(a, m, n, v);
+            epilogue_store<EPI, OUT_BF16>(o, m, n, v);
         }
     }
 }
@@ -684,6 +711,9 @@ KArgs kargs(const GemmProblem& p, int bm, int bn) {
     a.K = p.K;
     a.tiles_m = (int)((p.M + bm - 1) / bm);
     a.tiles_n = (int)((p.N + bn - 1) / bn);
+    a.splits = p.splits > 1 ? p.splits : 1;
+    a.ksplit = a.splits > 1 ? p.ksplit : p.K;
+    a.c_split = p.c_split;
     return a;
 }
 
@@ -697,10 +727,44 @@ bool nt_use_256(const GemmProblem& p) {
     return p.K <= 8192 && tiles * 10 >= waves * kCUs * 9;
 }
 
+// Split-K plan of an NT product written to fp32: the S in 1..kMaxSplits
+// that minimises a two-term cost model, (rounds of 256 concurrent 256 x 160
+// tiles) x (k per split) x (flops per k per tile), plus the fp32 slab
+// traffic of the splits (each written once and read once by the combining
+// pass) counted at equal per-CU flop and chip byte rates (about 4 TFLOP/s
+// per CU against about 4 TB/s).  Splits are taken only when the grid stays
+// within kMaxSplitTiles workgroups, every split covers at least 256 k in
+// whole 64-k steps, and the model gains at least 15%.
+int pick_splits(int64_t M, int64_t N, int64_t K, int64_t* ksplit) {
+    constexpr int64_t kCUs = 256;
+    const int64_t tiles = ((M + nt::BM - 1) / nt::BM) * ((N + 159) / 160);
+    const double flops_per_k = 2.0 * nt::BM * 160;
+    int best = 1;
+    double best_cost = (double)((tiles + kCUs - 1) / kCUs) * K * flops_per_k;
+    const double plain = best_cost;
+    *ksplit = K;
+    for (int S = 2; S <= kMaxSplits; ++S) {
+        const int64_t ks = ((K + S - 1) / S + 63) / 64 * 64;
+        if (ks < 256 || (K + ks - 1) / ks != S || tiles * S > kMaxSplitTiles) continue;
+        const double cost = (double)((tiles * S + kCUs - 1) / kCUs) * ks * flops_per_k +
+                            8.0 * S * (double)M * (double)N;
+        if (cost < best_cost) {
+            best = S;
+            best_cost = cost;
+            *ksplit = ks;
+        }
+    }
+    if (best > 1 && best_cost > 0.85 * plain) {
+        best = 1;
+        *ksplit = K;
+    }
+    return best;
+}
+
 template <class C, int EPI, bool OUT_BF16>
 hipError_t launch_nt_cfg(const GemmProblem& p, hipStream_t s) {
     const KArgs a = kargs(p, nt::BM, C::BN);
-    const int grid = a.tiles_m * a.tiles_n;
+    const int grid = a.tiles_m * a.tiles_n * a.splits;
     if (grid == 0) return hipSuccess;
     hipLaunchKernelGGL((gemm_nt_kernel<C, EPI, OUT_BF16>), dim3(grid), dim3(nt::NT), 0, s, a);
     return hipGetLastError();
@@ -708,6 +772,7 @@ hipError_t launch_nt_cfg(const GemmProblem& p, hipStream_t s) {
 
 template <int EPI, bool OUT_BF16>
 hipError_t launch_nt(const GemmProblem& p, hipStream_t s) {
+    if (p.splits > 1) return launch_nt_cfg<nt::Tile160, EPI, OUT_BF16>(p, s);
     return nt_use_256(p) ? launch_nt_cfg<nt::Tile256, EPI, OUT_BF16>(p, s)
                          : launch_nt_cfg<nt::Tile160, EPI, OUT_BF16>(p, s);
 }
@@ -729,6 +794,9 @@ hipError_t launch_t(const GemmProblem& p, hipStream_t s) {
     a.K = p.K;
     a.tiles_m = (int)((p.M + CFG_BM - 1) / CFG_BM);
     a.tiles_n = (int)((p.N + CFG_BN - 1) / CFG_BN);
+    a.splits = 1;
+    a.ksplit = p.K;
+    a.c_split = 0;
     const int grid = a.tiles_m * a.tiles_n;
     if (grid == 0) return hipSuccess;
     hipLaunchKernelGGL((gemm_kernel<CFG_BM, CFG_BN, CFG_BK, CFG_STAGES, CFG_WGM, CFG_WGN, A_K,
@@ -756,10 +824,14 @@ bool gemm_supported(int layout, int epi, bool out_bf16) {
 const char* gemm_kernel_name(const GemmProblem& p) {
     switch (p.layout) {
     case LAYOUT_NN: return "gemm_nn";
-    case LAYOUT_NT: return nt_use_256(p) ? "gemm_nt256" : "gemm_nt";
+    case LAYOUT_NT: return p.splits > 1 ? "gemm_nt_splitk" : nt_use_256(p) ? "gemm_nt256" : "gemm_nt";
     case LAYOUT_TN: return "gemm_tn";
     default: return "gemm_?";
     }
+}
+
+int nt_split_plan(int64_t M, int64_t N, int64_t K, int64_t* ksplit) {
+    return pick_splits(M, N, K, ksplit);
 }
 
 hipError_t launch_gemm(const GemmProblem& p, hipStream_t s) {
@@ -769,6 +841,13 @@ hipError_t launch_gemm(const GemmProblem& p, hipStream_t s) {
                          (p.lda > p.ldb ? p.lda : p.ldb) * 2;
     if (span > 0x7fffff00) return hipErrorInvalidValue;
     const bool b16 = p.out_bf16;
+    if (p.splits > 1) {
+        // split-K: NT, plain fp32 outputs, whole K steps per split, every split
+        // non-empty
+        if (p.layout != LAYOUT_NT || p.epi != EPI_NONE || b16 || p.ksplit <= 0 ||
+            p.ksplit % 64 || (int64_t)(p.splits - 1) * p.ksplit >= p.K || p.c_split < p.M * p.ldc)
+            return hipErrorInvalidValue;
+    }
     switch (p.layout) {
     case LAYOUT_NN:
         switch (p.epi) {

@@ -27,6 +27,11 @@ struct GemmProblem {
     const void* pre_in;           // bf16 [M, N] (ld ldc) for GELU_BWD
     void* pre_out;                // bf16 [M, N] (ld ldc) for BIAS_GELU, nullable
     int64_t M, N, K;
+    // split-K (NT, EPI_NONE, fp32 only): split s sums k in [s*ksplit,
+    // min(K, (s+1)*ksplit)) into the fp32 slab C + s*c_split (ld ldc);
+    // ksplit a multiple of 64, every split non-empty
+    int splits = 1;
+    int64_t ksplit = 0, c_split = 0;
 };
 
 // True if the kernel set has an instance for this (layout, epi, out) combination.
@@ -34,6 +39,14 @@ bool gemm_supported(int layout, int epi, bool out_bf16);
 hipError_t launch_gemm(const GemmProblem& p, hipStream_t s);
 // Profiling name of the kernel a problem launches (layout and tile configuration).
 const char* gemm_kernel_name(const GemmProblem& p);
+
+// Split-K plan for an NT product [M, N] over K written to fp32: returns the
+// split count S (1: no split) and the k per split (a multiple of 64; the
+// last split may be shorter).  The plan depends on M, N and K only; S *
+// (256-row tiles) * (160-column tiles) never exceeds kMaxSplitTiles.
+constexpr int kMaxSplits = 16;
+constexpr int64_t kMaxSplitTiles = 512;
+int nt_split_plan(int64_t M, int64_t N, int64_t K, int64_t* ksplit);
 
 constexpr int kMaxParts = 64;
 
@@ -49,6 +62,12 @@ struct ReduceProblem {
     void* pre_out;                  // bf16, ld ldo, nullable
 };
 hipError_t launch_reduce(const ReduceProblem& p, hipStream_t s);
+
+// out[r*ldo + c] = sum_{s<S} slab_s[r*ld + c] for slab_s = ws + s*stride,
+// r < rows, c < cols (fp32, summed in s order): the split-K partials of one
+// product combined into one partial.
+hipError_t launch_split_sum(const float* ws, int S, int64_t stride, int64_t ld, int64_t rows,
+                            int64_t cols, float* out, int64_t ldo, hipStream_t s);
 
 // db[n] = sum_t dy[t*ld + n], dy bf16 [T, N], db f32 [N]; fixed summation order.
 hipError_t launch_colsum(const void* dy, int64_t ld, int64_t T, int64_t N, float* db,

@@ -201,6 +201,26 @@ hipError_t launch_reduce(const ReduceProblem& p, hipStream_t s) {
     }
 }
 
+// The split slabs are parts of a reduction whose rows start at 0: the
+// reduction kernel adds them in slab order.
+hipError_t launch_split_sum(const float* ws, int S, int64_t stride, int64_t ld, int64_t rows,
+                            int64_t cols, float* out, int64_t ldo, hipStream_t s) {
+    if (S < 1 || S > kMaxParts || (cols & 7) || (ld & 3) || (ldo & 3))
+        return hipErrorInvalidValue;
+    ReduceProblem p{};
+    p.nparts = S;
+    for (int i = 0; i < S; ++i) p.parts[i] = ws + i * stride;
+    p.ldp = ld;
+    p.row0 = 0;
+    p.rows = rows;
+    p.ncols = cols;
+    p.epi = EPI_NONE;
+    p.out = out;
+    p.ldo = ldo;
+    p.out_bf16 = false;
+    return launch_reduce(p, s);
+}
+
 hipError_t launch_colsum(const void* dy, int64_t ld, int64_t T, int64_t N, float* db,
                          hipStream_t s) {
     if (N <= 0) return hipSuccess;

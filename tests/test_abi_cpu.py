@@ -206,17 +206,29 @@ def test_status_strings():
 
 def test_block_workspace_bytes_formula():
     # forward: W^T of the four shards; backward: X^T of x, attention block, H
-    # and dY^T of the four linears over the tokens; pieces rounded to 256 B
+    # and dY^T of the four linears over the tokens; pieces rounded to 256 B.
+    # Each side adds the fp32 split-K slabs of its chunk products, at most
+    # 512 tiles of 256 x 160 fp32 values, sized for the largest plan over every
+    # chunk count (a 64-chunk split of the 8 x 1 wide layer splits, 8 chunks
+    # do not); none without tokens
     r = lambda b: (b + 255) // 256 * 256  # noqa: E731
-    for (d1, d2), mode, T, h in [((8, 1), 0, 4096, 20480), ((2, 4), 1, 8192, 4096),
-                                 ((2, 2), 0, 132, 512), ((1, 1), 0, 0, 256)]:
+    slab_max = 512 * 256 * 160 * 4
+    for (d1, d2), mode, T, h, splits in [((8, 1), 0, 4096, 20480, True),
+                                         ((2, 4), 1, 8192, 4096, True),
+                                         ((2, 2), 0, 132, 512, True), ((1, 1), 0, 0, 256, False)]:
         m = B.mesh(d1, d2, 0, 0)
         G = B.block_geometry(m, mode, h)
         fwd = sum(r(g.k_loc * g.n_loc * 2) for g in G)
         bwd = (r(G[0].k_loc * T * 2) + r(G[1].k_loc * T * 2) + r(G[3].k_loc * T * 2) +
                sum(r(g.n_loc * T * 2) for g in G))
-        for chunks in (1, 2, 4):
-            assert B.atp_block_workspace_bytes(m, mode, T, h, chunks) == max(fwd, bwd)
+        sizes = {B.atp_block_workspace_bytes(m, mode, T, h, c) for c in (1, 2, 4)}
+        assert len(sizes) == 1, sizes          # the chunk count does not change it
+        ws = sizes.pop()
+        assert ws % 256 == 0
+        if splits:
+            assert max(fwd, bwd) < ws <= max(fwd, bwd) + slab_max
+        else:
+            assert ws == max(fwd, bwd)
     # invalid arguments give 0
     assert B.atp_block_workspace_bytes(B.mesh(2, 2, 0, 0), 7, 128, 512, 1) == 0
     assert B.atp_block_workspace_bytes(B.mesh(2, 2, 0, 0), 0, 128, 500, 1) == 0

@@ -7,7 +7,9 @@ backward) with chunk-based overlapping (Sec. 4.1).
   the true partials of its group members; the reduced blocks must equal the
   unsharded layer (the spec invariant) and be identical bit for bit
   across each reduction group.
-* chunking, stream overlap and the ROW/COL transposition never change a bit.
+* chunking, stream overlap and the ROW/COL transposition never change a bit
+  (on the workspace path chunking keeps the bits while every chunk product
+  keeps its split-K plan, as it does for the shapes here).
 * full-size workloads are checked on sampled token rows (rows are
   independent in every step) and, for dW, on sampled columns.
 """

@@ -2,12 +2,15 @@
 with a workspace (every product in the NT layout) against the same calls
 without one (NN forward, TN dW).
 
-The input-gradient products are NT in both paths and must agree bit for bit.
 The forward and dW products use different kernels (16x16x32 MFMAs in the NT
-kernel, 32x32x16 in the NN / TN kernel), which sum each element's products in
-a different order: they agree to fp32 rounding, and a bf16 output differs by
-at most one unit in the last place where the two fp32 values straddle a
-rounding boundary.  Both paths are checked against the oracle elsewhere."""
+kernel, 32x32x16 in the NN / TN kernel), and the chunked products that feed a
+reduction may be split over their contraction on the transposed path only:
+each element's products are summed in a different order, so the paths agree
+to fp32 rounding, and a bf16 output differs by at most one unit in the last
+place where the two fp32 values straddle a rounding boundary.  fc1's dW and
+db are token sums of the bf16 dh_pre, which may sit one unit apart between
+the paths, so they get a looser bound.  Both paths are checked against the
+oracle elsewhere."""
 import pytest
 import torch
 
@@ -23,19 +26,24 @@ def bits(t):
     return t.contiguous().view(torch.int16 if t.element_size() == 2 else torch.int32)
 
 
-def assert_paths_agree(a, b, what):
+def assert_paths_agree(a, b, what, rel=1e-4):
     """Two summation orders of the same fp32-accumulated products."""
     if a.dtype == torch.bfloat16:
-        ia, ib = bits(a).to(torch.int32), bits(b).to(torch.int32)
-        ulps = (ia - ib).abs()     # bf16 bit patterns of equal sign differ by ulps
-        assert int(ulps.max()) <= 2, f"{what}: bf16 outputs {int(ulps.max())} ulps apart"
-        frac = float((ulps != 0).float().mean())
+        # two units in the last place of the larger value (bf16 keeps 8
+        # significant bits), plus the fp32 sums' rounding on the tensor's scale
+        # for values that come out of cancellation near zero
+        fa, fb = a.double(), b.double()
+        scale = float(fa.abs().max()) + 1e-30
+        bound = 2.0 ** -6 * torch.maximum(fa.abs(), fb.abs()) + rel * scale
+        excess = float(((fa - fb).abs() - bound).max())
+        assert excess <= 0, f"{what}: bf16 outputs differ beyond two units in the last place"
+        frac = float((bits(a) != bits(b)).float().mean())
         assert frac < 0.05, f"{what}: {frac:.3%} of bf16 outputs differ"
     else:
         fa, fb = a.double(), b.double()
         scale = float(fa.abs().max()) + 1e-30
         err = float((fa - fb).abs().max())
-        assert err <= 1e-4 * scale, f"{what}: max diff {err:.3e} vs scale {scale:.3e}"
+        assert err <= rel * scale, f"{what}: max diff {err:.3e} vs scale {scale:.3e}"
 
 
 @pytest.mark.parametrize("rows,cols,pad_s,pad_d", [
@@ -98,11 +106,16 @@ def test_block_backward_transposed_equals_direct(case, aux):
     a = run_block_bwd(inp, chunks, aux=aux)
     b = run_block_bwd(inp, chunks, aux=aux, workspace=True)
     torch.cuda.synchronize()
+    _check_bwd_paths(a, b)
+
+
+def _check_bwd_paths(a, b):
     for k in ("dh_pre", "dx_qkv", "dx_fc1", "d_attn"):
-        assert torch.equal(bits(a[k]), bits(b[k])), k
+        assert_paths_agree(a[k], b[k], k)
     for i in range(4):
-        assert_paths_agree(a["dw"][i], b["dw"][i], f"dw {i}")
-        assert torch.equal(bits(a["db"][i]), bits(b["db"][i])), f"db {i}"
+        rel = 2e-3 if i == 2 else 1e-4
+        assert_paths_agree(a["dw"][i], b["dw"][i], f"dw {i}", rel)
+        assert_paths_agree(a["db"][i], b["db"][i], f"db {i}", rel)
 
 
 def test_benchmark_workload_transposed_equals_direct():
@@ -117,7 +130,4 @@ def test_benchmark_workload_transposed_equals_direct():
     torch.cuda.synchronize()
     for k in ("qkv", "o", "h", "pre", "z"):
         assert_paths_agree(fa[k], fb[k], k)
-    for k in ("dh_pre", "dx_qkv", "dx_fc1", "d_attn"):
-        assert torch.equal(bits(ba[k]), bits(bb[k])), k
-    for i in range(4):
-        assert_paths_agree(ba["dw"][i], bb["dw"][i], f"dw {i}")
+    _check_bwd_paths(ba, bb)
