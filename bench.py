@@ -46,9 +46,7 @@ def parse():
     ap.add_argument("--serial", action="store_true",
                     help="run reductions on the compute stream (no overlap)")
     ap.add_argument("--no-workspace", action="store_true",
-                    help="no workspace: forward reads W directly (NN), dW reads X, dY (TN)")
-    ap.add_argument("--no-aux", action="store_true",
-                    help="no second compute stream (independent GEMMs do not share the chip)")
+                    help="no workspace: chunk products are never split over k")
     ap.add_argument("--graph", action="store_true",
                     help="replay the step as a captured HIP graph (measured slower than "
                          "launching it: the replay loses part of the reduce/GEMM overlap)")
@@ -114,9 +112,8 @@ def step_flops(st, fwd_only):
     return f if fwd_only else 3.0 * f
 
 
-def make_step(torch, atp, st, fwd_only, serial, aux):
+def make_step(torch, atp, st, fwd_only, serial):
     ms = None if serial else torch.cuda.Stream()
-    ax = torch.cuda.Stream() if (aux and not serial) else None
 
     def step():
         # the stream current at call time (the capture stream inside a graph)
@@ -125,14 +122,14 @@ def make_step(torch, atp, st, fwd_only, serial, aux):
         atp.atp_block_fwd(st["m"], st["bm"], st["T"], st["h"], st["chunks"], st["w"], st["b"],
                           st["x"], st["a"], st["fwd_tabs"], st["qkv"], st["o"], st["hh"],
                           st["pre"], st["z"], workspace=st["ws"], compute_stream=cs,
-                          comm_stream=ms_, aux_stream=ax)
+                          comm_stream=ms_)
         if fwd_only:
             return
         atp.atp_block_bwd(st["m"], st["bm"], st["T"], st["h"], st["chunks"], st["w"], st["b"],
                           st["x"], st["a"], st["hh"], st["pre"], st["dz"], st["dqkv"], st["do"],
                           st["bwd_tabs"], st["dh_pre"], st["dx_qkv"], st["dx_fc1"],
                           st["d_attn"], st["dw"], st["db"], workspace=st["ws"], compute_stream=cs,
-                          comm_stream=ms_, aux_stream=ax)
+                          comm_stream=ms_)
     return step
 
 
@@ -272,7 +269,7 @@ def main():
         nb = atp.atp_block_workspace_bytes(st["m"], st["bm"], st["T"], st["h"], chunks)
         st["ws"] = torch.empty(max(nb, 1), dtype=torch.uint8, device="cuda:0")
     torch.cuda.synchronize()
-    step = make_step(torch, atp, st, fwd_only, args.serial, not args.no_aux)
+    step = make_step(torch, atp, st, fwd_only, args.serial)
     flops = step_flops(st, fwd_only)
 
     for _ in range(args.warmup):
@@ -341,7 +338,7 @@ def main():
     if not args.serial:
         # the same launches with nothing beside them: one more pass of the
         # step with every launch serialized on the compute stream
-        solo = make_step(torch, atp, st, fwd_only, True, False)
+        solo = make_step(torch, atp, st, fwd_only, True)
         atp.atp_profile_enable(True)
         for _ in range(args.steps):
             solo()
@@ -408,8 +405,7 @@ def main():
         config=dict(workload=args.workload, mode=wl["mode"], mesh=[d1, d2], coord=[0, 0],
                     tokens=wl["tokens"], h=wl["h"], chunks=chunks,
                     **{"pass": "fwd" if fwd_only else "fwd+bwd"},
-                    serial=bool(args.serial), aux_stream=not args.no_aux,
-                    transposed_layout=not args.no_workspace,
+                    serial=bool(args.serial), workspace=not args.no_workspace,
                     hip_graph=bool(args.graph and not args.no_workspace),
                     gflop_per_step=round(flops / 1e9, 1)),
         step_ms=step_ms, mfma_util=round(value / PEAK_BF16_TFLOPS, 4),

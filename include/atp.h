@@ -247,26 +247,25 @@ atp_status atp_transpose_bf16(int64_t rows, int64_t cols, const void* src, int64
  * chunk's reduction runs on comm_stream as soon as that chunk's partial is
  * written; fc2's chunk c waits for fc1's reduced chunk c.  A group of one
  * needs no reduction: its bias (and GeLU) are applied in the GEMM epilogue
- * and it runs as one launch.
+ * and it runs as one launch.  Every GEMM runs on compute_stream, in the order
+ * out-proj, fc1, QKV, fc2; aux_stream is accepted for compatibility and not
+ * used (may be NULL).  With comm_stream == compute_stream nothing overlaps.
  * workspace (nullable, 256-byte aligned): when ws_bytes is at least the
  * forward's need (see atp_block_workspace_bytes) the call first writes W^T
- * of each shard there and runs every product in the GEMM's NT layout, all on
- * compute_stream in the order out-proj, fc1, QKV, fc2 (aux_stream unused); a
- * chunk product with too few output tiles to fill the chip is split over its
- * contraction, the splits' fp32 slabs summed in split order into the own
- * partial before the chunk's reduction reads it.  Without the workspace the
- * call reads W directly, issues fc1, out-proj, QKV, fc2, and aux_stream
- * (nullable) is a second compute stream: each GEMM goes to whichever of
- * compute_stream and aux_stream has less work issued so far (in FLOPs), with
- * events for the data dependencies.  With comm_stream == compute_stream
- * nothing overlaps.  The two paths sum each element's products in different
- * orders (they agree to fp32 rounding); on either path the results do not
- * depend on the streams used, and are the same for every chunk count that
- * gives each chunk product the same split plan (on the direct path: every
- * chunk count).  compute_stream's earlier work happens before the block's,
- * and on return compute_stream is ordered after all of it; the workspace
- * may be reused once compute_stream reaches that point.  The direct path
- * refuses a compute_stream under HIP graph capture (UNSUPPORTED). */
+ * of each shard there and runs every product from it (both operands
+ * contiguous along k, the faster layout), and a chunk product with too few
+ * output tiles to fill the chip is split over its contraction, the splits'
+ * fp32 slabs summed in split order into the own partial before the chunk's
+ * reduction reads it.  Without the workspace the products read W directly.
+ * Both layouts sum each element's products in the same order: the paths
+ * give the same bits except where a product splits (then they agree to
+ * fp32 rounding).  Results do not depend on the streams used, and are the
+ * same for every chunk count that gives each chunk product the same split
+ * plan (without a workspace: every chunk count).  compute_stream's earlier
+ * work happens before the block's, and on return compute_stream is ordered
+ * after all of it; the workspace may be reused once compute_stream reaches
+ * that point.  Without a workspace the call refuses a compute_stream under
+ * HIP graph capture (UNSUPPORTED). */
 atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
                          int32_t chunks, const atp_block_weights* w,
                          const atp_block_fwd_io* io, void* workspace, size_t ws_bytes,
@@ -275,16 +274,17 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
 /* One device's backward share of the layer (Sec. 4.2): dX = dY W^T per
  * linear, chunked and reduced on comm_stream where its group has more than
  * one member, dW = X^T dY and db = column sums of dY; fc1's dY is fc2's
- * reduced dX times GeLU'(pre).  Issue order: fc2's dX (fc1 waits for it),
- * QKV's and out-proj's dX, fc1's dX, then the four dW largest first, each
- * GEMM on the less loaded of compute_stream and aux_stream (as in
- * atp_block_fwd), so the dX reductions overlap the later GEMMs.
+ * reduced dX times GeLU'(pre).  Issue order on compute_stream: fc2's dX
+ * (fc1 waits for it), QKV's and out-proj's dX, fc1's dX, then the four dW
+ * largest first, so the dX reductions overlap the later GEMMs; aux_stream
+ * is not used (as in atp_block_fwd).
  * workspace: when ws_bytes is at least the backward's need and tokens % 8
- * == 0, X^T and dY^T are written there, every dW runs in the NT layout, all
- * GEMMs run on compute_stream, and the chunked dX products are split over
- * their contraction as in atp_block_fwd; otherwise dW reads X and dY
- * directly.  The paths agree to fp32 rounding (as in atp_block_fwd).  On
- * return compute_stream is ordered after all work. */
+ * == 0, X^T and dY^T are written there and every dW runs from them, and the
+ * chunked dX products are split over their contraction as in atp_block_fwd;
+ * otherwise dW reads X and dY directly.  The paths give the same bits except
+ * where a product splits (as in atp_block_fwd).  On return compute_stream is
+ * ordered after all work.  Without a workspace the call refuses a
+ * compute_stream under HIP graph capture (UNSUPPORTED). */
 atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
                          int32_t chunks, const atp_block_weights* w,
                          const atp_block_bwd_io* io, void* workspace, size_t ws_bytes,

@@ -312,10 +312,12 @@ atp_status block_plan(const atp_mesh* m, int32_t bm, int64_t h, BlockPlan* p) {
     return ATP_OK;
 }
 
-// Workspace of the all-NT block path.  The forward keeps W^T of the four
-// linears ([n_loc][k_loc]); the backward keeps X^T of x (shared by QKV and
-// fc1), the attention block and H, and dY^T of the four linears, each
-// [cols][tokens].  Pieces are 256-byte aligned.
+// Workspace of the block calls.  The forward keeps W^T of the four linears
+// ([n_loc][k_loc]); the backward keeps X^T of x (shared by QKV and fc1), the
+// attention block and H, and dY^T of the four linears, each [cols][tokens]:
+// with them every product runs with both operands contiguous along k, the
+// layout the GEMM kernel streams fastest.  Each side adds the split-K slabs
+// of its chunk products.  Pieces are 256-byte aligned.
 constexpr size_t kWsAlign = 256;
 size_t ws_round(size_t b) { return (b + kWsAlign - 1) / kWsAlign * kWsAlign; }
 
@@ -355,8 +357,8 @@ size_t ws_bwd_bytes(const BlockPlan& P, int64_t tokens) {
     return b;
 }
 
-// An fp32 product [M, N] over K on the NT path: split over K into `slab`
-// when the plan says so, the splits then summed in split order into C.
+// An fp32 product [M, N] over K: split over K into `slab` when a slab is
+// given and the plan says so, the splits then summed in split order into C.
 atp_status run_nt_partial(atp::GemmProblem p, float* slab, hipStream_t s) {
     int64_t ks = 0;
     const int S = slab ? atp::nt_split_plan(p.M, p.N, p.K, &ks) : 1;
@@ -405,63 +407,48 @@ atp_status check_group(float* const* tab, int32_t size, int64_t rows, int64_t ld
 
 const char* const kLinearName[4] = {"qkv", "out", "fc1", "fc2"};
 
-// The block's streams: the compute stream (cs), the comm stream (ms) that
-// runs the chunk reductions, and an optional auxiliary compute stream (ax).
-// GEMMs are issued in dependency order and each goes to the compute lane
-// (0 = cs, 1 = ax) with less work issued to it so far, counted in FLOPs, so
-// the two lanes stay busy side by side and one lane's tail wave shares the
-// chip with the other lane's work.  Without an auxiliary stream everything
-// computes on cs, in issue order.
+// The block's streams: the compute stream (cs), on which every GEMM, split
+// sum and column sum runs in issue order, and the comm stream (ms) that runs
+// the chunk reductions.  The GEMM kernel's tiles fill the chip by
+// themselves (a 512-row chunk is one tile per CU), so a kernel beside one
+// delays its last tiles (measured: a second GEMM stream, or transposes and
+// column sums beside the GEMMs, made the step 3-6% slower); only the
+// reductions, which overlap by design, run beside them.
 struct Streams {
-    hipStream_t cs, ms, ax;
-    bool two;
-    bool gemm_one_lane = false;   // every kernel of the block on cs (ax unused)
-    double load[2] = {0.0, 0.0};
-    Streams(void* c, void* m, void* a)
-        : cs(static_cast<hipStream_t>(c)), ms(static_cast<hipStream_t>(m)),
-          ax(a ? static_cast<hipStream_t>(a) : static_cast<hipStream_t>(c)),
-          two(a != nullptr && a != c) {}
-    hipStream_t lane(int i) const { return i ? ax : cs; }
-    // the lane of the next GEMM: cs when GEMMs keep to one lane, else the
-    // less loaded lane (ties go to cs), charged with `flops`
-    int take(double flops) {
-        const int i = (!gemm_one_lane && two && load[1] < load[0]) ? 1 : 0;
-        load[i] += flops;
-        return i;
-    }
+    hipStream_t cs, ms;
+    Streams(void* c, void* m) : cs(static_cast<hipStream_t>(c)), ms(static_cast<hipStream_t>(m)) {}
+    hipStream_t lane(int) const { return cs; }
+    int take(double) const { return 0; }
 
     // everything already queued on cs happens before the block's work
     atp_status begin(hipEvent_t start) const {
         HIP_CHECK(hipEventRecord(start, cs), "hipEventRecord");
         if (ms != cs) HIP_CHECK(hipStreamWaitEvent(ms, start, 0), "hipStreamWaitEvent");
-        if (two) HIP_CHECK(hipStreamWaitEvent(ax, start, 0), "hipStreamWaitEvent");
         return ATP_OK;
     }
-    // cs is ordered after all of the block's work on ms and ax
-    atp_status end(hipEvent_t ms_end, hipEvent_t ax_end) const {
+    // cs is ordered after all of the block's work on ms
+    atp_status end(hipEvent_t ms_end) const {
         if (ms != cs) {
             HIP_CHECK(hipEventRecord(ms_end, ms), "hipEventRecord");
             HIP_CHECK(hipStreamWaitEvent(cs, ms_end, 0), "hipStreamWaitEvent");
-        }
-        if (two) {
-            HIP_CHECK(hipEventRecord(ax_end, ax), "hipEventRecord");
-            HIP_CHECK(hipStreamWaitEvent(cs, ax_end, 0), "hipStreamWaitEvent");
         }
         return ATP_OK;
     }
 };
 
-// Capturing the direct path into a HIP graph made hipStreamEndCapture crash
-// inside the runtime (host segmentation fault; the cause is not identified),
-// so that path refuses a capturing compute stream.  The workspace path is
-// captured and replayed bit for bit (tested).
-atp_status refuse_capture_of_direct_path(void* compute_stream) {
+// Capturing a block call without a workspace into a HIP graph once made
+// hipStreamEndCapture crash inside the runtime (a host segmentation fault,
+// at a time when such calls also ran GEMMs on a second stream; the cause was
+// never identified), so a call without a workspace refuses a capturing
+// compute stream.  Calls with a workspace are captured and replayed bit for
+// bit (tested).
+atp_status refuse_capture_without_workspace(void* compute_stream) {
     hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
     HIP_CHECK(hipStreamIsCapturing(static_cast<hipStream_t>(compute_stream), &st),
               "hipStreamIsCapturing");
     if (st != hipStreamCaptureStatusNone)
         return set_error(ATP_ERR_UNSUPPORTED,
-                         "graph capture needs the workspace path (pass a workspace of "
+                         "graph capture needs a workspace (pass one of "
                          "atp_block_workspace_bytes bytes)");
     return ATP_OK;
 }
@@ -670,59 +657,47 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         ATP_CHECK(check_group(io->partials[i], P.g[i].red_size, tokens, io->ldp[i], P.g[i].n_loc, nm));
     }
 
-    // with a large enough workspace every product runs in the NT layout from
-    // a transposed weight copy (W^T is contiguous along k)
-    const bool nt = workspace && ws_bytes >= ws_fwd_bytes(P, tokens);
-    if (nt && reinterpret_cast<uintptr_t>(workspace) % kWsAlign)
+    // with a large enough workspace every forward product runs from a
+    // transposed weight copy (both operands contiguous along k: the layout
+    // the GEMM kernel streams fastest), and chunk products with too few tiles
+    // to fill the chip are split over k into slabs there
+    const bool ws = workspace && ws_bytes >= ws_fwd_bytes(P, tokens);
+    if (workspace && reinterpret_cast<uintptr_t>(workspace) % kWsAlign)
         return set_error(ATP_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kWsAlign);
-    if (!nt) ATP_CHECK(refuse_capture_of_direct_path(compute_stream));
+    if (!workspace) ATP_CHECK(refuse_capture_without_workspace(compute_stream));
 
-    Streams S(compute_stream, comm_stream, aux_stream);
-    // The NT kernel's tiles fill the chip by themselves (a 512-row chunk is
-    // exactly one tile per CU), so any kernel beside one delays its last
-    // tiles (measured: a second GEMM lane, or transposes on the auxiliary
-    // lane, make the step 3-6% slower): on this path every GEMM and every
-    // transpose runs on the compute lane and the auxiliary stream is unused.
-    S.gemm_one_lane = nt;
+    Streams S(compute_stream, comm_stream);
+    (void)aux_stream;   // unused: every GEMM runs on compute_stream
     hipEvent_t* ev = nullptr;
-    // [0] start  [1] comm end  [2] aux end  [3] fc1's single launch done,
-    // then per linear per chunk GEMM-done, then fc1 reduce-done per chunk,
-    // then per linear its W^T done
-    const size_t n_ev = 4 + 4 * (size_t)chunks + (size_t)chunks + 4;
+    // [0] start  [1] comm end  [2] unused  [3] fc1's single launch done,
+    // then per linear per chunk GEMM-done, then fc1 reduce-done per chunk
+    const size_t n_ev = 4 + 4 * (size_t)chunks + (size_t)chunks;
     ATP_CHECK(sync_events(n_ev, &ev));
     hipEvent_t* ev_gemm = ev + 4;
     hipEvent_t* ev_red1 = ev + 4 + 4 * chunks;
-    hipEvent_t* ev_wt = ev + 4 + 5 * chunks;
     ATP_CHECK(S.begin(ev[0]));
 
     uint16_t* wt[4] = {nullptr, nullptr, nullptr, nullptr};
     float* slab = nullptr;
-    int wt_lane[4] = {-1, -1, -1, -1};
-    if (nt) {
+    if (ws) {
         Carver c{static_cast<char*>(workspace)};
         for (int L = 0; L < 4; ++L) wt[L] = c.take((size_t)P.g[L].n_loc * P.g[L].k_loc * 2);
         slab = reinterpret_cast<float*>(c.take(slab_bytes(P, tokens, false)));
     }
-    // W^T of linear L for a GEMM on `lane`: written once, on the lane of the
-    // linear's first GEMM; other lanes wait for it
-    auto need_wt = [&](int L, int lane) -> atp_status {
-        if (!nt) return ATP_OK;
+    // W^T of linear L, written before the linear's first GEMM (same stream)
+    bool wt_done[4] = {false, false, false, false};
+    auto need_wt = [&](int L) -> atp_status {
+        if (!ws || wt_done[L]) return ATP_OK;
         const atp_shard& g = P.g[L];
-        if (wt_lane[L] < 0) {
-            ATP_CHECK(run_transpose(w->w[L], w->ldw[L], g.k_loc, g.n_loc, wt[L], g.k_loc,
-                                    S.lane(lane)));
-            HIP_CHECK(hipEventRecord(ev_wt[L], S.lane(lane)), "hipEventRecord");
-            wt_lane[L] = lane;
-        } else if (wt_lane[L] != lane) {
-            HIP_CHECK(hipStreamWaitEvent(S.lane(lane), ev_wt[L], 0), "hipStreamWaitEvent");
-        }
+        ATP_CHECK(run_transpose(w->w[L], w->ldw[L], g.k_loc, g.n_loc, wt[L], g.k_loc, S.cs));
+        wt_done[L] = true;
         return ATP_OK;
     };
-    // the product X W of linear L: NN from W, or NT from W^T
+    // the product X W of linear L: NT from W^T, or NN from W as given
     auto fwd_problem = [&](int L, const void* A, int64_t lda, void* C, int64_t ldc, bool b16,
                            int epi, int64_t M) {
         const atp_shard& g = P.g[L];
-        if (nt)
+        if (ws)
             return gemm_problem(atp::LAYOUT_NT, A, lda, wt[L], g.k_loc, C, ldc, b16, epi, M,
                                 g.n_loc, g.k_loc);
         return gemm_problem(atp::LAYOUT_NN, A, lda, w->w[L], w->ldw[L], C, ldc, b16, epi, M,
@@ -751,7 +726,7 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         const int lane = S.take(gemm_flops(tokens, g.n_loc, g.k_loc));
         hipStream_t s = S.lane(lane);
         if (L == 3) ATP_CHECK(wait_h(lane, chunks - 1));
-        ATP_CHECK(need_wt(L, lane));
+        ATP_CHECK(need_wt(L));
         atp::GemmProblem p = fwd_problem(L, A_in[L], lda_in[L], outp[L], ldo[L], true,
                                          L == 2 ? atp::EPI_BIAS_GELU : atp::EPI_BIAS, tokens);
         p.bias = w->b[L];
@@ -771,7 +746,7 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         hipStream_t s = S.lane(lane);
         const int64_t r0 = (int64_t)c * mc;
         if (L == 3) ATP_CHECK(wait_h(lane, c));
-        ATP_CHECK(need_wt(L, lane));
+        ATP_CHECK(need_wt(L));
         float* own = io->partials[L][g.red_index];
         atp::GemmProblem p = fwd_problem(L, static_cast<const uint16_t*>(A_in[L]) + r0 * lda_in[L],
                                          lda_in[L], own + r0 * io->ldp[L], io->ldp[L], false,
@@ -793,22 +768,11 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         for (int c = 0; c < chunks; ++c) ATP_CHECK(chunk(L, c));
         return ATP_OK;
     };
-    if (S.gemm_one_lane) {
-        // one lane: out-proj first (its weight is the smallest to transpose
-        // and its reductions start at once), then fc1, QKV, and fc2 behind
-        // fc1's output
-        const int order[4] = {1, 2, 0, 3};
-        for (int L : order) ATP_CHECK(linear(L));
-        return S.end(ev[1], ev[2]);
-    }
-    // fc1 first, since fc2 waits for it; the attention projections fill the
-    // other lane meanwhile (out first, so its reductions start early); fc2
-    // last, chunk by chunk behind fc1's output
-    ATP_CHECK(linear(2));
-    ATP_CHECK(linear(1));
-    ATP_CHECK(linear(0));
-    ATP_CHECK(linear(3));
-    return S.end(ev[1], ev[2]);
+    // out-proj first (its reductions start at once), then fc1, QKV, and fc2
+    // behind fc1's output
+    const int order[4] = {1, 2, 0, 3};
+    for (int L : order) ATP_CHECK(linear(L));
+    return S.end(ev[1]);
 }
 
 atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
@@ -852,32 +816,32 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     }
 
     // with a large enough workspace (and whole 16-byte rows of tokens) dW runs
-    // in the NT layout from X^T and dY^T (both contiguous along the tokens)
-    const bool nt = workspace && ws_bytes >= ws_bwd_bytes(P, tokens) && tokens % 8 == 0;
-    if (nt && reinterpret_cast<uintptr_t>(workspace) % kWsAlign)
+    // from X^T and dY^T (both contiguous along the tokens), and chunked dX
+    // products with too few tiles to fill the chip are split over k into
+    // slabs there
+    const bool ws = workspace && ws_bytes >= ws_bwd_bytes(P, tokens) && tokens % 8 == 0;
+    if (workspace && reinterpret_cast<uintptr_t>(workspace) % kWsAlign)
         return set_error(ATP_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kWsAlign);
-    if (!nt) ATP_CHECK(refuse_capture_of_direct_path(compute_stream));
+    if (!workspace) ATP_CHECK(refuse_capture_without_workspace(compute_stream));
 
-    Streams S(compute_stream, comm_stream, aux_stream);
-    S.gemm_one_lane = nt;     // as in the forward: one lane on this path
+    Streams S(compute_stream, comm_stream);
+    (void)aux_stream;   // unused: every GEMM runs on compute_stream
     hipEvent_t* ev = nullptr;
-    // [0] start  [1] comm end  [2] aux end  [3] fc2's single dX launch done,
-    // then per linear per chunk GEMM-done, then fc2 reduce-done per chunk,
-    // then X^T done for x, the attention block and H
-    const size_t n_ev = 4 + 4 * (size_t)chunks + (size_t)chunks + 3;
+    // [0] start  [1] comm end  [2] unused  [3] fc2's single dX launch done,
+    // then per linear per chunk GEMM-done, then fc2 reduce-done per chunk
+    const size_t n_ev = 4 + 4 * (size_t)chunks + (size_t)chunks;
     ATP_CHECK(sync_events(n_ev, &ev));
     hipEvent_t* ev_gemm = ev + 4;
     hipEvent_t* ev_red2 = ev + 4 + 4 * chunks;
-    hipEvent_t* ev_xt = ev + 4 + 5 * chunks;
     ATP_CHECK(S.begin(ev[0]));
 
     // X^T pieces: 0 = x (QKV and fc1), 1 = attention block (out), 2 = H (fc2)
     const int xsrc[4] = {0, 1, 0, 2};
     uint16_t* xt[3] = {nullptr, nullptr, nullptr};
     uint16_t* dyt[4] = {nullptr, nullptr, nullptr, nullptr};
-    int xt_lane[3] = {-1, -1, -1};
+    bool xt_done[3] = {false, false, false};
     float* slab = nullptr;
-    if (nt) {
+    if (ws) {
         Carver c{static_cast<char*>(workspace)};
         const size_t t2 = (size_t)tokens * 2;
         xt[0] = c.take(P.g[0].k_loc * t2);
@@ -960,21 +924,18 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         hipStream_t s = S.lane(lane);
         if (L == 2) ATP_CHECK(wait_dpre(lane, chunks - 1));
         if (io->db[L]) ATP_CHECK(run_colsum(dY[L], ld_dy[L], tokens, g.n_loc, io->db[L], s));
-        if (!nt) {
+        if (!ws) {
             atp::GemmProblem p = gemm_problem(atp::LAYOUT_TN, Xin[L], ldx_in[L], dY[L], ld_dy[L],
                                               io->dw[L], w->ldw[L], false, atp::EPI_NONE,
                                               g.k_loc, g.n_loc, tokens);
             return run_gemm(p, s);
         }
-        // X^T once per source (x serves QKV and fc1, maybe on two lanes), dY^T
-        // on this lane, then dW = X^T dY as an NT product over the tokens
+        // X^T once per source (x serves QKV and fc1), dY^T, then dW = X^T dY
+        // as an NT product over the tokens
         const int xi = xsrc[L];
-        if (xt_lane[xi] < 0) {
+        if (!xt_done[xi]) {
             ATP_CHECK(run_transpose(Xin[L], ldx_in[L], tokens, g.k_loc, xt[xi], tokens, s));
-            HIP_CHECK(hipEventRecord(ev_xt[xi], s), "hipEventRecord");
-            xt_lane[xi] = lane;
-        } else if (xt_lane[xi] != lane) {
-            HIP_CHECK(hipStreamWaitEvent(s, ev_xt[xi], 0), "hipStreamWaitEvent");
+            xt_done[xi] = true;
         }
         ATP_CHECK(run_transpose(dY[L], ld_dy[L], tokens, g.n_loc, dyt[L], tokens, s));
         atp::GemmProblem p = gemm_problem(atp::LAYOUT_NT, xt[xi], tokens, dyt[L], tokens,
@@ -994,7 +955,7 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         return P.g[i].k_loc * P.g[i].n_loc > P.g[j].k_loc * P.g[j].n_loc;
     });
     for (int L : order) ATP_CHECK(dw(L));
-    return S.end(ev[1], ev[2]);
+    return S.end(ev[1]);
 }
 
 void atp_profile_enable(int32_t on) {

@@ -1,90 +1,42 @@
 // bf16 x bf16 -> fp32 MFMA GEMMs for gfx950 (CDNA4) with fused epilogues.
 //
-// Two kernels serve the three products of a shard linear (Sec. 3.2 forward
-// Y = X W; Sec. 4.2 backward dX = dY W^T, dW = X^T dY):
+// One kernel, gemm_nt_kernel, serves the three products of a shard linear
+// (Sec. 3.2 forward Y = X W; Sec. 4.2 backward dX = dY W^T, dW = X^T dY) in
+// each operand layout: an operand is either contiguous along k (X, dY, and
+// W in dX; the transposed copies W^T, X^T, dY^T of the workspace path) or
+// contiguous along its rows (W in the forward, X and dY in dW without a
+// workspace).  The kernel is described below; every layout sums an output
+// element's products in the same order, so the layouts give the same bits.
 //
-//   * gemm_nt_kernel: both operands contiguous along k (C = A B^T).  Every
-//     product of the block runs in this layout when a workspace holds the
-//     transposed copies, so it is the tuned kernel (described below, after
-//     the generic one).
-//   * gemm_kernel: the generic template, any of NN / NT / TN, used for the
-//     forward (NN) and dW (TN) products without a workspace.
-//
-// Generic kernel data path
 //   * Operands go global -> LDS with buffer_load_dwordx4 ... lds (no
 //     register staging).  A buffer resource per operand gives zero fill for
 //     every out-of-range lane (its offset is pushed past num_records), so
 //     ragged M, N and K need no separate path.
-//   * STAGES LDS buffers form a ring: the loads of K-step kt+STAGES-1 are
-//     issued while step kt is multiplied, and a step is consumed after an
-//     explicit vmcnt wait plus one workgroup barrier.
-//   * An operand contiguous along K (X and dY as the M side; W in dX) is
-//     kept [row][k]; an MFMA fragment is one ds_read_b128.  An operand
-//     contiguous along its M/N side (W in the forward, X and dY in dW) is
-//     kept [k][row] and its fragments are read with two ds_read_b64_tr_b16
-//     (gfx950's transposing LDS read): no register transposes.
-//   * Both layouts are XOR-swizzled in 16-byte units.  The direct-to-LDS
-//     copy writes LDS linearly by lane, so the swizzle is applied by
-//     choosing which global chunk each lane fetches.  The swizzles are
-//     conflict free for 8- and 16-lane LDS phases.
-//   * Wave tile (BM/WGM) x (BN/WGN) of v_mfma_f32_32x32x16_bf16 blocks.  The
-//     MFMA takes the N-side fragment first, so a lane's 16 accumulators are
-//     4 runs of 4 consecutive output columns and the epilogue stores 16 B
-//     (fp32) or 8 B (bf16) per lane.
-//   * Every output element accumulates its K products in the same order
-//     (K steps of BK, MFMA k order inside) for every tile shape, so token
-//     chunking never changes a value.
 //   * Workgroups are renumbered so consecutive tiles land on one XCD (the
 //     dispatcher deals workgroups round-robin over the 8 XCDs) and visited
-//     in groups of GROUP_M row tiles, so tiles sharing a weight panel run
-//     together on one L2.
+//     in groups of row tiles, so tiles sharing operand panels run together
+//     on one L2.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "kernels.h"
 
-// Tile and schedule parameters (compile-time).
-#ifndef ATP_GEMM_GROUP_M
-#define ATP_GEMM_GROUP_M 8
-#endif
 #ifndef ATP_GEMM_XCD_REMAP
 #define ATP_GEMM_XCD_REMAP 1
-#endif
-#ifndef ATP_GEMM_BK
-#define ATP_GEMM_BK 64
-#endif
-#ifndef ATP_GEMM_PIPE
-#define ATP_GEMM_PIPE 0
-#endif
-#ifndef ATP_GEMM_STAGES
-#define ATP_GEMM_STAGES 2
-#endif
-#ifndef ATP_GEMM_BM
-#define ATP_GEMM_BM 256
-#endif
-#ifndef ATP_GEMM_BN
-#define ATP_GEMM_BN 256
-#endif
-#ifndef ATP_GEMM_WGM
-#define ATP_GEMM_WGM 2
-#endif
-#ifndef ATP_GEMM_WGN
-#define ATP_GEMM_WGN 4
 #endif
 
 namespace atp {
 namespace {
 
-constexpr int GROUP_M = ATP_GEMM_GROUP_M;
 constexpr int NUM_XCD = 8;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr uint32_t kRsrcWord3 = 0x00020000u;   // raw 32-bit buffer access
@@ -113,17 +65,23 @@ __device__ __forceinline__ float gelu_grad_f(float x) {
 
 // 16-byte chunk swizzles.  K-major rows hold BK/8 chunks; MN-major rows
 // (one per k) hold at least 16 chunks.
-template <int CPR>
-__device__ __forceinline__ int swz_k(int r) {
-    if constexpr (CPR == 8) return (r ^ ((r >> 3) & 1)) & 7;
-    else return ((r >> 1) + (r >> 3)) & 3;
-}
-__device__ __forceinline__ int swz_mn(int k) { return ((k & 2) << 1) | ((k & 1) * 10); }
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+// The NT kernel's copies into LDS (buffer_load_dwordx4 ... lds) are issued
+// from inline assembly, so the compiler does not track them: it would make
+// every transposing LDS read wait for all copies in flight, even those into
+// another stage.  The kernel orders copies and reads itself (vmcnt waits and
+// barriers).  The resource is passed as its four descriptor words.
+__device__ __forceinline__ u32x4 rsrc_words(const void* base, int64_t bytes) {
     const int64_t cap = 0x7fffff00;   // keep offsets and sizes in 31 bits
-    const int n = (int)(bytes < 0 ? 0 : (bytes > cap ? cap : bytes));
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, kRsrcWord3);
+    const uint32_t n = (uint32_t)(bytes < 0 ? 0 : (bytes > cap ? cap : bytes));
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    return u32x4{(uint32_t)a, (uint32_t)(a >> 32) & 0xffffu, n, kRsrcWord3};
+}
+__device__ __forceinline__ void lds_dma16(const u32x4& rs, const uint16_t* lds_dst, uint32_t voff,
+                                          uint32_t soff) {
+    typedef __attribute__((address_space(3))) const void* lds_cptr;
+    const uint32_t m = (uint32_t)(uintptr_t)(lds_cptr)lds_dst;   // LDS byte address
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :: "s"(m), "v"(voff), "s"(rs), "s"(soff) : "memory", "m0");
 }
 
 struct KArgs {
@@ -170,110 +128,6 @@ __device__ __forceinline__ void group_coords(int logical, int tiles_m, int tiles
     tn = r / gsize;
 }
 
-template <int GM = GROUP_M>
-__device__ __forceinline__ void tile_coords(int tiles_m, int tiles_n, int& tm, int& tn) {
-    group_coords<GM>(xcd_logical(), tiles_m, tiles_n, tm, tn);
-}
-
-// ---------------------------------------------------------------------------
-// One operand of the tile: issue the direct-to-LDS copy of one K step, and
-// read MFMA fragments back.  ROWS = BM or BN (the operand's M/N extent).
-// ---------------------------------------------------------------------------
-template <int ROWS, int BK, int NT, bool KCONTIG>
-struct Operand {
-    static constexpr int CHUNKS = ROWS * BK / 8;          // 16-byte chunks per K step
-    static constexpr int PER_THREAD = CHUNKS / NT;
-    static_assert(CHUNKS % NT == 0, "tile not divisible by the thread count");
-    static constexpr int CPR = KCONTIG ? BK / 8 : ROWS / 8;   // chunks per LDS row
-
-    const uint16_t* base;
-    int64_t ld;
-    int64_t row0, rows, K;
-    // Per-lane byte offsets of this thread's chunks relative to the step's
-    // first element (row0, k0); out-of-range rows / columns hold kOob.  They
-    // do not depend on the K step.
-    uint32_t voff[PER_THREAD];
-    int kchunk[PER_THREAD];    // K-major: the chunk's first k within the step
-
-    __device__ __forceinline__ void init(int tid) {
-        const int wave = tid >> 6;
-        const int lane = tid & 63;
-#pragma unroll
-        for (int i = 0; i < PER_THREAD; ++i) {
-            const int p = (i * (NT / 64) + wave) * 64 + lane;     // LDS chunk slot
-            if constexpr (KCONTIG) {
-                const int r = p / CPR;
-                const int c = (p % CPR) ^ swz_k<CPR>(r);
-                kchunk[i] = c * 8;
-                voff[i] = (row0 + r < rows) ? (uint32_t)((r * ld + c * 8) * 2) : kOob;
-            } else {
-                const int k = p / CPR;
-                const int c = (p % CPR) ^ swz_mn(k);
-                kchunk[i] = k;
-                voff[i] = (row0 + c * 8 < rows) ? (uint32_t)((k * ld + c * 8) * 2) : kOob;
-            }
-        }
-    }
-
-    // Copy K step [k0, k0+BK) into LDS stage `dst` (ROWS*BK elements).  A
-    // step at or past K fills the stage with zeros (every lane out of range),
-    // so each step issues the same number of loads.
-    __device__ __forceinline__ void issue(uint16_t* dst, int64_t k0, int tid) const {
-        const int wave = tid >> 6;
-        const bool live = k0 < K;
-        if constexpr (KCONTIG) {
-            // whole rows bound the range; k past K inside a row is masked per
-            // lane, which only the last step of a ragged K needs
-            const uint16_t* b = base + row0 * ld + (live ? k0 : 0);
-            const int64_t left = rows - row0;
-            const int64_t valid_rows = live ? (left < ROWS ? left : ROWS) : 0;
-            const __amdgpu_buffer_rsrc_t rs = make_rsrc(b, valid_rows * ld * 2);
-            const bool tail = k0 + BK > K;
-#pragma unroll
-            for (int i = 0; i < PER_THREAD; ++i) {
-                const uint32_t off = (tail && k0 + kchunk[i] >= K) ? kOob : voff[i];
-                lds_void* d = (lds_void*)(dst + (size_t)(i * (NT / 64) + wave) * 64 * 8);
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, d, 16, off, 0, 0, 0);
-            }
-        } else {
-            // rows k0.. of a [K][ld] matrix: the range ends at row K
-            const uint16_t* b = base + (live ? k0 : 0) * ld + row0;
-            const int64_t valid_k = live ? (K - k0 < BK ? K - k0 : BK) : 0;
-            const __amdgpu_buffer_rsrc_t rs = make_rsrc(b, valid_k * ld * 2);
-#pragma unroll
-            for (int i = 0; i < PER_THREAD; ++i) {
-                lds_void* d = (lds_void*)(dst + (size_t)(i * (NT / 64) + wave) * 64 * 8);
-                const uint32_t off = voff[i];
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, d, 16, off, 0, 0, 0);
-            }
-        }
-    }
-
-    // MFMA 32x32x16 fragment: lane holds rows r0 + lane%32, k = ks*16 + 8*(lane/32) + 0..7.
-    static __device__ __forceinline__ bf16x8 frag(const uint16_t* src, int r0, int ks,
-                                                  int lane) {
-        if constexpr (KCONTIG) {
-            const int r = r0 + (lane & 31);
-            const int c = (ks * 2 + (lane >> 5)) ^ swz_k<CPR>(r);
-            return *reinterpret_cast<const bf16x8*>(src + r * BK + c * 8);
-        } else {
-            // two transposing reads of 4 k values each (lane group of 16:
-            // rows r0 + 16*(g%2) + 0..15, k base ks*16 + 8*(g/2))
-            const int g = lane >> 4;
-            const int j = lane & 15;
-            const int mn = r0 + 16 * (g & 1) + 4 * (j & 3);
-            const int kb = ks * 16 + 8 * (g >> 1) + (j >> 2);
-            const int k0 = kb, k1 = kb + 4;
-            const uint16_t* p0 = src + k0 * ROWS + (((mn >> 3) ^ swz_mn(k0)) << 3) + (mn & 7);
-            const uint16_t* p1 = src + k1 * ROWS + (((mn >> 3) ^ swz_mn(k1)) << 3) + (mn & 7);
-            const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p0);
-            const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p1);
-            typedef short i16x8 __attribute__((ext_vector_type(8)));
-            const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-            return __builtin_bit_cast(bf16x8, v);
-        }
-    }
-};
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -322,139 +176,11 @@ __device__ __forceinline__ void epilogue_store(const KArgs& a, int64_t m, int64_
     }
 }
 
-template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, bool A_K, bool B_K, int EPI,
-          bool OUT_BF16>
-__global__ __launch_bounds__(WGM* WGN * 64, 1) void gemm_kernel(KArgs a) {
-    constexpr int NT = WGM * WGN * 64;
-    constexpr int WM = BM / WGM;
-    constexpr int WN = BN / WGN;
-    constexpr int FM = WM / 32;
-    constexpr int FN = WN / 32;
-    constexpr int A_ELEMS = BM * BK;
-    constexpr int STAGE = (BM + BN) * BK;
-    using OpA = Operand<BM, BK, NT, A_K>;
-    using OpB = Operand<BN, BK, NT, B_K>;
-    constexpr int LOADS = OpA::PER_THREAD + OpB::PER_THREAD;   // vm ops per stage per thread
-
-    __shared__ __attribute__((aligned(1024))) uint16_t smem[STAGES * STAGE];
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int wm = wave / WGN;
-    const int wn = wave % WGN;
-
-    int tm, tn;
-    tile_coords(a.tiles_m, a.tiles_n, tm, tn);
-    const int64_t m0 = (int64_t)tm * BM;
-    const int64_t n0 = (int64_t)tn * BN;
-
-    OpA opa{a.A, a.lda, m0, a.M, a.K};
-    OpB opb{a.B, a.ldb, n0, a.N, a.K};
-    opa.init(tid);
-    opb.init(tid);
-
-    f32x16 acc[FM][FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-
-    const int nk = (int)((a.K + BK - 1) / BK);
-    constexpr int KS = BK / 16;   // MFMA k-steps per K step
-
-    // prologue: steps 0 .. STAGES-2 in flight (steps past K fill zeros)
-#pragma unroll
-    for (int s = 0; s < STAGES - 1; ++s) {
-        opa.issue(smem + s * STAGE, (int64_t)s * BK, tid);
-        opb.issue(smem + s * STAGE + A_ELEMS, (int64_t)s * BK, tid);
-    }
-
-    for (int kt = 0; kt < nk; ++kt) {
-        // step kt's copy is the oldest of STAGES-1 in flight
-        wait_vmcnt<LOADS * (STAGES - 2)>();
-        __syncthreads();
-        const uint16_t* sa = smem + (kt % STAGES) * STAGE;
-        const uint16_t* sb = sa + A_ELEMS;
-        bf16x8 fa[2][FM], fb[2][FN];
-#pragma unroll
-        for (int i = 0; i < FM; ++i) fa[0][i] = OpA::frag(sa, wm * WM + i * 32, 0, lane);
-#pragma unroll
-        for (int j = 0; j < FN; ++j) fb[0][j] = OpB::frag(sb, wn * WN + j * 32, 0, lane);
-        {
-            // refill the buffer step kt-1 used with step kt+STAGES-1
-            const int kn = kt + STAGES - 1;
-            uint16_t* dst = smem + (kn % STAGES) * STAGE;
-            opa.issue(dst, (int64_t)kn * BK, tid);
-            opb.issue(dst + A_ELEMS, (int64_t)kn * BK, tid);
-        }
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            const int cur = ks & 1;
-            if (ks + 1 < KS) {
-#pragma unroll
-                for (int i = 0; i < FM; ++i)
-                    fa[cur ^ 1][i] = OpA::frag(sa, wm * WM + i * 32, ks + 1, lane);
-#pragma unroll
-                for (int j = 0; j < FN; ++j)
-                    fb[cur ^ 1][j] = OpB::frag(sb, wn * WN + j * 32, ks + 1, lane);
-            }
-#if ATP_GEMM_PIPE
-            // keep the next k-step's LDS reads ahead of this k-step's MFMAs
-            __builtin_amdgcn_sched_barrier(0);
-#endif
-#pragma unroll
-            for (int i = 0; i < FM; ++i)
-#pragma unroll
-                for (int j = 0; j < FN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[cur][j], fa[cur][i],
-                                                                        acc[i][j], 0, 0, 0);
-        }
-#if defined(ATP_GEMM_SCHED) && ATP_GEMM_SCHED
-        // interleave: the step's global loads and the next fragments' LDS
-        // reads are spread between the MFMAs
-#pragma unroll
-        for (int q = 0; q < LOADS; ++q) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
-        }
-#pragma unroll
-        for (int q = 0; q < (KS - 1) * (FM + FN) * (A_K ? 1 : 2) && q < KS * FM * FN; ++q) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
-        }
-#endif
-    }
-    wait_vmcnt<0>();
-
-    // Epilogue.  Lane holds C(m = base_m + lane%32, n = base_n + 8g + 4*(lane/32) + 0..3)
-    // in acc[..][..][4g .. 4g+3].
-    const int lrow = lane & 31;
-    const int lcol = (lane >> 5) * 4;
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-        const int64_t m = m0 + wm * WM + i * 32 + lrow;
-        if (m >= a.M) continue;
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int64_t n = n0 + wn * WN + j * 32 + g * 8 + lcol;
-                if (n >= a.N) continue;
-                float v[4];
-#pragma unroll
-                for (int r = 0; r < 4; ++r) v[r] = acc[i][j][4 * g + r];
-                epilogue_store<EPI, OUT_BF16>(a, m, n, v);
-            }
-        }
-    }
-}
-
 // ---------------------------------------------------------------------------
-// NT kernel: C[M,N] = A[M,K] B[N,K]^T, 256 x 160 tiles, eight waves in two
-// groups that take turns on the matrix cores ("ping-pong").
+// The kernel: C[M,N] = A B with A [M,K] and B [K,N] each stored contiguous
+// along k (A_K / B_K; B then reads [N][K], the NT layout) or along its rows
+// (A [K][M], B [K][N]); 256 x 160 tiles, eight waves in two groups that take
+// turns on the matrix cores ("ping-pong").
 //
 //   * Tile 256 x 160 x 64: three LDS stages of (256 + 160) x 64 bf16 fill
 //     156 KB of the 160 KB, so the copy of step p+2 is issued while step p is
@@ -477,9 +203,17 @@ __global__ __launch_bounds__(WGM* WGN * 64, 1) void gemm_kernel(KArgs a) {
 //   * The swizzle of a row depends only on the row's index within its copy
 //     instruction, so one byte offset per lane serves every copy; rows past
 //     the operand's end lie beyond the buffer's num_records and read zeros.
+//   * An operand contiguous along its rows is kept [k][row] in LDS and its
+//     fragments come from two ds_read_b64_tr_b16 (gfx950's transposing LDS
+//     read); a chunk rotation (160-wide tiles) or XOR (256-wide) keeps each
+//     32-lane half of a read on distinct banks (measured: zero conflicts).
+//     These reads cost 1.5x the LDS time per byte of ds_read_b128, and
+//     160-wide rows (320 bytes) straddle cache lines, so this layout runs
+//     15-25% slower than the k-contiguous one on the forward shapes; the
+//     block calls use it only without a workspace.
 //   * An output element's products are accumulated in the same order for
-//     every M (K steps of 64, two MFMA k-slices of 32 each), so token
-//     chunking never changes a value.
+//     every M and every layout (K steps of 64, two MFMA k-slices of 32
+//     each), so token chunking and the layout never change a value.
 // ---------------------------------------------------------------------------
 namespace nt {
 
@@ -521,7 +255,7 @@ struct Copy {
     static constexpr int WI = ROWS / RPI;          // copy instructions per stage
     static constexpr int PER = (WI + NW - 1) / NW; // per wave (some waves one fewer)
     static_assert(ROWS % RPI == 0, "rows per copy instruction");
-    __amdgpu_buffer_rsrc_t rs;
+    u32x4 rs;
     uint32_t vlane;       // this lane's byte offset within its instruction's rows
     uint32_t ins_stride;  // bytes from one instruction's rows to the next
     int kc;               // first k of this lane's chunk
@@ -533,7 +267,7 @@ struct Copy {
         K = K_;
         const int64_t left = rows - row0;
         const int64_t vr = left < 0 ? 0 : (left < ROWS ? left : ROWS);
-        rs = make_rsrc(base + row0 * ld, vr * ld * 2);
+        rs = rsrc_words(base + row0 * ld, vr * ld * 2);
         const int r = lane / CPR;
         const int c = (lane % CPR) ^ swz(r);
         kc = c * 8;
@@ -553,8 +287,7 @@ struct Copy {
             if (PER * NW != WI && ins >= WI) break;   // wave-uniform
             uint32_t off = vlane + (uint32_t)ins * ins_stride;
             if (tail && k0 + kc >= K) off = kOob;
-            lds_void* d = (lds_void*)(dst + (size_t)ins * 64 * 8);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, d, 16, off, (int)(k0 * 2), 0, 0);
+            lds_dma16(rs, dst + (size_t)ins * 64 * 8, off, (uint32_t)(k0 * 2));
         }
     }
 };
@@ -564,6 +297,93 @@ __device__ __forceinline__ bf16x8 frag(const uint16_t* src, int r0, int ks, int 
     const int r = r0 + (lane & 15);
     const int c = (ks * 4 + (lane >> 4)) ^ swz(r);
     return *reinterpret_cast<const bf16x8*>(src + r * BK + c * 8);
+}
+
+// One operand tile stored [k][ROWS]: BK rows of a [K][ld] matrix that is
+// contiguous along M or N (X in dW, W in the forward, dY in dW), copied
+// 16 bytes (8 columns) per lane.  Each k row holds CPK chunks of 16 bytes;
+// chunk c of row k sits at position tpos(k, c), so that the transposing
+// fragment reads below touch 16 distinct bank quads per 32-lane half (the
+// LDS serves lanes 0-31 and 32-63 of a 64-bit read separately).  Slot p of
+// a stage (row p / CPK, position p % CPK) is filled by lane p % 64 of copy
+// instruction p / 64, which fetches the chunk that belongs there.
+template <int ROWS>
+__device__ __forceinline__ int tpos(int k, int c) {
+    if constexpr (ROWS == 160) return (c + 2 * ((k >> 3) & 1)) % 20;   // rotation by 0 / 2
+    else return c ^ (2 * (k & 3) + 8 * ((k >> 3) & 1));                // XOR, 32 chunks
+}
+template <int ROWS>
+__device__ __forceinline__ int tchunk(int k, int pos) {   // inverse of tpos
+    if constexpr (ROWS == 160) return (pos + 20 - 2 * ((k >> 3) & 1)) % 20;
+    else return pos ^ (2 * (k & 3) + 8 * ((k >> 3) & 1));
+}
+
+template <int ROWS>
+struct CopyT {
+    static_assert(ROWS == 160 || ROWS == 256, "tile widths with a conflict-free layout");
+    static constexpr int CPK = ROWS / 8;            // 16-byte chunks per k row
+    static constexpr int WI = BK * CPK / 64;        // copy instructions per stage
+    static constexpr int PER = (WI + NW - 1) / NW;  // per wave (some waves one fewer)
+    static_assert(BK * CPK % 64 == 0, "whole copy instructions");
+    const uint16_t* base;   // element (k = 0, column col0)
+    int64_t ld, K;
+    uint32_t voff[PER];     // this lane's byte offset in each of its instructions
+    int nmine;
+
+    __device__ __forceinline__ void init(const uint16_t* base_, int64_t ld_, int64_t col0,
+                                         int64_t cols, int64_t K_, int wave, int lane) {
+        base = base_ + col0;
+        ld = ld_;
+        K = K_;
+        nmine = 0;
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int ins = wave + NW * i;
+            const int p = ins * 64 + lane;
+            const int k = p / CPK;
+            const int c = tchunk<ROWS>(k, p % CPK);
+            voff[i] = (col0 + 8 * c < cols) ? (uint32_t)((k * ld + 8 * c) * 2) : kOob;
+            if (ins < WI) nmine = i + 1;
+        }
+    }
+    // Copy of the K step at k0 into LDS stage `dst` (rows past K read zeros).
+    __device__ __forceinline__ void issue(uint16_t* dst, int64_t k0, int wave) const {
+        const int64_t left = K - k0;
+        const int64_t vk = left < 0 ? 0 : (left < BK ? left : BK);
+        const u32x4 rs = rsrc_words(base + k0 * ld, vk * ld * 2);
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int ins = wave + NW * i;
+            if (PER * NW != WI && ins >= WI) break;   // wave-uniform
+            lds_dma16(rs, dst + (size_t)ins * 64 * 8, voff[i], 0u);
+        }
+    }
+};
+
+// 16x16x32 fragment of a [k][ROWS] tile: lane holds column r0 + lane%16,
+// k = ks*32 + 8*(lane/16) + 0..7, from two transposing reads (within each
+// 16-lane group, lane j names 4 consecutive columns of row k + j/4 and
+// receives column j's 4 values).
+template <int ROWS>
+__device__ __forceinline__ bf16x8 frag_t(const uint16_t* src, int r0, int ks, int lane) {
+    const int g = lane >> 4, j = lane & 15;
+    const int mn = r0 + 4 * (j & 3);
+    const int k = ks * 32 + 8 * g + (j >> 2);       // k and k + 4 share tpos
+    const uint16_t* p0 = src + k * ROWS + tpos<ROWS>(k, mn >> 3) * 8 + (mn & 7);
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p0);
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0 + 4 * ROWS));
+    const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
+}
+
+// Operand copy and fragment read for a tile contiguous along k (KC) or
+// along its rows.
+template <int ROWS, bool KC>
+using OpCopy = typename std::conditional<KC, Copy<ROWS>, CopyT<ROWS>>::type;
+template <int ROWS, bool KC>
+__device__ __forceinline__ bf16x8 op_frag(const uint16_t* src, int r0, int ks, int lane) {
+    if constexpr (KC) return frag(src, r0, ks, lane);
+    else return frag_t<ROWS>(src, r0, ks, lane);
 }
 
 __device__ __forceinline__ void barrier() {
@@ -576,7 +396,7 @@ __device__ __forceinline__ void barrier() {
 
 }  // namespace nt
 
-template <class C, int EPI, bool OUT_BF16>
+template <class C, bool A_K, bool B_K, int EPI, bool OUT_BF16>
 __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
     using namespace nt;
     constexpr int BN = C::BN, WGN = C::WGN, STAGES = C::STAGES;
@@ -602,11 +422,12 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
     const int64_t kb = (int64_t)split * a.ksplit;
     const int64_t kn = min(a.K - kb, a.ksplit);    // this split's contraction
 
-    Copy<BM> ca;
-    Copy<BN> cb;
-    ca.init(a.A + kb, a.lda, m0, a.M, kn, wave, lane);
-    cb.init(a.B + kb, a.ldb, n0, a.N, kn, wave, lane);
-    constexpr int LA = Copy<BM>::PER, LB = Copy<BN>::PER;
+    // split k offset: along a row (k-contiguous operand) or down the rows
+    OpCopy<BM, A_K> ca;
+    OpCopy<BN, B_K> cb;
+    ca.init(a.A + (A_K ? kb : kb * a.lda), a.lda, m0, a.M, kn, wave, lane);
+    cb.init(a.B + (B_K ? kb : kb * a.ldb), a.ldb, n0, a.N, kn, wave, lane);
+    constexpr int LA = OpCopy<BM, A_K>::PER, LB = OpCopy<BN, B_K>::PER;
     const int loads = ca.nmine + cb.nmine;   // copy instructions per step (wave-uniform)
 
     f32x4 acc[FM][FN];
@@ -648,9 +469,11 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
-                for (int i = 0; i < FM; ++i) fa[ks][i] = frag(sa, wm * WM + i * MF, ks, lane);
+                for (int i = 0; i < FM; ++i)
+                    fa[ks][i] = op_frag<BM, A_K>(sa, wm * WM + i * MF, ks, lane);
 #pragma unroll
-                for (int j = 0; j < FN; ++j) fb[ks][j] = frag(sb, wn * WN + j * MF, ks, lane);
+                for (int j = 0; j < FN; ++j)
+                    fb[ks][j] = op_frag<BN, B_K>(sb, wn * WN + j * MF, ks, lane);
             }
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
             // before group A's next memory phase this wave's copies of step
@@ -690,10 +513,6 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
         }
     }
 }
-
-// Tile configuration: 256 x 256 workgroup tile, 4 waves of 128 x 128.
-constexpr int CFG_BM = ATP_GEMM_BM, CFG_BN = ATP_GEMM_BN, CFG_BK = ATP_GEMM_BK,
-              CFG_STAGES = ATP_GEMM_STAGES, CFG_WGM = ATP_GEMM_WGM, CFG_WGN = ATP_GEMM_WGN;
 
 KArgs kargs(const GemmProblem& p, int bm, int bn) {
     KArgs a;
@@ -761,48 +580,23 @@ int pick_splits(int64_t M, int64_t N, int64_t K, int64_t* ksplit) {
     return best;
 }
 
-template <class C, int EPI, bool OUT_BF16>
-hipError_t launch_nt_cfg(const GemmProblem& p, hipStream_t s) {
+template <class C, bool A_K, bool B_K, int EPI, bool OUT_BF16>
+hipError_t launch_pp_cfg(const GemmProblem& p, hipStream_t s) {
     const KArgs a = kargs(p, nt::BM, C::BN);
     const int grid = a.tiles_m * a.tiles_n * a.splits;
     if (grid == 0) return hipSuccess;
-    hipLaunchKernelGGL((gemm_nt_kernel<C, EPI, OUT_BF16>), dim3(grid), dim3(nt::NT), 0, s, a);
+    hipLaunchKernelGGL((gemm_nt_kernel<C, A_K, B_K, EPI, OUT_BF16>), dim3(grid), dim3(nt::NT), 0,
+                       s, a);
     return hipGetLastError();
 }
 
-template <int EPI, bool OUT_BF16>
-hipError_t launch_nt(const GemmProblem& p, hipStream_t s) {
-    if (p.splits > 1) return launch_nt_cfg<nt::Tile160, EPI, OUT_BF16>(p, s);
-    return nt_use_256(p) ? launch_nt_cfg<nt::Tile256, EPI, OUT_BF16>(p, s)
-                         : launch_nt_cfg<nt::Tile160, EPI, OUT_BF16>(p, s);
-}
-
+// The ping-pong kernel for operands contiguous along k (A_K / B_K) or along
+// their rows; split-K launches use the 256 x 160 configuration.
 template <bool A_K, bool B_K, int EPI, bool OUT_BF16>
-hipError_t launch_t(const GemmProblem& p, hipStream_t s) {
-    KArgs a;
-    a.A = static_cast<const uint16_t*>(p.A);
-    a.lda = p.lda;
-    a.B = static_cast<const uint16_t*>(p.B);
-    a.ldb = p.ldb;
-    a.C = p.C;
-    a.ldc = p.ldc;
-    a.bias = static_cast<const uint16_t*>(p.bias);
-    a.pre_in = static_cast<const uint16_t*>(p.pre_in);
-    a.pre_out = static_cast<uint16_t*>(p.pre_out);
-    a.M = p.M;
-    a.N = p.N;
-    a.K = p.K;
-    a.tiles_m = (int)((p.M + CFG_BM - 1) / CFG_BM);
-    a.tiles_n = (int)((p.N + CFG_BN - 1) / CFG_BN);
-    a.splits = 1;
-    a.ksplit = p.K;
-    a.c_split = 0;
-    const int grid = a.tiles_m * a.tiles_n;
-    if (grid == 0) return hipSuccess;
-    hipLaunchKernelGGL((gemm_kernel<CFG_BM, CFG_BN, CFG_BK, CFG_STAGES, CFG_WGM, CFG_WGN, A_K,
-                                    B_K, EPI, OUT_BF16>),
-                       dim3(grid), dim3(CFG_WGM * CFG_WGN * 64), 0, s, a);
-    return hipGetLastError();
+hipError_t launch_pp(const GemmProblem& p, hipStream_t s) {
+    if (p.splits > 1) return launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
+    return nt_use_256(p) ? launch_pp_cfg<nt::Tile256, A_K, B_K, EPI, OUT_BF16>(p, s)
+                         : launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
 }
 
 }  // namespace
@@ -822,12 +616,12 @@ bool gemm_supported(int layout, int epi, bool out_bf16) {
 }
 
 const char* gemm_kernel_name(const GemmProblem& p) {
-    switch (p.layout) {
-    case LAYOUT_NN: return "gemm_nn";
-    case LAYOUT_NT: return p.splits > 1 ? "gemm_nt_splitk" : nt_use_256(p) ? "gemm_nt256" : "gemm_nt";
-    case LAYOUT_TN: return "gemm_tn";
-    default: return "gemm_?";
-    }
+    static const char* const names[3][3] = {{"gemm_nn", "gemm_nn256", "gemm_nn_splitk"},
+                                            {"gemm_nt", "gemm_nt256", "gemm_nt_splitk"},
+                                            {"gemm_tn", "gemm_tn256", "gemm_tn_splitk"}};
+    const int l = p.layout == LAYOUT_NN ? 0 : p.layout == LAYOUT_NT ? 1 : p.layout == LAYOUT_TN ? 2 : -1;
+    if (l < 0) return "gemm_?";
+    return names[l][p.splits > 1 ? 2 : nt_use_256(p) ? 1 : 0];
 }
 
 int nt_split_plan(int64_t M, int64_t N, int64_t K, int64_t* ksplit) {
@@ -837,42 +631,42 @@ int nt_split_plan(int64_t M, int64_t N, int64_t K, int64_t* ksplit) {
 hipError_t launch_gemm(const GemmProblem& p, hipStream_t s) {
     if (p.M <= 0 || p.N <= 0) return hipSuccess;
     // buffer offsets are 32-bit: one tile's rows of either operand must span < 2 GiB
-    const int64_t span = (int64_t)(CFG_BM > CFG_BN ? CFG_BM : CFG_BN) *
+    const int64_t span = (int64_t)256 *
                          (p.lda > p.ldb ? p.lda : p.ldb) * 2;
     if (span > 0x7fffff00) return hipErrorInvalidValue;
     const bool b16 = p.out_bf16;
     if (p.splits > 1) {
-        // split-K: NT, plain fp32 outputs, whole K steps per split, every split
+        // split-K: plain fp32 outputs, whole K steps per split, every split
         // non-empty
-        if (p.layout != LAYOUT_NT || p.epi != EPI_NONE || b16 || p.ksplit <= 0 ||
-            p.ksplit % 64 || (int64_t)(p.splits - 1) * p.ksplit >= p.K || p.c_split < p.M * p.ldc)
+        if (p.epi != EPI_NONE || b16 || p.ksplit <= 0 || p.ksplit % 64 ||
+            (int64_t)(p.splits - 1) * p.ksplit >= p.K || p.c_split < p.M * p.ldc)
             return hipErrorInvalidValue;
     }
     switch (p.layout) {
-    case LAYOUT_NN:
+    case LAYOUT_NN:   // X W: A contiguous along k, B = W along its columns
         switch (p.epi) {
         case EPI_NONE:
-            return b16 ? launch_t<true, false, EPI_NONE, true>(p, s)
-                       : launch_t<true, false, EPI_NONE, false>(p, s);
+            return b16 ? launch_pp<true, false, EPI_NONE, true>(p, s)
+                       : launch_pp<true, false, EPI_NONE, false>(p, s);
         case EPI_BIAS:
-            return b16 ? launch_t<true, false, EPI_BIAS, true>(p, s)
-                       : launch_t<true, false, EPI_BIAS, false>(p, s);
+            return b16 ? launch_pp<true, false, EPI_BIAS, true>(p, s)
+                       : launch_pp<true, false, EPI_BIAS, false>(p, s);
         case EPI_BIAS_GELU:
-            return b16 ? launch_t<true, false, EPI_BIAS_GELU, true>(p, s)
-                       : launch_t<true, false, EPI_BIAS_GELU, false>(p, s);
+            return b16 ? launch_pp<true, false, EPI_BIAS_GELU, true>(p, s)
+                       : launch_pp<true, false, EPI_BIAS_GELU, false>(p, s);
         default:
             return hipErrorInvalidValue;
         }
-    case LAYOUT_NT:
+    case LAYOUT_NT:   // dY W^T with B = W (contiguous along the contraction)
         if (p.epi == EPI_NONE)
-            return b16 ? launch_nt<EPI_NONE, true>(p, s) : launch_nt<EPI_NONE, false>(p, s);
-        if (p.epi == EPI_GELU_BWD && b16) return launch_nt<EPI_GELU_BWD, true>(p, s);
-        // the forward with a transposed weight copy (B = W^T, contiguous along k)
-        if (p.epi == EPI_BIAS && b16) return launch_nt<EPI_BIAS, true>(p, s);
-        if (p.epi == EPI_BIAS_GELU && b16) return launch_nt<EPI_BIAS_GELU, true>(p, s);
+            return b16 ? launch_pp<true, true, EPI_NONE, true>(p, s)
+                       : launch_pp<true, true, EPI_NONE, false>(p, s);
+        if (p.epi == EPI_GELU_BWD && b16) return launch_pp<true, true, EPI_GELU_BWD, true>(p, s);
+        if (p.epi == EPI_BIAS && b16) return launch_pp<true, true, EPI_BIAS, true>(p, s);
+        if (p.epi == EPI_BIAS_GELU && b16) return launch_pp<true, true, EPI_BIAS_GELU, true>(p, s);
         return hipErrorInvalidValue;
-    case LAYOUT_TN:
-        if (p.epi == EPI_NONE && !b16) return launch_t<false, false, EPI_NONE, false>(p, s);
+    case LAYOUT_TN:   // X^T dY: both operands contiguous along their columns
+        if (p.epi == EPI_NONE && !b16) return launch_pp<false, false, EPI_NONE, false>(p, s);
         return hipErrorInvalidValue;
     default:
         return hipErrorInvalidValue;

@@ -127,7 +127,8 @@ def block_workspace(inp):
 def run_block_fwd(inp, chunks, compute=None, comm=None, same_stream=False, aux=True,
                   workspace=False):
     """Allocate outputs, call atp_block_fwd, return outputs + own partials.
-    aux=True also gives the block a second compute stream; workspace=True
+    aux=True also hands the block a second compute stream (accepted and left
+    unused by the library); workspace=True
     hands it a workspace, so it runs the transposed-layout path."""
     T, G, m = inp["T"], inp["G"], inp["m"]
     dev_ = inp["x"].device

@@ -208,9 +208,9 @@ def test_block_workspace_bytes_formula():
     # forward: W^T of the four shards; backward: X^T of x, attention block, H
     # and dY^T of the four linears over the tokens; pieces rounded to 256 B.
     # Each side adds the fp32 split-K slabs of its chunk products, at most
-    # 512 tiles of 256 x 160 fp32 values, sized for the largest plan over every
-    # chunk count (a 64-chunk split of the 8 x 1 wide layer splits, 8 chunks
-    # do not); none without tokens
+    # 512 tiles of 256 x 160 fp32 values, sized for the largest plan over
+    # every chunk count (a 64-chunk split of the 8 x 1 wide layer splits, 8
+    # chunks do not); no slabs without tokens
     r = lambda b: (b + 255) // 256 * 256  # noqa: E731
     slab_max = 512 * 256 * 160 * 4
     for (d1, d2), mode, T, h, splits in [((8, 1), 0, 4096, 20480, True),

@@ -173,7 +173,7 @@ def test_mesh_simulation_equals_unsharded_layer(mode, mesh):
 
 
 # ------------------------------------------------------------------ invariances
-@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "transposed"])
+@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "workspace"])
 def test_chunk_count_never_changes_a_bit(workspace):
     base = None
     inp = make_block_inputs("col", (2, 4), (1, 2), 512, 1024, 0.02, seed=4)
@@ -248,7 +248,7 @@ def _check_bwd(out, ref, inp, what=""):
         assert_close(out["db"][i], ref["db_" + n], f"{what} db_{n}", floor=fl)
 
 
-@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "transposed"])
+@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "workspace"])
 @pytest.mark.parametrize("mode,mesh,coord", [("col", (2, 2), (1, 0)), ("row", (2, 4), (1, 3)),
                                              ("col", (4, 1), (2, 0))])
 def test_block_fwd_bwd_integer_chain_bit_exact(mode, mesh, coord, workspace):
@@ -268,7 +268,7 @@ def test_block_fwd_bwd_integer_chain_bit_exact(mode, mesh, coord, workspace):
         np.testing.assert_array_equal(to64(out["db"][i]), ref["db_" + n], err_msg=n)
 
 
-@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "transposed"])
+@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "workspace"])
 @pytest.mark.parametrize("mode", ["col", "row"])
 def test_block_bwd_tiny_every_coordinate(mode, workspace):
     w = TINY
@@ -289,7 +289,7 @@ def test_block_bwd_groups_of_one(mesh):
     _check_bwd(out, _oracle_bwd(inp), inp, f"{mesh}")
 
 
-@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "transposed"])
+@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "workspace"])
 def test_block_bwd_chunk_invariance(workspace):
     inp = make_block_inputs("col", (2, 4), (1, 3), 512, 1024, 0.02, seed=9, bwd=True)
     base = run_block_bwd(inp, 1, workspace=workspace)

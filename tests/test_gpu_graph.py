@@ -54,7 +54,7 @@ def _block_call(inp, chunks, workspace):
     pytest.param(False, marks=pytest.mark.skip(
         reason="capturing the direct path crashed in hipStreamEndCapture (host segfault in "
                "the runtime, cause not identified); the library refuses it"))],
-    ids=["transposed", "direct"])
+    ids=["workspace", "direct"])
 @pytest.mark.parametrize("case", [("col", (2, 4), (1, 2), 512, 1024, 4),
                                   ("col", (8, 1), (3, 0), 256, 2048, 2),
                                   ("row", (4, 2), (2, 1), 384, 1024, 3)],

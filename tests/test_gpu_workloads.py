@@ -34,7 +34,7 @@ def _cols(n_loc, n=4, seed=1):
     return sorted(set([0, n_loc - 1] + rng.choice(n_loc, size=n, replace=False).tolist()))
 
 
-@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "transposed"])
+@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "workspace"])
 @pytest.mark.parametrize("name", BIG)
 def test_workload_forward_sampled_rows(name, workspace):
     w = S.WORKLOADS[name]
@@ -92,7 +92,7 @@ def _oracle_bwd_sampled(inp, rows, cols):
     return r
 
 
-@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "transposed"])
+@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "workspace"])
 @pytest.mark.parametrize("name", [k for k in BIG if S.WORKLOADS[k]["bwd"]])
 def test_workload_backward_sampled(name, workspace):
     w = S.WORKLOADS[name]
