@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--chunks", type=int, default=None, help="override the chunk count")
+    ap.add_argument("--mesh", default=None,
+                    help="override the workload's mesh, as D1xD2 (one device's share of it)")
     ap.add_argument("--fwd-only", action="store_true", help="time the forward only")
     ap.add_argument("--serial", action="store_true",
                     help="run reductions on the compute stream (no overlap)")
@@ -258,6 +260,8 @@ def main():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(3)
     wl = dict(S.WORKLOADS[args.workload])
+    if args.mesh:
+        wl["mesh"] = tuple(int(v) for v in args.mesh.lower().split("x"))
     chunks = args.chunks or wl["chunks"]
     fwd_only = args.fwd_only or not wl.get("bwd", False)
     atp.load_library()
