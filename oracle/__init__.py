@@ -23,6 +23,11 @@ Models" (arXiv 2301.08658).  What is computed and where the paper says so:
   oracle therefore has no notion of chunks.
 * Sec. 4.2 -- backward of Y = XW: dX = dY W^T, dW = X^T dY (``linear_bwd``,
   ``block_bwd``).
+* Sec. 2.1 Formula (mha) and Sec. 3.2.1's attention block -- the causal
+  attention core of one head (``attention_fwd`` / ``attention_bwd``) and one
+  device's share of it: the heads of its reduced QKV block scattered over
+  the QKV output's reduction group (``attention_core_local``,
+  ``attention_core_bwd_local``).
 
 Every array crossing into C is float64; bf16 inputs are widened exactly.
 """
@@ -93,6 +98,9 @@ def _load():
     lib.orc_num_threads.restype = ctypes.c_int
     lib.orc_round_bf16.argtypes = [ctypes.c_double]
     lib.orc_round_bf16.restype = ctypes.c_double
+    lib.orc_attention_fwd.argtypes = [i64, i64, dp, i64, dp, i64, dp, i64, dp, i64, dp]
+    lib.orc_attention_bwd.argtypes = [i64, i64, dp, i64, dp, i64, dp, i64, dp, i64,
+                                      dp, i64, dp, i64, dp, i64]
     _lib = lib
     return lib
 
@@ -397,3 +405,90 @@ def block_bwd_local(block_mode, mesh, coord, x_loc, a_loc, h_loc, pre_loc, w,
     dxq, res["dw_qkv"], res["db_qkv"] = linear_bwd(x_loc, w["qkv"], dqkv)
     res["dx_qkv"] = reduced_dx("qkv", dxq)
     return res
+
+
+# --------------------------------------------------------------------------
+# Sec. 2.1 Formula (mha), Sec. 3.2.1 attention block
+# --------------------------------------------------------------------------
+def attention_fwd(q, k, v):
+    """Causal attention of one head over one sequence: q, k, v [S, d].
+    Returns (o [S, d], lse [S]) with lse the natural log of the softmax
+    denominator of each row (scores scaled by 1/sqrt(d))."""
+    q, k, v = (np.ascontiguousarray(_f64(a)) for a in (q, k, v))
+    S, d = q.shape
+    o = np.empty((S, d), dtype=np.float64)
+    lse = np.empty((S,), dtype=np.float64)
+    if S:
+        _load().orc_attention_fwd(S, d, _dptr(q), d, _dptr(k), d, _dptr(v), d, _dptr(o), d,
+                                  _dptr(lse))
+    return o, lse
+
+
+def attention_bwd(q, k, v, dout):
+    """Gradients (dq, dk, dv) of the causal attention above for dO = dout."""
+    q, k, v, dout = (np.ascontiguousarray(_f64(a)) for a in (q, k, v, dout))
+    S, d = q.shape
+    dq, dk, dv = (np.empty((S, d), dtype=np.float64) for _ in range(3))
+    if S:
+        _load().orc_attention_bwd(S, d, _dptr(q), d, _dptr(k), d, _dptr(v), d, _dptr(dout), d,
+                                  _dptr(dq), d, _dptr(dk), d, _dptr(dv), d)
+    return dq, dk, dv
+
+
+def attention_heads(n_qkv_cols, head_dim, scatter_size, scatter_index):
+    """The heads of a QKV block a device attends over.  The block holds
+    n_qkv_cols / (3 head_dim) whole heads, each as [q | k | v] columns (the
+    per-head column order of the QKV weight; the paper does not fix it).
+    Sec. 3.2.1 scatters the block over the group that reduced it (it is
+    replicated there), so member j of a group of g takes the j-th of g equal
+    runs of heads.  Returns (first head, number of heads)."""
+    per_block = n_qkv_cols // (3 * head_dim)
+    assert per_block * 3 * head_dim == n_qkv_cols and per_block % scatter_size == 0
+    hd = per_block // scatter_size
+    return scatter_index * hd, hd
+
+
+def attention_core_local(qkv_loc, batch, seq, head_dim, scatter_size, scatter_index):
+    """One device's attention core: its heads of the reduced QKV block
+    qkv_loc [batch*seq, 3*h_blk] (token rows sequence-major).  Returns
+    (o [batch*seq, Hd*head_dim] with the device's heads in order, lse
+    [Hd, batch*seq])."""
+    qkv = _f64(qkv_loc)
+    T = batch * seq
+    h0, hd = attention_heads(qkv.shape[1], head_dim, scatter_size, scatter_index)
+    o = np.zeros((T, hd * head_dim))
+    lse = np.zeros((hd, T))
+    for j in range(hd):
+        c = 3 * head_dim * (h0 + j)
+        for b in range(batch):
+            r = slice(b * seq, (b + 1) * seq)
+            q = qkv[r, c:c + head_dim]
+            k = qkv[r, c + head_dim:c + 2 * head_dim]
+            v = qkv[r, c + 2 * head_dim:c + 3 * head_dim]
+            o[r, j * head_dim:(j + 1) * head_dim], lse[j, r] = attention_fwd(q, k, v)
+    return o, lse
+
+
+def attention_core_bwd_local(qkv_loc, dout_dev, batch, seq, head_dim, scatter_size,
+                             scatter_index):
+    """Gradient of attention_core_local: dout_dev [batch*seq, Hd*head_dim] ->
+    d_qkv [batch*seq, Hd*3*head_dim] for the device's heads, each as
+    [dq | dk | dv] (the QKV block's column order, restricted to its heads)."""
+    qkv = _f64(qkv_loc)
+    do = _f64(dout_dev)
+    T = batch * seq
+    h0, hd = attention_heads(qkv.shape[1], head_dim, scatter_size, scatter_index)
+    dqkv = np.zeros((T, hd * 3 * head_dim))
+    for j in range(hd):
+        c = 3 * head_dim * (h0 + j)
+        o3 = 3 * head_dim * j
+        for b in range(batch):
+            r = slice(b * seq, (b + 1) * seq)
+            q = qkv[r, c:c + head_dim]
+            k = qkv[r, c + head_dim:c + 2 * head_dim]
+            v = qkv[r, c + 2 * head_dim:c + 3 * head_dim]
+            dq, dk, dv = attention_bwd(q, k, v, do[r, j * head_dim:(j + 1) * head_dim])
+            dqkv[r, o3:o3 + head_dim] = dq
+            dqkv[r, o3 + head_dim:o3 + 2 * head_dim] = dk
+            dqkv[r, o3 + 2 * head_dim:o3 + 3 * head_dim] = dv
+    return dqkv

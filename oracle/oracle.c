@@ -9,6 +9,7 @@
 
 #include <math.h>
 #include <stddef.h>
+#include <stdlib.h>
 #ifdef _OPENMP
 #include <omp.h>
 #endif
@@ -149,4 +150,95 @@ int orc_num_threads(void) {
 #else
     return 1;
 #endif
+}
+
+/* Scores of row t against keys 0..t, in ascending u. */
+static void attn_scores(int64_t t, int64_t d, const double* q, int64_t ldq, const double* k,
+                        int64_t ldk, double* s) {
+    const double inv = 1.0 / sqrt((double)d);
+    for (int64_t u = 0; u <= t; ++u) {
+        double acc = 0.0;
+        for (int64_t e = 0; e < d; ++e) acc += q[t * ldq + e] * k[u * ldk + e];
+        s[u] = acc * inv;
+    }
+}
+
+/* lse of scores s[0..n-1]: the largest score is taken out before exp. */
+static double attn_lse(int64_t n, const double* s) {
+    double mx = s[0];
+    for (int64_t u = 1; u < n; ++u)
+        if (s[u] > mx) mx = s[u];
+    double sum = 0.0;
+    for (int64_t u = 0; u < n; ++u) sum += exp(s[u] - mx);
+    return mx + log(sum);
+}
+
+void orc_attention_fwd(int64_t S, int64_t d, const double* q, int64_t ldq, const double* k,
+                       int64_t ldk, const double* v, int64_t ldv, double* o, int64_t ldo,
+                       double* lse) {
+#pragma omp parallel
+    {
+        double* s = (double*)malloc(sizeof(double) * (size_t)(S > 0 ? S : 1));
+#pragma omp for schedule(dynamic, 8)
+        for (int64_t t = 0; t < S; ++t) {
+            attn_scores(t, d, q, ldq, k, ldk, s);
+            const double l = attn_lse(t + 1, s);
+            for (int64_t e = 0; e < d; ++e) {
+                double acc = 0.0;
+                for (int64_t u = 0; u <= t; ++u) acc += exp(s[u] - l) * v[u * ldv + e];
+                o[t * ldo + e] = acc;
+            }
+            if (lse) lse[t] = l;
+        }
+        free(s);
+    }
+}
+
+void orc_attention_bwd(int64_t S, int64_t d, const double* q, int64_t ldq, const double* k,
+                       int64_t ldk, const double* v, int64_t ldv, const double* dout,
+                       int64_t lddo, double* dq, int64_t lddq, double* dk, int64_t lddk,
+                       double* dv, int64_t lddv) {
+    const double inv = 1.0 / sqrt((double)d);
+    /* dS (lower triangle, row-major [S][S]) from P and dP = dO V^T */
+    double* ds = (double*)calloc((size_t)(S > 0 ? S * S : 1), sizeof(double));
+    double* p = (double*)calloc((size_t)(S > 0 ? S * S : 1), sizeof(double));
+#pragma omp parallel
+    {
+        double* s = (double*)malloc(sizeof(double) * (size_t)(S > 0 ? S : 1));
+#pragma omp for schedule(dynamic, 8)
+        for (int64_t t = 0; t < S; ++t) {
+            attn_scores(t, d, q, ldq, k, ldk, s);
+            const double l = attn_lse(t + 1, s);
+            double D = 0.0;
+            for (int64_t u = 0; u <= t; ++u) {
+                p[t * S + u] = exp(s[u] - l);
+                double dp = 0.0;
+                for (int64_t e = 0; e < d; ++e) dp += dout[t * lddo + e] * v[u * ldv + e];
+                ds[t * S + u] = dp;          /* dP for now */
+                D += p[t * S + u] * dp;
+            }
+            for (int64_t u = 0; u <= t; ++u) ds[t * S + u] = p[t * S + u] * (ds[t * S + u] - D);
+        }
+        free(s);
+    }
+#pragma omp parallel for schedule(dynamic, 8)
+    for (int64_t t = 0; t < S; ++t)
+        for (int64_t e = 0; e < d; ++e) {
+            double acc = 0.0;
+            for (int64_t u = 0; u <= t; ++u) acc += ds[t * S + u] * k[u * ldk + e];
+            dq[t * lddq + e] = acc * inv;
+        }
+#pragma omp parallel for schedule(dynamic, 8)
+    for (int64_t u = 0; u < S; ++u)
+        for (int64_t e = 0; e < d; ++e) {
+            double ak = 0.0, av = 0.0;
+            for (int64_t t = u; t < S; ++t) {
+                ak += ds[t * S + u] * q[t * ldq + e];
+                av += p[t * S + u] * dout[t * lddo + e];
+            }
+            dk[u * lddk + e] = ak * inv;
+            dv[u * lddv + e] = av;
+        }
+    free(ds);
+    free(p);
 }

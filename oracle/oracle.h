@@ -95,6 +95,28 @@ double orc_round_bf16(double x);
 /* Number of OpenMP threads the oracle runs with. */
 int orc_num_threads(void);
 
+/* Attention core of one head over one sequence of S tokens (Sec. 2.1,
+ * Formula (mha), with the causal mask of a decoder-only GPT, Sec. 5):
+ *   s[t][u] = (q_t . k_u) / sqrt(d)              for u <= t
+ *   p[t][u] = exp(s[t][u] - lse[t]),  lse[t] = log sum_{u<=t} exp(s[t][u])
+ *   o[t]    = sum_{u<=t} p[t][u] v_u
+ * q, k, v, o are [S][d] rows with leading dimensions ldq, ldk, ldv, ldo;
+ * lse is [S]. */
+void orc_attention_fwd(int64_t S, int64_t d, const double* q, int64_t ldq, const double* k,
+                       int64_t ldk, const double* v, int64_t ldv, double* o, int64_t ldo,
+                       double* lse);
+
+/* Its gradient given dO: with P as above and D[t] = sum_u p[t][u] (dO_t . v_u),
+ *   dV_u = sum_{t>=u} p[t][u] dO_t
+ *   dS[t][u] = p[t][u] (dO_t . v_u - D[t])
+ *   dQ_t = sum_{u<=t} dS[t][u] k_u / sqrt(d),   dK_u = sum_{t>=u} dS[t][u] q_t / sqrt(d)
+ * (the derivative of softmax and of the scaled products; D[t] equals
+ * dO_t . o_t). */
+void orc_attention_bwd(int64_t S, int64_t d, const double* q, int64_t ldq, const double* k,
+                       int64_t ldk, const double* v, int64_t ldv, const double* dout,
+                       int64_t lddo, double* dq, int64_t lddq, double* dk, int64_t lddk,
+                       double* dv, int64_t lddv);
+
 #ifdef __cplusplus
 }
 #endif
