@@ -290,6 +290,29 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
                          const atp_block_bwd_io* io, void* workspace, size_t ws_bytes,
                          void* compute_stream, void* comm_stream, void* aux_stream);
 
+/* One device's attention core (Sec. 2.1 Formula (mha), causal; the
+ * attention block of Sec. 3.2.1).  qkv is the device's reduced QKV output
+ * block for block_mode on the mesh (bf16 [batch*seq, ld_qkv], token rows
+ * sequence-major, the n_loc columns atp_block_fwd's QKV linear produces).
+ * The block holds n_loc / 384 whole heads of dimension h / heads, which
+ * must be 128, each as [q | k | v] columns.  The block is replicated over
+ * the group that reduced it; the attention block scatters it over that
+ * group, so the device attends over the r-th of g equal runs of heads,
+ * r = its index in the group, g = the group's size.  The output goes to
+ * out (bf16 [batch*seq, ld_out], at least n_loc / 3 columns: the gathered
+ * input of out-proj): the device writes its heads' columns, the r-th run of
+ * h/heads-wide column blocks, and leaves the other members' columns (the
+ * all-gather) alone.  lse (fp32 [heads_of_device][batch*seq]) receives the
+ * natural-log softmax denominator of every row, for the backward.  The
+ * caller owns every buffer; work is enqueued on `stream`.
+ * Errors: INVALID_ARGUMENT for a bad mesh, negative sizes, NULL or aliased
+ * buffers, ld below the row length; SHAPE when h is not a multiple of
+ * heads or the heads do not divide over the group; UNSUPPORTED for a head
+ * dimension other than 128, sizes above 2^24, misalignment. */
+atp_status atp_attention_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t batch, int64_t seq,
+                             int64_t h, int32_t heads, const void* qkv, int64_t ld_qkv,
+                             void* out, int64_t ld_out, float* lse, void* stream);
+
 /* Per-kernel timing of the library's own launches.  When enabled, every
  * kernel the library enqueues is bracketed by HIP events on its stream;
  * atp_profile_collect synchronises those events, fills up to `max`

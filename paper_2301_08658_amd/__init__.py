@@ -14,4 +14,5 @@ from .binding import Hcm, hcm_mi355x_xgmi, model_dims  # noqa: F401
 
 __all__ = [n for n in dir() if n.startswith(("atp_", "ATP_"))] + [
     "load_library", "AtpError", "HipEvent", "LIB_PATH", "EXPORTS", "mesh", "block_geometry",
+    "attention_heads",
     "Hcm", "hcm_mi355x_xgmi", "model_dims"]

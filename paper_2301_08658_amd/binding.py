@@ -126,6 +126,7 @@ EXPORTS = (
     "atp_shard_linear_bwd", "atp_block_workspace_bytes", "atp_block_fwd", "atp_block_bwd",
     "atp_profile_enable", "atp_profile_collect", "atp_status_string", "atp_last_error",
     "atp_version", "atp_tcomm", "atp_hcm_mesh_cost", "atp_plan_mesh", "atp_transpose_bf16",
+    "atp_attention_fwd",
 )
 
 _lib = None
@@ -174,6 +175,8 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.atp_version.restype = ctypes.c_char_p
     lib.atp_transpose_bf16.argtypes = [i64, i64, _vp, i64, _vp, i64, _vp]
     lib.atp_transpose_bf16.restype = i32
+    lib.atp_attention_fwd.argtypes = [mp, i32, i64, i64, i64, i32, _vp, i64, _vp, i64, _vp, _vp]
+    lib.atp_attention_fwd.restype = i32
     hp, dp, cp = (ctypes.POINTER(atp_hcm_layer), ctypes.POINTER(atp_model_dims),
                   ctypes.POINTER(atp_mesh_cost))
     lib.atp_tcomm.argtypes = [dp, i32, i32, ctypes.c_double, ctypes.c_double,
@@ -488,6 +491,31 @@ def atp_transpose_bf16(src, dst, stream=None):
     dp_, ldd = _mat(dst, cols, rows, torch.bfloat16, "dst")
     _check(load_library().atp_transpose_bf16(int(rows), int(cols), sp, lds, dp_, ldd,
                                              _stream(stream)))
+
+
+def attention_heads(m: atp_mesh, block_mode: int, h: int, heads: int):
+    """(first head, number of heads) of the device's run of its QKV block's
+    heads (block-local indices), and the block's head count."""
+    g = block_geometry(m, block_mode, h)[0]
+    per_block = g.n_loc // (3 * (h // heads))
+    hd = per_block // g.red_size
+    return g.red_index * hd, hd, per_block
+
+
+def atp_attention_fwd(m: atp_mesh, block_mode: int, batch: int, seq: int, h: int, heads: int,
+                      qkv, out, lse, stream=None):
+    """The device's attention core: qkv [batch*seq, n_loc] bf16 (its reduced
+    QKV block), out [batch*seq, >= n_loc/3] bf16 (the gathered out-proj
+    input; the device's columns are written), lse [heads_dev, batch*seq] fp32."""
+    T = batch * seq
+    g = block_geometry(m, block_mode, h)[0]
+    qp, ldq = _mat(qkv, T, g.n_loc, torch.bfloat16, "qkv")
+    op, ldo = _mat(out, T, g.n_loc // 3, torch.bfloat16, "out")
+    if lse is not None and (lse.dtype != torch.float32 or not lse.is_contiguous()):
+        raise ValueError("lse must be a contiguous float32 tensor")
+    _check(load_library().atp_attention_fwd(ctypes.byref(m), int(block_mode), int(batch), int(seq),
+                                            int(h), int(heads), qp, ldq, op, ldo, _ptr(lse),
+                                            _stream(stream)))
 
 
 # ---------------------------------------------------------------------------

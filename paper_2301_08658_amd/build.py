@@ -11,7 +11,7 @@ CSRC = os.path.join(HERE, "csrc")
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libatp.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
-SOURCES = ["gemm.hip", "reduce.hip", "transpose.hip", "abi.hip"]
+SOURCES = ["gemm.hip", "reduce.hip", "transpose.hip", "attention.hip", "abi.hip"]
 HOST_SOURCES = ["planner.cpp"]
 ARCH = "gfx950"
 

@@ -455,6 +455,45 @@ atp_status refuse_capture_without_workspace(void* compute_stream) {
 
 double gemm_flops(int64_t m, int64_t n, int64_t k) { return 2.0 * (double)m * (double)n * (double)k; }
 
+// One device's share of the attention core (Sec. 3.2.1): its QKV block holds
+// heads_blk whole heads ([q | k | v] columns each); the block is replicated
+// over the group that reduced it, and member j of that group takes the j-th
+// of red_size equal runs of heads.
+constexpr int kHeadDim = 128;
+struct AttnPlan {
+    int64_t T, qkv_cols, out_cols;
+    int heads_blk, hd, first;
+};
+
+atp_status attention_plan(const atp_mesh* mesh, int32_t bm, int64_t batch, int64_t seq,
+                          int64_t h, int32_t heads, AttnPlan* ap) {
+    ATP_CHECK(check_mesh(mesh));
+    BlockPlan P;
+    ATP_CHECK(block_plan(mesh, bm, h, &P));
+    if (batch < 0 || seq < 0) return set_error(ATP_ERR_INVALID_ARGUMENT, "negative batch or seq");
+    if (seq > (1 << 24) || batch > (1 << 24))
+        return set_error(ATP_ERR_UNSUPPORTED, "batch and seq must be at most 2^24");
+    if (heads <= 0 || h % heads)
+        return set_error(ATP_ERR_SHAPE, "h=%lld is not a multiple of heads=%d", (long long)h, heads);
+    if (h / heads != kHeadDim)
+        return set_error(ATP_ERR_UNSUPPORTED, "head dimension %lld: only %d is built",
+                         (long long)(h / heads), kHeadDim);
+    const atp_shard& g = P.g[0];
+    if (g.n_loc % (3 * kHeadDim))
+        return set_error(ATP_ERR_SHAPE, "the QKV block (%lld columns) does not hold whole heads",
+                         (long long)g.n_loc);
+    ap->heads_blk = (int)(g.n_loc / (3 * kHeadDim));
+    if (ap->heads_blk % g.red_size)
+        return set_error(ATP_ERR_SHAPE, "%d heads of the QKV block do not divide over a group of %d",
+                         ap->heads_blk, g.red_size);
+    ap->hd = ap->heads_blk / g.red_size;
+    ap->first = g.red_index * ap->hd;
+    ap->T = batch * seq;
+    ap->qkv_cols = g.n_loc;
+    ap->out_cols = (int64_t)ap->heads_blk * kHeadDim;
+    return ATP_OK;
+}
+
 }  // namespace
 
 // ===========================================================================
@@ -609,6 +648,37 @@ size_t atp_block_workspace_bytes(const atp_mesh* mesh, int32_t block_mode, int64
         tokens < 0)
         return 0;
     return std::max(ws_fwd_bytes(P, tokens), ws_bwd_bytes(P, tokens));
+}
+
+atp_status atp_attention_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t batch,
+                             int64_t seq, int64_t h, int32_t heads, const void* qkv,
+                             int64_t ld_qkv, void* out, int64_t ld_out, float* lse,
+                             void* stream) {
+    AttnPlan ap;
+    ATP_CHECK(attention_plan(mesh, block_mode, batch, seq, h, heads, &ap));
+    ATP_CHECK(check_mat(qkv, ap.T, ld_qkv, ap.qkv_cols, "qkv"));
+    ATP_CHECK(check_mat(out, ap.T, ld_out, ap.out_cols, "out"));
+    if (ap.T == 0) return ATP_OK;
+    ATP_CHECK(check_vec(lse, "lse"));
+    if (qkv == out) return set_error(ATP_ERR_INVALID_ARGUMENT, "qkv and out must not alias");
+    atp::AttentionProblem p;
+    p.qkv = qkv;
+    p.ld_qkv = ld_qkv;
+    p.qkv_col0 = (int64_t)ap.first * 3 * kHeadDim;
+    p.out = out;
+    p.ld_out = ld_out;
+    p.out_col0 = (int64_t)ap.first * kHeadDim;
+    p.lse = lse;
+    p.batch = batch;
+    p.seq = seq;
+    p.heads = ap.hd;
+    p.head_dim = kHeadDim;
+    // causal: 2 d flops per (query, key <= query) pair in each of QK^T and PV
+    const double pairs = (double)batch * ap.hd * (double)seq * (double)(seq + 1) / 2.0;
+    const double flops = 4.0 * kHeadDim * pairs;
+    const double bytes = (double)ap.T * ap.hd * (4.0 * kHeadDim * 2.0 + 4.0);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return timed("attention_fwd", flops, bytes, s, [&] { return atp::launch_attention_fwd(p, s); });
 }
 
 atp_status atp_transpose_bf16(int64_t rows, int64_t cols, const void* src, int64_t lds, void* dst,

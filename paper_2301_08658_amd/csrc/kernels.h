@@ -69,6 +69,21 @@ hipError_t launch_reduce(const ReduceProblem& p, hipStream_t s);
 hipError_t launch_split_sum(const float* ws, int S, int64_t stride, int64_t ld, int64_t rows,
                             int64_t cols, float* out, int64_t ldo, hipStream_t s);
 
+// Causal attention of `heads` consecutive heads over `batch` sequences of
+// `seq` tokens (token rows sequence-major).  Head j's q, k, v are the
+// head_dim-wide column runs at qkv_col0 + 3*head_dim*j + {0, 1, 2}*head_dim of
+// qkv (bf16, ld ld_qkv); its output goes to columns out_col0 + head_dim*j of
+// out (bf16, ld ld_out) and its row log-sum-exps to lse[j*batch*seq + t]
+// (fp32, natural log).  head_dim must be 128.
+struct AttentionProblem {
+    const void* qkv; int64_t ld_qkv, qkv_col0;
+    void* out; int64_t ld_out, out_col0;
+    float* lse;
+    int64_t batch, seq;
+    int heads, head_dim;
+};
+hipError_t launch_attention_fwd(const AttentionProblem& p, hipStream_t s);
+
 // db[n] = sum_t dy[t*ld + n], dy bf16 [T, N], db f32 [N]; fixed summation order.
 hipError_t launch_colsum(const void* dy, int64_t ld, int64_t T, int64_t N, float* db,
                          hipStream_t s);

@@ -1,0 +1,94 @@
+"""The attention core of one device (Sec. 2.1 Formula (mha), causal; the
+attention block of Sec. 3.2.1) against the oracle on the same seeded QKV
+block: the device's run of heads, its output columns of the gathered
+out-proj input (the other members' columns untouched) and the row
+log-sum-exps, over meshes, block modes, coordinates, ragged sequence
+lengths and several sequences."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2301_08658_amd as atp
+import synth_inputs as S
+from helpers import DEV, assert_close, block_mode_code, to64
+
+pytestmark = pytest.mark.gpu
+HD = 128
+
+
+def _run(mode, mesh, coord, batch, seq, h, seed, sigma=1.0):
+    m = atp.mesh(mesh[0], mesh[1], coord[0], coord[1])
+    bm = block_mode_code(mode)
+    heads = h // HD
+    g = atp.block_geometry(m, bm, h)[0]
+    T = batch * seq
+    qkv = S.randn_bf16((T, g.n_loc), sigma, seed, 301).to(DEV)
+    first, hd, per_block = atp.attention_heads(m, bm, h, heads)
+    out = torch.full((T, g.n_loc // 3), -7.0, dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty((hd, T), dtype=torch.float32, device=DEV)
+    atp.atp_attention_fwd(m, bm, batch, seq, h, heads, qkv, out, lse)
+    torch.cuda.synchronize()
+    ref_o, ref_lse = O.attention_core_local(qkv.cpu(), batch, seq, HD, g.red_size, g.red_index)
+    return out, lse, ref_o, ref_lse, first, hd
+
+
+@pytest.mark.parametrize("mode,mesh,coord,batch,seq,h", [
+    ("col", (2, 2), (1, 0), 1, 64, 512),
+    ("col", (2, 2), (0, 1), 2, 100, 512),      # ragged tile
+    ("row", (2, 2), (1, 1), 3, 130, 512),
+    ("col", (1, 1), (0, 0), 2, 1, 512),        # one token
+    ("col", (2, 4), (1, 2), 2, 257, 4096),     # GPT h=4096 heads, 4 per device
+    ("row", (4, 2), (3, 1), 1, 192, 4096),
+    ("col", (8, 1), (5, 0), 1, 320, 4096),     # Megatron's mesh: whole block per device
+])
+def test_attention_fwd_matches_oracle(mode, mesh, coord, batch, seq, h):
+    print(f"attention {mode} {mesh} {coord} b={batch} s={seq} h={h}", flush=True)
+    out, lse, ref_o, ref_lse, first, hd = _run(mode, mesh, coord, batch, seq, h, seed=51)
+    cols = slice(first * HD, (first + hd) * HD)
+    assert_close(out[:, cols], ref_o, "attention output")
+    np.testing.assert_allclose(to64(lse), ref_lse, rtol=0, atol=2e-3)
+    rest = torch.ones(out.shape[1], dtype=torch.bool)
+    rest[cols] = False
+    assert torch.all(out[:, rest.to(DEV)] == -7.0), "columns of other group members written"
+
+
+def test_attention_fwd_full_gpt_sequence():
+    """Four 2048-token sequences of the GPT h=4096 layer on the 2 x 4 mesh."""
+    out, lse, ref_o, ref_lse, first, hd = _run("col", (2, 4), (0, 3), 4, 2048, 4096, seed=52)
+    cols = slice(first * HD, (first + hd) * HD)
+    assert_close(out[:, cols], ref_o, "attention output")
+    np.testing.assert_allclose(to64(lse), ref_lse, rtol=0, atol=2e-3)
+
+
+def test_attention_fwd_uniform_queries_give_prefix_means():
+    """q = 0: every row averages the values of its prefix (closed form)."""
+    m = atp.mesh(1, 1, 0, 0)
+    h, seq = 512, 150
+    g = atp.block_geometry(m, atp.ATP_BLOCK_COL, h)[0]
+    qkv = S.randn_bf16((seq, g.n_loc), 1.0, 53, 302).to(DEV)
+    for hh in range(4):
+        qkv[:, hh * 3 * HD:hh * 3 * HD + HD] = 0
+    out = torch.empty((seq, h), dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty((4, seq), dtype=torch.float32, device=DEV)
+    atp.atp_attention_fwd(m, atp.ATP_BLOCK_COL, 1, seq, h, 4, qkv, out, lse)
+    torch.cuda.synchronize()
+    q = to64(qkv)
+    for hh in range(4):
+        v = q[:, hh * 3 * HD + 2 * HD:hh * 3 * HD + 3 * HD]
+        prefix = np.cumsum(v, axis=0) / np.arange(1, seq + 1)[:, None]
+        assert_close(out[:, hh * HD:(hh + 1) * HD], prefix, f"head {hh}")
+    np.testing.assert_allclose(to64(lse), np.log(np.arange(1, seq + 1))[None, :].repeat(4, 0),
+                               rtol=0, atol=1e-5)
+
+
+def test_attention_fwd_empty_and_errors():
+    m = atp.mesh(2, 2, 0, 0)
+    z = torch.empty((0, 768), dtype=torch.bfloat16, device=DEV)
+    atp.atp_attention_fwd(m, atp.ATP_BLOCK_COL, 0, 64, 512, 4, z,
+                          torch.empty((0, 256), dtype=torch.bfloat16, device=DEV), None)
+    qkv = torch.zeros((64, 768), dtype=torch.bfloat16, device=DEV)
+    out = torch.zeros((64, 256), dtype=torch.bfloat16, device=DEV)
+    lse = torch.zeros((2, 64), dtype=torch.float32, device=DEV)
+    with pytest.raises(atp.AtpError):       # head dimension 64 is not built
+        atp.atp_attention_fwd(m, atp.ATP_BLOCK_COL, 1, 64, 512, 8, qkv, out, lse)
