@@ -313,6 +313,25 @@ atp_status atp_attention_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t b
                              int64_t h, int32_t heads, const void* qkv, int64_t ld_qkv,
                              void* out, int64_t ld_out, float* lse, void* stream);
 
+/* Gradient of atp_attention_fwd (Sec. 2.1 Formula (mha), the backward of
+ * Sec. 4.2 applied to the attention core).  qkv, out and lse are the
+ * forward's input, output (the gathered block; the device's columns are
+ * read) and saved row log-sum-exps; d_out (bf16, same shape and columns as
+ * out) is the gradient of the gathered out-proj input.  The device writes
+ * dq, dk, dv of its heads into d_qkv (bf16, the QKV block's shape and
+ * column order) at its heads' columns and leaves the other members'
+ * columns alone (the conjugate of the scatter).  delta is caller-owned fp32
+ * scratch of heads_of_device * batch * seq values.  P is recomputed from
+ * lse; with delta_t = dO_t . O_t: dV = P^T dO, dS = P o (dO V^T - delta),
+ * dQ = dS K / sqrt(d), dK = dS^T Q / sqrt(d), each accumulated by one
+ * workgroup (deterministic).  Errors as atp_attention_fwd; d_qkv must not
+ * alias an input. */
+atp_status atp_attention_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t batch, int64_t seq,
+                             int64_t h, int32_t heads, const void* qkv, int64_t ld_qkv,
+                             const void* out, int64_t ld_out, const float* lse, const void* d_out,
+                             int64_t ld_dout, void* d_qkv, int64_t ld_dqkv, float* delta,
+                             void* stream);
+
 /* Per-kernel timing of the library's own launches.  When enabled, every
  * kernel the library enqueues is bracketed by HIP events on its stream;
  * atp_profile_collect synchronises those events, fills up to `max`

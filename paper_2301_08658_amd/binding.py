@@ -126,7 +126,7 @@ EXPORTS = (
     "atp_shard_linear_bwd", "atp_block_workspace_bytes", "atp_block_fwd", "atp_block_bwd",
     "atp_profile_enable", "atp_profile_collect", "atp_status_string", "atp_last_error",
     "atp_version", "atp_tcomm", "atp_hcm_mesh_cost", "atp_plan_mesh", "atp_transpose_bf16",
-    "atp_attention_fwd",
+    "atp_attention_fwd", "atp_attention_bwd",
 )
 
 _lib = None
@@ -177,6 +177,9 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.atp_transpose_bf16.restype = i32
     lib.atp_attention_fwd.argtypes = [mp, i32, i64, i64, i64, i32, _vp, i64, _vp, i64, _vp, _vp]
     lib.atp_attention_fwd.restype = i32
+    lib.atp_attention_bwd.argtypes = [mp, i32, i64, i64, i64, i32, _vp, i64, _vp, i64, _vp, _vp,
+                                      i64, _vp, i64, _vp, _vp]
+    lib.atp_attention_bwd.restype = i32
     hp, dp, cp = (ctypes.POINTER(atp_hcm_layer), ctypes.POINTER(atp_model_dims),
                   ctypes.POINTER(atp_mesh_cost))
     lib.atp_tcomm.argtypes = [dp, i32, i32, ctypes.c_double, ctypes.c_double,
@@ -516,6 +519,24 @@ def atp_attention_fwd(m: atp_mesh, block_mode: int, batch: int, seq: int, h: int
     _check(load_library().atp_attention_fwd(ctypes.byref(m), int(block_mode), int(batch), int(seq),
                                             int(h), int(heads), qp, ldq, op, ldo, _ptr(lse),
                                             _stream(stream)))
+
+
+def atp_attention_bwd(m: atp_mesh, block_mode: int, batch: int, seq: int, h: int, heads: int,
+                      qkv, out, lse, d_out, d_qkv, delta, stream=None):
+    """Gradient of atp_attention_fwd: d_qkv (the QKV block's shape) receives
+    dq, dk, dv of the device's heads; delta is fp32 scratch [heads_dev*T]."""
+    T = batch * seq
+    g = block_geometry(m, block_mode, h)[0]
+    qp, ldq = _mat(qkv, T, g.n_loc, torch.bfloat16, "qkv")
+    op, ldo = _mat(out, T, g.n_loc // 3, torch.bfloat16, "out")
+    dop, lddo = _mat(d_out, T, g.n_loc // 3, torch.bfloat16, "d_out")
+    dqp, lddq = _mat(d_qkv, T, g.n_loc, torch.bfloat16, "d_qkv")
+    for t, nm in ((lse, "lse"), (delta, "delta")):
+        if t is not None and (t.dtype != torch.float32 or not t.is_contiguous()):
+            raise ValueError(f"{nm} must be a contiguous float32 tensor")
+    _check(load_library().atp_attention_bwd(ctypes.byref(m), int(block_mode), int(batch), int(seq),
+                                            int(h), int(heads), qp, ldq, op, ldo, _ptr(lse), dop,
+                                            lddo, dqp, lddq, _ptr(delta), _stream(stream)))
 
 
 # ---------------------------------------------------------------------------

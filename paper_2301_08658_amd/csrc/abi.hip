@@ -681,6 +681,48 @@ atp_status atp_attention_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t b
     return timed("attention_fwd", flops, bytes, s, [&] { return atp::launch_attention_fwd(p, s); });
 }
 
+atp_status atp_attention_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t batch,
+                             int64_t seq, int64_t h, int32_t heads, const void* qkv,
+                             int64_t ld_qkv, const void* out, int64_t ld_out, const float* lse,
+                             const void* d_out, int64_t ld_dout, void* d_qkv, int64_t ld_dqkv,
+                             float* delta, void* stream) {
+    AttnPlan ap;
+    ATP_CHECK(attention_plan(mesh, block_mode, batch, seq, h, heads, &ap));
+    ATP_CHECK(check_mat(qkv, ap.T, ld_qkv, ap.qkv_cols, "qkv"));
+    ATP_CHECK(check_mat(out, ap.T, ld_out, ap.out_cols, "out"));
+    ATP_CHECK(check_mat(d_out, ap.T, ld_dout, ap.out_cols, "d_out"));
+    ATP_CHECK(check_mat(d_qkv, ap.T, ld_dqkv, ap.qkv_cols, "d_qkv"));
+    if (ap.T == 0) return ATP_OK;
+    ATP_CHECK(check_vec(lse, "lse"));
+    ATP_CHECK(check_vec(delta, "delta"));
+    if (d_qkv == qkv || d_qkv == out || d_qkv == d_out)
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "d_qkv must not alias an input");
+    atp::AttentionBwdProblem p;
+    p.qkv = qkv;
+    p.ld_qkv = ld_qkv;
+    p.qkv_col0 = (int64_t)ap.first * 3 * kHeadDim;
+    p.out = out;
+    p.ld_out = ld_out;
+    p.out_col0 = (int64_t)ap.first * kHeadDim;
+    p.dout = d_out;
+    p.ld_dout = ld_dout;
+    p.lse = lse;
+    p.delta = delta;
+    p.dqkv = d_qkv;
+    p.ld_dqkv = ld_dqkv;
+    p.batch = batch;
+    p.seq = seq;
+    p.heads = ap.hd;
+    p.head_dim = kHeadDim;
+    // the five products of the backward over the causal pairs
+    const double pairs = (double)batch * ap.hd * (double)seq * (double)(seq + 1) / 2.0;
+    const double flops = 2.0 * kHeadDim * pairs * 5.0;   // S, dP, dV, dK, dQ (S and dP are
+                                                         // computed twice: not counted)
+    const double bytes = (double)ap.T * ap.hd * (10.0 * kHeadDim * 2.0 + 12.0);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return timed("attention_bwd", flops, bytes, s, [&] { return atp::launch_attention_bwd(p, s); });
+}
+
 atp_status atp_transpose_bf16(int64_t rows, int64_t cols, const void* src, int64_t lds, void* dst,
                               int64_t ldd, void* stream) {
     if (rows < 0 || cols < 0) return set_error(ATP_ERR_INVALID_ARGUMENT, "negative size");

@@ -22,6 +22,18 @@
 //     8 ((n >> 2) & 1)), distinct banks per 32-lane half).
 //   * Exponentials in base 2 (scores scaled by log2(e) / sqrt(128)); the
 //     log-sum-exp of each row is saved (natural log) for the backward.
+//
+// Backward (the gradient of softmax(S) V, S = Q K^T / sqrt(d)): with P
+// recomputed from the saved log-sum-exps and delta_t = dO_t . O_t,
+//   dV = P^T dO,  dS = P o (dO V^T - delta),  dQ = dS K / sqrt(d),
+//   dK = dS^T Q / sqrt(d).
+// One kernel per 64-key tile accumulates dK and dV over the query tiles
+// that see it; one per 64-query tile accumulates dQ over its key tiles; no
+// atomics, so the result does not depend on scheduling.  Every contraction
+// over keys or queries uses the same lane-local ordering as the forward's
+// P V, so probabilities and score gradients never leave their lanes.  All
+// bwd LDS tiles use the layout vpos, which is conflict-free for both
+// ds_read_b128 fragments and the transposing reads.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -234,7 +246,340 @@ __global__ __launch_bounds__(NTHR, 2) void attention_fwd_kernel(AttnArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// backward
+// ---------------------------------------------------------------------------
+struct AttnBwdArgs {
+    const uint16_t* qkv;  int64_t ldq, col0;     // device's heads at col0, [q|k|v] each
+    const uint16_t* out;  int64_t ldo, ocol0;    // forward output
+    const uint16_t* dout; int64_t lddo, docol0;  // its gradient
+    const float* lse;                            // [heads][T], natural log
+    float* delta;                                // [heads][T] scratch
+    uint16_t* dqkv;       int64_t lddq, dcol0;   // gradients, [dq|dk|dv] per head
+    int batch, seq, heads, tiles;
+    float scale_log2, inv_sqrt_d;
+};
+
+__device__ __forceinline__ bf16x8 frag_b128(const uint16_t* t, int n, int c) {
+    return *reinterpret_cast<const bf16x8*>(t + n * D + vpos(n, c) * 8);
+}
+// Transposing fragment of a [row][d] tile: lane (group g, j) gets column
+// 16 dt + j and rows rb + 4 g + 0..3, rb + 16 + 4 g + 0..3.
+__device__ __forceinline__ bf16x8 frag_tr(const uint16_t* t, int rb, int dt, int lane) {
+    const int g = lane >> 4, j16 = lane & 15;
+    const int r0 = rb + 4 * g + (j16 >> 2), r1 = r0 + 16;
+    const int col = 16 * dt + 4 * (j16 & 3), c = col >> 3;
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4*)(t + r0 * D + vpos(r0, c) * 8 + (col & 7)));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4*)(t + r1 * D + vpos(r1, c) * 8 + (col & 7)));
+    const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
+}
+__device__ __forceinline__ bf16x8 pack_pair(const f32x4& a, const f32x4& b) {
+    const u32x4 w = {pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3]), pack_bf16x2(b[0], b[1]),
+                     pack_bf16x2(b[2], b[3])};
+    return __builtin_bit_cast(bf16x8, w);
+}
+
+// Rows [r0, r0 + 64) of two [T][ld] column runs (at c0 and c1) of one
+// sequence into registers; rows past the sequence read zeros.
+__device__ __forceinline__ void load_tiles(const uint16_t* b0, int64_t ld0, const uint16_t* b1,
+                                           int64_t ld1, int64_t tok0, int r0, int seq,
+                                           u32x4 (&x)[4], u32x4 (&y)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int q = threadIdx.x + i * NTHR;
+        const int n = q / CH, c = q % CH;
+        if (r0 + n < seq) {
+            x[i] = *reinterpret_cast<const u32x4*>(b0 + (tok0 + r0 + n) * ld0 + 8 * c);
+            y[i] = *reinterpret_cast<const u32x4*>(b1 + (tok0 + r0 + n) * ld1 + 8 * c);
+        } else {
+            x[i] = u32x4{0, 0, 0, 0};
+            y[i] = u32x4{0, 0, 0, 0};
+        }
+    }
+}
+__device__ __forceinline__ void store_tiles(uint16_t* t0, uint16_t* t1, const u32x4 (&x)[4],
+                                            const u32x4 (&y)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int q = threadIdx.x + i * NTHR;
+        const int n = q / CH, c = q % CH;
+        *reinterpret_cast<u32x4*>(t0 + n * D + vpos(n, c) * 8) = x[i];
+        *reinterpret_cast<u32x4*>(t1 + n * D + vpos(n, c) * 8) = y[i];
+    }
+}
+
+// delta[h][t] = dO_t . O_t over the head's 128 columns (16 lanes per row)
+__global__ __launch_bounds__(NTHR) void attention_delta_kernel(AttnBwdArgs a) {
+    const int64_t T = (int64_t)a.batch * a.seq;
+    const int64_t rid = (int64_t)blockIdx.x * (NTHR / 16) + (threadIdx.x >> 4);
+    const int l16 = threadIdx.x & 15;
+    float acc = 0.f;
+    const bool live = rid < T * a.heads;
+    const int64_t hh = live ? rid / T : 0, t = live ? rid % T : 0;
+    if (live) {
+        const u32x4 o = *reinterpret_cast<const u32x4*>(a.out + t * a.ldo + a.ocol0 + hh * D + 8 * l16);
+        const u32x4 g = *reinterpret_cast<const u32x4*>(a.dout + t * a.lddo + a.docol0 + hh * D +
+                                                        8 * l16);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            acc += __uint_as_float(o[e] << 16) * __uint_as_float(g[e] << 16);
+            acc += __uint_as_float(o[e] & 0xffff0000u) * __uint_as_float(g[e] & 0xffff0000u);
+        }
+    }
+#pragma unroll
+    for (int m = 8; m >= 1; m >>= 1) acc += __shfl_xor(acc, m);
+    if (live && l16 == 0) a.delta[hh * T + t] = acc;
+}
+
+// dK, dV of one 64-key tile (4 waves x 16 keys)
+__global__ __launch_bounds__(NTHR, 2) void attention_dkv_kernel(AttnBwdArgs a) {
+    __shared__ __attribute__((aligned(16))) uint16_t qd[2][2][BM * D];   // [buf][Q|dO]
+    __shared__ float rowv[2][2][BM];                                    // [buf][lse2|delta]
+    const int lane = threadIdx.x & 63, g = lane >> 4;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int bhn = a.batch * a.heads;
+    const int kt = blockIdx.x / bhn;            // short loops (late keys) last
+    const int bh = blockIdx.x % bhn;
+    const int b = bh / a.heads, hh = bh % a.heads;
+    const int64_t tok0 = (int64_t)b * a.seq, T = (int64_t)a.batch * a.seq;
+    const int64_t qc = a.col0 + (int64_t)hh * 3 * D;
+    const uint16_t* qbase = a.qkv + qc;
+    const uint16_t* dobase = a.dout + a.docol0 + (int64_t)hh * D;
+
+    const int kabs = kt * BN + wave * 16 + (lane & 15);
+    bf16x8 kf[4], vf[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+        if (kabs < a.seq) {
+            const uint16_t* row = a.qkv + (tok0 + kabs) * a.ldq + qc;
+            kf[ks] = *reinterpret_cast<const bf16x8*>(row + D + 32 * ks + 8 * g);
+            vf[ks] = *reinterpret_cast<const bf16x8*>(row + 2 * D + 32 * ks + 8 * g);
+        } else {
+            kf[ks] = __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0});
+            vf[ks] = kf[ks];
+        }
+    }
+    f32x4 dk[8], dv[8];
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) {
+        dk[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        dv[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+
+    auto load_rows = [&](int qt, float& l2, float& dl) {
+        const int t = qt * BM + (int)threadIdx.x;
+        if (threadIdx.x < BM && t < a.seq) {
+            l2 = a.lse[(int64_t)hh * T + tok0 + t] * 1.44269504088896340736f;
+            dl = a.delta[(int64_t)hh * T + tok0 + t];
+        } else {
+            l2 = 0.f;
+            dl = 0.f;
+        }
+    };
+    u32x4 xr[4], yr[4];
+    float l2r, dlr;
+    const int q0 = kt, nq = a.tiles;
+    load_tiles(qbase, a.ldq, dobase, a.lddo, tok0, q0 * BM, a.seq, xr, yr);
+    load_rows(q0, l2r, dlr);
+    store_tiles(qd[0][0], qd[0][1], xr, yr);
+    if (threadIdx.x < BM) { rowv[0][0][threadIdx.x] = l2r; rowv[0][1][threadIdx.x] = dlr; }
+    __syncthreads();
+    for (int qt = q0; qt < nq; ++qt) {
+        const int buf = (qt - q0) & 1;
+        const uint16_t* qs = qd[buf][0];
+        const uint16_t* ds_ = qd[buf][1];
+        if (qt + 1 < nq) {
+            load_tiles(qbase, a.ldq, dobase, a.lddo, tok0, (qt + 1) * BM, a.seq, xr, yr);
+            load_rows(qt + 1, l2r, dlr);
+        }
+        // S^T and dP^T: lane holds (key = kabs, query = 16 j + 4 g + e)
+        f32x4 p[4], dsv[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f}, dacc = sacc;
+            const int n = 16 * j + (lane & 15);
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+                sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_b128(qs, n, 4 * ks + g), kf[ks],
+                                                               sacc, 0, 0, 0);
+                dacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_b128(ds_, n, 4 * ks + g), vf[ks],
+                                                               dacc, 0, 0, 0);
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int ql = 16 * j + 4 * g + e;
+                const int qabs = qt * BM + ql;
+                float pv = __builtin_amdgcn_exp2f(sacc[e] * a.scale_log2 - rowv[buf][0][ql]);
+                if (qabs < kabs || qabs >= a.seq) pv = 0.f;
+                p[j][e] = pv;
+                dsv[j][e] = pv * (dacc[e] - rowv[buf][1][ql]);
+            }
+        }
+        // dV += P^T dO, dK += dS^T Q over two 32-query slices
+#pragma unroll
+        for (int sl = 0; sl < 2; ++sl) {
+            const bf16x8 pf = pack_pair(p[2 * sl], p[2 * sl + 1]);
+            const bf16x8 sf = pack_pair(dsv[2 * sl], dsv[2 * sl + 1]);
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt) {
+                dv[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_tr(ds_, 32 * sl, dt, lane), pf,
+                                                                 dv[dt], 0, 0, 0);
+                dk[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_tr(qs, 32 * sl, dt, lane), sf,
+                                                                 dk[dt], 0, 0, 0);
+            }
+        }
+        if (qt + 1 < nq) {
+            __syncthreads();
+            const int nb = buf ^ 1;
+            store_tiles(qd[nb][0], qd[nb][1], xr, yr);
+            if (threadIdx.x < BM) { rowv[nb][0][threadIdx.x] = l2r; rowv[nb][1][threadIdx.x] = dlr; }
+            __syncthreads();
+        }
+    }
+    if (kabs < a.seq) {
+        uint16_t* row = a.dqkv + (tok0 + kabs) * a.lddq + a.dcol0 + (int64_t)hh * 3 * D;
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) {
+            const u32x2 wk = {pack_bf16x2(dk[dt][0] * a.inv_sqrt_d, dk[dt][1] * a.inv_sqrt_d),
+                              pack_bf16x2(dk[dt][2] * a.inv_sqrt_d, dk[dt][3] * a.inv_sqrt_d)};
+            const u32x2 wv = {pack_bf16x2(dv[dt][0], dv[dt][1]), pack_bf16x2(dv[dt][2], dv[dt][3])};
+            *reinterpret_cast<u32x2*>(row + D + 16 * dt + 4 * g) = wk;
+            *reinterpret_cast<u32x2*>(row + 2 * D + 16 * dt + 4 * g) = wv;
+        }
+    }
+}
+
+// dQ of one 64-query tile (4 waves x 16 queries)
+__global__ __launch_bounds__(NTHR, 2) void attention_dq_kernel(AttnBwdArgs a) {
+    __shared__ __attribute__((aligned(16))) uint16_t kv[2][2][BN * D];   // [buf][K|V]
+    const int lane = threadIdx.x & 63, g = lane >> 4;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int bhn = a.batch * a.heads;
+    const int qt = a.tiles - 1 - blockIdx.x / bhn;   // long loops first
+    const int bh = blockIdx.x % bhn;
+    const int b = bh / a.heads, hh = bh % a.heads;
+    const int64_t tok0 = (int64_t)b * a.seq, T = (int64_t)a.batch * a.seq;
+    const int64_t qc = a.col0 + (int64_t)hh * 3 * D;
+
+    const int qabs = qt * BM + wave * 16 + (lane & 15);
+    bf16x8 qf[4], of[4];
+    float l2 = 0.f, dl = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+        if (qabs < a.seq) {
+            qf[ks] = *reinterpret_cast<const bf16x8*>(a.qkv + (tok0 + qabs) * a.ldq + qc + 32 * ks +
+                                                      8 * g);
+            of[ks] = *reinterpret_cast<const bf16x8*>(a.dout + (tok0 + qabs) * a.lddo + a.docol0 +
+                                                      (int64_t)hh * D + 32 * ks + 8 * g);
+        } else {
+            qf[ks] = __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0});
+            of[ks] = qf[ks];
+        }
+    }
+    if (qabs < a.seq) {
+        l2 = a.lse[(int64_t)hh * T + tok0 + qabs] * 1.44269504088896340736f;
+        dl = a.delta[(int64_t)hh * T + tok0 + qabs];
+    }
+    f32x4 dq[8];
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) dq[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const uint16_t* kbase = a.qkv + qc + D;
+    const uint16_t* vbase = a.qkv + qc + 2 * D;
+    const int nk = qt + 1;
+    u32x4 xr[4], yr[4];
+    load_tiles(kbase, a.ldq, vbase, a.ldq, tok0, 0, a.seq, xr, yr);
+    store_tiles(kv[0][0], kv[0][1], xr, yr);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+        const uint16_t* ks_ = kv[kt & 1][0];
+        const uint16_t* vs_ = kv[kt & 1][1];
+        if (kt + 1 < nk) load_tiles(kbase, a.ldq, vbase, a.ldq, tok0, (kt + 1) * BN, a.seq, xr, yr);
+        // S and dP: lane holds (query = qabs, key = 16 j + 4 g + e)
+        f32x4 dsv[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f}, dacc = sacc;
+            const int n = 16 * j + (lane & 15);
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+                sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_b128(ks_, n, 4 * ks + g), qf[ks],
+                                                               sacc, 0, 0, 0);
+                dacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_b128(vs_, n, 4 * ks + g), of[ks],
+                                                               dacc, 0, 0, 0);
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int kabs = kt * BN + 16 * j + 4 * g + e;
+                float pv = __builtin_amdgcn_exp2f(sacc[e] * a.scale_log2 - l2);
+                if (kabs > qabs || kabs >= a.seq) pv = 0.f;
+                dsv[j][e] = pv * (dacc[e] - dl);
+            }
+        }
+        // dQ += dS K over two 32-key slices
+#pragma unroll
+        for (int sl = 0; sl < 2; ++sl) {
+            const bf16x8 sf = pack_pair(dsv[2 * sl], dsv[2 * sl + 1]);
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt)
+                dq[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_tr(ks_, 32 * sl, dt, lane), sf,
+                                                                 dq[dt], 0, 0, 0);
+        }
+        if (kt + 1 < nk) {
+            __syncthreads();
+            store_tiles(kv[(kt + 1) & 1][0], kv[(kt + 1) & 1][1], xr, yr);
+            __syncthreads();
+        }
+    }
+    if (qabs < a.seq) {
+        uint16_t* row = a.dqkv + (tok0 + qabs) * a.lddq + a.dcol0 + (int64_t)hh * 3 * D;
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) {
+            const u32x2 w = {pack_bf16x2(dq[dt][0] * a.inv_sqrt_d, dq[dt][1] * a.inv_sqrt_d),
+                             pack_bf16x2(dq[dt][2] * a.inv_sqrt_d, dq[dt][3] * a.inv_sqrt_d)};
+            *reinterpret_cast<u32x2*>(row + 16 * dt + 4 * g) = w;
+        }
+    }
+}
+
 }  // namespace
+
+hipError_t launch_attention_bwd(const AttentionBwdProblem& p, hipStream_t s) {
+    if (p.batch <= 0 || p.seq <= 0 || p.heads <= 0) return hipSuccess;
+    if (p.head_dim != D) return hipErrorInvalidValue;
+    AttnBwdArgs a;
+    a.qkv = static_cast<const uint16_t*>(p.qkv);
+    a.ldq = p.ld_qkv;
+    a.col0 = p.qkv_col0;
+    a.out = static_cast<const uint16_t*>(p.out);
+    a.ldo = p.ld_out;
+    a.ocol0 = p.out_col0;
+    a.dout = static_cast<const uint16_t*>(p.dout);
+    a.lddo = p.ld_dout;
+    a.docol0 = p.out_col0;
+    a.lse = p.lse;
+    a.delta = p.delta;
+    a.dqkv = static_cast<uint16_t*>(p.dqkv);
+    a.lddq = p.ld_dqkv;
+    a.dcol0 = p.qkv_col0;
+    a.batch = (int)p.batch;
+    a.seq = (int)p.seq;
+    a.heads = p.heads;
+    a.tiles = (int)((p.seq + BM - 1) / BM);
+    a.scale_log2 = 1.44269504088896340736f / sqrtf((float)D);
+    a.inv_sqrt_d = 1.0f / sqrtf((float)D);
+    const int64_t rows = p.batch * p.seq * p.heads;
+    const int64_t dgrid = (rows + NTHR / 16 - 1) / (NTHR / 16);
+    const int64_t grid = (int64_t)a.tiles * a.batch * a.heads;
+    if (dgrid > 0x7fffffff || grid > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(attention_delta_kernel, dim3((unsigned)dgrid), dim3(NTHR), 0, s, a);
+    hipLaunchKernelGGL(attention_dkv_kernel, dim3((unsigned)grid), dim3(NTHR), 0, s, a);
+    hipLaunchKernelGGL(attention_dq_kernel, dim3((unsigned)grid), dim3(NTHR), 0, s, a);
+    return hipGetLastError();
+}
 
 hipError_t launch_attention_fwd(const AttentionProblem& p, hipStream_t s) {
     if (p.batch <= 0 || p.seq <= 0 || p.heads <= 0) return hipSuccess;

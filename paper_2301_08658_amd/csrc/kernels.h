@@ -84,6 +84,23 @@ struct AttentionProblem {
 };
 hipError_t launch_attention_fwd(const AttentionProblem& p, hipStream_t s);
 
+// Its gradient: from qkv, the forward output out (its heads at out_col0),
+// the output gradient dout (same columns, ld ld_dout) and the saved lse,
+// write dq, dk, dv of the heads into dqkv at qkv_col0 (the qkv layout, ld
+// ld_dqkv).  delta is fp32 scratch [heads*batch*seq].  Three launches:
+// delta = rowsum(dO o O), dK/dV per key tile, dQ per query tile.
+struct AttentionBwdProblem {
+    const void* qkv; int64_t ld_qkv, qkv_col0;
+    const void* out; int64_t ld_out, out_col0;
+    const void* dout; int64_t ld_dout;
+    const float* lse;
+    float* delta;
+    void* dqkv; int64_t ld_dqkv;
+    int64_t batch, seq;
+    int heads, head_dim;
+};
+hipError_t launch_attention_bwd(const AttentionBwdProblem& p, hipStream_t s);
+
 // db[n] = sum_t dy[t*ld + n], dy bf16 [T, N], db f32 [N]; fixed summation order.
 hipError_t launch_colsum(const void* dy, int64_t ld, int64_t T, int64_t N, float* db,
                          hipStream_t s);

@@ -92,3 +92,64 @@ def test_attention_fwd_empty_and_errors():
     lse = torch.zeros((2, 64), dtype=torch.float32, device=DEV)
     with pytest.raises(atp.AtpError):       # head dimension 64 is not built
         atp.atp_attention_fwd(m, atp.ATP_BLOCK_COL, 1, 64, 512, 8, qkv, out, lse)
+
+
+@pytest.mark.parametrize("mode,mesh,coord,batch,seq,h", [
+    ("col", (2, 2), (1, 0), 1, 64, 512),
+    ("col", (2, 2), (0, 1), 2, 100, 512),      # ragged tile
+    ("row", (2, 2), (1, 1), 3, 130, 512),
+    ("col", (1, 1), (0, 0), 2, 1, 512),        # one token
+    ("col", (2, 4), (1, 2), 2, 257, 4096),
+    ("row", (4, 2), (3, 1), 1, 192, 4096),
+])
+def test_attention_bwd_matches_oracle(mode, mesh, coord, batch, seq, h):
+    print(f"attention bwd {mode} {mesh} {coord} b={batch} s={seq} h={h}", flush=True)
+    m = atp.mesh(mesh[0], mesh[1], coord[0], coord[1])
+    bm = block_mode_code(mode)
+    heads = h // HD
+    g = atp.block_geometry(m, bm, h)[0]
+    T = batch * seq
+    qkv = S.randn_bf16((T, g.n_loc), 1.0, 61, 303).to(DEV)
+    first, hd, per_block = atp.attention_heads(m, bm, h, heads)
+    out = torch.zeros((T, g.n_loc // 3), dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty((hd, T), dtype=torch.float32, device=DEV)
+    atp.atp_attention_fwd(m, bm, batch, seq, h, heads, qkv, out, lse)
+    d_out = S.randn_bf16((T, g.n_loc // 3), 1.0, 61, 304).to(DEV)
+    d_qkv = torch.full((T, g.n_loc), -5.0, dtype=torch.bfloat16, device=DEV)
+    delta = torch.empty((hd * T,), dtype=torch.float32, device=DEV)
+    atp.atp_attention_bwd(m, bm, batch, seq, h, heads, qkv, out, lse, d_out, d_qkv, delta)
+    torch.cuda.synchronize()
+    cols = slice(first * HD, (first + hd) * HD)
+    ref = O.attention_core_bwd_local(qkv.cpu(), d_out[:, cols].cpu(), batch, seq, HD,
+                                     g.red_size, g.red_index)
+    mine = slice(first * 3 * HD, (first + hd) * 3 * HD)
+    got = d_qkv[:, mine]
+    for part, nm in ((0, "dq"), (1, "dk"), (2, "dv")):
+        sel = np.concatenate([np.arange(j * 3 * HD + part * HD, j * 3 * HD + (part + 1) * HD)
+                              for j in range(hd)])
+        assert_close(got[:, torch.as_tensor(sel, device=DEV)], ref[:, sel], nm)
+    rest = torch.ones(g.n_loc, dtype=torch.bool)
+    rest[mine] = False
+    assert torch.all(d_qkv[:, rest.to(DEV)] == -5.0), "columns of other group members written"
+
+
+def test_attention_bwd_deterministic():
+    m = atp.mesh(2, 4, 1, 1)
+    h, batch, seq = 4096, 2, 300
+    g = atp.block_geometry(m, atp.ATP_BLOCK_COL, h)[0]
+    T = batch * seq
+    qkv = S.randn_bf16((T, g.n_loc), 1.0, 62, 305).to(DEV)
+    first, hd, _ = atp.attention_heads(m, atp.ATP_BLOCK_COL, h, 32)
+    out = torch.zeros((T, g.n_loc // 3), dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty((hd, T), dtype=torch.float32, device=DEV)
+    atp.atp_attention_fwd(m, atp.ATP_BLOCK_COL, batch, seq, h, 32, qkv, out, lse)
+    d_out = S.randn_bf16((T, g.n_loc // 3), 1.0, 62, 306).to(DEV)
+    res = []
+    for _ in range(2):
+        d_qkv = torch.zeros((T, g.n_loc), dtype=torch.bfloat16, device=DEV)
+        delta = torch.empty((hd * T,), dtype=torch.float32, device=DEV)
+        atp.atp_attention_bwd(m, atp.ATP_BLOCK_COL, batch, seq, h, 32, qkv, out, lse, d_out,
+                              d_qkv, delta)
+        res.append(d_qkv)
+    torch.cuda.synchronize()
+    assert torch.equal(res[0], res[1])
