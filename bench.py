@@ -58,6 +58,9 @@ def parse():
     ap.add_argument("--copy-calib-mb", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB "
                          "(reference kernel for scaling HBM counters)")
+    ap.add_argument("--attention", action="store_true",
+                    help="time the attention core (fwd+bwd) of one device's heads instead of "
+                         "the linear block: sequences of min(2048, tokens), head dim 128")
     ap.add_argument("--seed", type=int, default=21)
     ap.add_argument("--profile-detail", action="store_true",
                     help="also print per-shape kernel timings to stderr")
@@ -107,6 +110,84 @@ def setup(torch, atp, S, wl, chunks, seed):
     st["dw"] = [torch.empty((g.k_loc, g.n_loc), dtype=torch.float32, device=dev) for g in G]
     st["db"] = [torch.empty((g.n_loc,), dtype=torch.float32, device=dev) for g in G]
     return st
+
+
+def attention_bench(torch, atp, S, args, wl):
+    """The attention core of one device (Sec. 3.2.1): its run of heads of
+    the reduced QKV block, causal, forward then backward, K timed steps."""
+    dev = "cuda:0"
+    d1, d2 = wl["mesh"]
+    m = atp.mesh(d1, d2, 0, 0)
+    bm = atp.ATP_BLOCK_COL if wl["mode"] == "col" else atp.ATP_BLOCK_ROW
+    h, T = wl["h"], wl["tokens"]
+    heads = h // 128
+    seq = min(2048, T)
+    batch = T // seq
+    T = batch * seq
+    g = atp.block_geometry(m, bm, h)[0]
+    first, hd, per_block = atp.attention_heads(m, bm, h, heads)
+    rnd = lambda shape, tid: S.randn_device(shape, 1.0, args.seed, tid, dev)  # noqa: E731
+    qkv = rnd((T, g.n_loc), 401)
+    d_out = rnd((T, g.n_loc // 3), 402)
+    out = torch.empty((T, g.n_loc // 3), dtype=torch.bfloat16, device=dev)
+    d_qkv = torch.empty((T, g.n_loc), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((hd, T), dtype=torch.float32, device=dev)
+    delta = torch.empty((hd * T,), dtype=torch.float32, device=dev)
+
+    def step():
+        atp.atp_attention_fwd(m, bm, batch, seq, h, heads, qkv, out, lse)
+        atp.atp_attention_bwd(m, bm, batch, seq, h, heads, qkv, out, lse, d_out, d_qkv, delta)
+
+    pairs = batch * hd * seq * (seq + 1) / 2.0
+    flops = 2.0 * 128 * pairs * (2 + 5)       # forward QK^T, PV; backward five products
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_step = max(e0.elapsed_time(e1), (time.perf_counter() - t0) * 1e3) / args.steps
+    value = flops / (ms_step * 1e-3) / 1e12
+    atp.atp_profile_enable(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    atp.atp_profile_enable(False)
+    kernels = []
+    for r in atp.atp_profile_collect(16):
+        kernels.append(dict(name=r["name"], avg_us=round(r["total_ms"] / r["launches"] * 1e3, 2),
+                            tflops=round(r["flops"] / (r["total_ms"] * 1e-3) / 1e12, 1)))
+    dom = max(kernels, key=lambda k: k["avg_us"])
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle as O
+        import numpy as np
+        q = qkv[:seq, first * 384:first * 384 + 384].float().cpu().numpy()
+        t1 = time.perf_counter()
+        o_ref, _ = O.attention_fwd(q[:, :128], q[:, 128:256], q[:, 256:])
+        O.attention_bwd(q[:, :128], q[:, 128:256], q[:, 256:], np.ones_like(o_ref))
+        sec = time.perf_counter() - t1
+        cpu = dict(value=round(2.0 * 128 * seq * (seq + 1) / 2.0 * 7 / sec / 1e12, 6),
+                   unit="TFLOP/s", cores=O.num_threads(), kind="oracle",
+                   sample=f"one head, one {seq}-token sequence, forward and backward",
+                   seconds=round(sec, 3))
+    out_line = dict(
+        metric="TFLOP/s, attention core fwd+bwd of one device's heads (causal)",
+        value=round(value, 2), unit="TFLOP/s", n_gpus=1, steps=args.steps, warmup=args.warmup,
+        ms_per_step=round(ms_step, 4), higher_is_better=True, scaling="weak", vs_baseline=None,
+        dtype="bf16", data="synthetic",
+        config=dict(workload=args.workload, part="attention", mode=wl["mode"], mesh=[d1, d2],
+                    coord=[0, 0], h=h, heads=heads, heads_per_device=hd, batch=batch, seq=seq,
+                    gflop_per_step=round(flops / 1e9, 1)),
+        roofline=dict(bound="mfma", kernel=dom["name"], achieved=dom["tflops"],
+                      peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
+                      frac=round(dom["tflops"] / PEAK_BF16_TFLOPS, 4), traffic=None),
+        kernels=kernels, cpu_baseline=cpu)
+    print(json.dumps(out_line), flush=True)
 
 
 def step_flops(st, fwd_only):
@@ -265,6 +346,9 @@ def main():
     chunks = args.chunks or wl["chunks"]
     fwd_only = args.fwd_only or not wl.get("bwd", False)
     atp.load_library()
+    if args.attention:
+        attention_bench(torch, atp, S, args, wl)
+        return
     log(f"[bench] {atp.atp_version()} workload={args.workload} chunks={chunks} "
         f"pass={'fwd' if fwd_only else 'fwd+bwd'}")
     st = setup(torch, atp, S, wl, chunks, args.seed)
