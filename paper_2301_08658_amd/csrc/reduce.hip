@@ -137,21 +137,20 @@ hipError_t launch_r(const ReduceProblem& p, hipStream_t s) {
     return hipGetLastError();
 }
 
-// Column sums: a block owns 16 columns; 32 row lanes x 2 column lanes, each
-// thread 8 columns (one 16-byte load per row), rows t = ty, ty+32, ... in
-// ascending order; the 32 row-lane sums are then added in ascending order.
-// One wave per block and a short block keep every CU busy (N / 16 blocks).
-// Blocks are renumbered so that neighbouring column groups, which share
-// cache lines, run on the same XCD (the dispatcher deals blocks round-robin
-// over the 8 XCDs, each with its own L2).
-constexpr int CS_CL = 2;                 // column lanes
+// Column sums: a block owns 64 columns (128 bytes of every row): 8 column
+// lanes x 128 row lanes, each thread 8 columns (one 16-byte load per row)
+// over rows t = ty, ty + 128, ... in ascending order; the 128 row-lane sums
+// of a column are then added in ascending order.  Sixteen waves per block
+// keep enough loads in flight with few blocks (N / 64); blocks are
+// renumbered so neighbouring column groups run on the same XCD.
+constexpr int CS_CL = 8;                 // column lanes
 constexpr int CS_COLS = CS_CL * 8;       // columns per block
-constexpr int CS_ROWL = 32;              // row lanes
+constexpr int CS_ROWL = 128;             // row lanes
 constexpr int CS_T = CS_CL * CS_ROWL;    // threads per block
 
 __global__ __launch_bounds__(CS_T) void colsum_kernel(const uint16_t* __restrict__ dy, int64_t ld,
                                                       int64_t T, int64_t N, float* __restrict__ db) {
-    __shared__ float part[CS_ROWL][CS_COLS];
+    __shared__ float part[CS_ROWL][CS_COLS + 1];
     const int tx = threadIdx.x % CS_CL;
     const int ty = threadIdx.x / CS_CL;
     const int G = gridDim.x, xcd = blockIdx.x % 8, idx = blockIdx.x / 8;
@@ -162,7 +161,7 @@ __global__ __launch_bounds__(CS_T) void colsum_kernel(const uint16_t* __restrict
 #pragma unroll
     for (int e = 0; e < 8; ++e) s[e] = 0.0f;
     if (c < N) {
-#pragma unroll 8
+#pragma unroll 4
         for (int64_t t = ty; t < T; t += CS_ROWL) {
             float f[8];
             unpack8(*reinterpret_cast<const u32x4*>(dy + t * ld + c), f);
