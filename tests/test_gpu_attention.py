@@ -153,3 +153,43 @@ def test_attention_bwd_deterministic():
         res.append(d_qkv)
     torch.cuda.synchronize()
     assert torch.equal(res[0], res[1])
+
+
+@pytest.mark.parametrize("mode,mesh", [("col", (2, 2)), ("row", (2, 4)), ("col", (4, 2)),
+                                       ("col", (8, 1))])
+def test_attention_block_scatter_gather_equals_unsharded(mode, mesh):
+    """Every coordinate of the mesh: the members of each scatter group write
+    their heads into one shared buffer (the all-gather); it equals the
+    attention of the unsharded layer restricted to the block's heads, and
+    the group's lse rows are the unsharded ones."""
+    h, batch, seq = 1024, 2, 96
+    heads = h // HD
+    T = batch * seq
+    bm = block_mode_code(mode)
+    qkv_full = S.randn_bf16((T, 3 * h), 1.0, 71, 307)          # unsharded QKV output
+    ref_full, ref_lse = O.attention_core_local(qkv_full, batch, seq, HD, 1, 0)
+    d1, d2 = mesh
+    gathered = {}
+    for i1 in range(d1):
+        for i2 in range(d2):
+            m = atp.mesh(d1, d2, i1, i2)
+            g = atp.block_geometry(m, bm, h)[0]
+            blk = qkv_full[:, g.n_off:g.n_off + g.n_loc].contiguous().to(DEV)
+            key = g.n_off                       # the group sharing this block
+            if key not in gathered:
+                gathered[key] = (torch.full((T, g.n_loc // 3), -9.0, dtype=torch.bfloat16,
+                                            device=DEV), [], g)
+            first, hd, _ = atp.attention_heads(m, bm, h, heads)
+            lse = torch.empty((hd, T), dtype=torch.float32, device=DEV)
+            atp.atp_attention_fwd(m, bm, batch, seq, h, heads, blk, gathered[key][0], lse)
+            gathered[key][1].append((first, lse))
+    torch.cuda.synchronize()
+    assert len(gathered) * next(iter(gathered.values()))[2].red_size == d1 * d2
+    for n_off, (buf, lses, g) in gathered.items():
+        h0 = n_off // (3 * HD)                  # the block's first head in the layer
+        cols = slice(h0 * HD, h0 * HD + g.n_loc // 3)
+        assert_close(buf, ref_full[:, cols], f"block at column {n_off}")
+        for first, lse in lses:
+            hd = lse.shape[0]
+            np.testing.assert_allclose(to64(lse), ref_lse[h0 + first:h0 + first + hd],
+                                       rtol=0, atol=2e-3)
