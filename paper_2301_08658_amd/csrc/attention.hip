@@ -60,14 +60,23 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 __device__ __forceinline__ int kpos(int n, int c) { return c ^ (n & 15); }
 __device__ __forceinline__ int vpos(int n, int c) { return c ^ (2 * (n & 3) + 8 * ((n >> 2) & 1)); }
 
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Two floats to bf16 (round to nearest even: one v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-    auto rne = [](float f) -> uint32_t {
-        uint32_t u = __float_as_uint(f);
-        if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return 0x7fc0u;
-        u += 0x7fffu + ((u >> 16) & 1u);
-        return u >> 16;
-    };
-    return rne(a) | (rne(b) << 16);
+    const f32x2 v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+// Element offsets of a lane's transposing reads of a [key][d] tile in the
+// vpos layout, rows 4 g + lane%16 / 4 (+ 32 sl, + 16 for the second read:
+// same swizzle), columns 16 dt + 4 (lane % 4): one per dt.
+__device__ __forceinline__ int tr_offset(int lane, int dt) {
+    const int g = lane >> 4, j16 = lane & 15;
+    const int r = 4 * g + (j16 >> 2);
+    const int col = 16 * dt + 4 * (j16 & 3);
+    return r * D + vpos(r, col >> 3) * 8 + (col & 7);
 }
 
 struct AttnArgs {
@@ -146,48 +155,56 @@ __global__ __launch_bounds__(NTHR, 2) void attention_fwd_kernel(AttnArgs a) {
     load_kv(a, tok0, kc, vc, 0, kr, vr);
     store_kv(kv[0][0], kv[0][1], kr, vr);
     __syncthreads();
-    const int g = lane >> 4;
+    const int g = lane >> 4, l16 = lane & 15;
+    // K fragment offsets (key row 16 j + l16: j adds 16 rows), V read offsets
+    int koff[4], voff[8];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) koff[ks] = l16 * D + kpos(l16, 4 * ks + g) * 8;
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) voff[dt] = tr_offset(lane, dt);
     for (int kt = 0; kt < nkt; ++kt) {
         const uint16_t* ks_ = kv[kt & 1][0];
         const uint16_t* vs_ = kv[kt & 1][1];
         if (kt + 1 < nkt) load_kv(a, tok0, kc, vc, (kt + 1) * BN, kr, vr);
 
-        // S = Q K^T for 16 rows x 64 keys
+        // S = Q K^T for 16 rows x 64 keys (raw scores)
         f32x4 s[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             s[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-            const int n = 16 * j + (lane & 15);
 #pragma unroll
             for (int ks = 0; ks < 4; ++ks) {
-                const int c = 4 * ks + g;
-                const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks_ + n * D + kpos(n, c) * 8);
+                const bf16x8 kf =
+                    *reinterpret_cast<const bf16x8*>(ks_ + 16 * j * D + koff[ks]);
                 s[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], s[j], 0, 0, 0);
             }
         }
-        // scale, causal mask (and keys past the sequence), row maximum
+        // causal mask (and keys past the sequence): only the diagonal tile
+        // and a ragged last tile have masked keys
+        if (kt == qt || (kt + 1) * BN > a.seq) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int nabs = kt * BN + 16 * j + 4 * g + e;
+                    if (nabs > mrow || nabs >= a.seq) s[j][e] = -INFINITY;
+                }
+        }
         float mx = -INFINITY;
-        const int qabs = mrow;
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int nabs = kt * BN + 16 * j + 4 * g + e;
-                float v = s[j][e] * a.scale_log2;
-                if (nabs > qabs || nabs >= a.seq) v = -INFINITY;
-                s[j][e] = v;
-                mx = fmaxf(mx, v);
-            }
+            for (int e = 0; e < 4; ++e) mx = fmaxf(mx, s[j][e]);
         mx = fmaxf(mx, __shfl_xor(mx, 16));
         mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float mnew = fmaxf(mrun, mx);
+        const float mnew = fmaxf(mrun, mx * a.scale_log2);   // base-2 scaled domain
         const float alpha = __builtin_amdgcn_exp2f(mrun - mnew);
         float rs = 0.f;
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const float p = __builtin_amdgcn_exp2f(s[j][e] - mnew);
+                const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[j][e], a.scale_log2, -mnew));
                 s[j][e] = p;
                 rs += p;
             }
@@ -206,18 +223,11 @@ __global__ __launch_bounds__(NTHR, 2) void attention_fwd_kernel(AttnArgs a) {
                               pack_bf16x2(s[2 * sl + 1][0], s[2 * sl + 1][1]),
                               pack_bf16x2(s[2 * sl + 1][2], s[2 * sl + 1][3])};
             const bf16x8 pf = __builtin_bit_cast(bf16x8, pw);
-            // lane j of group g names 4 columns of key row rb + j / 4
-            const int j16 = lane & 15;
-            const int r0 = 32 * sl + 4 * g + (j16 >> 2);
-            const int r1 = r0 + 16;
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt) {
-                const int col = 16 * dt + 4 * (j16 & 3);
-                const int c = col >> 3;
-                const uint16_t* p0 = vs_ + r0 * D + vpos(r0, c) * 8 + (col & 7);
-                const uint16_t* p1 = vs_ + r1 * D + vpos(r1, c) * 8 + (col & 7);
+                const uint16_t* p0 = vs_ + 32 * sl * D + voff[dt];
                 const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p0);
-                const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p1);
+                const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0 + 16 * D));
                 const i16x8 vv = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
                 o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vv),
                                                                 pf, o[dt], 0, 0, 0);
@@ -260,19 +270,21 @@ struct AttnBwdArgs {
     float scale_log2, inv_sqrt_d;
 };
 
-__device__ __forceinline__ bf16x8 frag_b128(const uint16_t* t, int n, int c) {
-    return *reinterpret_cast<const bf16x8*>(t + n * D + vpos(n, c) * 8);
+// Lane offsets into a [row][d] tile in the vpos layout: ds_read_b128
+// fragments of row 16 j + lane%16, chunk 4 ks + lane/16 (boff[ks]; j adds
+// 16 rows, same swizzle), and transposing reads (toff[dt], see tr_offset).
+__device__ __forceinline__ void offsets(int lane, int (&boff)[4], int (&toff)[8]) {
+    const int g = lane >> 4, l16 = lane & 15;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) boff[ks] = l16 * D + vpos(l16, 4 * ks + g) * 8;
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) toff[dt] = tr_offset(lane, dt);
 }
-// Transposing fragment of a [row][d] tile: lane (group g, j) gets column
-// 16 dt + j and rows rb + 4 g + 0..3, rb + 16 + 4 g + 0..3.
-__device__ __forceinline__ bf16x8 frag_tr(const uint16_t* t, int rb, int dt, int lane) {
-    const int g = lane >> 4, j16 = lane & 15;
-    const int r0 = rb + 4 * g + (j16 >> 2), r1 = r0 + 16;
-    const int col = 16 * dt + 4 * (j16 & 3), c = col >> 3;
-    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_i16x4*)(t + r0 * D + vpos(r0, c) * 8 + (col & 7)));
-    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (lds_i16x4*)(t + r1 * D + vpos(r1, c) * 8 + (col & 7)));
+// Transposing fragment at p (rows p, p + 16 D): lane (group g, j) gets
+// column 16 dt + j, keys or queries rb + 4 g + 0..3 and rb + 16 + 4 g + 0..3.
+__device__ __forceinline__ bf16x8 frag_tr_at(const uint16_t* p) {
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 16 * D));
     const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
     return __builtin_bit_cast(bf16x8, v);
 }
@@ -379,6 +391,8 @@ __global__ __launch_bounds__(NTHR, 2) void attention_dkv_kernel(AttnBwdArgs a) {
             dl = 0.f;
         }
     };
+    int boff[4], toff[8];
+    offsets(lane, boff, toff);
     u32x4 xr[4], yr[4];
     float l2r, dlr;
     const int q0 = kt, nq = a.tiles;
@@ -396,24 +410,29 @@ __global__ __launch_bounds__(NTHR, 2) void attention_dkv_kernel(AttnBwdArgs a) {
             load_rows(qt + 1, l2r, dlr);
         }
         // S^T and dP^T: lane holds (key = kabs, query = 16 j + 4 g + e)
+        const bool masked = qt == kt || (qt + 1) * BM > a.seq;
         f32x4 p[4], dsv[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f}, dacc = sacc;
-            const int n = 16 * j + (lane & 15);
 #pragma unroll
             for (int ks = 0; ks < 4; ++ks) {
-                sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_b128(qs, n, 4 * ks + g), kf[ks],
-                                                               sacc, 0, 0, 0);
-                dacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_b128(ds_, n, 4 * ks + g), vf[ks],
-                                                               dacc, 0, 0, 0);
+                sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    *reinterpret_cast<const bf16x8*>(qs + 16 * j * D + boff[ks]), kf[ks], sacc,
+                    0, 0, 0);
+                dacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    *reinterpret_cast<const bf16x8*>(ds_ + 16 * j * D + boff[ks]), vf[ks], dacc,
+                    0, 0, 0);
             }
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int ql = 16 * j + 4 * g + e;
-                const int qabs = qt * BM + ql;
-                float pv = __builtin_amdgcn_exp2f(sacc[e] * a.scale_log2 - rowv[buf][0][ql]);
-                if (qabs < kabs || qabs >= a.seq) pv = 0.f;
+                float pv = __builtin_amdgcn_exp2f(
+                    __builtin_fmaf(sacc[e], a.scale_log2, -rowv[buf][0][ql]));
+                if (masked) {
+                    const int qabs = qt * BM + ql;
+                    if (qabs < kabs || qabs >= a.seq) pv = 0.f;
+                }
                 p[j][e] = pv;
                 dsv[j][e] = pv * (dacc[e] - rowv[buf][1][ql]);
             }
@@ -425,10 +444,10 @@ __global__ __launch_bounds__(NTHR, 2) void attention_dkv_kernel(AttnBwdArgs a) {
             const bf16x8 sf = pack_pair(dsv[2 * sl], dsv[2 * sl + 1]);
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt) {
-                dv[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_tr(ds_, 32 * sl, dt, lane), pf,
-                                                                 dv[dt], 0, 0, 0);
-                dk[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_tr(qs, 32 * sl, dt, lane), sf,
-                                                                 dk[dt], 0, 0, 0);
+                dv[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    frag_tr_at(ds_ + 32 * sl * D + toff[dt]), pf, dv[dt], 0, 0, 0);
+                dk[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    frag_tr_at(qs + 32 * sl * D + toff[dt]), sf, dk[dt], 0, 0, 0);
             }
         }
         if (qt + 1 < nq) {
@@ -487,6 +506,8 @@ __global__ __launch_bounds__(NTHR, 2) void attention_dq_kernel(AttnBwdArgs a) {
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) dq[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    int boff[4], toff[8];
+    offsets(lane, boff, toff);
     const uint16_t* kbase = a.qkv + qc + D;
     const uint16_t* vbase = a.qkv + qc + 2 * D;
     const int nk = qt + 1;
@@ -499,23 +520,27 @@ __global__ __launch_bounds__(NTHR, 2) void attention_dq_kernel(AttnBwdArgs a) {
         const uint16_t* vs_ = kv[kt & 1][1];
         if (kt + 1 < nk) load_tiles(kbase, a.ldq, vbase, a.ldq, tok0, (kt + 1) * BN, a.seq, xr, yr);
         // S and dP: lane holds (query = qabs, key = 16 j + 4 g + e)
+        const bool masked = kt == qt || (kt + 1) * BN > a.seq;
         f32x4 dsv[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f}, dacc = sacc;
-            const int n = 16 * j + (lane & 15);
 #pragma unroll
             for (int ks = 0; ks < 4; ++ks) {
-                sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_b128(ks_, n, 4 * ks + g), qf[ks],
-                                                               sacc, 0, 0, 0);
-                dacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_b128(vs_, n, 4 * ks + g), of[ks],
-                                                               dacc, 0, 0, 0);
+                sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    *reinterpret_cast<const bf16x8*>(ks_ + 16 * j * D + boff[ks]), qf[ks], sacc,
+                    0, 0, 0);
+                dacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    *reinterpret_cast<const bf16x8*>(vs_ + 16 * j * D + boff[ks]), of[ks], dacc,
+                    0, 0, 0);
             }
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const int kabs = kt * BN + 16 * j + 4 * g + e;
-                float pv = __builtin_amdgcn_exp2f(sacc[e] * a.scale_log2 - l2);
-                if (kabs > qabs || kabs >= a.seq) pv = 0.f;
+                float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[e], a.scale_log2, -l2));
+                if (masked) {
+                    const int kabs = kt * BN + 16 * j + 4 * g + e;
+                    if (kabs > qabs || kabs >= a.seq) pv = 0.f;
+                }
                 dsv[j][e] = pv * (dacc[e] - dl);
             }
         }
@@ -525,8 +550,8 @@ __global__ __launch_bounds__(NTHR, 2) void attention_dq_kernel(AttnBwdArgs a) {
             const bf16x8 sf = pack_pair(dsv[2 * sl], dsv[2 * sl + 1]);
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt)
-                dq[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(frag_tr(ks_, 32 * sl, dt, lane), sf,
-                                                                 dq[dt], 0, 0, 0);
+                dq[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    frag_tr_at(ks_ + 32 * sl * D + toff[dt]), sf, dq[dt], 0, 0, 0);
         }
         if (kt + 1 < nk) {
             __syncthreads();
