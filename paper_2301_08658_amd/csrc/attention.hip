@@ -38,6 +38,7 @@
 #include <stdint.h>
 
 #include "kernels.h"
+#include "lds_dma.h"
 
 namespace atp {
 namespace {
@@ -89,35 +90,41 @@ struct AttnArgs {
     float scale_log2;      // log2(e) / sqrt(D)
 };
 
-// Copy rows [n0, n0 + BN) of K and V of one head into registers (rows past
-// the sequence read zeros): thread t takes chunks t, t + 256, ... of each.
-__device__ __forceinline__ void load_kv(const AttnArgs& a, int64_t tok0, int64_t kc, int64_t vc,
-                                        int n0, u32x4 (&kr)[4], u32x4 (&vr)[4]) {
+
+
+// Rows [n0, n0 + 64) of two 128-column runs of one sequence's token rows
+// straight into two LDS tiles (the first in the kpos layout when KPOS0,
+// else vpos; the second in vpos): copy instruction i (wave w issues
+// i = w + 4 r) fills slots 64 i .. 64 i + 63, i.e. row 4 w + 16 r + lane/16,
+// position lane % 16, so the lane fetches the chunk its slot holds (kpos and
+// vpos are XORs, their own inverses, and depend only on the row's low four
+// bits).  Rows past the sequence are past the range and read zeros.
+template <bool KPOS0>
+struct TileDma2 {
+    uint32_t off0, off1, st0, st1;   // lane offsets of r = 0, bytes per 16 rows
+    __device__ __forceinline__ void init(int64_t ld0, int64_t ld1, int wave, int lane) {
+        const int n = 4 * wave + lane / 16, pos = lane % 16;
+        const int c0 = KPOS0 ? kpos(n, pos) : vpos(n, pos);
+        off0 = (uint32_t)((n * ld0 + 8 * c0) * 2);
+        off1 = (uint32_t)((n * ld1 + 8 * vpos(n, pos)) * 2);
+        st0 = (uint32_t)(16 * ld0 * 2);
+        st1 = (uint32_t)(16 * ld1 * 2);
+    }
+    __device__ __forceinline__ void issue(const uint16_t* b0, int64_t ld0, const uint16_t* b1,
+                                          int64_t ld1, int64_t tok0, int n0, int seq, uint16_t* t0,
+                                          uint16_t* t1, int wave) const {
+        const int64_t left = seq - n0;
+        const int64_t vr = left < 0 ? 0 : (left < 64 ? left : 64);
+        const dma::u32x4 r0 = dma::rsrc_words(b0 + (tok0 + n0) * ld0, vr * ld0 * 2);
+        const dma::u32x4 r1 = dma::rsrc_words(b1 + (tok0 + n0) * ld1, vr * ld1 * 2);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int q = threadIdx.x + i * NTHR;
-        const int n = q / CH, c = q % CH;
-        if (n0 + n < a.seq) {
-            const uint16_t* row = a.qkv + (tok0 + n0 + n) * a.ldq;
-            kr[i] = *reinterpret_cast<const u32x4*>(row + kc + 8 * c);
-            vr[i] = *reinterpret_cast<const u32x4*>(row + vc + 8 * c);
-        } else {
-            kr[i] = u32x4{0, 0, 0, 0};
-            vr[i] = u32x4{0, 0, 0, 0};
+        for (int r = 0; r < 4; ++r) {
+            const int ins = wave + NWAVE * r;
+            dma::lds_dma16(r0, t0 + ins * 64 * 8, off0 + r * st0, 0u);
+            dma::lds_dma16(r1, t1 + ins * 64 * 8, off1 + r * st1, 0u);
         }
     }
-}
-
-__device__ __forceinline__ void store_kv(uint16_t* ks, uint16_t* vs, const u32x4 (&kr)[4],
-                                         const u32x4 (&vr)[4]) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int q = threadIdx.x + i * NTHR;
-        const int n = q / CH, c = q % CH;
-        *reinterpret_cast<u32x4*>(ks + n * D + kpos(n, c) * 8) = kr[i];
-        *reinterpret_cast<u32x4*>(vs + n * D + vpos(n, c) * 8) = vr[i];
-    }
-}
+};
 
 __global__ __launch_bounds__(NTHR, 2) void attention_fwd_kernel(AttnArgs a) {
     __shared__ __attribute__((aligned(16))) uint16_t kv[2][2][BN * D];   // [buf][K|V]
@@ -151,9 +158,12 @@ __global__ __launch_bounds__(NTHR, 2) void attention_fwd_kernel(AttnArgs a) {
     float mrun = -INFINITY, lrun = 0.f;
 
     const int nkt = qt + 1;   // causal: key tiles 0..qt
-    u32x4 kr[4], vr[4];
-    load_kv(a, tok0, kc, vc, 0, kr, vr);
-    store_kv(kv[0][0], kv[0][1], kr, vr);
+    TileDma2<true> cp;
+    cp.init(a.ldq, a.ldq, wave, lane);
+    const uint16_t* kbase = a.qkv + kc;
+    const uint16_t* vbase = a.qkv + vc;
+    cp.issue(kbase, a.ldq, vbase, a.ldq, tok0, 0, a.seq, kv[0][0], kv[0][1], wave);
+    dma::wait_vmcnt<0>();
     __syncthreads();
     const int g = lane >> 4, l16 = lane & 15;
     // K fragment offsets (key row 16 j + l16: j adds 16 rows), V read offsets
@@ -165,7 +175,10 @@ __global__ __launch_bounds__(NTHR, 2) void attention_fwd_kernel(AttnArgs a) {
     for (int kt = 0; kt < nkt; ++kt) {
         const uint16_t* ks_ = kv[kt & 1][0];
         const uint16_t* vs_ = kv[kt & 1][1];
-        if (kt + 1 < nkt) load_kv(a, tok0, kc, vc, (kt + 1) * BN, kr, vr);
+        // the other buffer was last read in step kt - 1, before its barrier
+        if (kt + 1 < nkt)
+            cp.issue(kbase, a.ldq, vbase, a.ldq, tok0, (kt + 1) * BN, a.seq, kv[(kt + 1) & 1][0],
+                     kv[(kt + 1) & 1][1], wave);
 
         // S = Q K^T for 16 rows x 64 keys (raw scores)
         f32x4 s[4];
@@ -233,11 +246,10 @@ __global__ __launch_bounds__(NTHR, 2) void attention_fwd_kernel(AttnArgs a) {
                                                                 pf, o[dt], 0, 0, 0);
             }
         }
-        if (kt + 1 < nkt) {
-            __syncthreads();   // every wave is done with the other buffer
-            store_kv(kv[(kt + 1) & 1][0], kv[(kt + 1) & 1][1], kr, vr);
-            __syncthreads();
-        }
+        // this wave's copies of step kt + 1 have landed; after the barrier
+        // every wave's have, and no wave reads buffer kt & 1 any more
+        dma::wait_vmcnt<0>();
+        __syncthreads();
     }
 
     // O / l as bf16: lane holds O(m = mrow, d = 16 dt + 4 g + 0..3)
@@ -294,34 +306,6 @@ __device__ __forceinline__ bf16x8 pack_pair(const f32x4& a, const f32x4& b) {
     return __builtin_bit_cast(bf16x8, w);
 }
 
-// Rows [r0, r0 + 64) of two [T][ld] column runs (at c0 and c1) of one
-// sequence into registers; rows past the sequence read zeros.
-__device__ __forceinline__ void load_tiles(const uint16_t* b0, int64_t ld0, const uint16_t* b1,
-                                           int64_t ld1, int64_t tok0, int r0, int seq,
-                                           u32x4 (&x)[4], u32x4 (&y)[4]) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int q = threadIdx.x + i * NTHR;
-        const int n = q / CH, c = q % CH;
-        if (r0 + n < seq) {
-            x[i] = *reinterpret_cast<const u32x4*>(b0 + (tok0 + r0 + n) * ld0 + 8 * c);
-            y[i] = *reinterpret_cast<const u32x4*>(b1 + (tok0 + r0 + n) * ld1 + 8 * c);
-        } else {
-            x[i] = u32x4{0, 0, 0, 0};
-            y[i] = u32x4{0, 0, 0, 0};
-        }
-    }
-}
-__device__ __forceinline__ void store_tiles(uint16_t* t0, uint16_t* t1, const u32x4 (&x)[4],
-                                            const u32x4 (&y)[4]) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int q = threadIdx.x + i * NTHR;
-        const int n = q / CH, c = q % CH;
-        *reinterpret_cast<u32x4*>(t0 + n * D + vpos(n, c) * 8) = x[i];
-        *reinterpret_cast<u32x4*>(t1 + n * D + vpos(n, c) * 8) = y[i];
-    }
-}
 
 // delta[h][t] = dO_t . O_t over the head's 128 columns (16 lanes per row)
 __global__ __launch_bounds__(NTHR) void attention_delta_kernel(AttnBwdArgs a) {
@@ -393,20 +377,23 @@ __global__ __launch_bounds__(NTHR, 2) void attention_dkv_kernel(AttnBwdArgs a) {
     };
     int boff[4], toff[8];
     offsets(lane, boff, toff);
-    u32x4 xr[4], yr[4];
+    TileDma2<false> cp;
+    cp.init(a.ldq, a.lddo, wave, lane);
     float l2r, dlr;
     const int q0 = kt, nq = a.tiles;
-    load_tiles(qbase, a.ldq, dobase, a.lddo, tok0, q0 * BM, a.seq, xr, yr);
+    cp.issue(qbase, a.ldq, dobase, a.lddo, tok0, q0 * BM, a.seq, qd[0][0], qd[0][1], wave);
     load_rows(q0, l2r, dlr);
-    store_tiles(qd[0][0], qd[0][1], xr, yr);
     if (threadIdx.x < BM) { rowv[0][0][threadIdx.x] = l2r; rowv[0][1][threadIdx.x] = dlr; }
+    dma::wait_vmcnt<0>();
     __syncthreads();
     for (int qt = q0; qt < nq; ++qt) {
         const int buf = (qt - q0) & 1;
         const uint16_t* qs = qd[buf][0];
         const uint16_t* ds_ = qd[buf][1];
+        // the other buffers were last read in step qt - 1, before its barrier
         if (qt + 1 < nq) {
-            load_tiles(qbase, a.ldq, dobase, a.lddo, tok0, (qt + 1) * BM, a.seq, xr, yr);
+            cp.issue(qbase, a.ldq, dobase, a.lddo, tok0, (qt + 1) * BM, a.seq, qd[buf ^ 1][0],
+                     qd[buf ^ 1][1], wave);
             load_rows(qt + 1, l2r, dlr);
         }
         // S^T and dP^T: lane holds (key = kabs, query = 16 j + 4 g + e)
@@ -450,13 +437,14 @@ __global__ __launch_bounds__(NTHR, 2) void attention_dkv_kernel(AttnBwdArgs a) {
                     frag_tr_at(qs + 32 * sl * D + toff[dt]), sf, dk[dt], 0, 0, 0);
             }
         }
-        if (qt + 1 < nq) {
-            __syncthreads();
-            const int nb = buf ^ 1;
-            store_tiles(qd[nb][0], qd[nb][1], xr, yr);
-            if (threadIdx.x < BM) { rowv[nb][0][threadIdx.x] = l2r; rowv[nb][1][threadIdx.x] = dlr; }
-            __syncthreads();
+        if (qt + 1 < nq && threadIdx.x < BM) {
+            rowv[buf ^ 1][0][threadIdx.x] = l2r;
+            rowv[buf ^ 1][1][threadIdx.x] = dlr;
         }
+        // this wave's copies of step qt + 1 have landed; after the barrier
+        // every wave's have, and no wave reads buffer buf any more
+        dma::wait_vmcnt<0>();
+        __syncthreads();
     }
     if (kabs < a.seq) {
         uint16_t* row = a.dqkv + (tok0 + kabs) * a.lddq + a.dcol0 + (int64_t)hh * 3 * D;
@@ -511,14 +499,17 @@ __global__ __launch_bounds__(NTHR, 2) void attention_dq_kernel(AttnBwdArgs a) {
     const uint16_t* kbase = a.qkv + qc + D;
     const uint16_t* vbase = a.qkv + qc + 2 * D;
     const int nk = qt + 1;
-    u32x4 xr[4], yr[4];
-    load_tiles(kbase, a.ldq, vbase, a.ldq, tok0, 0, a.seq, xr, yr);
-    store_tiles(kv[0][0], kv[0][1], xr, yr);
+    TileDma2<false> cp;
+    cp.init(a.ldq, a.ldq, wave, lane);
+    cp.issue(kbase, a.ldq, vbase, a.ldq, tok0, 0, a.seq, kv[0][0], kv[0][1], wave);
+    dma::wait_vmcnt<0>();
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
         const uint16_t* ks_ = kv[kt & 1][0];
         const uint16_t* vs_ = kv[kt & 1][1];
-        if (kt + 1 < nk) load_tiles(kbase, a.ldq, vbase, a.ldq, tok0, (kt + 1) * BN, a.seq, xr, yr);
+        if (kt + 1 < nk)
+            cp.issue(kbase, a.ldq, vbase, a.ldq, tok0, (kt + 1) * BN, a.seq, kv[(kt + 1) & 1][0],
+                     kv[(kt + 1) & 1][1], wave);
         // S and dP: lane holds (query = qabs, key = 16 j + 4 g + e)
         const bool masked = kt == qt || (kt + 1) * BN > a.seq;
         f32x4 dsv[4];
@@ -553,11 +544,8 @@ __global__ __launch_bounds__(NTHR, 2) void attention_dq_kernel(AttnBwdArgs a) {
                 dq[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                     frag_tr_at(ks_ + 32 * sl * D + toff[dt]), sf, dq[dt], 0, 0, 0);
         }
-        if (kt + 1 < nk) {
-            __syncthreads();
-            store_tiles(kv[(kt + 1) & 1][0], kv[(kt + 1) & 1][1], xr, yr);
-            __syncthreads();
-        }
+        dma::wait_vmcnt<0>();
+        __syncthreads();
     }
     if (qabs < a.seq) {
         uint16_t* row = a.dqkv + (tok0 + qabs) * a.lddq + a.dcol0 + (int64_t)hh * 3 * D;

@@ -22,6 +22,7 @@
 #include <type_traits>
 
 #include "kernels.h"
+#include "lds_dma.h"
 
 #ifndef ATP_GEMM_XCD_REMAP
 #define ATP_GEMM_XCD_REMAP 1
@@ -39,8 +40,6 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
-constexpr uint32_t kRsrcWord3 = 0x00020000u;   // raw 32-bit buffer access
-constexpr uint32_t kOob = 0x80000000u;          // offset beyond any num_records
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
     return __uint_as_float(bits16 << 16);
@@ -65,24 +64,10 @@ __device__ __forceinline__ float gelu_grad_f(float x) {
 
 // 16-byte chunk swizzles.  K-major rows hold BK/8 chunks; MN-major rows
 // (one per k) hold at least 16 chunks.
-// The NT kernel's copies into LDS (buffer_load_dwordx4 ... lds) are issued
-// from inline assembly, so the compiler does not track them: it would make
-// every transposing LDS read wait for all copies in flight, even those into
-// another stage.  The kernel orders copies and reads itself (vmcnt waits and
-// barriers).  The resource is passed as its four descriptor words.
-__device__ __forceinline__ u32x4 rsrc_words(const void* base, int64_t bytes) {
-    const int64_t cap = 0x7fffff00;   // keep offsets and sizes in 31 bits
-    const uint32_t n = (uint32_t)(bytes < 0 ? 0 : (bytes > cap ? cap : bytes));
-    const uint64_t a = reinterpret_cast<uint64_t>(base);
-    return u32x4{(uint32_t)a, (uint32_t)(a >> 32) & 0xffffu, n, kRsrcWord3};
-}
-__device__ __forceinline__ void lds_dma16(const u32x4& rs, const uint16_t* lds_dst, uint32_t voff,
-                                          uint32_t soff) {
-    typedef __attribute__((address_space(3))) const void* lds_cptr;
-    const uint32_t m = (uint32_t)(uintptr_t)(lds_cptr)lds_dst;   // LDS byte address
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-                 :: "s"(m), "v"(voff), "s"(rs), "s"(soff) : "memory", "m0");
-}
+using dma::kOob;
+using dma::kRsrcWord3;
+using dma::lds_dma16;
+using dma::rsrc_words;
 
 struct KArgs {
     const uint16_t* A; int64_t lda;
@@ -129,11 +114,7 @@ __device__ __forceinline__ void group_coords(int logical, int tiles_m, int tiles
 }
 
 
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
+using dma::wait_vmcnt;
 
 // Epilogue of four consecutive outputs C[m][n..n+3] (fp32 accumulators):
 // bias, bias + GeLU (optionally saving the bf16 pre-activation), GeLU'
