@@ -220,11 +220,13 @@ typedef struct {
 
 /* Workspace for the block calls' transposed-layout path (bytes): the larger
  * of the forward's need (a transposed copy W^T of the four local weight
- * shards, sum of k_loc * n_loc * 2 bytes) and the backward's (X^T of x, the
- * attention block and H, and dY^T of the four linears, each tokens * cols *
- * 2 bytes), each plus the fp32 split-K slabs of the chunked products that
- * feed a reduction (S * chunk rows * cols * 4 bytes for the largest split
- * plan S over every valid chunk count), every piece rounded up to 256 bytes.
+ * shards, n_loc rows of k_loc + 64 bf16 values each) and the backward's (X^T
+ * of x, the attention block and H, and dY^T of the four linears, cols rows
+ * of tokens + 64 bf16 values each; the 64 values pad the row pitch off
+ * memory-channel-aligned strides), each plus the fp32 split-K slabs of the
+ * chunked products that feed a reduction (S * chunk rows * cols * 4 bytes
+ * for the largest split plan S over every valid chunk count), every piece
+ * rounded up to 256 bytes.
  * Returns 0 for invalid arguments.  `chunks` does not change the size. */
 size_t atp_block_workspace_bytes(const atp_mesh* mesh, int32_t block_mode, int64_t tokens,
                                  int64_t h, int32_t chunks);

@@ -206,7 +206,8 @@ def test_status_strings():
 
 def test_block_workspace_bytes_formula():
     # forward: W^T of the four shards; backward: X^T of x, attention block, H
-    # and dY^T of the four linears over the tokens; pieces rounded to 256 B.
+    # and dY^T of the four linears over the tokens; every row of a copy padded
+    # by 64 values (128 bytes); pieces rounded to 256 B.
     # Each side adds the fp32 split-K slabs of its chunk products, at most
     # 512 tiles of 256 x 160 fp32 values, sized for the largest plan over
     # every chunk count (a 64-chunk split of the 8 x 1 wide layer splits, 8
@@ -218,9 +219,10 @@ def test_block_workspace_bytes_formula():
                                          ((2, 2), 0, 132, 512, True), ((1, 1), 0, 0, 256, False)]:
         m = B.mesh(d1, d2, 0, 0)
         G = B.block_geometry(m, mode, h)
-        fwd = sum(r(g.k_loc * g.n_loc * 2) for g in G)
-        bwd = (r(G[0].k_loc * T * 2) + r(G[1].k_loc * T * 2) + r(G[3].k_loc * T * 2) +
-               sum(r(g.n_loc * T * 2) for g in G))
+        fwd = sum(r((g.k_loc + 64) * g.n_loc * 2) for g in G)
+        tp = T + 64
+        bwd = (r(G[0].k_loc * tp * 2) + r(G[1].k_loc * tp * 2) + r(G[3].k_loc * tp * 2) +
+               sum(r(g.n_loc * tp * 2) for g in G))
         sizes = {B.atp_block_workspace_bytes(m, mode, T, h, c) for c in (1, 2, 4)}
         assert len(sizes) == 1, sizes          # the chunk count does not change it
         ws = sizes.pop()
