@@ -3,9 +3,11 @@
 // over the group that reduced it, each device attends over its run of heads,
 // and the outputs are gathered before out-proj).
 //
-// Forward, one workgroup per (sequence, head, 64-row query tile), four waves
-// of 16 query rows, head dimension 128, keys in steps of 64 (flash-attention
-// style: running row maximum and sum, the output rescaled as they grow).
+// Forward, one workgroup per (sequence, head, query tile), head dimension
+// 128, keys in steps of 64 (flash-attention style: running row maximum and
+// sum, the output rescaled as they grow).  Large grids: 128-row tiles, four
+// waves of two 16-row blocks.  Small grids: 64-row tiles, two groups of four
+// waves of 16 rows that split the tile's keys and merge at the end.
 //
 //   * S = Q K^T on v_mfma_f32_16x16x32_bf16: Q fragments stay in registers
 //     for the whole row tile; K fragments are ds_read_b128 from a [key][d]
@@ -49,6 +51,7 @@ constexpr int BN = 64;          // keys per step
 constexpr int NWAVE = 4;
 constexpr int NTHR = NWAVE * 64;
 constexpr int CH = D / 8;       // 16-byte chunks per row
+constexpr int64_t kFwdWideGrid = 512;   // two workgroups per CU on 256 CUs
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
@@ -126,10 +129,21 @@ struct TileDma2 {
     }
 };
 
-__global__ __launch_bounds__(NTHR, 2) void attention_fwd_kernel(AttnArgs a) {
-    __shared__ __attribute__((aligned(16))) uint16_t kv[2][2][BN * D];   // [buf][K|V]
+// RB row blocks of 16 queries per wave (query tile of 64 RB rows): every K
+// and V fragment read from LDS feeds RB MFMAs.  Block r of wave w holds rows
+// 64 r + 16 w .. + 15 of the tile.  KG groups of four waves split the tile's
+// key tiles between them (group 0 the first half, group 1 the rest, which
+// holds the diagonal): each group keeps its own running maximum, sum and
+// output for the same rows, and group 1 hands them to group 0 through LDS at
+// the end, so no row loop is longer than half the causal row.
+template <int RB, int KG>
+__global__ __launch_bounds__(NTHR * KG, 2 / KG) void attention_fwd_kernel(AttnArgs a) {
+    constexpr int QT = 64 * RB;   // query rows per workgroup
+    __shared__ __attribute__((aligned(16))) uint16_t kv[KG][2][2][BN * D];   // [group][buf][K|V]
+    __shared__ float mls[KG > 1 ? NWAVE * RB * 2 * 64 : 1];                // group 1's m, l
     const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int grp = wv / NWAVE, wave = wv % NWAVE;
     // longest rows first: the last query tile of every (sequence, head) leads
     const int per = a.qtiles;
     const int bid = blockIdx.x;
@@ -139,30 +153,46 @@ __global__ __launch_bounds__(NTHR, 2) void attention_fwd_kernel(AttnArgs a) {
     const int64_t tok0 = (int64_t)b * a.seq;
     const int64_t qc = a.col0 + (int64_t)hh * 3 * D, kc = qc + D, vc = qc + 2 * D;
 
-    // Q fragments: row m0 + lane % 16, d = 32 ks + 8 (lane / 16) + 0..7
-    const int m0 = qt * BM + wave * 16;
-    const int mrow = m0 + (lane & 15);
-    bf16x8 qf[4];
+    // Q fragments: row mrow[r], d = 32 ks + 8 (lane / 16) + 0..7
+    int mrow[RB];
+    bf16x8 qf[RB][4];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-        if (mrow < a.seq)
-            qf[ks] = *reinterpret_cast<const bf16x8*>(a.qkv + (tok0 + mrow) * a.ldq + qc +
-                                                      32 * ks + 8 * (lane >> 4));
-        else
-            qf[ks] = __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0});
+    for (int r = 0; r < RB; ++r) {
+        mrow[r] = qt * QT + 64 * r + wave * 16 + (lane & 15);
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            if (mrow[r] < a.seq)
+                qf[r][ks] = *reinterpret_cast<const bf16x8*>(
+                    a.qkv + (tok0 + mrow[r]) * a.ldq + qc + 32 * ks + 8 * (lane >> 4));
+            else
+                qf[r][ks] = __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0});
+        }
     }
 
-    f32x4 o[8];
+    f32x4 o[RB][8];
+    float mrun[RB], lrun[RB];
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float mrun = -INFINITY, lrun = 0.f;
+    for (int r = 0; r < RB; ++r) {
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) o[r][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        mrun[r] = -INFINITY;
+        lrun[r] = 0.f;
+    }
 
-    const int nkt = qt + 1;   // causal: key tiles 0..qt
+    // causal: keys up to the tile's last row inside the sequence; group 0
+    // takes key tiles [0, half), group 1 [half, nkt)
+    const int last = min(qt * QT + QT, a.seq) - 1;
+    const int nkt = last / BN + 1;
+    const int half = KG > 1 ? (nkt + 1) / 2 : nkt;
+    const int kt0 = grp == 0 ? 0 : half;
+    const int mine = grp == 0 ? half : nkt - half;   // <= half
+    uint16_t(*buf)[2][BN * D] = kv[grp];
     TileDma2<true> cp;
     cp.init(a.ldq, a.ldq, wave, lane);
     const uint16_t* kbase = a.qkv + kc;
     const uint16_t* vbase = a.qkv + vc;
-    cp.issue(kbase, a.ldq, vbase, a.ldq, tok0, 0, a.seq, kv[0][0], kv[0][1], wave);
+    if (mine > 0)
+        cp.issue(kbase, a.ldq, vbase, a.ldq, tok0, kt0 * BN, a.seq, buf[0][0], buf[0][1], wave);
     dma::wait_vmcnt<0>();
     __syncthreads();
     const int g = lane >> 4, l16 = lane & 15;
@@ -172,99 +202,160 @@ __global__ __launch_bounds__(NTHR, 2) void attention_fwd_kernel(AttnArgs a) {
     for (int ks = 0; ks < 4; ++ks) koff[ks] = l16 * D + kpos(l16, 4 * ks + g) * 8;
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) voff[dt] = tr_offset(lane, dt);
-    for (int kt = 0; kt < nkt; ++kt) {
-        const uint16_t* ks_ = kv[kt & 1][0];
-        const uint16_t* vs_ = kv[kt & 1][1];
-        // the other buffer was last read in step kt - 1, before its barrier
-        if (kt + 1 < nkt)
-            cp.issue(kbase, a.ldq, vbase, a.ldq, tok0, (kt + 1) * BN, a.seq, kv[(kt + 1) & 1][0],
-                     kv[(kt + 1) & 1][1], wave);
+    // both groups step together (one barrier per step); a group with fewer
+    // key tiles idles through the last step
+    for (int i = 0; i < half; ++i) {
+        if (i < mine) {
+            const int kt = kt0 + i;
+            const uint16_t* ks_ = buf[i & 1][0];
+            const uint16_t* vs_ = buf[i & 1][1];
+            // the other buffer was last read in step i - 1, before its barrier
+            if (i + 1 < mine)
+                cp.issue(kbase, a.ldq, vbase, a.ldq, tok0, (kt + 1) * BN, a.seq,
+                         buf[(i + 1) & 1][0], buf[(i + 1) & 1][1], wave);
 
-        // S = Q K^T for 16 rows x 64 keys (raw scores)
-        f32x4 s[4];
+            // S = Q K^T for RB x 16 rows x 64 keys (raw scores)
+            f32x4 s[RB][4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            s[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int j = 0; j < 4; ++j) {
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                const bf16x8 kf =
-                    *reinterpret_cast<const bf16x8*>(ks_ + 16 * j * D + koff[ks]);
-                s[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[ks], s[j], 0, 0, 0);
-            }
-        }
-        // causal mask (and keys past the sequence): only the diagonal tile
-        // and a ragged last tile have masked keys
-        if (kt == qt || (kt + 1) * BN > a.seq) {
+                for (int r = 0; r < RB; ++r) s[r][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+                for (int ks = 0; ks < 4; ++ks) {
+                    const bf16x8 kf =
+                        *reinterpret_cast<const bf16x8*>(ks_ + 16 * j * D + koff[ks]);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int nabs = kt * BN + 16 * j + 4 * g + e;
-                    if (nabs > mrow || nabs >= a.seq) s[j][e] = -INFINITY;
+                    for (int r = 0; r < RB; ++r)
+                        s[r][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[r][ks], s[r][j],
+                                                                          0, 0, 0);
                 }
-        }
-        float mx = -INFINITY;
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) mx = fmaxf(mx, s[j][e]);
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float mnew = fmaxf(mrun, mx * a.scale_log2);   // base-2 scaled domain
-        const float alpha = __builtin_amdgcn_exp2f(mrun - mnew);
-        float rs = 0.f;
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[j][e], a.scale_log2, -mnew));
-                s[j][e] = p;
-                rs += p;
             }
-        rs += __shfl_xor(rs, 16);
-        rs += __shfl_xor(rs, 32);
-        lrun = lrun * alpha + rs;
-        mrun = mnew;
+            // causal mask (and keys past the sequence): only key tiles that
+            // reach past the tile's first row and a ragged last tile have
+            // masked keys.  A block whose rows all precede the key tile gets
+            // no probability mass from it (its running maximum is finite or,
+            // in group 1 before its first visible key, stays -inf with zero
+            // weights: exp2(-inf) = 0 and the rescale factor is taken as 1).
+            if ((kt + 1) * BN > qt * QT || (kt + 1) * BN > a.seq) {
 #pragma unroll
-        for (int dt = 0; dt < 8; ++dt) o[dt] *= alpha;
+                for (int r = 0; r < RB; ++r)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int nabs = kt * BN + 16 * j + 4 * g + e;
+                            if (nabs > mrow[r] || nabs >= a.seq) s[r][j][e] = -INFINITY;
+                        }
+            }
+#pragma unroll
+            for (int r = 0; r < RB; ++r) {
+                float mx = -INFINITY;
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) mx = fmaxf(mx, s[r][j][e]);
+                mx = fmaxf(mx, __shfl_xor(mx, 16));
+                mx = fmaxf(mx, __shfl_xor(mx, 32));
+                const float mnew = fmaxf(mrun[r], mx * a.scale_log2);   // base-2 scaled domain
+                // a row with no visible key yet keeps mnew = -inf: subtract 0
+                const float msub = mnew == -INFINITY ? 0.f : mnew;
+                const float alpha = __builtin_amdgcn_exp2f(mrun[r] - msub);
+                float rs = 0.f;
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float p = __builtin_amdgcn_exp2f(
+                            __builtin_fmaf(s[r][j][e], a.scale_log2, -msub));
+                        s[r][j][e] = p;
+                        rs += p;
+                    }
+                rs += __shfl_xor(rs, 16);
+                rs += __shfl_xor(rs, 32);
+                lrun[r] = lrun[r] * alpha + rs;
+                mrun[r] = mnew;
+#pragma unroll
+                for (int dt = 0; dt < 8; ++dt) o[r][dt] *= alpha;
+            }
 
-        // O += P V over two 32-key slices
+            // O += P V over two 32-key slices
 #pragma unroll
-        for (int sl = 0; sl < 2; ++sl) {
-            const u32x4 pw = {pack_bf16x2(s[2 * sl][0], s[2 * sl][1]),
-                              pack_bf16x2(s[2 * sl][2], s[2 * sl][3]),
-                              pack_bf16x2(s[2 * sl + 1][0], s[2 * sl + 1][1]),
-                              pack_bf16x2(s[2 * sl + 1][2], s[2 * sl + 1][3])};
-            const bf16x8 pf = __builtin_bit_cast(bf16x8, pw);
+            for (int sl = 0; sl < 2; ++sl) {
+                bf16x8 pf[RB];
 #pragma unroll
-            for (int dt = 0; dt < 8; ++dt) {
-                const uint16_t* p0 = vs_ + 32 * sl * D + voff[dt];
-                const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p0);
-                const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0 + 16 * D));
-                const i16x8 vv = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-                o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vv),
-                                                                pf, o[dt], 0, 0, 0);
+                for (int r = 0; r < RB; ++r) {
+                    const u32x4 pw = {pack_bf16x2(s[r][2 * sl][0], s[r][2 * sl][1]),
+                                      pack_bf16x2(s[r][2 * sl][2], s[r][2 * sl][3]),
+                                      pack_bf16x2(s[r][2 * sl + 1][0], s[r][2 * sl + 1][1]),
+                                      pack_bf16x2(s[r][2 * sl + 1][2], s[r][2 * sl + 1][3])};
+                    pf[r] = __builtin_bit_cast(bf16x8, pw);
+                }
+#pragma unroll
+                for (int dt = 0; dt < 8; ++dt) {
+                    const uint16_t* p0 = vs_ + 32 * sl * D + voff[dt];
+                    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p0);
+                    const i16x4 hi =
+                        __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p0 + 16 * D));
+                    const i16x8 vv = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                    const bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
+#pragma unroll
+                    for (int r = 0; r < RB; ++r)
+                        o[r][dt] =
+                            __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[r], o[r][dt], 0, 0, 0);
+                }
             }
         }
-        // this wave's copies of step kt + 1 have landed; after the barrier
-        // every wave's have, and no wave reads buffer kt & 1 any more
+        // this wave's copies of its next step have landed; after the barrier
+        // every wave's have, and no wave reads the buffers of this step
         dma::wait_vmcnt<0>();
         __syncthreads();
     }
 
+    if constexpr (KG > 1) {
+        // group 1 -> LDS (its own K/V buffers, free now): per wave, block,
+        // column tile and lane one f32x4, and per lane m and l
+        f32x4* ox = reinterpret_cast<f32x4*>(&kv[1][0][0][0]);
+        if (grp == 1) {
+#pragma unroll
+            for (int r = 0; r < RB; ++r) {
+#pragma unroll
+                for (int dt = 0; dt < 8; ++dt) ox[((wave * RB + r) * 8 + dt) * 64 + lane] = o[r][dt];
+                mls[((wave * RB + r) * 2 + 0) * 64 + lane] = mrun[r];
+                mls[((wave * RB + r) * 2 + 1) * 64 + lane] = lrun[r];
+            }
+        }
+        __syncthreads();
+        if (grp == 1) return;
+#pragma unroll
+        for (int r = 0; r < RB; ++r) {
+            const float m1 = mls[((wave * RB + r) * 2 + 0) * 64 + lane];
+            const float l1 = mls[((wave * RB + r) * 2 + 1) * 64 + lane];
+            const float mn = fmaxf(mrun[r], m1);          // finite: key 0 is group 0's
+            const float a0 = __builtin_amdgcn_exp2f(mrun[r] - mn);
+            const float a1 = __builtin_amdgcn_exp2f(m1 - mn);   // 0 when m1 = -inf
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt)
+                o[r][dt] = o[r][dt] * a0 + ox[((wave * RB + r) * 8 + dt) * 64 + lane] * a1;
+            lrun[r] = lrun[r] * a0 + l1 * a1;
+            mrun[r] = mn;
+        }
+    }
+
     // O / l as bf16: lane holds O(m = mrow, d = 16 dt + 4 g + 0..3)
-    if (mrow < a.seq) {
-        const float inv = 1.0f / lrun;
-        uint16_t* orow = a.out + (tok0 + mrow) * a.ldo + a.ocol0 + (int64_t)hh * D;
+#pragma unroll
+    for (int r = 0; r < RB; ++r) {
+        if (mrow[r] >= a.seq) continue;
+        const float inv = 1.0f / lrun[r];
+        uint16_t* orow = a.out + (tok0 + mrow[r]) * a.ldo + a.ocol0 + (int64_t)hh * D;
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) {
-            const u32x2 w = {pack_bf16x2(o[dt][0] * inv, o[dt][1] * inv),
-                             pack_bf16x2(o[dt][2] * inv, o[dt][3] * inv)};
+            const u32x2 w = {pack_bf16x2(o[r][dt][0] * inv, o[r][dt][1] * inv),
+                             pack_bf16x2(o[r][dt][2] * inv, o[r][dt][3] * inv)};
             *reinterpret_cast<u32x2*>(orow + 16 * dt + 4 * g) = w;
         }
         if (g == 0)
-            a.lse[(int64_t)hh * a.batch * a.seq + tok0 + mrow] =
-                (mrun + __log2f(lrun)) * 0.69314718055994530942f;
+            a.lse[(int64_t)hh * a.batch * a.seq + tok0 + mrow[r]] =
+                (mrun[r] + __log2f(lrun[r])) * 0.69314718055994530942f;
     }
 }
 
@@ -608,11 +699,24 @@ hipError_t launch_attention_fwd(const AttentionProblem& p, hipStream_t s) {
     a.batch = (int)p.batch;
     a.seq = (int)p.seq;
     a.heads = p.heads;
-    a.qtiles = (int)((p.seq + BM - 1) / BM);
     a.scale_log2 = 1.44269504088896340736f / sqrtf((float)D);
-    const int64_t grid = (int64_t)a.qtiles * a.batch * a.heads;
+    // Enough 128-row query tiles for two workgroups on every CU: four waves
+    // of two row blocks, two workgroups per CU (measured on the wide layer's
+    // share: 546-558 TFLOP/s, against 488-495 for the other shapes).  Fewer:
+    // 64-row tiles whose key range is split over two groups of four waves
+    // (one workgroup per CU), so the longest causal rows take half as many
+    // steps (GPT-3 share 339 against 248 for one group, 191 for 128 rows).
+    const int64_t bh = p.batch * (int64_t)p.heads;
+    const bool wide = ((p.seq + 127) / 128) * bh >= kFwdWideGrid;
+    a.qtiles = (int)(wide ? (p.seq + 127) / 128 : (p.seq + 63) / 64);
+    const int64_t grid = (int64_t)a.qtiles * bh;
     if (grid > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(attention_fwd_kernel, dim3((unsigned)grid), dim3(NTHR), 0, s, a);
+    if (wide)
+        hipLaunchKernelGGL((attention_fwd_kernel<2, 1>), dim3((unsigned)grid), dim3(NTHR), 0, s,
+                           a);
+    else
+        hipLaunchKernelGGL((attention_fwd_kernel<1, 2>), dim3((unsigned)grid), dim3(2 * NTHR), 0,
+                           s, a);
     return hipGetLastError();
 }
 

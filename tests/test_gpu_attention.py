@@ -61,6 +61,43 @@ def test_attention_fwd_full_gpt_sequence():
     np.testing.assert_allclose(to64(lse), ref_lse, rtol=0, atol=2e-3)
 
 
+def test_attention_fwd_128_row_tiles_ragged():
+    """Enough heads and sequences for 128-row query tiles (two workgroups per
+    CU): four 130-token sequences, 64 heads, so each second tile holds two
+    live rows."""
+    batch, seq, h = 4, 130, 8192
+    assert ((seq + 127) // 128) * batch * (h // HD) >= 512
+    out, lse, ref_o, ref_lse, first, hd = _run("col", (1, 1), (0, 0), batch, seq, h, seed=54)
+    cols = slice(first * HD, (first + hd) * HD)
+    assert_close(out[:, cols], ref_o, "attention output")
+    np.testing.assert_allclose(to64(lse), ref_lse, rtol=0, atol=2e-3)
+
+
+def test_attention_fwd_wide_share_sampled():
+    """The benchmark's attention share (h = 20480 on the 8 x 1 mesh: 20 heads
+    per device, two 2048-token sequences; 128-row tiles) against the oracle
+    on sampled (sequence, head) pairs, each computed alone."""
+    m = atp.mesh(8, 1, 3, 0)
+    h, batch, seq = 20480, 2, 2048
+    g = atp.block_geometry(m, atp.ATP_BLOCK_COL, h)[0]
+    first, hd, _ = atp.attention_heads(m, atp.ATP_BLOCK_COL, h, h // HD)
+    assert (first, hd) == (0, 20)
+    T = batch * seq
+    qkv = S.randn_bf16((T, g.n_loc), 1.0, 55, 308).to(DEV)
+    out = torch.empty((T, g.n_loc // 3), dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty((hd, T), dtype=torch.float32, device=DEV)
+    atp.atp_attention_fwd(m, atp.ATP_BLOCK_COL, batch, seq, h, h // HD, qkv, out, lse)
+    torch.cuda.synchronize()
+    q = qkv.cpu()
+    for b, hh in ((1, 0), (0, 11), (1, 19)):
+        rows = slice(b * seq, (b + 1) * seq)
+        c = 3 * HD * hh
+        ref_o, ref_lse = O.attention_fwd(q[rows, c:c + HD], q[rows, c + HD:c + 2 * HD],
+                                         q[rows, c + 2 * HD:c + 3 * HD])
+        assert_close(out[rows, hh * HD:(hh + 1) * HD], ref_o, f"sequence {b} head {hh}")
+        np.testing.assert_allclose(to64(lse[hh, rows]), ref_lse, rtol=0, atol=2e-3)
+
+
 def test_attention_fwd_uniform_queries_give_prefix_means():
     """q = 0: every row averages the values of its prefix (closed form)."""
     m = atp.mesh(1, 1, 0, 0)
