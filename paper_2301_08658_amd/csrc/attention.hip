@@ -52,6 +52,7 @@ constexpr int NWAVE = 4;
 constexpr int NTHR = NWAVE * 64;
 constexpr int CH = D / 8;       // 16-byte chunks per row
 constexpr int64_t kFwdWideGrid = 512;   // two workgroups per CU on 256 CUs
+constexpr int64_t kBwdSplitGrid = 1024;  // 64-row tiles below which loops are split
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
@@ -421,12 +422,17 @@ __global__ __launch_bounds__(NTHR) void attention_delta_kernel(AttnBwdArgs a) {
     if (live && l16 == 0) a.delta[hh * T + t] = acc;
 }
 
-// dK, dV of one 64-key tile (4 waves x 16 keys)
-__global__ __launch_bounds__(NTHR, 2) void attention_dkv_kernel(AttnBwdArgs a) {
-    __shared__ __attribute__((aligned(16))) uint16_t qd[2][2][BM * D];   // [buf][Q|dO]
-    __shared__ float rowv[2][2][BM];                                    // [buf][lse2|delta]
+// dK, dV of one 64-key tile (4 waves x 16 keys).  KG groups of four waves
+// split the query tiles that see the key tile (group 0 the first half, group
+// 1 the rest); group 1 adds its sums into group 0's through LDS at the end.
+template <int KG>
+__global__ __launch_bounds__(NTHR * KG, 2 / KG) void attention_dkv_kernel(AttnBwdArgs a) {
+    __shared__ __attribute__((aligned(16))) uint16_t qd[KG][2][2][BM * D];   // [grp][buf][Q|dO]
+    __shared__ float rowv[KG][2][2][BM];                                    // [grp][buf][lse2|delta]
     const int lane = threadIdx.x & 63, g = lane >> 4;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int grp = wv / NWAVE, wave = wv % NWAVE;
+    const int tid = (int)threadIdx.x % NTHR;   // thread index within the group
     const int bhn = a.batch * a.heads;
     const int kt = blockIdx.x / bhn;            // short loops (late keys) last
     const int bh = blockIdx.x % bhn;
@@ -457,8 +463,8 @@ __global__ __launch_bounds__(NTHR, 2) void attention_dkv_kernel(AttnBwdArgs a) {
     }
 
     auto load_rows = [&](int qt, float& l2, float& dl) {
-        const int t = qt * BM + (int)threadIdx.x;
-        if (threadIdx.x < BM && t < a.seq) {
+        const int t = qt * BM + tid;
+        if (tid < BM && t < a.seq) {
             l2 = a.lse[(int64_t)hh * T + tok0 + t] * 1.44269504088896340736f;
             dl = a.delta[(int64_t)hh * T + tok0 + t];
         } else {
@@ -470,72 +476,102 @@ __global__ __launch_bounds__(NTHR, 2) void attention_dkv_kernel(AttnBwdArgs a) {
     offsets(lane, boff, toff);
     TileDma2<false> cp;
     cp.init(a.ldq, a.lddo, wave, lane);
-    float l2r, dlr;
-    const int q0 = kt, nq = a.tiles;
-    cp.issue(qbase, a.ldq, dobase, a.lddo, tok0, q0 * BM, a.seq, qd[0][0], qd[0][1], wave);
-    load_rows(q0, l2r, dlr);
-    if (threadIdx.x < BM) { rowv[0][0][threadIdx.x] = l2r; rowv[0][1][threadIdx.x] = dlr; }
+    // query tiles kt .. tiles-1 see this key tile: group 0 the first half
+    const int nsteps = a.tiles - kt;
+    const int half = KG > 1 ? (nsteps + 1) / 2 : nsteps;
+    const int q0 = kt + (grp == 0 ? 0 : half);
+    const int mine = grp == 0 ? half : nsteps - half;   // <= half
+    uint16_t(*qb)[2][BM * D] = qd[grp];
+    float(*rv)[2][BM] = rowv[grp];
+    float l2r = 0.f, dlr = 0.f;
+    if (mine > 0) {
+        cp.issue(qbase, a.ldq, dobase, a.lddo, tok0, q0 * BM, a.seq, qb[0][0], qb[0][1], wave);
+        load_rows(q0, l2r, dlr);
+        if (tid < BM) { rv[0][0][tid] = l2r; rv[0][1][tid] = dlr; }
+    }
     dma::wait_vmcnt<0>();
     __syncthreads();
-    for (int qt = q0; qt < nq; ++qt) {
-        const int buf = (qt - q0) & 1;
-        const uint16_t* qs = qd[buf][0];
-        const uint16_t* ds_ = qd[buf][1];
-        // the other buffers were last read in step qt - 1, before its barrier
-        if (qt + 1 < nq) {
-            cp.issue(qbase, a.ldq, dobase, a.lddo, tok0, (qt + 1) * BM, a.seq, qd[buf ^ 1][0],
-                     qd[buf ^ 1][1], wave);
-            load_rows(qt + 1, l2r, dlr);
-        }
-        // S^T and dP^T: lane holds (key = kabs, query = 16 j + 4 g + e)
-        const bool masked = qt == kt || (qt + 1) * BM > a.seq;
-        f32x4 p[4], dsv[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f}, dacc = sacc;
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    *reinterpret_cast<const bf16x8*>(qs + 16 * j * D + boff[ks]), kf[ks], sacc,
-                    0, 0, 0);
-                dacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    *reinterpret_cast<const bf16x8*>(ds_ + 16 * j * D + boff[ks]), vf[ks], dacc,
-                    0, 0, 0);
+    for (int i = 0; i < half; ++i) {
+        if (i < mine) {
+            const int qt = q0 + i;
+            const int buf = i & 1;
+            const uint16_t* qs = qb[buf][0];
+            const uint16_t* ds_ = qb[buf][1];
+            // the other buffers were last read in step i - 1, before its barrier
+            if (i + 1 < mine) {
+                cp.issue(qbase, a.ldq, dobase, a.lddo, tok0, (qt + 1) * BM, a.seq, qb[buf ^ 1][0],
+                         qb[buf ^ 1][1], wave);
+                load_rows(qt + 1, l2r, dlr);
             }
+            // S^T and dP^T: lane holds (key = kabs, query = 16 j + 4 g + e)
+            const bool masked = qt == kt || (qt + 1) * BM > a.seq;
+            f32x4 p[4], dsv[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int ql = 16 * j + 4 * g + e;
-                float pv = __builtin_amdgcn_exp2f(
-                    __builtin_fmaf(sacc[e], a.scale_log2, -rowv[buf][0][ql]));
-                if (masked) {
-                    const int qabs = qt * BM + ql;
-                    if (qabs < kabs || qabs >= a.seq) pv = 0.f;
+            for (int j = 0; j < 4; ++j) {
+                f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f}, dacc = sacc;
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks) {
+                    sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        *reinterpret_cast<const bf16x8*>(qs + 16 * j * D + boff[ks]), kf[ks],
+                        sacc, 0, 0, 0);
+                    dacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        *reinterpret_cast<const bf16x8*>(ds_ + 16 * j * D + boff[ks]), vf[ks],
+                        dacc, 0, 0, 0);
                 }
-                p[j][e] = pv;
-                dsv[j][e] = pv * (dacc[e] - rowv[buf][1][ql]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int ql = 16 * j + 4 * g + e;
+                    float pv = __builtin_amdgcn_exp2f(
+                        __builtin_fmaf(sacc[e], a.scale_log2, -rv[buf][0][ql]));
+                    if (masked) {
+                        const int qabs = qt * BM + ql;
+                        if (qabs < kabs || qabs >= a.seq) pv = 0.f;
+                    }
+                    p[j][e] = pv;
+                    dsv[j][e] = pv * (dacc[e] - rv[buf][1][ql]);
+                }
+            }
+            // dV += P^T dO, dK += dS^T Q over two 32-query slices
+#pragma unroll
+            for (int sl = 0; sl < 2; ++sl) {
+                const bf16x8 pf = pack_pair(p[2 * sl], p[2 * sl + 1]);
+                const bf16x8 sf = pack_pair(dsv[2 * sl], dsv[2 * sl + 1]);
+#pragma unroll
+                for (int dt = 0; dt < 8; ++dt) {
+                    dv[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        frag_tr_at(ds_ + 32 * sl * D + toff[dt]), pf, dv[dt], 0, 0, 0);
+                    dk[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        frag_tr_at(qs + 32 * sl * D + toff[dt]), sf, dk[dt], 0, 0, 0);
+                }
+            }
+            if (i + 1 < mine && tid < BM) {
+                rv[buf ^ 1][0][tid] = l2r;
+                rv[buf ^ 1][1][tid] = dlr;
             }
         }
-        // dV += P^T dO, dK += dS^T Q over two 32-query slices
-#pragma unroll
-        for (int sl = 0; sl < 2; ++sl) {
-            const bf16x8 pf = pack_pair(p[2 * sl], p[2 * sl + 1]);
-            const bf16x8 sf = pack_pair(dsv[2 * sl], dsv[2 * sl + 1]);
-#pragma unroll
-            for (int dt = 0; dt < 8; ++dt) {
-                dv[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    frag_tr_at(ds_ + 32 * sl * D + toff[dt]), pf, dv[dt], 0, 0, 0);
-                dk[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    frag_tr_at(qs + 32 * sl * D + toff[dt]), sf, dk[dt], 0, 0, 0);
-            }
-        }
-        if (qt + 1 < nq && threadIdx.x < BM) {
-            rowv[buf ^ 1][0][threadIdx.x] = l2r;
-            rowv[buf ^ 1][1][threadIdx.x] = dlr;
-        }
-        // this wave's copies of step qt + 1 have landed; after the barrier
-        // every wave's have, and no wave reads buffer buf any more
+        // this wave's copies of its next step have landed; after the barrier
+        // every wave's have, and no wave reads this step's buffers any more
         dma::wait_vmcnt<0>();
         __syncthreads();
+    }
+    if constexpr (KG > 1) {
+        // group 1's sums -> LDS (its own Q/dO buffers, free now), added by
+        // group 0 in a fixed order: group 0's + group 1's
+        f32x4* x = reinterpret_cast<f32x4*>(&qd[1][0][0][0]);
+        if (grp == 1) {
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt) {
+                x[((wave * 2 + 0) * 8 + dt) * 64 + lane] = dk[dt];
+                x[((wave * 2 + 1) * 8 + dt) * 64 + lane] = dv[dt];
+            }
+        }
+        __syncthreads();
+        if (grp == 1) return;
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) {
+            dk[dt] += x[((wave * 2 + 0) * 8 + dt) * 64 + lane];
+            dv[dt] += x[((wave * 2 + 1) * 8 + dt) * 64 + lane];
+        }
     }
     if (kabs < a.seq) {
         uint16_t* row = a.dqkv + (tok0 + kabs) * a.lddq + a.dcol0 + (int64_t)hh * 3 * D;
@@ -543,18 +579,22 @@ __global__ __launch_bounds__(NTHR, 2) void attention_dkv_kernel(AttnBwdArgs a) {
         for (int dt = 0; dt < 8; ++dt) {
             const u32x2 wk = {pack_bf16x2(dk[dt][0] * a.inv_sqrt_d, dk[dt][1] * a.inv_sqrt_d),
                               pack_bf16x2(dk[dt][2] * a.inv_sqrt_d, dk[dt][3] * a.inv_sqrt_d)};
-            const u32x2 wv = {pack_bf16x2(dv[dt][0], dv[dt][1]), pack_bf16x2(dv[dt][2], dv[dt][3])};
+            const u32x2 wv2 = {pack_bf16x2(dv[dt][0], dv[dt][1]), pack_bf16x2(dv[dt][2], dv[dt][3])};
             *reinterpret_cast<u32x2*>(row + D + 16 * dt + 4 * g) = wk;
-            *reinterpret_cast<u32x2*>(row + 2 * D + 16 * dt + 4 * g) = wv;
+            *reinterpret_cast<u32x2*>(row + 2 * D + 16 * dt + 4 * g) = wv2;
         }
     }
 }
 
-// dQ of one 64-query tile (4 waves x 16 queries)
-__global__ __launch_bounds__(NTHR, 2) void attention_dq_kernel(AttnBwdArgs a) {
-    __shared__ __attribute__((aligned(16))) uint16_t kv[2][2][BN * D];   // [buf][K|V]
+// dQ of one 64-query tile (4 waves x 16 queries).  KG groups of four waves
+// split its key tiles (group 0 the first half, group 1 the rest, with the
+// diagonal); group 1 adds its sum into group 0's through LDS at the end.
+template <int KG>
+__global__ __launch_bounds__(NTHR * KG, 2 / KG) void attention_dq_kernel(AttnBwdArgs a) {
+    __shared__ __attribute__((aligned(16))) uint16_t kv[KG][2][2][BN * D];   // [grp][buf][K|V]
     const int lane = threadIdx.x & 63, g = lane >> 4;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int grp = wv / NWAVE, wave = wv % NWAVE;
     const int bhn = a.batch * a.heads;
     const int qt = a.tiles - 1 - blockIdx.x / bhn;   // long loops first
     const int bh = blockIdx.x % bhn;
@@ -589,54 +629,74 @@ __global__ __launch_bounds__(NTHR, 2) void attention_dq_kernel(AttnBwdArgs a) {
     offsets(lane, boff, toff);
     const uint16_t* kbase = a.qkv + qc + D;
     const uint16_t* vbase = a.qkv + qc + 2 * D;
+    // key tiles 0 .. qt: group 0 the first half, group 1 the rest
     const int nk = qt + 1;
+    const int half = KG > 1 ? (nk + 1) / 2 : nk;
+    const int k0 = grp == 0 ? 0 : half;
+    const int mine = grp == 0 ? half : nk - half;   // <= half
+    uint16_t(*kb)[2][BN * D] = kv[grp];
     TileDma2<false> cp;
     cp.init(a.ldq, a.ldq, wave, lane);
-    cp.issue(kbase, a.ldq, vbase, a.ldq, tok0, 0, a.seq, kv[0][0], kv[0][1], wave);
+    if (mine > 0)
+        cp.issue(kbase, a.ldq, vbase, a.ldq, tok0, k0 * BN, a.seq, kb[0][0], kb[0][1], wave);
     dma::wait_vmcnt<0>();
     __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const uint16_t* ks_ = kv[kt & 1][0];
-        const uint16_t* vs_ = kv[kt & 1][1];
-        if (kt + 1 < nk)
-            cp.issue(kbase, a.ldq, vbase, a.ldq, tok0, (kt + 1) * BN, a.seq, kv[(kt + 1) & 1][0],
-                     kv[(kt + 1) & 1][1], wave);
-        // S and dP: lane holds (query = qabs, key = 16 j + 4 g + e)
-        const bool masked = kt == qt || (kt + 1) * BN > a.seq;
-        f32x4 dsv[4];
+    for (int i = 0; i < half; ++i) {
+        if (i < mine) {
+            const int kt = k0 + i;
+            const uint16_t* ks_ = kb[i & 1][0];
+            const uint16_t* vs_ = kb[i & 1][1];
+            if (i + 1 < mine)
+                cp.issue(kbase, a.ldq, vbase, a.ldq, tok0, (kt + 1) * BN, a.seq,
+                         kb[(i + 1) & 1][0], kb[(i + 1) & 1][1], wave);
+            // S and dP: lane holds (query = qabs, key = 16 j + 4 g + e)
+            const bool masked = kt == qt || (kt + 1) * BN > a.seq;
+            f32x4 dsv[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f}, dacc = sacc;
+            for (int j = 0; j < 4; ++j) {
+                f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f}, dacc = sacc;
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    *reinterpret_cast<const bf16x8*>(ks_ + 16 * j * D + boff[ks]), qf[ks], sacc,
-                    0, 0, 0);
-                dacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    *reinterpret_cast<const bf16x8*>(vs_ + 16 * j * D + boff[ks]), of[ks], dacc,
-                    0, 0, 0);
-            }
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[e], a.scale_log2, -l2));
-                if (masked) {
-                    const int kabs = kt * BN + 16 * j + 4 * g + e;
-                    if (kabs > qabs || kabs >= a.seq) pv = 0.f;
+                for (int ks = 0; ks < 4; ++ks) {
+                    sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        *reinterpret_cast<const bf16x8*>(ks_ + 16 * j * D + boff[ks]), qf[ks],
+                        sacc, 0, 0, 0);
+                    dacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        *reinterpret_cast<const bf16x8*>(vs_ + 16 * j * D + boff[ks]), of[ks],
+                        dacc, 0, 0, 0);
                 }
-                dsv[j][e] = pv * (dacc[e] - dl);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[e], a.scale_log2, -l2));
+                    if (masked) {
+                        const int kabs = kt * BN + 16 * j + 4 * g + e;
+                        if (kabs > qabs || kabs >= a.seq) pv = 0.f;
+                    }
+                    dsv[j][e] = pv * (dacc[e] - dl);
+                }
             }
-        }
-        // dQ += dS K over two 32-key slices
+            // dQ += dS K over two 32-key slices
 #pragma unroll
-        for (int sl = 0; sl < 2; ++sl) {
-            const bf16x8 sf = pack_pair(dsv[2 * sl], dsv[2 * sl + 1]);
+            for (int sl = 0; sl < 2; ++sl) {
+                const bf16x8 sf = pack_pair(dsv[2 * sl], dsv[2 * sl + 1]);
 #pragma unroll
-            for (int dt = 0; dt < 8; ++dt)
-                dq[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    frag_tr_at(ks_ + 32 * sl * D + toff[dt]), sf, dq[dt], 0, 0, 0);
+                for (int dt = 0; dt < 8; ++dt)
+                    dq[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        frag_tr_at(ks_ + 32 * sl * D + toff[dt]), sf, dq[dt], 0, 0, 0);
+            }
         }
         dma::wait_vmcnt<0>();
         __syncthreads();
+    }
+    if constexpr (KG > 1) {
+        f32x4* x = reinterpret_cast<f32x4*>(&kv[1][0][0][0]);
+        if (grp == 1) {
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt) x[(wave * 8 + dt) * 64 + lane] = dq[dt];
+        }
+        __syncthreads();
+        if (grp == 1) return;
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) dq[dt] += x[(wave * 8 + dt) * 64 + lane];
     }
     if (qabs < a.seq) {
         uint16_t* row = a.dqkv + (tok0 + qabs) * a.lddq + a.dcol0 + (int64_t)hh * 3 * D;
@@ -680,8 +740,18 @@ hipError_t launch_attention_bwd(const AttentionBwdProblem& p, hipStream_t s) {
     const int64_t grid = (int64_t)a.tiles * a.batch * a.heads;
     if (dgrid > 0x7fffffff || grid > 0x7fffffff) return hipErrorInvalidValue;
     hipLaunchKernelGGL(attention_delta_kernel, dim3((unsigned)dgrid), dim3(NTHR), 0, s, a);
-    hipLaunchKernelGGL(attention_dkv_kernel, dim3((unsigned)grid), dim3(NTHR), 0, s, a);
-    hipLaunchKernelGGL(attention_dq_kernel, dim3((unsigned)grid), dim3(NTHR), 0, s, a);
+    // small grids: split each workgroup's loop over two groups of four waves
+    // (one workgroup per CU), so the longest loops take half as many steps
+    const bool split = grid < kBwdSplitGrid;
+    if (split) {
+        hipLaunchKernelGGL((attention_dkv_kernel<2>), dim3((unsigned)grid), dim3(2 * NTHR), 0, s,
+                           a);
+        hipLaunchKernelGGL((attention_dq_kernel<2>), dim3((unsigned)grid), dim3(2 * NTHR), 0, s,
+                           a);
+    } else {
+        hipLaunchKernelGGL((attention_dkv_kernel<1>), dim3((unsigned)grid), dim3(NTHR), 0, s, a);
+        hipLaunchKernelGGL((attention_dq_kernel<1>), dim3((unsigned)grid), dim3(NTHR), 0, s, a);
+    }
     return hipGetLastError();
 }
 

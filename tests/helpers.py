@@ -17,12 +17,14 @@ def to64(t) -> np.ndarray:
     return t.detach().to("cpu", torch.float64).numpy()
 
 
-def assert_close(gpu, ref, what="", elem_tol=ELEM_TOL, frob_tol=FROB_TOL, floor=1.0):
-    """Elementwise |gpu - ref| <= elem_tol * (|ref| + floor) and relative
-    Frobenius error <= frob_tol.  floor="rms" uses the reference's RMS as the
-    absolute floor: for token-sums of a bf16-stored intermediate (dW, db of
-    fc1 in the chained backward), where a tie of that intermediate rounded the
-    other way moves a whole column by ulp(dY) * |x| whatever the column's size."""
+def assert_close(gpu, ref, what="", elem_tol=ELEM_TOL, frob_tol=FROB_TOL, floor=1.0, extra=None):
+    """Elementwise |gpu - ref| <= elem_tol * (|ref| + floor) (+ extra, an
+    array of per-element error terms derived for a specific computation) and
+    relative Frobenius error <= frob_tol.  floor="rms" uses the reference's
+    RMS as the absolute floor: for token-sums of a bf16-stored intermediate
+    (dW, db of fc1 in the chained backward), where a tie of that intermediate
+    rounded the other way moves a whole column by ulp(dY) * |x| whatever the
+    column's size."""
     g = to64(gpu)
     r = to64(ref)
     assert g.shape == r.shape, (what, g.shape, r.shape)
@@ -31,6 +33,8 @@ def assert_close(gpu, ref, what="", elem_tol=ELEM_TOL, frob_tol=FROB_TOL, floor=
     if floor == "rms":
         floor = float(np.sqrt(np.mean(r * r))) if r.size else 1.0
     bound = elem_tol * (np.abs(r) + floor)
+    if extra is not None:
+        bound = bound + to64(extra)
     bad = err > bound
     if bad.any():
         idx = np.argwhere(bad)[0]

@@ -17,6 +17,30 @@ pytestmark = pytest.mark.gpu
 HD = 128
 
 
+def delta_bounds(q, k, v, do):
+    """Error terms for dQ and dK of one (sequence, head) from delta_t = dO_t . O_t
+    taken over the stored bf16 output (the kernels never see the exact O).
+    The stored O carries two roundings of relative size 2^-9 (the bf16
+    probabilities that enter P V, and the output's own rounding), so
+    |dO_t[e]| (|O_t[e]| + (P |V|)_t[e]) scales the error of each term; taken
+    as independent uniform roundings, delta_t's error has RMS
+        r_t = 2^-9 / sqrt(3) * sqrt(sum_e dO_t[e]^2 (O_t[e]^2 + (P|V|)_t[e]^2)).
+    It enters dS[t, u] = P[t, u] (dP[t, u] - delta_t), hence
+        dK_u[e] error RMS = sqrt(sum_t P[t,u]^2 r_t^2 q_t[e]^2) / sqrt(d),
+        dQ_t[e] error RMS = r_t sqrt(sum_u P[t,u]^2 k_u[e]^2) / sqrt(d);
+    the bounds are six times these RMS values.  P, O come from the oracle."""
+    q, k, v, do = (to64(a) for a in (q, k, v, do))
+    S, d = q.shape
+    o, lse = O.attention_fwd(q, k, v)
+    s = q @ k.T / np.sqrt(d)
+    s[np.triu(np.ones((S, S), dtype=bool), 1)] = -np.inf
+    P = np.exp(s - lse[:, None])
+    r = 2.0 ** -9 / np.sqrt(3) * np.sqrt((do * do * (o * o + (P @ np.abs(v)) ** 2)).sum(1))
+    bk = 6 / np.sqrt(d) * np.sqrt((P * P).T @ ((r * r)[:, None] * q * q))
+    bq = 6 / np.sqrt(d) * r[:, None] * np.sqrt((P * P) @ (k * k))
+    return bq, bk
+
+
 def _run(mode, mesh, coord, batch, seq, h, seed, sigma=1.0):
     m = atp.mesh(mesh[0], mesh[1], coord[0], coord[1])
     bm = block_mode_code(mode)
@@ -138,6 +162,7 @@ def test_attention_fwd_empty_and_errors():
     ("col", (1, 1), (0, 0), 2, 1, 512),        # one token
     ("col", (2, 4), (1, 2), 2, 257, 4096),
     ("row", (4, 2), (3, 1), 1, 192, 4096),
+    ("col", (1, 1), (0, 0), 4, 260, 8192),     # 1280 tiles: loops not split
 ])
 def test_attention_bwd_matches_oracle(mode, mesh, coord, batch, seq, h):
     print(f"attention bwd {mode} {mesh} {coord} b={batch} s={seq} h={h}", flush=True)
@@ -161,13 +186,56 @@ def test_attention_bwd_matches_oracle(mode, mesh, coord, batch, seq, h):
                                      g.red_size, g.red_index)
     mine = slice(first * 3 * HD, (first + hd) * 3 * HD)
     got = d_qkv[:, mine]
+    # error terms of dQ and dK from delta over the stored bf16 output
+    extra = np.zeros((T, 3 * HD * hd))
+    qc, dc = qkv.cpu(), d_out.cpu()
+    for bb in range(batch):
+        rows = slice(bb * seq, (bb + 1) * seq)
+        for j in range(hd):
+            c = 3 * HD * (first + j)
+            bq, bk = delta_bounds(qc[rows, c:c + HD], qc[rows, c + HD:c + 2 * HD],
+                                  qc[rows, c + 2 * HD:c + 3 * HD],
+                                  dc[rows, (first + j) * HD:(first + j + 1) * HD])
+            extra[rows, 3 * HD * j:3 * HD * j + HD] = bq
+            extra[rows, 3 * HD * j + HD:3 * HD * j + 2 * HD] = bk
     for part, nm in ((0, "dq"), (1, "dk"), (2, "dv")):
         sel = np.concatenate([np.arange(j * 3 * HD + part * HD, j * 3 * HD + (part + 1) * HD)
                               for j in range(hd)])
-        assert_close(got[:, torch.as_tensor(sel, device=DEV)], ref[:, sel], nm)
+        assert_close(got[:, torch.as_tensor(sel, device=DEV)], ref[:, sel], nm,
+                     extra=extra[:, sel])
     rest = torch.ones(g.n_loc, dtype=torch.bool)
     rest[mine] = False
     assert torch.all(d_qkv[:, rest.to(DEV)] == -5.0), "columns of other group members written"
+
+
+def test_attention_bwd_wide_share_sampled():
+    """The benchmark's attention share backward (h = 20480 on 8 x 1: 20 heads,
+    two 2048-token sequences) against the oracle on one (sequence, head)."""
+    m = atp.mesh(8, 1, 6, 0)
+    h, batch, seq, heads = 20480, 2, 2048, 160
+    g = atp.block_geometry(m, atp.ATP_BLOCK_COL, h)[0]
+    first, hd, _ = atp.attention_heads(m, atp.ATP_BLOCK_COL, h, heads)
+    T = batch * seq
+    qkv = S.randn_bf16((T, g.n_loc), 1.0, 63, 309).to(DEV)
+    out = torch.empty((T, g.n_loc // 3), dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty((hd, T), dtype=torch.float32, device=DEV)
+    atp.atp_attention_fwd(m, atp.ATP_BLOCK_COL, batch, seq, h, heads, qkv, out, lse)
+    d_out = S.randn_bf16((T, g.n_loc // 3), 1.0, 63, 310).to(DEV)
+    d_qkv = torch.empty((T, g.n_loc), dtype=torch.bfloat16, device=DEV)
+    delta = torch.empty((hd * T,), dtype=torch.float32, device=DEV)
+    atp.atp_attention_bwd(m, atp.ATP_BLOCK_COL, batch, seq, h, heads, qkv, out, lse, d_out,
+                          d_qkv, delta)
+    torch.cuda.synchronize()
+    b, hh = 1, 13
+    rows = slice(b * seq, (b + 1) * seq)
+    c = 3 * HD * hh
+    q = qkv[rows].cpu()
+    args = (q[:, c:c + HD], q[:, c + HD:c + 2 * HD], q[:, c + 2 * HD:c + 3 * HD],
+            d_out[rows, hh * HD:(hh + 1) * HD].cpu())
+    dq, dk, dv = O.attention_bwd(*args)
+    bq, bk = delta_bounds(*args)
+    for part, ref, nm, ex in ((0, dq, "dq", bq), (1, dk, "dk", bk), (2, dv, "dv", None)):
+        assert_close(d_qkv[rows, c + part * HD:c + (part + 1) * HD], ref, nm, extra=ex)
 
 
 def test_attention_bwd_deterministic():
