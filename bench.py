@@ -423,16 +423,39 @@ def main():
                     algorithmic_bytes_per_launch=dom["bytes"] / dom["launches"],
                     flops_per_launch=dom["flops"] / dom["launches"],
                     avg_launch_us=round(dom["total_ms"] / dom["launches"] * 1e3, 2))
+    overlap = None
     if not args.serial:
-        # the same launches with nothing beside them: one more pass of the
-        # step with every launch serialized on the compute stream
+        # the same launches with nothing beside them: the step with every
+        # launch serialized on the compute stream, timed like the pipelined
+        # step, then once more with per-launch events
         solo = make_step(torch, atp, st, fwd_only, True)
+        solo()
+        sev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        sev[0].record()
+        for _ in range(args.steps):
+            solo()
+        sev[1].record()
+        torch.cuda.synchronize()
+        serial_ms = sev[0].elapsed_time(sev[1]) / args.steps
         atp.atp_profile_enable(True)
         for _ in range(args.steps):
             solo()
         torch.cuda.synchronize()
         atp.atp_profile_enable(False)
-        alone = [s for s in atp.atp_profile_collect(64) if s["name"] == dom["name"]]
+        solo_stats = atp.atp_profile_collect(64)
+        red_solo = sum(s["total_ms"] for s in solo_stats if s["name"] == "partial_reduce")
+        red_solo /= args.steps
+        if red_solo > 0:
+            # Sec. 4.1's overlap: the share of the reductions' own time that
+            # the pipelined step hides behind the GEMMs
+            overlap = dict(serial_ms=round(serial_ms, 4), pipelined_ms=round(ms_step, 4),
+                           reduce_ms=round(red_solo, 4),
+                           hidden=round((serial_ms - ms_step) / red_solo, 4),
+                           note="(serial - pipelined) / reduction kernel time of the serialized "
+                                "step; serial: every launch on the compute stream")
+            log(f"[bench] overlap: {overlap}")
+        alone = [s for s in solo_stats if s["name"] == dom["name"]]
         if alone:
             a = alone[0]
             tf = a["flops"] / (a["total_ms"] * 1e-3) / 1e12
@@ -497,7 +520,8 @@ def main():
                     hip_graph=bool(args.graph and not args.no_workspace),
                     gflop_per_step=round(flops / 1e9, 1)),
         step_ms=step_ms, mfma_util=round(value / PEAK_BF16_TFLOPS, 4),
-        roofline=roofline, reduce=reduce_info, kernels=kernels, cpu_baseline=cpu)
+        roofline=roofline, reduce=reduce_info, overlap=overlap, kernels=kernels,
+        cpu_baseline=cpu)
     print(json.dumps(out), flush=True)
 
 

@@ -28,6 +28,11 @@ __device__ __forceinline__ u32x4 rsrc_words(const void* base, int64_t bytes) {
 
 // One 64-lane copy instruction: lane l's 16 bytes at base + voff (+ soff)
 // land in LDS at lds_dst + 16 l.  Only voff is checked against the range.
+// The LDS address travels in M0.  The compiler treats M0 as reserved and
+// warns that the clobber below is not honoured, i.e. it would not reload a
+// value of its own after this statement.  The kernels calling this keep
+// nothing in M0 (no LDS-DMA builtins, no indexed register moves, every loop
+// over registers unrolled); a kernel that needs M0 itself must not use it.
 __device__ __forceinline__ void lds_dma16(const u32x4& rs, const uint16_t* lds_dst, uint32_t voff,
                                           uint32_t soff) {
     typedef __attribute__((address_space(3))) const void* lds_cptr;
