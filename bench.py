@@ -61,6 +61,10 @@ def parse():
     ap.add_argument("--attention", action="store_true",
                     help="time the attention core (fwd+bwd) of one device's heads instead of "
                          "the linear block: sequences of min(2048, tokens), head dim 128")
+    ap.add_argument("--linear", action="store_true",
+                    help="time one reduced linear of the block (fc2: the largest reduction) "
+                         "as the chunked pipeline with f32 and with bf16 partials, serialized, "
+                         "unchunked, and with the reduction fused into the GEMM epilogue")
     ap.add_argument("--seed", type=int, default=21)
     ap.add_argument("--profile-detail", action="store_true",
                     help="also print per-shape kernel timings to stderr")
@@ -110,6 +114,93 @@ def setup(torch, atp, S, wl, chunks, seed):
     st["dw"] = [torch.empty((g.k_loc, g.n_loc), dtype=torch.float32, device=dev) for g in G]
     st["db"] = [torch.empty((g.n_loc,), dtype=torch.float32, device=dev) for g in G]
     return st
+
+
+def linear_bench(torch, atp, S, args, wl, chunks):
+    """fc2 of the workload's block on one device (Sec. 3.2: row-first in the
+    column-first block, reduced over its group with the bias): the paper's
+    chunked overlap (Sec. 4.1) with f32 partials and with bf16 partials (the
+    16-bit all-reduce of Sec. 5), the same serialized and unchunked, and the
+    fused GEMM + reduction that Sec. 4.1 contrasts it with.  All variants
+    run the product from W as given (no transposed copy)."""
+    dev = "cuda:0"
+    d1, d2 = wl["mesh"]
+    m = atp.mesh(d1, d2, 0, 0)
+    bm = atp.ATP_BLOCK_COL if wl["mode"] == "col" else atp.ATP_BLOCK_ROW
+    T, h, sw = wl["tokens"], wl["h"], wl["sigma_w"]
+    G = atp.block_geometry(m, bm, h)
+    L = 3
+    g = G[L]
+    mode = atp.ATP_ROW_FIRST if bm == atp.ATP_BLOCK_COL else atp.ATP_COL_FIRST
+    K, N = 4 * h, h
+    if g.red_size < 2:
+        raise SystemExit(f"bench.py --linear: fc2 of {args.workload} has no reduction")
+    rnd = lambda shape, std, tid, dt=torch.bfloat16: S.randn_device(  # noqa: E731
+        shape, std, args.seed, tid, dev, dtype=dt)
+    x = rnd((T, g.k_loc), 1.0, S.TID["h"])
+    w = rnd((g.k_loc, g.n_loc), sw, S.TID["w_fc2"])
+    bias = rnd((g.n_loc,), 0.02, S.TID["b_fc2"])
+    sp = S.peer_sigma(g.k_loc, sw, 1.0)
+    tab = [rnd((T, g.n_loc), sp, S.PEER_TID_BASE + 100 * L + j, torch.float32)
+           for j in range(g.red_size)]
+    tab16 = [t.to(torch.bfloat16) for t in tab]
+    out = torch.empty((T, g.n_loc), dtype=torch.bfloat16, device=dev)
+    evs = [atp.HipEvent() for _ in range(chunks)]
+    side = torch.cuda.Stream()
+    flops = 2.0 * T * g.k_loc * g.n_loc
+    own = g.red_index
+
+    def chunked(c, parts16, serial):
+        def run():
+            cs = torch.cuda.current_stream()
+            ms = cs if serial else side
+            t = tab16 if parts16 else tab
+            atp.atp_shard_linear_fwd(m, mode, T, K, N, c, x, w, None, atp.ATP_EPI_NONE, t[own],
+                                     stream=cs, chunk_done=None if serial else evs[:c])
+            red = atp.atp_chunked_partial_reduce_bf16 if parts16 else \
+                atp.atp_chunked_partial_reduce
+            red(g.red_size, T, g.n_loc, c, t, bias, atp.ATP_EPI_BIAS, out, stream=ms,
+                chunk_ready=None if serial else evs[:c])
+            if not serial:
+                e = torch.cuda.Event()
+                e.record(ms)
+                cs.wait_event(e)
+        return run
+
+    def fused():
+        peers = [None if j == own else tab[j] for j in range(g.red_size)]
+        atp.atp_shard_linear_fwd_fused(m, mode, T, K, N, x, w, peers, bias, atp.ATP_EPI_BIAS,
+                                       out, stream=torch.cuda.current_stream())
+
+    variants = [("chunked_f32", chunked(chunks, False, False)),
+                ("chunked_f32_serial", chunked(chunks, False, True)),
+                ("unchunked_f32", chunked(1, False, True)),
+                ("chunked_bf16_partials", chunked(chunks, True, False)),
+                ("fused_epilogue", fused)]
+    res = {}
+    for name, run in variants:
+        for _ in range(args.warmup):
+            run()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            run()
+        e1.record()
+        torch.cuda.synchronize()
+        ms_ = e0.elapsed_time(e1) / args.steps
+        res[name] = dict(ms=round(ms_, 4), tflops=round(flops / (ms_ * 1e-3) / 1e12, 1))
+        log(f"[linear] {name}: {res[name]}")
+    base = res["chunked_f32"]["ms"]
+    out_line = dict(
+        metric="fc2 forward of one device (GEMM + reduction of its group), ms", value=base,
+        unit="ms", n_gpus=1, steps=args.steps, warmup=args.warmup, higher_is_better=False,
+        scaling="weak", vs_baseline=None, dtype="bf16", data="synthetic",
+        config=dict(workload=args.workload, linear="fc2", mesh=[d1, d2], tokens=T, h=h,
+                    chunks=chunks, red_size=g.red_size, gemm=[T, g.k_loc, g.n_loc],
+                    gflop=round(flops / 1e9, 1)),
+        variants=res)
+    print(json.dumps(out_line), flush=True)
 
 
 def attention_bench(torch, atp, S, args, wl):
@@ -348,6 +439,9 @@ def main():
     atp.load_library()
     if args.attention:
         attention_bench(torch, atp, S, args, wl)
+        return
+    if args.linear:
+        linear_bench(torch, atp, S, args, wl, chunks)
         return
     log(f"[bench] {atp.atp_version()} workload={args.workload} chunks={chunks} "
         f"pass={'fwd' if fwd_only else 'fwd+bwd'}")

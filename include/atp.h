@@ -107,8 +107,10 @@ atp_status atp_shard_geometry(const atp_mesh* mesh, int32_t mode, int64_t k, int
  *   y[t, :] = epi( x_loc[t, :] . w_loc )   for t in each chunk, in order.
  * x_loc  bf16 [tokens, k_loc], ld ldx.   w_loc bf16 [k_loc, n_loc], ld ldw.
  * If the reduction group has more than one member, y is this device's
- * Partial(SUM) block: y_dtype must be ATP_F32 and epi ATP_EPI_NONE (the
- * bias and GeLU belong after the reduction).  With a group of one, epi may
+ * Partial(SUM) block: epi must be ATP_EPI_NONE (the bias and GeLU belong
+ * after the reduction); y_dtype ATP_F32, or ATP_BF16 for partials kept in
+ * the training precision as the paper all-reduces them (Sec. 5: FP16),
+ * reduced by atp_chunked_partial_reduce_bf16.  With a group of one, epi may
  * be NONE, BIAS or BIAS_GELU and y f32 or bf16; bias_loc bf16 [n_loc]
  * (the block n_off..), preact (nullable, bf16, ld ldy) receives s + b for
  * BIAS_GELU.  chunk_done (nullable) holds `chunks` caller-created events;
@@ -139,6 +141,39 @@ atp_status atp_chunked_partial_reduce(int32_t red_size, int64_t tokens, int64_t 
                                       const void* preact_in, void* out, int32_t out_dtype,
                                       int64_t ldo, void* preact_out, void* stream,
                                       void* const* chunk_ready);
+
+/* The same reduction over bf16 Partial(SUM) blocks (partials: red_size
+ * device pointers, bf16 [tokens, ldp]): each value widened to f32 and
+ * summed in group order, then epi as above.  This is the variant of Sec. 5's
+ * half-precision training, where the all-reduced activations are 16-bit;
+ * it halves the bytes each reduction reads.  Errors as above. */
+atp_status atp_chunked_partial_reduce_bf16(int32_t red_size, int64_t tokens, int64_t n_loc,
+                                           int32_t chunks, const void* const* partials,
+                                           int64_t ldp, const void* bias_loc, int32_t epi,
+                                           const void* preact_in, void* out, int32_t out_dtype,
+                                           int64_t ldo, void* preact_out, void* stream,
+                                           void* const* chunk_ready);
+
+/* One shard linear with the group's reduction fused into the GEMM's
+ * epilogue: the fused GEMM-and-all-reduce design that Sec. 4.1 contrasts
+ * with chunked overlapping.  In one launch, unchunked:
+ *   out[t, :] = epi( sum_{j=0..red_size-1} P_j[t, :] ),
+ * with P_own = x_loc[t, :] . w_loc formed in the tile's registers and never
+ * stored, and P_j (j != red_index) read from peers[j] (f32 [tokens, ldp],
+ * the other members' partials; peers[red_index] is not read and may be
+ * NULL).  The terms are summed in group order, so out has the same bits as
+ * atp_shard_linear_fwd + atp_chunked_partial_reduce on the same inputs.
+ * x_loc, w_loc, bias_loc, epi (NONE, BIAS, BIAS_GELU), preact (nullable,
+ * bf16, ld ldo) as for atp_shard_linear_fwd; out f32 or bf16.
+ * Errors: as atp_shard_linear_fwd; UNSUPPORTED for a group of more than 8;
+ * INVALID_ARGUMENT for a missing peer or GELU_BWD. */
+atp_status atp_shard_linear_fwd_fused(const atp_mesh* mesh, int32_t mode, int64_t tokens,
+                                      int64_t k, int64_t n, const void* x_loc, int64_t ldx,
+                                      const void* w_loc, int64_t ldw,
+                                      const float* const* peers, int64_t ldp,
+                                      const void* bias_loc, int32_t epi, void* out,
+                                      int32_t out_dtype, int64_t ldo, void* preact,
+                                      void* stream);
 
 /* Backward of one shard linear (Sec. 4.2): with dy the gradient of this
  * device's reduced output block (bf16 [tokens, n_loc], ld lddy),

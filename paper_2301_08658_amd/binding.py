@@ -126,7 +126,8 @@ EXPORTS = (
     "atp_shard_linear_bwd", "atp_block_workspace_bytes", "atp_block_fwd", "atp_block_bwd",
     "atp_profile_enable", "atp_profile_collect", "atp_status_string", "atp_last_error",
     "atp_version", "atp_tcomm", "atp_hcm_mesh_cost", "atp_plan_mesh", "atp_transpose_bf16",
-    "atp_attention_fwd", "atp_attention_bwd",
+    "atp_attention_fwd", "atp_attention_bwd", "atp_chunked_partial_reduce_bf16",
+    "atp_shard_linear_fwd_fused",
 )
 
 _lib = None
@@ -152,6 +153,11 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.atp_chunked_partial_reduce.argtypes = [i32, i64, i64, i32, _fpp, i64, _vp, i32, _vp, _vp,
                                                i32, i64, _vp, _vp, _fpp]
     lib.atp_chunked_partial_reduce.restype = i32
+    lib.atp_chunked_partial_reduce_bf16.argtypes = lib.atp_chunked_partial_reduce.argtypes
+    lib.atp_chunked_partial_reduce_bf16.restype = i32
+    lib.atp_shard_linear_fwd_fused.argtypes = [mp, i32, i64, i64, i64, _vp, i64, _vp, i64, _fpp,
+                                               i64, _vp, i32, _vp, i32, i64, _vp, _vp]
+    lib.atp_shard_linear_fwd_fused.restype = i32
     lib.atp_shard_linear_bwd.argtypes = [mp, i32, i64, i64, i64, i32, _vp, i64, _vp, i64, _vp, i64,
                                          _vp, i64, _vp, i64, _vp, _vp, _fpp]
     lib.atp_shard_linear_bwd.restype = i32
@@ -266,11 +272,15 @@ def _dtype_code(t: torch.Tensor) -> int:
     raise TypeError(f"unsupported dtype {t.dtype}")
 
 
-def _ptr_table(ts: Sequence[torch.Tensor], rows: int, cols: int, name: str):
+def _ptr_table(ts: Sequence[Optional[torch.Tensor]], rows: int, cols: int, name: str,
+               dtype=torch.float32):
+    """Host array of device pointers (None entries stay NULL) and their common ld."""
     arr = (ctypes.c_void_p * len(ts))()
     ld = None
     for j, t in enumerate(ts):
-        p, l = _mat(t, rows, cols, torch.float32, f"{name}[{j}]")
+        if t is None:
+            continue
+        p, l = _mat(t, rows, cols, dtype, f"{name}[{j}]")
         arr[j] = p
         if ld is None:
             ld = l
@@ -347,6 +357,45 @@ def atp_chunked_partial_reduce(red_size: int, tokens: int, n_loc: int, chunks: i
     _check(load_library().atp_chunked_partial_reduce(
         int(red_size), int(tokens), int(n_loc), int(chunks), tab, ldp, bp, int(epi), ip, op,
         _dtype_code(out), ldo, qp, _stream(stream), _events(chunk_ready)))
+
+
+def atp_chunked_partial_reduce_bf16(red_size: int, tokens: int, n_loc: int, chunks: int,
+                                    partials, bias_loc, epi: int, out, preact_in=None,
+                                    preact_out=None, stream=None, chunk_ready=None):
+    if len(partials) != red_size:
+        raise ValueError("need exactly red_size partial buffers")
+    tab, _keep, ldp = _ptr_table(partials, tokens, n_loc, "partials", torch.bfloat16)
+    op, ldo = _mat(out, tokens, n_loc, out.dtype, "out")
+    ip, ldi = _mat(preact_in, tokens, n_loc, torch.bfloat16, "preact_in")
+    qp, ldq = _mat(preact_out, tokens, n_loc, torch.bfloat16, "preact_out")
+    for t, l in ((preact_in, ldi), (preact_out, ldq)):
+        if t is not None and l != ldo:
+            raise ValueError("pre-activation buffers must share out's leading dimension")
+    bp = _vec(bias_loc, n_loc, torch.bfloat16, "bias_loc")
+    _check(load_library().atp_chunked_partial_reduce_bf16(
+        int(red_size), int(tokens), int(n_loc), int(chunks), tab, ldp, bp, int(epi), ip, op,
+        _dtype_code(out), ldo, qp, _stream(stream), _events(chunk_ready)))
+
+
+def atp_shard_linear_fwd_fused(m: atp_mesh, mode: int, tokens: int, k: int, n: int, x_loc,
+                               w_loc, peers, bias_loc, epi: int, out, preact=None, stream=None):
+    """peers: red_size entries, the other members' f32 partials (the own
+    entry may be None; it is not read)."""
+    g = atp_shard_geometry(m, mode, k, n)
+    if len(peers) != g.red_size:
+        raise ValueError("need exactly red_size peer entries")
+    xp, ldx = _mat(x_loc, tokens, g.k_loc, torch.bfloat16, "x_loc")
+    wp, ldw = _mat(w_loc, g.k_loc, g.n_loc, torch.bfloat16, "w_loc")
+    tab, _keep, ldp = _ptr_table(peers, tokens, g.n_loc, "peers")
+    op, ldo = _mat(out, tokens, g.n_loc, out.dtype, "out")
+    pp, ldq = _mat(preact, tokens, g.n_loc, torch.bfloat16, "preact")
+    if preact is not None and ldq != ldo:
+        raise ValueError("preact must share out's leading dimension")
+    bp = _vec(bias_loc, g.n_loc, torch.bfloat16, "bias_loc")
+    _check(load_library().atp_shard_linear_fwd_fused(
+        ctypes.byref(m), int(mode), int(tokens), int(k), int(n), xp, ldx, wp, ldw,
+        tab if g.red_size > 1 else None, ldp, bp, int(epi), op, _dtype_code(out), ldo, pp,
+        _stream(stream)))
 
 
 def atp_shard_linear_bwd(m: atp_mesh, mode: int, tokens: int, k: int, n: int, chunks: int,

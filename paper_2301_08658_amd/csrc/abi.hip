@@ -217,7 +217,7 @@ atp_status run_gemm(const atp::GemmProblem& p, hipStream_t s) {
 atp_status run_reduce(const atp::ReduceProblem& p, hipStream_t s) {
     if (p.rows <= 0 || p.ncols <= 0) return ATP_OK;
     const double el = (double)p.rows * (double)p.ncols;
-    const double bytes = el * (4.0 * p.nparts + (p.out_bf16 ? 2.0 : 4.0)) +
+    const double bytes = el * ((p.parts_bf16 ? 2.0 : 4.0) * p.nparts + (p.out_bf16 ? 2.0 : 4.0)) +
                          ((p.epi == atp::EPI_GELU_BWD || p.pre_out) ? 2.0 * el : 0.0);
     std::string name = "partial_reduce";
     if (g_prof_on && g_prof_detail) {
@@ -262,13 +262,16 @@ atp::GemmProblem gemm_problem(int layout, const void* A, int64_t lda, const void
     return p;
 }
 
-atp::ReduceProblem reduce_problem(int nparts, const float* const* parts, int64_t ldp,
+// parts: any array of nparts device pointers (fp32, or bf16 with parts_bf16)
+template <class PartTable>
+atp::ReduceProblem reduce_problem(int nparts, PartTable parts, int64_t ldp,
                                   int64_t row0, int64_t rows, int64_t ncols, int epi,
                                   const void* bias, const void* pre_in, void* out, int64_t ldo,
-                                  bool out_bf16, void* pre_out) {
+                                  bool out_bf16, void* pre_out, bool parts_bf16 = false) {
     atp::ReduceProblem p;
     memset(&p, 0, sizeof p);
     p.nparts = nparts;
+    p.parts_bf16 = parts_bf16;
     for (int j = 0; j < nparts; ++j) p.parts[j] = parts[j];
     p.ldp = ldp;
     p.row0 = row0;
@@ -543,10 +546,10 @@ atp_status atp_shard_linear_fwd(const atp_mesh* mesh, int32_t mode, int64_t toke
     if (!valid_epi(epi) || epi == ATP_EPI_GELU_BWD)
         return set_error(ATP_ERR_INVALID_ARGUMENT, "epilogue %d not valid for a forward GEMM", epi);
     if (!valid_dtype(y_dtype)) return set_error(ATP_ERR_INVALID_ARGUMENT, "y_dtype %d", y_dtype);
-    if (g.red_size > 1 && (epi != ATP_EPI_NONE || y_dtype != ATP_F32))
+    if (g.red_size > 1 && epi != ATP_EPI_NONE)
         return set_error(ATP_ERR_INVALID_ARGUMENT,
-                    "reduction group of %d: y is a Partial(SUM) block, it must be f32 with no "
-                    "epilogue (bias and GeLU act after the reduction)", g.red_size);
+                    "reduction group of %d: y is a Partial(SUM) block, it takes no epilogue "
+                    "(bias and GeLU act after the reduction)", g.red_size);
     if (epi == ATP_EPI_BIAS || epi == ATP_EPI_BIAS_GELU) ATP_CHECK(check_vec(bias_loc, "bias"));
     if (preact) {
         if (epi != ATP_EPI_BIAS_GELU)
@@ -571,11 +574,14 @@ atp_status atp_shard_linear_fwd(const atp_mesh* mesh, int32_t mode, int64_t toke
     return ATP_OK;
 }
 
-atp_status atp_chunked_partial_reduce(int32_t red_size, int64_t tokens, int64_t n_loc,
-                                      int32_t chunks, const float* const* partials, int64_t ldp,
-                                      const void* bias_loc, int32_t epi, const void* preact_in,
-                                      void* out, int32_t out_dtype, int64_t ldo, void* preact_out,
-                                      void* stream, void* const* chunk_ready) {
+extern "C++" {
+namespace {
+
+template <class PartTable>
+atp_status chunked_reduce(int32_t red_size, int64_t tokens, int64_t n_loc, int32_t chunks,
+                          PartTable partials, bool parts_bf16, int64_t ldp, const void* bias_loc,
+                          int32_t epi, const void* preact_in, void* out, int32_t out_dtype,
+                          int64_t ldo, void* preact_out, void* stream, void* const* chunk_ready) {
     if (red_size < 1) return set_error(ATP_ERR_INVALID_ARGUMENT, "red_size must be >= 1");
     if (red_size > ATP_MAX_GROUP)
         return set_error(ATP_ERR_UNSUPPORTED, "red_size %d exceeds %d", red_size, ATP_MAX_GROUP);
@@ -605,10 +611,79 @@ atp_status atp_chunked_partial_reduce(int32_t red_size, int64_t tokens, int64_t 
                       "hipStreamWaitEvent");
         atp::ReduceProblem p = reduce_problem(red_size, partials, ldp, (int64_t)c * mc, mc, n_loc,
                                               epi, bias_loc, preact_in, out, ldo,
-                                              out_dtype == ATP_BF16, preact_out);
+                                              out_dtype == ATP_BF16, preact_out, parts_bf16);
         ATP_CHECK(run_reduce(p, s));
     }
     return ATP_OK;
+}
+
+}  // namespace
+}  // extern "C++"
+
+atp_status atp_chunked_partial_reduce(int32_t red_size, int64_t tokens, int64_t n_loc,
+                                      int32_t chunks, const float* const* partials, int64_t ldp,
+                                      const void* bias_loc, int32_t epi, const void* preact_in,
+                                      void* out, int32_t out_dtype, int64_t ldo, void* preact_out,
+                                      void* stream, void* const* chunk_ready) {
+    return chunked_reduce(red_size, tokens, n_loc, chunks, partials, false, ldp, bias_loc, epi,
+                          preact_in, out, out_dtype, ldo, preact_out, stream, chunk_ready);
+}
+
+atp_status atp_chunked_partial_reduce_bf16(int32_t red_size, int64_t tokens, int64_t n_loc,
+                                           int32_t chunks, const void* const* partials,
+                                           int64_t ldp, const void* bias_loc, int32_t epi,
+                                           const void* preact_in, void* out, int32_t out_dtype,
+                                           int64_t ldo, void* preact_out, void* stream,
+                                           void* const* chunk_ready) {
+    return chunked_reduce(red_size, tokens, n_loc, chunks, partials, true, ldp, bias_loc, epi,
+                          preact_in, out, out_dtype, ldo, preact_out, stream, chunk_ready);
+}
+
+atp_status atp_shard_linear_fwd_fused(const atp_mesh* mesh, int32_t mode, int64_t tokens,
+                                      int64_t k, int64_t n, const void* x_loc, int64_t ldx,
+                                      const void* w_loc, int64_t ldw,
+                                      const float* const* peers, int64_t ldp,
+                                      const void* bias_loc, int32_t epi, void* out,
+                                      int32_t out_dtype, int64_t ldo, void* preact,
+                                      void* stream) {
+    atp_shard g;
+    ATP_CHECK(geometry(mesh, mode, k, n, &g));
+    if (tokens < 0) return set_error(ATP_ERR_INVALID_ARGUMENT, "tokens must be >= 0");
+    ATP_CHECK(check_mat(x_loc, tokens, ldx, g.k_loc, "x_loc"));
+    ATP_CHECK(check_mat(w_loc, g.k_loc, ldw, g.n_loc, "w_loc"));
+    ATP_CHECK(check_mat(out, tokens, ldo, g.n_loc, "out"));
+    if (!valid_epi(epi) || epi == ATP_EPI_GELU_BWD)
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "epilogue %d not valid for a forward GEMM", epi);
+    if (!valid_dtype(out_dtype)) return set_error(ATP_ERR_INVALID_ARGUMENT, "out_dtype %d", out_dtype);
+    if (g.red_size > atp::kMaxFusedParts)
+        return set_error(ATP_ERR_UNSUPPORTED, "fused epilogue: group of %d exceeds %d",
+                         g.red_size, atp::kMaxFusedParts);
+    if (g.red_size > 1) {
+        if (!peers) return set_error(ATP_ERR_INVALID_ARGUMENT, "peers is NULL");
+        for (int j = 0; j < g.red_size; ++j) {
+            if (j == g.red_index) continue;
+            char nm[32];
+            snprintf(nm, sizeof nm, "peers[%d]", j);
+            ATP_CHECK(check_mat(peers[j], tokens, ldp, g.n_loc, nm));
+        }
+    }
+    if (epi == ATP_EPI_BIAS || epi == ATP_EPI_BIAS_GELU) ATP_CHECK(check_vec(bias_loc, "bias"));
+    if (preact) {
+        if (epi != ATP_EPI_BIAS_GELU)
+            return set_error(ATP_ERR_INVALID_ARGUMENT, "preact is only written by BIAS_GELU");
+        ATP_CHECK(check_mat(preact, tokens, ldo, g.n_loc, "preact"));
+    }
+    atp::GemmProblem p = gemm_problem(atp::LAYOUT_NN, x_loc, ldx, w_loc, ldw, out, ldo,
+                                      out_dtype == ATP_BF16, epi, tokens, g.n_loc, g.k_loc);
+    p.bias = bias_loc;
+    p.pre_out = preact;
+    if (g.red_size > 1) {
+        p.nparts = g.red_size;
+        p.own = g.red_index;
+        p.ldp = ldp;
+        for (int j = 0; j < g.red_size; ++j) p.peers[j] = j == g.red_index ? nullptr : peers[j];
+    }
+    return run_gemm(p, static_cast<hipStream_t>(stream));
 }
 
 atp_status atp_shard_linear_bwd(const atp_mesh* mesh, int32_t mode, int64_t tokens, int64_t k,

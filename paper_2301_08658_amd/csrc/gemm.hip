@@ -21,6 +21,7 @@
 
 #include <type_traits>
 
+#include "epilogue_math.h"
 #include "kernels.h"
 #include "lds_dma.h"
 
@@ -41,26 +42,10 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 
-__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
-    return __uint_as_float(bits16 << 16);
-}
-
-__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return 0x7fc0u;  // NaN
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return u >> 16;
-}
-
-__device__ __forceinline__ float gelu_f(float x) {
-    return 0.5f * x * (1.0f + erff(x * 0.70710678118654752440f));
-}
-
-__device__ __forceinline__ float gelu_grad_f(float x) {
-    const float cdf = 0.5f * (1.0f + erff(x * 0.70710678118654752440f));
-    const float pdf = 0.39894228040143267794f * expf(-0.5f * x * x);
-    return cdf + x * pdf;
-}
+using epi::bf16_to_f32;
+using epi::f32_to_bf16_rne;
+using epi::gelu_f;
+using epi::gelu_grad_f;
 
 // 16-byte chunk swizzles.  K-major rows hold BK/8 chunks; MN-major rows
 // (one per k) hold at least 16 chunks.
@@ -82,6 +67,11 @@ struct KArgs {
     // and writes C + s*c_split (an fp32 slab per split); splits == 1: plain
     int splits;
     int64_t ksplit, c_split;
+    // fused peer sum (nparts > 1): the group's partials summed in group
+    // order, the tile's own accumulators at position own
+    int nparts, own;
+    const float* peers[kMaxFusedParts];
+    int64_t ldp;
 };
 
 // Workgroup -> logical tile index: the dispatcher deals workgroups
@@ -122,6 +112,25 @@ using dma::wait_vmcnt;
 // bf16 (round to nearest even) store.
 template <int EPI, bool OUT_BF16>
 __device__ __forceinline__ void epilogue_store(const KArgs& a, int64_t m, int64_t n, float* v) {
+    if (a.nparts > 1) {
+        // Partial(SUM) of the group, summed in group order 0..nparts-1 (the
+        // reduction kernel's order, so the bits equal a separate reduction
+        // of the same partials); position own is this tile's accumulators
+        float t[4] = {v[0], v[1], v[2], v[3]};
+#pragma unroll
+        for (int j = 0; j < kMaxFusedParts; ++j) {
+            if (j >= a.nparts) break;
+            f32x4 q = f32x4{t[0], t[1], t[2], t[3]};
+            if (j != a.own) q = *reinterpret_cast<const f32x4*>(a.peers[j] + m * a.ldp + n);
+            if (j == 0) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] = q[r];
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] += q[r];
+            }
+        }
+    }
     if constexpr (EPI == EPI_BIAS || EPI == EPI_BIAS_GELU) {
         const u32x2 bb = *reinterpret_cast<const u32x2*>(a.bias + n);
         v[0] += bf16_to_f32(bb[0] & 0xffffu);
@@ -514,6 +523,10 @@ KArgs kargs(const GemmProblem& p, int bm, int bn) {
     a.splits = p.splits > 1 ? p.splits : 1;
     a.ksplit = a.splits > 1 ? p.ksplit : p.K;
     a.c_split = p.c_split;
+    a.nparts = p.nparts > 1 ? p.nparts : 1;
+    a.own = p.own;
+    for (int j = 0; j < kMaxFusedParts; ++j) a.peers[j] = p.peers[j];
+    a.ldp = p.ldp;
     return a;
 }
 
@@ -616,6 +629,9 @@ hipError_t launch_gemm(const GemmProblem& p, hipStream_t s) {
                          (p.lda > p.ldb ? p.lda : p.ldb) * 2;
     if (span > 0x7fffff00) return hipErrorInvalidValue;
     const bool b16 = p.out_bf16;
+    if (p.nparts > kMaxFusedParts || (p.nparts > 1 && (p.splits > 1 || p.own < 0 ||
+                                                       p.own >= p.nparts || p.ldp % 4)))
+        return hipErrorInvalidValue;
     if (p.splits > 1) {
         // split-K: plain fp32 outputs, whole K steps per split, every split
         // non-empty

@@ -32,7 +32,14 @@ struct GemmProblem {
     // ksplit a multiple of 64, every split non-empty
     int splits = 1;
     int64_t ksplit = 0, c_split = 0;
+    // fused peer sum (NN, no split): when nparts > 1 the epilogue forms
+    // sum_{j < nparts} P_j in group order before bias / GeLU, with P_own the
+    // tile's own accumulators and the others read from peers[j] (fp32, ld ldp)
+    int nparts = 1, own = 0;
+    const float* peers[8] = {};   // kMaxFusedParts
+    int64_t ldp = 0;
 };
+constexpr int kMaxFusedParts = 8;
 
 // True if the kernel set has an instance for this (layout, epi, out) combination.
 bool gemm_supported(int layout, int epi, bool out_bf16);
@@ -52,7 +59,8 @@ constexpr int kMaxParts = 64;
 
 struct ReduceProblem {
     int nparts;
-    const float* parts[kMaxParts];  // each f32 [.., ldp]
+    const void* parts[kMaxParts];   // each f32 (or bf16 if parts_bf16) [.., ldp]
+    bool parts_bf16;
     int64_t ldp;
     int64_t row0, rows, ncols;      // rows [row0, row0+rows), columns [0, ncols)
     int epi;

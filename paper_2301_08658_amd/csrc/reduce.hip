@@ -12,6 +12,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "epilogue_math.h"
 #include "kernels.h"
 
 namespace atp {
@@ -23,26 +24,10 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int RT = 256;        // threads per block
 constexpr int PGROUP = 8;      // parts loaded before summing
 
-__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
-    return __uint_as_float(bits16 << 16);
-}
-
-__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return 0x7fc0u;
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return u >> 16;
-}
-
-__device__ __forceinline__ float gelu_f(float x) {
-    return 0.5f * x * (1.0f + erff(x * 0.70710678118654752440f));
-}
-
-__device__ __forceinline__ float gelu_grad_f(float x) {
-    const float cdf = 0.5f * (1.0f + erff(x * 0.70710678118654752440f));
-    const float pdf = 0.39894228040143267794f * expf(-0.5f * x * x);
-    return cdf + x * pdf;
-}
+using epi::bf16_to_f32;
+using epi::f32_to_bf16_rne;
+using epi::gelu_f;
+using epi::gelu_grad_f;
 
 __device__ __forceinline__ void unpack8(const u32x4& w, float* f) {
 #pragma unroll
@@ -60,7 +45,7 @@ __device__ __forceinline__ u32x4 pack8(const float* f) {
     return w;
 }
 
-template <int EPI, bool OUT_BF16>
+template <int EPI, bool OUT_BF16, bool PART_BF16>
 __global__ __launch_bounds__(RT) void reduce_kernel(ReduceProblem p) {
     const int64_t cols8 = p.ncols >> 3;
     const int64_t total = p.rows * cols8;
@@ -74,17 +59,30 @@ __global__ __launch_bounds__(RT) void reduce_kernel(ReduceProblem p) {
     float s[8];
     for (int j0 = 0; j0 < p.nparts; j0 += PGROUP) {
         f32x4 lo[PGROUP], hi[PGROUP];
+        u32x4 hw[PGROUP];   // eight bf16 parts
 #pragma unroll
         for (int u = 0; u < PGROUP; ++u) {
             if (j0 + u < p.nparts) {
-                const f32x4* q = reinterpret_cast<const f32x4*>(p.parts[j0 + u] + off);
-                lo[u] = __builtin_nontemporal_load(q);
-                hi[u] = __builtin_nontemporal_load(q + 1);
+                if constexpr (PART_BF16) {
+                    hw[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(
+                        static_cast<const uint16_t*>(p.parts[j0 + u]) + off));
+                } else {
+                    const f32x4* q = reinterpret_cast<const f32x4*>(
+                        static_cast<const float*>(p.parts[j0 + u]) + off);
+                    lo[u] = __builtin_nontemporal_load(q);
+                    hi[u] = __builtin_nontemporal_load(q + 1);
+                }
             }
         }
 #pragma unroll
         for (int u = 0; u < PGROUP; ++u) {
             if (j0 + u < p.nparts) {
+                if constexpr (PART_BF16) {
+                    float f[8];
+                    unpack8(hw[u], f);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) { lo[u][e] = f[e]; hi[u][e] = f[4 + e]; }
+                }
                 if (j0 + u == 0) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e) { s[e] = lo[u][e]; s[4 + e] = hi[u][e]; }
@@ -128,12 +126,13 @@ __global__ __launch_bounds__(RT) void reduce_kernel(ReduceProblem p) {
     }
 }
 
-template <int EPI, bool OUT_BF16>
+template <int EPI, bool OUT_BF16, bool PART_BF16>
 hipError_t launch_r(const ReduceProblem& p, hipStream_t s) {
     const int64_t total = p.rows * (p.ncols >> 3);
     if (total == 0) return hipSuccess;
     const int64_t blocks = (total + RT - 1) / RT;
-    hipLaunchKernelGGL((reduce_kernel<EPI, OUT_BF16>), dim3((unsigned)blocks), dim3(RT), 0, s, p);
+    hipLaunchKernelGGL((reduce_kernel<EPI, OUT_BF16, PART_BF16>), dim3((unsigned)blocks), dim3(RT),
+                       0, s, p);
     return hipGetLastError();
 }
 
@@ -182,26 +181,33 @@ __global__ __launch_bounds__(CS_T) void colsum_kernel(const uint16_t* __restrict
     }
 }
 
-}  // namespace
-
-hipError_t launch_reduce(const ReduceProblem& p, hipStream_t s) {
+template <bool PART_BF16>
+hipError_t launch_reduce_parts(const ReduceProblem& p, hipStream_t s) {
     const bool b = p.out_bf16;
     switch (p.epi) {
     case EPI_NONE:
-        return b ? launch_r<EPI_NONE, true>(p, s) : launch_r<EPI_NONE, false>(p, s);
+        return b ? launch_r<EPI_NONE, true, PART_BF16>(p, s)
+                 : launch_r<EPI_NONE, false, PART_BF16>(p, s);
     case EPI_BIAS:
-        return b ? launch_r<EPI_BIAS, true>(p, s) : launch_r<EPI_BIAS, false>(p, s);
+        return b ? launch_r<EPI_BIAS, true, PART_BF16>(p, s)
+                 : launch_r<EPI_BIAS, false, PART_BF16>(p, s);
     case EPI_BIAS_GELU:
-        return b ? launch_r<EPI_BIAS_GELU, true>(p, s) : launch_r<EPI_BIAS_GELU, false>(p, s);
+        return b ? launch_r<EPI_BIAS_GELU, true, PART_BF16>(p, s)
+                 : launch_r<EPI_BIAS_GELU, false, PART_BF16>(p, s);
     case EPI_GELU_BWD:
-        return b ? launch_r<EPI_GELU_BWD, true>(p, s) : launch_r<EPI_GELU_BWD, false>(p, s);
+        return b ? launch_r<EPI_GELU_BWD, true, PART_BF16>(p, s)
+                 : launch_r<EPI_GELU_BWD, false, PART_BF16>(p, s);
     default:
         return hipErrorInvalidValue;
     }
 }
 
-// The split slabs are parts of a reduction whose rows start at 0: the
-// reduction kernel adds them in slab order.
+}  // namespace
+
+hipError_t launch_reduce(const ReduceProblem& p, hipStream_t s) {
+    return p.parts_bf16 ? launch_reduce_parts<true>(p, s) : launch_reduce_parts<false>(p, s);
+}
+
 hipError_t launch_split_sum(const float* ws, int S, int64_t stride, int64_t ld, int64_t rows,
                             int64_t cols, float* out, int64_t ldo, hipStream_t s) {
     if (S < 1 || S > kMaxParts || (cols & 7) || (ld & 3) || (ldo & 3))

@@ -96,10 +96,10 @@ def test_linear_fwd_validation():
     assert _fwd(m, ldx=64) == B.ATP_ERR_INVALID_ARGUMENT         # ld < k_loc = 128
     assert _fwd(m, ldw=132) == B.ATP_ERR_UNSUPPORTED             # ld not a multiple of 8
     assert _fwd(m, k=255) == B.ATP_ERR_SHAPE
-    # a partial output (group of 2) cannot take the bias / GeLU or a bf16 store
+    # a partial output (group of 2) cannot take the bias / GeLU (f32 or bf16)
     assert _fwd(m, epi=1, bias=FAKE) == B.ATP_ERR_INVALID_ARGUMENT
     assert "Partial" in atp.binding.last_error()
-    assert _fwd(m, ydt=1) == B.ATP_ERR_INVALID_ARGUMENT
+    assert _fwd(m, ydt=1, epi=2, bias=FAKE) == B.ATP_ERR_INVALID_ARGUMENT
     # group of one: BIAS needs the bias vector; GELU_BWD is not a forward epilogue
     m1 = atp.mesh(1, 1, 0, 0)
     assert _fwd(m1, epi=1, bias=None) == B.ATP_ERR_INVALID_ARGUMENT
@@ -132,6 +132,45 @@ def test_reduce_validation():
     assert _red(epi=9) == B.ATP_ERR_INVALID_ARGUMENT
     assert _red(epi=1, bias=FAKE, pout=FAKE) == B.ATP_ERR_INVALID_ARGUMENT
     assert _red(odt=5) == B.ATP_ERR_INVALID_ARGUMENT
+
+
+def test_reduce_bf16_validation():
+    lib = atp.load_library()
+
+    def red16(red_size=2, parts=(FAKE, FAKE), epi=0, bias=None):
+        arr = (ctypes.c_void_p * max(1, len(parts)))(*parts)
+        return lib.atp_chunked_partial_reduce_bf16(red_size, 64, 256, 2, ctypes.cast(arr, B._fpp),
+                                                   256, bias, epi, None, FAKE, 1, 256, None,
+                                                   None, None)
+    assert red16(red_size=0) == B.ATP_ERR_INVALID_ARGUMENT
+    assert red16(parts=(FAKE, 0)) == B.ATP_ERR_INVALID_ARGUMENT
+    assert "partials[1]" in atp.binding.last_error()
+    assert red16(parts=(FAKE, MISALIGNED)) == B.ATP_ERR_UNSUPPORTED
+    assert red16(epi=1) == B.ATP_ERR_INVALID_ARGUMENT               # bias missing
+
+
+def test_fused_linear_validation():
+    lib = atp.load_library()
+
+    def fused(m, tokens=64, k=256, n=512, peers=(FAKE, None), epi=0, bias=None, pre=None,
+              odt=1):
+        g = atp.atp_shard_geometry(m, 0, k, n)
+        arr = (ctypes.c_void_p * max(1, len(peers)))(*[p or 0 for p in peers]) \
+            if peers is not None else None
+        tab = ctypes.cast(arr, B._fpp) if arr is not None else None
+        return lib.atp_shard_linear_fwd_fused(ctypes.byref(m), 0, tokens, k, n, FAKE, g.k_loc,
+                                              FAKE, g.n_loc, tab, g.n_loc, bias, epi, FAKE, odt,
+                                              g.n_loc, pre, None)
+    m = atp.mesh(2, 2, 1, 0)                  # row-first: group over d1, own index 1
+    assert fused(m, epi=3) == B.ATP_ERR_INVALID_ARGUMENT            # GELU_BWD
+    assert fused(m, peers=None) == B.ATP_ERR_INVALID_ARGUMENT
+    assert fused(m, peers=(None, FAKE)) == B.ATP_ERR_INVALID_ARGUMENT
+    assert "peers[0]" in atp.binding.last_error()
+    assert fused(m, tokens=-1) == B.ATP_ERR_INVALID_ARGUMENT
+    assert fused(m, epi=1) == B.ATP_ERR_INVALID_ARGUMENT            # bias missing
+    assert fused(m, pre=FAKE) == B.ATP_ERR_INVALID_ARGUMENT         # preact only with GeLU
+    assert fused(m, odt=4) == B.ATP_ERR_INVALID_ARGUMENT
+    assert fused(atp.mesh(16, 1, 0, 0), k=4096, peers=(FAKE,) * 16) == B.ATP_ERR_UNSUPPORTED
 
 
 def test_linear_bwd_validation():
