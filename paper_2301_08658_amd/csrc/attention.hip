@@ -586,11 +586,14 @@ __global__ __launch_bounds__(NTHR * KG, 2 / KG) void attention_dkv_kernel(AttnBw
     }
 }
 
-// dQ of one 64-query tile (4 waves x 16 queries).  KG groups of four waves
-// split its key tiles (group 0 the first half, group 1 the rest, with the
-// diagonal); group 1 adds its sum into group 0's through LDS at the end.
-template <int KG>
+// dQ of one query tile: RB row blocks of 16 queries per wave (64 RB rows;
+// block r of wave w holds rows 64 r + 16 w .. + 15), so every K and V
+// fragment read from LDS feeds RB MFMAs.  KG groups of four waves split the
+// tile's key tiles (group 0 the first half, group 1 the rest, with the
+// diagonal); group 1 adds its sums into group 0's through LDS at the end.
+template <int RB, int KG>
 __global__ __launch_bounds__(NTHR * KG, 2 / KG) void attention_dq_kernel(AttnBwdArgs a) {
+    constexpr int QT = 64 * RB;
     __shared__ __attribute__((aligned(16))) uint16_t kv[KG][2][2][BN * D];   // [grp][buf][K|V]
     const int lane = threadIdx.x & 63, g = lane >> 4;
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -602,35 +605,46 @@ __global__ __launch_bounds__(NTHR * KG, 2 / KG) void attention_dq_kernel(AttnBwd
     const int64_t tok0 = (int64_t)b * a.seq, T = (int64_t)a.batch * a.seq;
     const int64_t qc = a.col0 + (int64_t)hh * 3 * D;
 
-    const int qabs = qt * BM + wave * 16 + (lane & 15);
-    bf16x8 qf[4], of[4];
-    float l2 = 0.f, dl = 0.f;
+    int qabs[RB];
+    bf16x8 qf[RB][4], of[RB][4];
+    float l2[RB], dl[RB];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-        if (qabs < a.seq) {
-            qf[ks] = *reinterpret_cast<const bf16x8*>(a.qkv + (tok0 + qabs) * a.ldq + qc + 32 * ks +
-                                                      8 * g);
-            of[ks] = *reinterpret_cast<const bf16x8*>(a.dout + (tok0 + qabs) * a.lddo + a.docol0 +
-                                                      (int64_t)hh * D + 32 * ks + 8 * g);
-        } else {
-            qf[ks] = __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0});
-            of[ks] = qf[ks];
+    for (int r = 0; r < RB; ++r) {
+        qabs[r] = qt * QT + 64 * r + wave * 16 + (lane & 15);
+        l2[r] = 0.f;
+        dl[r] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            if (qabs[r] < a.seq) {
+                qf[r][ks] = *reinterpret_cast<const bf16x8*>(
+                    a.qkv + (tok0 + qabs[r]) * a.ldq + qc + 32 * ks + 8 * g);
+                of[r][ks] = *reinterpret_cast<const bf16x8*>(
+                    a.dout + (tok0 + qabs[r]) * a.lddo + a.docol0 + (int64_t)hh * D + 32 * ks +
+                    8 * g);
+            } else {
+                qf[r][ks] = __builtin_bit_cast(bf16x8, u32x4{0, 0, 0, 0});
+                of[r][ks] = qf[r][ks];
+            }
+        }
+        if (qabs[r] < a.seq) {
+            l2[r] = a.lse[(int64_t)hh * T + tok0 + qabs[r]] * 1.44269504088896340736f;
+            dl[r] = a.delta[(int64_t)hh * T + tok0 + qabs[r]];
         }
     }
-    if (qabs < a.seq) {
-        l2 = a.lse[(int64_t)hh * T + tok0 + qabs] * 1.44269504088896340736f;
-        dl = a.delta[(int64_t)hh * T + tok0 + qabs];
-    }
-    f32x4 dq[8];
+    f32x4 dq[RB][8];
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) dq[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int r = 0; r < RB; ++r)
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) dq[r][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     int boff[4], toff[8];
     offsets(lane, boff, toff);
     const uint16_t* kbase = a.qkv + qc + D;
     const uint16_t* vbase = a.qkv + qc + 2 * D;
-    // key tiles 0 .. qt: group 0 the first half, group 1 the rest
-    const int nk = qt + 1;
+    // key tiles up to the tile's last row inside the sequence: group 0 the
+    // first half, group 1 the rest
+    const int last = min(qt * QT + QT, a.seq) - 1;
+    const int nk = last / BN + 1;
     const int half = KG > 1 ? (nk + 1) / 2 : nk;
     const int k0 = grp == 0 ? 0 : half;
     const int mine = grp == 0 ? half : nk - half;   // <= half
@@ -649,39 +663,58 @@ __global__ __launch_bounds__(NTHR * KG, 2 / KG) void attention_dq_kernel(AttnBwd
             if (i + 1 < mine)
                 cp.issue(kbase, a.ldq, vbase, a.ldq, tok0, (kt + 1) * BN, a.seq,
                          kb[(i + 1) & 1][0], kb[(i + 1) & 1][1], wave);
-            // S and dP: lane holds (query = qabs, key = 16 j + 4 g + e)
-            const bool masked = kt == qt || (kt + 1) * BN > a.seq;
-            f32x4 dsv[4];
+            // S and dP: lane holds (query = qabs[r], key = 16 j + 4 g + e); a
+            // key tile reaching past the tile's first row, or a ragged one,
+            // has masked keys
+            const bool masked = (kt + 1) * BN > qt * QT || (kt + 1) * BN > a.seq;
+            f32x4 dsv[RB][4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f}, dacc = sacc;
+                f32x4 sacc[RB], dacc[RB];
+#pragma unroll
+                for (int r = 0; r < RB; ++r) {
+                    sacc[r] = f32x4{0.f, 0.f, 0.f, 0.f};
+                    dacc[r] = sacc[r];
+                }
 #pragma unroll
                 for (int ks = 0; ks < 4; ++ks) {
-                    sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        *reinterpret_cast<const bf16x8*>(ks_ + 16 * j * D + boff[ks]), qf[ks],
-                        sacc, 0, 0, 0);
-                    dacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        *reinterpret_cast<const bf16x8*>(vs_ + 16 * j * D + boff[ks]), of[ks],
-                        dacc, 0, 0, 0);
+                    const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks_ + 16 * j * D + boff[ks]);
+                    const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vs_ + 16 * j * D + boff[ks]);
+#pragma unroll
+                    for (int r = 0; r < RB; ++r) {
+                        sacc[r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[r][ks], sacc[r],
+                                                                          0, 0, 0);
+                        dacc[r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, of[r][ks], dacc[r],
+                                                                          0, 0, 0);
+                    }
                 }
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[e], a.scale_log2, -l2));
-                    if (masked) {
-                        const int kabs = kt * BN + 16 * j + 4 * g + e;
-                        if (kabs > qabs || kabs >= a.seq) pv = 0.f;
+                for (int r = 0; r < RB; ++r)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        float pv = __builtin_amdgcn_exp2f(
+                            __builtin_fmaf(sacc[r][e], a.scale_log2, -l2[r]));
+                        if (masked) {
+                            const int kabs = kt * BN + 16 * j + 4 * g + e;
+                            if (kabs > qabs[r] || kabs >= a.seq) pv = 0.f;
+                        }
+                        dsv[r][j][e] = pv * (dacc[r][e] - dl[r]);
                     }
-                    dsv[j][e] = pv * (dacc[e] - dl);
-                }
             }
             // dQ += dS K over two 32-key slices
 #pragma unroll
             for (int sl = 0; sl < 2; ++sl) {
-                const bf16x8 sf = pack_pair(dsv[2 * sl], dsv[2 * sl + 1]);
+                bf16x8 sf[RB];
 #pragma unroll
-                for (int dt = 0; dt < 8; ++dt)
-                    dq[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        frag_tr_at(ks_ + 32 * sl * D + toff[dt]), sf, dq[dt], 0, 0, 0);
+                for (int r = 0; r < RB; ++r) sf[r] = pack_pair(dsv[r][2 * sl], dsv[r][2 * sl + 1]);
+#pragma unroll
+                for (int dt = 0; dt < 8; ++dt) {
+                    const bf16x8 kt_ = frag_tr_at(ks_ + 32 * sl * D + toff[dt]);
+#pragma unroll
+                    for (int r = 0; r < RB; ++r)
+                        dq[r][dt] =
+                            __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt_, sf[r], dq[r][dt], 0, 0, 0);
+                }
             }
         }
         dma::wait_vmcnt<0>();
@@ -691,19 +724,25 @@ __global__ __launch_bounds__(NTHR * KG, 2 / KG) void attention_dq_kernel(AttnBwd
         f32x4* x = reinterpret_cast<f32x4*>(&kv[1][0][0][0]);
         if (grp == 1) {
 #pragma unroll
-            for (int dt = 0; dt < 8; ++dt) x[(wave * 8 + dt) * 64 + lane] = dq[dt];
+            for (int r = 0; r < RB; ++r)
+#pragma unroll
+                for (int dt = 0; dt < 8; ++dt) x[((wave * RB + r) * 8 + dt) * 64 + lane] = dq[r][dt];
         }
         __syncthreads();
         if (grp == 1) return;
 #pragma unroll
-        for (int dt = 0; dt < 8; ++dt) dq[dt] += x[(wave * 8 + dt) * 64 + lane];
+        for (int r = 0; r < RB; ++r)
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt) dq[r][dt] += x[((wave * RB + r) * 8 + dt) * 64 + lane];
     }
-    if (qabs < a.seq) {
-        uint16_t* row = a.dqkv + (tok0 + qabs) * a.lddq + a.dcol0 + (int64_t)hh * 3 * D;
+#pragma unroll
+    for (int r = 0; r < RB; ++r) {
+        if (qabs[r] >= a.seq) continue;
+        uint16_t* row = a.dqkv + (tok0 + qabs[r]) * a.lddq + a.dcol0 + (int64_t)hh * 3 * D;
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) {
-            const u32x2 w = {pack_bf16x2(dq[dt][0] * a.inv_sqrt_d, dq[dt][1] * a.inv_sqrt_d),
-                             pack_bf16x2(dq[dt][2] * a.inv_sqrt_d, dq[dt][3] * a.inv_sqrt_d)};
+            const u32x2 w = {pack_bf16x2(dq[r][dt][0] * a.inv_sqrt_d, dq[r][dt][1] * a.inv_sqrt_d),
+                             pack_bf16x2(dq[r][dt][2] * a.inv_sqrt_d, dq[r][dt][3] * a.inv_sqrt_d)};
             *reinterpret_cast<u32x2*>(row + 16 * dt + 4 * g) = w;
         }
     }
@@ -746,12 +785,21 @@ hipError_t launch_attention_bwd(const AttentionBwdProblem& p, hipStream_t s) {
     if (split) {
         hipLaunchKernelGGL((attention_dkv_kernel<2>), dim3((unsigned)grid), dim3(2 * NTHR), 0, s,
                            a);
-        hipLaunchKernelGGL((attention_dq_kernel<2>), dim3((unsigned)grid), dim3(2 * NTHR), 0, s,
-                           a);
-    } else {
-        hipLaunchKernelGGL((attention_dkv_kernel<1>), dim3((unsigned)grid), dim3(NTHR), 0, s, a);
-        hipLaunchKernelGGL((attention_dq_kernel<1>), dim3((unsigned)grid), dim3(NTHR), 0, s, a);
+        hipLaunchKernelGGL((attention_dq_kernel<1, 2>), dim3((unsigned)grid), dim3(2 * NTHR), 0,
+                           s, a);
+        return hipGetLastError();
     }
+    hipLaunchKernelGGL((attention_dkv_kernel<1>), dim3((unsigned)grid), dim3(NTHR), 0, s, a);
+    // dQ in 128-row query tiles (two row blocks per wave) when they still give
+    // every CU two workgroups
+    AttnBwdArgs a2 = a;
+    a2.tiles = (int)((p.seq + 127) / 128);
+    const int64_t grid2 = (int64_t)a2.tiles * a.batch * a.heads;
+    if (grid2 >= kFwdWideGrid)
+        hipLaunchKernelGGL((attention_dq_kernel<2, 1>), dim3((unsigned)grid2), dim3(NTHR), 0, s,
+                           a2);
+    else
+        hipLaunchKernelGGL((attention_dq_kernel<1, 1>), dim3((unsigned)grid), dim3(NTHR), 0, s, a);
     return hipGetLastError();
 }
 
