@@ -3,12 +3,14 @@
 // epilogues, and the bias-gradient column sum (Sec. 4.2).
 //
 // The reduction is HBM-bound: per output element it streams nparts fp32
-// values in and one bf16/fp32 value out.  Each thread owns 8 consecutive
-// columns of one row: two 16-byte non-temporal loads per part, all parts
-// of a group of 8 issued before the first add so up to 16 loads are in
-// flight per thread; parts are then summed in group order 0..d-1, so the
-// result is bit-identical on every member of the group.  Rows of a chunk
-// are contiguous, so a launch is one linear sweep of [rows x ncols].
+// (or bf16: the 16-bit partials variant, Sec. 5) values in and one
+// bf16/fp32 value out.  Each thread owns 8 consecutive columns of one row:
+// two 16-byte non-temporal loads per fp32 part (one per bf16 part), all
+// parts of a group of 8 issued before the first add so up to 16 loads are
+// in flight per thread; parts are then summed in fp32 in group order
+// 0..d-1, so the result is bit-identical on every member of the group.
+// Rows of a chunk are contiguous, so a launch is one linear sweep of
+// [rows x ncols].
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
