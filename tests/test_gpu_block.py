@@ -300,3 +300,17 @@ def test_block_bwd_chunk_invariance(workspace):
             assert torch.equal(out[key], base[key]), (chunks, key)
         for i in range(4):
             assert torch.equal(out["dw"][i], base["dw"][i])
+
+
+@pytest.mark.parametrize("workspace", [False, True], ids=["direct", "workspace"])
+def test_block_without_tokens(workspace):
+    """No tokens: the forward has nothing to write; dW and db are sums over no
+    tokens, so they must come back as exact zeros (the buffers start as NaN)."""
+    print(f"block without tokens workspace={workspace}", flush=True)
+    inp = make_block_inputs("col", (2, 2), (1, 0), 0, 512, 0.02, seed=92, bwd=True)
+    run_block_fwd(inp, 2, workspace=workspace)
+    out = run_block_bwd(inp, 2, workspace=workspace)
+    torch.cuda.synchronize()
+    for i, n in enumerate(LIN):
+        assert torch.all(out["dw"][i] == 0), f"dw_{n}"
+        assert torch.all(out["db"][i] == 0), f"db_{n}"
