@@ -207,20 +207,23 @@ __device__ __forceinline__ void epilogue_store(const KArgs& a, int64_t m, int64_
 // ---------------------------------------------------------------------------
 namespace nt {
 
-constexpr int BM = 256, BK = 64;
+constexpr int BM = 256, BK = 64;              // BK: the K step of the layouts with
+                                              // row-contiguous operands
 constexpr int NW = 8, NT = NW * 64;           // two groups of four waves
 constexpr int MF = 16;
-constexpr int KS = BK / 32;                   // MFMA k-slices per step
 typedef short i16x8 __attribute__((ext_vector_type(8)));
 
 // Tile configurations.  Every one sums an output element's products in the
-// same order (K steps of 64, two 16x16x32 k-slices each), so they give the
-// same bits and may be mixed freely, e.g. across token chunks.
-template <int BN_, int WGM_, int WGN_, int STAGES_, int GROUP_>
+// same order (32-wide k-slices in ascending k, one 16x16x32 MFMA each, K
+// steps of 64 or 32 holding two or one of them), so they give the same bits
+// and may be mixed freely, e.g. across token chunks.
+template <int BN_, int WGM_, int WGN_, int STAGES_, int GROUP_, int BK_ = 64>
 struct Cfg {
     static constexpr int BN = BN_, WGM = WGM_, WGN = WGN_, STAGES = STAGES_, GROUP = GROUP_;
+    static constexpr int BK = BK_, KS = BK_ / 32;   // K step, MFMA k-slices per step
     static_assert(WGM * WGN == NW, "eight waves");
-    static_assert(STAGES == 2 || STAGES == 3, "two or three LDS stages");
+    static_assert(STAGES >= 2 && STAGES <= 4, "two to four LDS stages");
+    static_assert(BK == 64 || BK == 32, "K steps of 64 or 32");
     static constexpr int WM = BM / WGM, WN = BN / WGN;
     static constexpr int FM = WM / MF, FN = WN / MF;
     static_assert(FM * MF == WM && FN * MF == WN, "wave tile of whole MFMA tiles");
@@ -234,13 +237,25 @@ using Tile160 = Cfg<160, 4, 2, 3, 4>;
 // per FLOP, ~10% faster on the short-K (tokens) dW products, but 62.5% of
 // the tile count of 256 x 160 per launch
 using Tile256 = Cfg<256, 2, 4, 2, 8>;
+// 256 x 320 in K steps of 32: four stages (144 KB); waves of 128 x 80; 36 KB
+// copied per step for the 40 MFMAs each wave issues, against 52 KB for
+// 256 x 160 in steps of 64 (k-contiguous operands only)
+using Tile320 = Cfg<320, 2, 4, 4, 4, 32>;
 
-__device__ __forceinline__ int swz(int r) { return r & 6; }
+// Chunk swizzle of a k-contiguous LDS row.  Rows of 8 chunks (K step 64):
+// r & 6; rows of 4 chunks (K step 32, two rows per 128 bytes): (r >> 2) & 3.
+// Both give the 16 lanes of each ds_read_b128 service group distinct bank
+// quads under the measured lane grouping.
+template <int BK_>
+__device__ __forceinline__ int swz(int r) {
+    if constexpr (BK_ == 64) return r & 6;
+    else return (r >> 2) & 3;
+}
 
 // One operand tile: ROWS rows of a [rows][ld] matrix contiguous along k.
-template <int ROWS>
+template <int ROWS, int BK_>
 struct Copy {
-    static constexpr int CPR = BK / 8;             // 16-byte chunks per LDS row
+    static constexpr int CPR = BK_ / 8;            // 16-byte chunks per LDS row
     static constexpr int RPI = 64 / CPR;           // rows per copy instruction
     static constexpr int WI = ROWS / RPI;          // copy instructions per stage
     static constexpr int PER = (WI + NW - 1) / NW; // per wave (some waves one fewer)
@@ -259,7 +274,7 @@ struct Copy {
         const int64_t vr = left < 0 ? 0 : (left < ROWS ? left : ROWS);
         rs = rsrc_words(base + row0 * ld, vr * ld * 2);
         const int r = lane / CPR;
-        const int c = (lane % CPR) ^ swz(r);
+        const int c = (lane % CPR) ^ swz<BK_>(r);
         kc = c * 8;
         vlane = (uint32_t)((r * ld + c * 8) * 2);
         ins_stride = (uint32_t)(RPI * ld * 2);
@@ -270,7 +285,7 @@ struct Copy {
     }
     // Copy of the K step at k0 into LDS stage `dst` (k past K reads zeros).
     __device__ __forceinline__ void issue(uint16_t* dst, int64_t k0, int wave) const {
-        const bool tail = k0 + BK > K;
+        const bool tail = k0 + BK_ > K;
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
             const int ins = wave + NW * i;
@@ -283,10 +298,11 @@ struct Copy {
 };
 
 // 16x16x32 fragment: lane holds row r0 + lane%16, k = ks*32 + 8*(lane/16) + 0..7.
+template <int BK_>
 __device__ __forceinline__ bf16x8 frag(const uint16_t* src, int r0, int ks, int lane) {
     const int r = r0 + (lane & 15);
-    const int c = (ks * 4 + (lane >> 4)) ^ swz(r);
-    return *reinterpret_cast<const bf16x8*>(src + r * BK + c * 8);
+    const int c = (ks * 4 + (lane >> 4)) ^ swz<BK_>(r);
+    return *reinterpret_cast<const bf16x8*>(src + r * BK_ + c * 8);
 }
 
 // One operand tile stored [k][ROWS]: BK rows of a [K][ld] matrix that is
@@ -368,11 +384,11 @@ __device__ __forceinline__ bf16x8 frag_t(const uint16_t* src, int r0, int ks, in
 
 // Operand copy and fragment read for a tile contiguous along k (KC) or
 // along its rows.
-template <int ROWS, bool KC>
-using OpCopy = typename std::conditional<KC, Copy<ROWS>, CopyT<ROWS>>::type;
-template <int ROWS, bool KC>
+template <int ROWS, bool KC, int BK_>
+using OpCopy = typename std::conditional<KC, Copy<ROWS, BK_>, CopyT<ROWS>>::type;
+template <int ROWS, bool KC, int BK_>
 __device__ __forceinline__ bf16x8 op_frag(const uint16_t* src, int r0, int ks, int lane) {
-    if constexpr (KC) return frag(src, r0, ks, lane);
+    if constexpr (KC) return frag<BK_>(src, r0, ks, lane);
     else return frag_t<ROWS>(src, r0, ks, lane);
 }
 
@@ -389,7 +405,8 @@ __device__ __forceinline__ void barrier() {
 template <class C, bool A_K, bool B_K, int EPI, bool OUT_BF16>
 __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
     using namespace nt;
-    constexpr int BN = C::BN, WGN = C::WGN, STAGES = C::STAGES;
+    constexpr int BN = C::BN, WGN = C::WGN, STAGES = C::STAGES, BK = C::BK, KS = C::KS;
+    static_assert((A_K && B_K) || BK == nt::BK, "row-contiguous operands use K steps of 64");
     constexpr int WM = C::WM, WN = C::WN, FM = C::FM, FN = C::FN;
     constexpr int A_EL = C::A_EL, STAGE = C::STAGE;
     __shared__ __attribute__((aligned(1024))) uint16_t smem[STAGES * STAGE];
@@ -413,11 +430,11 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
     const int64_t kn = min(a.K - kb, a.ksplit);    // this split's contraction
 
     // split k offset: along a row (k-contiguous operand) or down the rows
-    OpCopy<BM, A_K> ca;
-    OpCopy<BN, B_K> cb;
+    OpCopy<BM, A_K, BK> ca;
+    OpCopy<BN, B_K, BK> cb;
     ca.init(a.A + (A_K ? kb : kb * a.lda), a.lda, m0, a.M, kn, wave, lane);
     cb.init(a.B + (B_K ? kb : kb * a.ldb), a.ldb, n0, a.N, kn, wave, lane);
-    constexpr int LA = OpCopy<BM, A_K>::PER, LB = OpCopy<BN, B_K>::PER;
+    constexpr int LA = OpCopy<BM, A_K, BK>::PER, LB = OpCopy<BN, B_K, BK>::PER;
     const int loads = ca.nmine + cb.nmine;   // copy instructions per step (wave-uniform)
 
     f32x4 acc[FM][FN];
@@ -432,18 +449,25 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
         ca.issue(dst, (int64_t)q * BK, wave);
         cb.issue(dst + A_EL, (int64_t)q * BK, wave);
     };
-    // wait until this wave's copies are complete except the newest step's
-    // (keep_one) or all of them; copies complete in issue order
-    auto wait_copies = [&](bool keep_one) {
-        if (!keep_one) { wait_vmcnt<0>(); return; }
-        if (loads == LA + LB) wait_vmcnt<LA + LB>();
-        else if (loads == LA + LB - 1) wait_vmcnt<LA + LB - 1>();
-        else wait_vmcnt<LA + LB - 2>();
+    // wait until this wave's copies are complete except those of the newest
+    // `keep` steps (0, 1, 2); copies complete in issue order
+    auto wait_copies = [&](int keep) {
+        if (keep <= 0) { wait_vmcnt<0>(); return; }
+        if (keep == 1) {
+            if (loads == LA + LB) wait_vmcnt<LA + LB>();
+            else if (loads == LA + LB - 1) wait_vmcnt<LA + LB - 1>();
+            else wait_vmcnt<LA + LB - 2>();
+            return;
+        }
+        if (loads == LA + LB) wait_vmcnt<2 * (LA + LB)>();
+        else if (loads == LA + LB - 1) wait_vmcnt<2 * (LA + LB - 1)>();
+        else wait_vmcnt<2 * (LA + LB - 2)>();
     };
 
     if (nk > 0) {   // (uniform) every wave runs the same number of barriers
         for (int q = 0; q < STAGES - 1 && q < nk; ++q) issue_step(q);
-        wait_copies(STAGES == 3 && nk > 1);
+        // step 0 landed; the later prologue steps may stay in flight
+        wait_copies(min(STAGES - 2, nk - 1));
         barrier();               // step 0 visible to every wave
         if (grpB) barrier();     // group B starts one phase late
 
@@ -454,16 +478,16 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
             const uint16_t* sa = smem + (p % STAGES) * STAGE;
             const uint16_t* sb = sa + A_EL;
             if (p + STAGES - 1 < nk) issue_step(p + STAGES - 1);
-            // with three stages the copy of step p+2 may stay in flight below
-            const bool more = STAGES == 3 && p + 2 < nk;
+            // the copies of steps p+2 .. p+STAGES-1 may stay in flight below
+            const int more = min(STAGES - 2, nk - 2 - p);
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
                 for (int i = 0; i < FM; ++i)
-                    fa[ks][i] = op_frag<BM, A_K>(sa, wm * WM + i * MF, ks, lane);
+                    fa[ks][i] = op_frag<BM, A_K, BK>(sa, wm * WM + i * MF, ks, lane);
 #pragma unroll
                 for (int j = 0; j < FN; ++j)
-                    fb[ks][j] = op_frag<BN, B_K>(sb, wn * WN + j * MF, ks, lane);
+                    fb[ks][j] = op_frag<BN, B_K, BK>(sb, wn * WN + j * MF, ks, lane);
             }
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
             // before group A's next memory phase this wave's copies of step
@@ -533,11 +557,24 @@ KArgs kargs(const GemmProblem& p, int bm, int bn) {
 // 256 x 256 tiles (30% fewer copied bytes per FLOP) for products whose last
 // wave of such tiles is at least 90% full (256 CUs): the dW products and the
 // QKV forward of the wide layer (1.10 -> 1.04 ms); 256 x 160 tiles otherwise
-bool nt_use_256(const GemmProblem& p) {
+// True when tiles of width bn fill their last wave of 256 concurrent tiles
+// to at least 90%.
+bool fills_waves(const GemmProblem& p, int64_t bn) {
     constexpr int64_t kCUs = 256;
-    const int64_t tiles = ((p.M + nt::BM - 1) / nt::BM) * ((p.N + 255) / 256);
+    const int64_t tiles = ((p.M + nt::BM - 1) / nt::BM) * ((p.N + bn - 1) / bn);
     const int64_t waves = (tiles + kCUs - 1) / kCUs;
     return tiles * 10 >= waves * kCUs * 9;
+}
+
+bool nt_use_256(const GemmProblem& p) { return fills_waves(p, 256); }
+
+// 256 x 320 tiles (K steps of 32) for k-contiguous operands, unsplit, when
+// 256 x 256 tiles would leave their last wave short and 320-wide ones do not
+// (measured: 4096 x 10240 x 20480 at 1289 TFLOP/s against 1208 for
+// 256 x 160; where 256 x 256 tiles fill their waves they are faster)
+bool nt_use_320(const GemmProblem& p) {
+    return p.layout == LAYOUT_NT && p.splits <= 1 && !fills_waves(p, 256) &&
+           fills_waves(p, 320);
 }
 
 // Split-K plan of an NT product written to fp32: the S in 1..kMaxSplits
@@ -589,6 +626,9 @@ hipError_t launch_pp_cfg(const GemmProblem& p, hipStream_t s) {
 template <bool A_K, bool B_K, int EPI, bool OUT_BF16>
 hipError_t launch_pp(const GemmProblem& p, hipStream_t s) {
     if (p.splits > 1) return launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
+    if constexpr (A_K && B_K) {
+        if (nt_use_320(p)) return launch_pp_cfg<nt::Tile320, A_K, B_K, EPI, OUT_BF16>(p, s);
+    }
     return nt_use_256(p) ? launch_pp_cfg<nt::Tile256, A_K, B_K, EPI, OUT_BF16>(p, s)
                          : launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
 }
@@ -615,6 +655,7 @@ const char* gemm_kernel_name(const GemmProblem& p) {
                                             {"gemm_tn", "gemm_tn256", "gemm_tn_splitk"}};
     const int l = p.layout == LAYOUT_NN ? 0 : p.layout == LAYOUT_NT ? 1 : p.layout == LAYOUT_TN ? 2 : -1;
     if (l < 0) return "gemm_?";
+    if (nt_use_320(p)) return "gemm_nt320";
     return names[l][p.splits > 1 ? 2 : nt_use_256(p) ? 1 : 0];
 }
 
