@@ -69,11 +69,52 @@ __global__ __launch_bounds__(THREADS) void transpose_kernel(const uint16_t* __re
     }
 }
 
+// Shapes whose rows and columns are multiples of 8 (every operand the block
+// transposes): no LDS.  A lane moves one 8 x 8 block: eight 16-byte loads
+// (source rows r..r+7, columns c..c+7), a register transpose (one byte
+// permute per output word), eight 16-byte stores (destination rows c..c+7).
+// A wave holds 8 row blocks x 8 column blocks (lane = 8 cb + rb), so every
+// load and every store instruction covers 8 rows x 128 contiguous bytes.
+// A workgroup of four waves spans 64 source rows x 256 source columns.
+__global__ __launch_bounds__(THREADS) void transpose8_kernel(const uint16_t* __restrict__ src,
+                                                             int64_t lds, int64_t rows,
+                                                             int64_t cols,
+                                                             uint16_t* __restrict__ dst,
+                                                             int64_t ldd, int tiles_c) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t r0 = (int64_t)(blockIdx.x / tiles_c) * 64;
+    const int64_t c0 = (int64_t)(blockIdx.x % tiles_c) * 256 + wave * 64;
+    const int64_t r = r0 + 8 * (lane & 7), c = c0 + 8 * (lane >> 3);
+    if (r >= rows || c >= cols) return;
+    u32x4 in[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) in[i] = *reinterpret_cast<const u32x4*>(src + (r + i) * lds + c);
+    // out row j (source column c + j), word k = (in[2k] element j, in[2k+1] element j):
+    // element j of a row sits in word j / 2, low half for even j
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+        u32x4 o;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            o[k] = __builtin_amdgcn_perm(in[2 * k + 1][j >> 1], in[2 * k][j >> 1], sel);
+        *reinterpret_cast<u32x4*>(dst + (c + j) * ldd + r) = o;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_transpose(const void* src, int64_t lds, int64_t rows, int64_t cols, void* dst,
                             int64_t ldd, hipStream_t s) {
     if (rows <= 0 || cols <= 0) return hipSuccess;
+    if (rows % 8 == 0 && cols % 8 == 0 && lds % 8 == 0 && ldd % 8 == 0) {
+        const int64_t tr = (rows + 63) / 64, tc = (cols + 255) / 256;
+        if (tr * tc > 0x7fffffff) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(transpose8_kernel, dim3((unsigned)(tr * tc)), dim3(THREADS), 0, s,
+                           static_cast<const uint16_t*>(src), lds, rows, cols,
+                           static_cast<uint16_t*>(dst), ldd, (int)tc);
+        return hipGetLastError();
+    }
     const int64_t tr = (rows + TILE - 1) / TILE, tc = (cols + TILE - 1) / TILE;
     if (tr * tc > 0x7fffffff) return hipErrorInvalidValue;
     hipLaunchKernelGGL(transpose_kernel, dim3((unsigned)(tr * tc)), dim3(THREADS), 0, s,

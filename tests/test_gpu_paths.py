@@ -50,7 +50,9 @@ def assert_paths_agree(a, b, what, rel=1e-4):
 
 @pytest.mark.parametrize("rows,cols,pad_s,pad_d", [
     (1, 8, 0, 0), (7, 16, 8, 0), (64, 64, 0, 8), (65, 72, 0, 0), (300, 200, 16, 24),
-    (513, 1032, 8, 8), (4096, 2560, 0, 0), (2, 4104, 0, 8)])
+    (513, 1032, 8, 8), (4096, 2560, 0, 0), (2, 4104, 0, 8),
+    # multiples of 8 (the register-block kernel), with partial 64 x 256 tiles
+    (8, 8, 0, 0), (72, 264, 8, 8), (4104, 520, 0, 8), (136, 2056, 16, 0)])
 def test_transpose_matches_torch(rows, cols, pad_s, pad_d):
     print(f"transpose {rows}x{cols} pads {pad_s},{pad_d}", flush=True)
     src_full = S.randint_bf16((rows, cols + pad_s), 7, 901).to(DEV)
