@@ -964,9 +964,15 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         for (int c = 0; c < chunks; ++c) ATP_CHECK(chunk(L, c));
         return ATP_OK;
     };
-    // out-proj first (its reductions start at once), then fc1, QKV, and fc2
-    // behind fc1's output
-    const int order[4] = {1, 2, 0, 3};
+    // out-proj first (its reductions start at once), then fc1; of QKV and fc2
+    // (behind fc1's output) the one with fewer reduced bytes goes last, so
+    // the other's last reductions run beside its GEMMs instead of after them
+    auto red_bytes = [&](int L) {
+        const atp_shard& g = P.g[L];
+        return g.red_size > 1 ? (double)g.red_size * (double)g.n_loc : 0.0;
+    };
+    const bool qkv_last = red_bytes(0) <= red_bytes(3);
+    const int order[4] = {1, 2, qkv_last ? 3 : 0, qkv_last ? 0 : 3};
     for (int L : order) ATP_CHECK(linear(L));
     return S.end(ev[1]);
 }
