@@ -258,7 +258,9 @@ typedef struct {
  * shards, n_loc rows of k_loc + 64 bf16 values each) and the backward's (X^T
  * of x, the attention block and H, and dY^T of the four linears, cols rows
  * of tokens + 64 bf16 values each; the 64 values pad the row pitch off
- * memory-channel-aligned strides), each plus the fp32 split-K slabs of the
+ * memory-channel-aligned strides; the backward also holds the fp32 column
+ * partials of dY that the transposes leave for db, ceil(tokens / 64) rows of
+ * the widest linear's columns), each plus the fp32 split-K slabs of the
  * chunked products that feed a reduction (S * chunk rows * cols * 4 bytes
  * for the largest split plan S over every valid chunk count), every piece
  * rounded up to 256 bytes.

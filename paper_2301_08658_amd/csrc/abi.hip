@@ -359,10 +359,18 @@ size_t ws_fwd_bytes(const BlockPlan& P, int64_t tokens) {
     return b;
 }
 
+// fp32 column partials of dY, one row per 64 tokens, for the widest linear
+size_t colpart_bytes(const BlockPlan& P, int64_t tokens) {
+    int64_t n = 0;
+    for (int L = 0; L < 4; ++L) n = std::max(n, P.g[L].n_loc);
+    return (size_t)((tokens + 63) / 64) * (size_t)n * 4;
+}
+
 size_t ws_bwd_bytes(const BlockPlan& P, int64_t tokens) {
     const size_t t2 = (size_t)ws_pitch(tokens) * 2;
     size_t b = ws_round(P.g[0].k_loc * t2) + ws_round(P.g[1].k_loc * t2) +
-               ws_round(P.g[3].k_loc * t2) + ws_round(slab_bytes(P, tokens, true));
+               ws_round(P.g[3].k_loc * t2) + ws_round(slab_bytes(P, tokens, true)) +
+               ws_round(colpart_bytes(P, tokens));
     for (int L = 0; L < 4; ++L) b += ws_round(P.g[L].n_loc * t2);
     return b;
 }
@@ -395,9 +403,17 @@ struct Carver {
 };
 
 atp_status run_transpose(const void* src, int64_t lds, int64_t rows, int64_t cols, void* dst,
-                         int64_t ldd, hipStream_t s) {
-    return timed("transpose", 0.0, 4.0 * (double)rows * (double)cols, s,
-                 [&] { return atp::launch_transpose(src, lds, rows, cols, dst, ldd, s); });
+                         int64_t ldd, hipStream_t s, float* part = nullptr, int64_t ldpart = 0) {
+    return timed("transpose", 0.0, 4.0 * (double)rows * (double)cols, s, [&] {
+        return atp::launch_transpose(src, lds, rows, cols, dst, ldd, s, part, ldpart);
+    });
+}
+
+// db from the 64-row-block column partials a transpose wrote
+atp_status run_colsum_finish(const float* part, int64_t ldp, int64_t nb, int64_t N, float* db,
+                             hipStream_t s) {
+    return timed("colsum", (double)nb * N, 4.0 * (nb + 1) * (double)N, s,
+                 [&] { return atp::launch_colsum_finish(part, ldp, nb, N, db, s); });
 }
 
 atp_status check_group(float* const* tab, int32_t size, int64_t rows, int64_t ld, int64_t cols,
@@ -1043,6 +1059,7 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     uint16_t* dyt[4] = {nullptr, nullptr, nullptr, nullptr};
     bool xt_done[3] = {false, false, false};
     float* slab = nullptr;
+    float* colpart = nullptr;   // db of the workspace path: dY^T's transpose writes partials
     if (ws) {
         Carver c{static_cast<char*>(workspace)};
         const size_t t2 = (size_t)ws_pitch(tokens) * 2;
@@ -1051,6 +1068,7 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         xt[2] = c.take(P.g[3].k_loc * t2);
         for (int L = 0; L < 4; ++L) dyt[L] = c.take(P.g[L].n_loc * t2);
         slab = reinterpret_cast<float*>(c.take(slab_bytes(P, tokens, true)));
+        colpart = reinterpret_cast<float*>(c.take(colpart_bytes(P, tokens)));
     }
 
     const int64_t mc = tokens / chunks;
@@ -1125,7 +1143,7 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         const int lane = S.take(gemm_flops(g.k_loc, g.n_loc, tokens));
         hipStream_t s = S.lane(lane);
         if (L == 2) ATP_CHECK(wait_dpre(lane, chunks - 1));
-        if (io->db[L]) ATP_CHECK(run_colsum(dY[L], ld_dy[L], tokens, g.n_loc, io->db[L], s));
+        if (io->db[L] && !ws) ATP_CHECK(run_colsum(dY[L], ld_dy[L], tokens, g.n_loc, io->db[L], s));
         if (!ws) {
             atp::GemmProblem p = gemm_problem(atp::LAYOUT_TN, Xin[L], ldx_in[L], dY[L], ld_dy[L],
                                               io->dw[L], w->ldw[L], false, atp::EPI_NONE,
@@ -1140,7 +1158,11 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
             ATP_CHECK(run_transpose(Xin[L], ldx_in[L], tokens, g.k_loc, xt[xi], tp, s));
             xt_done[xi] = true;
         }
-        ATP_CHECK(run_transpose(dY[L], ld_dy[L], tokens, g.n_loc, dyt[L], tp, s));
+        // dY^T, and with it the column partials of dY for db (one read of dY)
+        float* part = io->db[L] ? colpart : nullptr;
+        ATP_CHECK(run_transpose(dY[L], ld_dy[L], tokens, g.n_loc, dyt[L], tp, s, part, g.n_loc));
+        if (part)
+            ATP_CHECK(run_colsum_finish(part, g.n_loc, (tokens + 63) / 64, g.n_loc, io->db[L], s));
         atp::GemmProblem p = gemm_problem(atp::LAYOUT_NT, xt[xi], tp, dyt[L], tp, io->dw[L],
                                           w->ldw[L], false, atp::EPI_NONE, g.k_loc, g.n_loc,
                                           tokens);

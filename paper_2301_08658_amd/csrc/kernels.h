@@ -109,12 +109,21 @@ struct AttentionBwdProblem {
 };
 hipError_t launch_attention_bwd(const AttentionBwdProblem& p, hipStream_t s);
 
-// db[n] = sum_t dy[t*ld + n], dy bf16 [T, N], db f32 [N]; fixed summation order.
+// db[n] = sum_t dy[t*ld + n], dy bf16 [T, N], db f32 [N], in one fixed order:
+// 8-row groups, then the groups of each 64-row block, then the blocks, all
+// ascending (the same bits as transpose partials + launch_colsum_finish).
 hipError_t launch_colsum(const void* dy, int64_t ld, int64_t T, int64_t N, float* db,
                          hipStream_t s);
+// db[n] = sum over b < nb, ascending, of part[b*ldp + n] (fp32).
+hipError_t launch_colsum_finish(const float* part, int64_t ldp, int64_t nb, int64_t N, float* db,
+                                hipStream_t s);
 
-// dst[c*ldd + r] = src[r*lds + c] for r < rows, c < cols (bf16).
+// dst[c*ldd + r] = src[r*lds + c] for r < rows, c < cols (bf16).  With
+// part (rows, cols, lds, ldd multiples of 8): also the column sums of every
+// 64-row block of src in launch_colsum's order, part[(r / 64)*ldpart + c]
+// (fp32), for launch_colsum_finish.
 hipError_t launch_transpose(const void* src, int64_t lds, int64_t rows, int64_t cols, void* dst,
-                            int64_t ldd, hipStream_t s);
+                            int64_t ldd, hipStream_t s, float* part = nullptr,
+                            int64_t ldpart = 0);
 
 }  // namespace atp

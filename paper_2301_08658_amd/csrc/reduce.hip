@@ -138,15 +138,19 @@ hipError_t launch_r(const ReduceProblem& p, hipStream_t s) {
     return hipGetLastError();
 }
 
-// Column sums: a block owns 64 columns (128 bytes of every row): 8 column
-// lanes x 128 row lanes, each thread 8 columns (one 16-byte load per row)
-// over rows t = ty, ty + 128, ... in ascending order; the 128 row-lane sums
-// of a column are then added in ascending order.  Sixteen waves per block
-// keep enough loads in flight with few blocks (N / 64); blocks are
-// renumbered so neighbouring column groups run on the same XCD.
+// Column sums in one fixed order, the same on every path (so db has the
+// same bits whether or not it is formed during dY's transpose):
+//   db[c] = (((0 + S_0) + S_1) + ...),  S_b over the 64-row block b,
+//   S_b = (((0 + G_b0) + G_b1) + ...)   over its 8-row groups inside [0, T),
+//   G_bg = (((0 + x_r) + x_r+1) + ...)  over the group's rows inside [0, T).
+// A block owns 64 columns: 8 column lanes (8 columns, one 16-byte load per
+// row) x 128 row lanes; row lane ty forms S_b for b = ty, ty + 128, ... one
+// round of 128 blocks at a time, and 64 threads fold each round's S_b into
+// their column's sum in ascending b.  Blocks are renumbered so neighbouring
+// column groups run on the same XCD.
 constexpr int CS_CL = 8;                 // column lanes
 constexpr int CS_COLS = CS_CL * 8;       // columns per block
-constexpr int CS_ROWL = 128;             // row lanes
+constexpr int CS_ROWL = 128;             // row lanes (row blocks per round)
 constexpr int CS_T = CS_CL * CS_ROWL;    // threads per block
 
 __global__ __launch_bounds__(CS_T) void colsum_kernel(const uint16_t* __restrict__ dy, int64_t ld,
@@ -158,29 +162,57 @@ __global__ __launch_bounds__(CS_T) void colsum_kernel(const uint16_t* __restrict
     const int per = G / 8, rem = G % 8;
     const int64_t blk = (xcd < rem) ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
     const int64_t c = blk * CS_COLS + tx * 8;
-    float s[8];
+    const int64_t nb = (T + 63) / 64;
+    float acc = 0.0f;                      // column blk * 64 + threadIdx.x (first 64 threads)
+    for (int64_t b0 = 0; b0 < nb; b0 += CS_ROWL) {
+        const int64_t b = b0 + ty;
+        float sb[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) s[e] = 0.0f;
-    if (c < N) {
-#pragma unroll 4
-        for (int64_t t = ty; t < T; t += CS_ROWL) {
-            float f[8];
-            unpack8(*reinterpret_cast<const u32x4*>(dy + t * ld + c), f);
+        for (int e = 0; e < 8; ++e) sb[e] = 0.0f;
+        if (c < N && b < nb) {
+            for (int g = 0; g < 8; ++g) {
+                const int64_t r0 = b * 64 + g * 8;
+                if (r0 >= T) break;
+                float gs[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) s[e] += f[e];
+                for (int e = 0; e < 8; ++e) gs[e] = 0.0f;
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    if (r0 + i < T) {
+                        float f[8];
+                        unpack8(*reinterpret_cast<const u32x4*>(dy + (r0 + i) * ld + c), f);
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) gs[e] += f[e];
+                    }
+                }
+#pragma unroll
+                for (int e = 0; e < 8; ++e) sb[e] += gs[e];
+            }
         }
-    }
 #pragma unroll
-    for (int e = 0; e < 8; ++e) part[ty][tx * 8 + e] = s[e];
-    __syncthreads();
+        for (int e = 0; e < 8; ++e) part[ty][tx * 8 + e] = sb[e];
+        __syncthreads();
+        if (threadIdx.x < CS_COLS) {
+            const int64_t nr = nb - b0 < CS_ROWL ? nb - b0 : CS_ROWL;
+            for (int r = 0; r < nr; ++r) acc += part[r][threadIdx.x];
+        }
+        __syncthreads();
+    }
     if (threadIdx.x < CS_COLS) {
         const int64_t col = blk * CS_COLS + threadIdx.x;
-        if (col < N) {
-            float acc = part[0][threadIdx.x];
-            for (int r = 1; r < CS_ROWL; ++r) acc += part[r][threadIdx.x];
-            db[col] = acc;
-        }
+        if (col < N) db[col] = acc;
     }
+}
+
+// db[c] = (((0 + part_0[c]) + part_1[c]) + ...) over nb row-block partials.
+__global__ __launch_bounds__(256) void colsum_finish_kernel(const float* __restrict__ part,
+                                                            int64_t ldp, int64_t nb, int64_t N,
+                                                            float* __restrict__ db) {
+    const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (c >= N) return;
+    float acc = 0.0f;
+    for (int64_t b = 0; b < nb; ++b) acc += part[b * ldp + c];
+    db[c] = acc;
 }
 
 template <bool PART_BF16>
@@ -226,6 +258,14 @@ hipError_t launch_split_sum(const float* ws, int S, int64_t stride, int64_t ld, 
     p.ldo = ldo;
     p.out_bf16 = false;
     return launch_reduce(p, s);
+}
+
+hipError_t launch_colsum_finish(const float* part, int64_t ldp, int64_t nb, int64_t N, float* db,
+                                hipStream_t s) {
+    if (N <= 0) return hipSuccess;
+    hipLaunchKernelGGL(colsum_finish_kernel, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, s,
+                       part, ldp, nb, N, db);
+    return hipGetLastError();
 }
 
 hipError_t launch_colsum(const void* dy, int64_t ld, int64_t T, int64_t N, float* db,

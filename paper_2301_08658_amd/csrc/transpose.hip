@@ -21,6 +21,7 @@ constexpr int PAD = 8;                 // LDS row pitch 72 elements (144 B)
 constexpr int THREADS = 256;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __global__ __launch_bounds__(THREADS) void transpose_kernel(const uint16_t* __restrict__ src,
                                                             int64_t lds, int64_t rows,
@@ -76,16 +77,56 @@ __global__ __launch_bounds__(THREADS) void transpose_kernel(const uint16_t* __re
 // A wave holds 8 row blocks x 8 column blocks (lane = 8 cb + rb), so every
 // load and every store instruction covers 8 rows x 128 contiguous bytes.
 // A workgroup of four waves spans 64 source rows x 256 source columns.
+//
+// With part, the lanes also form the column sums of the 64-row block in the
+// column-sum order (8-row group of each lane, then the groups in ascending
+// row order through LDS) and write them to part[(r0 / 64) * ldpart + c].
 __global__ __launch_bounds__(THREADS) void transpose8_kernel(const uint16_t* __restrict__ src,
                                                              int64_t lds, int64_t rows,
                                                              int64_t cols,
                                                              uint16_t* __restrict__ dst,
-                                                             int64_t ldd, int tiles_c) {
+                                                             int64_t ldd, int tiles_c,
+                                                             float* __restrict__ part,
+                                                             int64_t ldpart) {
+    __shared__ float gsum[4][8][64 + 1];   // [wave][row group][column of the wave]
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int rb = lane & 7, cb = lane >> 3;
     const int64_t r0 = (int64_t)(blockIdx.x / tiles_c) * 64;
     const int64_t c0 = (int64_t)(blockIdx.x % tiles_c) * 256 + wave * 64;
-    const int64_t r = r0 + 8 * (lane & 7), c = c0 + 8 * (lane >> 3);
-    if (r >= rows || c >= cols) return;
+    const int64_t r = r0 + 8 * rb, c = c0 + 8 * cb;
+    const bool live = r < rows && c < cols;
+    if (part) {
+        float gs[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) gs[e] = 0.0f;
+        if (live) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const u32x4 w = *reinterpret_cast<const u32x4*>(src + (r + i) * lds + c);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    gs[2 * k] += __uint_as_float(w[k] << 16);
+                    gs[2 * k + 1] += __uint_as_float(w[k] & 0xffff0000u);
+                }
+            }
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) gsum[wave][rb][8 * cb + e] = gs[e];
+        __syncthreads();
+        if (rb == 0 && c < cols) {
+            const int ng = (int)((rows - r0 + 7) / 8 < 8 ? (rows - r0 + 7) / 8 : 8);
+            float sb[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) sb[e] = 0.0f;
+            for (int g = 0; g < ng; ++g)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) sb[e] += gsum[wave][g][8 * cb + e];
+            float* pp = part + (r0 / 64) * ldpart + c;
+            *reinterpret_cast<f32x4*>(pp) = f32x4{sb[0], sb[1], sb[2], sb[3]};
+            *reinterpret_cast<f32x4*>(pp + 4) = f32x4{sb[4], sb[5], sb[6], sb[7]};
+        }
+    }
+    if (!live || !dst) return;
     u32x4 in[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) in[i] = *reinterpret_cast<const u32x4*>(src + (r + i) * lds + c);
@@ -105,14 +146,16 @@ __global__ __launch_bounds__(THREADS) void transpose8_kernel(const uint16_t* __r
 }  // namespace
 
 hipError_t launch_transpose(const void* src, int64_t lds, int64_t rows, int64_t cols, void* dst,
-                            int64_t ldd, hipStream_t s) {
+                            int64_t ldd, hipStream_t s, float* part, int64_t ldpart) {
     if (rows <= 0 || cols <= 0) return hipSuccess;
-    if (rows % 8 == 0 && cols % 8 == 0 && lds % 8 == 0 && ldd % 8 == 0) {
+    const bool by8 = rows % 8 == 0 && cols % 8 == 0 && lds % 8 == 0 && ldd % 8 == 0;
+    if (part && (!by8 || ldpart < cols || ldpart % 4)) return hipErrorInvalidValue;
+    if (by8) {
         const int64_t tr = (rows + 63) / 64, tc = (cols + 255) / 256;
         if (tr * tc > 0x7fffffff) return hipErrorInvalidValue;
         hipLaunchKernelGGL(transpose8_kernel, dim3((unsigned)(tr * tc)), dim3(THREADS), 0, s,
                            static_cast<const uint16_t*>(src), lds, rows, cols,
-                           static_cast<uint16_t*>(dst), ldd, (int)tc);
+                           static_cast<uint16_t*>(dst), ldd, (int)tc, part, ldpart);
         return hipGetLastError();
     }
     const int64_t tr = (rows + TILE - 1) / TILE, tc = (cols + TILE - 1) / TILE;

@@ -260,8 +260,9 @@ def test_block_workspace_bytes_formula():
         G = B.block_geometry(m, mode, h)
         fwd = sum(r((g.k_loc + 64) * g.n_loc * 2) for g in G)
         tp = T + 64
+        colpart = ((T + 63) // 64) * max(g.n_loc for g in G) * 4   # fp32 column partials for db
         bwd = (r(G[0].k_loc * tp * 2) + r(G[1].k_loc * tp * 2) + r(G[3].k_loc * tp * 2) +
-               sum(r(g.n_loc * tp * 2) for g in G))
+               sum(r(g.n_loc * tp * 2) for g in G) + r(colpart))
         sizes = {B.atp_block_workspace_bytes(m, mode, T, h, c) for c in (1, 2, 4)}
         assert len(sizes) == 1, sizes          # the chunk count does not change it
         ws = sizes.pop()
