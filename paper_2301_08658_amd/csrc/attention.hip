@@ -50,7 +50,6 @@ constexpr int BM = 64;          // query rows per workgroup
 constexpr int BN = 64;          // keys per step
 constexpr int NWAVE = 4;
 constexpr int NTHR = NWAVE * 64;
-constexpr int CH = D / 8;       // 16-byte chunks per row
 constexpr int64_t kFwdWideGrid = 512;   // two workgroups per CU on 256 CUs
 constexpr int64_t kBwdSplitGrid = 1024;  // 64-row tiles below which loops are split
 
