@@ -33,6 +33,8 @@ __device__ __forceinline__ u32x4 rsrc_words(const void* base, int64_t bytes) {
 // value of its own after this statement.  The kernels calling this keep
 // nothing in M0 (no LDS-DMA builtins, no indexed register moves, every loop
 // over registers unrolled); a kernel that needs M0 itself must not use it.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"   // the M0 clobber, see above
 __device__ __forceinline__ void lds_dma16(const u32x4& rs, const uint16_t* lds_dst, uint32_t voff,
                                           uint32_t soff) {
     typedef __attribute__((address_space(3))) const void* lds_cptr;
@@ -40,6 +42,7 @@ __device__ __forceinline__ void lds_dma16(const u32x4& rs, const uint16_t* lds_d
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
                  :: "s"(m), "v"(voff), "s"(rs), "s"(soff) : "memory", "m0");
 }
+#pragma clang diagnostic pop
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
