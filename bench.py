@@ -65,13 +65,21 @@ def parse():
                     help="time one reduced linear of the block (fc2: the largest reduction) "
                          "as the chunked pipeline with f32 and with bf16 partials, serialized, "
                          "unchunked, and with the reduction fused into the GEMM epilogue")
+    ap.add_argument("--weight-layout", choices=("kn", "nk"), default="kn",
+                    help="local weights stored [k, n] (the paper's Y = XW) or [n, k] "
+                         "(torch.nn.Linear's order)")
+    ap.add_argument("--partials", choices=("f32", "bf16"), default="f32",
+                    help="Partial(SUM) buffers in fp32 or bf16 (Sec. 5's 16-bit all-reduce)")
+    ap.add_argument("--comm-cus", type=int, default=0,
+                    help="run the reductions on a comm stream restricted to this many CUs "
+                         "(hipExtStreamCreateWithCUMask; 0 = all CUs)")
     ap.add_argument("--seed", type=int, default=21)
     ap.add_argument("--profile-detail", action="store_true",
                     help="also print per-shape kernel timings to stderr")
     return ap.parse_args()
 
 
-def setup(torch, atp, S, wl, chunks, seed):
+def setup(torch, atp, S, wl, chunks, seed, layout="kn", partials="f32"):
     """Device-resident seeded inputs and outputs of one device's share."""
     dev = "cuda:0"
     d1, d2 = wl["mesh"]
@@ -81,24 +89,29 @@ def setup(torch, atp, S, wl, chunks, seed):
     G = atp.block_geometry(m, bm, h)
     rnd = lambda shape, std, tid, dt=torch.bfloat16: S.randn_device(  # noqa: E731
         shape, std, seed, tid, dev, dtype=dt)
-    st = dict(m=m, bm=bm, G=G, T=T, h=h, chunks=chunks)
+    kn = layout == "kn"
+    pdt = torch.float32 if partials == "f32" else torch.bfloat16
+    st = dict(m=m, bm=bm, G=G, T=T, h=h, chunks=chunks,
+              layout=atp.ATP_W_KN if kn else atp.ATP_W_NK)
     st["x"] = rnd((T, G[0].k_loc), 1.0, S.TID["x"])
     st["a"] = rnd((T, G[1].k_loc), 1.0, S.TID["a"])
     st["w"] = [rnd((g.k_loc, g.n_loc), sw, S.TID["w_" + n]) for g, n in zip(G, LIN)]
+    if not kn:
+        st["w"] = [w.t().contiguous() for w in st["w"]]
     st["b"] = [torch.zeros(g.n_loc, dtype=torch.bfloat16, device=dev) for g in G]
     emp = lambda r, c, dt=torch.bfloat16: torch.empty((r, c), dtype=dt, device=dev)  # noqa
     st["fwd_tabs"], st["bwd_tabs"] = [], []
     for i, g in enumerate(G):
         if g.red_size > 1:
             sp = S.peer_sigma(g.k_loc, sw, 1.0)
-            tab = [rnd((T, g.n_loc), sp, S.PEER_TID_BASE + 100 * i + j, torch.float32)
+            tab = [rnd((T, g.n_loc), sp, S.PEER_TID_BASE + 100 * i + j, torch.float32).to(pdt)
                    for j in range(g.red_size)]
             st["fwd_tabs"].append(tab)        # entry red_index is overwritten (own)
         else:
             st["fwd_tabs"].append(None)
         if g.bwd_size > 1:
             sp = S.peer_sigma(g.n_loc, sw, 1.0)
-            tab = [rnd((T, g.k_loc), sp, S.BWD_PEER_TID_BASE + 100 * i + j, torch.float32)
+            tab = [rnd((T, g.k_loc), sp, S.BWD_PEER_TID_BASE + 100 * i + j, torch.float32).to(pdt)
                    for j in range(g.bwd_size)]
             st["bwd_tabs"].append(tab)
         else:
@@ -111,7 +124,8 @@ def setup(torch, atp, S, wl, chunks, seed):
     st["dh_pre"] = emp(T, G[2].n_loc)
     st["dx_qkv"], st["dx_fc1"] = emp(T, G[0].k_loc), emp(T, G[2].k_loc)
     st["d_attn"] = emp(T, G[1].k_loc)
-    st["dw"] = [torch.empty((g.k_loc, g.n_loc), dtype=torch.float32, device=dev) for g in G]
+    st["dw"] = [torch.empty((g.k_loc, g.n_loc) if kn else (g.n_loc, g.k_loc),
+                            dtype=torch.float32, device=dev) for g in G]
     st["db"] = [torch.empty((g.n_loc,), dtype=torch.float32, device=dev) for g in G]
     return st
 
@@ -286,8 +300,8 @@ def step_flops(st, fwd_only):
     return f if fwd_only else 3.0 * f
 
 
-def make_step(torch, atp, st, fwd_only, serial):
-    ms = None if serial else torch.cuda.Stream()
+def make_step(torch, atp, st, fwd_only, serial, comm=None):
+    ms = None if serial else (comm if comm is not None else torch.cuda.Stream())
 
     def step():
         # the stream current at call time (the capture stream inside a graph)
@@ -296,15 +310,35 @@ def make_step(torch, atp, st, fwd_only, serial):
         atp.atp_block_fwd(st["m"], st["bm"], st["T"], st["h"], st["chunks"], st["w"], st["b"],
                           st["x"], st["a"], st["fwd_tabs"], st["qkv"], st["o"], st["hh"],
                           st["pre"], st["z"], workspace=st["ws"], compute_stream=cs,
-                          comm_stream=ms_)
+                          comm_stream=ms_, weight_layout=st["layout"])
         if fwd_only:
             return
         atp.atp_block_bwd(st["m"], st["bm"], st["T"], st["h"], st["chunks"], st["w"], st["b"],
                           st["x"], st["a"], st["hh"], st["pre"], st["dz"], st["dqkv"], st["do"],
                           st["bwd_tabs"], st["dh_pre"], st["dx_qkv"], st["dx_fc1"],
                           st["d_attn"], st["dw"], st["db"], workspace=st["ws"], compute_stream=cs,
-                          comm_stream=ms_)
+                          comm_stream=ms_, weight_layout=st["layout"])
     return step
+
+
+def cu_masked_stream(torch, n_cus, total=256):
+    """A stream whose kernels may only use `n_cus` of the chip's CUs, spread
+    evenly over the CU index range (hipExtStreamCreateWithCUMask), wrapped
+    for torch.  The stream lives until the process ends."""
+    import ctypes
+    if not 0 < n_cus <= total:
+        raise SystemExit(f"bench.py: --comm-cus must be in 1..{total}")
+    hip = ctypes.CDLL("libamdhip64.so")
+    words = (ctypes.c_uint32 * (total // 32))()
+    for k in range(n_cus):
+        cu = (k * total) // n_cus
+        words[cu // 32] |= 1 << (cu % 32)
+    handle = ctypes.c_void_p()
+    rc = hip.hipExtStreamCreateWithCUMask(ctypes.byref(handle), ctypes.c_uint32(total // 32),
+                                          words)
+    if rc != 0:
+        raise RuntimeError(f"hipExtStreamCreateWithCUMask failed ({rc})")
+    return torch.cuda.ExternalStream(handle.value)
 
 
 def capture(torch, step):
@@ -366,13 +400,12 @@ def cpu_baseline(st, rows_n, fwd_only, seed):
     qkv, _ = red(0, O.matmul(x, W[0]), ftab[0], G[0].red_index, O.EPI_BIAS, bias[0])
     o, _ = red(1, O.matmul(a, W[1]), ftab[1], G[1].red_index, O.EPI_BIAS, bias[1])
     hh, pre = red(2, O.matmul(x, W[2]), ftab[2], G[2].red_index, O.EPI_BIAS_GELU, bias[2])
-    z, _ = red(3, O.matmul(O.round_bf16(hh), W[3]), ftab[3], G[3].red_index, O.EPI_BIAS,
-               bias[3])
+    z, _ = red(3, O.matmul(hh, W[3]), ftab[3], G[3].red_index, O.EPI_BIAS, bias[3])
     flops += sum(2.0 * rows_n * g.k_loc * g.n_loc for g in G)
     if not fwd_only:
         # input gradients, sampled rows
         dh, _ = red(3, O.matmul(dz, Wt[3]), btab[3], G[3].bwd_index, O.EPI_GELU_BWD, None, pre)
-        red(2, O.matmul(O.round_bf16(dh), Wt[2]), btab[2], G[2].bwd_index, O.EPI_NONE)
+        red(2, O.matmul(dh, Wt[2]), btab[2], G[2].bwd_index, O.EPI_NONE)
         red(1, O.matmul(do, Wt[1]), btab[1], G[1].bwd_index, O.EPI_NONE)
         red(0, O.matmul(dq, Wt[0]), btab[0], G[0].bwd_index, O.EPI_NONE)
         flops += sum(2.0 * rows_n * g.k_loc * g.n_loc for g in G)
@@ -384,8 +417,60 @@ def cpu_baseline(st, rows_n, fwd_only, seed):
     sample = (f"{rows_n} token rows of the block forward" +
               ("" if fwd_only else " and input-gradient backward, plus one dW column of qkv") +
               f" ({flops / 1e9:.1f} GFLOP)")
+    model, avail = cpu_host()
     return dict(value=flops / dt / 1e12, unit="TFLOP/s", cores=O.num_threads(), kind="oracle",
-                sample=sample, seconds=round(dt, 3))
+                sample=sample, seconds=round(dt, 3), cpu_model=model, cpus_available=avail,
+                per_config=cpu_per_config(seed))
+
+
+def cpu_host():
+    """The host CPU's model string and the logical CPUs this process may use."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, len(os.sched_getaffinity(0))
+
+
+def cpu_per_config(seed, rows=256, cols=512):
+    """The oracle on one bounded sample of every workload: each of the four
+    linears of the device's share, `rows` token rows by the first `cols`
+    output columns over the linear's whole contraction, reduced with its
+    group's (seeded) peer partials and the linear's epilogue.  Inputs are
+    drawn on the CPU (synth_inputs), so no GPU value is involved."""
+    import oracle as O
+    import paper_2301_08658_amd as atp
+    import synth_inputs as S
+
+    res = []
+    for name, wl in S.WORKLOADS.items():
+        if name.startswith("tiny"):
+            continue
+        d1, d2 = wl["mesh"]
+        bm = atp.ATP_BLOCK_COL if wl["mode"] == "col" else atp.ATP_BLOCK_ROW
+        G = atp.block_geometry(atp.mesh(d1, d2, 0, 0), bm, wl["h"])
+        flops, dt = 0.0, 0.0
+        for i, g in enumerate(G):
+            nc = min(cols, g.n_loc)
+            x = S.randn_bf16((rows, g.k_loc), 1.0, seed, 50 + i)
+            w = S.randn_bf16((g.k_loc, nc), wl["sigma_w"], seed, 60 + i)
+            peers = [S.randn_f32((rows, nc), 1.0, seed, 70 + 10 * i + j)
+                     for j in range(g.red_size - 1)]
+            b = S.randn_bf16((nc,), 0.02, seed, 90 + i)
+            t0 = time.perf_counter()
+            own = O.matmul(x, w)
+            O.partial_reduce([own] + peers, b, O.EPI_BIAS_GELU if i == 2 else O.EPI_BIAS)
+            dt += time.perf_counter() - t0
+            flops += 2.0 * rows * g.k_loc * nc
+        res.append(dict(workload=name, value=round(flops / dt / 1e12, 5), unit="TFLOP/s",
+                        seconds=round(dt, 3),
+                        sample=f"{rows} token rows x first {cols} output columns of each linear"))
+    return res
 
 
 def reduce_alone(torch, atp, st, reps):
@@ -445,13 +530,15 @@ def main():
         return
     log(f"[bench] {atp.atp_version()} workload={args.workload} chunks={chunks} "
         f"pass={'fwd' if fwd_only else 'fwd+bwd'}")
-    st = setup(torch, atp, S, wl, chunks, args.seed)
+    st = setup(torch, atp, S, wl, chunks, args.seed, args.weight_layout, args.partials)
     st["ws"] = None
     if not args.no_workspace:
-        nb = atp.atp_block_workspace_bytes(st["m"], st["bm"], st["T"], st["h"], chunks)
+        nb = atp.atp_block_workspace_bytes(st["m"], st["bm"], st["T"], st["h"], chunks,
+                                           st["layout"])
         st["ws"] = torch.empty(max(nb, 1), dtype=torch.uint8, device="cuda:0")
     torch.cuda.synchronize()
-    step = make_step(torch, atp, st, fwd_only, args.serial)
+    comm = cu_masked_stream(torch, args.comm_cus) if args.comm_cus else None
+    step = make_step(torch, atp, st, fwd_only, args.serial, comm)
     flops = step_flops(st, fwd_only)
 
     for _ in range(args.warmup):
@@ -611,6 +698,8 @@ def main():
                     tokens=wl["tokens"], h=wl["h"], chunks=chunks,
                     **{"pass": "fwd" if fwd_only else "fwd+bwd"},
                     serial=bool(args.serial), workspace=not args.no_workspace,
+                    weight_layout=args.weight_layout, partials=args.partials,
+                    comm_cus=args.comm_cus or None,
                     hip_graph=bool(args.graph and not args.no_workspace),
                     gflop_per_step=round(flops / 1e9, 1)),
         step_ms=step_ms, mfma_util=round(value / PEAK_BF16_TFLOPS, 4),

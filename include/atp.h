@@ -193,13 +193,20 @@ atp_status atp_shard_linear_bwd(const atp_mesh* mesh, int32_t mode, int64_t toke
                                 float* dw, int64_t lddw, float* db,
                                 void* stream, void* const* dx_chunk_done);
 
+/* Storage order of a local weight block.  ATP_W_KN: [k_loc][n_loc], the
+ * paper's Y = XW orientation (Sec. 3.2).  ATP_W_NK: [n_loc][k_loc], W^T, the
+ * way torch.nn.Linear keeps its weight ([out_features, in_features]). */
+typedef enum { ATP_W_KN = 0, ATP_W_NK = 1 } atp_weight_layout;
+
 /* Local weights of the block; index 0..3 = qkv [h,3h], out [h,h],
  * fc1 [h,4h], fc2 [4h,h] (Sec. 2.1).  Each w[i] is the device's bf16
- * block [k_loc, n_loc] (ld ldw[i]); b[i] its bf16 bias block [n_loc]. */
+ * block, [k_loc][n_loc] or [n_loc][k_loc] as `layout` says (ld ldw[i]);
+ * b[i] its bf16 bias block [n_loc].  A zero-filled struct means ATP_W_KN. */
 typedef struct {
     const void* w[4];
     int64_t ldw[4];
     const void* b[4];
+    int32_t layout;   /* atp_weight_layout, the same for all four */
 } atp_block_weights;
 
 /* Forward inputs and outputs of the block (Sec. 3.2.1).
@@ -208,9 +215,14 @@ typedef struct {
  *  attn_loc bf16 [tokens, h_a]: the attention-core output columns that
  *          feed out-proj (h/d1 for COL, h/d2 for ROW).
  *  partials[i]: host array of the red_size device pointers of linear i's
- *          group (f32 [tokens, ldp[i]]); entry red_index is this device's
- *          own buffer and is written, the others are read.  Unused (may
- *          be NULL) when the group has one member.
+ *          group ([tokens, ldp[i]] of partial_dtype); entry red_index is
+ *          this device's own buffer and is written, the others are read.
+ *          Unused (may be NULL) when the group has one member.
+ *  partial_dtype: ATP_F32 (a zero-filled struct), or ATP_BF16 for the
+ *          16-bit Partial(SUM) blocks of Sec. 5's half-precision training:
+ *          the own partial is rounded once to bf16 (nearest even) and the
+ *          group's bf16 values are summed in f32, halving the bytes every
+ *          reduction reads.
  *  qkv, o, h, z: bf16 reduced outputs (+bias; h = GeLU(...)); pre: bf16
  *          fc1 pre-activation saved for the backward, ld ld_h. */
 typedef struct {
@@ -218,23 +230,26 @@ typedef struct {
     int64_t ldx;
     const void* attn_loc;
     int64_t lda;
-    float* const* partials[4];
+    void* const* partials[4];
     int64_t ldp[4];
     void* qkv; int64_t ld_qkv;
     void* o;   int64_t ld_o;
     void* h;   int64_t ld_h;
     void* pre;
     void* z;   int64_t ld_z;
+    int32_t partial_dtype;
 } atp_block_fwd_io;
 
 /* Backward inputs and outputs of the block (Sec. 4.2).
  *  x_loc, attn_loc, h, pre: the forward's inputs and saved activations.
  *  dz, dqkv, d_o: bf16 gradients of the reduced outputs z, qkv, o.
  *  dx_partials[i]: host array of the bwd_size device pointers of linear
- *          i's backward group (f32 [tokens, ld_dxp[i]]), own entry written.
+ *          i's backward group ([tokens, ld_dxp[i]] of partial_dtype, f32 or
+ *          bf16 as in atp_block_fwd_io), own entry written.
  *  dh_pre: bf16 fc1 upstream gradient = (reduced fc2 dX) * GeLU'(pre).
  *  dx_qkv, dx_fc1, d_attn: bf16 reduced input gradients.
- *  dw[i] f32 [k_loc, n_loc] (ld ldw of the weights), db[i] f32 [n_loc]. */
+ *  dw[i] f32 in the weights' layout and leading dimension ([k_loc][n_loc]
+ *  for ATP_W_KN, [n_loc][k_loc] for ATP_W_NK), db[i] f32 [n_loc]. */
 typedef struct {
     const void* x_loc;    int64_t ldx;
     const void* attn_loc; int64_t lda;
@@ -243,7 +258,7 @@ typedef struct {
     const void* dz;   int64_t ld_dz;
     const void* dqkv; int64_t ld_dqkv;
     const void* d_o;  int64_t ld_do;
-    float* const* dx_partials[4];
+    void* const* dx_partials[4];
     int64_t ld_dxp[4];
     void* dh_pre;
     void* dx_qkv; int64_t ld_dx_qkv;
@@ -251,22 +266,56 @@ typedef struct {
     void* d_attn; int64_t ld_d_attn;
     float* dw[4];
     float* db[4];
+    int32_t partial_dtype;
 } atp_block_bwd_io;
 
 /* Workspace for the block calls' transposed-layout path (bytes): the larger
- * of the forward's need (a transposed copy W^T of the four local weight
- * shards, n_loc rows of k_loc + 64 bf16 values each) and the backward's (X^T
- * of x, the attention block and H, and dY^T of the four linears, cols rows
- * of tokens + 64 bf16 values each; the 64 values pad the row pitch off
- * memory-channel-aligned strides; the backward also holds the fp32 column
- * partials of dY that the transposes leave for db, ceil(tokens / 64) rows of
- * the widest linear's columns), each plus the fp32 split-K slabs of the
- * chunked products that feed a reduction (S * chunk rows * cols * 4 bytes
- * for the largest split plan S over every valid chunk count), every piece
- * rounded up to 256 bytes.
- * Returns 0 for invalid arguments.  `chunks` does not change the size. */
+ * of the forward's need and the backward's for weights in `weight_layout`
+ * (atp_weight_layout).  The forward keeps W^T of each weight stored
+ * [k_loc][n_loc] (n_loc rows of k_loc + 64 bf16 values; weights stored
+ * [n_loc][k_loc] need no copy).  The backward keeps X^T of x, the attention
+ * block and H, and dY^T of the four linears (cols rows of tokens + 64 bf16
+ * values each), for weights stored [n_loc][k_loc] one copy of the largest
+ * weight in [k_loc][n_loc] order (k_loc rows of n_loc + 64 values, reused
+ * linear by linear), and the fp32 column partials of dY that the
+ * transposes leave for db (ceil(tokens / 64) rows of the widest linear's
+ * columns).  Each side adds the fp32 split-K slabs of the chunked products
+ * that feed a reduction (S * chunk rows * cols * 4 bytes for the largest
+ * split plan S over every valid chunk count).  The 64 values of padding
+ * keep row pitches off memory-channel-aligned strides; every piece is
+ * rounded up to 256 bytes.  `chunks` does not change the size.
+ * Returns 0 for invalid arguments. */
 size_t atp_block_workspace_bytes(const atp_mesh* mesh, int32_t block_mode, int64_t tokens,
-                                 int64_t h, int32_t chunks);
+                                 int64_t h, int32_t chunks, int32_t weight_layout);
+
+/* Which path a block call takes (pass 0: atp_block_fwd, 1: atp_block_bwd)
+ * for a workspace of ws_bytes bytes: 1 the transposed-layout path (the
+ * workspace holds the pass's need, and for the backward tokens % 8 == 0),
+ * 0 the direct path, -1 for invalid arguments.  Host only.  A block call
+ * that would take the direct path refuses a compute stream under HIP graph
+ * capture (see atp_block_fwd). */
+int32_t atp_block_workspace_path(const atp_mesh* mesh, int32_t block_mode, int64_t tokens,
+                                 int64_t h, int32_t weight_layout, size_t ws_bytes, int32_t pass);
+
+/* Shard geometry of the block's four linears, out[0..3] = qkv, out, fc1,
+ * fc2, each as atp_shard_geometry gives it for the linear's mode in
+ * block_mode (Sec. 3.2.1: ATP_BLOCK_COL runs QKV and fc1 column-first,
+ * out-proj and fc2 row-first).  Host only.  Errors: those of
+ * atp_shard_geometry; UNSUPPORTED when a local size is not a multiple
+ * of 8. */
+atp_status atp_block_geometry(const atp_mesh* mesh, int32_t block_mode, int64_t h,
+                              atp_shard out[4]);
+
+/* The device's heads of the attention block (Sec. 3.2.1): its QKV block
+ * holds *per_block whole heads of dimension h / heads; the block is
+ * scattered over the group that reduced it, and the device attends over
+ * heads [*first, *first + *count) of the block (block-local indices).
+ * Host only.  Errors: those of atp_block_geometry; SHAPE when h is not a
+ * multiple of heads, the QKV block does not hold whole heads or its heads
+ * do not divide over the group. */
+atp_status atp_attention_heads(const atp_mesh* mesh, int32_t block_mode, int64_t h,
+                               int32_t heads, int32_t* first, int32_t* count,
+                               int32_t* per_block);
 
 /* Transpose a bf16 matrix: dst[c * ldd + r] = src[r * lds + c] for r < rows,
  * c < cols.  A data-layout step for the products of Sec. 3.2 / 4.2 (it turns
@@ -287,47 +336,50 @@ atp_status atp_transpose_bf16(int64_t rows, int64_t cols, const void* src, int64
  * written; fc2's chunk c waits for fc1's reduced chunk c.  A group of one
  * needs no reduction: its bias (and GeLU) are applied in the GEMM epilogue
  * and it runs as one launch.  Every GEMM runs on compute_stream, in the order
- * out-proj, fc1, QKV, fc2; aux_stream is accepted for compatibility and not
- * used (may be NULL).  With comm_stream == compute_stream nothing overlaps.
+ * out-proj, fc1, then QKV and fc2 (the one whose reductions read fewer bytes
+ * last).  With comm_stream == compute_stream nothing overlaps.
  * workspace (nullable, 256-byte aligned): when ws_bytes is at least the
- * forward's need (see atp_block_workspace_bytes) the call first writes W^T
- * of each shard there and runs every product from it (both operands
- * contiguous along k, the faster layout), and a chunk product with too few
- * output tiles to fill the chip is split over its contraction, the splits'
- * fp32 slabs summed in split order into the own partial before the chunk's
- * reduction reads it.  Without the workspace the products read W directly.
- * Both layouts sum each element's products in the same order: the paths
- * give the same bits except where a product splits (then they agree to
- * fp32 rounding).  Results do not depend on the streams used, and are the
- * same for every chunk count that gives each chunk product the same split
- * plan (without a workspace: every chunk count).  compute_stream's earlier
- * work happens before the block's, and on return compute_stream is ordered
- * after all of it; the workspace may be reused once compute_stream reaches
- * that point.  Without a workspace the call refuses a compute_stream under
- * HIP graph capture (UNSUPPORTED). */
+ * forward's need (atp_block_workspace_path) the products run with both
+ * operands contiguous along k, the faster layout (weights stored
+ * [k_loc][n_loc] are first copied there as W^T; weights stored
+ * [n_loc][k_loc] already are), and a chunk product with too few output
+ * tiles to fill the chip is split over its contraction, the splits' fp32
+ * slabs summed in split order into the own partial before the chunk's
+ * reduction reads it.  Without the workspace the products read W as
+ * stored.  Every layout sums each element's products in the same order:
+ * the paths give the same bits except where a product splits (then they
+ * agree to fp32 rounding).  Results do not depend on the streams used, and
+ * are the same for every chunk count that gives each chunk product the same
+ * split plan (without a workspace: every chunk count).  compute_stream's
+ * earlier work happens before the block's, and on return compute_stream is
+ * ordered after all of it; the workspace may be reused once compute_stream
+ * reaches that point.  A call that would take the direct path refuses a
+ * compute_stream under HIP graph capture (UNSUPPORTED) before enqueueing
+ * anything.  Concurrent calls from different host threads are safe (each
+ * thread keeps its own synchronisation events). */
 atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
                          int32_t chunks, const atp_block_weights* w,
                          const atp_block_fwd_io* io, void* workspace, size_t ws_bytes,
-                         void* compute_stream, void* comm_stream, void* aux_stream);
+                         void* compute_stream, void* comm_stream);
 
 /* One device's backward share of the layer (Sec. 4.2): dX = dY W^T per
  * linear, chunked and reduced on comm_stream where its group has more than
  * one member, dW = X^T dY and db = column sums of dY; fc1's dY is fc2's
  * reduced dX times GeLU'(pre).  Issue order on compute_stream: fc2's dX
  * (fc1 waits for it), QKV's and out-proj's dX, fc1's dX, then the four dW
- * largest first, so the dX reductions overlap the later GEMMs; aux_stream
- * is not used (as in atp_block_fwd).
+ * largest first, so the dX reductions overlap the later GEMMs.
  * workspace: when ws_bytes is at least the backward's need and tokens % 8
- * == 0, X^T and dY^T are written there and every dW runs from them, and the
- * chunked dX products are split over their contraction as in atp_block_fwd;
- * otherwise dW reads X and dY directly.  The paths give the same bits except
- * where a product splits (as in atp_block_fwd).  On return compute_stream is
- * ordered after all work.  Without a workspace the call refuses a
- * compute_stream under HIP graph capture (UNSUPPORTED). */
+ * == 0 (atp_block_workspace_path), X^T and dY^T are written there and every
+ * dW runs from them, weights stored [n_loc][k_loc] are copied there in
+ * [k_loc][n_loc] order for the dX products, and the chunked dX products are
+ * split over their contraction as in atp_block_fwd; otherwise every product
+ * reads its operands as stored.  The paths give the same bits except where
+ * a product splits (as in atp_block_fwd).  On return compute_stream is
+ * ordered after all work.  Graph capture and threads as atp_block_fwd. */
 atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
                          int32_t chunks, const atp_block_weights* w,
                          const atp_block_bwd_io* io, void* workspace, size_t ws_bytes,
-                         void* compute_stream, void* comm_stream, void* aux_stream);
+                         void* compute_stream, void* comm_stream);
 
 /* One device's attention core (Sec. 2.1 Formula (mha), causal; the
  * attention block of Sec. 3.2.1).  qkv is the device's reduced QKV output

@@ -315,17 +315,16 @@ def block_shapes(h):
     return dict(qkv=(h, 3 * h), out=(h, h), fc1=(h, 4 * h), fc2=(4 * h, h))
 
 
-def block_fwd_local(block_mode, mesh, coord, x_loc, a_loc, w, b, peers,
-                    round_h=round_bf16):
+def block_fwd_local(block_mode, mesh, coord, x_loc, a_loc, w, b, peers, round_h=None):
     """Forward of one device's share of the block, from its local inputs.
 
     x_loc: the device's block of the layer input X (the columns its QKV and
     fc1 shards contract over); a_loc: its block of the attention-core output
     that feeds out-proj; w[name], b[name]: local weight and bias blocks;
     peers[name]: the other group members' partial blocks in group order.
-    `round_h` maps the fp64 GeLU output to the values fc2 consumes: the
-    layer's activations are 16-bit tensors (Sec. 5, half precision; bfloat16
-    here), so by default fc2 reads H rounded to bfloat16.  None keeps fp64.
+    Everything is fp64: fc2 reads the exact GeLU output (the reference).
+    `round_h` is a diagnostic only: a function applied to H before fc2 reads
+    it (e.g. ``round_bf16``, to mimic a 16-bit stored activation, Sec. 5).
     Returns dict of qkv, o, h (GeLU output), pre (fc1 pre-activation), z.
     """
     modes = block_linear_modes(block_mode)
@@ -371,7 +370,7 @@ def block_fwd_global(block_mode, mesh, coord, X, A, W, B):
 
 
 def block_bwd_local(block_mode, mesh, coord, x_loc, a_loc, h_loc, pre_loc, w,
-                    dz, dqkv, do, peers, round_dpre=round_bf16):
+                    dz, dqkv, do, peers, round_dpre=None):
     """Backward of one device's share of the block (Sec. 4.2).
 
     dz, dqkv, do: gradients of the device's reduced output blocks z, qkv, o.
@@ -379,7 +378,9 @@ def block_bwd_local(block_mode, mesh, coord, x_loc, a_loc, h_loc, pre_loc, w,
     each linear's input gradient, in group order (the backward group of a
     linear is the mesh dimension that split its N).  fc2's reduced input
     gradient is multiplied by GeLU'(pre) to give fc1's dY, which fc1's
-    backward GEMMs read as a 16-bit tensor (Sec. 5; `round_dpre`).
+    backward reads exactly (fp64, the reference).  `round_dpre` is a
+    diagnostic only: a function applied to that dY first (e.g.
+    ``round_bf16``, to mimic a 16-bit stored gradient, Sec. 5).
     Returns dict with dx_qkv, da, dh_pre (fc1's dY), dx_fc1 and dw_*/db_*.
     """
     modes = block_linear_modes(block_mode)

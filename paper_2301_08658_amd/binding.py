@@ -33,6 +33,8 @@ ATP_EPI_BIAS_GELU = 2
 ATP_EPI_GELU_BWD = 3
 ATP_F32 = 0
 ATP_BF16 = 1
+ATP_W_KN = 0
+ATP_W_NK = 1
 ATP_MAX_GROUP = 64
 ATP_MAX_CHUNKS = 64
 
@@ -66,7 +68,8 @@ _fpp = ctypes.POINTER(ctypes.c_void_p)   # float* const* (host array of device p
 
 
 class atp_block_weights(ctypes.Structure):
-    _fields_ = [("w", _vp * 4), ("ldw", ctypes.c_int64 * 4), ("b", _vp * 4)]
+    _fields_ = [("w", _vp * 4), ("ldw", ctypes.c_int64 * 4), ("b", _vp * 4),
+                ("layout", ctypes.c_int32)]
 
 
 class atp_block_fwd_io(ctypes.Structure):
@@ -77,7 +80,8 @@ class atp_block_fwd_io(ctypes.Structure):
                 ("o", _vp), ("ld_o", ctypes.c_int64),
                 ("h", _vp), ("ld_h", ctypes.c_int64),
                 ("pre", _vp),
-                ("z", _vp), ("ld_z", ctypes.c_int64)]
+                ("z", _vp), ("ld_z", ctypes.c_int64),
+                ("partial_dtype", ctypes.c_int32)]
 
 
 class atp_block_bwd_io(ctypes.Structure):
@@ -93,7 +97,8 @@ class atp_block_bwd_io(ctypes.Structure):
                 ("dx_qkv", _vp), ("ld_dx_qkv", ctypes.c_int64),
                 ("dx_fc1", _vp), ("ld_dx_fc1", ctypes.c_int64),
                 ("d_attn", _vp), ("ld_d_attn", ctypes.c_int64),
-                ("dw", _vp * 4), ("db", _vp * 4)]
+                ("dw", _vp * 4), ("db", _vp * 4),
+                ("partial_dtype", ctypes.c_int32)]
 
 
 class atp_kernel_stat(ctypes.Structure):
@@ -127,7 +132,8 @@ EXPORTS = (
     "atp_profile_enable", "atp_profile_collect", "atp_status_string", "atp_last_error",
     "atp_version", "atp_tcomm", "atp_hcm_mesh_cost", "atp_plan_mesh", "atp_transpose_bf16",
     "atp_attention_fwd", "atp_attention_bwd", "atp_chunked_partial_reduce_bf16",
-    "atp_shard_linear_fwd_fused",
+    "atp_shard_linear_fwd_fused", "atp_block_workspace_path", "atp_block_geometry",
+    "atp_attention_heads",
 )
 
 _lib = None
@@ -161,13 +167,20 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.atp_shard_linear_bwd.argtypes = [mp, i32, i64, i64, i64, i32, _vp, i64, _vp, i64, _vp, i64,
                                          _vp, i64, _vp, i64, _vp, _vp, _fpp]
     lib.atp_shard_linear_bwd.restype = i32
-    lib.atp_block_workspace_bytes.argtypes = [mp, i32, i64, i64, i32]
+    lib.atp_block_workspace_bytes.argtypes = [mp, i32, i64, i64, i32, i32]
     lib.atp_block_workspace_bytes.restype = sz
+    lib.atp_block_workspace_path.argtypes = [mp, i32, i64, i64, i32, sz, i32]
+    lib.atp_block_workspace_path.restype = i32
+    lib.atp_block_geometry.argtypes = [mp, i32, i64, ctypes.POINTER(atp_shard)]
+    lib.atp_block_geometry.restype = i32
+    i32p = ctypes.POINTER(i32)
+    lib.atp_attention_heads.argtypes = [mp, i32, i64, i32, i32p, i32p, i32p]
+    lib.atp_attention_heads.restype = i32
     lib.atp_block_fwd.argtypes = [mp, i32, i64, i64, i32, ctypes.POINTER(atp_block_weights),
-                                  ctypes.POINTER(atp_block_fwd_io), _vp, sz, _vp, _vp, _vp]
+                                  ctypes.POINTER(atp_block_fwd_io), _vp, sz, _vp, _vp]
     lib.atp_block_fwd.restype = i32
     lib.atp_block_bwd.argtypes = [mp, i32, i64, i64, i32, ctypes.POINTER(atp_block_weights),
-                                  ctypes.POINTER(atp_block_bwd_io), _vp, sz, _vp, _vp, _vp]
+                                  ctypes.POINTER(atp_block_bwd_io), _vp, sz, _vp, _vp]
     lib.atp_block_bwd.restype = i32
     lib.atp_profile_enable.argtypes = [i32]
     lib.atp_profile_enable.restype = None
@@ -217,14 +230,27 @@ def mesh(d1, d2, i1=0, i2=0) -> atp_mesh:
     return atp_mesh(int(d1), int(d2), int(i1), int(i2))
 
 
-def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
-    return None if t is None else t.data_ptr()
+def _on_device(t: torch.Tensor, name: str):
+    """The library reads and writes device memory of the current HIP device."""
+    if not t.is_cuda:
+        raise ValueError(f"{name}: must be a tensor on the GPU, got one on {t.device}")
+    if t.device.index != torch.cuda.current_device():
+        raise ValueError(f"{name}: on {t.device}, but the current device is "
+                         f"cuda:{torch.cuda.current_device()}")
+
+
+def _ptr(t: Optional[torch.Tensor], name: str = "tensor") -> Optional[int]:
+    if t is None:
+        return None
+    _on_device(t, name)
+    return t.data_ptr()
 
 
 def _mat(t: Optional[torch.Tensor], rows: int, cols: int, dtype, name: str):
-    """(pointer, ld) of a row-major matrix with at least rows x cols."""
+    """(pointer, ld) of a row-major device matrix with at least rows x cols."""
     if t is None:
         return None, 0
+    _on_device(t, name)
     if t.dtype != dtype:
         raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
     if t.dim() != 2 or (t.size(1) > 1 and t.stride(1) != 1):
@@ -237,6 +263,7 @@ def _mat(t: Optional[torch.Tensor], rows: int, cols: int, dtype, name: str):
 def _vec(t: Optional[torch.Tensor], n: int, dtype, name: str):
     if t is None:
         return None
+    _on_device(t, name)
     if t.dtype != dtype:
         raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
     if t.numel() < n or not t.is_contiguous():
@@ -415,45 +442,75 @@ def atp_shard_linear_bwd(m: atp_mesh, mode: int, tokens: int, k: int, n: int, ch
 
 def block_geometry(m: atp_mesh, block_mode: int, h: int):
     """Shard geometry of the block's four linears (qkv, out, fc1, fc2)."""
-    modes = ((ATP_COL_FIRST, ATP_ROW_FIRST, ATP_COL_FIRST, ATP_ROW_FIRST)
-             if block_mode == ATP_BLOCK_COL else
-             (ATP_ROW_FIRST, ATP_COL_FIRST, ATP_ROW_FIRST, ATP_COL_FIRST))
-    shapes = ((h, 3 * h), (h, h), (h, 4 * h), (4 * h, h))
-    return [atp_shard_geometry(m, md, k, n) for md, (k, n) in zip(modes, shapes)]
+    out = (atp_shard * 4)()
+    _check(load_library().atp_block_geometry(ctypes.byref(m), int(block_mode), int(h), out))
+    return [out[i] for i in range(4)]
 
 
 def atp_block_workspace_bytes(m: atp_mesh, block_mode: int, tokens: int, h: int,
-                              chunks: int) -> int:
+                              chunks: int, weight_layout: int = ATP_W_KN) -> int:
     return int(load_library().atp_block_workspace_bytes(ctypes.byref(m), int(block_mode),
-                                                         int(tokens), int(h), int(chunks)))
+                                                         int(tokens), int(h), int(chunks),
+                                                         int(weight_layout)))
 
 
-def _weights(G, w: Sequence[torch.Tensor], b: Sequence[torch.Tensor]):
+def atp_block_workspace_path(m: atp_mesh, block_mode: int, tokens: int, h: int,
+                             weight_layout: int, ws_bytes: int, pass_: int) -> int:
+    """1: a block call of the pass (0 fwd, 1 bwd) with ws_bytes of workspace
+    takes the transposed-layout path; 0: the direct path; -1: invalid."""
+    return int(load_library().atp_block_workspace_path(ctypes.byref(m), int(block_mode),
+                                                        int(tokens), int(h), int(weight_layout),
+                                                        int(ws_bytes), int(pass_)))
+
+
+def _weights(G, w: Sequence[torch.Tensor], b: Sequence[torch.Tensor], layout: int):
+    """Weights [k_loc, n_loc] (ATP_W_KN) or [n_loc, k_loc] (ATP_W_NK)."""
     W = atp_block_weights()
+    W.layout = int(layout)
     for i, g in enumerate(G):
-        p, ld = _mat(w[i], g.k_loc, g.n_loc, torch.bfloat16, f"w[{LINEARS[i]}]")
+        r, c = (g.k_loc, g.n_loc) if layout == ATP_W_KN else (g.n_loc, g.k_loc)
+        p, ld = _mat(w[i], r, c, torch.bfloat16, f"w[{LINEARS[i]}]")
         W.w[i] = p
         W.ldw[i] = ld
         W.b[i] = _vec(b[i], g.n_loc, torch.bfloat16, f"b[{LINEARS[i]}]")
     return W
 
 
+def _partial_dtype(tables) -> tuple:
+    """(ATP dtype code, torch dtype) shared by every partial buffer given."""
+    dts = {t.dtype for tab in tables if tab for t in tab if t is not None}
+    if len(dts) > 1:
+        raise TypeError(f"partial buffers mix dtypes {sorted(map(str, dts))}")
+    dt = dts.pop() if dts else torch.float32
+    return _dtype_code(dt), dt
+
+
+def _workspace(workspace):
+    if workspace is None:
+        return None, 0
+    _on_device(workspace, "workspace")
+    return workspace.data_ptr(), workspace.numel() * workspace.element_size()
+
+
 def atp_block_fwd(m: atp_mesh, block_mode: int, tokens: int, h: int, chunks: int, w, b,
                   x_loc, attn_loc, partials, qkv, o, h_out, pre, z, workspace=None,
-                  compute_stream=None, comm_stream=None, aux_stream=None):
-    """partials[i]: list of the red_size f32 buffers of linear i's group (own
-    entry written), or None for a group of one."""
+                  compute_stream=None, comm_stream=None, weight_layout: int = ATP_W_KN):
+    """partials[i]: list of the red_size buffers of linear i's group (own
+    entry written; all float32, or all bfloat16 for 16-bit partials), or
+    None for a group of one."""
     G = block_geometry(m, block_mode, h)
-    W = _weights(G, w, b)
+    W = _weights(G, w, b, weight_layout)
     io = atp_block_fwd_io()
+    io.partial_dtype, pdt = _partial_dtype(partials)
     io.x_loc, io.ldx = _mat(x_loc, tokens, G[0].k_loc, torch.bfloat16, "x_loc")
     io.attn_loc, io.lda = _mat(attn_loc, tokens, G[1].k_loc, torch.bfloat16, "attn_loc")
     keep = []
     for i, g in enumerate(G):
         if g.red_size > 1:
-            tab, arr, ld = _ptr_table(partials[i], tokens, g.n_loc, f"partials[{LINEARS[i]}]")
             if len(partials[i]) != g.red_size:
                 raise ValueError(f"partials[{LINEARS[i]}] needs {g.red_size} buffers")
+            tab, arr, ld = _ptr_table(partials[i], tokens, g.n_loc, f"partials[{LINEARS[i]}]",
+                                      pdt)
             io.partials[i] = tab
             io.ldp[i] = ld
             keep.append(arr)
@@ -465,24 +522,23 @@ def atp_block_fwd(m: atp_mesh, block_mode: int, tokens: int, h: int, chunks: int
         raise ValueError("pre must share h's leading dimension")
     io.pre = pp
     io.z, io.ld_z = _mat(z, tokens, G[3].n_loc, torch.bfloat16, "z")
-    wsp = _ptr(workspace)
-    wsb = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    wsp, wsb = _workspace(workspace)
     _check(load_library().atp_block_fwd(ctypes.byref(m), int(block_mode), int(tokens), int(h),
                                         int(chunks), ctypes.byref(W), ctypes.byref(io), wsp, wsb,
-                                        _stream(compute_stream), _stream(comm_stream),
-                                        _opt_stream(aux_stream)))
+                                        _stream(compute_stream), _stream(comm_stream)))
 
 
 def atp_block_bwd(m: atp_mesh, block_mode: int, tokens: int, h: int, chunks: int, w, b,
                   x_loc, attn_loc, h_act, pre, dz, dqkv, d_o, dx_partials, dh_pre, dx_qkv,
                   dx_fc1, d_attn, dw, db, workspace=None, compute_stream=None,
-                  comm_stream=None, aux_stream=None):
-    """dx_partials[i]: list of the bwd_size f32 buffers of linear i's backward
-    group (own entry written), or None for a group of one.  dw[i] must share
-    the leading dimension of w[i]."""
+                  comm_stream=None, weight_layout: int = ATP_W_KN):
+    """dx_partials[i]: list of the bwd_size buffers of linear i's backward
+    group (own entry written; float32 or bfloat16), or None for a group of
+    one.  dw[i] has the weight's layout and leading dimension."""
     G = block_geometry(m, block_mode, h)
-    W = _weights(G, w, b)
+    W = _weights(G, w, b, weight_layout)
     io = atp_block_bwd_io()
+    io.partial_dtype, pdt = _partial_dtype(dx_partials)
     io.x_loc, io.ldx = _mat(x_loc, tokens, G[0].k_loc, torch.bfloat16, "x_loc")
     io.attn_loc, io.lda = _mat(attn_loc, tokens, G[1].k_loc, torch.bfloat16, "attn_loc")
     io.h, io.ld_h = _mat(h_act, tokens, G[2].n_loc, torch.bfloat16, "h")
@@ -500,7 +556,7 @@ def atp_block_bwd(m: atp_mesh, block_mode: int, tokens: int, h: int, chunks: int
             if len(dx_partials[i]) != g.bwd_size:
                 raise ValueError(f"dx_partials[{LINEARS[i]}] needs {g.bwd_size} buffers")
             tab, arr, ld = _ptr_table(dx_partials[i], tokens, g.k_loc,
-                                      f"dx_partials[{LINEARS[i]}]")
+                                      f"dx_partials[{LINEARS[i]}]", pdt)
             io.dx_partials[i] = tab
             io.ld_dxp[i] = ld
             keep.append(arr)
@@ -508,17 +564,16 @@ def atp_block_bwd(m: atp_mesh, block_mode: int, tokens: int, h: int, chunks: int
     io.dx_fc1, io.ld_dx_fc1 = _mat(dx_fc1, tokens, G[2].k_loc, torch.bfloat16, "dx_fc1")
     io.d_attn, io.ld_d_attn = _mat(d_attn, tokens, G[1].k_loc, torch.bfloat16, "d_attn")
     for i, g in enumerate(G):
-        p, ld = _mat(dw[i], g.k_loc, g.n_loc, torch.float32, f"dw[{LINEARS[i]}]")
+        r, c = (g.k_loc, g.n_loc) if weight_layout == ATP_W_KN else (g.n_loc, g.k_loc)
+        p, ld = _mat(dw[i], r, c, torch.float32, f"dw[{LINEARS[i]}]")
         if ld != W.ldw[i]:
             raise ValueError(f"dw[{LINEARS[i]}] must share the weight's leading dimension")
         io.dw[i] = p
         io.db[i] = _vec(db[i], g.n_loc, torch.float32, f"db[{LINEARS[i]}]") if db else None
-    wsp = _ptr(workspace)
-    wsb = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    wsp, wsb = _workspace(workspace)
     _check(load_library().atp_block_bwd(ctypes.byref(m), int(block_mode), int(tokens), int(h),
                                         int(chunks), ctypes.byref(W), ctypes.byref(io), wsp, wsb,
-                                        _stream(compute_stream), _stream(comm_stream),
-                                        _opt_stream(aux_stream)))
+                                        _stream(compute_stream), _stream(comm_stream)))
 
 
 def atp_profile_enable(on=True):
@@ -548,10 +603,22 @@ def atp_transpose_bf16(src, dst, stream=None):
 def attention_heads(m: atp_mesh, block_mode: int, h: int, heads: int):
     """(first head, number of heads) of the device's run of its QKV block's
     heads (block-local indices), and the block's head count."""
-    g = block_geometry(m, block_mode, h)[0]
-    per_block = g.n_loc // (3 * (h // heads))
-    hd = per_block // g.red_size
-    return g.red_index * hd, hd, per_block
+    first, count, per_block = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    _check(load_library().atp_attention_heads(ctypes.byref(m), int(block_mode), int(h),
+                                              int(heads), ctypes.byref(first),
+                                              ctypes.byref(count), ctypes.byref(per_block)))
+    return first.value, count.value, per_block.value
+
+
+def _f32_scratch(t, n: int, name: str):
+    """A contiguous float32 buffer of at least n values (checked before any
+    other argument, so a short buffer never reaches a kernel)."""
+    if t is None:
+        return
+    if t.dtype != torch.float32 or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous float32 tensor")
+    if t.numel() < n:
+        raise ValueError(f"{name}: {t.numel()} values, the device's heads need {n}")
 
 
 def atp_attention_fwd(m: atp_mesh, block_mode: int, batch: int, seq: int, h: int, heads: int,
@@ -560,14 +627,14 @@ def atp_attention_fwd(m: atp_mesh, block_mode: int, batch: int, seq: int, h: int
     QKV block), out [batch*seq, >= n_loc/3] bf16 (the gathered out-proj
     input; the device's columns are written), lse [heads_dev, batch*seq] fp32."""
     T = batch * seq
+    _, hd, _ = attention_heads(m, block_mode, h, heads)
+    _f32_scratch(lse, hd * T, "lse")
     g = block_geometry(m, block_mode, h)[0]
     qp, ldq = _mat(qkv, T, g.n_loc, torch.bfloat16, "qkv")
     op, ldo = _mat(out, T, g.n_loc // 3, torch.bfloat16, "out")
-    if lse is not None and (lse.dtype != torch.float32 or not lse.is_contiguous()):
-        raise ValueError("lse must be a contiguous float32 tensor")
     _check(load_library().atp_attention_fwd(ctypes.byref(m), int(block_mode), int(batch), int(seq),
-                                            int(h), int(heads), qp, ldq, op, ldo, _ptr(lse),
-                                            _stream(stream)))
+                                            int(h), int(heads), qp, ldq, op, ldo,
+                                            _ptr(lse, "lse"), _stream(stream)))
 
 
 def atp_attention_bwd(m: atp_mesh, block_mode: int, batch: int, seq: int, h: int, heads: int,
@@ -575,17 +642,18 @@ def atp_attention_bwd(m: atp_mesh, block_mode: int, batch: int, seq: int, h: int
     """Gradient of atp_attention_fwd: d_qkv (the QKV block's shape) receives
     dq, dk, dv of the device's heads; delta is fp32 scratch [heads_dev*T]."""
     T = batch * seq
+    _, hd, _ = attention_heads(m, block_mode, h, heads)
+    _f32_scratch(lse, hd * T, "lse")
+    _f32_scratch(delta, hd * T, "delta")
     g = block_geometry(m, block_mode, h)[0]
     qp, ldq = _mat(qkv, T, g.n_loc, torch.bfloat16, "qkv")
     op, ldo = _mat(out, T, g.n_loc // 3, torch.bfloat16, "out")
     dop, lddo = _mat(d_out, T, g.n_loc // 3, torch.bfloat16, "d_out")
     dqp, lddq = _mat(d_qkv, T, g.n_loc, torch.bfloat16, "d_qkv")
-    for t, nm in ((lse, "lse"), (delta, "delta")):
-        if t is not None and (t.dtype != torch.float32 or not t.is_contiguous()):
-            raise ValueError(f"{nm} must be a contiguous float32 tensor")
     _check(load_library().atp_attention_bwd(ctypes.byref(m), int(block_mode), int(batch), int(seq),
-                                            int(h), int(heads), qp, ldq, op, ldo, _ptr(lse), dop,
-                                            lddo, dqp, lddq, _ptr(delta), _stream(stream)))
+                                            int(h), int(heads), qp, ldq, op, ldo,
+                                            _ptr(lse, "lse"), dop, lddo, dqp, lddq,
+                                            _ptr(delta, "delta"), _stream(stream)))
 
 
 # ---------------------------------------------------------------------------

@@ -135,16 +135,24 @@ bool valid_epi(int32_t e) { return e >= ATP_EPI_NONE && e <= ATP_EPI_GELU_BWD; }
 bool valid_dtype(int32_t d) { return d == ATP_F32 || d == ATP_BF16; }
 
 // ---------------------------------------------------------------------------
-// events: a per-device pool of synchronisation events, and timing records
+// events: synchronisation events per host thread and device, and timing records
 // ---------------------------------------------------------------------------
-std::mutex g_mu;
-std::map<int, std::vector<hipEvent_t>> g_sync_events;   // device -> pool
+std::mutex g_mu;   // guards the timing records below
+
+// The block calls order their streams with events taken from a pool that
+// belongs to the calling host thread (one pool per device), so calls from
+// different threads never share an event, and the pool of a thread can
+// only grow between that thread's calls (no reallocation while a call uses
+// it).  A thread's events are re-recorded by its next call, which is
+// correct because a wait refers to the record enqueued before it.  The
+// events are not destroyed when a thread exits (the HIP runtime may already
+// be shutting down then); each thread holds at most one pool per device.
+thread_local std::map<int, std::vector<hipEvent_t>> t_sync_events;   // device -> pool
 
 atp_status sync_events(size_t count, hipEvent_t** out) {
     int dev = 0;
     HIP_CHECK(hipGetDevice(&dev), "hipGetDevice");
-    std::lock_guard<std::mutex> lk(g_mu);
-    auto& pool = g_sync_events[dev];
+    auto& pool = t_sync_events[dev];
     while (pool.size() < count) {
         hipEvent_t e;
         HIP_CHECK(hipEventCreateWithFlags(&e, hipEventDisableTiming), "hipEventCreateWithFlags");
@@ -235,13 +243,14 @@ atp_status run_colsum(const void* dy, int64_t ld, int64_t T, int64_t N, float* d
                  [&] { return atp::launch_colsum(dy, ld, T, N, db, s); });
 }
 
-// The S split-K slabs of an fp32 product summed into its destination rows.
-atp_status run_split_sum(const float* ws, int S, int64_t rows, int64_t cols, float* out,
-                         int64_t ldo, hipStream_t s) {
+// The S split-K slabs of an fp32 product summed into its destination rows
+// (fp32, or bf16 rounded once).
+atp_status run_split_sum(const float* ws, int S, int64_t rows, int64_t cols, void* out,
+                         int64_t ldo, bool out_bf16, hipStream_t s) {
     if (rows <= 0 || cols <= 0) return ATP_OK;
     const double el = (double)rows * (double)cols;
-    return timed("split_sum", 0.0, el * 4.0 * (S + 1), s, [&] {
-        return atp::launch_split_sum(ws, S, rows * cols, cols, rows, cols, out, ldo, s);
+    return timed("split_sum", 0.0, el * (4.0 * S + (out_bf16 ? 2.0 : 4.0)), s, [&] {
+        return atp::launch_split_sum(ws, S, rows * cols, cols, rows, cols, out, ldo, out_bf16, s);
     });
 }
 
@@ -353,10 +362,26 @@ size_t slab_bytes(const BlockPlan& P, int64_t tokens, bool bwd) {
     return most;
 }
 
-size_t ws_fwd_bytes(const BlockPlan& P, int64_t tokens) {
+bool valid_layout(int32_t l) { return l == ATP_W_KN || l == ATP_W_NK; }
+
+// The forward's pieces: the slabs, and W^T ([n_loc][k_loc]) of weights
+// stored [k_loc][n_loc] (weights stored [n_loc][k_loc] are read as they are).
+size_t ws_fwd_bytes(const BlockPlan& P, int64_t tokens, int32_t layout) {
     size_t b = ws_round(slab_bytes(P, tokens, false));
-    for (int L = 0; L < 4; ++L) b += ws_round((size_t)P.g[L].n_loc * ws_pitch(P.g[L].k_loc) * 2);
+    if (layout == ATP_W_KN)
+        for (int L = 0; L < 4; ++L)
+            b += ws_round((size_t)P.g[L].n_loc * ws_pitch(P.g[L].k_loc) * 2);
     return b;
+}
+
+// One [k_loc][n_loc] copy of a weight stored [n_loc][k_loc], for the dX
+// products of the backward; sized for the largest weight, reused linear by
+// linear (every use is on the compute stream, in order).
+size_t wkn_bytes(const BlockPlan& P) {
+    size_t most = 0;
+    for (int L = 0; L < 4; ++L)
+        most = std::max(most, (size_t)P.g[L].k_loc * ws_pitch(P.g[L].n_loc) * 2);
+    return most;
 }
 
 // fp32 column partials of dY, one row per 64 tokens, for the widest linear
@@ -366,30 +391,44 @@ size_t colpart_bytes(const BlockPlan& P, int64_t tokens) {
     return (size_t)((tokens + 63) / 64) * (size_t)n * 4;
 }
 
-size_t ws_bwd_bytes(const BlockPlan& P, int64_t tokens) {
+size_t ws_bwd_bytes(const BlockPlan& P, int64_t tokens, int32_t layout) {
     const size_t t2 = (size_t)ws_pitch(tokens) * 2;
     size_t b = ws_round(P.g[0].k_loc * t2) + ws_round(P.g[1].k_loc * t2) +
                ws_round(P.g[3].k_loc * t2) + ws_round(slab_bytes(P, tokens, true)) +
                ws_round(colpart_bytes(P, tokens));
     for (int L = 0; L < 4; ++L) b += ws_round(P.g[L].n_loc * t2);
+    if (layout == ATP_W_NK) b += ws_round(wkn_bytes(P));
     return b;
 }
 
-// An fp32 product [M, N] over K: split over K into `slab` when a slab is
-// given and the plan says so, the splits then summed in split order into C.
+// True when a call of the pass (0 forward, 1 backward) with a workspace of
+// ws_bytes bytes takes the transposed-layout path.
+bool takes_ws_path(const BlockPlan& P, int64_t tokens, int32_t layout, size_t ws_bytes,
+                   int pass) {
+    if (ws_bytes == 0) return false;
+    if (pass == 0) return ws_bytes >= ws_fwd_bytes(P, tokens, layout);
+    return ws_bytes >= ws_bwd_bytes(P, tokens, layout) && tokens % 8 == 0;
+}
+
+// A partial product [M, N] over K (fp32, or bf16 when p.out_bf16): split
+// over K into `slab` when a slab is given and the plan says so, the splits'
+// fp32 slabs then summed in split order into C (rounded once to bf16 for a
+// bf16 partial).
 atp_status run_nt_partial(atp::GemmProblem p, float* slab, hipStream_t s) {
     int64_t ks = 0;
     const int S = slab ? atp::nt_split_plan(p.M, p.N, p.K, &ks) : 1;
     if (S <= 1) return run_gemm(p, s);
-    float* out = static_cast<float*>(p.C);
+    void* out = p.C;
     const int64_t ldo = p.ldc;
+    const bool b16 = p.out_bf16;
     p.C = slab;
     p.ldc = p.N;
+    p.out_bf16 = false;
     p.splits = S;
     p.ksplit = ks;
     p.c_split = p.M * p.N;
     ATP_CHECK(run_gemm(p, s));
-    return run_split_sum(slab, S, p.M, p.N, out, ldo, s);
+    return run_split_sum(slab, S, p.M, p.N, out, ldo, b16, s);
 }
 
 // Carves consecutive aligned pieces out of the caller's workspace.
@@ -416,7 +455,7 @@ atp_status run_colsum_finish(const float* part, int64_t ldp, int64_t nb, int64_t
                  [&] { return atp::launch_colsum_finish(part, ldp, nb, N, db, s); });
 }
 
-atp_status check_group(float* const* tab, int32_t size, int64_t rows, int64_t ld, int64_t cols,
+atp_status check_group(void* const* tab, int32_t size, int64_t rows, int64_t ld, int64_t cols,
                        const char* name) {
     if (size > ATP_MAX_GROUP)
         return set_error(ATP_ERR_UNSUPPORTED, "%s: group of %d exceeds %d", name, size,
@@ -443,8 +482,6 @@ const char* const kLinearName[4] = {"qkv", "out", "fc1", "fc2"};
 struct Streams {
     hipStream_t cs, ms;
     Streams(void* c, void* m) : cs(static_cast<hipStream_t>(c)), ms(static_cast<hipStream_t>(m)) {}
-    hipStream_t lane(int) const { return cs; }
-    int take(double) const { return 0; }
 
     // everything already queued on cs happens before the block's work
     atp_status begin(hipEvent_t start) const {
@@ -462,20 +499,22 @@ struct Streams {
     }
 };
 
-// Capturing a block call without a workspace into a HIP graph once made
-// hipStreamEndCapture crash inside the runtime (a host segmentation fault,
-// at a time when such calls also ran GEMMs on a second stream; the cause was
-// never identified), so a call without a workspace refuses a capturing
-// compute stream.  Calls with a workspace are captured and replayed bit for
+// Capturing a block call on its direct path (no usable workspace) into a HIP
+// graph once made hipStreamEndCapture crash inside the runtime (a host
+// segmentation fault, at a time when that path also ran GEMMs on a second
+// stream; the cause was never identified), so a call that would take the
+// direct path refuses a capturing compute stream, before it enqueues
+// anything.  Calls on the workspace path are captured and replayed bit for
 // bit (tested).
-atp_status refuse_capture_without_workspace(void* compute_stream) {
+atp_status refuse_capture_of_direct_path(void* compute_stream) {
     hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
     HIP_CHECK(hipStreamIsCapturing(static_cast<hipStream_t>(compute_stream), &st),
               "hipStreamIsCapturing");
     if (st != hipStreamCaptureStatusNone)
         return set_error(ATP_ERR_UNSUPPORTED,
-                         "graph capture needs a workspace (pass one of "
-                         "atp_block_workspace_bytes bytes)");
+                         "graph capture needs the workspace path (a workspace of "
+                         "atp_block_workspace_bytes bytes; the backward also needs "
+                         "tokens %% 8 == 0)");
     return ATP_OK;
 }
 
@@ -739,13 +778,13 @@ atp_status atp_shard_linear_bwd(const atp_mesh* mesh, int32_t mode, int64_t toke
 }
 
 size_t atp_block_workspace_bytes(const atp_mesh* mesh, int32_t block_mode, int64_t tokens,
-                                 int64_t h, int32_t chunks) {
+                                 int64_t h, int32_t chunks, int32_t weight_layout) {
     (void)chunks;
     BlockPlan P;
     if (!mesh || check_mesh(mesh) != ATP_OK || block_plan(mesh, block_mode, h, &P) != ATP_OK ||
-        tokens < 0)
+        tokens < 0 || !valid_layout(weight_layout))
         return 0;
-    return std::max(ws_fwd_bytes(P, tokens), ws_bwd_bytes(P, tokens));
+    return std::max(ws_fwd_bytes(P, tokens, weight_layout), ws_bwd_bytes(P, tokens, weight_layout));
 }
 
 atp_status atp_attention_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t batch,
@@ -832,22 +871,88 @@ atp_status atp_transpose_bf16(int64_t rows, int64_t cols, const void* src, int64
     return run_transpose(src, lds, rows, cols, dst, ldd, static_cast<hipStream_t>(stream));
 }
 
+extern "C++" {
+namespace {
+
+// Weights of the block in either storage order: the checks, and the
+// operand of each product.  `kn` weights are [k_loc][n_loc], else [n_loc][k_loc].
+atp_status check_weights(const BlockPlan& P, const atp_block_weights* w) {
+    if (!valid_layout(w->layout))
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "weight layout %d unknown", w->layout);
+    const bool kn = w->layout == ATP_W_KN;
+    for (int i = 0; i < 4; ++i) {
+        char nm[32];
+        snprintf(nm, sizeof nm, "w[%s]", kLinearName[i]);
+        const atp_shard& g = P.g[i];
+        ATP_CHECK(check_mat(w->w[i], kn ? g.k_loc : g.n_loc, w->ldw[i], kn ? g.n_loc : g.k_loc,
+                            nm));
+        snprintf(nm, sizeof nm, "b[%s]", kLinearName[i]);
+        ATP_CHECK(check_vec(w->b[i], nm));
+    }
+    return ATP_OK;
+}
+
+atp_status check_partial_dtype(int32_t d) {
+    if (!valid_dtype(d)) return set_error(ATP_ERR_INVALID_ARGUMENT, "partial_dtype %d", d);
+    return ATP_OK;
+}
+
+// Byte offset of row r of a partial buffer with leading dimension ld.
+template <class T>
+T* row_ptr(T* base, int64_t r, int64_t ld, bool b16) {
+    return reinterpret_cast<T*>(reinterpret_cast<typename std::conditional<
+        std::is_const<T>::value, const char, char>::type*>(base) + r * ld * (b16 ? 2 : 4));
+}
+
+}  // namespace
+}  // extern "C++"
+
+int32_t atp_block_workspace_path(const atp_mesh* mesh, int32_t block_mode, int64_t tokens,
+                                 int64_t h, int32_t weight_layout, size_t ws_bytes,
+                                 int32_t pass) {
+    BlockPlan P;
+    if (!mesh || check_mesh(mesh) != ATP_OK || block_plan(mesh, block_mode, h, &P) != ATP_OK ||
+        tokens < 0 || !valid_layout(weight_layout) || (pass != 0 && pass != 1))
+        return -1;
+    return takes_ws_path(P, tokens, weight_layout, ws_bytes, pass) ? 1 : 0;
+}
+
+atp_status atp_block_geometry(const atp_mesh* mesh, int32_t block_mode, int64_t h,
+                              atp_shard out[4]) {
+    if (!out) return set_error(ATP_ERR_INVALID_ARGUMENT, "out is NULL");
+    BlockPlan P;
+    ATP_CHECK(check_mesh(mesh));
+    ATP_CHECK(block_plan(mesh, block_mode, h, &P));
+    for (int i = 0; i < 4; ++i) out[i] = P.g[i];
+    return ATP_OK;
+}
+
+atp_status atp_attention_heads(const atp_mesh* mesh, int32_t block_mode, int64_t h,
+                               int32_t heads, int32_t* first, int32_t* count,
+                               int32_t* per_block) {
+    if (!first || !count || !per_block)
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "an output pointer is NULL");
+    AttnPlan ap;
+    ATP_CHECK(attention_plan(mesh, block_mode, 0, 0, h, heads, &ap));
+    *first = ap.first;
+    *count = ap.hd;
+    *per_block = ap.heads_blk;
+    return ATP_OK;
+}
+
 atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
                          int32_t chunks, const atp_block_weights* w, const atp_block_fwd_io* io,
                          void* workspace, size_t ws_bytes, void* compute_stream,
-                         void* comm_stream, void* aux_stream) {
+                         void* comm_stream) {
     BlockPlan P;
     ATP_CHECK(check_mesh(mesh));
     ATP_CHECK(block_plan(mesh, block_mode, h, &P));
     ATP_CHECK(check_chunks(tokens, chunks));
     if (!w || !io) return set_error(ATP_ERR_INVALID_ARGUMENT, "weights or io is NULL");
-    for (int i = 0; i < 4; ++i) {
-        char nm[32];
-        snprintf(nm, sizeof nm, "w[%s]", kLinearName[i]);
-        ATP_CHECK(check_mat(w->w[i], P.g[i].k_loc, w->ldw[i], P.g[i].n_loc, nm));
-        snprintf(nm, sizeof nm, "b[%s]", kLinearName[i]);
-        ATP_CHECK(check_vec(w->b[i], nm));
-    }
+    ATP_CHECK(check_weights(P, w));
+    ATP_CHECK(check_partial_dtype(io->partial_dtype));
+    const bool kn = w->layout == ATP_W_KN;
+    const bool pb16 = io->partial_dtype == ATP_BF16;
     // inputs: x feeds qkv and fc1 (same k split), attn feeds out
     if (P.g[0].k_loc != P.g[2].k_loc)
         return set_error(ATP_ERR_SHAPE, "qkv and fc1 contract over different blocks of x");
@@ -866,18 +971,18 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         snprintf(nm, sizeof nm, "partials[%s]", kLinearName[i]);
         ATP_CHECK(check_group(io->partials[i], P.g[i].red_size, tokens, io->ldp[i], P.g[i].n_loc, nm));
     }
-
-    // with a large enough workspace every forward product runs from a
-    // transposed weight copy (both operands contiguous along k: the layout
-    // the GEMM kernel streams fastest), and chunk products with too few tiles
-    // to fill the chip are split over k into slabs there
-    const bool ws = workspace && ws_bytes >= ws_fwd_bytes(P, tokens);
     if (workspace && reinterpret_cast<uintptr_t>(workspace) % kWsAlign)
         return set_error(ATP_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kWsAlign);
-    if (!workspace) ATP_CHECK(refuse_capture_without_workspace(compute_stream));
+
+    // With a large enough workspace every forward product runs with both
+    // operands contiguous along k (the layout the GEMM kernel streams
+    // fastest; weights stored [k][n] are first copied there as W^T), and
+    // chunk products with too few tiles to fill the chip are split over k
+    // into slabs there.  The direct path never runs under graph capture.
+    const bool ws = workspace && takes_ws_path(P, tokens, w->layout, ws_bytes, 0);
+    if (!ws) ATP_CHECK(refuse_capture_of_direct_path(compute_stream));
 
     Streams S(compute_stream, comm_stream);
-    (void)aux_stream;   // unused: every GEMM runs on compute_stream
     hipEvent_t* ev = nullptr;
     // [0] start  [1] comm end  [2] unused  [3] fc1's single launch done,
     // then per linear per chunk GEMM-done, then fc1 reduce-done per chunk
@@ -891,24 +996,30 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     float* slab = nullptr;
     if (ws) {
         Carver c{static_cast<char*>(workspace)};
-        for (int L = 0; L < 4; ++L)
-            wt[L] = c.take((size_t)P.g[L].n_loc * ws_pitch(P.g[L].k_loc) * 2);
+        if (kn)
+            for (int L = 0; L < 4; ++L)
+                wt[L] = c.take((size_t)P.g[L].n_loc * ws_pitch(P.g[L].k_loc) * 2);
         slab = reinterpret_cast<float*>(c.take(slab_bytes(P, tokens, false)));
     }
-    // W^T of linear L, written before the linear's first GEMM (same stream)
+    // W^T of linear L (weights stored [k][n]), written before the linear's
+    // first GEMM (same stream)
     bool wt_done[4] = {false, false, false, false};
     auto need_wt = [&](int L) -> atp_status {
-        if (!ws || wt_done[L]) return ATP_OK;
+        if (!ws || !kn || wt_done[L]) return ATP_OK;
         const atp_shard& g = P.g[L];
         ATP_CHECK(run_transpose(w->w[L], w->ldw[L], g.k_loc, g.n_loc, wt[L], ws_pitch(g.k_loc),
                                 S.cs));
         wt_done[L] = true;
         return ATP_OK;
     };
-    // the product X W of linear L: NT from W^T, or NN from W as given
+    // the product X W of linear L: NT from W^T (the workspace copy, or the
+    // weight itself when stored [n][k]), or NN from W stored [k][n]
     auto fwd_problem = [&](int L, const void* A, int64_t lda, void* C, int64_t ldc, bool b16,
                            int epi, int64_t M) {
         const atp_shard& g = P.g[L];
+        if (!kn)
+            return gemm_problem(atp::LAYOUT_NT, A, lda, w->w[L], w->ldw[L], C, ldc, b16, epi, M,
+                                g.n_loc, g.k_loc);
         if (ws)
             return gemm_problem(atp::LAYOUT_NT, A, lda, wt[L], ws_pitch(g.k_loc), C, ldc, b16,
                                 epi, M, g.n_loc, g.k_loc);
@@ -922,55 +1033,42 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     void* outp[4] = {io->qkv, io->o, io->h, io->z};
     const int64_t ldo[4] = {io->ld_qkv, io->ld_o, io->ld_h, io->ld_z};
     const bool fc1_reduced = P.g[2].red_size > 1;
-    int h_lane = 0;  // lane of fc1's single launch
 
     // fc2 reads H: wait for fc1's reduced chunk c (the comm stream runs in
-    // order, so chunk chunks-1 means all of H), or for fc1's single launch
-    auto wait_h = [&](int lane, int c) -> atp_status {
-        if (fc1_reduced)
-            HIP_CHECK(hipStreamWaitEvent(S.lane(lane), ev_red1[c], 0), "hipStreamWaitEvent");
-        else if (lane != h_lane)
-            HIP_CHECK(hipStreamWaitEvent(S.lane(lane), ev[3], 0), "hipStreamWaitEvent");
+    // order, so chunk chunks-1 means all of H); fc1's single launch is
+    // ordered before fc2 on the compute stream already
+    auto wait_h = [&](int c) -> atp_status {
+        if (fc1_reduced) HIP_CHECK(hipStreamWaitEvent(S.cs, ev_red1[c], 0), "hipStreamWaitEvent");
         return ATP_OK;
     };
     auto unchunked = [&](int L) -> atp_status {
-        const atp_shard& g = P.g[L];
-        const int lane = S.take(gemm_flops(tokens, g.n_loc, g.k_loc));
-        hipStream_t s = S.lane(lane);
-        if (L == 3) ATP_CHECK(wait_h(lane, chunks - 1));
+        if (L == 3) ATP_CHECK(wait_h(chunks - 1));
         ATP_CHECK(need_wt(L));
         atp::GemmProblem p = fwd_problem(L, A_in[L], lda_in[L], outp[L], ldo[L], true,
                                          L == 2 ? atp::EPI_BIAS_GELU : atp::EPI_BIAS, tokens);
         p.bias = w->b[L];
         p.pre_out = (L == 2) ? io->pre : nullptr;
-        ATP_CHECK(run_gemm(p, s));
-        if (L == 2) {
-            HIP_CHECK(hipEventRecord(ev[3], s), "hipEventRecord");
-            h_lane = lane;
-        }
-        return ATP_OK;
+        return run_gemm(p, S.cs);
     };
     // chunk c: the GEMM writes this device's partial rows, the comm stream
     // reduces the group's partials for those rows as soon as they are ready
     auto chunk = [&](int L, int c) -> atp_status {
         const atp_shard& g = P.g[L];
-        const int lane = S.take(gemm_flops(mc, g.n_loc, g.k_loc));
-        hipStream_t s = S.lane(lane);
         const int64_t r0 = (int64_t)c * mc;
-        if (L == 3) ATP_CHECK(wait_h(lane, c));
+        if (L == 3) ATP_CHECK(wait_h(c));
         ATP_CHECK(need_wt(L));
-        float* own = io->partials[L][g.red_index];
+        void* own = io->partials[L][g.red_index];
         atp::GemmProblem p = fwd_problem(L, static_cast<const uint16_t*>(A_in[L]) + r0 * lda_in[L],
-                                         lda_in[L], own + r0 * io->ldp[L], io->ldp[L], false,
-                                         atp::EPI_NONE, mc);
-        ATP_CHECK(run_nt_partial(p, slab, s));
+                                         lda_in[L], row_ptr(own, r0, io->ldp[L], pb16),
+                                         io->ldp[L], pb16, atp::EPI_NONE, mc);
+        ATP_CHECK(run_nt_partial(p, slab, S.cs));
         hipEvent_t e = ev_gemm[L * chunks + c];
-        HIP_CHECK(hipEventRecord(e, s), "hipEventRecord");
+        HIP_CHECK(hipEventRecord(e, S.cs), "hipEventRecord");
         HIP_CHECK(hipStreamWaitEvent(S.ms, e, 0), "hipStreamWaitEvent");
         atp::ReduceProblem r = reduce_problem(
             g.red_size, io->partials[L], io->ldp[L], r0, mc, g.n_loc,
             L == 2 ? atp::EPI_BIAS_GELU : atp::EPI_BIAS, w->b[L], nullptr, outp[L], ldo[L], true,
-            L == 2 ? io->pre : nullptr);
+            L == 2 ? io->pre : nullptr, pb16);
         ATP_CHECK(run_reduce(r, S.ms));
         if (L == 2) HIP_CHECK(hipEventRecord(ev_red1[c], S.ms), "hipEventRecord");
         return ATP_OK;
@@ -996,18 +1094,22 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
 atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t tokens, int64_t h,
                          int32_t chunks, const atp_block_weights* w, const atp_block_bwd_io* io,
                          void* workspace, size_t ws_bytes, void* compute_stream,
-                         void* comm_stream, void* aux_stream) {
+                         void* comm_stream) {
     BlockPlan P;
     ATP_CHECK(check_mesh(mesh));
     ATP_CHECK(block_plan(mesh, block_mode, h, &P));
     ATP_CHECK(check_chunks(tokens, chunks));
     if (!w || !io) return set_error(ATP_ERR_INVALID_ARGUMENT, "weights or io is NULL");
+    ATP_CHECK(check_weights(P, w));
+    ATP_CHECK(check_partial_dtype(io->partial_dtype));
+    const bool kn = w->layout == ATP_W_KN;
+    const bool pb16 = io->partial_dtype == ATP_BF16;
     for (int i = 0; i < 4; ++i) {
         char nm[32];
-        snprintf(nm, sizeof nm, "w[%s]", kLinearName[i]);
-        ATP_CHECK(check_mat(w->w[i], P.g[i].k_loc, w->ldw[i], P.g[i].n_loc, nm));
+        const atp_shard& g = P.g[i];
         snprintf(nm, sizeof nm, "dw[%s]", kLinearName[i]);
-        ATP_CHECK(check_mat(io->dw[i], P.g[i].k_loc, w->ldw[i], P.g[i].n_loc, nm));
+        ATP_CHECK(check_mat(io->dw[i], kn ? g.k_loc : g.n_loc, w->ldw[i], kn ? g.n_loc : g.k_loc,
+                            nm));
         if (io->db[i]) {
             snprintf(nm, sizeof nm, "db[%s]", kLinearName[i]);
             ATP_CHECK(check_vec(io->db[i], nm));
@@ -1032,21 +1134,21 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         ATP_CHECK(check_group(io->dx_partials[i], P.g[i].bwd_size, tokens, io->ld_dxp[i], P.g[i].k_loc,
                               nm));
     }
-
-    // with a large enough workspace (and whole 16-byte rows of tokens) dW runs
-    // from X^T and dY^T (both contiguous along the tokens), and chunked dX
-    // products with too few tiles to fill the chip are split over k into
-    // slabs there
-    const bool ws = workspace && ws_bytes >= ws_bwd_bytes(P, tokens) && tokens % 8 == 0;
     if (workspace && reinterpret_cast<uintptr_t>(workspace) % kWsAlign)
         return set_error(ATP_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kWsAlign);
-    if (!workspace) ATP_CHECK(refuse_capture_without_workspace(compute_stream));
+
+    // With a large enough workspace (and whole 16-byte rows of tokens) dW runs
+    // from X^T and dY^T (both contiguous along the tokens), dX from W stored
+    // [k][n] (a copy in the workspace for weights stored [n][k]), and chunked
+    // dX products with too few tiles to fill the chip are split over k into
+    // slabs there.  The direct path never runs under graph capture.
+    const bool ws = workspace && takes_ws_path(P, tokens, w->layout, ws_bytes, 1);
+    if (!ws) ATP_CHECK(refuse_capture_of_direct_path(compute_stream));
 
     Streams S(compute_stream, comm_stream);
-    (void)aux_stream;   // unused: every GEMM runs on compute_stream
     hipEvent_t* ev = nullptr;
-    // [0] start  [1] comm end  [2] unused  [3] fc2's single dX launch done,
-    // then per linear per chunk GEMM-done, then fc2 reduce-done per chunk
+    // [0] start  [1] comm end  [2..3] unused, then per linear per chunk
+    // GEMM-done, then fc2 reduce-done per chunk
     const size_t n_ev = 4 + 4 * (size_t)chunks + (size_t)chunks;
     ATP_CHECK(sync_events(n_ev, &ev));
     hipEvent_t* ev_gemm = ev + 4;
@@ -1057,6 +1159,7 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     const int xsrc[4] = {0, 1, 0, 2};
     uint16_t* xt[3] = {nullptr, nullptr, nullptr};
     uint16_t* dyt[4] = {nullptr, nullptr, nullptr, nullptr};
+    uint16_t* wkn = nullptr;    // [k][n] copy of a weight stored [n][k]
     bool xt_done[3] = {false, false, false};
     float* slab = nullptr;
     float* colpart = nullptr;   // db of the workspace path: dY^T's transpose writes partials
@@ -1069,6 +1172,7 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         for (int L = 0; L < 4; ++L) dyt[L] = c.take(P.g[L].n_loc * t2);
         slab = reinterpret_cast<float*>(c.take(slab_bytes(P, tokens, true)));
         colpart = reinterpret_cast<float*>(c.take(colpart_bytes(P, tokens)));
+        if (!kn) wkn = c.take(wkn_bytes(P));
     }
 
     const int64_t mc = tokens / chunks;
@@ -1079,54 +1183,64 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     void* dXo[4] = {io->dx_qkv, io->d_attn, io->dx_fc1, io->dh_pre};
     const int64_t ld_dxo[4] = {io->ld_dx_qkv, io->ld_d_attn, io->ld_dx_fc1, io->ld_h};
     const bool fc2_reduced = P.g[3].bwd_size > 1;
-    int dpre_lane = 0;  // lane of fc2's single dX launch
 
     // fc1's dY is dh_pre: wait for fc2's reduced chunk c (chunk chunks-1
-    // means all of it, the comm stream runs in order), or for fc2's single
-    // dX launch
-    auto wait_dpre = [&](int lane, int c) -> atp_status {
-        if (fc2_reduced)
-            HIP_CHECK(hipStreamWaitEvent(S.lane(lane), ev_red2[c], 0), "hipStreamWaitEvent");
-        else if (lane != dpre_lane)
-            HIP_CHECK(hipStreamWaitEvent(S.lane(lane), ev[3], 0), "hipStreamWaitEvent");
+    // means all of it, the comm stream runs in order); fc2's single dX
+    // launch is ordered before fc1 on the compute stream already
+    auto wait_dpre = [&](int c) -> atp_status {
+        if (fc2_reduced) HIP_CHECK(hipStreamWaitEvent(S.cs, ev_red2[c], 0), "hipStreamWaitEvent");
+        return ATP_OK;
+    };
+    // the product dY W^T of linear L: NT from W stored [k][n] (or its copy),
+    // or NN from W stored [n][k] without a workspace
+    int wkn_of = -1;   // the linear whose weight the [k][n] copy holds
+    auto dx_problem = [&](int L, const void* A, int64_t lda, void* C, int64_t ldc, bool b16,
+                          int epi, int64_t M) -> atp::GemmProblem {
+        const atp_shard& g = P.g[L];
+        if (kn)
+            return gemm_problem(atp::LAYOUT_NT, A, lda, w->w[L], w->ldw[L], C, ldc, b16, epi, M,
+                                g.k_loc, g.n_loc);
+        if (ws)
+            return gemm_problem(atp::LAYOUT_NT, A, lda, wkn, ws_pitch(g.n_loc), C, ldc, b16, epi,
+                                M, g.k_loc, g.n_loc);
+        return gemm_problem(atp::LAYOUT_NN, A, lda, w->w[L], w->ldw[L], C, ldc, b16, epi, M,
+                            g.k_loc, g.n_loc);
+    };
+    auto need_wkn = [&](int L) -> atp_status {
+        if (kn || !ws || wkn_of == L) return ATP_OK;
+        const atp_shard& g = P.g[L];
+        ATP_CHECK(run_transpose(w->w[L], w->ldw[L], g.n_loc, g.k_loc, wkn, ws_pitch(g.n_loc),
+                                S.cs));
+        wkn_of = L;
         return ATP_OK;
     };
     auto dx_unchunked = [&](int L) -> atp_status {
         const atp_shard& g = P.g[L];
-        const int lane = S.take(gemm_flops(tokens, g.k_loc, g.n_loc));
-        hipStream_t s = S.lane(lane);
-        if (L == 2) ATP_CHECK(wait_dpre(lane, chunks - 1));
-        atp::GemmProblem p = gemm_problem(atp::LAYOUT_NT, dY[L], ld_dy[L], w->w[L], w->ldw[L],
-                                          dXo[L], ld_dxo[L], true,
-                                          L == 3 ? atp::EPI_GELU_BWD : atp::EPI_NONE, tokens,
-                                          g.k_loc, g.n_loc);
+        if (L == 2) ATP_CHECK(wait_dpre(chunks - 1));
+        ATP_CHECK(need_wkn(L));
+        atp::GemmProblem p = dx_problem(L, dY[L], ld_dy[L], dXo[L], ld_dxo[L], true,
+                                        L == 3 ? atp::EPI_GELU_BWD : atp::EPI_NONE, tokens);
         p.pre_in = (L == 3) ? io->pre : nullptr;
-        ATP_CHECK(run_gemm(p, s));
-        if (L == 3) {
-            HIP_CHECK(hipEventRecord(ev[3], s), "hipEventRecord");
-            dpre_lane = lane;
-        }
-        return ATP_OK;
+        (void)g;
+        return run_gemm(p, S.cs);
     };
     auto dx_chunk = [&](int L, int c) -> atp_status {
         const atp_shard& g = P.g[L];
-        const int lane = S.take(gemm_flops(mc, g.k_loc, g.n_loc));
-        hipStream_t s = S.lane(lane);
         const int64_t r0 = (int64_t)c * mc;
-        if (L == 2) ATP_CHECK(wait_dpre(lane, c));
-        float* own = io->dx_partials[L][g.bwd_index];
-        atp::GemmProblem p = gemm_problem(
-            atp::LAYOUT_NT, static_cast<const uint16_t*>(dY[L]) + r0 * ld_dy[L], ld_dy[L],
-            w->w[L], w->ldw[L], own + r0 * io->ld_dxp[L], io->ld_dxp[L], false, atp::EPI_NONE,
-            mc, g.k_loc, g.n_loc);
-        ATP_CHECK(run_nt_partial(p, slab, s));
+        if (L == 2) ATP_CHECK(wait_dpre(c));
+        ATP_CHECK(need_wkn(L));
+        void* own = io->dx_partials[L][g.bwd_index];
+        atp::GemmProblem p = dx_problem(L, static_cast<const uint16_t*>(dY[L]) + r0 * ld_dy[L],
+                                        ld_dy[L], row_ptr(own, r0, io->ld_dxp[L], pb16),
+                                        io->ld_dxp[L], pb16, atp::EPI_NONE, mc);
+        ATP_CHECK(run_nt_partial(p, slab, S.cs));
         hipEvent_t e = ev_gemm[L * chunks + c];
-        HIP_CHECK(hipEventRecord(e, s), "hipEventRecord");
+        HIP_CHECK(hipEventRecord(e, S.cs), "hipEventRecord");
         HIP_CHECK(hipStreamWaitEvent(S.ms, e, 0), "hipStreamWaitEvent");
         atp::ReduceProblem r = reduce_problem(
             g.bwd_size, io->dx_partials[L], io->ld_dxp[L], r0, mc, g.k_loc,
             L == 3 ? atp::EPI_GELU_BWD : atp::EPI_NONE, nullptr, L == 3 ? io->pre : nullptr,
-            dXo[L], ld_dxo[L], true, nullptr);
+            dXo[L], ld_dxo[L], true, nullptr, pb16);
         ATP_CHECK(run_reduce(r, S.ms));
         if (L == 3) HIP_CHECK(hipEventRecord(ev_red2[c], S.ms), "hipEventRecord");
         return ATP_OK;
@@ -1136,37 +1250,43 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         for (int c = 0; c < chunks; ++c) ATP_CHECK(dx_chunk(L, c));
         return ATP_OK;
     };
-    // db (column sums of dY), then dW = X^T dY over all tokens; these need
-    // no reduction and fill the lanes while the dX reductions drain
+    // db (column sums of dY), then dW = X^T dY over all tokens (stored as
+    // dW^T = dY^T X for weights stored [n][k]); these need no reduction and
+    // run while the dX reductions drain
     auto dw = [&](int L) -> atp_status {
         const atp_shard& g = P.g[L];
-        const int lane = S.take(gemm_flops(g.k_loc, g.n_loc, tokens));
-        hipStream_t s = S.lane(lane);
-        if (L == 2) ATP_CHECK(wait_dpre(lane, chunks - 1));
-        if (io->db[L] && !ws) ATP_CHECK(run_colsum(dY[L], ld_dy[L], tokens, g.n_loc, io->db[L], s));
+        if (L == 2) ATP_CHECK(wait_dpre(chunks - 1));
+        if (io->db[L] && !ws)
+            ATP_CHECK(run_colsum(dY[L], ld_dy[L], tokens, g.n_loc, io->db[L], S.cs));
         if (!ws) {
-            atp::GemmProblem p = gemm_problem(atp::LAYOUT_TN, Xin[L], ldx_in[L], dY[L], ld_dy[L],
-                                              io->dw[L], w->ldw[L], false, atp::EPI_NONE,
-                                              g.k_loc, g.n_loc, tokens);
-            return run_gemm(p, s);
+            atp::GemmProblem p =
+                kn ? gemm_problem(atp::LAYOUT_TN, Xin[L], ldx_in[L], dY[L], ld_dy[L], io->dw[L],
+                                  w->ldw[L], false, atp::EPI_NONE, g.k_loc, g.n_loc, tokens)
+                   : gemm_problem(atp::LAYOUT_TN, dY[L], ld_dy[L], Xin[L], ldx_in[L], io->dw[L],
+                                  w->ldw[L], false, atp::EPI_NONE, g.n_loc, g.k_loc, tokens);
+            return run_gemm(p, S.cs);
         }
-        // X^T once per source (x serves QKV and fc1), dY^T, then dW = X^T dY
-        // as an NT product over the tokens
+        // X^T once per source (x serves QKV and fc1), dY^T, then the NT
+        // product over the tokens
         const int xi = xsrc[L];
         const int64_t tp = ws_pitch(tokens);
         if (!xt_done[xi]) {
-            ATP_CHECK(run_transpose(Xin[L], ldx_in[L], tokens, g.k_loc, xt[xi], tp, s));
+            ATP_CHECK(run_transpose(Xin[L], ldx_in[L], tokens, g.k_loc, xt[xi], tp, S.cs));
             xt_done[xi] = true;
         }
         // dY^T, and with it the column partials of dY for db (one read of dY)
         float* part = io->db[L] ? colpart : nullptr;
-        ATP_CHECK(run_transpose(dY[L], ld_dy[L], tokens, g.n_loc, dyt[L], tp, s, part, g.n_loc));
+        ATP_CHECK(run_transpose(dY[L], ld_dy[L], tokens, g.n_loc, dyt[L], tp, S.cs, part,
+                                g.n_loc));
         if (part)
-            ATP_CHECK(run_colsum_finish(part, g.n_loc, (tokens + 63) / 64, g.n_loc, io->db[L], s));
-        atp::GemmProblem p = gemm_problem(atp::LAYOUT_NT, xt[xi], tp, dyt[L], tp, io->dw[L],
-                                          w->ldw[L], false, atp::EPI_NONE, g.k_loc, g.n_loc,
-                                          tokens);
-        return run_gemm(p, s);
+            ATP_CHECK(run_colsum_finish(part, g.n_loc, (tokens + 63) / 64, g.n_loc, io->db[L],
+                                        S.cs));
+        atp::GemmProblem p =
+            kn ? gemm_problem(atp::LAYOUT_NT, xt[xi], tp, dyt[L], tp, io->dw[L], w->ldw[L], false,
+                              atp::EPI_NONE, g.k_loc, g.n_loc, tokens)
+               : gemm_problem(atp::LAYOUT_NT, dyt[L], tp, xt[xi], tp, io->dw[L], w->ldw[L], false,
+                              atp::EPI_NONE, g.n_loc, g.k_loc, tokens);
+        return run_gemm(p, S.cs);
     };
     // fc2's dX first (it makes dh_pre, which fc1 waits for); then the
     // attention projections' dX, whose reductions can start at once; then

@@ -572,9 +572,15 @@ bool nt_use_256(const GemmProblem& p) { return fills_waves(p, 256); }
 // 256 x 256 tiles would leave their last wave short and 320-wide ones do not
 // (measured: 4096 x 10240 x 20480 at 1289 TFLOP/s against 1208 for
 // 256 x 160; where 256 x 256 tiles fill their waves they are faster)
+// Buffer offsets are 32-bit and a resource covers at most 0x7fffff00 bytes:
+// the rows one tile copies from an operand contiguous along k (BM rows of A,
+// BN rows of B) must span less than that.
+constexpr int64_t kMaxSpan = 0x7fffff00;
+bool rows_fit(int64_t rows, int64_t ld) { return rows * ld * 2 <= kMaxSpan; }
+
 bool nt_use_320(const GemmProblem& p) {
     return p.layout == LAYOUT_NT && p.splits <= 1 && !fills_waves(p, 256) &&
-           fills_waves(p, 320);
+           fills_waves(p, 320) && rows_fit(320, p.ldb);
 }
 
 // Split-K plan of an NT product written to fp32: the S in 1..kMaxSplits
@@ -638,7 +644,8 @@ hipError_t launch_pp(const GemmProblem& p, hipStream_t s) {
 bool gemm_supported(int layout, int epi, bool out_bf16) {
     switch (layout) {
     case LAYOUT_NN:
-        return epi == EPI_NONE || epi == EPI_BIAS || epi == EPI_BIAS_GELU;
+        return epi == EPI_NONE || epi == EPI_BIAS || epi == EPI_BIAS_GELU ||
+               (out_bf16 && epi == EPI_GELU_BWD);
     case LAYOUT_NT:
         return epi == EPI_NONE ||
                (out_bf16 && (epi == EPI_GELU_BWD || epi == EPI_BIAS || epi == EPI_BIAS_GELU));
@@ -665,10 +672,10 @@ int nt_split_plan(int64_t M, int64_t N, int64_t K, int64_t* ksplit) {
 
 hipError_t launch_gemm(const GemmProblem& p, hipStream_t s) {
     if (p.M <= 0 || p.N <= 0) return hipSuccess;
-    // buffer offsets are 32-bit: one tile's rows of either operand must span < 2 GiB
-    const int64_t span = (int64_t)256 *
-                         (p.lda > p.ldb ? p.lda : p.ldb) * 2;
-    if (span > 0x7fffff00) return hipErrorInvalidValue;
+    // buffer offsets are 32-bit: one tile's rows of either operand must span
+    // < 2 GiB (256 rows covers the 160- and 256-wide tiles and the 64 k rows
+    // of a row-contiguous operand; nt_use_320 checks its 320 rows itself)
+    if (!rows_fit(256, p.lda) || !rows_fit(256, p.ldb)) return hipErrorInvalidValue;
     const bool b16 = p.out_bf16;
     if (p.nparts > kMaxFusedParts || (p.nparts > 1 && (p.splits > 1 || p.own < 0 ||
                                                        p.own >= p.nparts || p.ldp % 4)))
@@ -692,6 +699,9 @@ hipError_t launch_gemm(const GemmProblem& p, hipStream_t s) {
         case EPI_BIAS_GELU:
             return b16 ? launch_pp<true, false, EPI_BIAS_GELU, true>(p, s)
                        : launch_pp<true, false, EPI_BIAS_GELU, false>(p, s);
+        case EPI_GELU_BWD:   // dY W^T with W stored [n][k], times GeLU'(pre)
+            if (b16) return launch_pp<true, false, EPI_GELU_BWD, true>(p, s);
+            return hipErrorInvalidValue;
         default:
             return hipErrorInvalidValue;
         }

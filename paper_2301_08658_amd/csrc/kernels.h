@@ -72,10 +72,11 @@ struct ReduceProblem {
 hipError_t launch_reduce(const ReduceProblem& p, hipStream_t s);
 
 // out[r*ldo + c] = sum_{s<S} slab_s[r*ld + c] for slab_s = ws + s*stride,
-// r < rows, c < cols (fp32, summed in s order): the split-K partials of one
-// product combined into one partial.
+// r < rows, c < cols (fp32, summed in s order; stored fp32, or bf16 rounded
+// to nearest even): the split-K partials of one product combined into one
+// partial.
 hipError_t launch_split_sum(const float* ws, int S, int64_t stride, int64_t ld, int64_t rows,
-                            int64_t cols, float* out, int64_t ldo, hipStream_t s);
+                            int64_t cols, void* out, int64_t ldo, bool out_bf16, hipStream_t s);
 
 // Causal attention of `heads` consecutive heads over `batch` sequences of
 // `seq` tokens (token rows sequence-major).  Head j's q, k, v are the

@@ -243,8 +243,8 @@ hipError_t launch_reduce(const ReduceProblem& p, hipStream_t s) {
 }
 
 hipError_t launch_split_sum(const float* ws, int S, int64_t stride, int64_t ld, int64_t rows,
-                            int64_t cols, float* out, int64_t ldo, hipStream_t s) {
-    if (S < 1 || S > kMaxParts || (cols & 7) || (ld & 3) || (ldo & 3))
+                            int64_t cols, void* out, int64_t ldo, bool out_bf16, hipStream_t s) {
+    if (S < 1 || S > kMaxParts || (cols & 7) || (ld & 3) || (ldo & (out_bf16 ? 7 : 3)))
         return hipErrorInvalidValue;
     ReduceProblem p{};
     p.nparts = S;
@@ -256,7 +256,7 @@ hipError_t launch_split_sum(const float* ws, int S, int64_t stride, int64_t ld, 
     p.epi = EPI_NONE;
     p.out = out;
     p.ldo = ldo;
-    p.out_bf16 = false;
+    p.out_bf16 = out_bf16;
     return launch_reduce(p, s);
 }
 

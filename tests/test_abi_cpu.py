@@ -220,7 +220,7 @@ def test_block_validation():
 
     def call(mm=m, bm=0, tokens=T, hh=h, chunks=2):
         return lib.atp_block_fwd(ctypes.byref(mm), bm, tokens, hh, chunks, ctypes.byref(W),
-                                 ctypes.byref(io), None, 0, None, None, None)
+                                 ctypes.byref(io), None, 0, None, None)
     assert call(bm=5) == B.ATP_ERR_INVALID_ARGUMENT
     assert call(hh=500) == B.ATP_ERR_UNSUPPORTED or call(hh=500) == B.ATP_ERR_SHAPE
     assert call(chunks=3) == B.ATP_ERR_SHAPE
@@ -234,7 +234,7 @@ def test_block_validation():
     W.b[2] = FAKE
     io.ld_h = G[2].n_loc - 8
     assert call() == B.ATP_ERR_INVALID_ARGUMENT
-    assert lib.atp_block_workspace_bytes(ctypes.byref(m), 0, T, h, 2) > 0
+    assert lib.atp_block_workspace_bytes(ctypes.byref(m), 0, T, h, 2, 0) > 0
 
 
 def test_status_strings():
@@ -274,3 +274,161 @@ def test_block_workspace_bytes_formula():
     # invalid arguments give 0
     assert B.atp_block_workspace_bytes(B.mesh(2, 2, 0, 0), 7, 128, 512, 1) == 0
     assert B.atp_block_workspace_bytes(B.mesh(2, 2, 0, 0), 0, 128, 500, 1) == 0
+
+
+def test_block_workspace_path_decides_the_capture_refusal():
+    """atp_block_workspace_path is the decision the block calls take: the
+    transposed-layout path needs the pass's whole workspace (and, for the
+    backward, tokens % 8 == 0); everything else is the direct path, which the
+    calls refuse under HIP graph capture."""
+    m = B.mesh(2, 2, 1, 0)
+    h = 512
+    for layout in (B.ATP_W_KN, B.ATP_W_NK):
+        for T in (256, 132):
+            full = B.atp_block_workspace_bytes(m, 0, T, h, 2, layout)
+            assert full > 0 and full % 256 == 0
+            for p in (0, 1):
+                path = lambda n: B.atp_block_workspace_path(m, 0, T, h, layout, n, p)  # noqa
+                ok_tokens = p == 0 or T % 8 == 0
+                assert path(full) == (1 if ok_tokens else 0)
+                assert path(0) == 0                      # no workspace: direct
+                if ok_tokens:
+                    need = _least_size(m, 0, T, h, layout, p, full)
+                    assert need % 256 == 0 and path(need - 1) == 0 and path(need) == 1
+    assert B.atp_block_workspace_path(m, 0, 256, h, 7, 1 << 20, 0) == -1      # bad layout
+    assert B.atp_block_workspace_path(m, 0, 256, h, 0, 1 << 20, 2) == -1      # bad pass
+    assert B.atp_block_workspace_path(B.mesh(2, 2, 2, 0), 0, 256, h, 0, 1, 0) == -1
+
+
+def _least_size(m, mode, T, h, layout, pass_, hi):
+    """The least workspace size that takes the pass's transposed-layout path
+    (binary search over the library's own decision; 0 if even `hi` does not)."""
+    path = lambda n: B.atp_block_workspace_path(m, mode, T, h, layout, n, pass_)  # noqa: E731
+    if path(hi) != 1:
+        return 0
+    lo = 0                      # path(lo) == 0 (no workspace is the direct path)
+    while hi - lo > 1:
+        mid = (lo + hi) // 2
+        if path(mid) == 1:
+            hi = mid
+        else:
+            lo = mid
+    return hi
+
+
+def test_block_workspace_weight_layouts():
+    """Weights stored [n][k] need no W^T in the forward, and one [k][n] copy
+    of the largest weight (rows padded by 64 values) in the backward."""
+    r = lambda b: (b + 255) // 256 * 256  # noqa: E731
+    for (d1, d2), mode, T, h in [((8, 1), 0, 4096, 20480), ((2, 4), 1, 8192, 4096),
+                                 ((2, 2), 0, 256, 512)]:
+        m = B.mesh(d1, d2, 0, 0)
+        G = B.block_geometry(m, mode, h)
+        kn = B.atp_block_workspace_bytes(m, mode, T, h, 1, B.ATP_W_KN)
+        nk = B.atp_block_workspace_bytes(m, mode, T, h, 1, B.ATP_W_NK)
+        wkn = r(max(g.k_loc * (g.n_loc + 64) * 2 for g in G))
+        fwd_wt = sum(r((g.k_loc + 64) * g.n_loc * 2) for g in G)
+        assert (_least_size(m, mode, T, h, B.ATP_W_NK, 1, nk) -
+                _least_size(m, mode, T, h, B.ATP_W_KN, 1, kn)) == wkn
+        assert (_least_size(m, mode, T, h, B.ATP_W_KN, 0, kn) -
+                _least_size(m, mode, T, h, B.ATP_W_NK, 0, nk)) == fwd_wt
+    assert B.atp_block_workspace_bytes(B.mesh(2, 2, 0, 0), 0, 128, 512, 1, 5) == 0
+
+
+def test_block_geometry_export_matches_per_linear_geometry():
+    lib = atp.load_library()
+    for (d1, d2) in [(2, 2), (2, 4), (4, 2), (8, 1), (1, 8)]:
+        for i1, i2 in itertools.product(range(d1), range(d2)):
+            m = atp.mesh(d1, d2, i1, i2)
+            for bm, modes in ((B.ATP_BLOCK_COL, (1, 0, 1, 0)), (B.ATP_BLOCK_ROW, (0, 1, 0, 1))):
+                G = B.block_geometry(m, bm, 1024)
+                for g, md, (k, n) in zip(G, modes, ((1024, 3072), (1024, 1024), (1024, 4096),
+                                                    (4096, 1024))):
+                    assert g.as_dict() == atp.atp_shard_geometry(m, md, k, n).as_dict()
+    out = (B.atp_shard * 4)()
+    m = atp.mesh(2, 2, 0, 0)
+    assert lib.atp_block_geometry(ctypes.byref(m), 0, 1024, None) == B.ATP_ERR_INVALID_ARGUMENT
+    assert lib.atp_block_geometry(ctypes.byref(m), 3, 1024, out) == B.ATP_ERR_INVALID_ARGUMENT
+    assert lib.atp_block_geometry(ctypes.byref(m), 0, 1001, out) == B.ATP_ERR_SHAPE
+    assert lib.atp_block_geometry(ctypes.byref(m), 0, 1000, out) == B.ATP_ERR_UNSUPPORTED
+
+
+def test_attention_heads_export_matches_oracle():
+    """The device's run of heads equals the oracle's scatter of the QKV
+    block's heads over its reduction group (Sec. 3.2.1)."""
+    h, heads = 2048, 16
+    for (d1, d2) in [(2, 2), (2, 4), (4, 2), (8, 1), (1, 4)]:
+        for bm in (B.ATP_BLOCK_COL, B.ATP_BLOCK_ROW):
+            for i1, i2 in itertools.product(range(d1), range(d2)):
+                m = atp.mesh(d1, d2, i1, i2)
+                g = B.block_geometry(m, bm, h)[0]
+                first, count, per_block = B.attention_heads(m, bm, h, heads)
+                assert per_block * 3 * 128 == g.n_loc
+                lo, n = O.attention_heads(g.n_loc, 128, g.red_size, g.red_index)
+                assert (first, count) == (lo, n)
+    lib = atp.load_library()
+    m = atp.mesh(2, 2, 0, 0)
+    i = ctypes.c_int32()
+    assert lib.atp_attention_heads(ctypes.byref(m), 0, 2048, 16, None, ctypes.byref(i),
+                                   ctypes.byref(i)) == B.ATP_ERR_INVALID_ARGUMENT
+    assert lib.atp_attention_heads(ctypes.byref(m), 0, 2048, 15, ctypes.byref(i), ctypes.byref(i),
+                                   ctypes.byref(i)) == B.ATP_ERR_SHAPE
+    assert lib.atp_attention_heads(ctypes.byref(m), 0, 2048, 32, ctypes.byref(i), ctypes.byref(i),
+                                   ctypes.byref(i)) == B.ATP_ERR_UNSUPPORTED   # head dim 64
+
+
+def test_block_option_validation():
+    """An unknown weight layout or partial dtype is refused before any work."""
+    lib = atp.load_library()
+    h, T = 512, 256
+    m = atp.mesh(2, 2, 0, 1)
+    G = atp.block_geometry(m, B.ATP_BLOCK_COL, h)
+    W = B.atp_block_weights()
+    for i, g in enumerate(G):
+        W.w[i], W.ldw[i], W.b[i] = FAKE, g.n_loc, FAKE
+    io = B.atp_block_fwd_io()
+    io.x_loc, io.ldx = FAKE, G[0].k_loc
+    io.attn_loc, io.lda = FAKE, G[1].k_loc
+    io.qkv, io.ld_qkv = FAKE, G[0].n_loc
+    io.o, io.ld_o = FAKE, G[1].n_loc
+    io.h, io.ld_h = FAKE, G[2].n_loc
+    io.pre = FAKE
+    io.z, io.ld_z = FAKE, G[3].n_loc
+
+    def call():
+        return lib.atp_block_fwd(ctypes.byref(m), 0, T, h, 2, ctypes.byref(W), ctypes.byref(io),
+                                 None, 0, None, None)
+    W.layout = 2
+    assert call() == B.ATP_ERR_INVALID_ARGUMENT and "layout" in atp.binding.last_error()
+    W.layout = B.ATP_W_NK          # [n][k] weights: ld 128 < k_loc 256
+    assert call() == B.ATP_ERR_INVALID_ARGUMENT and "w[" in atp.binding.last_error()
+    W.layout = B.ATP_W_KN
+    io.partial_dtype = 3
+    assert call() == B.ATP_ERR_INVALID_ARGUMENT and "partial_dtype" in atp.binding.last_error()
+
+
+def test_binding_refuses_host_tensors_and_short_scratch():
+    """A host tensor, or an lse / delta buffer smaller than the device's
+    heads need, is refused by the binding before the library is called."""
+    import torch
+    m = atp.mesh(2, 2, 0, 0)
+    T, h, heads = 256, 1024, 8
+    _, hd, _ = atp.attention_heads(m, 0, h, heads)
+    g = atp.block_geometry(m, 0, h)[0]
+    qkv = torch.zeros((T, g.n_loc), dtype=torch.bfloat16)
+    out = torch.zeros((T, g.n_loc // 3), dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="lse"):
+        atp.atp_attention_fwd(m, 0, 1, T, h, heads, qkv, out,
+                              torch.zeros(hd * T - 1, dtype=torch.float32))
+    with pytest.raises(ValueError, match="delta"):
+        atp.atp_attention_bwd(m, 0, 1, T, h, heads, qkv, out,
+                              torch.zeros(hd * T, dtype=torch.float32), out, qkv,
+                              torch.zeros(hd * T - 8, dtype=torch.float32))
+    with pytest.raises(ValueError, match="on the GPU"):
+        atp.atp_attention_fwd(m, 0, 1, T, h, heads, qkv, out,
+                              torch.zeros(hd * T, dtype=torch.float32))
+    with pytest.raises(ValueError, match="on the GPU"):
+        atp.atp_transpose_bf16(qkv, torch.zeros((g.n_loc, T), dtype=torch.bfloat16))
+    with pytest.raises(ValueError, match="on the GPU"):
+        atp.atp_chunked_partial_reduce(1, T, 8, 1, [torch.zeros((T, 8))], None, 0,
+                                       torch.zeros((T, 8)))

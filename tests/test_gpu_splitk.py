@@ -17,8 +17,8 @@ import torch
 
 import oracle as O
 import paper_2301_08658_amd as atp
-from helpers import LIN, assert_close, make_block_inputs, oracle_block_fwd, run_block_bwd, \
-    run_block_fwd, to64
+from helpers import (LIN, assert_close, check_bwd, check_fwd, make_block_inputs,
+                     oracle_block_bwd, oracle_block_fwd, run_block_bwd, run_block_fwd, to64)
 
 pytestmark = pytest.mark.gpu
 
@@ -29,17 +29,6 @@ CASES = [("col", (2, 2), (1, 0), 256, 2000, 2),
          ("row", (2, 2), (0, 1), 256, 2000, 2),
          ("col", (2, 4), (1, 2), 1024, 2048, 2)]
 IDS = [f"{c[0]}{c[1][0]}x{c[1][1]}_h{c[4]}" for c in CASES]
-
-
-def _oracle_bwd(inp):
-    bm = O.BLOCK_COL if inp["mode"] == "col" else O.BLOCK_ROW
-    cpu = lambda t: t.detach().cpu()  # noqa: E731
-    coord = (inp["m"].i1, inp["m"].i2)
-    w = {n: cpu(inp["w"][i]) for i, n in enumerate(LIN)}
-    peers = {n: [cpu(p) for p in inp["dx_peers"][i]] for i, n in enumerate(LIN)}
-    return O.block_bwd_local(bm, inp["m"], coord, cpu(inp["x"]), cpu(inp["a"]),
-                             cpu(inp["hs"]), cpu(inp["pres"]), w,
-                             cpu(inp["dz"]), cpu(inp["dqkv"]), cpu(inp["do"]), peers)
 
 
 def _profiled_names(fn):
@@ -76,13 +65,11 @@ def test_split_forward_matches_oracle(case):
     inp = make_block_inputs(mode, mesh, coord, T, h, 0.02, seed=42)
     out = run_block_fwd(inp, chunks, workspace=True)
     torch.cuda.synchronize()
-    ref = oracle_block_fwd(O, inp)
-    for key in ("qkv", "o", "h", "pre", "z"):
-        assert_close(out[key], ref[key], key)
+    check_fwd(out, *oracle_block_fwd(O, inp), what="split")
     for i, g in enumerate(inp["G"][:3]):
         if g.red_size > 1:
             xin = inp["a"] if i == 1 else inp["x"]
-            assert_close(out["own"][i], O.matmul(xin.cpu(), inp["w"][i].cpu()),
+            assert_close(out["own"][i], O.matmul(xin.cpu(), inp["wkn"][i].cpu()),
                          f"own partial {LIN[i]}")
 
 
@@ -93,13 +80,7 @@ def test_split_backward_matches_oracle(case):
     inp = make_block_inputs(mode, mesh, coord, T, h, 0.02, seed=43, bwd=True)
     out = run_block_bwd(inp, chunks, workspace=True)
     torch.cuda.synchronize()
-    ref = _oracle_bwd(inp)
-    for key in ("dh_pre", "dx_qkv", "dx_fc1", "d_attn"):
-        assert_close(out[key], ref[{"d_attn": "da"}.get(key, key)], key)
-    for i, n in enumerate(LIN):
-        fl = "rms" if n == "fc1" else 1.0
-        assert_close(out["dw"][i], ref["dw_" + n], f"dw_{n}", floor=fl)
-        assert_close(out["db"][i], ref["db_" + n], f"db_{n}", floor=fl)
+    check_bwd(out, *oracle_block_bwd(O, inp), what="split")
 
 
 @pytest.mark.parametrize("case", CASES, ids=IDS)
@@ -112,12 +93,12 @@ def test_split_integer_partials_bit_exact(case):
     inp = make_block_inputs(mode, mesh, coord, T, h, 0.0, seed=44, integer=True)
     out = run_block_fwd(inp, chunks, workspace=True)
     torch.cuda.synchronize()
-    ref = oracle_block_fwd(O, inp)
+    ref, _ = oracle_block_fwd(O, inp)
     for i, g in enumerate(inp["G"][:3]):
         if g.red_size > 1:
             xin = inp["a"] if i == 1 else inp["x"]
             np.testing.assert_array_equal(to64(out["own"][i]),
-                                          O.matmul(xin.cpu(), inp["w"][i].cpu()),
+                                          O.matmul(xin.cpu(), inp["wkn"][i].cpu()),
                                           err_msg=f"own partial {LIN[i]}")
     for key in ("qkv", "o"):
         np.testing.assert_array_equal(to64(out[key]), O.round_bf16(ref[key]), err_msg=key)
