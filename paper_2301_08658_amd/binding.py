@@ -101,6 +101,33 @@ class atp_block_bwd_io(ctypes.Structure):
                 ("partial_dtype", ctypes.c_int32)]
 
 
+class atp_attn_block_fwd_io(ctypes.Structure):
+    _fields_ = [("x_loc", _vp), ("ldx", ctypes.c_int64),
+                ("qkv_partials", _fpp), ("ldp_qkv", ctypes.c_int64),
+                ("qkv", _vp), ("ld_qkv", ctypes.c_int64),
+                ("attn", _vp), ("ld_attn", ctypes.c_int64),
+                ("lse", _vp),
+                ("o_partials", _fpp), ("ldp_o", ctypes.c_int64),
+                ("o", _vp), ("ld_o", ctypes.c_int64),
+                ("partial_dtype", ctypes.c_int32)]
+
+
+class atp_attn_block_bwd_io(ctypes.Structure):
+    _fields_ = [("x_loc", _vp), ("ldx", ctypes.c_int64),
+                ("qkv", _vp), ("ld_qkv", ctypes.c_int64),
+                ("attn", _vp), ("ld_attn", ctypes.c_int64),
+                ("lse", _vp),
+                ("d_o", _vp), ("ld_do", ctypes.c_int64),
+                ("d_attn_partials", _fpp), ("ldp_da", ctypes.c_int64),
+                ("d_attn", _vp), ("ld_d_attn", ctypes.c_int64),
+                ("delta", _vp),
+                ("d_qkv", _vp), ("ld_dqkv", ctypes.c_int64),
+                ("dx_partials", _fpp), ("ldp_dx", ctypes.c_int64),
+                ("dx", _vp), ("ld_dx", ctypes.c_int64),
+                ("dw", _vp * 2), ("db", _vp * 2),
+                ("partial_dtype", ctypes.c_int32)]
+
+
 class atp_kernel_stat(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 64), ("launches", ctypes.c_int64),
                 ("total_ms", ctypes.c_double), ("flops", ctypes.c_double),
@@ -133,7 +160,7 @@ EXPORTS = (
     "atp_version", "atp_tcomm", "atp_hcm_mesh_cost", "atp_plan_mesh", "atp_transpose_bf16",
     "atp_attention_fwd", "atp_attention_bwd", "atp_chunked_partial_reduce_bf16",
     "atp_shard_linear_fwd_fused", "atp_block_workspace_path", "atp_block_geometry",
-    "atp_attention_heads",
+    "atp_attention_heads", "atp_attention_block_fwd", "atp_attention_block_bwd",
 )
 
 _lib = None
@@ -176,6 +203,14 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     i32p = ctypes.POINTER(i32)
     lib.atp_attention_heads.argtypes = [mp, i32, i64, i32, i32p, i32p, i32p]
     lib.atp_attention_heads.restype = i32
+    lib.atp_attention_block_fwd.argtypes = [mp, i32, i64, i64, i64, i32, i32,
+                                            ctypes.POINTER(atp_block_weights),
+                                            ctypes.POINTER(atp_attn_block_fwd_io), _vp, _vp]
+    lib.atp_attention_block_fwd.restype = i32
+    lib.atp_attention_block_bwd.argtypes = [mp, i32, i64, i64, i64, i32, i32,
+                                            ctypes.POINTER(atp_block_weights),
+                                            ctypes.POINTER(atp_attn_block_bwd_io), _vp, _vp]
+    lib.atp_attention_block_bwd.restype = i32
     lib.atp_block_fwd.argtypes = [mp, i32, i64, i64, i32, ctypes.POINTER(atp_block_weights),
                                   ctypes.POINTER(atp_block_fwd_io), _vp, sz, _vp, _vp]
     lib.atp_block_fwd.restype = i32
@@ -482,7 +517,9 @@ def _partial_dtype(tables) -> tuple:
     if len(dts) > 1:
         raise TypeError(f"partial buffers mix dtypes {sorted(map(str, dts))}")
     dt = dts.pop() if dts else torch.float32
-    return _dtype_code(dt), dt
+    if dt not in (torch.float32, torch.bfloat16):
+        raise TypeError(f"partial buffers must be float32 or bfloat16, not {dt}")
+    return (ATP_F32 if dt == torch.float32 else ATP_BF16), dt
 
 
 def _workspace(workspace):
@@ -654,6 +691,101 @@ def atp_attention_bwd(m: atp_mesh, block_mode: int, batch: int, seq: int, h: int
                                             int(h), int(heads), qp, ldq, op, ldo,
                                             _ptr(lse, "lse"), dop, lddo, dqp, lddq,
                                             _ptr(delta, "delta"), _stream(stream)))
+
+
+def _attn_weights(G, w, b, layout: int):
+    """Weights of QKV and out-proj (entries 0 and 1) for the attention block."""
+    W = atp_block_weights()
+    W.layout = int(layout)
+    for i in range(2):
+        g = G[i]
+        r, c = (g.k_loc, g.n_loc) if layout == ATP_W_KN else (g.n_loc, g.k_loc)
+        W.w[i], W.ldw[i] = _mat(w[i], r, c, torch.bfloat16, f"w[{LINEARS[i]}]")
+        W.b[i] = _vec(b[i], g.n_loc, torch.bfloat16, f"b[{LINEARS[i]}]")
+    return W
+
+
+def atp_attention_block_fwd(m: atp_mesh, block_mode: int, batch: int, seq: int, h: int,
+                            heads: int, chunks: int, w, b, x_loc, qkv_partials, qkv, attn, lse,
+                            o_partials, o, compute_stream=None, comm_stream=None,
+                            weight_layout: int = ATP_W_KN):
+    """The device's attention block: QKV -> its heads' attention -> out-proj.
+    w, b: [qkv, out] weights and biases; qkv_partials / o_partials: the
+    groups' buffers (own entry written) or None for a group of one; attn: the
+    gathered out-proj input, whose other members' columns must be filled."""
+    T = batch * seq
+    G = block_geometry(m, block_mode, h)
+    _, hd, _ = attention_heads(m, block_mode, h, heads)
+    _f32_scratch(lse, hd * T, "lse")
+    W = _attn_weights(G, w, b, weight_layout)
+    io = atp_attn_block_fwd_io()
+    io.partial_dtype, pdt = _partial_dtype([qkv_partials, o_partials])
+    io.x_loc, io.ldx = _mat(x_loc, T, G[0].k_loc, torch.bfloat16, "x_loc")
+    keep = []
+    for name, parts, g, attr in (("qkv_partials", qkv_partials, G[0], "qkv"),
+                                 ("o_partials", o_partials, G[1], "o")):
+        if g.red_size > 1:
+            if len(parts) != g.red_size:
+                raise ValueError(f"{name} needs {g.red_size} buffers")
+            tab, arr, ld = _ptr_table(parts, T, g.n_loc, name, pdt)
+            setattr(io, name, tab)
+            setattr(io, "ldp_" + attr, ld)
+            keep.append(arr)
+    io.qkv, io.ld_qkv = _mat(qkv, T, G[0].n_loc, torch.bfloat16, "qkv")
+    io.attn, io.ld_attn = _mat(attn, T, G[1].k_loc, torch.bfloat16, "attn")
+    io.lse = _ptr(lse, "lse")
+    io.o, io.ld_o = _mat(o, T, G[1].n_loc, torch.bfloat16, "o")
+    _check(load_library().atp_attention_block_fwd(
+        ctypes.byref(m), int(block_mode), int(batch), int(seq), int(h), int(heads), int(chunks),
+        ctypes.byref(W), ctypes.byref(io), _stream(compute_stream), _stream(comm_stream)))
+
+
+def atp_attention_block_bwd(m: atp_mesh, block_mode: int, batch: int, seq: int, h: int,
+                            heads: int, chunks: int, w, b, x_loc, qkv, attn, lse, d_o,
+                            d_attn_partials, d_attn, delta, d_qkv, dx_partials, dx, dw, db,
+                            compute_stream=None, comm_stream=None,
+                            weight_layout: int = ATP_W_KN):
+    """Backward of atp_attention_block_fwd.  d_qkv: the QKV block's
+    gradient, whose other members' columns must be filled; dw, db: [qkv, out]
+    (dw in the weights' layout, db entries may be None)."""
+    T = batch * seq
+    G = block_geometry(m, block_mode, h)
+    _, hd, _ = attention_heads(m, block_mode, h, heads)
+    _f32_scratch(lse, hd * T, "lse")
+    _f32_scratch(delta, hd * T, "delta")
+    W = _attn_weights(G, w, b, weight_layout)
+    io = atp_attn_block_bwd_io()
+    io.partial_dtype, pdt = _partial_dtype([d_attn_partials, dx_partials])
+    io.x_loc, io.ldx = _mat(x_loc, T, G[0].k_loc, torch.bfloat16, "x_loc")
+    io.qkv, io.ld_qkv = _mat(qkv, T, G[0].n_loc, torch.bfloat16, "qkv")
+    io.attn, io.ld_attn = _mat(attn, T, G[1].k_loc, torch.bfloat16, "attn")
+    io.lse = _ptr(lse, "lse")
+    io.d_o, io.ld_do = _mat(d_o, T, G[1].n_loc, torch.bfloat16, "d_o")
+    keep = []
+    for name, parts, g, ldname in (("d_attn_partials", d_attn_partials, G[1], "ldp_da"),
+                                   ("dx_partials", dx_partials, G[0], "ldp_dx")):
+        if g.bwd_size > 1:
+            if len(parts) != g.bwd_size:
+                raise ValueError(f"{name} needs {g.bwd_size} buffers")
+            tab, arr, ld = _ptr_table(parts, T, g.k_loc, name, pdt)
+            setattr(io, name, tab)
+            setattr(io, ldname, ld)
+            keep.append(arr)
+    io.d_attn, io.ld_d_attn = _mat(d_attn, T, G[1].k_loc, torch.bfloat16, "d_attn")
+    io.delta = _ptr(delta, "delta")
+    io.d_qkv, io.ld_dqkv = _mat(d_qkv, T, G[0].n_loc, torch.bfloat16, "d_qkv")
+    io.dx, io.ld_dx = _mat(dx, T, G[0].k_loc, torch.bfloat16, "dx")
+    for i in range(2):
+        g = G[i]
+        r, c = (g.k_loc, g.n_loc) if weight_layout == ATP_W_KN else (g.n_loc, g.k_loc)
+        p, ld = _mat(dw[i], r, c, torch.float32, f"dw[{LINEARS[i]}]")
+        if ld != W.ldw[i]:
+            raise ValueError(f"dw[{LINEARS[i]}] must share the weight's leading dimension")
+        io.dw[i] = p
+        io.db[i] = _vec(db[i], g.n_loc, torch.float32, f"db[{LINEARS[i]}]") if db else None
+    _check(load_library().atp_attention_block_bwd(
+        ctypes.byref(m), int(block_mode), int(batch), int(seq), int(h), int(heads), int(chunks),
+        ctypes.byref(W), ctypes.byref(io), _stream(compute_stream), _stream(comm_stream)))
 
 
 # ---------------------------------------------------------------------------

@@ -432,3 +432,15 @@ def test_binding_refuses_host_tensors_and_short_scratch():
     with pytest.raises(ValueError, match="on the GPU"):
         atp.atp_chunked_partial_reduce(1, T, 8, 1, [torch.zeros((T, 8))], None, 0,
                                        torch.zeros((T, 8)))
+
+
+def test_binding_partial_dtype_of_tables():
+    import torch
+    f, h = torch.zeros(2), torch.zeros(2, dtype=torch.bfloat16)
+    assert B._partial_dtype([None, [f, None, f]]) == (B.ATP_F32, torch.float32)
+    assert B._partial_dtype([[h], None]) == (B.ATP_BF16, torch.bfloat16)
+    assert B._partial_dtype([None, None]) == (B.ATP_F32, torch.float32)
+    with pytest.raises(TypeError):
+        B._partial_dtype([[f], [h]])
+    with pytest.raises(TypeError):
+        B._partial_dtype([[torch.zeros(2, dtype=torch.float16)]])
