@@ -484,8 +484,9 @@ def reduce_alone(torch, atp, st, reps):
     rows = T // c
     tab = [p[:rows] for p in st["fwd_tabs"][L]]
     out = torch.empty((rows, g.n_loc), dtype=torch.bfloat16, device="cuda:0")
-    run = lambda: atp.atp_chunked_partial_reduce(len(tab), rows, g.n_loc, 1, tab, st["b"][L],  # noqa: E731
-                                                 atp.ATP_EPI_BIAS, out)
+    b16 = tab[0].dtype == torch.bfloat16
+    red = atp.atp_chunked_partial_reduce_bf16 if b16 else atp.atp_chunked_partial_reduce
+    run = lambda: red(len(tab), rows, g.n_loc, 1, tab, st["b"][L], atp.ATP_EPI_BIAS, out)  # noqa
     for _ in range(3):
         run()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -496,7 +497,7 @@ def reduce_alone(torch, atp, st, reps):
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / reps
-    nbytes = len(tab) * rows * g.n_loc * 4 + rows * g.n_loc * 2 + g.n_loc * 2
+    nbytes = len(tab) * rows * g.n_loc * (2 if b16 else 4) + rows * g.n_loc * 2 + g.n_loc * 2
     gbs = nbytes / (ms * 1e-3) / 1e9
     return dict(linear=LIN[L], red_size=len(tab), rows=rows, n_loc=g.n_loc,
                 avg_us=round(ms * 1e3, 2), achieved=round(gbs, 1), peak=PEAK_HBM_GBS,
@@ -522,6 +523,8 @@ def main():
     chunks = args.chunks or wl["chunks"]
     fwd_only = args.fwd_only or not wl.get("bwd", False)
     atp.load_library()
+    # a CU-masked stream needs a hardware queue of its own: made first
+    comm = cu_masked_stream(torch, args.comm_cus) if args.comm_cus else None
     if args.attention:
         attention_bench(torch, atp, S, args, wl)
         return
@@ -537,7 +540,6 @@ def main():
                                            st["layout"])
         st["ws"] = torch.empty(max(nb, 1), dtype=torch.uint8, device="cuda:0")
     torch.cuda.synchronize()
-    comm = cu_masked_stream(torch, args.comm_cus) if args.comm_cus else None
     step = make_step(torch, atp, st, fwd_only, args.serial, comm)
     flops = step_flops(st, fwd_only)
 

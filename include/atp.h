@@ -423,6 +423,87 @@ atp_status atp_attention_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t b
                              int64_t ld_dout, void* d_qkv, int64_t ld_dqkv, float* delta,
                              void* stream);
 
+/* The attention block of one device (Sec. 3.2.1, with Sec. 2.1 Formula
+ * (mha) as its core), chained: QKV (chunked, reduced with its bias over its
+ * group) -> scatter of the reduced QKV block's heads over that group ->
+ * causal attention core on the device's run of heads -> all-gather of the
+ * heads' outputs (the out-proj input block) -> out-proj (chunked, reduced
+ * with its bias).  One GPU holds one device: the all-gather's other columns
+ * are the peers' data, as the partial tables are.
+ *  x_loc        bf16 [tokens, k_loc of QKV]: the layer input block.
+ *  qkv_partials host table of the QKV group's red_size buffers
+ *               ([tokens, ldp_qkv] of partial_dtype; own entry written).
+ *  qkv          bf16 [tokens, n_loc of QKV]: reduced QKV block (+ bias),
+ *               written; token rows sequence-major (b * seq + t).
+ *  attn         bf16 [tokens, k_loc of out-proj]: the gathered out-proj
+ *               input.  The call writes its heads' columns (as
+ *               atp_attention_fwd); the other columns must hold the other
+ *               group members' outputs when the call is made.
+ *  lse          fp32 [heads of the device][tokens], written.
+ *  o_partials / o: out-proj's partial table and reduced output (+ bias).
+ * Weights: entries 0 (qkv) and 1 (out) of w, in w->layout; 2 and 3 are
+ * not read.  Products read the weights as stored (no workspace); the
+ * attention core starts once the whole QKV block is reduced (a causal
+ * sequence spans chunks), out-proj's chunks follow on compute_stream and
+ * their reductions overlap the next chunk's GEMM on comm_stream (Sec. 4.1).
+ * The call refuses a compute_stream under HIP graph capture.  Errors as
+ * atp_block_fwd and atp_attention_fwd. */
+typedef struct {
+    const void* x_loc; int64_t ldx;
+    void* const* qkv_partials; int64_t ldp_qkv;
+    void* qkv; int64_t ld_qkv;
+    void* attn; int64_t ld_attn;
+    float* lse;
+    void* const* o_partials; int64_t ldp_o;
+    void* o; int64_t ld_o;
+    int32_t partial_dtype;
+} atp_attn_block_fwd_io;
+
+atp_status atp_attention_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t batch,
+                                   int64_t seq, int64_t h, int32_t heads, int32_t chunks,
+                                   const atp_block_weights* w, const atp_attn_block_fwd_io* io,
+                                   void* compute_stream, void* comm_stream);
+
+/* Backward of atp_attention_block_fwd (Sec. 4.2 through the chain):
+ * out-proj's dX (chunked, reduced over its backward group) gives d_attn;
+ * out-proj's dW and db; the attention core's backward on the device's heads
+ * writes their dq, dk, dv columns of d_qkv (the conjugate of the scatter);
+ * QKV's dX (chunked, reduced over its backward group), dW and db follow.
+ *  x_loc, qkv, attn, lse: the forward's input, outputs and saved lse.
+ *  d_o          bf16 gradient of o.
+ *  d_attn_partials / d_attn: out-proj's backward table and the reduced
+ *               gradient of the gathered block (bf16, written).
+ *  delta        fp32 scratch of heads-of-device * tokens values.
+ *  d_qkv        bf16 [tokens, n_loc of QKV]: the device's heads' columns are
+ *               written; the other columns must hold the other group
+ *               members' (the all-gather of the QKV block's gradient).
+ *  dx_partials / dx: QKV's backward table and reduced input gradient.
+ *  dw[0], db[0] (qkv), dw[1], db[1] (out): f32, as atp_block_bwd_io
+ *               (dw in the weights' layout and leading dimension; db
+ *               nullable).
+ * Errors as atp_block_bwd and atp_attention_bwd. */
+typedef struct {
+    const void* x_loc; int64_t ldx;
+    const void* qkv; int64_t ld_qkv;
+    const void* attn; int64_t ld_attn;
+    const float* lse;
+    const void* d_o; int64_t ld_do;
+    void* const* d_attn_partials; int64_t ldp_da;
+    void* d_attn; int64_t ld_d_attn;
+    float* delta;
+    void* d_qkv; int64_t ld_dqkv;
+    void* const* dx_partials; int64_t ldp_dx;
+    void* dx; int64_t ld_dx;
+    float* dw[2];
+    float* db[2];
+    int32_t partial_dtype;
+} atp_attn_block_bwd_io;
+
+atp_status atp_attention_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t batch,
+                                   int64_t seq, int64_t h, int32_t heads, int32_t chunks,
+                                   const atp_block_weights* w, const atp_attn_block_bwd_io* io,
+                                   void* compute_stream, void* comm_stream);
+
 /* Per-kernel timing of the library's own launches.  When enabled, every
  * kernel the library enqueues is bracketed by HIP events on its stream;
  * atp_profile_collect synchronises those events, fills up to `max`

@@ -27,7 +27,9 @@ Models" (arXiv 2301.08658).  What is computed and where the paper says so:
   attention core of one head (``attention_fwd`` / ``attention_bwd``) and one
   device's share of it: the heads of its reduced QKV block scattered over
   the QKV output's reduction group (``attention_core_local``,
-  ``attention_core_bwd_local``).
+  ``attention_core_bwd_local``); the unsharded attention block, QKV ->
+  core -> out-proj, forward and backward (``attention_block_global``,
+  ``attention_block_global_bwd``).
 
 Every array crossing into C is float64; bf16 inputs are widened exactly.
 """
@@ -493,3 +495,34 @@ def attention_core_bwd_local(qkv_loc, dout_dev, batch, seq, head_dim, scatter_si
             dqkv[r, o3 + head_dim:o3 + 2 * head_dim] = dk
             dqkv[r, o3 + 2 * head_dim:o3 + 3 * head_dim] = dv
     return dqkv
+
+
+def attention_block_global(X, W_qkv, b_qkv, W_o, b_o, batch, seq, head_dim):
+    """The unsharded attention block of one layer (Sec. 3.2.1 with Sec. 2.1
+    Formula (mha) as its core), in fp64: qkv = X W_qkv + b_qkv; every head
+    j (columns [3 d j, 3 d (j + 1)) of qkv, [q | k | v]) attends causally
+    within each sequence; the heads' outputs side by side form A (head j at
+    columns [d j, d (j + 1))); o = A W_o + b_o.  Token rows are
+    sequence-major.  Returns dict(qkv, attn=A, o, lse [heads, T])."""
+    X = _f64(X)
+    qkv = matmul(X, W_qkv) + _f64(b_qkv)[None, :]
+    T = batch * seq
+    heads = qkv.shape[1] // (3 * head_dim)
+    A, lse = attention_core_local(qkv, batch, seq, head_dim, 1, 0)
+    assert A.shape == (T, heads * head_dim)
+    o = matmul(A, W_o) + _f64(b_o)[None, :]
+    return dict(qkv=qkv, attn=A, o=o, lse=lse)
+
+
+def attention_block_global_bwd(X, W_qkv, W_o, fwd, d_o, batch, seq, head_dim):
+    """Gradients of attention_block_global for dL/do = d_o (Sec. 4.2 through
+    each product, Formula (mha)'s gradient in the core).  Returns dict with
+    d_attn, d_qkv, dx, dw_qkv, db_qkv, dw_out, db_out."""
+    d_o = _f64(d_o)
+    W_o = _f64(W_o)
+    W_qkv = _f64(W_qkv)
+    d_attn, dw_out, db_out = linear_bwd(fwd["attn"], W_o, d_o)
+    d_qkv = attention_core_bwd_local(fwd["qkv"], d_attn, batch, seq, head_dim, 1, 0)
+    dx, dw_qkv, db_qkv = linear_bwd(X, W_qkv, d_qkv)
+    return dict(d_attn=d_attn, d_qkv=d_qkv, dx=dx, dw_qkv=dw_qkv, db_qkv=db_qkv, dw_out=dw_out,
+                db_out=db_out)

@@ -904,6 +904,99 @@ T* row_ptr(T* base, int64_t r, int64_t ld, bool b16) {
         std::is_const<T>::value, const char, char>::type*>(base) + r * ld * (b16 ? 2 : 4));
 }
 
+// ------------------------------------------------------------------------
+// The attention block's chain reads the weights as stored (no workspace).
+// X W: NN from [k][n] weights, NT from [n][k].  dY W^T: NT from [k][n], NN
+// from [n][k].  dW = X^T dY ([k][n]) or dW^T = dY^T X ([n][k]) over the
+// tokens: TN.
+atp::GemmProblem xw_problem(const atp_shard& g, bool kn, const void* W, int64_t ldw,
+                            const void* A, int64_t lda, void* C, int64_t ldc, bool b16, int epi,
+                            int64_t M) {
+    return gemm_problem(kn ? atp::LAYOUT_NN : atp::LAYOUT_NT, A, lda, W, ldw, C, ldc, b16, epi, M,
+                        g.n_loc, g.k_loc);
+}
+
+atp::GemmProblem dyw_problem(const atp_shard& g, bool kn, const void* W, int64_t ldw,
+                             const void* dY, int64_t lddy, void* C, int64_t ldc, bool b16, int epi,
+                             int64_t M) {
+    return gemm_problem(kn ? atp::LAYOUT_NT : atp::LAYOUT_NN, dY, lddy, W, ldw, C, ldc, b16, epi,
+                        M, g.k_loc, g.n_loc);
+}
+
+atp_status weight_grads(const atp_shard& g, bool kn, const void* X, int64_t ldx, const void* dY,
+                        int64_t lddy, float* dw, int64_t ldw, float* db, int64_t T,
+                        hipStream_t s) {
+    if (db) ATP_CHECK(run_colsum(dY, lddy, T, g.n_loc, db, s));
+    atp::GemmProblem p =
+        kn ? gemm_problem(atp::LAYOUT_TN, X, ldx, dY, lddy, dw, ldw, false, atp::EPI_NONE, g.k_loc,
+                          g.n_loc, T)
+           : gemm_problem(atp::LAYOUT_TN, dY, lddy, X, ldx, dw, ldw, false, atp::EPI_NONE, g.n_loc,
+                          g.k_loc, T);
+    return run_gemm(p, s);
+}
+
+// One reduced product of the chain, chunked (Sec. 4.1): chunk c's GEMM on
+// cs writes the own partial rows (or, for a group of one, the whole output
+// with its epilogue in one launch), and ms reduces the group's partials of
+// those rows with the epilogue as soon as they are written.  `done` is
+// recorded after the last chunk's reduction (on ms), or after the single
+// launch (on cs).  make(A_rows, C_rows, ldc, b16, epi, M) builds the product.
+template <class Make>
+atp_status chained_linear(const Streams& S, int red_size, int red_index, void* const* parts,
+                          int64_t ldp, bool pb16, const void* A, int64_t lda, int64_t ncols,
+                          int epi, const void* bias, const void* pre_in, void* out, int64_t ldo,
+                          int64_t T, int32_t chunks, hipEvent_t* ev_chunk, hipEvent_t done,
+                          Make make) {
+    if (red_size == 1) {
+        atp::GemmProblem p = make(A, out, ldo, true, epi, T);
+        p.bias = bias;
+        p.pre_in = pre_in;
+        ATP_CHECK(run_gemm(p, S.cs));
+        HIP_CHECK(hipEventRecord(done, S.cs), "hipEventRecord");
+        return ATP_OK;
+    }
+    const int64_t mc = T / chunks;
+    void* own = parts[red_index];
+    for (int32_t c = 0; c < chunks; ++c) {
+        const int64_t r0 = (int64_t)c * mc;
+        atp::GemmProblem p = make(static_cast<const uint16_t*>(A) + r0 * lda,
+                                  row_ptr(own, r0, ldp, pb16), ldp, pb16, atp::EPI_NONE, mc);
+        ATP_CHECK(run_gemm(p, S.cs));
+        HIP_CHECK(hipEventRecord(ev_chunk[c], S.cs), "hipEventRecord");
+        HIP_CHECK(hipStreamWaitEvent(S.ms, ev_chunk[c], 0), "hipStreamWaitEvent");
+        atp::ReduceProblem r = reduce_problem(red_size, parts, ldp, r0, mc, ncols, epi, bias,
+                                              pre_in, out, ldo, true, nullptr, pb16);
+        ATP_CHECK(run_reduce(r, S.ms));
+    }
+    HIP_CHECK(hipEventRecord(done, S.ms), "hipEventRecord");
+    return ATP_OK;
+}
+
+atp_status check_attn_weights(const BlockPlan& P, const atp_block_weights* w) {
+    if (!valid_layout(w->layout))
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "weight layout %d unknown", w->layout);
+    const bool kn = w->layout == ATP_W_KN;
+    for (int i = 0; i < 2; ++i) {
+        char nm[32];
+        snprintf(nm, sizeof nm, "w[%s]", kLinearName[i]);
+        const atp_shard& g = P.g[i];
+        ATP_CHECK(check_mat(w->w[i], kn ? g.k_loc : g.n_loc, w->ldw[i], kn ? g.n_loc : g.k_loc,
+                            nm));
+        snprintf(nm, sizeof nm, "b[%s]", kLinearName[i]);
+        ATP_CHECK(check_vec(w->b[i], nm));
+    }
+    return ATP_OK;
+}
+
+bool overlaps(const void* a, int64_t rows_a, int64_t ld_a, size_t esz_a, const void* b,
+              int64_t rows_b, int64_t ld_b, size_t esz_b) {
+    if (!a || !b || rows_a == 0 || rows_b == 0) return false;
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+    const uintptr_t a1 = a0 + (uintptr_t)(rows_a * ld_a) * esz_a;
+    const uintptr_t b1 = b0 + (uintptr_t)(rows_b * ld_b) * esz_b;
+    return a0 < b1 && b0 < a1;
+}
+
 }  // namespace
 }  // extern "C++"
 
@@ -1300,6 +1393,183 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         return P.g[i].k_loc * P.g[i].n_loc > P.g[j].k_loc * P.g[j].n_loc;
     });
     for (int L : order) ATP_CHECK(dw(L));
+    return S.end(ev[1]);
+}
+
+atp_status atp_attention_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t batch,
+                                   int64_t seq, int64_t h, int32_t heads, int32_t chunks,
+                                   const atp_block_weights* w, const atp_attn_block_fwd_io* io,
+                                   void* compute_stream, void* comm_stream) {
+    AttnPlan ap;
+    ATP_CHECK(attention_plan(mesh, block_mode, batch, seq, h, heads, &ap));
+    BlockPlan P;
+    ATP_CHECK(block_plan(mesh, block_mode, h, &P));
+    const int64_t T = ap.T;
+    ATP_CHECK(check_chunks(T, chunks));
+    if (!w || !io) return set_error(ATP_ERR_INVALID_ARGUMENT, "weights or io is NULL");
+    ATP_CHECK(check_attn_weights(P, w));
+    ATP_CHECK(check_partial_dtype(io->partial_dtype));
+    const bool kn = w->layout == ATP_W_KN;
+    const bool pb16 = io->partial_dtype == ATP_BF16;
+    const atp_shard& gq = P.g[0];
+    const atp_shard& go = P.g[1];
+    if (go.k_loc != ap.out_cols)
+        return set_error(ATP_ERR_SHAPE, "out-proj contracts over %lld columns, the heads give %lld",
+                         (long long)go.k_loc, (long long)ap.out_cols);
+    ATP_CHECK(check_mat(io->x_loc, T, io->ldx, gq.k_loc, "x_loc"));
+    ATP_CHECK(check_mat(io->qkv, T, io->ld_qkv, gq.n_loc, "qkv"));
+    ATP_CHECK(check_mat(io->attn, T, io->ld_attn, go.k_loc, "attn"));
+    ATP_CHECK(check_mat(io->o, T, io->ld_o, go.n_loc, "o"));
+    ATP_CHECK(check_group(io->qkv_partials, gq.red_size, T, io->ldp_qkv, gq.n_loc, "qkv_partials"));
+    ATP_CHECK(check_group(io->o_partials, go.red_size, T, io->ldp_o, go.n_loc, "o_partials"));
+    if (T > 0) ATP_CHECK(check_vec(io->lse, "lse"));
+    if (overlaps(io->qkv, T, io->ld_qkv, 2, io->attn, T, io->ld_attn, 2))
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "qkv and attn must not overlap");
+    ATP_CHECK(refuse_capture_of_direct_path(compute_stream));
+
+    Streams S(compute_stream, comm_stream);
+    hipEvent_t* ev = nullptr;
+    // [0] start  [1] comm end  [2] QKV reduced  [3] out-proj done, then the
+    // chunk events of QKV and of out-proj
+    ATP_CHECK(sync_events(4 + 2 * (size_t)chunks, &ev));
+    ATP_CHECK(S.begin(ev[0]));
+    auto make = [&](int L) {
+        return [&, L](const void* A, void* C, int64_t ldc, bool b16, int epi, int64_t M) {
+            const int64_t lda = L == 0 ? io->ldx : io->ld_attn;
+            return xw_problem(P.g[L], kn, w->w[L], w->ldw[L], A, lda, C, ldc, b16, epi, M);
+        };
+    };
+    ATP_CHECK(chained_linear(S, gq.red_size, gq.red_index, io->qkv_partials, io->ldp_qkv, pb16,
+                             io->x_loc, io->ldx, gq.n_loc, atp::EPI_BIAS, w->b[0], nullptr,
+                             io->qkv, io->ld_qkv, T, chunks, ev + 4, ev[2], make(0)));
+    // a causal sequence spans chunks: the core waits for the whole QKV block
+    HIP_CHECK(hipStreamWaitEvent(S.cs, ev[2], 0), "hipStreamWaitEvent");
+    if (T > 0) {
+        atp::AttentionProblem p;
+        p.qkv = io->qkv;
+        p.ld_qkv = io->ld_qkv;
+        p.qkv_col0 = (int64_t)ap.first * 3 * kHeadDim;
+        p.out = io->attn;
+        p.ld_out = io->ld_attn;
+        p.out_col0 = (int64_t)ap.first * kHeadDim;
+        p.lse = io->lse;
+        p.batch = batch;
+        p.seq = seq;
+        p.heads = ap.hd;
+        p.head_dim = kHeadDim;
+        const double pairs = (double)batch * ap.hd * (double)seq * (double)(seq + 1) / 2.0;
+        ATP_CHECK(timed("attention_fwd", 4.0 * kHeadDim * pairs,
+                        (double)T * ap.hd * (4.0 * kHeadDim * 2.0 + 4.0), S.cs,
+                        [&] { return atp::launch_attention_fwd(p, S.cs); }));
+    }
+    ATP_CHECK(chained_linear(S, go.red_size, go.red_index, io->o_partials, io->ldp_o, pb16,
+                             io->attn, io->ld_attn, go.n_loc, atp::EPI_BIAS, w->b[1], nullptr,
+                             io->o, io->ld_o, T, chunks, ev + 4 + chunks, ev[3], make(1)));
+    return S.end(ev[1]);
+}
+
+atp_status atp_attention_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t batch,
+                                   int64_t seq, int64_t h, int32_t heads, int32_t chunks,
+                                   const atp_block_weights* w, const atp_attn_block_bwd_io* io,
+                                   void* compute_stream, void* comm_stream) {
+    AttnPlan ap;
+    ATP_CHECK(attention_plan(mesh, block_mode, batch, seq, h, heads, &ap));
+    BlockPlan P;
+    ATP_CHECK(block_plan(mesh, block_mode, h, &P));
+    const int64_t T = ap.T;
+    ATP_CHECK(check_chunks(T, chunks));
+    if (!w || !io) return set_error(ATP_ERR_INVALID_ARGUMENT, "weights or io is NULL");
+    ATP_CHECK(check_attn_weights(P, w));
+    ATP_CHECK(check_partial_dtype(io->partial_dtype));
+    const bool kn = w->layout == ATP_W_KN;
+    const bool pb16 = io->partial_dtype == ATP_BF16;
+    const atp_shard& gq = P.g[0];
+    const atp_shard& go = P.g[1];
+    if (go.k_loc != ap.out_cols)
+        return set_error(ATP_ERR_SHAPE, "out-proj contracts over %lld columns, the heads give %lld",
+                         (long long)go.k_loc, (long long)ap.out_cols);
+    ATP_CHECK(check_mat(io->x_loc, T, io->ldx, gq.k_loc, "x_loc"));
+    ATP_CHECK(check_mat(io->qkv, T, io->ld_qkv, gq.n_loc, "qkv"));
+    ATP_CHECK(check_mat(io->attn, T, io->ld_attn, go.k_loc, "attn"));
+    ATP_CHECK(check_mat(io->d_o, T, io->ld_do, go.n_loc, "d_o"));
+    ATP_CHECK(check_mat(io->d_attn, T, io->ld_d_attn, go.k_loc, "d_attn"));
+    ATP_CHECK(check_mat(io->d_qkv, T, io->ld_dqkv, gq.n_loc, "d_qkv"));
+    ATP_CHECK(check_mat(io->dx, T, io->ld_dx, gq.k_loc, "dx"));
+    ATP_CHECK(check_group(io->d_attn_partials, go.bwd_size, T, io->ldp_da, go.k_loc,
+                          "d_attn_partials"));
+    ATP_CHECK(check_group(io->dx_partials, gq.bwd_size, T, io->ldp_dx, gq.k_loc, "dx_partials"));
+    for (int i = 0; i < 2; ++i) {
+        char nm[32];
+        const atp_shard& g = P.g[i];
+        snprintf(nm, sizeof nm, "dw[%s]", kLinearName[i]);
+        ATP_CHECK(check_mat(io->dw[i], kn ? g.k_loc : g.n_loc, w->ldw[i], kn ? g.n_loc : g.k_loc,
+                            nm));
+        if (io->db[i]) {
+            snprintf(nm, sizeof nm, "db[%s]", kLinearName[i]);
+            ATP_CHECK(check_vec(io->db[i], nm));
+        }
+    }
+    if (T > 0) {
+        ATP_CHECK(check_vec(io->lse, "lse"));
+        ATP_CHECK(check_vec(io->delta, "delta"));
+    }
+    if (overlaps(io->d_qkv, T, io->ld_dqkv, 2, io->qkv, T, io->ld_qkv, 2) ||
+        overlaps(io->d_qkv, T, io->ld_dqkv, 2, io->attn, T, io->ld_attn, 2) ||
+        overlaps(io->d_qkv, T, io->ld_dqkv, 2, io->d_attn, T, io->ld_d_attn, 2))
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "d_qkv must not overlap an input");
+    ATP_CHECK(refuse_capture_of_direct_path(compute_stream));
+
+    Streams S(compute_stream, comm_stream);
+    hipEvent_t* ev = nullptr;
+    // [0] start  [1] comm end  [2] d_attn reduced  [3] QKV dX done, then the
+    // chunk events of out-proj's dX and of QKV's dX
+    ATP_CHECK(sync_events(4 + 2 * (size_t)chunks, &ev));
+    ATP_CHECK(S.begin(ev[0]));
+    auto make = [&](int L, const void* dY, int64_t lddy) {
+        return [&, L, lddy](const void* A, void* C, int64_t ldc, bool b16, int epi, int64_t M) {
+            return dyw_problem(P.g[L], kn, w->w[L], w->ldw[L], A, lddy, C, ldc, b16, epi, M);
+        };
+    };
+    // out-proj: dX chunks (reduced on ms into d_attn), then its dW and db
+    // on cs while those reductions drain
+    ATP_CHECK(chained_linear(S, go.bwd_size, go.bwd_index, io->d_attn_partials, io->ldp_da, pb16,
+                             io->d_o, io->ld_do, go.k_loc, atp::EPI_NONE, nullptr, nullptr,
+                             io->d_attn, io->ld_d_attn, T, chunks, ev + 4, ev[2],
+                             make(1, io->d_o, io->ld_do)));
+    ATP_CHECK(weight_grads(go, kn, io->attn, io->ld_attn, io->d_o, io->ld_do, io->dw[1],
+                           w->ldw[1], io->db[1], T, S.cs));
+    // the core's backward reads the device's columns of the whole d_attn
+    HIP_CHECK(hipStreamWaitEvent(S.cs, ev[2], 0), "hipStreamWaitEvent");
+    if (T > 0) {
+        atp::AttentionBwdProblem p;
+        p.qkv = io->qkv;
+        p.ld_qkv = io->ld_qkv;
+        p.qkv_col0 = (int64_t)ap.first * 3 * kHeadDim;
+        p.out = io->attn;
+        p.ld_out = io->ld_attn;
+        p.out_col0 = (int64_t)ap.first * kHeadDim;
+        p.dout = io->d_attn;
+        p.ld_dout = io->ld_d_attn;
+        p.lse = io->lse;
+        p.delta = io->delta;
+        p.dqkv = io->d_qkv;
+        p.ld_dqkv = io->ld_dqkv;
+        p.batch = batch;
+        p.seq = seq;
+        p.heads = ap.hd;
+        p.head_dim = kHeadDim;
+        const double pairs = (double)batch * ap.hd * (double)seq * (double)(seq + 1) / 2.0;
+        ATP_CHECK(timed("attention_bwd", 2.0 * kHeadDim * pairs * 5.0,
+                        (double)T * ap.hd * (10.0 * kHeadDim * 2.0 + 12.0), S.cs,
+                        [&] { return atp::launch_attention_bwd(p, S.cs); }));
+    }
+    // QKV: dX chunks from the gathered d_qkv (reduced on ms into dx), dW, db
+    ATP_CHECK(chained_linear(S, gq.bwd_size, gq.bwd_index, io->dx_partials, io->ldp_dx, pb16,
+                             io->d_qkv, io->ld_dqkv, gq.k_loc, atp::EPI_NONE, nullptr, nullptr,
+                             io->dx, io->ld_dx, T, chunks, ev + 4 + chunks, ev[3],
+                             make(0, io->d_qkv, io->ld_dqkv)));
+    ATP_CHECK(weight_grads(gq, kn, io->x_loc, io->ldx, io->d_qkv, io->ld_dqkv, io->dw[0],
+                           w->ldw[0], io->db[0], T, S.cs));
     return S.end(ev[1]);
 }
 

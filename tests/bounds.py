@@ -24,6 +24,8 @@ These terms are added to the stated elementwise tolerance
 """
 import numpy as np
 
+import oracle as O
+
 SIGMAS = 6.0
 
 
@@ -62,3 +64,93 @@ def right(x, var) -> np.ndarray:
 def colsum(var) -> np.ndarray:
     """Column sums of V with V carrying errors of variance var."""
     return SIGMAS * np.sqrt(np.asarray(var, dtype=np.float64).sum(axis=0))
+
+
+def delta_bounds(q, k, v, do):
+    """Error terms for dQ and dK of one (sequence, head) from delta_t = dO_t . O_t
+    taken over the stored bf16 output (the kernels never see the exact O).
+    The stored O carries two roundings of relative size 2^-9 (the bf16
+    probabilities that enter P V, and the output's own rounding), so
+    |dO_t[e]| (|O_t[e]| + (P |V|)_t[e]) scales the error of each term; taken
+    as independent uniform roundings, delta_t's error has RMS
+        r_t = 2^-9 / sqrt(3) * sqrt(sum_e dO_t[e]^2 (O_t[e]^2 + (P|V|)_t[e]^2)).
+    It enters dS[t, u] = P[t, u] (dP[t, u] - delta_t), hence
+        dK_u[e] error RMS = sqrt(sum_t P[t,u]^2 r_t^2 q_t[e]^2) / sqrt(d),
+        dQ_t[e] error RMS = r_t sqrt(sum_u P[t,u]^2 k_u[e]^2) / sqrt(d);
+    the bounds are six times these RMS values.  P, O come from the oracle."""
+    q, k, v, do = (np.asarray(O._f64(a)) for a in (q, k, v, do))
+    S, d = q.shape
+    o, lse = O.attention_fwd(q, k, v)
+    s = q @ k.T / np.sqrt(d)
+    s[np.triu(np.ones((S, S), dtype=bool), 1)] = -np.inf
+    P = np.exp(s - lse[:, None])
+    r = 2.0 ** -9 / np.sqrt(3) * np.sqrt((do * do * (o * o + (P @ np.abs(v)) ** 2)).sum(1))
+    bk = 6 / np.sqrt(d) * np.sqrt((P * P).T @ ((r * r)[:, None] * q * q))
+    bq = 6 / np.sqrt(d) * r[:, None] * np.sqrt((P * P) @ (k * k))
+    return bq, bk
+
+
+def attention_dout_sensitivity(q, k, v, var_do):
+    """Variances that a bf16 handoff of the output gradient dO (independent
+    errors of variance var_do [S, d]) adds to the causal attention backward
+    of one (sequence, head), from the oracle's q, k, v.  For fixed P the
+    backward is linear in dO:
+        dV_u = sum_t P[t,u] dO_t,
+        dS[t,u] = P[t,u] (dO_t . (V_u - O_t))        (dP - delta, delta = dO_t . O_t),
+        dQ_t = sum_u dS[t,u] K_u / sqrt(d),  dK_u = sum_t dS[t,u] Q_t / sqrt(d).
+    Returns the per-element variances of dQ, dK, dV ([S, d] each) and the
+    variances of their column sums over the tokens ([d] each), taken from the
+    same linear maps (the column sums are not sums of the per-element
+    variances: sum_u dV_u = sum_t dO_t, sum_u dK_u = 0 whatever dO is)."""
+    q, k, v = (np.asarray(O._f64(a)) for a in (q, k, v))
+    var = np.asarray(var_do, dtype=np.float64)
+    S, d = q.shape
+    o, lse = O.attention_fwd(q, k, v)
+    s = q @ k.T / np.sqrt(d)
+    s[np.triu(np.ones((S, S), dtype=bool), 1)] = -np.inf
+    P = np.exp(s - lse[:, None])
+    P2 = P * P
+    var_dv = P2.T @ var
+    # dQ_t[f] = sum_e dO_t[e] C[t, e, f],
+    # C[t, e, f] = (sum_u P[t,u] V[u,e] K[u,f] - O[t,e] (P K)[t,f]) / sqrt(d)
+    vk = (v[:, :, None] * k[:, None, :]).reshape(S, d * d)
+    C = ((P @ vk).reshape(S, d, d) - o[:, :, None] * (P @ k)[:, None, :]) / np.sqrt(d)
+    var_dq = np.einsum("tef,te->tf", C * C, var)
+    # dK_u[f] = sum_t P[t,u] (dO_t . (V_u - O_t)) Q_t[f] / sqrt(d)
+    w2 = var @ (v * v).T - 2.0 * (o * var) @ v.T + (o * o * var).sum(1)[:, None]
+    var_dk = (P2 * w2).T @ (q * q) / d
+    return dict(dq=var_dq, dk=var_dk, dv=var_dv, sum_dq=var_dq.sum(0),
+                sum_dk=np.zeros(d), sum_dv=var.sum(0))
+
+
+def attention_qkv_sensitivity(q, k, v, var_q, var_k, var_v):
+    """Variance that independent errors in q, k, v (variances var_* [S, d],
+    e.g. their bf16 handoff) add to each output O_t[e] of the causal
+    attention of one (sequence, head), to first order:
+        dO_t = sum_u P[t,u] dV_u + sum_u P[t,u] (V_u - O_t) ds_tu,
+        ds_tu = (dQ_t . K_u + Q_t . dK_u) / sqrt(d).
+    dQ_t is shared by every u of row t; dK_u and dV_u are independent."""
+    q, k, v = (np.asarray(O._f64(a)) for a in (q, k, v))
+    vq, vk_, vv = (np.asarray(a, dtype=np.float64) for a in (var_q, var_k, var_v))
+    S, d = q.shape
+    o, lse = O.attention_fwd(q, k, v)
+    s = q @ k.T / np.sqrt(d)
+    s[np.triu(np.ones((S, S), dtype=bool), 1)] = -np.inf
+    P = np.exp(s - lse[:, None])
+    P2 = P * P
+    out = P2 @ vv
+    # the row's dQ: C[t, e, f] = sum_u P[t,u] (V[u,e] - O[t,e]) K[u,f] / sqrt(d)
+    vkp = (v[:, :, None] * k[:, None, :]).reshape(S, d * d)
+    C = ((P @ vkp).reshape(S, d, d) - o[:, :, None] * (P @ k)[:, None, :]) / np.sqrt(d)
+    out += np.einsum("tef,tf->te", C * C, vq)
+    # the keys' dK: sum_u P^2 (V_u - O_t)^2 (sum_f Q_t[f]^2 var_k[u,f]) / d
+    W = P2 * ((q * q) @ vk_.T) / d
+    out += W @ (v * v) - 2.0 * o * (W @ v) + o * o * W.sum(1)[:, None]
+    return out
+
+
+def right_var(var, y) -> np.ndarray:
+    """Y^T-side product Z = V^T Y (a weight gradient) with V carrying errors
+    of variance var and Y exact: SIGMAS standard deviations of each output."""
+    y = np.asarray(y, dtype=np.float64)
+    return SIGMAS * np.sqrt(np.asarray(var, dtype=np.float64).T @ (y * y))

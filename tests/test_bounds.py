@@ -1,0 +1,66 @@
+"""The derived error terms (tests/bounds.py) pinned on the CPU: the bf16
+spacing against torch's rounding, and the attention backward's sensitivity
+to a rounded output gradient against the oracle's own linear response (the
+backward is linear in dO for fixed q, k, v, so a unit change of one dO
+element gives one column of the exact Jacobian)."""
+import numpy as np
+import torch
+
+import bounds
+import oracle as O
+
+
+def test_ulp_bf16_is_the_rounding_step():
+    x = np.concatenate([np.linspace(-5, 5, 2001), [1.0, 2.0 ** -126, 3.0e5]])
+    u = bounds.ulp_bf16(x)
+    xb = torch.tensor(x, dtype=torch.float64).to(torch.float32).to(torch.bfloat16)
+    err = np.abs(xb.to(torch.float64).numpy() - x)
+    assert np.all(err <= 0.5 * u * (1 + 1e-12))
+    assert bounds.ulp_bf16(1.0) == 2.0 ** -7 and bounds.ulp_bf16(1.999) == 2.0 ** -7
+
+
+def test_attention_dout_sensitivity_matches_the_oracles_jacobian():
+    rng = np.random.default_rng(3)
+    S, d = 7, 4
+    q, k, v, do = (rng.standard_normal((S, d)) for _ in range(4))
+    sig2 = rng.uniform(0.01, 1.0, (S, d))
+    r = bounds.attention_dout_sensitivity(q, k, v, sig2)
+    base = O.attention_bwd(q, k, v, do)
+    J = np.zeros((3, S, d, S, d))
+    for t in range(S):
+        for e in range(d):
+            dd = do.copy()
+            dd[t, e] += 1.0
+            for i, out in enumerate(O.attention_bwd(q, k, v, dd)):
+                J[i, :, :, t, e] = out - base[i]
+    for i, key in enumerate(("dq", "dk", "dv")):
+        var = np.einsum("abte,te->ab", J[i] ** 2, sig2)
+        np.testing.assert_allclose(r[key], var, rtol=1e-9, atol=1e-14)
+        col = np.einsum("bte,te->b", J[i].sum(0) ** 2, sig2)
+        np.testing.assert_allclose(r["sum_" + key], col, rtol=1e-9, atol=1e-12)
+    # the column sums' identities: sum_u dV_u = sum_t dO_t, sum_u dK_u = 0
+    np.testing.assert_allclose(r["sum_dv"], sig2.sum(0), rtol=1e-12)
+    assert np.all(r["sum_dk"] == 0)
+
+
+def test_attention_qkv_sensitivity_matches_a_numerical_jacobian():
+    """First-order variance of the attention output under independent errors
+    of q, k, v, against central differences of the oracle's forward."""
+    rng = np.random.default_rng(4)
+    S, d = 6, 4
+    q, k, v = (rng.standard_normal((S, d)) for _ in range(3))
+    var = [rng.uniform(0.01, 1.0, (S, d)) for _ in range(3)]
+    got = bounds.attention_qkv_sensitivity(q, k, v, *var)
+    want = np.zeros((S, d))
+    eps = 1e-6
+    for which in range(3):
+        for t in range(S):
+            for e in range(d):
+                args = [q.copy(), k.copy(), v.copy()]
+                args[which][t, e] += eps
+                up, _ = O.attention_fwd(*args)
+                args[which][t, e] -= 2 * eps
+                dn, _ = O.attention_fwd(*args)
+                col = (up - dn) / (2 * eps)
+                want += col ** 2 * var[which][t, e]
+    np.testing.assert_allclose(got, want, rtol=1e-6, atol=1e-12)

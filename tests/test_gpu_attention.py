@@ -11,34 +11,11 @@ import torch
 import oracle as O
 import paper_2301_08658_amd as atp
 import synth_inputs as S
+from bounds import delta_bounds
 from helpers import DEV, assert_close, block_mode_code, to64
 
 pytestmark = pytest.mark.gpu
 HD = 128
-
-
-def delta_bounds(q, k, v, do):
-    """Error terms for dQ and dK of one (sequence, head) from delta_t = dO_t . O_t
-    taken over the stored bf16 output (the kernels never see the exact O).
-    The stored O carries two roundings of relative size 2^-9 (the bf16
-    probabilities that enter P V, and the output's own rounding), so
-    |dO_t[e]| (|O_t[e]| + (P |V|)_t[e]) scales the error of each term; taken
-    as independent uniform roundings, delta_t's error has RMS
-        r_t = 2^-9 / sqrt(3) * sqrt(sum_e dO_t[e]^2 (O_t[e]^2 + (P|V|)_t[e]^2)).
-    It enters dS[t, u] = P[t, u] (dP[t, u] - delta_t), hence
-        dK_u[e] error RMS = sqrt(sum_t P[t,u]^2 r_t^2 q_t[e]^2) / sqrt(d),
-        dQ_t[e] error RMS = r_t sqrt(sum_u P[t,u]^2 k_u[e]^2) / sqrt(d);
-    the bounds are six times these RMS values.  P, O come from the oracle."""
-    q, k, v, do = (to64(a) for a in (q, k, v, do))
-    S, d = q.shape
-    o, lse = O.attention_fwd(q, k, v)
-    s = q @ k.T / np.sqrt(d)
-    s[np.triu(np.ones((S, S), dtype=bool), 1)] = -np.inf
-    P = np.exp(s - lse[:, None])
-    r = 2.0 ** -9 / np.sqrt(3) * np.sqrt((do * do * (o * o + (P @ np.abs(v)) ** 2)).sum(1))
-    bk = 6 / np.sqrt(d) * np.sqrt((P * P).T @ ((r * r)[:, None] * q * q))
-    bq = 6 / np.sqrt(d) * r[:, None] * np.sqrt((P * P) @ (k * k))
-    return bq, bk
 
 
 def _run(mode, mesh, coord, batch, seq, h, seed, sigma=1.0):

@@ -144,3 +144,49 @@ def test_scatter_backward_matches_per_head_backward():
                                          do[r, jj * hd:(jj + 1) * hd])
             got = dqkv[r, 3 * hd * jj:3 * hd * (jj + 1)]
             np.testing.assert_array_equal(got, np.concatenate([dq, dk, dv], axis=1))
+
+
+def test_attention_block_matches_torch_autograd():
+    """The unsharded attention block (QKV -> causal core -> out-proj) and
+    every gradient against torch float64: the core as
+    scaled_dot_product_attention(is_causal=True) per head and autograd through
+    the whole chain (library routines).  Pins the [q | k | v] column order of
+    each head, the heads' side-by-side order in A, the biases and the
+    gradients the chained backward produces."""
+    rng = np.random.default_rng(21)
+    batch, seq, d, heads = 2, 6, 4, 3
+    h, T = d * heads, 2 * 6
+    X = rng.standard_normal((T, h))
+    Wq, bq = rng.standard_normal((h, 3 * h)) * 0.4, rng.standard_normal(3 * h) * 0.1
+    Wo, bo = rng.standard_normal((h, h)) * 0.4, rng.standard_normal(h) * 0.1
+    dO = rng.standard_normal((T, h))
+    f = O.attention_block_global(X, Wq, bq, Wo, bo, batch, seq, d)
+    g = O.attention_block_global_bwd(X, Wq, Wo, f, dO, batch, seq, d)
+
+    t = {k: torch.tensor(v, requires_grad=True) for k, v in
+         dict(X=X, Wq=Wq, bq=bq, Wo=Wo, bo=bo).items()}
+    qkv = t["X"] @ t["Wq"] + t["bq"]
+    qkv.retain_grad()
+    q, k, v = qkv.view(batch, seq, heads, 3, d).permute(3, 0, 2, 1, 4).unbind(0)
+    a = torch.nn.functional.scaled_dot_product_attention(q, k, v, is_causal=True)
+    A = a.permute(0, 2, 1, 3).reshape(T, h)
+    A.retain_grad()
+    o = A @ t["Wo"] + t["bo"]
+    (o * torch.tensor(dO)).sum().backward()
+    scores = (q @ k.transpose(-1, -2)) / np.sqrt(d)
+    scores = scores.masked_fill(torch.triu(torch.ones(seq, seq, dtype=torch.bool), 1), -np.inf)
+    lse = torch.logsumexp(scores, -1).permute(1, 0, 2).reshape(heads, T)
+
+    close = lambda a_, b_: np.testing.assert_allclose(a_, b_.detach().numpy(), rtol=1e-10,  # noqa
+                                                      atol=1e-12)
+    close(f["qkv"], qkv)
+    close(f["attn"], A)
+    close(f["o"], o)
+    close(f["lse"], lse)
+    close(g["d_attn"], A.grad)
+    close(g["d_qkv"], qkv.grad)
+    close(g["dx"], t["X"].grad)
+    close(g["dw_qkv"], t["Wq"].grad)
+    close(g["db_qkv"], t["bq"].grad)
+    close(g["dw_out"], t["Wo"].grad)
+    close(g["db_out"], t["bo"].grad)
