@@ -504,6 +504,23 @@ atp_status atp_attention_block_bwd(const atp_mesh* mesh, int32_t block_mode, int
                                    const atp_block_weights* w, const atp_attn_block_bwd_io* io,
                                    void* compute_stream, void* comm_stream);
 
+/* atp_attention_bwd without the delta argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): delta lives in a scratch array
+ * the library holds on each GPU it runs on (4 MiB, 2^20 fp32 values, kept
+ * until the process ends; its address is looked up once per device, on the
+ * first call there).  The call allocates nothing.  heads-of-device * batch *
+ * seq must be at most 2^20, else ATP_ERR_UNSUPPORTED before any work.  Every
+ * call on one GPU shares that GPU's array (the backward writes each value
+ * before reading it, so nothing needs clearing): calls that overlap on one
+ * GPU -- on different streams, or from different threads -- race.  Other
+ * arguments, results and errors as atp_attention_bwd. */
+atp_status atp_attention_bwd_noalloc(const atp_mesh* mesh, int32_t block_mode, int64_t batch,
+                                     int64_t seq, int64_t h, int32_t heads, const void* qkv,
+                                     int64_t ld_qkv, const void* out, int64_t ld_out,
+                                     const float* lse, const void* d_out, int64_t ld_dout,
+                                     void* d_qkv, int64_t ld_dqkv, void* stream);
+
 /* Per-kernel timing of the library's own launches.  When enabled, every
  * kernel the library enqueues is bracketed by HIP events on its stream;
  * atp_profile_collect synchronises those events, fills up to `max`

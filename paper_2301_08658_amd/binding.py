@@ -161,7 +161,9 @@ EXPORTS = (
     "atp_attention_fwd", "atp_attention_bwd", "atp_chunked_partial_reduce_bf16",
     "atp_shard_linear_fwd_fused", "atp_block_workspace_path", "atp_block_geometry",
     "atp_attention_heads", "atp_attention_block_fwd", "atp_attention_block_bwd",
+    "atp_attention_bwd_noalloc",
 )
+ATP_NOALLOC_DELTA_MAX = 1 << 20   # values of atp_attention_bwd_noalloc's scratch
 
 _lib = None
 
@@ -234,6 +236,9 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.atp_attention_bwd.argtypes = [mp, i32, i64, i64, i64, i32, _vp, i64, _vp, i64, _vp, _vp,
                                       i64, _vp, i64, _vp, _vp]
     lib.atp_attention_bwd.restype = i32
+    lib.atp_attention_bwd_noalloc.argtypes = [mp, i32, i64, i64, i64, i32, _vp, i64, _vp, i64,
+                                              _vp, _vp, i64, _vp, i64, _vp]
+    lib.atp_attention_bwd_noalloc.restype = i32
     hp, dp, cp = (ctypes.POINTER(atp_hcm_layer), ctypes.POINTER(atp_model_dims),
                   ctypes.POINTER(atp_mesh_cost))
     lib.atp_tcomm.argtypes = [dp, i32, i32, ctypes.c_double, ctypes.c_double,
@@ -691,6 +696,23 @@ def atp_attention_bwd(m: atp_mesh, block_mode: int, batch: int, seq: int, h: int
                                             int(h), int(heads), qp, ldq, op, ldo,
                                             _ptr(lse, "lse"), dop, lddo, dqp, lddq,
                                             _ptr(delta, "delta"), _stream(stream)))
+
+
+def atp_attention_bwd_noalloc(m: atp_mesh, block_mode: int, batch: int, seq: int, h: int,
+                              heads: int, qkv, out, lse, d_out, d_qkv, stream=None):
+    """atp_attention_bwd without caller scratch: delta lives in the library's
+    own per-GPU array (for callers that cannot allocate)."""
+    T = batch * seq
+    _, hd, _ = attention_heads(m, block_mode, h, heads)
+    _f32_scratch(lse, hd * T, "lse")
+    g = block_geometry(m, block_mode, h)[0]
+    qp, ldq = _mat(qkv, T, g.n_loc, torch.bfloat16, "qkv")
+    op, ldo = _mat(out, T, g.n_loc // 3, torch.bfloat16, "out")
+    dop, lddo = _mat(d_out, T, g.n_loc // 3, torch.bfloat16, "d_out")
+    dqp, lddq = _mat(d_qkv, T, g.n_loc, torch.bfloat16, "d_qkv")
+    _check(load_library().atp_attention_bwd_noalloc(
+        ctypes.byref(m), int(block_mode), int(batch), int(seq), int(h), int(heads), qp, ldq, op,
+        ldo, _ptr(lse, "lse"), dop, lddo, dqp, lddq, _stream(stream)))
 
 
 def _attn_weights(G, w, b, layout: int):

@@ -561,6 +561,37 @@ atp_status attention_plan(const atp_mesh* mesh, int32_t bm, int64_t batch, int64
 
 }  // namespace
 
+// ---------------------------------------------------------------------------
+// Scratch of atp_attention_bwd_noalloc: the attention backward's delta lives
+// in this file-scope device array instead of a caller buffer.  Every GPU the
+// library runs on holds its own copy (4 MiB) until the process ends; host
+// code never uses the array's name as an address, only the per-device
+// address that hipGetSymbolAddress returns with that device current.
+// ---------------------------------------------------------------------------
+constexpr int64_t kNoAllocDeltaMax = (int64_t)1 << 20;   // floats
+static __device__ __align__(256) float scratch[kNoAllocDeltaMax];
+
+namespace {
+std::mutex g_scratch_mu;
+std::map<int, float*> g_scratch_ptr;   // device -> its copy of `scratch`
+
+// The current device's copy of `scratch`, looked up once per device.
+atp_status noalloc_scratch(float** out) {
+    int dev = 0;
+    HIP_CHECK(hipGetDevice(&dev), "hipGetDevice");
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    auto it = g_scratch_ptr.find(dev);
+    if (it == g_scratch_ptr.end()) {
+        void* ptr = nullptr;
+        HIP_CHECK(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)), "hipGetSymbolAddress");
+        if (!ptr) return set_error(ATP_ERR_DEVICE, "hipGetSymbolAddress gave a NULL address");
+        it = g_scratch_ptr.emplace(dev, static_cast<float*>(ptr)).first;
+    }
+    *out = it->second;
+    return ATP_OK;
+}
+}  // namespace
+
 // ===========================================================================
 // exported
 // ===========================================================================
@@ -858,6 +889,25 @@ atp_status atp_attention_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t b
     const double bytes = (double)ap.T * ap.hd * (10.0 * kHeadDim * 2.0 + 12.0);
     hipStream_t s = static_cast<hipStream_t>(stream);
     return timed("attention_bwd", flops, bytes, s, [&] { return atp::launch_attention_bwd(p, s); });
+}
+
+atp_status atp_attention_bwd_noalloc(const atp_mesh* mesh, int32_t block_mode, int64_t batch,
+                                     int64_t seq, int64_t h, int32_t heads, const void* qkv,
+                                     int64_t ld_qkv, const void* out, int64_t ld_out,
+                                     const float* lse, const void* d_out, int64_t ld_dout,
+                                     void* d_qkv, int64_t ld_dqkv, void* stream) {
+    AttnPlan ap;
+    ATP_CHECK(attention_plan(mesh, block_mode, batch, seq, h, heads, &ap));
+    if ((int64_t)ap.hd * ap.T > kNoAllocDeltaMax)
+        return set_error(ATP_ERR_UNSUPPORTED,
+                         "%d heads x %lld tokens need %lld scratch values; the library's "
+                         "scratch holds %lld (use atp_attention_bwd with a delta buffer)",
+                         ap.hd, (long long)ap.T, (long long)ap.hd * ap.T,
+                         (long long)kNoAllocDeltaMax);
+    float* delta = nullptr;
+    if (ap.T > 0) ATP_CHECK(noalloc_scratch(&delta));
+    return atp_attention_bwd(mesh, block_mode, batch, seq, h, heads, qkv, ld_qkv, out, ld_out, lse,
+                             d_out, ld_dout, d_qkv, ld_dqkv, delta, stream);
 }
 
 atp_status atp_transpose_bf16(int64_t rows, int64_t cols, const void* src, int64_t lds, void* dst,

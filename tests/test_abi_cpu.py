@@ -444,3 +444,17 @@ def test_binding_partial_dtype_of_tables():
         B._partial_dtype([[f], [h]])
     with pytest.raises(TypeError):
         B._partial_dtype([[torch.zeros(2, dtype=torch.float16)]])
+
+
+def test_noalloc_attention_bwd_refuses_beyond_its_scratch():
+    """More delta values than the library's scratch holds is refused before
+    any device work (the pointers are never dereferenced)."""
+    lib = atp.load_library()
+    m = atp.mesh(1, 1, 0, 0)
+    h, heads = 4096, 32                      # 32 heads on the device
+    seq = B.ATP_NOALLOC_DELTA_MAX // heads + 1
+    g = atp.block_geometry(m, 0, h)[0]
+    st = lib.atp_attention_bwd_noalloc(ctypes.byref(m), 0, 1, seq, h, heads, FAKE, g.n_loc, FAKE,
+                                       g.n_loc // 3, FAKE, FAKE, g.n_loc // 3, FAKE, g.n_loc, None)
+    assert st == B.ATP_ERR_UNSUPPORTED
+    assert "scratch" in atp.binding.last_error()
