@@ -42,6 +42,10 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--chunks", type=int, default=None, help="override the chunk count")
+    ap.add_argument("--bwd-chunks", type=int, default=1,
+                    help="chunk count of the backward call.  The paper chunks the forward "
+                         "only (Sec. 4.1); in the backward each linear's dX all-reduce "
+                         "overlaps the dW products (Sec. 4.2), which is 1 here")
     ap.add_argument("--mesh", default=None,
                     help="override the workload's mesh, as D1xD2 (one device's share of it)")
     ap.add_argument("--fwd-only", action="store_true", help="time the forward only")
@@ -301,6 +305,7 @@ def step_flops(st, fwd_only):
 
 
 def make_step(torch, atp, st, fwd_only, serial, comm=None):
+    bwd_chunks = st.get("bwd_chunks") or st["chunks"]
     ms = None if serial else (comm if comm is not None else torch.cuda.Stream())
 
     def step():
@@ -313,7 +318,7 @@ def make_step(torch, atp, st, fwd_only, serial, comm=None):
                           comm_stream=ms_, weight_layout=st["layout"])
         if fwd_only:
             return
-        atp.atp_block_bwd(st["m"], st["bm"], st["T"], st["h"], st["chunks"], st["w"], st["b"],
+        atp.atp_block_bwd(st["m"], st["bm"], st["T"], st["h"], bwd_chunks, st["w"], st["b"],
                           st["x"], st["a"], st["hh"], st["pre"], st["dz"], st["dqkv"], st["do"],
                           st["bwd_tabs"], st["dh_pre"], st["dx_qkv"], st["dx_fc1"],
                           st["d_attn"], st["dw"], st["db"], workspace=st["ws"], compute_stream=cs,
@@ -322,17 +327,16 @@ def make_step(torch, atp, st, fwd_only, serial, comm=None):
 
 
 def cu_masked_stream(torch, n_cus, total=256):
-    """A stream whose kernels may only use `n_cus` of the chip's CUs, spread
-    evenly over the CU index range (hipExtStreamCreateWithCUMask), wrapped
-    for torch.  The stream lives until the process ends."""
+    """A stream whose kernels may only use `n_cus` of the chip's CUs: the
+    lowest n_cus / 8 of every 32-bit word of the mask, i.e. the same number
+    in each 32-CU group (hipExtStreamCreateWithCUMask), wrapped for torch.
+    The stream lives until the process ends."""
     import ctypes
-    if not 0 < n_cus <= total:
-        raise SystemExit(f"bench.py: --comm-cus must be in 1..{total}")
+    per = n_cus // (total // 32)
+    if n_cus % (total // 32) or not 0 < per <= 32:
+        raise SystemExit(f"bench.py: --comm-cus must be a multiple of {total // 32} up to {total}")
     hip = ctypes.CDLL("libamdhip64.so")
-    words = (ctypes.c_uint32 * (total // 32))()
-    for k in range(n_cus):
-        cu = (k * total) // n_cus
-        words[cu // 32] |= 1 << (cu % 32)
+    words = (ctypes.c_uint32 * (total // 32))(*([(1 << per) - 1] * (total // 32)))
     handle = ctypes.c_void_p()
     rc = hip.hipExtStreamCreateWithCUMask(ctypes.byref(handle), ctypes.c_uint32(total // 32),
                                           words)
@@ -534,6 +538,7 @@ def main():
     log(f"[bench] {atp.atp_version()} workload={args.workload} chunks={chunks} "
         f"pass={'fwd' if fwd_only else 'fwd+bwd'}")
     st = setup(torch, atp, S, wl, chunks, args.seed, args.weight_layout, args.partials)
+    st["bwd_chunks"] = args.bwd_chunks
     st["ws"] = None
     if not args.no_workspace:
         nb = atp.atp_block_workspace_bytes(st["m"], st["bm"], st["T"], st["h"], chunks,
@@ -698,6 +703,7 @@ def main():
         scaling="weak", vs_baseline=None, dtype="bf16", data="synthetic",
         config=dict(workload=args.workload, mode=wl["mode"], mesh=[d1, d2], coord=[0, 0],
                     tokens=wl["tokens"], h=wl["h"], chunks=chunks,
+                    bwd_chunks=None if fwd_only else st["bwd_chunks"],
                     **{"pass": "fwd" if fwd_only else "fwd+bwd"},
                     serial=bool(args.serial), workspace=not args.no_workspace,
                     weight_layout=args.weight_layout, partials=args.partials,
