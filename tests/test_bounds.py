@@ -64,3 +64,33 @@ def test_attention_qkv_sensitivity_matches_a_numerical_jacobian():
                 col = (up - dn) / (2 * eps)
                 want += col ** 2 * var[which][t, e]
     np.testing.assert_allclose(got, want, rtol=1e-6, atol=1e-12)
+
+
+def test_propagated_sums_cover_real_roundings():
+    """left/right/colsum: the variance they propagate is the exact variance of
+    a product of V's uniform rounding errors (a Monte Carlo of real bf16
+    roundings of random V stays inside six standard deviations, and its
+    sample variance matches the model), and for at most 12 terms six standard
+    deviations bound even the worst case, where every error is ulp/2 with the
+    sign of its weight."""
+    rng = np.random.default_rng(5)
+    T, K, N = 64, 48, 16
+    w = rng.standard_normal((K, N))
+    x = rng.standard_normal((K, T))
+    errs_l, errs_r, errs_c = [], [], []
+    for _ in range(200):
+        v = rng.standard_normal((T, K)) * rng.uniform(0.1, 10.0)
+        vb = torch.tensor(v).to(torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
+        d = vb - v
+        var = bounds.rounding_var(v)
+        for got, bnd, acc in ((d @ w, bounds.left(var, w), errs_l),
+                              (x @ d, bounds.right(x.T, var), errs_r),
+                              (d.sum(0), bounds.colsum(var), errs_c)):
+            assert np.all(np.abs(got) <= bnd)
+            acc.append((got / (bnd / bounds.SIGMAS)) ** 2)
+    for acc in (errs_l, errs_r, errs_c):
+        ratio = float(np.mean(np.concatenate([a.ravel() for a in acc])))
+        assert 0.8 < ratio < 1.2, ratio           # the model's variance is the real one
+    for n in range(1, 13):
+        worst = n * 0.5                            # n errors of ulp/2 (ulp = 1), all aligned
+        assert bounds.SIGMAS * np.sqrt(n / 12.0) >= worst - 1e-12
