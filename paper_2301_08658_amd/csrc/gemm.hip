@@ -217,30 +217,42 @@ typedef short i16x8 __attribute__((ext_vector_type(8)));
 // same order (32-wide k-slices in ascending k, one 16x16x32 MFMA each, K
 // steps of 64 or 32 holding two or one of them), so they give the same bits
 // and may be mixed freely, e.g. across token chunks.
-template <int BN_, int WGM_, int WGN_, int STAGES_, int GROUP_, int BK_ = 64>
+template <int BN_, int WGM_, int WGN_, int STAGES_, int GROUP_, int BK_ = 64, bool SPLIT_ = false>
 struct Cfg {
     static constexpr int BN = BN_, WGM = WGM_, WGN = WGN_, STAGES = STAGES_, GROUP = GROUP_;
     static constexpr int BK = BK_, KS = BK_ / 32;   // K step, MFMA k-slices per step
+    // SPLIT: separate rings, three stages of A and two of B, each filled by
+    // one group of waves (see the kernel); STAGES is then unused
+    static constexpr bool SPLIT = SPLIT_;
+    static constexpr int RA = 3, RB = 2;
     static_assert(WGM * WGN == NW, "eight waves");
     static_assert(STAGES >= 2 && STAGES <= 4, "two to four LDS stages");
     static_assert(BK == 64 || BK == 32, "K steps of 64 or 32");
     static constexpr int WM = BM / WGM, WN = BN / WGN;
     static constexpr int FM = WM / MF, FN = WN / MF;
     static_assert(FM * MF == WM && FN * MF == WN, "wave tile of whole MFMA tiles");
-    static constexpr int A_EL = BM * BK, STAGE = (BM + BN) * BK;
+    static constexpr int A_EL = BM * BK, STAGE = (BM + BN) * BK, B_EL = BN * BK;
+    static constexpr int LDS_EL = SPLIT ? RA * A_EL + RB * B_EL : STAGES * STAGE;
 };
 // 256 x 160: three stages (156 KB of LDS); waves of 64 x 80; the 32 tiles an
 // XCD runs at once form a 4 x 8 block (4*256 + 8*160 rows per K step, L2 hit
 // rate 81% against 74% for 8 x 4)
 using Tile160 = Cfg<160, 4, 2, 3, 4>;
 // 256 x 256: two stages (128 KB); waves of 128 x 64; 30% fewer copied bytes
-// per FLOP, ~10% faster on the short-K (tokens) dW products, but 62.5% of
-// the tile count of 256 x 160 per launch
+// per FLOP than 256 x 160, but 62.5% of its tile count per launch.  Used for
+// row-contiguous operands; with two shared stages group B's copies must land
+// within the phase that issues them, which Tile256S avoids.
 using Tile256 = Cfg<256, 2, 4, 2, 8>;
 // 256 x 320 in K steps of 32: four stages (144 KB); waves of 128 x 80; 36 KB
 // copied per step for the 40 MFMAs each wave issues, against 52 KB for
 // 256 x 160 in steps of 64 (k-contiguous operands only)
 using Tile320 = Cfg<320, 2, 4, 4, 4, 32>;
+// 256 x 256 in K steps of 64 with split rings (160 KB): group B copies A into
+// a three-stage ring and group A copies B into a two-stage ring, so every
+// copy has at least two phases to land (k-contiguous operands only).
+// Measured in the benchmark step against Tile256: every 256 x 256 product
+// 10-13% faster (20480 x 10240 x 4096: 1523 -> 1344 us).
+using Tile256S = Cfg<256, 2, 4, 2, 8, 64, true>;
 
 // Chunk swizzle of a k-contiguous LDS row.  Rows of 8 chunks (K step 64):
 // r & 6; rows of 4 chunks (K step 32, two rows per 128 bytes): (r >> 2) & 3.
@@ -253,12 +265,12 @@ __device__ __forceinline__ int swz(int r) {
 }
 
 // One operand tile: ROWS rows of a [rows][ld] matrix contiguous along k.
-template <int ROWS, int BK_>
+template <int ROWS, int BK_, int NI = NW>
 struct Copy {
     static constexpr int CPR = BK_ / 8;            // 16-byte chunks per LDS row
     static constexpr int RPI = 64 / CPR;           // rows per copy instruction
     static constexpr int WI = ROWS / RPI;          // copy instructions per stage
-    static constexpr int PER = (WI + NW - 1) / NW; // per wave (some waves one fewer)
+    static constexpr int PER = (WI + NI - 1) / NI; // per issuing wave (some one fewer)
     static_assert(ROWS % RPI == 0, "rows per copy instruction");
     u32x4 rs;
     uint32_t vlane;       // this lane's byte offset within its instruction's rows
@@ -281,15 +293,16 @@ struct Copy {
         nmine = 0;
 #pragma unroll
         for (int i = 0; i < PER; ++i)
-            if (wave + NW * i < WI) nmine = i + 1;
+            if (wave + NI * i < WI) nmine = i + 1;
     }
-    // Copy of the K step at k0 into LDS stage `dst` (k past K reads zeros).
+    // Copy of the K step at k0 into LDS stage `dst` (k past K reads zeros);
+    // `wave` is this wave's index among the NI issuing waves.
     __device__ __forceinline__ void issue(uint16_t* dst, int64_t k0, int wave) const {
         const bool tail = k0 + BK_ > K;
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
-            const int ins = wave + NW * i;
-            if (PER * NW != WI && ins >= WI) break;   // wave-uniform
+            const int ins = wave + NI * i;
+            if (PER * NI != WI && ins >= WI) break;   // wave-uniform
             uint32_t off = vlane + (uint32_t)ins * ins_stride;
             if (tail && k0 + kc >= K) off = kOob;
             lds_dma16(rs, dst + (size_t)ins * 64 * 8, off, (uint32_t)(k0 * 2));
@@ -409,7 +422,8 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
     static_assert((A_K && B_K) || BK == nt::BK, "row-contiguous operands use K steps of 64");
     constexpr int WM = C::WM, WN = C::WN, FM = C::FM, FN = C::FN;
     constexpr int A_EL = C::A_EL, STAGE = C::STAGE;
-    __shared__ __attribute__((aligned(1024))) uint16_t smem[STAGES * STAGE];
+    static_assert(!C::SPLIT || (A_K && B_K), "split rings: k-contiguous operands");
+    __shared__ __attribute__((aligned(1024))) uint16_t smem[C::LDS_EL];
     // issue priority above the reduction waves that share the CUs while
     // the next chunk's reduction runs beside this GEMM (measured +0.4%)
     __builtin_amdgcn_s_setprio(1);
@@ -429,85 +443,161 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
     const int64_t kb = (int64_t)split * a.ksplit;
     const int64_t kn = min(a.K - kb, a.ksplit);    // this split's contraction
 
-    // split k offset: along a row (k-contiguous operand) or down the rows
-    OpCopy<BM, A_K, BK> ca;
-    OpCopy<BN, B_K, BK> cb;
-    ca.init(a.A + (A_K ? kb : kb * a.lda), a.lda, m0, a.M, kn, wave, lane);
-    cb.init(a.B + (B_K ? kb : kb * a.ldb), a.ldb, n0, a.N, kn, wave, lane);
-    constexpr int LA = OpCopy<BM, A_K, BK>::PER, LB = OpCopy<BN, B_K, BK>::PER;
-    const int loads = ca.nmine + cb.nmine;   // copy instructions per step (wave-uniform)
-
     f32x4 acc[FM][FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
     const int nk = (int)((kn + BK - 1) / BK);
-    auto issue_step = [&](int q) {
-        uint16_t* dst = smem + (q % STAGES) * STAGE;
-        ca.issue(dst, (int64_t)q * BK, wave);
-        cb.issue(dst + A_EL, (int64_t)q * BK, wave);
-    };
-    // wait until this wave's copies are complete except those of the newest
-    // `keep` steps (0, 1, 2); copies complete in issue order
-    auto wait_copies = [&](int keep) {
-        if (keep <= 0) { wait_vmcnt<0>(); return; }
-        if (keep == 1) {
-            if (loads == LA + LB) wait_vmcnt<LA + LB>();
-            else if (loads == LA + LB - 1) wait_vmcnt<LA + LB - 1>();
-            else wait_vmcnt<LA + LB - 2>();
-            return;
-        }
-        if (loads == LA + LB) wait_vmcnt<2 * (LA + LB)>();
-        else if (loads == LA + LB - 1) wait_vmcnt<2 * (LA + LB - 1)>();
-        else wait_vmcnt<2 * (LA + LB - 2)>();
-    };
-
-    if (nk > 0) {   // (uniform) every wave runs the same number of barriers
-        for (int q = 0; q < STAGES - 1 && q < nk; ++q) issue_step(q);
-        // step 0 landed; the later prologue steps may stay in flight
-        wait_copies(min(STAGES - 2, nk - 1));
-        barrier();               // step 0 visible to every wave
-        if (grpB) barrier();     // group B starts one phase late
-
-        bf16x8 fa[KS][FM], fb[KS][FN];
-        for (int p = 0; p < nk; ++p) {
-            // memory phase: copy step p+STAGES-1 into the stage step p-1 used
-            // (both groups finished reading it before this phase), read step p
-            const uint16_t* sa = smem + (p % STAGES) * STAGE;
-            const uint16_t* sb = sa + A_EL;
-            if (p + STAGES - 1 < nk) issue_step(p + STAGES - 1);
-            // the copies of steps p+2 .. p+STAGES-1 may stay in flight below
-            const int more = min(STAGES - 2, nk - 2 - p);
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-                for (int i = 0; i < FM; ++i)
-                    fa[ks][i] = op_frag<BM, A_K, BK>(sa, wm * WM + i * MF, ks, lane);
-#pragma unroll
-                for (int j = 0; j < FN; ++j)
-                    fb[ks][j] = op_frag<BN, B_K, BK>(sb, wn * WN + j * MF, ks, lane);
+    if constexpr (C::SPLIT) {
+        // Split rings.  Group A (waves 0-3) copies the B tile of step p+1 in
+        // its memory phase of step p into the two-stage B ring; group B
+        // (waves 4-7) copies the A tile of step p+2 in its memory phase of
+        // step p into the three-stage A ring.  The slots written are those of
+        // step p-1, which both groups have read by then.  Group A waits for
+        // its copies at the end of its compute phase (two phases after
+        // issue), group B for those of step p+1 at the end of its memory
+        // phase (three phases after issue), so that no copy must land within
+        // the phase it was issued in.  Each wave issues 8 copy instructions
+        // per step, as in the shared ring.
+        constexpr int B_EL = C::B_EL, RA = C::RA, RB = C::RB;
+        uint16_t* ringA = smem;
+        uint16_t* ringB = smem + RA * A_EL;
+        Copy<BM, BK, 4> ca;
+        Copy<BN, BK, 4> cb;
+        const int w4 = wave & 3;
+        // both initialised by every wave, so the resources stay scalar
+        ca.init(a.A + kb, a.lda, m0, a.M, kn, w4, lane);
+        cb.init(a.B + kb, a.ldb, n0, a.N, kn, w4, lane);
+        static_assert(Copy<BM, BK, 4>::PER * 4 == Copy<BM, BK, 4>::WI &&
+                      Copy<BN, BK, 4>::PER * 4 == Copy<BN, BK, 4>::WI, "equal shares");
+        constexpr int LA = Copy<BM, BK, 4>::PER;   // copy instructions per step, group B
+        if (nk > 0) {   // (uniform) every wave runs the same number of barriers
+            if (grpB) {
+                ca.issue(ringA, 0, w4);
+                if (nk > 1) ca.issue(ringA + A_EL, BK, w4);
+                if (nk > 1) wait_vmcnt<LA>();   // step 0 landed, step 1 may fly
+                else wait_vmcnt<0>();
+            } else {
+                cb.issue(ringB, 0, w4);
+                wait_vmcnt<0>();
             }
-            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-            // before group A's next memory phase this wave's copies of step
-            // p+1 have landed (with three stages those of step p+2 may still
-            // be in flight)
-            if (grpB) wait_copies(more);
-            barrier();
-            // compute phase
+            barrier();               // step 0 visible to every wave
+            if (grpB) barrier();     // group B starts one phase late
+
+            bf16x8 fa[KS][FM], fb[KS][FN];
+            for (int p = 0; p < nk; ++p) {
+                const uint16_t* sa = ringA + (p % RA) * A_EL;
+                const uint16_t* sb = ringB + (p % RB) * B_EL;
+                const bool ahead = p + 2 < nk;
+                if (!grpB) {
+                    if (p + 1 < nk) cb.issue(ringB + ((p + 1) % RB) * B_EL, (int64_t)(p + 1) * BK, w4);
+                } else if (ahead) {
+                    ca.issue(ringA + ((p + 2) % RA) * A_EL, (int64_t)(p + 2) * BK, w4);
+                }
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks)
+                for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
-                for (int i = 0; i < FM; ++i)
+                    for (int i = 0; i < FM; ++i) fa[ks][i] = frag<BK>(sa, wm * WM + i * MF, ks, lane);
+#pragma unroll
+                    for (int j = 0; j < FN; ++j) fb[ks][j] = frag<BK>(sb, wn * WN + j * MF, ks, lane);
+                }
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+                // group B: its copies of step p+1 have landed (those of p+2 may fly)
+                if (grpB) {
+                    if (ahead) wait_vmcnt<LA>();
+                    else wait_vmcnt<0>();
+                }
+                barrier();
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+                    for (int i = 0; i < FM; ++i)
+#pragma unroll
+                        for (int j = 0; j < FN; ++j)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                fb[ks][j], fa[ks][i], acc[i][j], 0, 0, 0);
+                // group A: its copies of step p+1 have landed
+                if (!grpB) wait_vmcnt<0>();
+                if (!(grpB && p == nk - 1)) barrier();
+            }
+            wait_vmcnt<0>();
+        }
+    } else {
+        // split k offset: along a row (k-contiguous operand) or down the rows
+        OpCopy<BM, A_K, BK> ca;
+        OpCopy<BN, B_K, BK> cb;
+        ca.init(a.A + (A_K ? kb : kb * a.lda), a.lda, m0, a.M, kn, wave, lane);
+        cb.init(a.B + (B_K ? kb : kb * a.ldb), a.ldb, n0, a.N, kn, wave, lane);
+        constexpr int LA = OpCopy<BM, A_K, BK>::PER, LB = OpCopy<BN, B_K, BK>::PER;
+        const int loads = ca.nmine + cb.nmine;   // copy instructions per step (wave-uniform)
+
+
+        auto issue_step = [&](int q) {
+            uint16_t* dst = smem + (q % STAGES) * STAGE;
+            ca.issue(dst, (int64_t)q * BK, wave);
+            cb.issue(dst + A_EL, (int64_t)q * BK, wave);
+        };
+        // wait until this wave's copies are complete except those of the newest
+        // `keep` steps (0, 1, 2); copies complete in issue order
+        auto wait_copies = [&](int keep) {
+            if (keep <= 0) { wait_vmcnt<0>(); return; }
+            if (keep == 1) {
+                if (loads == LA + LB) wait_vmcnt<LA + LB>();
+                else if (loads == LA + LB - 1) wait_vmcnt<LA + LB - 1>();
+                else wait_vmcnt<LA + LB - 2>();
+                return;
+            }
+            if (loads == LA + LB) wait_vmcnt<2 * (LA + LB)>();
+            else if (loads == LA + LB - 1) wait_vmcnt<2 * (LA + LB - 1)>();
+            else wait_vmcnt<2 * (LA + LB - 2)>();
+        };
+
+        if (nk > 0) {   // (uniform) every wave runs the same number of barriers
+            for (int q = 0; q < STAGES - 1 && q < nk; ++q) issue_step(q);
+            // step 0 landed; the later prologue steps may stay in flight
+            wait_copies(min(STAGES - 2, nk - 1));
+            barrier();               // step 0 visible to every wave
+            if (grpB) barrier();     // group B starts one phase late
+
+            bf16x8 fa[KS][FM], fb[KS][FN];
+            for (int p = 0; p < nk; ++p) {
+                // memory phase: copy step p+STAGES-1 into the stage step p-1 used
+                // (both groups finished reading it before this phase), read step p
+                const uint16_t* sa = smem + (p % STAGES) * STAGE;
+                const uint16_t* sb = sa + A_EL;
+                if (p + STAGES - 1 < nk) issue_step(p + STAGES - 1);
+                // the copies of steps p+2 .. p+STAGES-1 may stay in flight below
+                const int more = min(STAGES - 2, nk - 2 - p);
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+                    for (int i = 0; i < FM; ++i)
+                        fa[ks][i] = op_frag<BM, A_K, BK>(sa, wm * WM + i * MF, ks, lane);
 #pragma unroll
                     for (int j = 0; j < FN; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[ks][j], fa[ks][i],
-                                                                            acc[i][j], 0, 0, 0);
-            if (!grpB) wait_copies(more);
-            if (!(grpB && p == nk - 1)) barrier();
+                        fb[ks][j] = op_frag<BN, B_K, BK>(sb, wn * WN + j * MF, ks, lane);
+                }
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+                // before group A's next memory phase this wave's copies of step
+                // p+1 have landed (with three stages those of step p+2 may still
+                // be in flight)
+                if (grpB) wait_copies(more);
+                barrier();
+                // compute phase
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+                    for (int i = 0; i < FM; ++i)
+#pragma unroll
+                        for (int j = 0; j < FN; ++j)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[ks][j], fa[ks][i],
+                                                                                acc[i][j], 0, 0, 0);
+                if (!grpB) wait_copies(more);
+                if (!(grpB && p == nk - 1)) barrier();
+            }
+            wait_vmcnt<0>();
         }
-        wait_vmcnt<0>();
     }
 
     // Epilogue.  Lane holds C(m = base_m + lane%16, n = base_n + 4*(lane/16) + 0..3)
@@ -634,6 +724,7 @@ hipError_t launch_pp(const GemmProblem& p, hipStream_t s) {
     if (p.splits > 1) return launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
     if constexpr (A_K && B_K) {
         if (nt_use_320(p)) return launch_pp_cfg<nt::Tile320, A_K, B_K, EPI, OUT_BF16>(p, s);
+        if (nt_use_256(p)) return launch_pp_cfg<nt::Tile256S, A_K, B_K, EPI, OUT_BF16>(p, s);
     }
     return nt_use_256(p) ? launch_pp_cfg<nt::Tile256, A_K, B_K, EPI, OUT_BF16>(p, s)
                          : launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
