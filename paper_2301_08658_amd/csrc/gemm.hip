@@ -644,11 +644,9 @@ KArgs kargs(const GemmProblem& p, int bm, int bn) {
     return a;
 }
 
-// 256 x 256 tiles (30% fewer copied bytes per FLOP) for products whose last
-// wave of such tiles is at least 90% full (256 CUs): the dW products and the
-// QKV forward of the wide layer (1.10 -> 1.04 ms); 256 x 160 tiles otherwise
-// True when tiles of width bn fill their last wave of 256 concurrent tiles
-// to at least 90%.
+// Products with a row-contiguous operand (the path without a workspace):
+// 256 x 256 tiles (30% fewer copied bytes per FLOP) when their last wave of
+// 256 concurrent tiles is at least 90% full, 256 x 160 otherwise.
 bool fills_waves(const GemmProblem& p, int64_t bn) {
     constexpr int64_t kCUs = 256;
     const int64_t tiles = ((p.M + nt::BM - 1) / nt::BM) * ((p.N + bn - 1) / bn);
@@ -658,20 +656,39 @@ bool fills_waves(const GemmProblem& p, int64_t bn) {
 
 bool nt_use_256(const GemmProblem& p) { return fills_waves(p, 256); }
 
-// 256 x 320 tiles (K steps of 32) for k-contiguous operands, unsplit, when
-// 256 x 256 tiles would leave their last wave short and 320-wide ones do not
-// (measured: 4096 x 10240 x 20480 at 1289 TFLOP/s against 1208 for
-// 256 x 160; where 256 x 256 tiles fill their waves they are faster)
 // Buffer offsets are 32-bit and a resource covers at most 0x7fffff00 bytes:
 // the rows one tile copies from an operand contiguous along k (BM rows of A,
 // BN rows of B) must span less than that.
 constexpr int64_t kMaxSpan = 0x7fffff00;
 bool rows_fit(int64_t rows, int64_t ld) { return rows * ld * 2 <= kMaxSpan; }
 
-bool nt_use_320(const GemmProblem& p) {
-    return p.layout == LAYOUT_NT && p.splits <= 1 && !fills_waves(p, 256) &&
-           fills_waves(p, 320) && rows_fit(320, p.ldb);
+// Tile configuration of an unsplit product with both operands contiguous
+// along k: the one with the least modelled time, (waves of 256 concurrent
+// tiles) x (tile width / relative per-CU rate), where a last wave that is a
+// fraction f full costs 0.5 + 0.5 f of a full one (its tiles share L2 and
+// HBM with fewer others).  Relative rates measured on the block's products
+// with every CU busy: 256 x 160 0.8, 256 x 320 (K steps of 32) 0.9,
+// 256 x 256 with split rings 1.0.  The 256 x 256 tiles are preferred within
+// 5%: they leave CUs to the reductions that run beside a one-wave product.
+enum NtCfg { NT_160, NT_256S, NT_320 };
+
+double nt_cost(const GemmProblem& p, int64_t bn, double rate) {
+    constexpr int64_t kCUs = 256;
+    const int64_t tiles = ((p.M + nt::BM - 1) / nt::BM) * ((p.N + bn - 1) / bn);
+    const int64_t full = tiles / kCUs, rest = tiles % kCUs;
+    const double waves = (double)full + (rest ? 0.5 + 0.5 * (double)rest / kCUs : 0.0);
+    return waves * (double)bn / rate;
 }
+
+NtCfg nt_pick(const GemmProblem& p) {
+    const double c160 = nt_cost(p, 160, 0.8), c256 = nt_cost(p, 256, 1.0);
+    const double c320 = rows_fit(320, p.ldb) ? nt_cost(p, 320, 0.9) : 1e300;
+    const double other = c160 < c320 ? c160 : c320;
+    if (c256 <= 1.05 * other) return NT_256S;
+    return c160 <= c320 ? NT_160 : NT_320;
+}
+
+bool nt_kcontig(const GemmProblem& p) { return p.layout == LAYOUT_NT && p.splits <= 1; }
 
 // Split-K plan of an NT product written to fp32: the S in 1..kMaxSplits
 // that minimises a two-term cost model, (rounds of 256 concurrent 256 x 160
@@ -723,8 +740,11 @@ template <bool A_K, bool B_K, int EPI, bool OUT_BF16>
 hipError_t launch_pp(const GemmProblem& p, hipStream_t s) {
     if (p.splits > 1) return launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
     if constexpr (A_K && B_K) {
-        if (nt_use_320(p)) return launch_pp_cfg<nt::Tile320, A_K, B_K, EPI, OUT_BF16>(p, s);
-        if (nt_use_256(p)) return launch_pp_cfg<nt::Tile256S, A_K, B_K, EPI, OUT_BF16>(p, s);
+        switch (nt_pick(p)) {
+        case NT_256S: return launch_pp_cfg<nt::Tile256S, A_K, B_K, EPI, OUT_BF16>(p, s);
+        case NT_320: return launch_pp_cfg<nt::Tile320, A_K, B_K, EPI, OUT_BF16>(p, s);
+        default: return launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
+        }
     }
     return nt_use_256(p) ? launch_pp_cfg<nt::Tile256, A_K, B_K, EPI, OUT_BF16>(p, s)
                          : launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
@@ -753,7 +773,10 @@ const char* gemm_kernel_name(const GemmProblem& p) {
                                             {"gemm_tn", "gemm_tn256", "gemm_tn_splitk"}};
     const int l = p.layout == LAYOUT_NN ? 0 : p.layout == LAYOUT_NT ? 1 : p.layout == LAYOUT_TN ? 2 : -1;
     if (l < 0) return "gemm_?";
-    if (nt_use_320(p)) return "gemm_nt320";
+    if (nt_kcontig(p)) {
+        const NtCfg c = nt_pick(p);
+        return c == NT_320 ? "gemm_nt320" : c == NT_256S ? "gemm_nt256" : "gemm_nt";
+    }
     return names[l][p.splits > 1 ? 2 : nt_use_256(p) ? 1 : 0];
 }
 
@@ -765,7 +788,7 @@ hipError_t launch_gemm(const GemmProblem& p, hipStream_t s) {
     if (p.M <= 0 || p.N <= 0) return hipSuccess;
     // buffer offsets are 32-bit: one tile's rows of either operand must span
     // < 2 GiB (256 rows covers the 160- and 256-wide tiles and the 64 k rows
-    // of a row-contiguous operand; nt_use_320 checks its 320 rows itself)
+    // of a row-contiguous operand; nt_pick checks the 320 rows itself)
     if (!rows_fit(256, p.lda) || !rows_fit(256, p.ldb)) return hipErrorInvalidValue;
     const bool b16 = p.out_bf16;
     if (p.nparts > kMaxFusedParts || (p.nparts > 1 && (p.splits > 1 || p.own < 0 ||
