@@ -271,9 +271,11 @@ typedef struct {
 
 /* Workspace for the block calls' transposed-layout path (bytes): the larger
  * of the forward's need and the backward's for weights in `weight_layout`
- * (atp_weight_layout).  The forward keeps W^T of each weight stored
- * [k_loc][n_loc] (n_loc rows of k_loc + 64 bf16 values; weights stored
- * [n_loc][k_loc] need no copy).  The backward keeps X^T of x, the attention
+ * (atp_weight_layout).  The forward keeps W^T of a weight stored
+ * [k_loc][n_loc] (n_loc rows of k_loc + 64 bf16 values) when, at some
+ * valid chunk count, its products are split over k or are not shaped for
+ * the 256 x 256 tiles that stream W as stored as fast as W^T; weights
+ * stored [n_loc][k_loc] need no copy.  The backward keeps X^T of x, the attention
  * block and H, and dY^T of the four linears (cols rows of tokens + 64 bf16
  * values each), for weights stored [n_loc][k_loc] one copy of the largest
  * weight in [k_loc][n_loc] order (k_loc rows of n_loc + 64 values, reused
@@ -341,8 +343,10 @@ atp_status atp_transpose_bf16(int64_t rows, int64_t cols, const void* src, int64
  * workspace (nullable, 256-byte aligned): when ws_bytes is at least the
  * forward's need (atp_block_workspace_path) the products run with both
  * operands contiguous along k, the faster layout (weights stored
- * [k_loc][n_loc] are first copied there as W^T; weights stored
- * [n_loc][k_loc] already are), and a chunk product with too few output
+ * [k_loc][n_loc] are first copied there as W^T, except for a linear whose
+ * products, at this chunk count, run unsplit on the 256 x 256 tiles that
+ * stream W as stored as fast; weights stored [n_loc][k_loc] already are
+ * contiguous along k), and a chunk product with too few output
  * tiles to fill the chip is split over its contraction, the splits' fp32
  * slabs summed in split order into the own partial before the chunk's
  * reduction reads it.  Without the workspace the products read W as

@@ -364,13 +364,38 @@ size_t slab_bytes(const BlockPlan& P, int64_t tokens, bool bwd) {
 
 bool valid_layout(int32_t l) { return l == ATP_W_KN || l == ATP_W_NK; }
 
+// True when the forward of linear L with `chunks` chunks reads weights
+// stored [k][n] as they are on the workspace path: its products stream NN
+// as fast as NT from a W^T copy and are not split over k.  A linear whose
+// group has one member runs one product over all tokens; the others run one
+// product per chunk.  Otherwise the forward first copies W^T into the
+// workspace.
+bool fwd_reads_w(const BlockPlan& P, int L, int64_t tokens, int chunks) {
+    const atp_shard& g = P.g[L];
+    if (g.red_size <= 1) return atp::nn_streams_like_nt(tokens, g.n_loc);
+    const int64_t mc = tokens / chunks;
+    int64_t ks = 0;
+    return atp::nt_split_plan(mc, g.n_loc, g.k_loc, &ks) <= 1 &&
+           atp::nn_streams_like_nt(mc, g.n_loc);
+}
+
+// True when some chunk count makes the forward of linear L copy W^T (the
+// workspace holds its copy whatever the chunk count, as for the slabs).
+bool fwd_may_copy_w(const BlockPlan& P, int L, int64_t tokens) {
+    for (int c = 1; c <= ATP_MAX_CHUNKS; ++c)
+        if (tokens % c == 0 && !fwd_reads_w(P, L, tokens, c)) return true;
+    return false;
+}
+
 // The forward's pieces: the slabs, and W^T ([n_loc][k_loc]) of weights
-// stored [k_loc][n_loc] (weights stored [n_loc][k_loc] are read as they are).
+// stored [k_loc][n_loc] that the forward may copy (weights stored
+// [n_loc][k_loc] are read as they are).
 size_t ws_fwd_bytes(const BlockPlan& P, int64_t tokens, int32_t layout) {
     size_t b = ws_round(slab_bytes(P, tokens, false));
     if (layout == ATP_W_KN)
         for (int L = 0; L < 4; ++L)
-            b += ws_round((size_t)P.g[L].n_loc * ws_pitch(P.g[L].k_loc) * 2);
+            if (fwd_may_copy_w(P, L, tokens))
+                b += ws_round((size_t)P.g[L].n_loc * ws_pitch(P.g[L].k_loc) * 2);
     return b;
 }
 
@@ -1119,9 +1144,10 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
 
     // With a large enough workspace every forward product runs with both
     // operands contiguous along k (the layout the GEMM kernel streams
-    // fastest; weights stored [k][n] are first copied there as W^T), and
-    // chunk products with too few tiles to fill the chip are split over k
-    // into slabs there.  The direct path never runs under graph capture.
+    // fastest; weights stored [k][n] are first copied there as W^T, unless
+    // the linear's products stream NN as fast: fwd_reads_w), and chunk
+    // products with too few tiles to fill the chip are split over k into
+    // slabs there.  The direct path never runs under graph capture.
     const bool ws = workspace && takes_ws_path(P, tokens, w->layout, ws_bytes, 0);
     if (!ws) ATP_CHECK(refuse_capture_of_direct_path(compute_stream));
 
@@ -1141,14 +1167,17 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         Carver c{static_cast<char*>(workspace)};
         if (kn)
             for (int L = 0; L < 4; ++L)
-                wt[L] = c.take((size_t)P.g[L].n_loc * ws_pitch(P.g[L].k_loc) * 2);
+                if (fwd_may_copy_w(P, L, tokens)) {
+                    uint16_t* t = c.take((size_t)P.g[L].n_loc * ws_pitch(P.g[L].k_loc) * 2);
+                    if (!fwd_reads_w(P, L, tokens, chunks)) wt[L] = t;
+                }
         slab = reinterpret_cast<float*>(c.take(slab_bytes(P, tokens, false)));
     }
     // W^T of linear L (weights stored [k][n]), written before the linear's
     // first GEMM (same stream)
     bool wt_done[4] = {false, false, false, false};
     auto need_wt = [&](int L) -> atp_status {
-        if (!ws || !kn || wt_done[L]) return ATP_OK;
+        if (!wt[L] || wt_done[L]) return ATP_OK;
         const atp_shard& g = P.g[L];
         ATP_CHECK(run_transpose(w->w[L], w->ldw[L], g.k_loc, g.n_loc, wt[L], ws_pitch(g.k_loc),
                                 S.cs));
@@ -1156,14 +1185,14 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         return ATP_OK;
     };
     // the product X W of linear L: NT from W^T (the workspace copy, or the
-    // weight itself when stored [n][k]), or NN from W stored [k][n]
+    // weight itself when stored [n][k]), or NN from W stored [k][n] (no copy)
     auto fwd_problem = [&](int L, const void* A, int64_t lda, void* C, int64_t ldc, bool b16,
                            int epi, int64_t M) {
         const atp_shard& g = P.g[L];
         if (!kn)
             return gemm_problem(atp::LAYOUT_NT, A, lda, w->w[L], w->ldw[L], C, ldc, b16, epi, M,
                                 g.n_loc, g.k_loc);
-        if (ws)
+        if (wt[L])
             return gemm_problem(atp::LAYOUT_NT, A, lda, wt[L], ws_pitch(g.k_loc), C, ldc, b16,
                                 epi, M, g.n_loc, g.k_loc);
         return gemm_problem(atp::LAYOUT_NN, A, lda, w->w[L], w->ldw[L], C, ldc, b16, epi, M,

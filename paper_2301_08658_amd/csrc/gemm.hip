@@ -239,8 +239,9 @@ struct Cfg {
 // rate 81% against 74% for 8 x 4)
 using Tile160 = Cfg<160, 4, 2, 3, 4>;
 // 256 x 256: two stages (128 KB); waves of 128 x 64; 30% fewer copied bytes
-// per FLOP than 256 x 160, but 62.5% of its tile count per launch.  Used for
-// row-contiguous operands; with two shared stages group B's copies must land
+// per FLOP than 256 x 160, but 62.5% of its tile count per launch.  Used when
+// both operands are row-contiguous (split rings would need more than 256
+// registers there); with two shared stages group B's copies must land
 // within the phase that issues them, which Tile256S avoids.
 using Tile256 = Cfg<256, 2, 4, 2, 8>;
 // 256 x 320 in K steps of 32: four stages (144 KB); waves of 128 x 80; 36 KB
@@ -249,7 +250,7 @@ using Tile256 = Cfg<256, 2, 4, 2, 8>;
 using Tile320 = Cfg<320, 2, 4, 4, 4, 32>;
 // 256 x 256 in K steps of 64 with split rings (160 KB): group B copies A into
 // a three-stage ring and group A copies B into a two-stage ring, so every
-// copy has at least two phases to land (k-contiguous operands only).
+// copy has at least two phases to land.
 // Measured in the benchmark step against Tile256: every 256 x 256 product
 // 10-13% faster (20480 x 10240 x 4096: 1523 -> 1344 us).
 using Tile256S = Cfg<256, 2, 4, 2, 8, 64, true>;
@@ -337,12 +338,12 @@ __device__ __forceinline__ int tchunk(int k, int pos) {   // inverse of tpos
     else return pos ^ (2 * (k & 3) + 8 * ((k >> 3) & 1));
 }
 
-template <int ROWS>
+template <int ROWS, int NI = NW>
 struct CopyT {
     static_assert(ROWS == 160 || ROWS == 256, "tile widths with a conflict-free layout");
     static constexpr int CPK = ROWS / 8;            // 16-byte chunks per k row
     static constexpr int WI = BK * CPK / 64;        // copy instructions per stage
-    static constexpr int PER = (WI + NW - 1) / NW;  // per wave (some waves one fewer)
+    static constexpr int PER = (WI + NI - 1) / NI;  // per issuing wave (some one fewer)
     static_assert(BK * CPK % 64 == 0, "whole copy instructions");
     const uint16_t* base;   // element (k = 0, column col0)
     int64_t ld, K;
@@ -357,7 +358,7 @@ struct CopyT {
         nmine = 0;
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
-            const int ins = wave + NW * i;
+            const int ins = wave + NI * i;
             const int p = ins * 64 + lane;
             const int k = p / CPK;
             const int c = tchunk<ROWS>(k, p % CPK);
@@ -365,15 +366,16 @@ struct CopyT {
             if (ins < WI) nmine = i + 1;
         }
     }
-    // Copy of the K step at k0 into LDS stage `dst` (rows past K read zeros).
+    // Copy of the K step at k0 into LDS stage `dst` (rows past K read zeros);
+    // `wave` is this wave's index among the NI issuing waves.
     __device__ __forceinline__ void issue(uint16_t* dst, int64_t k0, int wave) const {
         const int64_t left = K - k0;
         const int64_t vk = left < 0 ? 0 : (left < BK ? left : BK);
         const u32x4 rs = rsrc_words(base + k0 * ld, vk * ld * 2);
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
-            const int ins = wave + NW * i;
-            if (PER * NW != WI && ins >= WI) break;   // wave-uniform
+            const int ins = wave + NI * i;
+            if (PER * NI != WI && ins >= WI) break;   // wave-uniform
             lds_dma16(rs, dst + (size_t)ins * 64 * 8, voff[i], 0u);
         }
     }
@@ -397,8 +399,8 @@ __device__ __forceinline__ bf16x8 frag_t(const uint16_t* src, int r0, int ks, in
 
 // Operand copy and fragment read for a tile contiguous along k (KC) or
 // along its rows.
-template <int ROWS, bool KC, int BK_>
-using OpCopy = typename std::conditional<KC, Copy<ROWS, BK_>, CopyT<ROWS>>::type;
+template <int ROWS, bool KC, int BK_, int NI = NW>
+using OpCopy = typename std::conditional<KC, Copy<ROWS, BK_, NI>, CopyT<ROWS, NI>>::type;
 template <int ROWS, bool KC, int BK_>
 __device__ __forceinline__ bf16x8 op_frag(const uint16_t* src, int r0, int ks, int lane) {
     if constexpr (KC) return frag<BK_>(src, r0, ks, lane);
@@ -422,7 +424,6 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
     static_assert((A_K && B_K) || BK == nt::BK, "row-contiguous operands use K steps of 64");
     constexpr int WM = C::WM, WN = C::WN, FM = C::FM, FN = C::FN;
     constexpr int A_EL = C::A_EL, STAGE = C::STAGE;
-    static_assert(!C::SPLIT || (A_K && B_K), "split rings: k-contiguous operands");
     __shared__ __attribute__((aligned(1024))) uint16_t smem[C::LDS_EL];
     // issue priority above the reduction waves that share the CUs while
     // the next chunk's reduction runs beside this GEMM (measured +0.4%)
@@ -463,16 +464,16 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
         constexpr int B_EL = C::B_EL, RA = C::RA, RB = C::RB;
         uint16_t* ringA = smem;
         uint16_t* ringB = smem + RA * A_EL;
-        Copy<BM, BK, 4> ca;
-        Copy<BN, BK, 4> cb;
+        using CA = OpCopy<BM, A_K, BK, 4>;
+        using CB = OpCopy<BN, B_K, BK, 4>;
+        static_assert(CA::PER * 4 == CA::WI && CB::PER * 4 == CB::WI, "equal shares");
+        constexpr int LA = CA::PER;   // copy instructions per step, group B
         const int w4 = wave & 3;
-        // both initialised by every wave, so the resources stay scalar
-        ca.init(a.A + kb, a.lda, m0, a.M, kn, w4, lane);
-        cb.init(a.B + kb, a.ldb, n0, a.N, kn, w4, lane);
-        static_assert(Copy<BM, BK, 4>::PER * 4 == Copy<BM, BK, 4>::WI &&
-                      Copy<BN, BK, 4>::PER * 4 == Copy<BN, BK, 4>::WI, "equal shares");
-        constexpr int LA = Copy<BM, BK, 4>::PER;   // copy instructions per step, group B
-        if (nk > 0) {   // (uniform) every wave runs the same number of barriers
+        const uint16_t* baseA = a.A + (A_K ? kb : kb * a.lda);
+        const uint16_t* baseB = a.B + (B_K ? kb : kb * a.ldb);
+        // ca copies A (group B), cb copies B (group A)
+        auto mainloop = [&](const auto& ca, const auto& cb) {
+            if (nk <= 0) return;   // (uniform) every wave runs the same number of barriers
             if (grpB) {
                 ca.issue(ringA, 0, w4);
                 if (nk > 1) ca.issue(ringA + A_EL, BK, w4);
@@ -498,9 +499,11 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
-                    for (int i = 0; i < FM; ++i) fa[ks][i] = frag<BK>(sa, wm * WM + i * MF, ks, lane);
+                    for (int i = 0; i < FM; ++i)
+                        fa[ks][i] = op_frag<BM, A_K, BK>(sa, wm * WM + i * MF, ks, lane);
 #pragma unroll
-                    for (int j = 0; j < FN; ++j) fb[ks][j] = frag<BK>(sb, wn * WN + j * MF, ks, lane);
+                    for (int j = 0; j < FN; ++j)
+                        fb[ks][j] = op_frag<BN, B_K, BK>(sb, wn * WN + j * MF, ks, lane);
                 }
                 asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
                 // group B: its copies of step p+1 have landed (those of p+2 may fly)
@@ -522,6 +525,21 @@ __global__ __launch_bounds__(nt::NT, 1) void gemm_nt_kernel(KArgs a) {
                 if (!(grpB && p == nk - 1)) barrier();
             }
             wait_vmcnt<0>();
+        };
+        if constexpr (std::is_same<CA, CB>::value) {
+            // one copier per wave, its operand picked by a uniform select
+            // (the resources stay scalar and one set of offsets is held)
+            CA c;
+            c.init(grpB ? baseA : baseB, grpB ? a.lda : a.ldb, grpB ? m0 : n0, grpB ? a.M : a.N,
+                   kn, w4, lane);
+            mainloop(c, c);
+        } else {
+            // both initialised by every wave, so the resources stay scalar
+            CA ca;
+            CB cb;
+            ca.init(baseA, a.lda, m0, a.M, kn, w4, lane);
+            cb.init(baseB, a.ldb, n0, a.N, kn, w4, lane);
+            mainloop(ca, cb);
         }
     } else {
         // split k offset: along a row (k-contiguous operand) or down the rows
@@ -644,9 +662,9 @@ KArgs kargs(const GemmProblem& p, int bm, int bn) {
     return a;
 }
 
-// Products with a row-contiguous operand (the path without a workspace):
-// 256 x 256 tiles (30% fewer copied bytes per FLOP) when their last wave of
-// 256 concurrent tiles is at least 90% full, 256 x 160 otherwise.
+// Products with both operands row-contiguous (TN: dW on the path without a
+// workspace): 256 x 256 tiles (30% fewer copied bytes per FLOP) when their
+// last wave of 256 concurrent tiles is at least 90% full, 256 x 160 otherwise.
 bool fills_waves(const GemmProblem& p, int64_t bn) {
     constexpr int64_t kCUs = 256;
     const int64_t tiles = ((p.M + nt::BM - 1) / nt::BM) * ((p.N + bn - 1) / bn);
@@ -680,9 +698,9 @@ double nt_cost(const GemmProblem& p, int64_t bn, double rate) {
     return waves * (double)bn / rate;
 }
 
-NtCfg nt_pick(const GemmProblem& p) {
+NtCfg nt_pick(const GemmProblem& p, bool allow320) {
     const double c160 = nt_cost(p, 160, 0.8), c256 = nt_cost(p, 256, 1.0);
-    const double c320 = rows_fit(320, p.ldb) ? nt_cost(p, 320, 0.9) : 1e300;
+    const double c320 = allow320 && rows_fit(320, p.ldb) ? nt_cost(p, 320, 0.9) : 1e300;
     const double other = c160 < c320 ? c160 : c320;
     if (c256 <= 1.05 * other) return NT_256S;
     return c160 <= c320 ? NT_160 : NT_320;
@@ -740,14 +758,23 @@ template <bool A_K, bool B_K, int EPI, bool OUT_BF16>
 hipError_t launch_pp(const GemmProblem& p, hipStream_t s) {
     if (p.splits > 1) return launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
     if constexpr (A_K && B_K) {
-        switch (nt_pick(p)) {
+        switch (nt_pick(p, true)) {
         case NT_256S: return launch_pp_cfg<nt::Tile256S, A_K, B_K, EPI, OUT_BF16>(p, s);
         case NT_320: return launch_pp_cfg<nt::Tile320, A_K, B_K, EPI, OUT_BF16>(p, s);
         default: return launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
         }
     }
-    return nt_use_256(p) ? launch_pp_cfg<nt::Tile256, A_K, B_K, EPI, OUT_BF16>(p, s)
-                         : launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
+    if constexpr (!A_K && !B_K) {
+        // both operands row-contiguous: split rings would need more than 256
+        // registers per lane (the transposing fragment reads' addresses)
+        return nt_use_256(p) ? launch_pp_cfg<nt::Tile256, A_K, B_K, EPI, OUT_BF16>(p, s)
+                             : launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
+    }
+    // A contiguous along k, B along its rows (the forward from W as given):
+    // the same model without the 256 x 320 tiles (k-contiguous only)
+    return nt_pick(p, false) == NT_256S
+               ? launch_pp_cfg<nt::Tile256S, A_K, B_K, EPI, OUT_BF16>(p, s)
+               : launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
 }
 
 }  // namespace
@@ -774,10 +801,20 @@ const char* gemm_kernel_name(const GemmProblem& p) {
     const int l = p.layout == LAYOUT_NN ? 0 : p.layout == LAYOUT_NT ? 1 : p.layout == LAYOUT_TN ? 2 : -1;
     if (l < 0) return "gemm_?";
     if (nt_kcontig(p)) {
-        const NtCfg c = nt_pick(p);
+        const NtCfg c = nt_pick(p, true);
         return c == NT_320 ? "gemm_nt320" : c == NT_256S ? "gemm_nt256" : "gemm_nt";
     }
+    if (p.layout == LAYOUT_NN && p.splits <= 1)
+        return nt_pick(p, false) == NT_256S ? "gemm_nn256" : "gemm_nn";
     return names[l][p.splits > 1 ? 2 : nt_use_256(p) ? 1 : 0];
+}
+
+bool nn_streams_like_nt(int64_t M, int64_t N) {
+    GemmProblem p;
+    p.layout = LAYOUT_NN;
+    p.M = M;
+    p.N = N;
+    return nt_pick(p, false) == NT_256S;
 }
 
 int nt_split_plan(int64_t M, int64_t N, int64_t K, int64_t* ksplit) {

@@ -51,6 +51,11 @@ const char* gemm_kernel_name(const GemmProblem& p);
 // split count S (1: no split) and the k per split (a multiple of 64; the
 // last split may be shorter).  The plan depends on M, N and K only; S *
 // (256-row tiles) * (160-column tiles) never exceeds kMaxSplitTiles.
+// True when an unsplit NN product [M, N] (B read along its rows, the
+// forward from W stored [k][n]) runs on the 256 x 256 tiles with split copy
+// rings, which stream it as fast as NT from a transposed copy.
+bool nn_streams_like_nt(int64_t M, int64_t N);
+
 constexpr int kMaxSplits = 16;
 constexpr int64_t kMaxSplitTiles = 512;
 int nt_split_plan(int64_t M, int64_t N, int64_t K, int64_t* ksplit);

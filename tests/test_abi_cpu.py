@@ -244,7 +244,8 @@ def test_status_strings():
 
 
 def test_block_workspace_bytes_formula():
-    # forward: W^T of the four shards; backward: X^T of x, attention block, H
+    # forward: at most W^T of the four shards (a linear whose products stream
+    # the weight as stored keeps no copy); backward: X^T of x, attention block, H
     # and dY^T of the four linears over the tokens; every row of a copy padded
     # by 64 values (128 bytes); pieces rounded to 256 B.
     # Each side adds the fp32 split-K slabs of its chunk products, at most
@@ -258,7 +259,7 @@ def test_block_workspace_bytes_formula():
                                          ((2, 2), 0, 132, 512, True), ((1, 1), 0, 0, 256, False)]:
         m = B.mesh(d1, d2, 0, 0)
         G = B.block_geometry(m, mode, h)
-        fwd = sum(r((g.k_loc + 64) * g.n_loc * 2) for g in G)
+        fwd = sum(r((g.k_loc + 64) * g.n_loc * 2) for g in G)   # every W^T: an upper bound
         tp = T + 64
         colpart = ((T + 63) // 64) * max(g.n_loc for g in G) * 4   # fp32 column partials for db
         bwd = (r(G[0].k_loc * tp * 2) + r(G[1].k_loc * tp * 2) + r(G[3].k_loc * tp * 2) +
@@ -268,9 +269,9 @@ def test_block_workspace_bytes_formula():
         ws = sizes.pop()
         assert ws % 256 == 0
         if splits:
-            assert max(fwd, bwd) < ws <= max(fwd, bwd) + slab_max
+            assert bwd < ws <= max(fwd, bwd) + slab_max
         else:
-            assert ws == max(fwd, bwd)
+            assert bwd <= ws <= max(fwd, bwd)
     # invalid arguments give 0
     assert B.atp_block_workspace_bytes(B.mesh(2, 2, 0, 0), 7, 128, 512, 1) == 0
     assert B.atp_block_workspace_bytes(B.mesh(2, 2, 0, 0), 0, 128, 500, 1) == 0
@@ -318,7 +319,12 @@ def _least_size(m, mode, T, h, layout, pass_, hi):
 
 def test_block_workspace_weight_layouts():
     """Weights stored [n][k] need no W^T in the forward, and one [k][n] copy
-    of the largest weight (rows padded by 64 values) in the backward."""
+    of the largest weight (rows padded by 64 values) in the backward.  Weights
+    stored [k][n] add the W^T copies of some of the linears to the forward:
+    those whose products, at some chunk count, are split over k or do not
+    run on the 256 x 256 tiles.  On the wide 8 x 1 layer the two unchunked
+    linears (QKV, fc1: one 4096-row product each) read W as stored, while
+    out-proj and fc2 split at 64 chunks and keep their copies."""
     r = lambda b: (b + 255) // 256 * 256  # noqa: E731
     for (d1, d2), mode, T, h in [((8, 1), 0, 4096, 20480), ((2, 4), 1, 8192, 4096),
                                  ((2, 2), 0, 256, 512)]:
@@ -327,11 +333,15 @@ def test_block_workspace_weight_layouts():
         kn = B.atp_block_workspace_bytes(m, mode, T, h, 1, B.ATP_W_KN)
         nk = B.atp_block_workspace_bytes(m, mode, T, h, 1, B.ATP_W_NK)
         wkn = r(max(g.k_loc * (g.n_loc + 64) * 2 for g in G))
-        fwd_wt = sum(r((g.k_loc + 64) * g.n_loc * 2) for g in G)
+        wt = [r((g.k_loc + 64) * g.n_loc * 2) for g in G]
         assert (_least_size(m, mode, T, h, B.ATP_W_NK, 1, nk) -
                 _least_size(m, mode, T, h, B.ATP_W_KN, 1, kn)) == wkn
-        assert (_least_size(m, mode, T, h, B.ATP_W_KN, 0, kn) -
-                _least_size(m, mode, T, h, B.ATP_W_NK, 0, nk)) == fwd_wt
+        extra = (_least_size(m, mode, T, h, B.ATP_W_KN, 0, kn) -
+                 _least_size(m, mode, T, h, B.ATP_W_NK, 0, nk))
+        subsets = {sum(w for i, w in enumerate(wt) if mask >> i & 1) for mask in range(16)}
+        assert extra in subsets, (extra, wt)
+        if (d1, d2) == (8, 1):
+            assert extra == wt[1] + wt[3]
     assert B.atp_block_workspace_bytes(B.mesh(2, 2, 0, 0), 0, 128, 512, 1, 5) == 0
 
 
