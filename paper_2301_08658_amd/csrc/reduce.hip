@@ -205,13 +205,25 @@ __global__ __launch_bounds__(CS_T) void colsum_kernel(const uint16_t* __restrict
 }
 
 // db[c] = (((0 + part_0[c]) + part_1[c]) + ...) over nb row-block partials.
+// The loads of 32 partials are issued before their sums, so a thread waits
+// for memory once per 32 blocks instead of once per block; the additions
+// keep the block order.
 __global__ __launch_bounds__(256) void colsum_finish_kernel(const float* __restrict__ part,
                                                             int64_t ldp, int64_t nb, int64_t N,
                                                             float* __restrict__ db) {
+    constexpr int U = 32;
     const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (c >= N) return;
     float acc = 0.0f;
-    for (int64_t b = 0; b < nb; ++b) acc += part[b * ldp + c];
+    int64_t b = 0;
+    for (; b + U <= nb; b += U) {
+        float v[U];
+#pragma unroll
+        for (int i = 0; i < U; ++i) v[i] = part[(b + i) * ldp + c];
+#pragma unroll
+        for (int i = 0; i < U; ++i) acc += v[i];
+    }
+    for (; b < nb; ++b) acc += part[b * ldp + c];
     db[c] = acc;
 }
 
