@@ -252,8 +252,11 @@ using Tile320 = Cfg<320, 2, 4, 4, 4, 32>;
 // a three-stage ring and group A copies B into a two-stage ring, so every
 // copy has at least two phases to land.
 // Measured in the benchmark step against Tile256: every 256 x 256 product
-// 10-13% faster (20480 x 10240 x 4096: 1523 -> 1344 us).
-using Tile256S = Cfg<256, 2, 4, 2, 8, 64, true>;
+// 10-13% faster (20480 x 10240 x 4096: 1523 -> 1344 us).  The 32 tiles an
+// XCD runs at once form a block of 4 row tiles x 8 column tiles (against 8 x
+// 4: the dominant fp32 products 1.2-1.7% faster, the step 0.4-0.7%, three
+// same-box pairs on each of two boxes).
+using Tile256S = Cfg<256, 2, 4, 2, 4, 64, true>;
 
 // Chunk swizzle of a k-contiguous LDS row.  Rows of 8 chunks (K step 64):
 // r & 6; rows of 4 chunks (K step 32, two rows per 128 bytes): (r >> 2) & 3.
