@@ -766,18 +766,19 @@ hipError_t launch_pp(const GemmProblem& p, hipStream_t s) {
         case NT_320: return launch_pp_cfg<nt::Tile320, A_K, B_K, EPI, OUT_BF16>(p, s);
         default: return launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
         }
-    }
-    if constexpr (!A_K && !B_K) {
+    } else if constexpr (!A_K && !B_K) {
         // both operands row-contiguous: split rings would need more than 256
         // registers per lane (the transposing fragment reads' addresses)
         return nt_use_256(p) ? launch_pp_cfg<nt::Tile256, A_K, B_K, EPI, OUT_BF16>(p, s)
                              : launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
+    } else {
+        // A contiguous along k, B along its rows (the forward from W as
+        // given): the same model without the 256 x 320 tiles (k-contiguous
+        // only)
+        return nt_pick(p, false) == NT_256S
+                   ? launch_pp_cfg<nt::Tile256S, A_K, B_K, EPI, OUT_BF16>(p, s)
+                   : launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
     }
-    // A contiguous along k, B along its rows (the forward from W as given):
-    // the same model without the 256 x 320 tiles (k-contiguous only)
-    return nt_pick(p, false) == NT_256S
-               ? launch_pp_cfg<nt::Tile256S, A_K, B_K, EPI, OUT_BF16>(p, s)
-               : launch_pp_cfg<nt::Tile160, A_K, B_K, EPI, OUT_BF16>(p, s);
 }
 
 }  // namespace
