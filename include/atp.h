@@ -400,10 +400,11 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
  * all-gather) alone.  lse (fp32 [heads_of_device][batch*seq]) receives the
  * natural-log softmax denominator of every row, for the backward.  The
  * caller owns every buffer; work is enqueued on `stream`.
- * Errors: INVALID_ARGUMENT for a bad mesh, negative sizes, NULL or aliased
- * buffers, ld below the row length; SHAPE when h is not a multiple of
- * heads or the heads do not divide over the group; UNSUPPORTED for a head
- * dimension other than 128, sizes above 2^24, misalignment. */
+ * Errors: INVALID_ARGUMENT for a bad mesh, negative sizes, NULL buffers,
+ * qkv and out sharing memory, ld below the row length; SHAPE when h is not
+ * a multiple of heads or the heads do not divide over the group;
+ * UNSUPPORTED for a head dimension other than 128, sizes above 2^24,
+ * misalignment. */
 atp_status atp_attention_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t batch, int64_t seq,
                              int64_t h, int32_t heads, const void* qkv, int64_t ld_qkv,
                              void* out, int64_t ld_out, float* lse, void* stream);
@@ -420,7 +421,7 @@ atp_status atp_attention_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t b
  * lse; with delta_t = dO_t . O_t: dV = P^T dO, dS = P o (dO V^T - delta),
  * dQ = dS K / sqrt(d), dK = dS^T Q / sqrt(d), each accumulated by one
  * workgroup (deterministic).  Errors as atp_attention_fwd; d_qkv must not
- * alias an input. */
+ * share memory with qkv, out or d_out (INVALID_ARGUMENT). */
 atp_status atp_attention_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t batch, int64_t seq,
                              int64_t h, int32_t heads, const void* qkv, int64_t ld_qkv,
                              const void* out, int64_t ld_out, const float* lse, const void* d_out,

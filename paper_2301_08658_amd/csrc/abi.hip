@@ -131,6 +131,17 @@ atp_status check_vec(const void* p, const char* name) {
     return ATP_OK;
 }
 
+// Whether two row-major buffers (rows x ld elements of the given sizes) share
+// any byte; NULL or empty buffers overlap nothing.
+bool overlaps(const void* a, int64_t rows_a, int64_t ld_a, size_t esz_a, const void* b,
+              int64_t rows_b, int64_t ld_b, size_t esz_b) {
+    if (!a || !b || rows_a == 0 || rows_b == 0) return false;
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+    const uintptr_t a1 = a0 + (uintptr_t)(rows_a * ld_a) * esz_a;
+    const uintptr_t b1 = b0 + (uintptr_t)(rows_b * ld_b) * esz_b;
+    return a0 < b1 && b0 < a1;
+}
+
 bool valid_epi(int32_t e) { return e >= ATP_EPI_NONE && e <= ATP_EPI_GELU_BWD; }
 bool valid_dtype(int32_t d) { return d == ATP_F32 || d == ATP_BF16; }
 
@@ -853,7 +864,8 @@ atp_status atp_attention_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t b
     ATP_CHECK(check_mat(out, ap.T, ld_out, ap.out_cols, "out"));
     if (ap.T == 0) return ATP_OK;
     ATP_CHECK(check_vec(lse, "lse"));
-    if (qkv == out) return set_error(ATP_ERR_INVALID_ARGUMENT, "qkv and out must not alias");
+    if (overlaps(qkv, ap.T, ld_qkv, 2, out, ap.T, ld_out, 2))
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "qkv and out must not overlap");
     atp::AttentionProblem p;
     p.qkv = qkv;
     p.ld_qkv = ld_qkv;
@@ -888,8 +900,10 @@ atp_status atp_attention_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t b
     if (ap.T == 0) return ATP_OK;
     ATP_CHECK(check_vec(lse, "lse"));
     ATP_CHECK(check_vec(delta, "delta"));
-    if (d_qkv == qkv || d_qkv == out || d_qkv == d_out)
-        return set_error(ATP_ERR_INVALID_ARGUMENT, "d_qkv must not alias an input");
+    if (overlaps(d_qkv, ap.T, ld_dqkv, 2, qkv, ap.T, ld_qkv, 2) ||
+        overlaps(d_qkv, ap.T, ld_dqkv, 2, out, ap.T, ld_out, 2) ||
+        overlaps(d_qkv, ap.T, ld_dqkv, 2, d_out, ap.T, ld_dout, 2))
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "d_qkv must not overlap an input");
     atp::AttentionBwdProblem p;
     p.qkv = qkv;
     p.ld_qkv = ld_qkv;
@@ -1061,15 +1075,6 @@ atp_status check_attn_weights(const BlockPlan& P, const atp_block_weights* w) {
         ATP_CHECK(check_vec(w->b[i], nm));
     }
     return ATP_OK;
-}
-
-bool overlaps(const void* a, int64_t rows_a, int64_t ld_a, size_t esz_a, const void* b,
-              int64_t rows_b, int64_t ld_b, size_t esz_b) {
-    if (!a || !b || rows_a == 0 || rows_b == 0) return false;
-    const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
-    const uintptr_t a1 = a0 + (uintptr_t)(rows_a * ld_a) * esz_a;
-    const uintptr_t b1 = b0 + (uintptr_t)(rows_b * ld_b) * esz_b;
-    return a0 < b1 && b0 < a1;
 }
 
 }  // namespace

@@ -468,3 +468,27 @@ def test_noalloc_attention_bwd_refuses_beyond_its_scratch():
                                        g.n_loc // 3, FAKE, FAKE, g.n_loc // 3, FAKE, g.n_loc, None)
     assert st == B.ATP_ERR_UNSUPPORTED
     assert "scratch" in atp.binding.last_error()
+
+
+def test_attention_refuses_overlapping_buffers():
+    """The attention core refuses an output that shares memory with an input
+    (not only an identical pointer) before any device work; the addresses
+    are never dereferenced."""
+    lib = atp.load_library()
+    m = atp.mesh(1, 1, 0, 0)
+    T, h, heads = 256, 1024, 8
+    g = atp.block_geometry(m, 0, h)[0]
+    nq, no = g.n_loc, g.n_loc // 3
+    inside = FAKE + 2 * (T // 2) * nq           # a row in the middle of qkv (bf16)
+    past = FAKE + 2 * T * nq                    # the first byte after qkv
+    fwd = lambda out: lib.atp_attention_fwd(ctypes.byref(m), 0, 1, T, h, heads,  # noqa: E731
+                                            FAKE, nq, out, no, FAKE, None)
+    assert fwd(inside) == B.ATP_ERR_INVALID_ARGUMENT
+    assert "overlap" in atp.binding.last_error()
+    far = 0x40000000                            # disjoint from qkv; d_qkv below overlaps it
+    bwd = lambda dqkv: lib.atp_attention_bwd(  # noqa: E731
+        ctypes.byref(m), 0, 1, T, h, heads, FAKE, nq, far, no, FAKE, past, no, dqkv, nq,
+        FAKE, None)
+    for dqkv in (FAKE + 16 * nq, far - 16 * nq, past + 32):
+        assert bwd(dqkv) == B.ATP_ERR_INVALID_ARGUMENT, hex(dqkv)
+        assert "overlap" in atp.binding.last_error()
