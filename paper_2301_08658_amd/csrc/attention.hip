@@ -15,7 +15,7 @@
 //     which puts the 16 lanes of each gfx950 read group on distinct banks.
 //   * A lane holds S(m = lane % 16, n = 16 j + 4 (lane / 16) + e): the rows
 //     are lane-uniform, so the row maximum and sum need only two lane
-//     exchanges (xor 16, xor 32).
+//     exchanges (lane swaps of 16 and 32).
 //   * O += P V: the MFMA sums over its 32 keys in any order as long as both
 //     operands agree, so each 32-key slice takes the keys {4g + e} and
 //     {16 + 4g + e} for lane group g: then P's fragment is the lane's own
@@ -66,6 +66,31 @@ __device__ __forceinline__ int vpos(int n, int c) { return c ^ (2 * (n & 3) + 8 
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// The four lanes l, l ^ 16, l ^ 32, l ^ 48 hold one score row's columns.
+// Their maximum and sum come from gfx950's lane swaps (v_permlane16_swap
+// pairs the 16-lane rows 0-1 and 2-3, v_permlane32_swap the two halves),
+// which stay in the VALU instead of a round trip through LDS.  With both
+// operands x, the first result is the lower member of each pair and the
+// second the upper, so every lane of the four combines the same values in
+// the same order: (r0 op r1) op (r2 op r3), bit-identical in all four.
+__device__ __forceinline__ float row_max4(float x) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x),
+                                                    false, false);
+    x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                    false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+__device__ __forceinline__ float row_sum4(float x) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x),
+                                                    false, false);
+    x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                    false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
 
 // Two floats to bf16 (round to nearest even: one v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
@@ -254,8 +279,7 @@ __global__ __launch_bounds__(NTHR * KG, 2 / KG) void attention_fwd_kernel(AttnAr
                 for (int j = 0; j < 4; ++j)
 #pragma unroll
                     for (int e = 0; e < 4; ++e) mx = fmaxf(mx, s[r][j][e]);
-                mx = fmaxf(mx, __shfl_xor(mx, 16));
-                mx = fmaxf(mx, __shfl_xor(mx, 32));
+                mx = row_max4(mx);
                 const float mnew = fmaxf(mrun[r], mx * a.scale_log2);   // base-2 scaled domain
                 // a row with no visible key yet keeps mnew = -inf: subtract 0
                 const float msub = mnew == -INFINITY ? 0.f : mnew;
@@ -270,8 +294,7 @@ __global__ __launch_bounds__(NTHR * KG, 2 / KG) void attention_fwd_kernel(AttnAr
                         s[r][j][e] = p;
                         rs += p;
                     }
-                rs += __shfl_xor(rs, 16);
-                rs += __shfl_xor(rs, 32);
+                rs = row_sum4(rs);
                 lrun[r] = lrun[r] * alpha + rs;
                 mrun[r] = mnew;
 #pragma unroll
