@@ -77,22 +77,34 @@ def parse():
     ap.add_argument("--comm-cus", type=int, default=0,
                     help="run the reductions on a comm stream restricted to this many CUs "
                          "(hipExtStreamCreateWithCUMask; 0 = all CUs)")
+    ap.add_argument("--pad", type=int, default=0,
+                    help="elements added to the row pitch of every activation, gradient, "
+                         "weight and partial buffer")
     ap.add_argument("--seed", type=int, default=21)
     ap.add_argument("--profile-detail", action="store_true",
                     help="also print per-shape kernel timings to stderr")
     return ap.parse_args()
 
 
-def setup(torch, atp, S, wl, chunks, seed, layout="kn", partials="f32"):
-    """Device-resident seeded inputs and outputs of one device's share."""
+def setup(torch, atp, S, wl, chunks, seed, layout="kn", partials="f32", pad=0):
+    """Device-resident seeded inputs and outputs of one device's share; every
+    2-D buffer's rows are `pad` elements longer than its columns."""
     dev = "cuda:0"
     d1, d2 = wl["mesh"]
     m = atp.mesh(d1, d2, 0, 0)
     bm = atp.ATP_BLOCK_COL if wl["mode"] == "col" else atp.ATP_BLOCK_ROW
     h, T, sw = wl["h"], wl["tokens"], wl["sigma_w"]
     G = atp.block_geometry(m, bm, h)
-    rnd = lambda shape, std, tid, dt=torch.bfloat16: S.randn_device(  # noqa: E731
-        shape, std, seed, tid, dev, dtype=dt)
+    def padded(r, c, dt):
+        return torch.empty((r, c + pad), dtype=dt, device=dev)[:, :c]
+
+    def rnd(shape, std, tid, dt=torch.bfloat16):
+        t = S.randn_device(shape, std, seed, tid, dev, dtype=dt)
+        if pad == 0 or len(shape) != 2:
+            return t
+        out = padded(shape[0], shape[1], dt)
+        out.copy_(t)
+        return out
     kn = layout == "kn"
     pdt = torch.float32 if partials == "f32" else torch.bfloat16
     st = dict(m=m, bm=bm, G=G, T=T, h=h, chunks=chunks,
@@ -101,21 +113,23 @@ def setup(torch, atp, S, wl, chunks, seed, layout="kn", partials="f32"):
     st["a"] = rnd((T, G[1].k_loc), 1.0, S.TID["a"])
     st["w"] = [rnd((g.k_loc, g.n_loc), sw, S.TID["w_" + n]) for g, n in zip(G, LIN)]
     if not kn:
-        st["w"] = [w.t().contiguous() for w in st["w"]]
+        st["w"] = [padded(w.shape[1], w.shape[0], w.dtype).copy_(w.t()) for w in st["w"]]
     st["b"] = [torch.zeros(g.n_loc, dtype=torch.bfloat16, device=dev) for g in G]
-    emp = lambda r, c, dt=torch.bfloat16: torch.empty((r, c), dtype=dt, device=dev)  # noqa
+    emp = lambda r, c, dt=torch.bfloat16: padded(r, c, dt)  # noqa: E731
     st["fwd_tabs"], st["bwd_tabs"] = [], []
     for i, g in enumerate(G):
         if g.red_size > 1:
             sp = S.peer_sigma(g.k_loc, sw, 1.0)
-            tab = [rnd((T, g.n_loc), sp, S.PEER_TID_BASE + 100 * i + j, torch.float32).to(pdt)
+            tab = [padded(T, g.n_loc, pdt).copy_(
+                       rnd((T, g.n_loc), sp, S.PEER_TID_BASE + 100 * i + j, torch.float32))
                    for j in range(g.red_size)]
             st["fwd_tabs"].append(tab)        # entry red_index is overwritten (own)
         else:
             st["fwd_tabs"].append(None)
         if g.bwd_size > 1:
             sp = S.peer_sigma(g.n_loc, sw, 1.0)
-            tab = [rnd((T, g.k_loc), sp, S.BWD_PEER_TID_BASE + 100 * i + j, torch.float32).to(pdt)
+            tab = [padded(T, g.k_loc, pdt).copy_(
+                       rnd((T, g.k_loc), sp, S.BWD_PEER_TID_BASE + 100 * i + j, torch.float32))
                    for j in range(g.bwd_size)]
             st["bwd_tabs"].append(tab)
         else:
@@ -128,8 +142,8 @@ def setup(torch, atp, S, wl, chunks, seed, layout="kn", partials="f32"):
     st["dh_pre"] = emp(T, G[2].n_loc)
     st["dx_qkv"], st["dx_fc1"] = emp(T, G[0].k_loc), emp(T, G[2].k_loc)
     st["d_attn"] = emp(T, G[1].k_loc)
-    st["dw"] = [torch.empty((g.k_loc, g.n_loc) if kn else (g.n_loc, g.k_loc),
-                            dtype=torch.float32, device=dev) for g in G]
+    st["dw"] = [padded(*((g.k_loc, g.n_loc) if kn else (g.n_loc, g.k_loc)), torch.float32)
+                for g in G]
     st["db"] = [torch.empty((g.n_loc,), dtype=torch.float32, device=dev) for g in G]
     return st
 
@@ -537,7 +551,8 @@ def main():
         return
     log(f"[bench] {atp.atp_version()} workload={args.workload} chunks={chunks} "
         f"pass={'fwd' if fwd_only else 'fwd+bwd'}")
-    st = setup(torch, atp, S, wl, chunks, args.seed, args.weight_layout, args.partials)
+    st = setup(torch, atp, S, wl, chunks, args.seed, args.weight_layout, args.partials,
+               args.pad)
     st["bwd_chunks"] = args.bwd_chunks
     st["ws"] = None
     if not args.no_workspace:
