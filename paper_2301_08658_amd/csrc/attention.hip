@@ -239,14 +239,18 @@ __global__ __launch_bounds__(NTHR * KG, 2 / KG) void attention_fwd_kernel(AttnAr
                 cp.issue(kbase, a.ldq, vbase, a.ldq, tok0, (kt + 1) * BN, a.seq,
                          buf[(i + 1) & 1][0], buf[(i + 1) & 1][1], wave);
 
-            // S = Q K^T for RB x 16 rows x 64 keys (raw scores)
+            // S = Q K^T for RB x 16 rows x 64 keys (raw scores); the 4 RB
+            // accumulators advance together over the head dimension, so
+            // consecutive products are independent
             f32x4 s[RB][4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < 4; ++j)
 #pragma unroll
                 for (int r = 0; r < RB; ++r) s[r][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int ks = 0; ks < 4; ++ks) {
+            for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
                     const bf16x8 kf =
                         *reinterpret_cast<const bf16x8*>(ks_ + 16 * j * D + koff[ks]);
 #pragma unroll
@@ -254,7 +258,6 @@ __global__ __launch_bounds__(NTHR * KG, 2 / KG) void attention_fwd_kernel(AttnAr
                         s[r][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[r][ks], s[r][j],
                                                                           0, 0, 0);
                 }
-            }
             // causal mask (and keys past the sequence): only key tiles that
             // reach past the tile's first row and a ragged last tile have
             // masked keys.  A block whose rows all precede the key tile gets
@@ -525,34 +528,42 @@ __global__ __launch_bounds__(NTHR * KG, 2 / KG) void attention_dkv_kernel(AttnBw
                          qb[buf ^ 1][1], wave);
                 load_rows(qt + 1, l2r, dlr);
             }
-            // S^T and dP^T: lane holds (key = kabs, query = 16 j + 4 g + e)
+            // S^T and dP^T: lane holds (key = kabs, query = 16 j + 4 g + e).
+            // The eight accumulators of the four 16-query blocks advance
+            // together over the head dimension, so consecutive products are
+            // independent; P and dS then replace S and dP in place.
             const bool masked = qt == kt || (qt + 1) * BM > a.seq;
             f32x4 p[4], dsv[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f}, dacc = sacc;
+                p[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+                dsv[j] = p[j];
+            }
 #pragma unroll
-                for (int ks = 0; ks < 4; ++ks) {
-                    sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    p[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                         *reinterpret_cast<const bf16x8*>(qs + 16 * j * D + boff[ks]), kf[ks],
-                        sacc, 0, 0, 0);
-                    dacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        p[j], 0, 0, 0);
+                    dsv[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                         *reinterpret_cast<const bf16x8*>(ds_ + 16 * j * D + boff[ks]), vf[ks],
-                        dacc, 0, 0, 0);
+                        dsv[j], 0, 0, 0);
                 }
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int ql = 16 * j + 4 * g + e;
                     float pv = __builtin_amdgcn_exp2f(
-                        __builtin_fmaf(sacc[e], a.scale_log2, -rv[buf][0][ql]));
+                        __builtin_fmaf(p[j][e], a.scale_log2, -rv[buf][0][ql]));
                     if (masked) {
                         const int qabs = qt * BM + ql;
                         if (qabs < kabs || qabs >= a.seq) pv = 0.f;
                     }
                     p[j][e] = pv;
-                    dsv[j][e] = pv * (dacc[e] - rv[buf][1][ql]);
+                    dsv[j][e] = pv * (dsv[j][e] - rv[buf][1][ql]);
                 }
-            }
             // dV += P^T dO, dK += dS^T Q over two 32-query slices
 #pragma unroll
             for (int sl = 0; sl < 2; ++sl) {
@@ -689,39 +700,52 @@ __global__ __launch_bounds__(NTHR * KG, 2 / KG) void attention_dq_kernel(AttnBwd
             // key tile reaching past the tile's first row, or a ragged one,
             // has masked keys
             const bool masked = (kt + 1) * BN > qt * QT || (kt + 1) * BN > a.seq;
+            // JG 16-key blocks at a time advance together over the head
+            // dimension (2 JG RB independent accumulators), then become dS
+            constexpr int JG = RB == 1 ? 4 : 2;
             f32x4 dsv[RB][4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                f32x4 sacc[RB], dacc[RB];
-#pragma unroll
-                for (int r = 0; r < RB; ++r) {
-                    sacc[r] = f32x4{0.f, 0.f, 0.f, 0.f};
-                    dacc[r] = sacc[r];
-                }
-#pragma unroll
-                for (int ks = 0; ks < 4; ++ks) {
-                    const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks_ + 16 * j * D + boff[ks]);
-                    const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vs_ + 16 * j * D + boff[ks]);
-#pragma unroll
-                    for (int r = 0; r < RB; ++r) {
-                        sacc[r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[r][ks], sacc[r],
-                                                                          0, 0, 0);
-                        dacc[r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, of[r][ks], dacc[r],
-                                                                          0, 0, 0);
-                    }
-                }
+            for (int j0 = 0; j0 < 4; j0 += JG) {
+                f32x4 sacc[RB][JG], dacc[RB][JG];
 #pragma unroll
                 for (int r = 0; r < RB; ++r)
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        float pv = __builtin_amdgcn_exp2f(
-                            __builtin_fmaf(sacc[r][e], a.scale_log2, -l2[r]));
-                        if (masked) {
-                            const int kabs = kt * BN + 16 * j + 4 * g + e;
-                            if (kabs > qabs[r] || kabs >= a.seq) pv = 0.f;
-                        }
-                        dsv[r][j][e] = pv * (dacc[r][e] - dl[r]);
+                    for (int jj = 0; jj < JG; ++jj) {
+                        sacc[r][jj] = f32x4{0.f, 0.f, 0.f, 0.f};
+                        dacc[r][jj] = sacc[r][jj];
                     }
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                    for (int jj = 0; jj < JG; ++jj) {
+                        const int j = j0 + jj;
+                        const bf16x8 kf =
+                            *reinterpret_cast<const bf16x8*>(ks_ + 16 * j * D + boff[ks]);
+                        const bf16x8 vf =
+                            *reinterpret_cast<const bf16x8*>(vs_ + 16 * j * D + boff[ks]);
+#pragma unroll
+                        for (int r = 0; r < RB; ++r) {
+                            sacc[r][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                kf, qf[r][ks], sacc[r][jj], 0, 0, 0);
+                            dacc[r][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                vf, of[r][ks], dacc[r][jj], 0, 0, 0);
+                        }
+                    }
+#pragma unroll
+                for (int jj = 0; jj < JG; ++jj)
+#pragma unroll
+                    for (int r = 0; r < RB; ++r)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int j = j0 + jj;
+                            float pv = __builtin_amdgcn_exp2f(
+                                __builtin_fmaf(sacc[r][jj][e], a.scale_log2, -l2[r]));
+                            if (masked) {
+                                const int kabs = kt * BN + 16 * j + 4 * g + e;
+                                if (kabs > qabs[r] || kabs >= a.seq) pv = 0.f;
+                            }
+                            dsv[r][j][e] = pv * (dacc[r][jj][e] - dl[r]);
+                        }
             }
             // dQ += dS K over two 32-key slices
 #pragma unroll
