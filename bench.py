@@ -65,6 +65,9 @@ def parse():
     ap.add_argument("--attention", action="store_true",
                     help="time the attention core (fwd+bwd) of one device's heads instead of "
                          "the linear block: sequences of min(2048, tokens), head dim 128")
+    ap.add_argument("--attention-block", action="store_true",
+                    help="time the attention block of one device instead: QKV and out-proj "
+                         "with their chunked reductions around the causal core, fwd+bwd")
     ap.add_argument("--linear", action="store_true",
                     help="time one reduced linear of the block (fc2: the largest reduction) "
                          "as the chunked pipeline with f32 and with bf16 partials, serialized, "
@@ -313,6 +316,114 @@ def attention_bench(torch, atp, S, args, wl):
     print(json.dumps(out_line), flush=True)
 
 
+def attention_block_bench(torch, atp, S, args, wl, chunks):
+    """The attention block of one device (Sec. 3.2.1): QKV, its Partial(SUM)
+    reduced over the group in chunks beside the next chunk's product
+    (Sec. 4.1), the causal core on the device's heads, the out-proj reduced
+    the same way; then the backward (Sec. 4.2).  The other members' partials
+    and gathered columns are seeded inputs resident in HBM."""
+    dev = "cuda:0"
+    d1, d2 = wl["mesh"]
+    m = atp.mesh(d1, d2, 0, 0)
+    bm = atp.ATP_BLOCK_COL if wl["mode"] == "col" else atp.ATP_BLOCK_ROW
+    h, T, sw = wl["h"], wl["tokens"], wl["sigma_w"]
+    heads = h // 128
+    seq = min(2048, T)
+    batch = T // seq
+    T = batch * seq
+    gq, go = atp.block_geometry(m, bm, h)[:2]
+    _, hd, _ = atp.attention_heads(m, bm, h, heads)
+    bf = torch.bfloat16
+
+    def rnd(shape, std, tid, dt=bf):
+        return S.randn_device(shape, std, args.seed, tid, dev, dtype=dt)
+
+    def table(size, cols, sigma, tid0):
+        if size == 1:
+            return None
+        return [rnd((T, cols), sigma, tid0 + j, torch.float32) for j in range(size)]
+
+    x = rnd((T, gq.k_loc), 1.0, 411)
+    w = [rnd((gq.k_loc, gq.n_loc), sw, 412), rnd((go.k_loc, go.n_loc), sw, 413)]
+    b = [torch.zeros(gq.n_loc, dtype=bf, device=dev), torch.zeros(go.n_loc, dtype=bf, device=dev)]
+    qtab = table(gq.red_size, gq.n_loc, S.peer_sigma(gq.k_loc, sw, 1.0), 420)
+    otab = table(go.red_size, go.n_loc, S.peer_sigma(go.k_loc, sw, 1.0), 440)
+    atab = table(go.bwd_size, go.k_loc, S.peer_sigma(go.n_loc, sw, 1.0), 460)
+    xtab = table(gq.bwd_size, gq.k_loc, S.peer_sigma(gq.n_loc, sw, 1.0), 480)
+    qkv = torch.empty((T, gq.n_loc), dtype=bf, device=dev)
+    attn = rnd((T, go.k_loc), 1.0, 414)        # the other members' gathered columns
+    lse = torch.empty((hd, T), dtype=torch.float32, device=dev)
+    o = torch.empty((T, go.n_loc), dtype=bf, device=dev)
+    d_o = rnd((T, go.n_loc), 1.0, 415)
+    d_attn = torch.empty((T, go.k_loc), dtype=bf, device=dev)
+    delta = torch.empty((hd * T,), dtype=torch.float32, device=dev)
+    d_qkv = rnd((T, gq.n_loc), 1.0, 416)       # the other members' columns
+    dx = torch.empty((T, gq.k_loc), dtype=bf, device=dev)
+    dw = [torch.empty((g.k_loc, g.n_loc), dtype=torch.float32, device=dev) for g in (gq, go)]
+    db = [torch.empty((g.n_loc,), dtype=torch.float32, device=dev) for g in (gq, go)]
+    comm = torch.cuda.Stream()
+    bwd_chunks = args.bwd_chunks or chunks
+    ws = None
+    if not args.no_workspace:
+        nb = atp.atp_block_workspace_bytes(m, bm, T, h, chunks, atp.ATP_W_KN)
+        ws = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
+
+    def step():
+        cs = torch.cuda.current_stream()
+        atp.atp_attention_block_fwd(m, bm, batch, seq, h, heads, chunks, w, b, x, qtab, qkv,
+                                    attn, lse, otab, o, workspace=ws, compute_stream=cs,
+                                    comm_stream=comm)
+        atp.atp_attention_block_bwd(m, bm, batch, seq, h, heads, bwd_chunks, w, b, x, qkv, attn,
+                                    lse, d_o, atab, d_attn, delta, d_qkv, xtab, dx, dw, db,
+                                    workspace=ws, compute_stream=cs, comm_stream=comm)
+
+    pairs = batch * hd * seq * (seq + 1) / 2.0
+    lin = sum(2.0 * T * g.k_loc * g.n_loc for g in (gq, go))
+    flops = 3.0 * lin + 2.0 * 128 * pairs * (2 + 5)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_step = max(e0.elapsed_time(e1), (time.perf_counter() - t0) * 1e3) / args.steps
+    value = flops / (ms_step * 1e-3) / 1e12
+    atp.atp_profile_enable(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    atp.atp_profile_enable(False)
+    kernels = []
+    for r in atp.atp_profile_collect(32):
+        k = dict(name=r["name"], launches_per_step=r["launches"] // args.steps,
+                 avg_us=round(r["total_ms"] / r["launches"] * 1e3, 2),
+                 ms_per_step=round(r["total_ms"] / args.steps, 4))
+        if r["flops"] > 0:
+            k["tflops"] = round(r["flops"] / (r["total_ms"] * 1e-3) / 1e12, 1)
+        if r["bytes"] > 0:
+            k["gbs"] = round(r["bytes"] / (r["total_ms"] * 1e-3) / 1e9, 1)
+        kernels.append(k)
+    dom = max((k for k in kernels if "tflops" in k), key=lambda k: k["ms_per_step"])
+    out_line = dict(
+        metric="TFLOP/s, attention block fwd+bwd of one device (QKV, causal core, out-proj)",
+        value=round(value, 2), unit="TFLOP/s", n_gpus=1, steps=args.steps, warmup=args.warmup,
+        ms_per_step=round(ms_step, 4), higher_is_better=True, scaling="weak", vs_baseline=None,
+        dtype="bf16", data="synthetic",
+        config=dict(workload=args.workload, part="attention_block", mode=wl["mode"],
+                    mesh=[d1, d2], coord=[0, 0], h=h, heads=heads, heads_per_device=hd,
+                    batch=batch, seq=seq, chunks=chunks, bwd_chunks=bwd_chunks,
+                    workspace=ws is not None, gflop_per_step=round(flops / 1e9, 1)),
+        roofline=dict(bound="mfma", kernel=dom["name"], achieved=dom["tflops"],
+                      peak=PEAK_BF16_TFLOPS, unit="TFLOP/s",
+                      frac=round(dom["tflops"] / PEAK_BF16_TFLOPS, 4), traffic=None),
+        kernels=kernels, cpu_baseline=None)
+    print(json.dumps(out_line), flush=True)
+
+
 def step_flops(st, fwd_only):
     f = sum(2.0 * st["T"] * g.k_loc * g.n_loc for g in st["G"])
     return f if fwd_only else 3.0 * f
@@ -545,6 +656,9 @@ def main():
     comm = cu_masked_stream(torch, args.comm_cus) if args.comm_cus else None
     if args.attention:
         attention_bench(torch, atp, S, args, wl)
+        return
+    if args.attention_block:
+        attention_block_bench(torch, atp, S, args, wl, chunks)
         return
     if args.linear:
         linear_bench(torch, atp, S, args, wl, chunks)

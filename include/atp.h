@@ -447,10 +447,19 @@ atp_status atp_attention_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t b
  *  lse          fp32 [heads of the device][tokens], written.
  *  o_partials / o: out-proj's partial table and reduced output (+ bias).
  * Weights: entries 0 (qkv) and 1 (out) of w, in w->layout; 2 and 3 are
- * not read.  Products read the weights as stored (no workspace); the
- * attention core starts once the whole QKV block is reduced (a causal
- * sequence spans chunks), out-proj's chunks follow on compute_stream and
- * their reductions overlap the next chunk's GEMM on comm_stream (Sec. 4.1).
+ * not read.  The attention core starts once the whole QKV block is reduced
+ * (a causal sequence spans chunks), out-proj's chunks follow on
+ * compute_stream and their reductions overlap the next chunk's GEMM on
+ * comm_stream (Sec. 4.1).
+ * workspace / ws_bytes: optional, caller-owned device memory (256-byte
+ * aligned; atp_block_workspace_bytes() for the same mesh, mode, tokens, h,
+ * chunks and weight layout is enough).  With it, as in atp_block_fwd, a
+ * chunk product with too few tiles to fill the chip is split over k into
+ * fp32 slabs there, summed in split order (so its bits can differ from the
+ * unsplit product's by fp32 rounding), and weights stored [k][n] are copied
+ * there as W^T where the products stream faster from it; without it the
+ * products read the weights as stored.  Nothing in the workspace is read
+ * before the call writes it.
  * The call refuses a compute_stream under HIP graph capture.  Errors as
  * atp_block_fwd and atp_attention_fwd. */
 typedef struct {
@@ -467,7 +476,8 @@ typedef struct {
 atp_status atp_attention_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t batch,
                                    int64_t seq, int64_t h, int32_t heads, int32_t chunks,
                                    const atp_block_weights* w, const atp_attn_block_fwd_io* io,
-                                   void* compute_stream, void* comm_stream);
+                                   void* workspace, size_t ws_bytes, void* compute_stream,
+                                   void* comm_stream);
 
 /* Backward of atp_attention_block_fwd (Sec. 4.2 through the chain):
  * out-proj's dX (chunked, reduced over its backward group) gives d_attn;
@@ -486,6 +496,14 @@ atp_status atp_attention_block_fwd(const atp_mesh* mesh, int32_t block_mode, int
  *  dw[0], db[0] (qkv), dw[1], db[1] (out): f32, as atp_block_bwd_io
  *               (dw in the weights' layout and leading dimension; db
  *               nullable).
+ * workspace / ws_bytes: optional, caller-owned device memory (256-byte
+ * aligned).  A workspace of atp_block_workspace_bytes() bytes for the same
+ * mesh, mode, tokens, h and weight layout (or larger), with tokens a
+ * multiple of 8, runs both dW products from transposed copies of X and dY
+ * kept there (both operands contiguous along the tokens) and forms db from
+ * the dY transpose; otherwise dW reads X and dY as given.  Both paths give
+ * the same bits.  The workspace is scratch: nothing in it is read before
+ * the call writes it.
  * Errors as atp_block_bwd and atp_attention_bwd. */
 typedef struct {
     const void* x_loc; int64_t ldx;
@@ -507,7 +525,8 @@ typedef struct {
 atp_status atp_attention_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t batch,
                                    int64_t seq, int64_t h, int32_t heads, int32_t chunks,
                                    const atp_block_weights* w, const atp_attn_block_bwd_io* io,
-                                   void* compute_stream, void* comm_stream);
+                                   void* workspace, size_t ws_bytes, void* compute_stream,
+                                   void* comm_stream);
 
 /* atp_attention_bwd without the delta argument, for callers that cannot
  * allocate device memory (code under HIP graph capture, tight serving

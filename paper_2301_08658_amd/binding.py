@@ -207,11 +207,13 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.atp_attention_heads.restype = i32
     lib.atp_attention_block_fwd.argtypes = [mp, i32, i64, i64, i64, i32, i32,
                                             ctypes.POINTER(atp_block_weights),
-                                            ctypes.POINTER(atp_attn_block_fwd_io), _vp, _vp]
+                                            ctypes.POINTER(atp_attn_block_fwd_io), _vp,
+                                            ctypes.c_size_t, _vp, _vp]
     lib.atp_attention_block_fwd.restype = i32
     lib.atp_attention_block_bwd.argtypes = [mp, i32, i64, i64, i64, i32, i32,
                                             ctypes.POINTER(atp_block_weights),
-                                            ctypes.POINTER(atp_attn_block_bwd_io), _vp, _vp]
+                                            ctypes.POINTER(atp_attn_block_bwd_io), _vp,
+                                            ctypes.c_size_t, _vp, _vp]
     lib.atp_attention_block_bwd.restype = i32
     lib.atp_block_fwd.argtypes = [mp, i32, i64, i64, i32, ctypes.POINTER(atp_block_weights),
                                   ctypes.POINTER(atp_block_fwd_io), _vp, sz, _vp, _vp]
@@ -729,12 +731,14 @@ def _attn_weights(G, w, b, layout: int):
 
 def atp_attention_block_fwd(m: atp_mesh, block_mode: int, batch: int, seq: int, h: int,
                             heads: int, chunks: int, w, b, x_loc, qkv_partials, qkv, attn, lse,
-                            o_partials, o, compute_stream=None, comm_stream=None,
+                            o_partials, o, workspace=None, compute_stream=None, comm_stream=None,
                             weight_layout: int = ATP_W_KN):
     """The device's attention block: QKV -> its heads' attention -> out-proj.
     w, b: [qkv, out] weights and biases; qkv_partials / o_partials: the
     groups' buffers (own entry written) or None for a group of one; attn: the
-    gathered out-proj input, whose other members' columns must be filled."""
+    gathered out-proj input, whose other members' columns must be filled;
+    workspace: an optional uint8 device buffer (atp_block_workspace_bytes
+    covers it)."""
     T = batch * seq
     G = block_geometry(m, block_mode, h)
     _, hd, _ = attention_heads(m, block_mode, h, heads)
@@ -757,19 +761,22 @@ def atp_attention_block_fwd(m: atp_mesh, block_mode: int, batch: int, seq: int, 
     io.attn, io.ld_attn = _mat(attn, T, G[1].k_loc, torch.bfloat16, "attn")
     io.lse = _ptr(lse, "lse")
     io.o, io.ld_o = _mat(o, T, G[1].n_loc, torch.bfloat16, "o")
+    wsp, wsb = _workspace(workspace)
     _check(load_library().atp_attention_block_fwd(
         ctypes.byref(m), int(block_mode), int(batch), int(seq), int(h), int(heads), int(chunks),
-        ctypes.byref(W), ctypes.byref(io), _stream(compute_stream), _stream(comm_stream)))
+        ctypes.byref(W), ctypes.byref(io), wsp, wsb, _stream(compute_stream),
+        _stream(comm_stream)))
 
 
 def atp_attention_block_bwd(m: atp_mesh, block_mode: int, batch: int, seq: int, h: int,
                             heads: int, chunks: int, w, b, x_loc, qkv, attn, lse, d_o,
                             d_attn_partials, d_attn, delta, d_qkv, dx_partials, dx, dw, db,
-                            compute_stream=None, comm_stream=None,
+                            workspace=None, compute_stream=None, comm_stream=None,
                             weight_layout: int = ATP_W_KN):
     """Backward of atp_attention_block_fwd.  d_qkv: the QKV block's
     gradient, whose other members' columns must be filled; dw, db: [qkv, out]
-    (dw in the weights' layout, db entries may be None)."""
+    (dw in the weights' layout, db entries may be None); workspace: an
+    optional uint8 device buffer (atp_block_workspace_bytes covers it)."""
     T = batch * seq
     G = block_geometry(m, block_mode, h)
     _, hd, _ = attention_heads(m, block_mode, h, heads)
@@ -805,9 +812,11 @@ def atp_attention_block_bwd(m: atp_mesh, block_mode: int, batch: int, seq: int, 
             raise ValueError(f"dw[{LINEARS[i]}] must share the weight's leading dimension")
         io.dw[i] = p
         io.db[i] = _vec(db[i], g.n_loc, torch.float32, f"db[{LINEARS[i]}]") if db else None
+    wsp, wsb = _workspace(workspace)
     _check(load_library().atp_attention_block_bwd(
         ctypes.byref(m), int(block_mode), int(batch), int(seq), int(h), int(heads), int(chunks),
-        ctypes.byref(W), ctypes.byref(io), _stream(compute_stream), _stream(comm_stream)))
+        ctypes.byref(W), ctypes.byref(io), wsp, wsb, _stream(compute_stream),
+        _stream(comm_stream)))
 
 
 # ---------------------------------------------------------------------------

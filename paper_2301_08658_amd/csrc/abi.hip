@@ -356,12 +356,12 @@ int64_t ws_pitch(int64_t len) { return len + kWsPad; }
 // dY W^T likewise.  One region serves every chunk of every linear (they run
 // in order on one stream); it is sized for the largest plan over all chunk
 // counts, so the size does not depend on the chunk count.
-size_t slab_bytes(const BlockPlan& P, int64_t tokens, bool bwd) {
+size_t slab_bytes(const BlockPlan& P, int64_t tokens, bool bwd, int nlin = 4) {
     size_t most = 0;
     for (int c = 1; c <= ATP_MAX_CHUNKS; ++c) {
         if (tokens % c) continue;
         const int64_t mc = tokens / c;
-        for (int L = 0; L < 4; ++L) {
+        for (int L = 0; L < nlin; ++L) {
             const atp_shard& g = P.g[L];
             if ((bwd ? g.bwd_size : g.red_size) <= 1) continue;
             const int64_t N = bwd ? g.k_loc : g.n_loc, K = bwd ? g.n_loc : g.k_loc;
@@ -401,10 +401,11 @@ bool fwd_may_copy_w(const BlockPlan& P, int L, int64_t tokens) {
 // The forward's pieces: the slabs, and W^T ([n_loc][k_loc]) of weights
 // stored [k_loc][n_loc] that the forward may copy (weights stored
 // [n_loc][k_loc] are read as they are).
-size_t ws_fwd_bytes(const BlockPlan& P, int64_t tokens, int32_t layout) {
-    size_t b = ws_round(slab_bytes(P, tokens, false));
+// (nlin = 2: the attention block's QKV and out-proj only, a subset)
+size_t ws_fwd_bytes(const BlockPlan& P, int64_t tokens, int32_t layout, int nlin = 4) {
+    size_t b = ws_round(slab_bytes(P, tokens, false, nlin));
     if (layout == ATP_W_KN)
-        for (int L = 0; L < 4; ++L)
+        for (int L = 0; L < nlin; ++L)
             if (fwd_may_copy_w(P, L, tokens))
                 b += ws_round((size_t)P.g[L].n_loc * ws_pitch(P.g[L].k_loc) * 2);
     return b;
@@ -1029,13 +1030,14 @@ atp_status weight_grads(const atp_shard& g, bool kn, const void* X, int64_t ldx,
 // with its epilogue in one launch), and ms reduces the group's partials of
 // those rows with the epilogue as soon as they are written.  `done` is
 // recorded after the last chunk's reduction (on ms), or after the single
-// launch (on cs).  make(A_rows, C_rows, ldc, b16, epi, M) builds the product.
+// launch (on cs).  make(A_rows, C_rows, ldc, b16, epi, M) builds the product;
+// with a slab, a chunk product with too few tiles is split over k there.
 template <class Make>
 atp_status chained_linear(const Streams& S, int red_size, int red_index, void* const* parts,
                           int64_t ldp, bool pb16, const void* A, int64_t lda, int64_t ncols,
                           int epi, const void* bias, const void* pre_in, void* out, int64_t ldo,
                           int64_t T, int32_t chunks, hipEvent_t* ev_chunk, hipEvent_t done,
-                          Make make) {
+                          Make make, float* slab = nullptr) {
     if (red_size == 1) {
         atp::GemmProblem p = make(A, out, ldo, true, epi, T);
         p.bias = bias;
@@ -1050,7 +1052,7 @@ atp_status chained_linear(const Streams& S, int red_size, int red_index, void* c
         const int64_t r0 = (int64_t)c * mc;
         atp::GemmProblem p = make(static_cast<const uint16_t*>(A) + r0 * lda,
                                   row_ptr(own, r0, ldp, pb16), ldp, pb16, atp::EPI_NONE, mc);
-        ATP_CHECK(run_gemm(p, S.cs));
+        ATP_CHECK(run_nt_partial(p, slab, S.cs));
         HIP_CHECK(hipEventRecord(ev_chunk[c], S.cs), "hipEventRecord");
         HIP_CHECK(hipStreamWaitEvent(S.ms, ev_chunk[c], 0), "hipStreamWaitEvent");
         atp::ReduceProblem r = reduce_problem(red_size, parts, ldp, r0, mc, ncols, epi, bias,
@@ -1059,6 +1061,37 @@ atp_status chained_linear(const Streams& S, int red_size, int red_index, void* c
     }
     HIP_CHECK(hipEventRecord(done, S.ms), "hipEventRecord");
     return ATP_OK;
+}
+
+// The attention block's backward with a workspace: X^T and dY^T of one
+// linear in the workspace (padded pitch), db from the dY transpose's column
+// partials, then dW as an NT product over the tokens (dW^T = dY^T X for
+// weights stored [n][k]); the same bits as weight_grads.
+atp_status weight_grads_ws(const atp_shard& g, bool kn, const void* X, int64_t ldx,
+                           const void* dY, int64_t lddy, float* dw, int64_t ldw, float* db,
+                           int64_t T, uint16_t* xt, uint16_t* dyt, float* colpart,
+                           hipStream_t s) {
+    const int64_t tp = ws_pitch(T);
+    ATP_CHECK(run_transpose(X, ldx, T, g.k_loc, xt, tp, s));
+    float* part = db ? colpart : nullptr;
+    ATP_CHECK(run_transpose(dY, lddy, T, g.n_loc, dyt, tp, s, part, g.n_loc));
+    if (part) ATP_CHECK(run_colsum_finish(part, g.n_loc, (T + 63) / 64, g.n_loc, db, s));
+    const atp::GemmProblem p =
+        kn ? gemm_problem(atp::LAYOUT_NT, xt, tp, dyt, tp, dw, ldw, false, atp::EPI_NONE, g.k_loc,
+                          g.n_loc, T)
+           : gemm_problem(atp::LAYOUT_NT, dyt, tp, xt, tp, dw, ldw, false, atp::EPI_NONE, g.n_loc,
+                          g.k_loc, T);
+    return run_gemm(p, s);
+}
+
+// Bytes the attention block's backward carves from a workspace: X^T of x
+// and of the gathered block, dY^T of d_qkv and d_o, db's column partials
+// (a subset of the block backward's pieces, so ws_bwd_bytes covers it).
+size_t attn_ws_bwd_bytes(const BlockPlan& P, int64_t tokens) {
+    const size_t t2 = (size_t)ws_pitch(tokens) * 2;
+    return ws_round(P.g[0].k_loc * t2) + ws_round(P.g[1].k_loc * t2) +
+           ws_round(P.g[0].n_loc * t2) + ws_round(P.g[1].n_loc * t2) +
+           ws_round(colpart_bytes(P, tokens));
 }
 
 atp_status check_attn_weights(const BlockPlan& P, const atp_block_weights* w) {
@@ -1483,7 +1516,8 @@ atp_status atp_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
 atp_status atp_attention_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t batch,
                                    int64_t seq, int64_t h, int32_t heads, int32_t chunks,
                                    const atp_block_weights* w, const atp_attn_block_fwd_io* io,
-                                   void* compute_stream, void* comm_stream) {
+                                   void* workspace, size_t ws_bytes, void* compute_stream,
+                                   void* comm_stream) {
     AttnPlan ap;
     ATP_CHECK(attention_plan(mesh, block_mode, batch, seq, h, heads, &ap));
     BlockPlan P;
@@ -1509,7 +1543,25 @@ atp_status atp_attention_block_fwd(const atp_mesh* mesh, int32_t block_mode, int
     if (T > 0) ATP_CHECK(check_vec(io->lse, "lse"));
     if (overlaps(io->qkv, T, io->ld_qkv, 2, io->attn, T, io->ld_attn, 2))
         return set_error(ATP_ERR_INVALID_ARGUMENT, "qkv and attn must not overlap");
+    if (workspace && reinterpret_cast<uintptr_t>(workspace) % kWsAlign)
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kWsAlign);
     ATP_CHECK(refuse_capture_of_direct_path(compute_stream));
+    // With a workspace, as in the block forward: chunk products with too few
+    // tiles to fill the chip are split over k into slabs there, from W^T
+    // copies kept there (weights stored [k][n])
+    const bool ws = workspace && ws_bytes >= ws_fwd_bytes(P, T, w->layout, 2);
+    uint16_t* wt[2] = {nullptr, nullptr};
+    float* slab = nullptr;
+    if (ws) {
+        Carver c{static_cast<char*>(workspace)};
+        if (kn)
+            for (int L = 0; L < 2; ++L)
+                if (fwd_may_copy_w(P, L, T)) {
+                    uint16_t* t = c.take((size_t)P.g[L].n_loc * ws_pitch(P.g[L].k_loc) * 2);
+                    if (!fwd_reads_w(P, L, T, chunks)) wt[L] = t;
+                }
+        slab = reinterpret_cast<float*>(c.take(slab_bytes(P, T, false, 2)));
+    }
 
     Streams S(compute_stream, comm_stream);
     hipEvent_t* ev = nullptr;
@@ -1520,12 +1572,23 @@ atp_status atp_attention_block_fwd(const atp_mesh* mesh, int32_t block_mode, int
     auto make = [&](int L) {
         return [&, L](const void* A, void* C, int64_t ldc, bool b16, int epi, int64_t M) {
             const int64_t lda = L == 0 ? io->ldx : io->ld_attn;
-            return xw_problem(P.g[L], kn, w->w[L], w->ldw[L], A, lda, C, ldc, b16, epi, M);
+            const atp_shard& g = P.g[L];
+            if (wt[L])
+                return gemm_problem(atp::LAYOUT_NT, A, lda, wt[L], ws_pitch(g.k_loc), C, ldc, b16,
+                                    epi, M, g.n_loc, g.k_loc);
+            return xw_problem(g, kn, w->w[L], w->ldw[L], A, lda, C, ldc, b16, epi, M);
         };
     };
+    // W^T of linear L, written before its first product (same stream)
+    auto need_wt = [&](int L) -> atp_status {
+        if (!wt[L]) return ATP_OK;
+        const atp_shard& g = P.g[L];
+        return run_transpose(w->w[L], w->ldw[L], g.k_loc, g.n_loc, wt[L], ws_pitch(g.k_loc), S.cs);
+    };
+    ATP_CHECK(need_wt(0));
     ATP_CHECK(chained_linear(S, gq.red_size, gq.red_index, io->qkv_partials, io->ldp_qkv, pb16,
                              io->x_loc, io->ldx, gq.n_loc, atp::EPI_BIAS, w->b[0], nullptr,
-                             io->qkv, io->ld_qkv, T, chunks, ev + 4, ev[2], make(0)));
+                             io->qkv, io->ld_qkv, T, chunks, ev + 4, ev[2], make(0), slab));
     // a causal sequence spans chunks: the core waits for the whole QKV block
     HIP_CHECK(hipStreamWaitEvent(S.cs, ev[2], 0), "hipStreamWaitEvent");
     if (T > 0) {
@@ -1546,16 +1609,18 @@ atp_status atp_attention_block_fwd(const atp_mesh* mesh, int32_t block_mode, int
                         (double)T * ap.hd * (4.0 * kHeadDim * 2.0 + 4.0), S.cs,
                         [&] { return atp::launch_attention_fwd(p, S.cs); }));
     }
+    ATP_CHECK(need_wt(1));
     ATP_CHECK(chained_linear(S, go.red_size, go.red_index, io->o_partials, io->ldp_o, pb16,
                              io->attn, io->ld_attn, go.n_loc, atp::EPI_BIAS, w->b[1], nullptr,
-                             io->o, io->ld_o, T, chunks, ev + 4 + chunks, ev[3], make(1)));
+                             io->o, io->ld_o, T, chunks, ev + 4 + chunks, ev[3], make(1), slab));
     return S.end(ev[1]);
 }
 
 atp_status atp_attention_block_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t batch,
                                    int64_t seq, int64_t h, int32_t heads, int32_t chunks,
                                    const atp_block_weights* w, const atp_attn_block_bwd_io* io,
-                                   void* compute_stream, void* comm_stream) {
+                                   void* workspace, size_t ws_bytes, void* compute_stream,
+                                   void* comm_stream) {
     AttnPlan ap;
     ATP_CHECK(attention_plan(mesh, block_mode, batch, seq, h, heads, &ap));
     BlockPlan P;
@@ -1601,7 +1666,30 @@ atp_status atp_attention_block_bwd(const atp_mesh* mesh, int32_t block_mode, int
         overlaps(io->d_qkv, T, io->ld_dqkv, 2, io->attn, T, io->ld_attn, 2) ||
         overlaps(io->d_qkv, T, io->ld_dqkv, 2, io->d_attn, T, io->ld_d_attn, 2))
         return set_error(ATP_ERR_INVALID_ARGUMENT, "d_qkv must not overlap an input");
+    if (workspace && reinterpret_cast<uintptr_t>(workspace) % kWsAlign)
+        return set_error(ATP_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kWsAlign);
     ATP_CHECK(refuse_capture_of_direct_path(compute_stream));
+    // dW from transposed copies when the workspace holds them (whole 16-byte
+    // rows of tokens for the transposes), else from X and dY as given
+    const bool ws = workspace && ws_bytes >= attn_ws_bwd_bytes(P, T) && T % 8 == 0;
+    uint16_t *xt_x = nullptr, *xt_a = nullptr, *dyt_q = nullptr, *dyt_o = nullptr;
+    float* colpart = nullptr;
+    if (ws) {
+        Carver c{static_cast<char*>(workspace)};
+        const size_t t2 = (size_t)ws_pitch(T) * 2;
+        xt_x = c.take(gq.k_loc * t2);
+        xt_a = c.take(go.k_loc * t2);
+        dyt_q = c.take(gq.n_loc * t2);
+        dyt_o = c.take(go.n_loc * t2);
+        colpart = reinterpret_cast<float*>(c.take(colpart_bytes(P, T)));
+    }
+    auto dweights = [&](const atp_shard& g, int L, const void* X, int64_t ldx, const void* dY,
+                        int64_t lddy, uint16_t* xt, uint16_t* dyt, hipStream_t s) {
+        if (ws)
+            return weight_grads_ws(g, kn, X, ldx, dY, lddy, io->dw[L], w->ldw[L], io->db[L], T,
+                                   xt, dyt, colpart, s);
+        return weight_grads(g, kn, X, ldx, dY, lddy, io->dw[L], w->ldw[L], io->db[L], T, s);
+    };
 
     Streams S(compute_stream, comm_stream);
     hipEvent_t* ev = nullptr;
@@ -1620,8 +1708,7 @@ atp_status atp_attention_block_bwd(const atp_mesh* mesh, int32_t block_mode, int
                              io->d_o, io->ld_do, go.k_loc, atp::EPI_NONE, nullptr, nullptr,
                              io->d_attn, io->ld_d_attn, T, chunks, ev + 4, ev[2],
                              make(1, io->d_o, io->ld_do)));
-    ATP_CHECK(weight_grads(go, kn, io->attn, io->ld_attn, io->d_o, io->ld_do, io->dw[1],
-                           w->ldw[1], io->db[1], T, S.cs));
+    ATP_CHECK(dweights(go, 1, io->attn, io->ld_attn, io->d_o, io->ld_do, xt_a, dyt_o, S.cs));
     // the core's backward reads the device's columns of the whole d_attn
     HIP_CHECK(hipStreamWaitEvent(S.cs, ev[2], 0), "hipStreamWaitEvent");
     if (T > 0) {
@@ -1652,8 +1739,7 @@ atp_status atp_attention_block_bwd(const atp_mesh* mesh, int32_t block_mode, int
                              io->d_qkv, io->ld_dqkv, gq.k_loc, atp::EPI_NONE, nullptr, nullptr,
                              io->dx, io->ld_dx, T, chunks, ev + 4 + chunks, ev[3],
                              make(0, io->d_qkv, io->ld_dqkv)));
-    ATP_CHECK(weight_grads(gq, kn, io->x_loc, io->ldx, io->d_qkv, io->ld_dqkv, io->dw[0],
-                           w->ldw[0], io->db[0], T, S.cs));
+    ATP_CHECK(dweights(gq, 0, io->x_loc, io->ldx, io->d_qkv, io->ld_dqkv, xt_x, dyt_q, S.cs));
     return S.end(ev[1]);
 }
 

@@ -302,3 +302,24 @@ def check_bwd(out, ref, extra, what=""):
     for i, n in enumerate(LIN):
         assert_close(out["dw_kn"][i], ref["dw_" + n], f"{what} dw_{n}", extra=extra.get("dw_" + n))
         assert_close(out["db"][i], ref["db_" + n], f"{what} db_{n}", extra=extra.get("db_" + n))
+
+
+def assert_paths_agree(a, b, what, rel=1e-4):
+    """Two summation orders of the same fp32-accumulated products."""
+    if a.dtype == torch.bfloat16:
+        # two units in the last place of the larger value (bf16 keeps 8
+        # significant bits), plus the fp32 sums' rounding on the tensor's scale
+        # for values that come out of cancellation near zero
+        fa, fb = a.double(), b.double()
+        scale = float(fa.abs().max()) + 1e-30
+        bound = 2.0 ** -6 * torch.maximum(fa.abs(), fb.abs()) + rel * scale
+        excess = float(((fa - fb).abs() - bound).max())
+        assert excess <= 0, f"{what}: bf16 outputs differ beyond two units in the last place"
+        frac = float((a.contiguous().view(torch.int16) !=
+                      b.contiguous().view(torch.int16)).float().mean())
+        assert frac < 0.05, f"{what}: {frac:.3%} of bf16 outputs differ"
+    else:
+        fa, fb = a.double(), b.double()
+        scale = float(fa.abs().max()) + 1e-30
+        err = float((fa - fb).abs().max())
+        assert err <= rel * scale, f"{what}: max diff {err:.3e} vs scale {scale:.3e}"

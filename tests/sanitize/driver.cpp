@@ -187,9 +187,11 @@ static void abi_checks() {
     // attention calls and the attention block
     atp_attn_block_fwd_io aio;
     memset(&aio, 0, sizeof aio);
-    EXPECT(atp_attention_block_fwd(&m, 0, 2, 128, 1024, 8, 3, &W, &aio, nullptr, nullptr) ==
+    EXPECT(atp_attention_block_fwd(&m, 0, 2, 128, 1024, 8, 3, &W, &aio, nullptr, 0, nullptr,
+                                   nullptr) ==
            ATP_ERR_SHAPE);
-    EXPECT(atp_attention_block_fwd(&m, 0, 2, 128, 1024, 8, 2, nullptr, &aio, nullptr, nullptr) ==
+    EXPECT(atp_attention_block_fwd(&m, 0, 2, 128, 1024, 8, 2, nullptr, &aio, nullptr, 0,
+                                   nullptr, nullptr) ==
            ATP_ERR_INVALID_ARGUMENT);
     EXPECT(atp_attention_fwd(&m, 0, 1, 64, 1024, 8, FAKE, 1536, FAKE, 512, nullptr, nullptr) ==
            ATP_ERR_INVALID_ARGUMENT);   // lse missing

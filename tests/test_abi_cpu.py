@@ -492,3 +492,36 @@ def test_attention_refuses_overlapping_buffers():
     for dqkv in (FAKE + 16 * nq, far - 16 * nq, past + 32):
         assert bwd(dqkv) == B.ATP_ERR_INVALID_ARGUMENT, hex(dqkv)
         assert "overlap" in atp.binding.last_error()
+
+
+def test_attention_block_bwd_refuses_misaligned_workspace():
+    """A workspace that is not 256-byte aligned is refused before any work;
+    every buffer address is distinct and never dereferenced (mesh 1 x 1: no
+    reduction tables)."""
+    lib = atp.load_library()
+    m = atp.mesh(1, 1, 0, 0)
+    h, heads, batch, seq = 1024, 8, 1, 256
+    T = batch * seq
+    gq, go = atp.block_geometry(m, B.ATP_BLOCK_COL, h)[:2]
+    addr = iter(range(1 << 36, 1 << 42, 1 << 36))   # far apart: no two buffers overlap
+    W = B.atp_block_weights()
+    W.layout = B.ATP_W_KN
+    for i, g in enumerate((gq, go)):
+        W.w[i], W.ldw[i], W.b[i] = next(addr), g.n_loc, next(addr)
+    io = B.atp_attn_block_bwd_io()
+    io.x_loc, io.ldx = next(addr), gq.k_loc
+    io.qkv, io.ld_qkv = next(addr), gq.n_loc
+    io.attn, io.ld_attn = next(addr), go.k_loc
+    io.lse = next(addr)
+    io.d_o, io.ld_do = next(addr), go.n_loc
+    io.d_attn, io.ld_d_attn = next(addr), go.k_loc
+    io.delta = next(addr)
+    io.d_qkv, io.ld_dqkv = next(addr), gq.n_loc
+    io.dx, io.ld_dx = next(addr), gq.k_loc
+    for i in range(2):
+        io.dw[i], io.db[i] = next(addr), next(addr)
+    ws = next(addr)
+    st = lib.atp_attention_block_bwd(ctypes.byref(m), 0, batch, seq, h, heads, 1, ctypes.byref(W),
+                                     ctypes.byref(io), ws + 16, 1 << 30, None, None)
+    assert st == B.ATP_ERR_INVALID_ARGUMENT
+    assert "workspace" in atp.binding.last_error()

@@ -226,6 +226,36 @@ def test_attention_block_every_coordinate(mode, mesh):
                                     out["d_qkv"], xtab if gq.bwd_size > 1 else None, out["dx"],
                                     out["dw"], out["db"], comm_stream=torch.cuda.Stream())
         B[c] = out
+        # the same call with a workspace (dW from transposed copies, db from
+        # the dY transpose) gives the same bits; the workspace starts as
+        # all-ones bytes (NaN in both dtypes), so nothing may be read from it
+        # before the call writes it
+        nb = atp.atp_block_workspace_bytes(l_["m"], bm, T, h, chunks, atp.ATP_W_KN)
+        assert atp.atp_block_workspace_path(l_["m"], bm, T, h, atp.ATP_W_KN, nb, 1) == 1
+        ws = torch.full((nb,), 255, dtype=torch.uint8, device=DEV)
+        d_qkv2 = Dq[_key(c, qax)].clone()
+        d_qkv2[:, qcols] = float("nan")
+        own_a2 = nan(T, go.k_loc) if go.bwd_size > 1 else None
+        own_x2 = nan(T, gq.k_loc) if gq.bwd_size > 1 else None
+        out2 = dict(d_attn=nan(T, go.k_loc, torch.bfloat16), d_qkv=d_qkv2,
+                    dx=nan(T, gq.k_loc, torch.bfloat16),
+                    dw=[nan(gq.k_loc, gq.n_loc), nan(go.k_loc, go.n_loc)],
+                    db=[torch.full((gq.n_loc,), float("nan"), device=DEV),
+                        torch.full((go.n_loc,), float("nan"), device=DEV)])
+        atp.atp_attention_block_bwd(
+            l_["m"], bm, batch, seq, h, heads, chunks, [l_["wq"], l_["wo"]],
+            [l_["bq"], l_["bo"]], l_["x"], F[c]["qkv"], F[c]["attn"], F[c]["lse"], l_["do"],
+            [own_a2 if p == c else Qa[p] for p in _group(c, obax, go.bwd_size)]
+            if go.bwd_size > 1 else None, out2["d_attn"], torch.empty(l_["hd"] * T, device=DEV),
+            out2["d_qkv"], [own_x2 if p == c else Qx[p] for p in _group(c, qbax, gq.bwd_size)]
+            if gq.bwd_size > 1 else None, out2["dx"], out2["dw"], out2["db"], workspace=ws,
+            comm_stream=torch.cuda.Stream())
+        torch.cuda.synchronize()
+        for key in ("d_attn", "d_qkv", "dx"):
+            assert torch.equal(_bits(out2[key]), _bits(out[key])), (c, key)
+        for i in range(2):
+            assert torch.equal(_bits(out2["dw"][i]), _bits(out["dw"][i])), (c, "dw", i)
+            assert torch.equal(_bits(out2["db"][i]), _bits(out["db"][i])), (c, "db", i)
     torch.cuda.synchronize()
 
     g = O.attention_block_global_bwd(X, Wq, Wo, ref, dO, batch, seq, HD)
@@ -343,3 +373,128 @@ def test_attention_block_nk_weights_and_bf16_partials():
         var_a[:, cols] = bounds.rounding_var(attn[:, cols])
         e = bounds.left(var_a, O._f64(wo)) + (bounds.single(own_o) if pb16 else 0.0)
         assert_close(out["o"], o, "o", extra=e)
+
+
+def test_attention_block_workspace_path_full_size():
+    """The benchmark's attention block (h = 20480 on DeviceMesh(8, 1), 2 x 2048
+    tokens, 8 forward chunks, one device with seeded peers): the backward with
+    a workspace (dW from transposed copies on the 256-wide NT tiles, db from
+    the dY transpose) gives the bits of the backward without one, on every
+    output.  The path without a workspace is checked against the oracle on
+    every coordinate above."""
+    w = S.WORKLOADS["wide_h20480_col_8x1"]
+    d1, d2 = w["mesh"]
+    h, T, chunks, sw = w["h"], w["tokens"], w["chunks"], w["sigma_w"]
+    heads, seq = h // HD, 2048
+    batch = T // seq
+    m = atp.mesh(d1, d2, d1 - 1, 0)
+    bm = atp.ATP_BLOCK_COL
+    gq, go = atp.block_geometry(m, bm, h)[:2]
+    _, hd, _ = atp.attention_heads(m, bm, h, heads)
+    rnd = lambda shape, std, tid, dt=torch.bfloat16: S.randn_device(  # noqa: E731
+        shape, std, 83, tid, DEV, dtype=dt)
+    nan = lambda r, c_, dt=torch.float32: torch.full((r, c_), float("nan"), dtype=dt,  # noqa
+                                                     device=DEV)
+
+    def table(size, cols, tid0):
+        return None if size == 1 else [rnd((T, cols), 0.5, tid0 + j, torch.float32)
+                                       for j in range(size)]
+    x = rnd((T, gq.k_loc), 1.0, 1)
+    wts = [rnd((gq.k_loc, gq.n_loc), sw, 2), rnd((go.k_loc, go.n_loc), sw, 3)]
+    bs = [rnd((gq.n_loc,), 0.02, 4), rnd((go.n_loc,), 0.02, 5)]
+    qkv = torch.empty((T, gq.n_loc), dtype=torch.bfloat16, device=DEV)
+    attn = rnd((T, go.k_loc), 1.0, 6)
+    lse = torch.empty((hd, T), device=DEV)
+    o = torch.empty((T, go.n_loc), dtype=torch.bfloat16, device=DEV)
+    print(f"attention block full size, forward (h={h}, T={T}, {hd} heads)", flush=True)
+    atp.atp_attention_block_fwd(m, bm, batch, seq, h, heads, chunks, wts, bs, x,
+                                table(gq.red_size, gq.n_loc, 10), qkv, attn, lse,
+                                table(go.red_size, go.n_loc, 30), o,
+                                comm_stream=torch.cuda.Stream())
+    d_o = rnd((T, go.n_loc), 1.0, 7)
+    dq0 = rnd((T, gq.n_loc), 1.0, 8)
+    atab, xtab = table(go.bwd_size, go.k_loc, 50), table(gq.bwd_size, gq.k_loc, 70)
+    nb = atp.atp_block_workspace_bytes(m, bm, T, h, chunks, atp.ATP_W_KN)
+    assert atp.atp_block_workspace_path(m, bm, T, h, atp.ATP_W_KN, nb, 1) == 1
+    res = []
+    for ws in (None, torch.full((nb,), 255, dtype=torch.uint8, device=DEV)):
+        print(f"attention block full size, backward, workspace {ws is not None}", flush=True)
+        def own(tab, idx):
+            """The group's table with a fresh own entry (written by the call)."""
+            return None if tab is None else [nan(T, t.shape[1]) if j == idx else t
+                                             for j, t in enumerate(tab)]
+        out = dict(d_attn=nan(T, go.k_loc, torch.bfloat16), d_qkv=dq0.clone(),
+                   dx=nan(T, gq.k_loc, torch.bfloat16),
+                   dw=[nan(gq.k_loc, gq.n_loc), nan(go.k_loc, go.n_loc)],
+                   db=[torch.full((gq.n_loc,), float("nan"), device=DEV),
+                       torch.full((go.n_loc,), float("nan"), device=DEV)])
+        atp.atp_attention_block_bwd(m, bm, batch, seq, h, heads, 1, wts, bs, x, qkv, attn, lse,
+                                    d_o, own(atab, go.bwd_index), out["d_attn"],
+                                    torch.empty(hd * T, device=DEV), out["d_qkv"],
+                                    own(xtab, gq.bwd_index), out["dx"], out["dw"], out["db"],
+                                    workspace=ws, comm_stream=torch.cuda.Stream())
+        torch.cuda.synchronize()
+        res.append(out)
+    a, b = res
+    for key in ("d_attn", "d_qkv", "dx"):
+        assert not torch.isnan(a[key].float()).any(), key
+        assert torch.equal(_bits(a[key]), _bits(b[key])), key
+    for i in range(2):
+        assert not torch.isnan(a["dw"][i]).any() and not torch.isnan(a["db"][i]).any(), i
+        assert torch.equal(_bits(a["dw"][i]), _bits(b["dw"][i])), ("dw", i)
+        assert torch.equal(_bits(a["db"][i]), _bits(b["db"][i])), ("db", i)
+
+
+@pytest.mark.parametrize("mode,mesh,coord,h,heads,batch,seq,chunks", [
+    ("col", (2, 4), (1, 2), 2048, 16, 2, 512, 2),
+    ("col", (8, 1), (3, 0), 2048, 16, 1, 512, 4),
+    ("row", (2, 2), (1, 1), 1024, 8, 2, 128, 2)])
+def test_attention_block_forward_workspace_path(mode, mesh, coord, h, heads, batch, seq, chunks):
+    """The forward with a workspace (chunk products split over k into slabs
+    where the chunk has too few tiles, from W^T copies) against the forward
+    without one: the split sums in another order, so the outputs agree to
+    fp32 rounding (bf16 outputs within two units in the last place), and the
+    split kernels run only on the workspace path."""
+    from helpers import assert_paths_agree
+    bm = block_mode_code(mode)
+    m = atp.mesh(*mesh, *coord)
+    gq, go = atp.block_geometry(m, bm, h)[:2]
+    _, hd, _ = atp.attention_heads(m, bm, h, heads)
+    T = batch * seq
+    rnd = lambda shape, std, tid, dt=torch.bfloat16: S.randn_device(  # noqa: E731
+        shape, std, 84, tid, DEV, dtype=dt)
+    x = rnd((T, gq.k_loc), 1.0, 1)
+    wts = [rnd((gq.k_loc, gq.n_loc), 0.02, 2), rnd((go.k_loc, go.n_loc), 0.02, 3)]
+    bs = [rnd((gq.n_loc,), 0.02, 4), rnd((go.n_loc,), 0.02, 5)]
+    peers = [None if g.red_size == 1 else [rnd((T, g.n_loc), 0.5, 10 * i + j, torch.float32)
+                                           for j in range(g.red_size)]
+             for i, g in enumerate((gq, go))]
+    gathered = rnd((T, go.k_loc), 1.0, 6)
+    nb = atp.atp_block_workspace_bytes(m, bm, T, h, chunks, atp.ATP_W_KN)
+    res, names = [], []
+    for ws in (None, torch.full((nb,), 255, dtype=torch.uint8, device=DEV)):
+        print(f"attention block forward {mode} {mesh} workspace {ws is not None}", flush=True)
+        tabs = [None if p is None else [torch.full_like(t, float("nan")) if j == g.red_index
+                                        else t for j, t in enumerate(p)]
+                for p, g in zip(peers, (gq, go))]
+        out = dict(qkv=torch.full((T, gq.n_loc), float("nan"), dtype=torch.bfloat16, device=DEV),
+                   attn=gathered.clone(), lse=torch.full((hd, T), float("nan"), device=DEV),
+                   o=torch.full((T, go.n_loc), float("nan"), dtype=torch.bfloat16, device=DEV))
+        atp.atp_profile_enable(2)
+        try:
+            atp.atp_attention_block_fwd(m, bm, batch, seq, h, heads, chunks, wts, bs, x, tabs[0],
+                                        out["qkv"], out["attn"], out["lse"], tabs[1], out["o"],
+                                        workspace=ws, comm_stream=torch.cuda.Stream())
+            torch.cuda.synchronize()
+            names.append([r["name"] for r in atp.atp_profile_collect(256)])
+        finally:
+            atp.atp_profile_enable(0)
+        res.append(out)
+    a, b = res
+    for key in ("qkv", "attn", "o"):
+        assert not torch.isnan(a[key].float()).any() and not torch.isnan(b[key].float()).any()
+        assert_paths_agree(a[key], b[key], key)
+    assert_paths_agree(a["lse"], b["lse"], "lse")
+    assert not any(n.startswith("gemm_nt_splitk") for n in names[0]), names[0]
+    if mode == "col" and mesh == (2, 4):
+        assert any(n.startswith("gemm_nt_splitk") for n in names[1]), names[1]

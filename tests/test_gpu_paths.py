@@ -18,7 +18,7 @@ import torch
 
 import paper_2301_08658_amd as atp
 import synth_inputs as S
-from helpers import make_block_inputs, run_block_bwd, run_block_fwd
+from helpers import assert_paths_agree, make_block_inputs, run_block_bwd, run_block_fwd
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -26,26 +26,6 @@ DEV = "cuda:0"
 
 def bits(t):
     return t.contiguous().view(torch.int16 if t.element_size() == 2 else torch.int32)
-
-
-def assert_paths_agree(a, b, what, rel=1e-4):
-    """Two summation orders of the same fp32-accumulated products."""
-    if a.dtype == torch.bfloat16:
-        # two units in the last place of the larger value (bf16 keeps 8
-        # significant bits), plus the fp32 sums' rounding on the tensor's scale
-        # for values that come out of cancellation near zero
-        fa, fb = a.double(), b.double()
-        scale = float(fa.abs().max()) + 1e-30
-        bound = 2.0 ** -6 * torch.maximum(fa.abs(), fb.abs()) + rel * scale
-        excess = float(((fa - fb).abs() - bound).max())
-        assert excess <= 0, f"{what}: bf16 outputs differ beyond two units in the last place"
-        frac = float((bits(a) != bits(b)).float().mean())
-        assert frac < 0.05, f"{what}: {frac:.3%} of bf16 outputs differ"
-    else:
-        fa, fb = a.double(), b.double()
-        scale = float(fa.abs().max()) + 1e-30
-        err = float((fa - fb).abs().max())
-        assert err <= rel * scale, f"{what}: max diff {err:.3e} vs scale {scale:.3e}"
 
 
 @pytest.mark.parametrize("rows,cols,pad_s,pad_d", [
