@@ -504,7 +504,8 @@ atp_status atp_attention_block_fwd(const atp_mesh* mesh, int32_t block_mode, int
  * the dY transpose; otherwise dW reads X and dY as given.  Both paths give
  * the same bits.  The workspace is scratch: nothing in it is read before
  * the call writes it.
- * Errors as atp_block_bwd and atp_attention_bwd. */
+ * The call refuses a compute_stream under HIP graph capture.  Errors as
+ * atp_block_bwd and atp_attention_bwd. */
 typedef struct {
     const void* x_loc; int64_t ldx;
     const void* qkv; int64_t ld_qkv;
