@@ -460,8 +460,9 @@ atp_status atp_attention_bwd(const atp_mesh* mesh, int32_t block_mode, int64_t b
  * there as W^T where the products stream faster from it; without it the
  * products read the weights as stored.  Nothing in the workspace is read
  * before the call writes it.
- * The call refuses a compute_stream under HIP graph capture.  Errors as
- * atp_block_fwd and atp_attention_fwd. */
+ * Without such a workspace the call refuses a compute_stream under HIP
+ * graph capture (as the block calls do).  Errors as atp_block_fwd and
+ * atp_attention_fwd. */
 typedef struct {
     const void* x_loc; int64_t ldx;
     void* const* qkv_partials; int64_t ldp_qkv;
@@ -504,7 +505,8 @@ atp_status atp_attention_block_fwd(const atp_mesh* mesh, int32_t block_mode, int
  * the dY transpose; otherwise dW reads X and dY as given.  Both paths give
  * the same bits.  The workspace is scratch: nothing in it is read before
  * the call writes it.
- * The call refuses a compute_stream under HIP graph capture.  Errors as
+ * Without such a workspace (or with tokens not a multiple of 8) the call
+ * refuses a compute_stream under HIP graph capture.  Errors as
  * atp_block_bwd and atp_attention_bwd. */
 typedef struct {
     const void* x_loc; int64_t ldx;

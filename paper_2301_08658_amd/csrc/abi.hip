@@ -1545,11 +1545,12 @@ atp_status atp_attention_block_fwd(const atp_mesh* mesh, int32_t block_mode, int
         return set_error(ATP_ERR_INVALID_ARGUMENT, "qkv and attn must not overlap");
     if (workspace && reinterpret_cast<uintptr_t>(workspace) % kWsAlign)
         return set_error(ATP_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kWsAlign);
-    ATP_CHECK(refuse_capture_of_direct_path(compute_stream));
     // With a workspace, as in the block forward: chunk products with too few
     // tiles to fill the chip are split over k into slabs there, from W^T
-    // copies kept there (weights stored [k][n])
+    // copies kept there (weights stored [k][n]).  As for the block calls,
+    // only that path may run under graph capture.
     const bool ws = workspace && ws_bytes >= ws_fwd_bytes(P, T, w->layout, 2);
+    if (!ws) ATP_CHECK(refuse_capture_of_direct_path(compute_stream));
     uint16_t* wt[2] = {nullptr, nullptr};
     float* slab = nullptr;
     if (ws) {
@@ -1668,10 +1669,11 @@ atp_status atp_attention_block_bwd(const atp_mesh* mesh, int32_t block_mode, int
         return set_error(ATP_ERR_INVALID_ARGUMENT, "d_qkv must not overlap an input");
     if (workspace && reinterpret_cast<uintptr_t>(workspace) % kWsAlign)
         return set_error(ATP_ERR_INVALID_ARGUMENT, "workspace must be %zu-byte aligned", kWsAlign);
-    ATP_CHECK(refuse_capture_of_direct_path(compute_stream));
     // dW from transposed copies when the workspace holds them (whole 16-byte
-    // rows of tokens for the transposes), else from X and dY as given
+    // rows of tokens for the transposes), else from X and dY as given; only
+    // the former may run under graph capture
     const bool ws = workspace && ws_bytes >= attn_ws_bwd_bytes(P, T) && T % 8 == 0;
+    if (!ws) ATP_CHECK(refuse_capture_of_direct_path(compute_stream));
     uint16_t *xt_x = nullptr, *xt_a = nullptr, *dyt_q = nullptr, *dyt_o = nullptr;
     float* colpart = nullptr;
     if (ws) {
