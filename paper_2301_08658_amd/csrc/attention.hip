@@ -29,9 +29,11 @@
 // recomputed from the saved log-sum-exps and delta_t = dO_t . O_t,
 //   dV = P^T dO,  dS = P o (dO V^T - delta),  dQ = dS K / sqrt(d),
 //   dK = dS^T Q / sqrt(d).
-// One kernel per 64-key tile accumulates dK and dV over the query tiles
-// that see it; one per 64-query tile accumulates dQ over its key tiles; no
-// atomics, so the result does not depend on scheduling.  Every contraction
+// One kernel per 64-query tile (128 on large grids) first forms delta for
+// its rows (stored for the next kernel) and accumulates dQ over its key
+// tiles; then one per 64-key tile accumulates dK and dV over the query
+// tiles that see it; no atomics, so the result does not depend on
+// scheduling.  Every contraction
 // over keys or queries uses the same lane-local ordering as the forward's
 // P V, so probabilities and score gradients never leave their lanes.  All
 // bwd LDS tiles use the layout vpos, which is conflict-free for both
@@ -424,29 +426,6 @@ __device__ __forceinline__ bf16x8 pack_pair(const f32x4& a, const f32x4& b) {
 }
 
 
-// delta[h][t] = dO_t . O_t over the head's 128 columns (16 lanes per row)
-__global__ __launch_bounds__(NTHR) void attention_delta_kernel(AttnBwdArgs a) {
-    const int64_t T = (int64_t)a.batch * a.seq;
-    const int64_t rid = (int64_t)blockIdx.x * (NTHR / 16) + (threadIdx.x >> 4);
-    const int l16 = threadIdx.x & 15;
-    float acc = 0.f;
-    const bool live = rid < T * a.heads;
-    const int64_t hh = live ? rid / T : 0, t = live ? rid % T : 0;
-    if (live) {
-        const u32x4 o = *reinterpret_cast<const u32x4*>(a.out + t * a.ldo + a.ocol0 + hh * D + 8 * l16);
-        const u32x4 g = *reinterpret_cast<const u32x4*>(a.dout + t * a.lddo + a.docol0 + hh * D +
-                                                        8 * l16);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            acc += __uint_as_float(o[e] << 16) * __uint_as_float(g[e] << 16);
-            acc += __uint_as_float(o[e] & 0xffff0000u) * __uint_as_float(g[e] & 0xffff0000u);
-        }
-    }
-#pragma unroll
-    for (int m = 8; m >= 1; m >>= 1) acc += __shfl_xor(acc, m);
-    if (live && l16 == 0) a.delta[hh * T + t] = acc;
-}
-
 // dK, dV of one 64-key tile (4 waves x 16 keys).  KG groups of four waves
 // split the query tiles that see the key tile (group 0 the first half, group
 // 1 the rest); group 1 adds its sums into group 0's through LDS at the end.
@@ -659,10 +638,26 @@ __global__ __launch_bounds__(NTHR * KG, 2 / KG) void attention_dq_kernel(AttnBwd
                 of[r][ks] = qf[r][ks];
             }
         }
+        // delta of the row = dO . O over the head's 128 columns: each of the
+        // row's four lanes sums its 32 columns, then the lane swaps add them
+        float acc = 0.f;
         if (qabs[r] < a.seq) {
             l2[r] = a.lse[(int64_t)hh * T + tok0 + qabs[r]] * 1.44269504088896340736f;
-            dl[r] = a.delta[(int64_t)hh * T + tok0 + qabs[r]];
+            const uint16_t* orow = a.out + (tok0 + qabs[r]) * a.ldo + a.ocol0 + (int64_t)hh * D;
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+                const u32x4 o = *reinterpret_cast<const u32x4*>(orow + 32 * ks + 8 * g);
+                const u32x4 d = __builtin_bit_cast(u32x4, of[r][ks]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    acc += __uint_as_float(o[e] << 16) * __uint_as_float(d[e] << 16);
+                    acc += __uint_as_float(o[e] & 0xffff0000u) * __uint_as_float(d[e] & 0xffff0000u);
+                }
+            }
         }
+        dl[r] = row_sum4(acc);   // every lane of the wave takes part
+        // the dK/dV kernel, launched after this one, reads it
+        if (grp == 0 && g == 0 && qabs[r] < a.seq) a.delta[(int64_t)hh * T + tok0 + qabs[r]] = dl[r];
     }
     f32x4 dq[RB][8];
 #pragma unroll
@@ -820,24 +815,21 @@ hipError_t launch_attention_bwd(const AttentionBwdProblem& p, hipStream_t s) {
     a.tiles = (int)((p.seq + BM - 1) / BM);
     a.scale_log2 = 1.44269504088896340736f / sqrtf((float)D);
     a.inv_sqrt_d = 1.0f / sqrtf((float)D);
-    const int64_t rows = p.batch * p.seq * p.heads;
-    const int64_t dgrid = (rows + NTHR / 16 - 1) / (NTHR / 16);
     const int64_t grid = (int64_t)a.tiles * a.batch * a.heads;
-    if (dgrid > 0x7fffffff || grid > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(attention_delta_kernel, dim3((unsigned)dgrid), dim3(NTHR), 0, s, a);
-    // small grids: split each workgroup's loop over two groups of four waves
-    // (one workgroup per CU), so the longest loops take half as many steps
+    if (grid > 0x7fffffff) return hipErrorInvalidValue;
+    // the dQ kernel first: it forms delta for its query rows and stores it
+    // for the dK/dV kernel.  Small grids split each workgroup's loop over two
+    // groups of four waves (one workgroup per CU), so the longest loops take
+    // half as many steps; dQ takes 128-row query tiles (two row blocks per
+    // wave) when they still give every CU two workgroups.
     const bool split = grid < kBwdSplitGrid;
     if (split) {
-        hipLaunchKernelGGL((attention_dkv_kernel<2>), dim3((unsigned)grid), dim3(2 * NTHR), 0, s,
-                           a);
         hipLaunchKernelGGL((attention_dq_kernel<1, 2>), dim3((unsigned)grid), dim3(2 * NTHR), 0,
                            s, a);
+        hipLaunchKernelGGL((attention_dkv_kernel<2>), dim3((unsigned)grid), dim3(2 * NTHR), 0, s,
+                           a);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL((attention_dkv_kernel<1>), dim3((unsigned)grid), dim3(NTHR), 0, s, a);
-    // dQ in 128-row query tiles (two row blocks per wave) when they still give
-    // every CU two workgroups
     AttnBwdArgs a2 = a;
     a2.tiles = (int)((p.seq + 127) / 128);
     const int64_t grid2 = (int64_t)a2.tiles * a.batch * a.heads;
@@ -846,6 +838,7 @@ hipError_t launch_attention_bwd(const AttentionBwdProblem& p, hipStream_t s) {
                            a2);
     else
         hipLaunchKernelGGL((attention_dq_kernel<1, 1>), dim3((unsigned)grid), dim3(NTHR), 0, s, a);
+    hipLaunchKernelGGL((attention_dkv_kernel<1>), dim3((unsigned)grid), dim3(NTHR), 0, s, a);
     return hipGetLastError();
 }
 
