@@ -57,7 +57,7 @@ def parse():
                     help="replay the step as a captured HIP graph (measured slower than "
                          "launching it: the replay loses part of the reduce/GEMM overlap)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=256,
+    ap.add_argument("--cpu-rows", type=int, default=384,
                     help="token rows in the oracle's timed CPU sample")
     ap.add_argument("--copy-calib-mb", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB "
