@@ -169,27 +169,29 @@ __device__ __forceinline__ void epilogue_store(const KArgs& a, int64_t m, int64_
 // ---------------------------------------------------------------------------
 // The kernel: C[M,N] = A B with A [M,K] and B [K,N] each stored contiguous
 // along k (A_K / B_K; B then reads [N][K], the NT layout) or along its rows
-// (A [K][M], B [K][N]); 256 x 160 tiles, eight waves in two groups that take
-// turns on the matrix cores ("ping-pong").
+// (A [K][M], B [K][N]); tiles of 256 rows by 160, 256 or 320 columns (the
+// configurations below), eight waves in two groups that take turns on the
+// matrix cores ("ping-pong").
 //
-//   * Tile 256 x 160 x 64: three LDS stages of (256 + 160) x 64 bf16 fill
-//     156 KB of the 160 KB, so the copy of step p+2 is issued while step p is
-//     multiplied.  160 divides every N of the block's products at the
-//     benchmark sizes (and a 512-row token chunk is exactly 256 tiles), so
-//     no launch ends on a partial wave of tiles.
 //   * Waves 0-3 (group A) and 4-7 (group B) share the four SIMDs pairwise.
 //     A K step is two phases separated by workgroup barriers: a memory phase
-//     (issue this wave's share of the direct-to-LDS copy of step p+2, read all
-//     of step p's MFMA fragments into registers) and a compute phase (the 40
-//     MFMAs of step p).  Group B starts one phase late, so on every SIMD one
-//     wave multiplies while the other one loads: the matrix core is fed from
-//     registers while the other wave's LDS reads and copy issue overlap it.
-//   * Each wave owns a 64 x 80 block of C as 4 x 5 tiles of
-//     v_mfma_f32_16x16x32_bf16.  A fragment is one ds_read_b128 (row r,
-//     8 consecutive k).  gfx950 serves a ds_read_b128 in lane groups
-//     {0-7, 24-31}, {8-15, 16-23} (and the same +32); the chunk swizzle
-//     s(r) = r & 6 gives the 16 lanes of each group distinct bank quads
-//     (measured: zero LDS bank conflicts).
+//     (issue this wave's share of the direct-to-LDS copy of a later step,
+//     read all of step p's MFMA fragments into registers) and a compute phase
+//     (the MFMAs of step p).  Group B starts one phase late, so on every SIMD
+//     one wave multiplies while the other one loads: the matrix core is fed
+//     from registers while the other wave's LDS reads and copy issue overlap
+//     it.
+//   * The copies run ahead through LDS: shared stages of both operands (three
+//     of (256 + 160) x 64 bf16, 156 KB, for 256 x 160 tiles), or split rings
+//     (256 x 256: three stages of A filled by group B, two of B filled by
+//     group A, 160 KB), so no copy has to land within the phase that issues
+//     it.
+//   * A wave owns a block of C as 16 x 16 tiles of v_mfma_f32_16x16x32_bf16
+//     (64 x 80 for 256 x 160 tiles, 128 x 64 for 256 x 256).  A fragment is
+//     one ds_read_b128 (row r, 8 consecutive k).  gfx950 serves a
+//     ds_read_b128 in lane groups {0-7, 24-31}, {8-15, 16-23} (and the same
+//     +32); the chunk swizzle s(r) = r & 6 gives the 16 lanes of each group
+//     distinct bank quads (measured: zero LDS bank conflicts).
 //   * The swizzle of a row depends only on the row's index within its copy
 //     instruction, so one byte offset per lane serves every copy; rows past
 //     the operand's end lie beyond the buffer's num_records and read zeros.
@@ -197,10 +199,9 @@ __device__ __forceinline__ void epilogue_store(const KArgs& a, int64_t m, int64_
 //     fragments come from two ds_read_b64_tr_b16 (gfx950's transposing LDS
 //     read); a chunk rotation (160-wide tiles) or XOR (256-wide) keeps each
 //     32-lane half of a read on distinct banks (measured: zero conflicts).
-//     These reads cost 1.5x the LDS time per byte of ds_read_b128, and
-//     160-wide rows (320 bytes) straddle cache lines, so this layout runs
-//     15-25% slower than the k-contiguous one on the forward shapes; the
-//     block calls use it only without a workspace.
+//     These reads cost 1.5x the LDS time per byte of ds_read_b128; with the
+//     split rings a product whose B is row-contiguous (the forward from W as
+//     stored) streams about as fast as the k-contiguous layout.
 //   * An output element's products are accumulated in the same order for
 //     every M and every layout (K steps of 64, two MFMA k-slices of 32
 //     each), so token chunking and the layout never change a value.
