@@ -56,14 +56,16 @@ def _key(c, axis):
     return c[1 - axis]
 
 
-@pytest.mark.parametrize("mode,mesh", [("col", (2, 2)), ("col", (2, 4)), ("col", (4, 2)),
-                                       ("col", (8, 1)), ("row", (2, 2))])
-def test_attention_block_every_coordinate(mode, mesh):
+@pytest.mark.parametrize("mode,mesh,seq", [("col", (2, 2), 128), ("col", (2, 4), 128),
+                                           ("col", (4, 2), 128), ("col", (8, 1), 128),
+                                           ("row", (2, 2), 128),
+                                           ("col", (2, 2), 200)])   # ragged key / query tiles
+def test_attention_block_every_coordinate(mode, mesh, seq):
     d1, d2 = mesh
-    h, heads, batch, seq, chunks = 1024, 8, 2, 128, 2
+    h, heads, batch, chunks = 1024, 8, 2, 2
     T = batch * seq
     bm = block_mode_code(mode)
-    print(f"attention block {mode} {mesh}", flush=True)
+    print(f"attention block {mode} {mesh} seq {seq}", flush=True)
     X = S.randn_bf16((T, h), 1.0, 81, 1)
     Wq = S.randn_bf16((h, 3 * h), 0.02, 81, 2)
     bq = S.randn_bf16((3 * h,), 0.02, 81, 3)
