@@ -337,9 +337,15 @@ atp_status atp_transpose_bf16(int64_t rows, int64_t cols, const void* src, int64
  * chunk's reduction runs on comm_stream as soon as that chunk's partial is
  * written; fc2's chunk c waits for fc1's reduced chunk c.  A group of one
  * needs no reduction: its bias (and GeLU) are applied in the GEMM epilogue
- * and it runs as one launch.  Every GEMM runs on compute_stream, in the order
- * out-proj, fc1, then QKV and fc2 (the one whose reductions read fewer bytes
- * last).  With comm_stream == compute_stream nothing overlaps.
+ * and it runs as one launch.  The GEMMs are issued on compute_stream in the
+ * order out-proj, fc1, then QKV and fc2 (the one whose reductions read fewer
+ * bytes last); with chunks > 1, comm_stream != compute_stream and outside
+ * HIP graph capture, every other chunk product of a linear whose chunks do
+ * not split over k runs on a second stream the library keeps per host
+ * thread and device (default priority, never destroyed), so a chunk's
+ * product can start on the CUs the previous chunk leaves idle; the call
+ * joins that stream back into compute_stream before it returns.  With
+ * comm_stream == compute_stream nothing overlaps.
  * workspace (nullable, 256-byte aligned): when ws_bytes is at least the
  * forward's need (atp_block_workspace_path) the products run with both
  * operands contiguous along k, the faster layout (weights stored

@@ -173,6 +173,25 @@ atp_status sync_events(size_t count, hipEvent_t** out) {
     return ATP_OK;
 }
 
+// A second compute stream of the calling host thread on the current device
+// (created on first use, default priority, never destroyed: like the event
+// pool it may outlive the runtime's shutdown).  The forward puts every other
+// chunk product of a linear on it, so one chunk's 160 tiles of 256 x 256 can
+// start on the CUs the previous chunk leaves idle.
+thread_local std::map<int, hipStream_t> t_lane2;   // device -> stream
+atp_status second_lane(hipStream_t* out) {
+    int dev = 0;
+    HIP_CHECK(hipGetDevice(&dev), "hipGetDevice");
+    auto it = t_lane2.find(dev);
+    if (it == t_lane2.end()) {
+        hipStream_t s = nullptr;
+        HIP_CHECK(hipStreamCreateWithFlags(&s, hipStreamNonBlocking), "hipStreamCreateWithFlags");
+        it = t_lane2.emplace(dev, s).first;
+    }
+    *out = it->second;
+    return ATP_OK;
+}
+
 struct ProfRec {
     std::string name;
     hipEvent_t beg, end;
@@ -1191,13 +1210,24 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
 
     Streams S(compute_stream, comm_stream);
     hipEvent_t* ev = nullptr;
-    // [0] start  [1] comm end  [2] unused  [3] fc1's single launch done,
-    // then per linear per chunk GEMM-done, then fc1 reduce-done per chunk
+    // [0] start  [1] comm end  [2] second lane forked  [3] second lane
+    // joined, then per linear per chunk GEMM-done, then fc1 reduce-done per
+    // chunk
     const size_t n_ev = 4 + 4 * (size_t)chunks + (size_t)chunks;
     ATP_CHECK(sync_events(n_ev, &ev));
     hipEvent_t* ev_gemm = ev + 4;
     hipEvent_t* ev_red1 = ev + 4 + 4 * chunks;
     ATP_CHECK(S.begin(ev[0]));
+    // A second compute lane for the chunk products, only when the caller
+    // overlaps at all (comm_stream != compute_stream) and outside graph
+    // capture (captures stay on the streams the caller gave)
+    hipStream_t lane2 = nullptr;
+    if (S.ms != S.cs && chunks > 1) {
+        hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+        HIP_CHECK(hipStreamIsCapturing(S.cs, &cap), "hipStreamIsCapturing");
+        if (cap == hipStreamCaptureStatusNone) ATP_CHECK(second_lane(&lane2));
+    }
+    bool lane2_used = false;
 
     uint16_t* wt[4] = {nullptr, nullptr, nullptr, nullptr};
     float* slab = nullptr;
@@ -1247,12 +1277,12 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     // fc2 reads H: wait for fc1's reduced chunk c (the comm stream runs in
     // order, so chunk chunks-1 means all of H); fc1's single launch is
     // ordered before fc2 on the compute stream already
-    auto wait_h = [&](int c) -> atp_status {
-        if (fc1_reduced) HIP_CHECK(hipStreamWaitEvent(S.cs, ev_red1[c], 0), "hipStreamWaitEvent");
+    auto wait_h = [&](int c, hipStream_t st) -> atp_status {
+        if (fc1_reduced) HIP_CHECK(hipStreamWaitEvent(st, ev_red1[c], 0), "hipStreamWaitEvent");
         return ATP_OK;
     };
     auto unchunked = [&](int L) -> atp_status {
-        if (L == 3) ATP_CHECK(wait_h(chunks - 1));
+        if (L == 3) ATP_CHECK(wait_h(chunks - 1, S.cs));
         ATP_CHECK(need_wt(L));
         atp::GemmProblem p = fwd_problem(L, A_in[L], lda_in[L], outp[L], ldo[L], true,
                                          L == 2 ? atp::EPI_BIAS_GELU : atp::EPI_BIAS, tokens);
@@ -1262,18 +1292,17 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     };
     // chunk c: the GEMM writes this device's partial rows, the comm stream
     // reduces the group's partials for those rows as soon as they are ready
-    auto chunk = [&](int L, int c) -> atp_status {
+    auto chunk = [&](int L, int c, hipStream_t st) -> atp_status {
         const atp_shard& g = P.g[L];
         const int64_t r0 = (int64_t)c * mc;
-        if (L == 3) ATP_CHECK(wait_h(c));
-        ATP_CHECK(need_wt(L));
+        if (L == 3) ATP_CHECK(wait_h(c, st));
         void* own = io->partials[L][g.red_index];
         atp::GemmProblem p = fwd_problem(L, static_cast<const uint16_t*>(A_in[L]) + r0 * lda_in[L],
                                          lda_in[L], row_ptr(own, r0, io->ldp[L], pb16),
                                          io->ldp[L], pb16, atp::EPI_NONE, mc);
-        ATP_CHECK(run_nt_partial(p, slab, S.cs));
+        ATP_CHECK(run_nt_partial(p, slab, st));
         hipEvent_t e = ev_gemm[L * chunks + c];
-        HIP_CHECK(hipEventRecord(e, S.cs), "hipEventRecord");
+        HIP_CHECK(hipEventRecord(e, st), "hipEventRecord");
         HIP_CHECK(hipStreamWaitEvent(S.ms, e, 0), "hipStreamWaitEvent");
         atp::ReduceProblem r = reduce_problem(
             g.red_size, io->partials[L], io->ldp[L], r0, mc, g.n_loc,
@@ -1283,9 +1312,22 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
         if (L == 2) HIP_CHECK(hipEventRecord(ev_red1[c], S.ms), "hipEventRecord");
         return ATP_OK;
     };
+    // Odd chunks go to the second lane unless the chunk products split over
+    // k (the splits of every chunk share one slab region, so they stay in
+    // order on one stream); the lane first waits for everything queued on
+    // compute_stream so far (fc1's output, the W^T copy).
     auto linear = [&](int L) -> atp_status {
-        if (P.g[L].red_size == 1) return unchunked(L);
-        for (int c = 0; c < chunks; ++c) ATP_CHECK(chunk(L, c));
+        const atp_shard& g = P.g[L];
+        if (g.red_size == 1) return unchunked(L);
+        ATP_CHECK(need_wt(L));
+        int64_t ks = 0;
+        const bool two = lane2 && (!slab || atp::nt_split_plan(mc, g.n_loc, g.k_loc, &ks) <= 1);
+        if (two) {
+            HIP_CHECK(hipEventRecord(ev[2], S.cs), "hipEventRecord");
+            HIP_CHECK(hipStreamWaitEvent(lane2, ev[2], 0), "hipStreamWaitEvent");
+            lane2_used = true;
+        }
+        for (int c = 0; c < chunks; ++c) ATP_CHECK(chunk(L, c, two && (c & 1) ? lane2 : S.cs));
         return ATP_OK;
     };
     // out-proj first (its reductions start at once), then fc1; of QKV and fc2
@@ -1298,6 +1340,11 @@ atp_status atp_block_fwd(const atp_mesh* mesh, int32_t block_mode, int64_t token
     const bool qkv_last = red_bytes(0) <= red_bytes(3);
     const int order[4] = {1, 2, qkv_last ? 3 : 0, qkv_last ? 0 : 3};
     for (int L : order) ATP_CHECK(linear(L));
+    if (lane2_used) {
+        // compute_stream is ordered after the second lane's products
+        HIP_CHECK(hipEventRecord(ev[3], lane2), "hipEventRecord");
+        HIP_CHECK(hipStreamWaitEvent(S.cs, ev[3], 0), "hipStreamWaitEvent");
+    }
     return S.end(ev[1]);
 }
 
