@@ -54,6 +54,9 @@ constexpr int NWAVE = 4;
 constexpr int NTHR = NWAVE * 64;
 constexpr int64_t kFwdWideGrid = 512;   // two workgroups per CU on 256 CUs
 constexpr int64_t kBwdSplitGrid = 1024;  // 64-row tiles below which loops are split
+// forward softmax: largest base-2 gain of a row maximum absorbed without
+// rescaling the running output (weights stay below 2^8, exact in bf16's range)
+constexpr float kSlack = 8.f;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
@@ -83,6 +86,17 @@ __device__ __forceinline__ float row_max4(float x) {
     const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
                                                     false, false);
     return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+// Maximum of a lane's 16 scores of one row block as a tree of three-input
+// maxima (seven v_max3_f32 and one v_max_f32 instead of a chain of sixteen).
+__device__ __forceinline__ float max16(const f32x4 (&v)[4]) {
+    const float a = fmaxf(fmaxf(v[0][0], v[0][1]), v[0][2]);
+    const float b = fmaxf(fmaxf(v[0][3], v[1][0]), v[1][1]);
+    const float c = fmaxf(fmaxf(v[1][2], v[1][3]), v[2][0]);
+    const float d = fmaxf(fmaxf(v[2][1], v[2][2]), v[2][3]);
+    const float e = fmaxf(fmaxf(v[3][0], v[3][1]), v[3][2]);
+    return fmaxf(fmaxf(fmaxf(a, b), c), fmaxf(fmaxf(d, e), v[3][3]));
 }
 
 __device__ __forceinline__ float row_sum4(float x) {
@@ -279,16 +293,25 @@ __global__ __launch_bounds__(NTHR * KG, 2 / KG) void attention_fwd_kernel(AttnAr
             }
 #pragma unroll
             for (int r = 0; r < RB; ++r) {
-                float mx = -INFINITY;
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) mx = fmaxf(mx, s[r][j][e]);
+                float mx = max16(s[r]);
                 mx = row_max4(mx);
                 const float mnew = fmaxf(mrun[r], mx * a.scale_log2);   // base-2 scaled domain
-                // a row with no visible key yet keeps mnew = -inf: subtract 0
-                const float msub = mnew == -INFINITY ? 0.f : mnew;
-                const float alpha = __builtin_amdgcn_exp2f(mrun[r] - msub);
+                // The reference point of the exponentials moves only when a
+                // row of the wave gains more than kSlack on it (one scalar
+                // branch for the wave); otherwise the weights exp2(x - m) stay
+                // below 2^kSlack and O and l keep their scale.  O / l and
+                // m + log2 l do not depend on the reference point, so the
+                // results differ from rescaling at every step by rounding only.
+                if (__builtin_amdgcn_ballot_w64(mnew > mrun[r] + kSlack) != 0) {
+                    // a row with no visible key yet keeps mnew = -inf: subtract 0
+                    const float alpha =
+                        __builtin_amdgcn_exp2f(mrun[r] - (mnew == -INFINITY ? 0.f : mnew));
+                    lrun[r] *= alpha;
+#pragma unroll
+                    for (int dt = 0; dt < 8; ++dt) o[r][dt] *= alpha;
+                    mrun[r] = mnew;
+                }
+                const float msub = mrun[r] == -INFINITY ? 0.f : mrun[r];
                 float rs = 0.f;
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
@@ -299,11 +322,7 @@ __global__ __launch_bounds__(NTHR * KG, 2 / KG) void attention_fwd_kernel(AttnAr
                         s[r][j][e] = p;
                         rs += p;
                     }
-                rs = row_sum4(rs);
-                lrun[r] = lrun[r] * alpha + rs;
-                mrun[r] = mnew;
-#pragma unroll
-                for (int dt = 0; dt < 8; ++dt) o[r][dt] *= alpha;
+                lrun[r] += row_sum4(rs);
             }
 
             // O += P V over two 32-key slices
