@@ -74,6 +74,55 @@ def test_attention_fwd_128_row_tiles_ragged():
     np.testing.assert_allclose(to64(lse), ref_lse, rtol=0, atol=2e-3)
 
 
+@pytest.mark.parametrize("batch,seq,h", [
+    (2, 300, 512),      # 64-row tiles, key range split between two wave groups
+    (4, 130, 8192),     # 128-row tiles, two workgroups per CU
+])
+def test_attention_fwd_sharp_scores(batch, seq, h):
+    """Queries scaled by 4 (exact in bf16): score rows with a standard
+    deviation of ~5.8 in base 2, so row maxima pass the running reference
+    point at irregular key steps and the softmax is close to one-hot (the
+    forward's conditional rescale).  Values keep std 1."""
+    m = atp.mesh(1, 1, 0, 0)
+    heads = h // HD
+    g = atp.block_geometry(m, atp.ATP_BLOCK_COL, h)[0]
+    T = batch * seq
+    qkv = S.randn_bf16((T, g.n_loc), 1.0, 56, 304)
+    for hh in range(heads):
+        qkv[:, hh * 3 * HD:hh * 3 * HD + HD] *= 4
+    ref_o, ref_lse = O.attention_core_local(qkv, batch, seq, HD, g.red_size, g.red_index)
+    qkv = qkv.to(DEV)
+    out = torch.empty((T, h), dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty((heads, T), dtype=torch.float32, device=DEV)
+    atp.atp_attention_fwd(m, atp.ATP_BLOCK_COL, batch, seq, h, heads, qkv, out, lse)
+    torch.cuda.synchronize()
+    assert_close(out, ref_o, "attention output")
+    np.testing.assert_allclose(to64(lse), ref_lse, rtol=0, atol=2e-3)
+
+
+def test_attention_fwd_growing_scores():
+    """q = 1 and key j = j/16 in every dimension: the score of key j is
+    8 j / sqrt(128), about 1.02 j in base 2, so every key step raises each
+    row's maximum by ~65 and the output is rescaled at every step; weights
+    fall off geometrically behind the diagonal."""
+    m = atp.mesh(1, 1, 0, 0)
+    h, seq, heads = 512, 300, 4
+    g = atp.block_geometry(m, atp.ATP_BLOCK_COL, h)[0]
+    qkv = S.randn_bf16((seq, g.n_loc), 1.0, 57, 303)
+    ramp = (torch.arange(seq, dtype=torch.float32) / 16).to(torch.bfloat16)
+    for hh in range(heads):
+        qkv[:, hh * 3 * HD:hh * 3 * HD + HD] = 1
+        qkv[:, hh * 3 * HD + HD:hh * 3 * HD + 2 * HD] = ramp[:, None]
+    ref_o, ref_lse = O.attention_core_local(qkv, 1, seq, HD, g.red_size, g.red_index)
+    qkv = qkv.to(DEV)
+    out = torch.empty((seq, h), dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty((heads, seq), dtype=torch.float32, device=DEV)
+    atp.atp_attention_fwd(m, atp.ATP_BLOCK_COL, 1, seq, h, heads, qkv, out, lse)
+    torch.cuda.synchronize()
+    assert_close(out, ref_o, "attention output")
+    np.testing.assert_allclose(to64(lse), ref_lse, rtol=1e-6, atol=2e-3)
+
+
 def test_attention_fwd_wide_share_sampled():
     """The benchmark's attention share (h = 20480 on the 8 x 1 mesh: 20 heads
     per device, two 2048-token sequences; 128-row tiles) against the oracle
