@@ -636,7 +636,7 @@ def reduce_alone(torch, atp, st, reps):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs one device's share on one GPU; --gpus {args.gpus} "
+        print(f"bench.py: this library runs one device's share on one GPU; --gpus {args.gpus} "
               "is not supported (the multi-GPU exchange is not part of it).", file=sys.stderr)
         sys.exit(2)
     import torch

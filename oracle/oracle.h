@@ -86,7 +86,7 @@ void orc_partial_reduce(int nparts, const double* const* parts, int64_t ldp,
 void orc_colsum(int64_t T, int64_t N, const double* dy, int64_t ld, double* db);
 
 /* Sec. 5: the model's tensors are 16-bit (the paper trains in half
- * precision; this build stores activations and activation gradients as
+ * precision; the GPU path stores activations and activation gradients as
  * bfloat16).  Rounds x to the nearest bfloat16 value (8 significant bits,
  * fp32 exponent range, ties to even, overflow to infinity) and returns it
  * as a double.  Used where one GEMM's output is the next GEMM's input. */
