@@ -88,8 +88,10 @@ __device__ __forceinline__ float row_max4(float x) {
     return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
-// Maximum of a lane's 16 scores of one row block as a tree of three-input
-// maxima (seven v_max3_f32 and one v_max_f32 instead of a chain of sixteen).
+// Maximum of a lane's 16 scores of one row block as a shallow tree: five
+// independent three-input maxima over 15 scores, two more over those and
+// the last score, and one two-input maximum (three dependent steps instead
+// of a chain through all sixteen).
 __device__ __forceinline__ float max16(const f32x4 (&v)[4]) {
     const float a = fmaxf(fmaxf(v[0][0], v[0][1]), v[0][2]);
     const float b = fmaxf(fmaxf(v[0][3], v[1][0]), v[1][1]);
