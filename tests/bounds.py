@@ -154,3 +154,27 @@ def right_var(var, y) -> np.ndarray:
     of variance var and Y exact: SIGMAS standard deviations of each output."""
     y = np.asarray(y, dtype=np.float64)
     return SIGMAS * np.sqrt(np.asarray(var, dtype=np.float64).T @ (y * y))
+
+
+def attention_prob_bounds(q, k, v, do):
+    """Error terms of dQ, dK, dV of one (sequence, head) from the two 16-bit
+    operands of the backward's second products: P rounded to bfloat16 for
+    dV_u = sum_t P[t,u] dO_t, and dS = P (dP - delta) rounded to bfloat16 for
+    dK_u = sum_t dS[t,u] q_t / sqrt(d) and dQ_t = sum_u dS[t,u] k_u / sqrt(d).
+    Each rounding is an independent error of variance rounding_var at the
+    oracle's P and dS.  Near one-hot rows (sharp scores) put P close to 1
+    for many queries of one key, where these terms outgrow 1e-2 (|ref| + 1)."""
+    q, k, v, do = (np.asarray(O._f64(a)) for a in (q, k, v, do))
+    S, d = q.shape
+    o, lse = O.attention_fwd(q, k, v)
+    s = q @ k.T / np.sqrt(d)
+    s[np.triu(np.ones((S, S), dtype=bool), 1)] = -np.inf
+    P = np.exp(s - lse[:, None])
+    dS = P * (do @ v.T - (do * o).sum(1)[:, None])
+    var_p, var_ds = rounding_var(P), rounding_var(dS)
+    var_p[P == 0] = 0.0
+    var_ds[dS == 0] = 0.0
+    bv = SIGMAS * np.sqrt(var_p.T @ (do * do))
+    bk = SIGMAS / np.sqrt(d) * np.sqrt(var_ds.T @ (q * q))
+    bq = SIGMAS / np.sqrt(d) * np.sqrt(var_ds @ (k * k))
+    return bq, bk, bv

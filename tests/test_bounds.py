@@ -2,7 +2,8 @@
 spacing against torch's rounding, and the attention backward's sensitivity
 to a rounded output gradient against the oracle's own linear response (the
 backward is linear in dO for fixed q, k, v, so a unit change of one dO
-element gives one column of the exact Jacobian)."""
+element gives one column of the exact Jacobian), and the terms of the
+backward's bf16 P and dS against sampled roundings."""
 import numpy as np
 import torch
 
@@ -94,3 +95,27 @@ def test_propagated_sums_cover_real_roundings():
     for n in range(1, 13):
         worst = n * 0.5                            # n errors of ulp/2 (ulp = 1), all aligned
         assert bounds.SIGMAS * np.sqrt(n / 12.0) >= worst - 1e-12
+
+
+def test_attention_prob_bounds_match_sampled_roundings():
+    """The terms of attention_prob_bounds against sampled roundings: P from
+    torch's float64 softmax, dS = P (dO V^T - rowsum(dO o)), errors drawn
+    uniform on +-ulp/2 at every nonzero P and dS and pushed through the
+    products dV = P^T dO, dK = dS^T Q / sqrt(d), dQ = dS K / sqrt(d); the
+    sampled standard deviations times SIGMAS give the bounds."""
+    rng = np.random.default_rng(5)
+    S, d, n = 6, 4, 20000
+    q, k, v, do = (rng.standard_normal((S, d)) for _ in range(4))
+    bq, bk, bv = bounds.attention_prob_bounds(q, k, v, do)
+    s = torch.tensor(q @ k.T / np.sqrt(d))
+    s = s.masked_fill(torch.triu(torch.ones(S, S, dtype=torch.bool), 1), float("-inf"))
+    P = torch.softmax(s, dim=1).numpy()
+    dS = P * (do @ v.T - (do * (P @ v)).sum(1)[:, None])
+    ep = rng.uniform(-0.5, 0.5, (n, S, S)) * (bounds.ulp_bf16(P) * (P != 0))
+    es = rng.uniform(-0.5, 0.5, (n, S, S)) * (bounds.ulp_bf16(dS) * (dS != 0))
+    sampled = (np.einsum("ntu,te->nue", ep, do),
+               np.einsum("ntu,te->nue", es, q) / np.sqrt(d),
+               np.einsum("ntu,ue->nte", es, k) / np.sqrt(d))
+    for err, b, nm in zip(sampled, (bv, bk, bq), ("dv", "dk", "dq")):
+        assert b.shape == (S, d), nm
+        np.testing.assert_allclose(bounds.SIGMAS * err.std(0), b, rtol=0.05, err_msg=nm)

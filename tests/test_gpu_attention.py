@@ -11,7 +11,7 @@ import torch
 import oracle as O
 import paper_2301_08658_amd as atp
 import synth_inputs as S
-from bounds import delta_bounds
+from bounds import attention_prob_bounds, delta_bounds
 from helpers import DEV, assert_close, block_mode_code, to64
 
 pytestmark = pytest.mark.gpu
@@ -232,6 +232,53 @@ def test_attention_bwd_matches_oracle(mode, mesh, coord, batch, seq, h):
     rest = torch.ones(g.n_loc, dtype=torch.bool)
     rest[mine] = False
     assert torch.all(d_qkv[:, rest.to(DEV)] == -5.0), "columns of other group members written"
+
+
+@pytest.mark.parametrize("batch,seq,h", [
+    (2, 300, 512),      # loops split between two wave groups
+    (4, 260, 8192),     # 1280 tiles: loops not split, 128-row dQ tiles
+])
+def test_attention_bwd_sharp_scores(batch, seq, h):
+    """The backward on queries scaled by 4 (exact in bf16; values and dO keep
+    std 1): near one-hot rows put P close to 1 for many queries of one key,
+    so the bf16 P and dS of the second products carry errors beyond the
+    generic tolerance; their derived terms (bounds.attention_prob_bounds)
+    join the delta terms."""
+    m = atp.mesh(1, 1, 0, 0)
+    heads = h // HD
+    g = atp.block_geometry(m, atp.ATP_BLOCK_COL, h)[0]
+    T = batch * seq
+    qkv = S.randn_bf16((T, g.n_loc), 1.0, 64, 311)
+    for hh in range(heads):
+        qkv[:, hh * 3 * HD:hh * 3 * HD + HD] *= 4
+    d_out = S.randn_bf16((T, h), 1.0, 64, 312)
+    ref = O.attention_core_bwd_local(qkv, d_out, batch, seq, HD, g.red_size, g.red_index)
+    extra = np.zeros((T, 3 * h))
+    for bb in range(batch):
+        rows = slice(bb * seq, (bb + 1) * seq)
+        for j in range(heads):
+            c = 3 * HD * j
+            args = (qkv[rows, c:c + HD], qkv[rows, c + HD:c + 2 * HD],
+                    qkv[rows, c + 2 * HD:c + 3 * HD], d_out[rows, j * HD:(j + 1) * HD])
+            bq, bk = delta_bounds(*args)
+            pq, pk, pv = attention_prob_bounds(*args)
+            extra[rows, c:c + HD] = bq + pq
+            extra[rows, c + HD:c + 2 * HD] = bk + pk
+            extra[rows, c + 2 * HD:c + 3 * HD] = pv
+    qkv, d_out = qkv.to(DEV), d_out.to(DEV)
+    out = torch.empty((T, h), dtype=torch.bfloat16, device=DEV)
+    lse = torch.empty((heads, T), dtype=torch.float32, device=DEV)
+    atp.atp_attention_fwd(m, atp.ATP_BLOCK_COL, batch, seq, h, heads, qkv, out, lse)
+    d_qkv = torch.full((T, 3 * h), -5.0, dtype=torch.bfloat16, device=DEV)
+    delta = torch.empty((heads * T,), dtype=torch.float32, device=DEV)
+    atp.atp_attention_bwd(m, atp.ATP_BLOCK_COL, batch, seq, h, heads, qkv, out, lse, d_out,
+                          d_qkv, delta)
+    torch.cuda.synchronize()
+    for part, nm in ((0, "dq"), (1, "dk"), (2, "dv")):
+        sel = np.concatenate([np.arange(j * 3 * HD + part * HD, j * 3 * HD + (part + 1) * HD)
+                              for j in range(heads)])
+        assert_close(d_qkv[:, torch.as_tensor(sel, device=DEV)], ref[:, sel], nm,
+                     extra=extra[:, sel])
 
 
 def test_attention_bwd_wide_share_sampled():
